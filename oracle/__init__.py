@@ -1,0 +1,244 @@
+"""CPU oracle for FleetSieve -- TEST INFRASTRUCTURE ONLY.
+
+Python access (ctypes) to ``fs_oracle.c``: the plain, slow, binary32-exact
+reference implementation of the fleet allocation (Section 3, Eq. 1-5), the
+acquisition score (Section 4.3) and the decision certificate (Section 4.2).
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  It shares no code with the HIP path and
+imports nothing from it.  A problem is any object with the attributes
+``tp, levels, demand, slo, floor_rps, budget`` (numpy arrays / int).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "fs_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+MAX_CLASSES = 64
+UNDECIDED, CERTIFIED_FEASIBLE, CERTIFIED_INFEASIBLE = 0, 1, 2
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc: binary32 arithmetic, no contraction."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp",
+               "-ffp-contract=off", "-fno-fast-math", "-Wall", "-Wextra",
+               "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True, cwd=_HERE)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Problem(ctypes.Structure):
+    _fields_ = [("n_classes", ctypes.c_int32), ("n_tp", ctypes.c_int32),
+                ("n_levels", ctypes.c_int32), ("budget", ctypes.c_int32),
+                ("tp", ctypes.POINTER(ctypes.c_int32)),
+                ("levels", ctypes.POINTER(ctypes.c_float)),
+                ("demand", ctypes.POINTER(ctypes.c_float)),
+                ("slo", ctypes.POINTER(ctypes.c_float)),
+                ("floor_rps", ctypes.POINTER(ctypes.c_float))]
+
+
+class _Alloc(ctypes.Structure):
+    _fields_ = [("tau", ctypes.c_float), ("floors_met", ctypes.c_int32),
+                ("gpus", ctypes.c_int32), ("goodput", ctypes.c_float),
+                ("tp_index", ctypes.c_int32 * MAX_CLASSES),
+                ("replicas", ctypes.c_int32 * MAX_CLASSES)]
+
+
+@dataclass
+class Alloc:
+    tau: float
+    floors_met: int
+    gpus: int
+    goodput: float
+    tp_index: list   # -1 = empty
+    replicas: list
+
+    def tp(self, problem) -> list:
+        """GPUs per replica per class (0 = empty)."""
+        return [0 if t < 0 else int(problem.tp[t]) for t in self.tp_index]
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB)
+        P, A = ctypes.POINTER(_Problem), ctypes.POINTER(_Alloc)
+        fp, u8p, i32p, f64p = (ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_uint8),
+                               ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_double))
+        lib.orc_check_problem.argtypes = [P]
+        lib.orc_bucket.argtypes = [P, ctypes.c_int, ctypes.c_int]
+        lib.orc_fulfillment.argtypes = [P, ctypes.c_int, ctypes.c_float, ctypes.c_float, ctypes.c_int]
+        lib.orc_fulfillment.restype = ctypes.c_float
+        for name in ("orc_solve_brute", "orc_solve_dp", "orc_solve_threshold"):
+            getattr(lib, name).argtypes = [P, fp, fp, A]
+        lib.orc_solve_batch.argtypes = [P, fp, fp, ctypes.c_int64, A, ctypes.c_int]
+        lib.orc_score.argtypes = [P, ctypes.c_int32, fp, fp, fp, fp, u8p, i32p, ctypes.c_int32,
+                                  fp, fp, ctypes.c_int32, f64p, f64p, i32p, fp, u8p, ctypes.c_int]
+        lib.orc_certify.argtypes = [P, ctypes.c_int32, fp, fp, fp, fp, u8p, ctypes.c_float,
+                                    i32p, A, A, f64p]
+        lib.orc_pairwise_sum.argtypes = [f64p, ctypes.c_int64]
+        lib.orc_pairwise_sum.restype = ctypes.c_double
+        _lib = lib
+    return _lib
+
+
+def _ptr(a, ctype):
+    return a.ctypes.data_as(ctypes.POINTER(ctype))
+
+
+class _ProblemRef:
+    """Holds the numpy buffers alive while the C struct points at them."""
+
+    def __init__(self, problem):
+        self.tp = np.ascontiguousarray(problem.tp, dtype=np.int32)
+        self.levels = np.ascontiguousarray(problem.levels, dtype=np.float32)
+        self.demand = np.ascontiguousarray(problem.demand, dtype=np.float32)
+        self.slo = np.ascontiguousarray(problem.slo, dtype=np.float32)
+        fl = getattr(problem, "floor_rps", None)
+        self.floor = None if fl is None else np.ascontiguousarray(fl, dtype=np.float32)
+        self.s = _Problem(len(self.demand), len(self.tp), len(self.levels), int(problem.budget),
+                          _ptr(self.tp, ctypes.c_int32), _ptr(self.levels, ctypes.c_float),
+                          _ptr(self.demand, ctypes.c_float), _ptr(self.slo, ctypes.c_float),
+                          None if self.floor is None else _ptr(self.floor, ctypes.c_float))
+        self.n_cells = len(self.demand) * len(self.tp) * len(self.levels)
+
+
+def _alloc_out(a: _Alloc, k: int) -> Alloc:
+    return Alloc(float(np.float32(a.tau)), int(a.floors_met), int(a.gpus), float(np.float32(a.goodput)),
+                 [int(a.tp_index[i]) for i in range(k)], [int(a.replicas[i]) for i in range(k)])
+
+
+def check_problem(problem) -> bool:
+    ref = _ProblemRef(problem)
+    return _load().orc_check_problem(ctypes.byref(ref.s)) == 0
+
+
+def bucket(problem, i: int, r: int) -> int:
+    ref = _ProblemRef(problem)
+    return int(_load().orc_bucket(ctypes.byref(ref.s), i, r))
+
+
+def fulfillment(problem, i: int, cap: float, tail: float, r: int) -> np.float32:
+    ref = _ProblemRef(problem)
+    return np.float32(_load().orc_fulfillment(ctypes.byref(ref.s), i, cap, tail, r))
+
+
+def solve(problem, cap, tail, method: str = "dp") -> Alloc:
+    """Solve the allocation on one point realisation (cap[N], tail[N])."""
+    ref = _ProblemRef(problem)
+    cap = np.ascontiguousarray(cap, dtype=np.float32)
+    tail = np.ascontiguousarray(tail, dtype=np.float32)
+    assert cap.shape == (ref.n_cells,) and tail.shape == (ref.n_cells,)
+    out = _Alloc()
+    fn = {"dp": "orc_solve_dp", "brute": "orc_solve_brute", "threshold": "orc_solve_threshold"}[method]
+    rc = getattr(_load(), fn)(ctypes.byref(ref.s), _ptr(cap, ctypes.c_float), _ptr(tail, ctypes.c_float),
+                              ctypes.byref(out))
+    if rc != 0:
+        raise ValueError(f"oracle {method} solve failed ({rc})")
+    return _alloc_out(out, len(ref.demand))
+
+
+def solve_batch(problem, cap, tail, n_threads: int = 1) -> list:
+    ref = _ProblemRef(problem)
+    cap = np.ascontiguousarray(cap, dtype=np.float32).reshape(-1, ref.n_cells)
+    tail = np.ascontiguousarray(tail, dtype=np.float32).reshape(-1, ref.n_cells)
+    n = cap.shape[0]
+    out = (_Alloc * max(n, 1))()
+    rc = _load().orc_solve_batch(ctypes.byref(ref.s), _ptr(cap, ctypes.c_float), _ptr(tail, ctypes.c_float),
+                                 n, out, n_threads)
+    if rc != 0:
+        raise ValueError("oracle batch solve failed")
+    return [_alloc_out(out[j], len(ref.demand)) for j in range(n)]
+
+
+@dataclass
+class ScoreResult:
+    score: np.ndarray     # [O][E] float64
+    gap_now: np.ndarray   # [O] float64
+    best: np.ndarray      # [O] int32
+    tau_dump: np.ndarray  # [O][E][S][2] float32 or None
+
+
+def score(problem, intervals, cand, cap_s, tail_s, tile_mask=None, dump: bool = True,
+          n_threads: int = 1) -> ScoreResult:
+    """Acquisition scores.  ``intervals`` has cap_lo, cap_hi, tail_lo,
+    tail_hi ([O][N] float32) and measured ([O][N] uint8)."""
+    ref = _ProblemRef(problem)
+    N = ref.n_cells
+    cl = np.ascontiguousarray(intervals.cap_lo, dtype=np.float32).reshape(-1, N)
+    O = cl.shape[0]
+    ch = np.ascontiguousarray(intervals.cap_hi, dtype=np.float32).reshape(O, N)
+    tl = np.ascontiguousarray(intervals.tail_lo, dtype=np.float32).reshape(O, N)
+    th = np.ascontiguousarray(intervals.tail_hi, dtype=np.float32).reshape(O, N)
+    ms = np.ascontiguousarray(intervals.measured, dtype=np.uint8).reshape(O, N)
+    cand = np.ascontiguousarray(cand, dtype=np.int32)
+    E = len(cand)
+    cs = np.ascontiguousarray(cap_s, dtype=np.float32).reshape(O, E, -1)
+    ts = np.ascontiguousarray(tail_s, dtype=np.float32).reshape(O, E, -1)
+    S = cs.shape[2]
+    sc = np.zeros((O, E), dtype=np.float64)
+    gap = np.zeros(O, dtype=np.float64)
+    best = np.full(O, -1, dtype=np.int32)
+    td = np.zeros((O, E, S, 2), dtype=np.float32) if dump else None
+    tm = None if tile_mask is None else np.ascontiguousarray(tile_mask, dtype=np.uint8).reshape(O * E)
+    rc = _load().orc_score(ctypes.byref(ref.s), O, _ptr(cl, ctypes.c_float), _ptr(ch, ctypes.c_float),
+                           _ptr(tl, ctypes.c_float), _ptr(th, ctypes.c_float), _ptr(ms, ctypes.c_uint8),
+                           _ptr(cand, ctypes.c_int32), E, _ptr(cs, ctypes.c_float), _ptr(ts, ctypes.c_float),
+                           S, _ptr(sc, ctypes.c_double), _ptr(gap, ctypes.c_double),
+                           _ptr(best, ctypes.c_int32), None if td is None else _ptr(td, ctypes.c_float),
+                           None if tm is None else _ptr(tm, ctypes.c_uint8), n_threads)
+    if rc != 0:
+        raise ValueError("oracle score failed")
+    return ScoreResult(sc, gap, best, td)
+
+
+@dataclass
+class CertifyResult:
+    state: np.ndarray   # [O] int32
+    gap: np.ndarray     # [O] float64
+    cons: list          # [O] Alloc (conservative, A-)
+    opt: list           # [O] Alloc (optimistic, A+)
+
+
+def certify(problem, intervals, eps: float = 0.05) -> CertifyResult:
+    ref = _ProblemRef(problem)
+    N = ref.n_cells
+    cl = np.ascontiguousarray(intervals.cap_lo, dtype=np.float32).reshape(-1, N)
+    O = cl.shape[0]
+    ch = np.ascontiguousarray(intervals.cap_hi, dtype=np.float32).reshape(O, N)
+    tl = np.ascontiguousarray(intervals.tail_lo, dtype=np.float32).reshape(O, N)
+    th = np.ascontiguousarray(intervals.tail_hi, dtype=np.float32).reshape(O, N)
+    ms = np.ascontiguousarray(intervals.measured, dtype=np.uint8).reshape(O, N)
+    state = np.zeros(O, dtype=np.int32)
+    gap = np.zeros(O, dtype=np.float64)
+    cons = (_Alloc * max(O, 1))()
+    opt = (_Alloc * max(O, 1))()
+    rc = _load().orc_certify(ctypes.byref(ref.s), O, _ptr(cl, ctypes.c_float), _ptr(ch, ctypes.c_float),
+                             _ptr(tl, ctypes.c_float), _ptr(th, ctypes.c_float), _ptr(ms, ctypes.c_uint8),
+                             float(eps), _ptr(state, ctypes.c_int32), cons, opt, _ptr(gap, ctypes.c_double))
+    if rc != 0:
+        raise ValueError("oracle certify failed")
+    k = len(ref.demand)
+    return CertifyResult(state, gap, [_alloc_out(cons[o], k) for o in range(O)],
+                         [_alloc_out(opt[o], k) for o in range(O)])
+
+
+def pairwise_sum(x) -> float:
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    return float(_load().orc_pairwise_sum(_ptr(x, ctypes.c_double), len(x)))
