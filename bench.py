@@ -1,0 +1,218 @@
+#!/usr/bin/env python3
+"""Throughput of libfleetsieve's acquisition scorer on one MI355X.
+
+A step is one fs_score_candidates call over the whole batch of the 4-class
+workload (TP {1,2,4,8}, G = 64 GPUs, 8 load levels, 128 candidate cells x
+4096 sampled outcomes x 16 reveal orders): base solves of every order, every
+scenario of every unmeasured candidate (two allocation solves each), scores
+and the argmax.  Inputs are synthetic (seeded) and resident in HBM before
+timing starts.
+
+Prints one JSON line.  The roofline object reports the dominant kernel (the
+per-scenario solve) against the VALU issue peak; its duration is measured
+with HIP events recorded by the library on the same stream.  The CPU
+baseline is the plain oracle timed on a bounded sample of the same
+workload's tiles.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "allocation scenarios/sec on 1 MI355X; % of VALU/HBM roofline; oracle-exact"
+# 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz: one 32-bit VALU operation per lane per clock.
+VALU_PEAK_OPS = 256 * 4 * 16 * 2.4e9
+# Cost of one binary32 quotient in the kernels, in VALU operations:
+# convert to binary64, multiply by the binary64 reciprocal, convert back.
+DIV_OPS = 3
+PROFILE_GLOB = os.path.join(ROOT, "profiles")
+
+
+def lane_work_per_scenario(problem, bmap_exists) -> int:
+    """Algorithmic VALU operations per scenario of the lane-per-scenario
+    kernel (two solves), counting only work the method needs:
+      per existing option: multiply, divide (DIV_OPS), min with 1, tail
+        compare, select, max into its budget slot           -> 5 + DIV_OPS
+      per class: prefix maximum over budgets 1..G           -> G - 1
+      per middle class (K - 2 of them): (max,min) pairs a = 1..g-1 for every
+        budget g = 2..G, two operations each                 -> 2 * G(G-1)/2
+      last class: pairs a = 1..G-1 for budget G              -> 2 * (G - 1)
+    The a = 0 and a = g terms of every convolution are min(x, 0) = 0 and are
+    not counted (the kernel does not compute them)."""
+    G, K = problem.budget, problem.n_classes
+    n_opt = int(bmap_exists.sum())
+    per_solve = n_opt * (5 + DIV_OPS) + K * (G - 1)
+    if K >= 2:
+        per_solve += (K - 2) * G * (G - 1) + 2 * (G - 1)
+    return 2 * per_solve
+
+
+def existing_options(problem):
+    """1 for every (class, TP, r) option whose per-replica load fits the grid."""
+    import numpy as np
+    rows = []
+    for i in range(problem.n_classes):
+        for t in problem.tp:
+            for r in range(1, problem.budget // int(t) + 1):
+                u = np.float32(problem.demand[i]) / np.float32(r)
+                rows.append(1 if np.any(u <= problem.levels) else 0)
+    return np.array(rows)
+
+
+def _kernel_source_digest() -> str:
+    h = hashlib.sha256()
+    with open(os.path.join(ROOT, "paper_2608_19659_amd", "csrc", "fs_kernels.hip"), "rb") as f:
+        h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic(kernel: str, workload_tag: str):
+    """HBM bytes per launch from the committed rocprofv3 PMC summary, or None
+    when there is none or the kernel source changed since it was taken."""
+    path = os.path.join(PROFILE_GLOB, f"{kernel}_{workload_tag}_pmc.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    d = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
+    if not m or not d or d.group(1) != _kernel_source_digest():
+        return None
+    return float(m.group(1))
+
+
+def cpu_baseline(w, target_seconds: float, threads: int):
+    """The oracle, as is, on a bounded sample of the workload's tiles."""
+    import numpy as np
+    import oracle
+    O, E, S = w.cap_s.shape
+    unmeasured = [(o, e) for o in range(O) for e in range(E) if not w.intervals.measured[o, w.cand[e]]]
+    rng = np.random.default_rng(1234)
+    order = rng.permutation(len(unmeasured))
+
+    def run(n_tiles, n_threads):
+        mask = np.zeros((O, E), np.uint8)
+        for j in order[:n_tiles]:
+            mask[unmeasured[j]] = 1
+        t0 = time.perf_counter()
+        oracle.score(w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, tile_mask=mask, dump=False,
+                     n_threads=n_threads)
+        return time.perf_counter() - t0
+
+    probe = max(threads, 1)
+    dt = run(probe, threads)
+    n_tiles = int(min(len(unmeasured), max(probe, probe * target_seconds / max(dt, 1e-3))))
+    dt = run(n_tiles, threads)
+    return {"value": n_tiles * S / dt, "unit": "scenarios/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n_tiles} unmeasured (order, candidate) tiles x {S} samples of the benchmark "
+                      f"workload, {threads} OpenMP threads, {dt:.1f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=2, help="workload configuration (default 2)")
+    ap.add_argument("--kernel", type=int, default=0, help="0 auto, 1 wave per scenario, 2 lane per scenario")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="wall budget of the oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the scorer is measured per GPU",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2608_19659_amd import fleetsieve as fs
+    from paper_2608_19659_amd.synth import CONFIGS, make_workload
+
+    dev = "cuda:0"
+    print(f"[bench] generating workload config {args.config}", file=sys.stderr, flush=True)
+    w = make_workload(args.config)
+    p = w.problem
+    O, E, S = w.cap_s.shape
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    iv = fs.DeviceIntervals.from_host(w.intervals, dev)
+    cand, cap_s, tail_s = t(w.cand), t(w.cap_s), t(w.tail_s)
+    ctx = fs.Context(0)
+    ctx.set_score_kernel(args.kernel)
+    ctx.set_option(fs.OPT_KERNEL_TIMING, 1)
+    out = fs.ScoreOutput(torch.empty((O, E), dtype=torch.float64, device=dev),
+                         torch.empty(O, dtype=torch.float64, device=dev),
+                         torch.empty(O, dtype=torch.int32, device=dev), None)
+    ws = ctx.workspace(fs.workspace_size(p, O, E, S))
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        fs.score_candidates(ctx, p, iv, cand, cap_s, tail_s, out=out, workspace=ws, stream=stream)
+    torch.cuda.synchronize()
+    ctx.kernel_timing()  # discard warm-up launches
+
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        fs.score_candidates(ctx, p, iv, cand, cap_s, tail_s, out=out, workspace=ws, stream=stream)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    total_ms = ev0.elapsed_time(ev1)
+    kernel_ms, launches = ctx.kernel_timing()
+    ms_per_step = total_ms / args.steps
+
+    measured_cand = w.intervals.measured[:, w.cand].astype(bool)
+    scenarios = int((~measured_cand).sum()) * S
+    value = scenarios / (ms_per_step / 1e3)
+
+    lane_ok = p.floor_rps is None and list(p.tp) == [1, 2, 4, 8] and p.budget in (16, 32, 64)
+    lane = args.kernel == 2 or (args.kernel == 0 and lane_ok)
+    kernel_name = f"k_score_lane<{p.budget}>" if lane else "k_score_wave"
+    roofline = None
+    if lane and launches:
+        ops = lane_work_per_scenario(p, existing_options(p))
+        kernel_avg_s = kernel_ms / launches / 1e3
+        achieved = ops * scenarios / kernel_avg_s
+        tag = f"cfg{args.config}"
+        traffic = committed_traffic(f"k_score_lane{p.budget}", tag)
+        roofline = {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_OPS / 1e12,
+                    "unit": "TOP/s", "frac": achieved / VALU_PEAK_OPS, "traffic": traffic,
+                    "kernel": kernel_name, "ops_per_scenario": ops,
+                    "kernel_ms_avg": kernel_ms / launches, "scenarios_per_launch": scenarios}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        threads = min(os.cpu_count() or 1, 16)
+        print(f"[bench] cpu baseline ({threads} threads)", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(w, args.cpu_seconds, threads)
+
+    c = CONFIGS[args.config]
+    line = {
+        "metric": METRIC, "value": value, "unit": "scenarios/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"config {args.config} ({c['name']}): {p.n_classes} classes, TP {list(p.tp)}, "
+                               f"G={p.budget}, {p.n_levels} load levels, {E} candidates x {S} samples x "
+                               f"{O} reveal orders",
+                   "scenarios_per_step": scenarios, "scenarios_in_config": O * E * S,
+                   "measured_candidates_skipped": int(measured_cand.sum()) * S,
+                   "kernel": kernel_name, "parallelism": "single GPU"},
+        "roofline": roofline, "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    ctx.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,195 @@
+/*
+ * fleetsieve.h -- C ABI of libfleetsieve, an MI355X (gfx950) implementation
+ * of FleetSieve's decision-critical acquisition scorer.
+ *
+ * The method (Sections 3-4 of the FleetSieve paper): a fleet planner assigns
+ * each workload class i one serving configuration -- a TP degree t and a
+ * replica count r -- under a GPU budget G, maximising the minimum satisfaction
+ * ratio over classes.  Performance of a (class, TP, load) cell is uncertain:
+ * capacity lies in [c_lo, c_hi] and the tail metric in [l_lo, l_hi].  The
+ * planner solves a conservative realisation (c_lo, l_hi) and an optimistic one
+ * (c_hi, l_lo); the gap between their objectives is what profiling must close.
+ * Each unmeasured cell is scored by the expected gap reduction its
+ * measurement would bring, estimated over sampled outcomes.
+ *
+ * Conventions for every call:
+ *   - Array arguments are DEVICE pointers owned by the caller, except the
+ *     fs_problem struct and what it points to, which are HOST memory read
+ *     during the call only.
+ *   - Work is enqueued on the caller's stream; the call returns without
+ *     synchronising.  Outputs are valid once the stream reaches that point.
+ *     The library allocates no device memory per call: temporary state lives
+ *     in a caller-provided workspace of at least fs_workspace_size() bytes,
+ *     which must not be used by anything else until the stream has passed
+ *     the call.
+ *   - The returned status covers argument validation and launch errors.  On
+ *     any status other than FS_OK nothing was enqueued and fs_last_error()
+ *     (thread-local) describes the problem.  No exception crosses the ABI.
+ *   - Numerics: every fulfillment value is the IEEE binary32 result of one
+ *     multiply and one correctly rounded divide, bit-identical to a plain
+ *     binary32 CPU evaluation; gaps and scores are binary64 with a fixed
+ *     summation order.  Results are deterministic run to run.
+ *
+ * Cell layout: cell(i, t, b) = (i * n_tp + t) * n_levels + b for class i,
+ * TP index t (into the ascending tp[] array) and load level b; N cells.
+ */
+#ifndef FLEETSIEVE_H
+#define FLEETSIEVE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FS_MAX_CLASSES 64
+#define FS_MAX_TP 8
+#define FS_MAX_LEVELS 32
+#define FS_MAX_BUDGET 4096
+#define FS_MAX_SAMPLES (1 << 20)
+#define FS_TP_NONE 0xFF
+
+typedef enum fs_status {
+  FS_OK = 0,
+  FS_ERR_INVALID_ARGUMENT = 1,
+  FS_ERR_UNSUPPORTED = 2,
+  FS_ERR_WORKSPACE_TOO_SMALL = 3,
+  FS_ERR_DEVICE = 4,
+  FS_ERR_INTERNAL = 5
+} fs_status;
+
+/* The three states of the decision certificate (Section 4.2). */
+typedef enum fs_cert {
+  FS_UNDECIDED = 0,
+  FS_CERTIFIED_FEASIBLE = 1,
+  FS_CERTIFIED_INFEASIBLE = 2
+} fs_cert;
+
+/* The allocation problem of Section 3 (host memory).
+ * Requirements (FS_ERR_INVALID_ARGUMENT otherwise):
+ *   1 <= n_classes <= 64, 1 <= n_tp <= 8, 1 <= n_levels <= 32,
+ *   tp[0] <= budget <= 4096; tp strictly ascending and >= 1; levels strictly
+ *   ascending, finite, > 0; demand in [2^-32, 2^32]; slo not NaN (+inf
+ *   allowed); floor_rps NULL or finite and >= 0 (0 = not a critical class).
+ * Device-side cell values must be finite and >= 0 with capacities 0 or in
+ * [2^-64, 2^64] (tails may be +inf); this keeps every quotient a normal
+ * binary32 number.  They are checked only when the environment variable
+ * FS_VALIDATE=1 is set, which adds a synchronous check per call. */
+typedef struct fs_problem {
+  int32_t n_classes;       /* K: workload classes                                */
+  int32_t n_tp;            /* |T|: candidate TP degrees                          */
+  int32_t n_levels;        /* B: per-replica load levels                         */
+  int32_t budget;          /* G: GPUs in the fleet (Eq. 3)                       */
+  const int32_t *tp;       /* [n_tp] GPUs per replica                            */
+  const float *levels;     /* [n_levels] per-replica load grid, req/s            */
+  const float *demand;     /* [K] lambda_i, offered demand, req/s                */
+  const float *slo;        /* [K] L_i, limit on the cell's tail metric (Eq. 5)   */
+  const float *floor_rps;  /* [K] critical floor in served req/s, or NULL        */
+} fs_problem;
+
+/* Per-order uncertainty state (Section 4.1), device memory, each [n_orders][N].
+ * A measured cell (measured = 1) has a point interval. */
+typedef struct fs_intervals {
+  const float *cap_lo, *cap_hi;    /* capacity bounds, req/s per replica     */
+  const float *tail_lo, *tail_hi;  /* tail-metric bounds                     */
+  const uint8_t *measured;         /* 1 = revealed                           */
+} fs_intervals;
+
+/* Allocation outputs, device memory, structure of arrays over n entries.
+ * Any pointer may be NULL to skip that output. */
+typedef struct fs_alloc {
+  float *objective;     /* [n] max-min fulfillment tau*                          */
+  uint8_t *tp_index;    /* [n][K] index into tp[], FS_TP_NONE = class unserved   */
+  uint16_t *replicas;   /* [n][K] replica count, 0 = class unserved              */
+  uint8_t *floors_met;  /* [n] 1 when every critical floor is met (or none exist)*/
+  float *goodput;       /* [n] total served req/s, binary32 sum in class order   */
+} fs_alloc;
+
+typedef struct fs_context fs_context;
+
+/* Options for fs_context_set_option. */
+typedef enum fs_option {
+  /* Scoring kernel: 0 = automatic, 1 = one wavefront per scenario (any
+   * problem), 2 = one lane per scenario (no floors, TP set {1,2,4,8},
+   * budget 16, 32 or 64).  Both give identical bits. */
+  FS_OPT_SCORE_KERNEL = 1,
+  /* 1 = record a pair of HIP events on the caller's stream around every
+   * launch of the scoring kernel (the per-scenario solve), for
+   * fs_context_kernel_timing; 0 = off (default). */
+  FS_OPT_KERNEL_TIMING = 2
+} fs_option;
+
+/* Creates a context bound to HIP device `hip_device`.  One context per host
+ * thread; a context is not thread-safe. */
+fs_status fs_context_create(int hip_device, fs_context **out);
+void fs_context_destroy(fs_context *ctx);
+fs_status fs_context_set_option(fs_context *ctx, fs_option option, int64_t value);
+
+/* Waits for the events recorded under FS_OPT_KERNEL_TIMING, returns the
+ * summed scoring-kernel time in milliseconds and the number of launches
+ * timed, and forgets them. */
+fs_status fs_context_kernel_timing(fs_context *ctx, double *total_ms, int64_t *launches);
+
+/* Thread-local description of the last failure in this thread. */
+const char *fs_last_error(void);
+
+/* Host-only check of a problem statement (no device work). */
+fs_status fs_validate_problem(const fs_problem *p);
+
+/* Workspace bytes sufficient for any call on problem p with up to n_orders
+ * orders, n_cand candidates and n_samples samples (pass 0 for unused). */
+fs_status fs_workspace_size(const fs_problem *p, int32_t n_orders, int32_t n_cand,
+                            int32_t n_samples, size_t *bytes);
+
+/* Solves the allocation (Section 3, Eq. 1-5, objective levels (1)-(2) with
+ * ties broken by fewer GPUs, then the lexicographically smaller TP vector) on
+ * n_scenarios dense point realisations: scenario j uses cap[j*N .. j*N+N-1]
+ * and tail[j*N ..].  Writes out.* for every scenario. */
+fs_status fs_solve_batch(fs_context *ctx, const fs_problem *p, const float *d_cap,
+                         const float *d_tail, int64_t n_scenarios, fs_alloc out,
+                         void *d_workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Acquisition scores (Section 4.3).  For order o, Gamma_t(o) is the gap
+ * tau(optimistic) - tau(conservative) on the order's intervals.  Scenario
+ * (o, e, s) replaces cell cand[e] in BOTH realisations by the sampled outcome
+ * (cap_s, tail_s)[o][e][s]; its gap is Gamma(o, e, s).
+ *   score[o][e] = Gamma_t(o) - (sum over s of Gamma(o, e, s)) / S
+ * with the sum taken as a pairwise tree over s zero-padded to a power of two.
+ * A candidate whose cell is measured in order o is not solved and scores
+ * exactly 0.  best[o] is the unmeasured candidate with the largest score,
+ * ties to the smaller profiling cost (TP degree of the cell), then the
+ * smaller cell index, then the smaller e; -1 if none.
+ *   d_cand    [n_cand] cell indices in [0, N)
+ *   d_cap_s, d_tail_s  [n_orders][n_cand][n_samples]
+ *   d_score   [n_orders][n_cand] binary64
+ *   d_gap_now [n_orders] binary64 (may be NULL)
+ *   d_best    [n_orders] int32 (may be NULL)
+ *   d_tau_dump NULL or [n_orders][n_cand][n_samples][2] = (tau-, tau+); for a
+ *             measured candidate it holds the order's base values. */
+fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals iv,
+                              int32_t n_orders, const int32_t *d_cand, int32_t n_cand,
+                              const float *d_cap_s, const float *d_tail_s, int32_t n_samples,
+                              double *d_score, double *d_gap_now, int32_t *d_best,
+                              float *d_tau_dump, void *d_workspace, size_t workspace_bytes,
+                              hipStream_t stream);
+
+/* Three-state certificate (Section 4.2, Algorithm 1) per order:
+ *   CERTIFIED_INFEASIBLE if some class is critical and even the optimistic
+ *     allocation cannot meet every critical floor;
+ *   CERTIFIED_FEASIBLE if the conservative allocation meets the floors, every
+ *     cell it commits to is measured with tail upper bound within the SLO,
+ *     and the gap is at most eps;
+ *   UNDECIDED otherwise.
+ * Writes state [n_orders], the conservative (cons) and optimistic (opt)
+ * allocations [n_orders] and the gap [n_orders] (binary64, may be NULL). */
+fs_status fs_certify(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders,
+                     float eps, int32_t *d_state, fs_alloc cons, fs_alloc opt, double *d_gap,
+                     void *d_workspace, size_t workspace_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FLEETSIEVE_H */

@@ -189,9 +189,13 @@ def score(problem, intervals, cand, cap_s, tail_s, tile_mask=None, dump: bool = 
     ms = np.ascontiguousarray(intervals.measured, dtype=np.uint8).reshape(O, N)
     cand = np.ascontiguousarray(cand, dtype=np.int32)
     E = len(cand)
-    cs = np.ascontiguousarray(cap_s, dtype=np.float32).reshape(O, E, -1)
-    ts = np.ascontiguousarray(tail_s, dtype=np.float32).reshape(O, E, -1)
-    S = cs.shape[2]
+    S = max(int(np.shape(cap_s)[-1]), 1)
+    cs = np.ascontiguousarray(cap_s, dtype=np.float32)
+    ts = np.ascontiguousarray(tail_s, dtype=np.float32)
+    if cs.size == 0:
+        cs = np.zeros((O, E, S), np.float32)
+        ts = np.zeros((O, E, S), np.float32)
+    cs, ts = cs.reshape(O, E, S), ts.reshape(O, E, S)
     sc = np.zeros((O, E), dtype=np.float64)
     gap = np.zeros(O, dtype=np.float64)
     best = np.full(O, -1, dtype=np.int32)

@@ -1,0 +1,329 @@
+// fs_api.cpp -- host side of libfleetsieve's C ABI (include/fleetsieve.h):
+// argument validation, problem constants, workspace layout and kernel
+// launches on the caller's stream.
+#include "fleetsieve.h"
+
+#include <cmath>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "fs_internal.h"
+
+struct fs_context {
+  int device;
+  int score_kernel;  // 0 auto, 1 wave per scenario, 2 lane per scenario
+  int timing;        // record events around the scoring kernel
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> events;
+};
+
+namespace {
+
+thread_local std::string g_error;
+
+fs_status fail(fs_status s, const std::string &msg) {
+  g_error = msg;
+  return s;
+}
+
+fs_status hip_fail(hipError_t e, const char *what) {
+  return fail(FS_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+bool env_validate() {
+  const char *v = std::getenv("FS_VALIDATE");
+  return v && v[0] == '1';
+}
+
+// Checks the problem statement and fills the kernel-side constants.
+fs_status make_problem(const fs_problem *p, fs::DevProblem *P) {
+  if (!p) return fail(FS_ERR_INVALID_ARGUMENT, "problem is NULL");
+  if (!p->tp || !p->levels || !p->demand || !p->slo)
+    return fail(FS_ERR_INVALID_ARGUMENT, "problem arrays tp/levels/demand/slo must not be NULL");
+  if (p->n_classes < 1 || p->n_classes > FS_MAX_CLASSES)
+    return fail(FS_ERR_INVALID_ARGUMENT, "n_classes must be in [1, 64]");
+  if (p->n_tp < 1 || p->n_tp > FS_MAX_TP) return fail(FS_ERR_INVALID_ARGUMENT, "n_tp must be in [1, 8]");
+  if (p->n_levels < 1 || p->n_levels > FS_MAX_LEVELS)
+    return fail(FS_ERR_INVALID_ARGUMENT, "n_levels must be in [1, 32]");
+  if (p->budget < 1 || p->budget > FS_MAX_BUDGET)
+    return fail(FS_ERR_INVALID_ARGUMENT, "budget must be in [1, 4096]");
+  std::memset(P, 0, sizeof(*P));
+  P->K = p->n_classes;
+  P->NT = p->n_tp;
+  P->B = p->n_levels;
+  P->G = p->budget;
+  P->N = P->K * P->NT * P->B;
+  for (int t = 0; t < p->n_tp; ++t) {
+    if (p->tp[t] < 1) return fail(FS_ERR_INVALID_ARGUMENT, "tp degrees must be >= 1");
+    if (t > 0 && p->tp[t] <= p->tp[t - 1])
+      return fail(FS_ERR_INVALID_ARGUMENT, "tp degrees must be strictly ascending");
+    P->tp[t] = p->tp[t];
+  }
+  if (p->budget < p->tp[0]) return fail(FS_ERR_INVALID_ARGUMENT, "budget is below the smallest TP degree");
+  for (int b = 0; b < p->n_levels; ++b) {
+    const float v = p->levels[b];
+    if (!(v > 0.0f) || !std::isfinite(v)) return fail(FS_ERR_INVALID_ARGUMENT, "levels must be finite and > 0");
+    if (b > 0 && !(v > p->levels[b - 1]))
+      return fail(FS_ERR_INVALID_ARGUMENT, "levels must be strictly ascending");
+    P->levels[b] = v;
+  }
+  for (int i = 0; i < p->n_classes; ++i) {
+    const float d = p->demand[i];
+    if (!(d >= 0x1p-32f && d <= 0x1p32f)) return fail(FS_ERR_INVALID_ARGUMENT, "demand must be in [2^-32, 2^32]");
+    if (std::isnan(p->slo[i])) return fail(FS_ERR_INVALID_ARGUMENT, "slo must not be NaN");
+    P->demand[i] = d;
+    P->slo[i] = p->slo[i];
+    P->rcp_demand[i] = 1.0 / (double)d;
+    if (p->floor_rps) {
+      const float f = p->floor_rps[i];
+      if (!(f >= 0.0f) || !std::isfinite(f))
+        return fail(FS_ERR_INVALID_ARGUMENT, "floor_rps must be finite and >= 0");
+      P->floor_rps[i] = f;
+      if (f > 0.0f) P->has_floor = 1;
+    }
+  }
+  return FS_OK;
+}
+
+struct DeviceGuard {
+  int prev = -1;
+  hipError_t err = hipSuccess;
+  explicit DeviceGuard(int dev) {
+    err = hipGetDevice(&prev);
+    if (err == hipSuccess) err = hipSetDevice(dev);
+  }
+  ~DeviceGuard() {
+    if (prev >= 0) (void)hipSetDevice(prev);
+  }
+};
+
+// FS_VALIDATE=1: wait for the flag words and turn them into a status.
+fs_status read_flags(const fs::WsLayout &L, uint8_t *ws, hipStream_t s, const char *what) {
+  int32_t flag[4] = {0, 0, 0, 0};
+  hipError_t e = hipMemcpyAsync(flag, ws + L.flag, sizeof(flag), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, what);
+  if (flag[0]) return fail(FS_ERR_INVALID_ARGUMENT, std::string(what) + ": " + std::to_string(flag[0]) +
+                                                       " cell values out of range (capacity must be 0 or in "
+                                                       "[2^-64, 2^64], tail >= 0 and not NaN)");
+  if (flag[1]) return fail(FS_ERR_INVALID_ARGUMENT, std::string(what) + ": " + std::to_string(flag[1]) +
+                                                       " candidate cell indices outside [0, N)");
+  return FS_OK;
+}
+
+fs::AllocOut to_out(const fs_alloc &a) {
+  return fs::AllocOut{a.objective, a.tp_index, a.replicas, a.floors_met, a.goodput};
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *fs_last_error(void) { return g_error.c_str(); }
+
+fs_status fs_context_create(int hip_device, fs_context **out) {
+  if (!out) return fail(FS_ERR_INVALID_ARGUMENT, "out is NULL");
+  *out = nullptr;
+  int n = 0;
+  hipError_t e = hipGetDeviceCount(&n);
+  if (e != hipSuccess || n == 0) return fail(FS_ERR_DEVICE, "no HIP device available");
+  if (hip_device < 0 || hip_device >= n) return fail(FS_ERR_INVALID_ARGUMENT, "hip_device out of range");
+  hipDeviceProp_t prop;
+  e = hipGetDeviceProperties(&prop, hip_device);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
+  if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+    return fail(FS_ERR_UNSUPPORTED, std::string("libfleetsieve is built for gfx950, device is ") + prop.gcnArchName);
+  *out = new fs_context{hip_device, 0, 0, {}};
+  return FS_OK;
+}
+
+void fs_context_destroy(fs_context *ctx) {
+  if (!ctx) return;
+  for (auto &ev : ctx->events) {
+    (void)hipEventDestroy(ev.first);
+    (void)hipEventDestroy(ev.second);
+  }
+  delete ctx;
+}
+
+fs_status fs_context_kernel_timing(fs_context *ctx, double *total_ms, int64_t *launches) {
+  if (!ctx || !total_ms || !launches) return fail(FS_ERR_INVALID_ARGUMENT, "NULL argument");
+  double sum = 0.0;
+  hipError_t err = hipSuccess;
+  for (auto &ev : ctx->events) {
+    float ms = 0.0f;
+    hipError_t e = hipEventSynchronize(ev.second);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, ev.first, ev.second);
+    if (e != hipSuccess && err == hipSuccess) err = e;
+    sum += ms;
+    (void)hipEventDestroy(ev.first);
+    (void)hipEventDestroy(ev.second);
+  }
+  *launches = (int64_t)ctx->events.size();
+  *total_ms = sum;
+  ctx->events.clear();
+  if (err != hipSuccess) return hip_fail(err, "kernel timing");
+  return FS_OK;
+}
+
+fs_status fs_context_set_option(fs_context *ctx, fs_option option, int64_t value) {
+  if (!ctx) return fail(FS_ERR_INVALID_ARGUMENT, "context is NULL");
+  if (option == FS_OPT_SCORE_KERNEL) {
+    if (value < 0 || value > 2) return fail(FS_ERR_INVALID_ARGUMENT, "score kernel must be 0, 1 or 2");
+    ctx->score_kernel = (int)value;
+    return FS_OK;
+  }
+  if (option == FS_OPT_KERNEL_TIMING) {
+    if (value < 0 || value > 1) return fail(FS_ERR_INVALID_ARGUMENT, "kernel timing must be 0 or 1");
+    ctx->timing = (int)value;
+    return FS_OK;
+  }
+  return fail(FS_ERR_INVALID_ARGUMENT, "unknown option");
+}
+
+fs_status fs_validate_problem(const fs_problem *p) {
+  fs::DevProblem P;
+  return make_problem(p, &P);
+}
+
+fs_status fs_workspace_size(const fs_problem *p, int32_t n_orders, int32_t n_cand, int32_t n_samples,
+                            size_t *bytes) {
+  if (!bytes) return fail(FS_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  if (n_orders < 0 || n_cand < 0 || n_samples < 0)
+    return fail(FS_ERR_INVALID_ARGUMENT, "sizes must be >= 0");
+  fs::DevProblem P;
+  fs_status st = make_problem(p, &P);
+  if (st != FS_OK) return st;
+  *bytes = fs::ws_layout(P, n_orders, n_cand, n_samples).total;
+  return FS_OK;
+}
+
+fs_status fs_solve_batch(fs_context *ctx, const fs_problem *p, const float *d_cap, const float *d_tail,
+                         int64_t n_scenarios, fs_alloc out, void *d_workspace, size_t workspace_bytes,
+                         hipStream_t stream) {
+  if (!ctx) return fail(FS_ERR_INVALID_ARGUMENT, "context is NULL");
+  fs::DevProblem P;
+  fs_status st = make_problem(p, &P);
+  if (st != FS_OK) return st;
+  if (n_scenarios < 0 || n_scenarios > 0x7fffffff)
+    return fail(FS_ERR_INVALID_ARGUMENT, "n_scenarios must be in [0, 2^31)");
+  if (n_scenarios > 0 && (!d_cap || !d_tail)) return fail(FS_ERR_INVALID_ARGUMENT, "cell arrays are NULL");
+  const fs::WsLayout L = fs::ws_layout(P, 0, 0, 0);
+  if (!d_workspace) return fail(FS_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  if (workspace_bytes < L.total)
+    return fail(FS_ERR_WORKSPACE_TOO_SMALL, "workspace needs " + std::to_string(L.total) + " bytes");
+  if (n_scenarios == 0) return FS_OK;
+  DeviceGuard dg(ctx->device);
+  if (dg.err != hipSuccess) return hip_fail(dg.err, "hipSetDevice");
+  uint8_t *ws = (uint8_t *)d_workspace;
+  hipError_t e = fs::launch_setup(P, nullptr, 0, ws, L, stream);
+  if (e != hipSuccess) return hip_fail(e, "set-up launch");
+  if (env_validate()) {
+    e = fs::launch_validate_cells(d_cap, d_tail, n_scenarios * (int64_t)P.N, (int32_t *)(ws + L.flag), stream);
+    if (e != hipSuccess) return hip_fail(e, "validation launch");
+    st = read_flags(L, ws, stream, "fs_solve_batch");
+    if (st != FS_OK) return st;
+  }
+  e = fs::launch_solve_batch(P, d_cap, d_tail, n_scenarios, to_out(out), ws, L, stream);
+  if (e != hipSuccess) return hip_fail(e, "solve launch");
+  return FS_OK;
+}
+
+fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders,
+                              const int32_t *d_cand, int32_t n_cand, const float *d_cap_s,
+                              const float *d_tail_s, int32_t n_samples, double *d_score,
+                              double *d_gap_now, int32_t *d_best, float *d_tau_dump, void *d_workspace,
+                              size_t workspace_bytes, hipStream_t stream) {
+  if (!ctx) return fail(FS_ERR_INVALID_ARGUMENT, "context is NULL");
+  fs::DevProblem P;
+  fs_status st = make_problem(p, &P);
+  if (st != FS_OK) return st;
+  if (n_orders < 0 || n_orders > 65535) return fail(FS_ERR_INVALID_ARGUMENT, "n_orders must be in [0, 65535]");
+  if (n_cand < 0 || n_cand > 65535) return fail(FS_ERR_INVALID_ARGUMENT, "n_cand must be in [0, 65535]");
+  if (n_cand > 0 && (n_samples < 1 || n_samples > FS_MAX_SAMPLES))
+    return fail(FS_ERR_INVALID_ARGUMENT, "n_samples must be in [1, 2^20]");
+  if (n_orders > 0 && (!iv.cap_lo || !iv.cap_hi || !iv.tail_lo || !iv.tail_hi || !iv.measured))
+    return fail(FS_ERR_INVALID_ARGUMENT, "interval arrays are NULL");
+  if (n_orders > 0 && n_cand > 0 && (!d_cand || !d_cap_s || !d_tail_s || !d_score))
+    return fail(FS_ERR_INVALID_ARGUMENT, "candidate, sample or score arrays are NULL");
+  int kernel = ctx->score_kernel;
+  if (kernel == 0) kernel = fs::lane_kernel_supported(P) ? 2 : 1;
+  if (kernel == 2 && !fs::lane_kernel_supported(P))
+    return fail(FS_ERR_UNSUPPORTED,
+                "lane-per-scenario scoring needs no floors, TP set {1,2,4,8} and budget 16, 32 or 64");
+  const int32_t S = n_cand > 0 ? n_samples : 0;
+  const fs::WsLayout L = fs::ws_layout(P, n_orders, n_cand, S);
+  if (!d_workspace) return fail(FS_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  if (workspace_bytes < L.total)
+    return fail(FS_ERR_WORKSPACE_TOO_SMALL, "workspace needs " + std::to_string(L.total) + " bytes");
+  if (n_orders == 0) return FS_OK;
+  DeviceGuard dg(ctx->device);
+  if (dg.err != hipSuccess) return hip_fail(dg.err, "hipSetDevice");
+  uint8_t *ws = (uint8_t *)d_workspace;
+  hipError_t e = fs::launch_setup(P, d_cand, n_cand, ws, L, stream);
+  if (e != hipSuccess) return hip_fail(e, "set-up launch");
+  if (env_validate()) {
+    int32_t *flag = (int32_t *)(ws + L.flag);
+    const int64_t cells = (int64_t)n_orders * P.N;
+    e = fs::launch_validate_cells(iv.cap_lo, iv.tail_lo, cells, flag, stream);
+    if (e == hipSuccess) e = fs::launch_validate_cells(iv.cap_hi, iv.tail_hi, cells, flag, stream);
+    if (e == hipSuccess && n_cand > 0)
+      e = fs::launch_validate_cells(d_cap_s, d_tail_s, (int64_t)n_orders * n_cand * S, flag, stream);
+    if (e != hipSuccess) return hip_fail(e, "validation launch");
+    st = read_flags(L, ws, stream, "fs_score_candidates");
+    if (st != FS_OK) return st;
+  }
+  fs::ScoreArgs a{iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi, iv.measured, d_cand, d_cap_s, d_tail_s,
+                  n_orders, n_cand, S, d_score, d_gap_now, d_best, d_tau_dump, ws, L, kernel,
+                  nullptr, nullptr};
+  if (ctx->timing && n_cand > 0) {
+    e = hipEventCreate(&a.ev_begin);
+    if (e == hipSuccess) e = hipEventCreate(&a.ev_end);
+    if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
+    ctx->events.emplace_back(a.ev_begin, a.ev_end);
+  }
+  e = fs::launch_score(P, a, stream);
+  if (e != hipSuccess) return hip_fail(e, "score launch");
+  return FS_OK;
+}
+
+fs_status fs_certify(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders, float eps,
+                     int32_t *d_state, fs_alloc cons, fs_alloc opt, double *d_gap, void *d_workspace,
+                     size_t workspace_bytes, hipStream_t stream) {
+  if (!ctx) return fail(FS_ERR_INVALID_ARGUMENT, "context is NULL");
+  fs::DevProblem P;
+  fs_status st = make_problem(p, &P);
+  if (st != FS_OK) return st;
+  if (n_orders < 0 || n_orders > 0x7fffffff) return fail(FS_ERR_INVALID_ARGUMENT, "n_orders must be >= 0");
+  if (std::isnan(eps)) return fail(FS_ERR_INVALID_ARGUMENT, "eps must not be NaN");
+  if (n_orders > 0 && (!iv.cap_lo || !iv.cap_hi || !iv.tail_lo || !iv.tail_hi || !iv.measured || !d_state))
+    return fail(FS_ERR_INVALID_ARGUMENT, "interval or state arrays are NULL");
+  const fs::WsLayout L = fs::ws_layout(P, 0, 0, 0);
+  if (!d_workspace) return fail(FS_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  if (workspace_bytes < L.total)
+    return fail(FS_ERR_WORKSPACE_TOO_SMALL, "workspace needs " + std::to_string(L.total) + " bytes");
+  if (n_orders == 0) return FS_OK;
+  DeviceGuard dg(ctx->device);
+  if (dg.err != hipSuccess) return hip_fail(dg.err, "hipSetDevice");
+  uint8_t *ws = (uint8_t *)d_workspace;
+  hipError_t e = fs::launch_setup(P, nullptr, 0, ws, L, stream);
+  if (e != hipSuccess) return hip_fail(e, "set-up launch");
+  if (env_validate()) {
+    int32_t *flag = (int32_t *)(ws + L.flag);
+    const int64_t cells = (int64_t)n_orders * P.N;
+    e = fs::launch_validate_cells(iv.cap_lo, iv.tail_lo, cells, flag, stream);
+    if (e == hipSuccess) e = fs::launch_validate_cells(iv.cap_hi, iv.tail_hi, cells, flag, stream);
+    if (e != hipSuccess) return hip_fail(e, "validation launch");
+    st = read_flags(L, ws, stream, "fs_certify");
+    if (st != FS_OK) return st;
+  }
+  e = fs::launch_certify(P, iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi, iv.measured, n_orders, eps,
+                         d_state, to_out(cons), to_out(opt), d_gap, ws, L, stream);
+  if (e != hipSuccess) return hip_fail(e, "certify launch");
+  return FS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,101 @@
+// fs_internal.h -- structures shared by the host runtime and the gfx950
+// kernels of libfleetsieve.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace fs {
+
+constexpr int kMaxClasses = 64;
+constexpr int kMaxTp = 8;
+constexpr int kMaxLevels = 32;
+constexpr int kMaxBudget = 4096;
+constexpr int kWave = 64;
+
+// Problem constants, passed by value as a kernel argument (about 1.5 KB).
+struct DevProblem {
+  int32_t K, NT, B, G;
+  int32_t N;          // cells = K * NT * B
+  int32_t has_floor;  // some class has floor_rps > 0
+  int32_t tp[kMaxTp];
+  float levels[kMaxLevels];
+  float demand[kMaxClasses];
+  float slo[kMaxClasses];
+  float floor_rps[kMaxClasses];
+  // binary64 reciprocal of each demand, correctly rounded.  For binary32 x,
+  // fl32(fl64(x * rcp)) equals the correctly rounded binary32 x / demand
+  // whenever the quotient is a normal number (the binary64 error, at most
+  // 2^-52 relative, is below the distance from any binary32 rounding
+  // midpoint, at least 2^-50 relative).
+  double rcp_demand[kMaxClasses];
+};
+
+// Where a candidate cell enters the allocation: its class, TP index, load
+// level, and the replica counts [rlo, rhi] whose per-replica load falls in
+// that level (contiguous, since the level is nonincreasing in r).  cls < 0
+// marks a candidate index outside [0, N).
+struct CandInfo {
+  int32_t cls, ti, rlo, rhi;
+  int32_t cell, tp;  // cell index, TP degree (profiling cost per second)
+  int32_t pad0, pad1;
+};
+
+// Workspace layout; every region is 256-byte aligned.
+struct WsLayout {
+  size_t bmap;     // int8  [K][G+1]   load level of r replicas (-1 = none)
+  size_t cand;     // CandInfo [E]
+  size_t base;     // int32 [O][2]     base tau bits (conservative, optimistic)
+  size_t opts;     // float [O][2][K][PP][2] option (cap, tail), lane kernel only
+  size_t partial;  // double [O][E][ceil(S/64)]
+  size_t flag;     // int32 [4]        validation / error flags
+  size_t total;
+  int64_t n_partial;  // ceil(S / 64)
+  int32_t pp;         // options per class of the lane kernel (0 if unused)
+};
+
+WsLayout ws_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S);
+
+// Lane-per-scenario scoring supports these shapes.
+bool lane_kernel_supported(const DevProblem &P);
+int lane_kernel_options(int G);
+
+// ---- launchers (fs_kernels.hip) --------------------------------------------
+struct ScoreArgs {
+  const float *cap_lo, *cap_hi, *tail_lo, *tail_hi;
+  const uint8_t *measured;
+  const int32_t *cand;
+  const float *cap_s, *tail_s;
+  int32_t O, E, S;
+  double *score, *gap_now;
+  int32_t *best;
+  float *tau_dump;
+  uint8_t *ws;
+  WsLayout L;
+  int kernel;  // 1 = wave per scenario, 2 = lane per scenario
+  hipEvent_t ev_begin, ev_end;  // recorded around the scoring kernel if set
+};
+
+struct AllocOut {
+  float *objective;
+  uint8_t *tp_index;
+  uint16_t *replicas;
+  uint8_t *floors_met;
+  float *goodput;
+};
+
+hipError_t launch_setup(const DevProblem &P, const int32_t *cand, int32_t E, uint8_t *ws,
+                        const WsLayout &L, hipStream_t s);
+hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s);
+hipError_t launch_solve_batch(const DevProblem &P, const float *cap, const float *tail, int64_t n,
+                              AllocOut out, uint8_t *ws, const WsLayout &L, hipStream_t s);
+hipError_t launch_certify(const DevProblem &P, const float *cap_lo, const float *cap_hi,
+                          const float *tail_lo, const float *tail_hi, const uint8_t *measured,
+                          int32_t O, float eps, int32_t *state, AllocOut cons, AllocOut opt,
+                          double *gap, uint8_t *ws, const WsLayout &L, hipStream_t s);
+// Device-side input checks (FS_VALIDATE=1): counts bad values into flag[0].
+hipError_t launch_validate_cells(const float *cap, const float *tail, int64_t n, int32_t *flag,
+                                 hipStream_t s);
+
+}  // namespace fs

@@ -1,0 +1,808 @@
+// fs_kernels.hip -- gfx950 kernels of libfleetsieve.
+//
+// The allocation (FleetSieve, Section 3, Eq. 1-5): class i picks one
+// configuration, t GPUs per replica and r replicas (t * r GPUs), or nothing;
+// its satisfaction ratio is min(1, fl32(fl32(r * c) / lambda_i)) when the
+// configuration's tail is within the SLO (Eq. 5), else 0; the total GPUs are
+// at most G (Eq. 3); the objective maximises the minimum ratio over classes
+// after enforcing critical floors whenever they can be met.  Its value is
+// tau* = D_K[G] of the (max,min) knapsack
+//   B_i[g] = best ratio of class i with at most g GPUs,
+//   D_1 = B_1,  D_k[g] = max_{a <= g} min(D_{k-1}[g - a], B_k[a]).
+// Tie-breaks (fewer GPUs, then the lexicographically smaller TP vector) are
+// resolved after tau* is known: each class takes the fewest GPUs reaching
+// tau* and, among those options, the smallest TP.
+//
+// Two kernel families:
+//  * wave-per-scenario (any problem): one wavefront owns a scenario; per-class
+//    tables live in LDS; options are spread over lanes and merged with LDS
+//    atomic max; prefix maxima use a wave scan; the DP spreads budgets over
+//    lanes and reduces with cross-lane max.
+//  * lane-per-scenario (no floors, TP set {1,2,4,8}, G in {16,32,64}): one
+//    lane owns a scenario; the 64 lanes of a wavefront are 64 samples of the
+//    same (order, candidate), so the order's option values are wave-uniform
+//    scalar loads and only the candidate's own cell differs per lane.  All
+//    tables are register-resident and the DP is fully unrolled.
+//
+// Fulfillment values are compared as int32 bit patterns: for binary32 values
+// >= +0 the integer order is the float order, -1 marks "no allowed choice"
+// (critical floors) and a -0 ratio (from a -0 capacity) sorts below every
+// usable value, which is how a zero ratio behaves in the max.
+#include "fs_internal.h"
+
+#include <limits.h>
+
+namespace fs {
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// Scalar helpers shared by both kernel families.
+// ---------------------------------------------------------------------------
+
+// Ratio of r replicas of a cell (cap, tail) for a class with SLO `slo` and
+// demand reciprocal `rcp`, as int32 bits (0 when the tail breaks the SLO).
+__device__ __forceinline__ int ratio_bits(float cap, float tail, int r, float slo, double rcp) {
+  const float capacity = (float)r * cap;
+  const float q = (float)((double)capacity * rcp);
+  const float f = fminf(q, 1.0f);
+  return (tail <= slo) ? __float_as_int(f) : 0;
+}
+
+__device__ __forceinline__ float served_rps(float cap, int r, float demand) {
+  const float capacity = (float)r * cap;
+  return capacity < demand ? capacity : demand;
+}
+
+__device__ __forceinline__ bool floor_ok(float cap, float tail, int r, float slo, float demand,
+                                         float floor_rps) {
+  return (tail <= slo) && served_rps(cap, r, demand) >= floor_rps;
+}
+
+__device__ __forceinline__ int wave_max(int v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v = max(v, __shfl_xor(v, off, kWave));
+  return v;
+}
+
+__device__ __forceinline__ int wave_min(int v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v = min(v, __shfl_xor(v, off, kWave));
+  return v;
+}
+
+// Inclusive prefix maximum across the 64 lanes.
+__device__ __forceinline__ int wave_scan_max(int v, int lane) {
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int t = __shfl_up(v, off, kWave);
+    if (lane >= off) v = max(v, t);
+  }
+  return v;
+}
+
+// Pairwise sum over the 64 lanes: after the step with offset 2^j every lane
+// holds the sum of its aligned block of 2^(j+1) lanes, so the association is
+// the balanced binary tree over lane order.
+__device__ __forceinline__ double wave_pairwise_sum(double v) {
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+__device__ __forceinline__ int cell_of(const DevProblem &P, int k, int ti, int b) {
+  return (k * P.NT + ti) * P.B + b;
+}
+
+// ---------------------------------------------------------------------------
+// Set-up: load level of every (class, replica count), and candidate info.
+// ---------------------------------------------------------------------------
+__global__ void k_setup_bucket(DevProblem P, int8_t *__restrict__ bmap, int32_t *__restrict__ flag) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx < 4) flag[idx] = 0;
+  const int n = P.K * (P.G + 1);
+  if (idx >= n) return;
+  const int k = idx / (P.G + 1), r = idx % (P.G + 1);
+  int b = -1;
+  if (r >= 1) {
+    // offered load per replica, binary32; smallest level at least that load
+    const float per_replica = P.demand[k] / (float)r;
+    for (int j = 0; j < P.B; ++j)
+      if (per_replica <= P.levels[j]) { b = j; break; }
+  }
+  bmap[idx] = (int8_t)b;
+}
+
+__global__ void k_setup_cand(DevProblem P, const int32_t *__restrict__ cand, int32_t E,
+                             const int8_t *__restrict__ bmap, CandInfo *__restrict__ info,
+                             int32_t *__restrict__ flag) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= E) return;
+  const int cell = cand[e];
+  CandInfo ci;
+  ci.cell = cell;
+  ci.pad0 = ci.pad1 = 0;
+  if (cell < 0 || cell >= P.N) {
+    ci.cls = -1; ci.ti = 0; ci.rlo = 1; ci.rhi = 0; ci.tp = 0;
+    atomicAdd(&flag[1], 1);
+    info[e] = ci;
+    return;
+  }
+  const int b = cell % P.B;
+  const int ti = (cell / P.B) % P.NT;
+  const int k = cell / (P.B * P.NT);
+  const int t = P.tp[ti];
+  int rlo = 1, rhi = 0;
+  bool seen = false;
+  for (int r = 1; t * r <= P.G; ++r) {
+    if (bmap[k * (P.G + 1) + r] == b) {
+      if (!seen) { rlo = r; seen = true; }
+      rhi = r;
+    }
+  }
+  ci.cls = k; ci.ti = ti; ci.rlo = rlo; ci.rhi = rhi; ci.tp = t;
+  info[e] = ci;
+}
+
+// ---------------------------------------------------------------------------
+// Wave-per-scenario solver.
+// ---------------------------------------------------------------------------
+
+// A point realisation: base cell arrays with at most one cell replaced.
+struct Realisation {
+  const float *cap;
+  const float *tail;
+  int ocell;
+  float ocap, otail;
+  __device__ __forceinline__ float c(int cell) const { return cell == ocell ? ocap : cap[cell]; }
+  __device__ __forceinline__ float l(int cell) const { return cell == ocell ? otail : tail[cell]; }
+};
+
+struct WaveAlloc {  // optional per-class allocation (LDS), filled on request
+  int *tp_index;    // [K] -1 = none
+  int *replicas;    // [K]
+};
+
+// Solves one realisation with the whole wavefront.  lds must hold
+// 3 * (G + 1) ints.  Returns tau* as int32 bits; *floors_met receives
+// objective level (1)'s outcome.  When alloc is non-null, the canonical
+// allocation is written to it and *goodput (lane 0) receives the served total.
+__device__ int wave_solve(const DevProblem &P, const int8_t *__restrict__ bmap,
+                          const Realisation &R, int *lds, int *floors_met_out,
+                          const WaveAlloc *alloc, float *goodput) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int K = P.K, G = P.G;
+
+  // Objective level (1): can every critical floor be met within G?
+  int floors_met = 1;
+  if (P.has_floor) {
+    int need = 0;
+    bool ok = true;
+    for (int k = 0; k < K && ok; ++k) {
+      if (!(P.floor_rps[k] > 0.0f)) continue;
+      int cheapest = INT_MAX;
+      for (int ti = 0; ti < P.NT; ++ti) {
+        const int t = P.tp[ti];
+        for (int r = 1 + lane; t * r <= G; r += kWave) {
+          const int b = bmap[k * (G + 1) + r];
+          if (b < 0) continue;
+          const int cell = cell_of(P, k, ti, b);
+          if (floor_ok(R.c(cell), R.l(cell), r, P.slo[k], P.demand[k], P.floor_rps[k]))
+            cheapest = min(cheapest, t * r);
+        }
+      }
+      cheapest = wave_min(cheapest);
+      if (cheapest == INT_MAX) ok = false;
+      else need += cheapest;
+    }
+    floors_met = (ok && need <= G) ? 1 : 0;
+  }
+  *floors_met_out = floors_met;
+
+  int *D = lds, *T = lds + (G + 1), *Dn = lds + 2 * (G + 1);
+  int tau = 0;
+  for (int k = 0; k < K; ++k) {
+    const bool restricted = P.has_floor && floors_met && (P.floor_rps[k] > 0.0f);
+    const int init = restricted ? -1 : 0;
+    for (int g = lane; g <= G; g += kWave) T[g] = init;
+    __syncthreads();
+    for (int ti = 0; ti < P.NT; ++ti) {
+      const int t = P.tp[ti];
+      for (int r = 1 + lane; t * r <= G; r += kWave) {
+        const int b = bmap[k * (G + 1) + r];
+        if (b < 0) continue;
+        const int cell = cell_of(P, k, ti, b);
+        const float c = R.c(cell), l = R.l(cell);
+        if (restricted && !floor_ok(c, l, r, P.slo[k], P.demand[k], P.floor_rps[k])) continue;
+        atomicMax(&T[t * r], ratio_bits(c, l, r, P.slo[k], P.rcp_demand[k]));
+      }
+    }
+    __syncthreads();
+    // B_k[g] = max over options with at most g GPUs: prefix maximum.
+    int carry = INT_MIN;
+    for (int base = 0; base <= G; base += kWave) {
+      const int g = base + lane;
+      int v = (g <= G) ? T[g] : INT_MIN;
+      v = max(wave_scan_max(v, lane), carry);
+      if (g <= G) T[g] = v;
+      carry = __shfl(v, kWave - 1, kWave);
+    }
+    __syncthreads();
+    if (k == 0) {
+      int *tmp = D; D = T; T = tmp;
+    } else if (k + 1 < K) {
+      for (int g = lane; g <= G; g += kWave) {
+        int best = INT_MIN;
+        for (int a = 0; a <= g; ++a) best = max(best, min(D[g - a], T[a]));
+        Dn[g] = best;
+      }
+      __syncthreads();
+      int *tmp = D; D = Dn; Dn = tmp;
+    } else {
+      int best = INT_MIN;
+      for (int a = lane; a <= G; a += kWave) best = max(best, min(D[G - a], T[a]));
+      tau = wave_max(best);
+    }
+    __syncthreads();
+  }
+  if (K == 1) tau = D[G];
+
+  if (alloc) {
+    float gp = 0.0f;
+    for (int k = 0; k < K; ++k) {
+      const bool restricted = P.has_floor && floors_met && (P.floor_rps[k] > 0.0f);
+      int ti_sel = -1, r_sel = 0;
+      if (restricted || tau > 0) {
+        // fewest GPUs reaching tau, then the smallest TP index
+        int key = INT_MAX;
+        for (int ti = 0; ti < P.NT; ++ti) {
+          const int t = P.tp[ti];
+          for (int r = 1 + lane; t * r <= G; r += kWave) {
+            const int b = bmap[k * (G + 1) + r];
+            if (b < 0) continue;
+            const int cell = cell_of(P, k, ti, b);
+            const float c = R.c(cell), l = R.l(cell);
+            if (restricted && !floor_ok(c, l, r, P.slo[k], P.demand[k], P.floor_rps[k])) continue;
+            if (ratio_bits(c, l, r, P.slo[k], P.rcp_demand[k]) < tau) continue;
+            key = min(key, (t * r) * 16 + ti);
+          }
+        }
+        key = wave_min(key);
+        if (key != INT_MAX) {
+          ti_sel = key & 15;
+          r_sel = (key >> 4) / P.tp[ti_sel];
+        }
+      }
+      if (lane == 0) {
+        alloc->tp_index[k] = ti_sel;
+        alloc->replicas[k] = r_sel;
+        if (r_sel > 0) {
+          const int cell = cell_of(P, k, ti_sel, bmap[k * (G + 1) + r_sel]);
+          gp += served_rps(R.c(cell), r_sel, P.demand[k]);
+        }
+      }
+    }
+    if (lane == 0) *goodput = gp;
+    __syncthreads();
+  }
+  return tau;
+}
+
+__device__ __forceinline__ void write_alloc(const AllocOut &out, int64_t j, int K, int tau,
+                                            int floors_met, float goodput, const WaveAlloc &wa) {
+  const int lane = threadIdx.x & (kWave - 1);
+  if (lane == 0) {
+    if (out.objective) out.objective[j] = __int_as_float(tau);
+    if (out.floors_met) out.floors_met[j] = (uint8_t)floors_met;
+    if (out.goodput) out.goodput[j] = goodput;
+  }
+  for (int k = lane; k < K; k += kWave) {
+    if (out.tp_index) out.tp_index[j * K + k] = wa.tp_index[k] < 0 ? 0xFF : (uint8_t)wa.tp_index[k];
+    if (out.replicas) out.replicas[j * K + k] = (uint16_t)wa.replicas[k];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Dense batch solve: one wavefront per scenario.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void k_solve_dense(DevProblem P, const int8_t *__restrict__ bmap,
+                                                    const float *__restrict__ cap,
+                                                    const float *__restrict__ tail, int64_t n,
+                                                    AllocOut out) {
+  extern __shared__ int lds[];
+  const int64_t j = blockIdx.x;
+  if (j >= n) return;
+  int *tp_index = lds + 3 * (P.G + 1);
+  int *replicas = tp_index + kMaxClasses;
+  WaveAlloc wa{tp_index, replicas};
+  Realisation R{cap + j * P.N, tail + j * P.N, -1, 0.0f, 0.0f};
+  int fm;
+  float gp;
+  const int tau = wave_solve(P, bmap, R, lds, &fm, &wa, &gp);
+  write_alloc(out, j, P.K, tau, fm, gp, wa);
+}
+
+// ---------------------------------------------------------------------------
+// Base realisations of each order: tau(conservative), tau(optimistic).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void k_base(DevProblem P, const int8_t *__restrict__ bmap,
+                                             const float *__restrict__ cap_lo,
+                                             const float *__restrict__ cap_hi,
+                                             const float *__restrict__ tail_lo,
+                                             const float *__restrict__ tail_hi,
+                                             int32_t *__restrict__ base) {
+  extern __shared__ int lds[];
+  const int R = blockIdx.x, o = blockIdx.y;
+  const size_t off = (size_t)o * P.N;
+  // Section 4.1: conservative = (low capacity, high tail); optimistic = (high, low).
+  Realisation real = R == 0 ? Realisation{cap_lo + off, tail_hi + off, -1, 0.0f, 0.0f}
+                            : Realisation{cap_hi + off, tail_lo + off, -1, 0.0f, 0.0f};
+  int fm;
+  const int tau = wave_solve(P, bmap, real, lds, &fm, nullptr, nullptr);
+  if (threadIdx.x == 0) base[o * 2 + R] = tau;
+}
+
+// ---------------------------------------------------------------------------
+// Scores, wave per scenario: block (chunk, e, o) handles samples
+// [64*chunk, 64*chunk + 64) one after another; lane j keeps Gamma of sample j.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void k_score_wave(DevProblem P, const int8_t *__restrict__ bmap,
+                                                   const CandInfo *__restrict__ info,
+                                                   const float *__restrict__ cap_lo,
+                                                   const float *__restrict__ cap_hi,
+                                                   const float *__restrict__ tail_lo,
+                                                   const float *__restrict__ tail_hi,
+                                                   const uint8_t *__restrict__ measured,
+                                                   const float *__restrict__ cap_s,
+                                                   const float *__restrict__ tail_s, int32_t E,
+                                                   int32_t S, const int32_t *__restrict__ base,
+                                                   double *__restrict__ partial, int64_t n_partial,
+                                                   float *__restrict__ tau_dump) {
+  extern __shared__ int lds[];
+  const int chunk = blockIdx.x, e = blockIdx.y, o = blockIdx.z;
+  const int lane = threadIdx.x;
+  const CandInfo ci = info[e];
+  const size_t tile = (size_t)o * E + e;
+  const size_t off = (size_t)o * P.N;
+  if (ci.cls < 0) return;
+  if (measured[off + ci.cell]) {
+    // nothing to learn from a revealed cell: not solved, score 0
+    const int s = chunk * kWave + lane;
+    if (tau_dump && s < S) {
+      tau_dump[(tile * S + s) * 2 + 0] = __int_as_float(base[o * 2 + 0]);
+      tau_dump[(tile * S + s) * 2 + 1] = __int_as_float(base[o * 2 + 1]);
+    }
+    return;
+  }
+  double mine = 0.0;
+  const int s0 = chunk * kWave;
+  const int ns = min(kWave, S - s0);
+  for (int j = 0; j < ns; ++j) {
+    const float cs = cap_s[tile * S + s0 + j];
+    const float ts = tail_s[tile * S + s0 + j];
+    int fm;
+    Realisation rm{cap_lo + off, tail_hi + off, ci.cell, cs, ts};
+    const int tm = wave_solve(P, bmap, rm, lds, &fm, nullptr, nullptr);
+    Realisation rp{cap_hi + off, tail_lo + off, ci.cell, cs, ts};
+    const int tp = wave_solve(P, bmap, rp, lds, &fm, nullptr, nullptr);
+    if (lane == j) mine = (double)__int_as_float(tp) - (double)__int_as_float(tm);
+    if (tau_dump && lane == 0) {
+      tau_dump[(tile * S + s0 + j) * 2 + 0] = __int_as_float(tm);
+      tau_dump[(tile * S + s0 + j) * 2 + 1] = __int_as_float(tp);
+    }
+  }
+  const double sum = wave_pairwise_sum(mine);
+  if (lane == 0) partial[tile * n_partial + chunk] = sum;
+}
+
+// ---------------------------------------------------------------------------
+// Scores, lane per scenario.  Option p of class k enumerates (TP index ti,
+// replicas r) as p = off(ti) + r - 1 with off = 0, G, G + G/2, G + G/2 + G/4.
+// ---------------------------------------------------------------------------
+template <int G>
+struct LaneShape {
+  static constexpr int PP = G + G / 2 + G / 4 + G / 8;
+  static constexpr int off(int ti) {
+    return ti == 0 ? 0 : ti == 1 ? G : ti == 2 ? G + G / 2 : G + G / 2 + G / 4;
+  }
+};
+
+// Per order and realisation, the (cap, tail) every option reads: a gather of
+// the order's cells through the load-level map.  Missing options read a zero
+// capacity, whose ratio is 0.
+template <int G>
+__global__ void k_gather_options(DevProblem P, const int8_t *__restrict__ bmap,
+                                 const float *__restrict__ cap_lo, const float *__restrict__ cap_hi,
+                                 const float *__restrict__ tail_lo,
+                                 const float *__restrict__ tail_hi, float *__restrict__ opts) {
+  constexpr int PP = LaneShape<G>::PP;
+  const int p = threadIdx.x;
+  const int k = blockIdx.x, R = blockIdx.y, o = blockIdx.z;
+  if (p >= PP) return;
+  int ti = 0;
+  while (ti < 3 && p >= LaneShape<G>::off(ti + 1)) ++ti;
+  const int r = p - LaneShape<G>::off(ti) + 1;
+  const int b = bmap[k * (G + 1) + r];
+  float c = 0.0f, l = 0.0f;
+  if (b >= 0) {
+    const size_t cell = (size_t)o * P.N + cell_of(P, k, ti, b);
+    c = R == 0 ? cap_lo[cell] : cap_hi[cell];
+    l = R == 0 ? tail_hi[cell] : tail_lo[cell];
+  }
+  const size_t dst = ((((size_t)o * 2 + R) * P.K + k) * PP + p);
+  opts[dst * 2 + 0] = c;
+  opts[dst * 2 + 1] = l;
+}
+
+// B[g-1] = best ratio with at most g GPUs, before the prefix maximum: every
+// option max-merged into the slot of its exact GPU count.
+template <int G, bool kCandClass>
+__device__ __forceinline__ void lane_table(int (&T)[G], const float *__restrict__ opt, float slo,
+                                           double rcp, int te, int rlo, int rhi, float cs, float ls) {
+#pragma unroll
+  for (int g = 0; g < G; ++g) T[g] = 0;
+#pragma unroll
+  for (int ti = 0; ti < 4; ++ti) {
+#pragma unroll
+    for (int r = 1; r <= (G >> ti); ++r) {
+      const int p = LaneShape<G>::off(ti) + r - 1;
+      float c = opt[2 * p], l = opt[2 * p + 1];
+      if (kCandClass) {
+        const bool sampled = (ti == te) & (r >= rlo) & (r <= rhi);
+        c = sampled ? cs : c;
+        l = sampled ? ls : l;
+      }
+      const int f = ratio_bits(c, l, r, slo, rcp);
+      T[(r << ti) - 1] = max(T[(r << ti) - 1], f);
+    }
+  }
+#pragma unroll
+  for (int g = 1; g < G; ++g) T[g] = max(T[g], T[g - 1]);
+}
+
+// D <- D (max,min) T in place.  Entries are budgets 1..G; budget 0 is 0 in
+// both, so the a = 0 and a = g terms are 0 and every other term is >= 0.
+// Targets run downwards so D[g - a] (a >= 1) is still the old value.
+template <int G>
+__device__ __forceinline__ void lane_conv(int (&D)[G], const int (&T)[G]) {
+#pragma unroll
+  for (int g = G; g >= 2; --g) {
+    int acc = min(D[g - 2], T[0]);
+#pragma unroll
+    for (int a = 2; a <= g - 1; ++a) acc = max(acc, min(D[g - a - 1], T[a - 1]));
+    D[g - 1] = acc;
+  }
+  D[0] = 0;
+}
+
+template <int G>
+__device__ __forceinline__ int lane_final(const int (&D)[G], const int (&T)[G]) {
+  int acc = min(D[G - 2], T[0]);
+#pragma unroll
+  for (int a = 2; a <= G - 1; ++a) acc = max(acc, min(D[G - a - 1], T[a - 1]));
+  return acc;
+}
+
+template <int G>
+__global__ __launch_bounds__(256) void k_score_lane(DevProblem P, const CandInfo *__restrict__ info,
+                                                    const uint8_t *__restrict__ measured,
+                                                    const float *__restrict__ opts,
+                                                    const float *__restrict__ cap_s,
+                                                    const float *__restrict__ tail_s, int32_t E,
+                                                    int32_t S, const int32_t *__restrict__ base,
+                                                    double *__restrict__ partial,
+                                                    int64_t n_partial,
+                                                    float *__restrict__ tau_dump) {
+  constexpr int PP = LaneShape<G>::PP;
+  __shared__ double wsum[4];
+  const int chunk = blockIdx.x, e = blockIdx.y, o = blockIdx.z;
+  const int s = chunk * 256 + threadIdx.x;
+  const CandInfo ci = info[e];
+  const size_t tile = (size_t)o * E + e;
+  if (ci.cls < 0) return;
+  if (measured[(size_t)o * P.N + ci.cell]) {
+    if (tau_dump && s < S) {
+      tau_dump[(tile * S + s) * 2 + 0] = __int_as_float(base[o * 2 + 0]);
+      tau_dump[(tile * S + s) * 2 + 1] = __int_as_float(base[o * 2 + 1]);
+    }
+    return;
+  }
+  const bool live = s < S;
+  float cs = 0.0f, ls = 0.0f;
+  if (live) {
+    cs = cap_s[tile * S + s];
+    ls = tail_s[tile * S + s];
+  }
+  const int K = P.K;
+  int tau_m = 0, tau_p = 0;
+#pragma unroll 1
+  for (int R = 0; R < 2; ++R) {
+    const float *opt = opts + (((size_t)o * 2 + R) * K) * PP * 2;
+    int D[G], T[G];
+    int tau = 0;
+#pragma unroll 1
+    for (int k = 0; k < K; ++k) {
+      const float *ok = opt + (size_t)k * PP * 2;
+      if (k == ci.cls)
+        lane_table<G, true>(T, ok, P.slo[k], P.rcp_demand[k], ci.ti, ci.rlo, ci.rhi, cs, ls);
+      else
+        lane_table<G, false>(T, ok, P.slo[k], P.rcp_demand[k], 0, 1, 0, 0.0f, 0.0f);
+      if (k == 0) {
+#pragma unroll
+        for (int g = 0; g < G; ++g) D[g] = T[g];
+      } else if (k + 1 < K) {
+        lane_conv<G>(D, T);
+      } else {
+        tau = lane_final<G>(D, T);
+      }
+    }
+    if (K == 1) tau = D[G - 1];
+    if (R == 0) tau_m = tau;
+    else tau_p = tau;
+  }
+  double gam = 0.0;
+  if (live) {
+    gam = (double)__int_as_float(tau_p) - (double)__int_as_float(tau_m);
+    if (tau_dump) {
+      tau_dump[(tile * S + s) * 2 + 0] = __int_as_float(tau_m);
+      tau_dump[(tile * S + s) * 2 + 1] = __int_as_float(tau_p);
+    }
+  }
+  gam = wave_pairwise_sum(gam);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) wsum[w] = gam;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    // 256 samples per block = four 64-sample blocks of the pairwise tree
+    const double sum = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
+    // a block covers 4 of the 64-sample partial slots; the first holds the
+    // sum, the other three hold zeros, which the final tree adds exactly
+    const int64_t slot = (int64_t)chunk * 4;
+    partial[tile * n_partial + slot] = sum;
+    for (int q = 1; q < 4 && slot + q < n_partial; ++q) partial[tile * n_partial + slot + q] = 0.0;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Finalize: score = Gamma_t - (pairwise sum of partials) / S, and the argmax.
+// ---------------------------------------------------------------------------
+struct Pick {
+  double score;
+  int tp, cell, e;  // e < 0: nothing
+};
+
+__device__ __forceinline__ bool better(const Pick &a, const Pick &b) {
+  if (a.e < 0) return false;
+  if (b.e < 0) return true;
+  if (a.score != b.score) return a.score > b.score;
+  if (a.tp != b.tp) return a.tp < b.tp;
+  if (a.cell != b.cell) return a.cell < b.cell;
+  return a.e < b.e;
+}
+
+__global__ __launch_bounds__(64) void k_finalize(DevProblem P, const CandInfo *__restrict__ info,
+                                                 const uint8_t *__restrict__ measured, int32_t E,
+                                                 int32_t S, const int32_t *__restrict__ base,
+                                                 const double *__restrict__ partial,
+                                                 int64_t n_partial, double *__restrict__ score,
+                                                 double *__restrict__ gap_now,
+                                                 int32_t *__restrict__ best) {
+  const int o = blockIdx.x, lane = threadIdx.x;
+  const double gap = (double)__int_as_float(base[o * 2 + 1]) - (double)__int_as_float(base[o * 2 + 0]);
+  if (lane == 0 && gap_now) gap_now[o] = gap;
+  Pick mine{0.0, 0, 0, -1};
+  for (int e = lane; e < E; e += kWave) {
+    const CandInfo ci = info[e];
+    const size_t tile = (size_t)o * E + e;
+    if (ci.cls < 0) {
+      score[tile] = __builtin_nan("");
+      continue;
+    }
+    if (measured[(size_t)o * P.N + ci.cell]) {
+      score[tile] = 0.0;
+      continue;
+    }
+    // pairwise tree over the partials, zero-padded to a power of two; the
+    // padding adds exact zeros, so the open stack folds from the top
+    const double *x = partial + tile * n_partial;
+    double stack[32];
+    int depth = 0;
+    for (int64_t i = 0; i < n_partial; ++i) {
+      double v = x[i];
+      for (int64_t m = i; m & 1; m >>= 1) v = stack[--depth] + v;
+      stack[depth++] = v;
+    }
+    double sum = stack[depth - 1];
+    for (int d = depth - 2; d >= 0; --d) sum = stack[d] + sum;
+    const double sc = gap - sum / (double)S;
+    score[tile] = sc;
+    const Pick cand{sc, ci.tp, ci.cell, e};
+    if (better(cand, mine)) mine = cand;
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    Pick other;
+    other.score = __shfl_xor(mine.score, off, kWave);
+    other.tp = __shfl_xor(mine.tp, off, kWave);
+    other.cell = __shfl_xor(mine.cell, off, kWave);
+    other.e = __shfl_xor(mine.e, off, kWave);
+    if (better(other, mine)) mine = other;
+  }
+  if (lane == 0 && best) best[o] = mine.e;
+}
+
+// ---------------------------------------------------------------------------
+// Certificate: one wavefront per order.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void k_certify(DevProblem P, const int8_t *__restrict__ bmap,
+                                                const float *__restrict__ cap_lo,
+                                                const float *__restrict__ cap_hi,
+                                                const float *__restrict__ tail_lo,
+                                                const float *__restrict__ tail_hi,
+                                                const uint8_t *__restrict__ measured, float eps,
+                                                int32_t *__restrict__ state, AllocOut cons,
+                                                AllocOut opt, double *__restrict__ gap_out) {
+  extern __shared__ int lds[];
+  const int o = blockIdx.x, lane = threadIdx.x;
+  const size_t off = (size_t)o * P.N;
+  int *tm_index = lds + 3 * (P.G + 1);
+  int *tm_rep = tm_index + kMaxClasses;
+  int *tp_index = tm_rep + kMaxClasses;
+  int *tp_rep = tp_index + kMaxClasses;
+  WaveAlloc am{tm_index, tm_rep}, ap{tp_index, tp_rep};
+  int fm_m, fm_p;
+  float gp_m, gp_p;
+  Realisation rm{cap_lo + off, tail_hi + off, -1, 0.0f, 0.0f};
+  const int tau_m = wave_solve(P, bmap, rm, lds, &fm_m, &am, &gp_m);
+  Realisation rp{cap_hi + off, tail_lo + off, -1, 0.0f, 0.0f};
+  const int tau_p = wave_solve(P, bmap, rp, lds, &fm_p, &ap, &gp_p);
+  write_alloc(cons, o, P.K, tau_m, fm_m, gp_m, am);
+  write_alloc(opt, o, P.K, tau_p, fm_p, gp_p, ap);
+  if (lane != 0) return;
+  const double gap = (double)__int_as_float(tau_p) - (double)__int_as_float(tau_m);
+  if (gap_out) gap_out[o] = gap;
+  int st;
+  if (P.has_floor && !fm_p) {
+    st = 2;  // even the optimistic allocation misses a critical floor
+  } else {
+    bool ok = fm_m != 0;
+    for (int k = 0; k < P.K && ok; ++k) {
+      const int r = tm_rep[k];
+      if (r == 0) continue;
+      const int cell = cell_of(P, k, tm_index[k], bmap[k * (P.G + 1) + r]);
+      // every committed tail upper bound must be known and within the SLO
+      if (!measured[off + cell]) ok = false;
+      else if (!(tail_hi[off + cell] <= P.slo[k])) ok = false;
+    }
+    st = (ok && gap <= (double)eps) ? 1 : 0;
+  }
+  state[o] = st;
+}
+
+__global__ void k_validate_cells(const float *__restrict__ cap, const float *__restrict__ tail,
+                                 int64_t n, int32_t *__restrict__ flag) {
+  int bad = 0;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const float c = cap[i], l = tail[i];
+    const bool cap_ok = (c == 0.0f && !signbit(c)) ||
+                        (c >= 0x1p-64f && c <= 0x1p64f);
+    const bool tail_ok = !isnan(l) && l >= 0.0f;
+    if (!cap_ok || !tail_ok) ++bad;
+  }
+  if (bad) atomicAdd(&flag[0], bad);
+}
+
+size_t lds_bytes_solver(const DevProblem &P, int n_alloc) {
+  return sizeof(int) * (3 * (size_t)(P.G + 1) + (size_t)n_alloc * 2 * kMaxClasses);
+}
+
+}  // namespace
+
+bool lane_kernel_supported(const DevProblem &P) {
+  if (P.has_floor) return false;
+  if (P.NT != 4 || P.tp[0] != 1 || P.tp[1] != 2 || P.tp[2] != 4 || P.tp[3] != 8) return false;
+  return P.G == 16 || P.G == 32 || P.G == 64;
+}
+
+int lane_kernel_options(int G) { return G + G / 2 + G / 4 + G / 8; }
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+WsLayout ws_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
+  WsLayout L{};
+  size_t at = 0;
+  L.bmap = at; at = align256(at + (size_t)P.K * (P.G + 1));
+  L.cand = at; at = align256(at + sizeof(CandInfo) * (size_t)(E > 0 ? E : 1));
+  L.base = at; at = align256(at + sizeof(int32_t) * 2 * (size_t)(O > 0 ? O : 1));
+  L.pp = lane_kernel_supported(P) ? lane_kernel_options(P.G) : 0;
+  L.opts = at; at = align256(at + sizeof(float) * 2 * (size_t)O * 2 * P.K * L.pp);
+  L.n_partial = S > 0 ? (S + kWave - 1) / kWave : 1;
+  L.partial = at; at = align256(at + sizeof(double) * (size_t)O * (size_t)E * L.n_partial);
+  L.flag = at; at = align256(at + sizeof(int32_t) * 4);
+  L.total = at;
+  return L;
+}
+
+hipError_t launch_setup(const DevProblem &P, const int32_t *cand, int32_t E, uint8_t *ws,
+                        const WsLayout &L, hipStream_t s) {
+  const int n = P.K * (P.G + 1);
+  k_setup_bucket<<<(n + 255) / 256, 256, 0, s>>>(P, (int8_t *)(ws + L.bmap), (int32_t *)(ws + L.flag));
+  if (E > 0) {
+    k_setup_cand<<<(E + 255) / 256, 256, 0, s>>>(P, cand, E, (const int8_t *)(ws + L.bmap),
+                                                (CandInfo *)(ws + L.cand), (int32_t *)(ws + L.flag));
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) {
+  const int8_t *bmap = (const int8_t *)(a.ws + a.L.bmap);
+  const CandInfo *info = (const CandInfo *)(a.ws + a.L.cand);
+  int32_t *base = (int32_t *)(a.ws + a.L.base);
+  double *partial = (double *)(a.ws + a.L.partial);
+  const size_t lds = lds_bytes_solver(P, 0);
+  if (a.O == 0) return hipSuccess;
+  k_base<<<dim3(2, a.O), 64, lds, s>>>(P, bmap, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, base);
+  if (a.E > 0) {
+    if (a.kernel == 2) {
+      float *opts = (float *)(a.ws + a.L.opts);
+      const dim3 grid((a.S + 255) / 256, a.E, a.O);
+#define FS_LANE_CASE(GG)                                                                         \
+  case GG:                                                                                       \
+    k_gather_options<GG><<<dim3(P.K, 2, a.O), 128, 0, s>>>(P, bmap, a.cap_lo, a.cap_hi,          \
+                                                           a.tail_lo, a.tail_hi, opts);          \
+    if (a.ev_begin) (void)hipEventRecord(a.ev_begin, s);                                         \
+    k_score_lane<GG><<<grid, 256, 0, s>>>(P, info, a.measured, opts, a.cap_s, a.tail_s, a.E,     \
+                                          a.S, base, partial, a.L.n_partial, a.tau_dump);        \
+    if (a.ev_end) (void)hipEventRecord(a.ev_end, s);                                             \
+    break;
+      switch (P.G) {
+        FS_LANE_CASE(16)
+        FS_LANE_CASE(32)
+        FS_LANE_CASE(64)
+        default:
+          return hipErrorInvalidValue;
+      }
+#undef FS_LANE_CASE
+    } else {
+      const dim3 grid((a.S + kWave - 1) / kWave, a.E, a.O);
+      if (a.ev_begin) (void)hipEventRecord(a.ev_begin, s);
+      k_score_wave<<<grid, 64, lds, s>>>(P, bmap, info, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
+                                         a.measured, a.cap_s, a.tail_s, a.E, a.S, base, partial,
+                                         a.L.n_partial, a.tau_dump);
+      if (a.ev_end) (void)hipEventRecord(a.ev_end, s);
+    }
+  }
+  k_finalize<<<a.O, 64, 0, s>>>(P, info, a.measured, a.E, a.S, base, partial, a.L.n_partial,
+                                a.score, a.gap_now, a.best);
+  return hipGetLastError();
+}
+
+hipError_t launch_solve_batch(const DevProblem &P, const float *cap, const float *tail, int64_t n,
+                              AllocOut out, uint8_t *ws, const WsLayout &L, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  k_solve_dense<<<(unsigned)n, 64, lds_bytes_solver(P, 1), s>>>(P, (const int8_t *)(ws + L.bmap),
+                                                                cap, tail, n, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_certify(const DevProblem &P, const float *cap_lo, const float *cap_hi,
+                          const float *tail_lo, const float *tail_hi, const uint8_t *measured,
+                          int32_t O, float eps, int32_t *state, AllocOut cons, AllocOut opt,
+                          double *gap, uint8_t *ws, const WsLayout &L, hipStream_t s) {
+  if (O == 0) return hipSuccess;
+  k_certify<<<O, 64, lds_bytes_solver(P, 2), s>>>(P, (const int8_t *)(ws + L.bmap), cap_lo, cap_hi,
+                                                  tail_lo, tail_hi, measured, eps, state, cons, opt,
+                                                  gap);
+  return hipGetLastError();
+}
+
+hipError_t launch_validate_cells(const float *cap, const float *tail, int64_t n, int32_t *flag,
+                                 hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const int64_t blocks = (n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096;
+  k_validate_cells<<<(unsigned)blocks, 256, 0, s>>>(cap, tail, n, flag);
+  return hipGetLastError();
+}
+
+}  // namespace fs
