@@ -36,23 +36,29 @@ DIV_OPS = 3
 PROFILE_GLOB = os.path.join(ROOT, "profiles")
 
 
-def lane_work_per_scenario(problem, bmap_exists) -> int:
-    """Algorithmic VALU operations per scenario of the lane-per-scenario
-    kernel (two solves), counting only work the method needs:
-      per existing option: multiply, divide (DIV_OPS), min with 1, tail
-        compare, select, max into its budget slot           -> 5 + DIV_OPS
-      per class: prefix maximum over budgets 1..G           -> G - 1
+# Issue slots of one (max,min) pair: two pairs take v_min, v_min, v_max3.
+PAIR_SLOTS = 1.5
+
+
+def lane_work_per_scenario(problem, bmap_exists) -> float:
+    """Algorithmic work per scenario (two solves) of the lane-per-scenario
+    kernel, in VALU lane-slots: the fewest gfx950 VALU issue slots that carry
+    the method's operations, counting only work the method needs.
+      per existing option: multiply, quotient (DIV_OPS), min with 1, tail
+        compare, select, max into its budget slot          -> 5 + DIV_OPS
+      per class: prefix maximum over budgets 1..G          -> G - 1
       per middle class (K - 2 of them): (max,min) pairs a = 1..g-1 for every
-        budget g = 2..G, two operations each                 -> 2 * G(G-1)/2
-      last class: pairs a = 1..G-1 for budget G              -> 2 * (G - 1)
+        budget g = 2..G                                     -> PAIR_SLOTS * G(G-1)/2
+      last class: pairs a = 1..G-1 for budget G             -> PAIR_SLOTS * (G - 1)
     The a = 0 and a = g terms of every convolution are min(x, 0) = 0 and are
-    not counted (the kernel does not compute them)."""
+    not computed.  Options whose per-replica load falls off the grid are not
+    counted even though the kernel evaluates them (as zero-capacity cells)."""
     G, K = problem.budget, problem.n_classes
     n_opt = int(bmap_exists.sum())
     per_solve = n_opt * (5 + DIV_OPS) + K * (G - 1)
     if K >= 2:
-        per_solve += (K - 2) * G * (G - 1) + 2 * (G - 1)
-    return 2 * per_solve
+        per_solve += (K - 2) * PAIR_SLOTS * G * (G - 1) / 2 + PAIR_SLOTS * (G - 1)
+    return 2.0 * per_solve
 
 
 def existing_options(problem):
@@ -124,6 +130,8 @@ def main():
     ap.add_argument("--kernel", type=int, default=0, help="0 auto, 1 wave per scenario, 2 lane per scenario")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="wall budget of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only a plain 1 GiB device copy (scales the HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the scorer is measured per GPU",
@@ -132,6 +140,17 @@ def main():
 
     import numpy as np
     import torch
+
+    if args.copy_calibration:
+        n = 1 << 28  # 2^28 float32 = 1 GiB read and 1 GiB written per copy
+        src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_read": 4 * n, "copy_calibration_bytes_written": 4 * n,
+                          "copies": 3}), flush=True)
+        return
 
     from paper_2608_19659_amd import fleetsieve as fs
     from paper_2608_19659_amd.synth import CONFIGS, make_workload
@@ -188,7 +207,7 @@ def main():
         traffic = committed_traffic(f"k_score_lane{p.budget}", tag)
         roofline = {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_OPS / 1e12,
                     "unit": "TOP/s", "frac": achieved / VALU_PEAK_OPS, "traffic": traffic,
-                    "kernel": kernel_name, "ops_per_scenario": ops,
+                    "kernel": kernel_name, "op": "VALU lane-slot", "ops_per_scenario": ops,
                     "kernel_ms_avg": kernel_ms / launches, "scenarios_per_launch": scenarios}
 
     cpu = None
@@ -202,7 +221,8 @@ def main():
         "metric": METRIC, "value": value, "unit": "scenarios/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": f"config {args.config} ({c['name']}): {p.n_classes} classes, TP {list(p.tp)}, "
+        "config": {"workload": f"config {args.config} ({c['name']}): {p.n_classes} classes, "
+                               f"TP {[int(x) for x in p.tp]}, "
                                f"G={p.budget}, {p.n_levels} load levels, {E} candidates x {S} samples x "
                                f"{O} reveal orders",
                    "scenarios_per_step": scenarios, "scenarios_in_config": O * E * S,
