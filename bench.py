@@ -30,12 +30,11 @@ sys.path.insert(0, ROOT)
 METRIC = "allocation scenarios/sec on 1 MI355X; % of VALU/HBM roofline; oracle-exact"
 # 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz: one 32-bit VALU operation per lane per clock.
 VALU_PEAK_OPS = 256 * 4 * 16 * 2.4e9
+HBM_PEAK_BYTES = 8.0e12
 # Cost of one binary32 quotient in the kernels, in VALU operations:
 # convert to binary64, multiply by the binary64 reciprocal, convert back.
 DIV_OPS = 3
 PROFILE_GLOB = os.path.join(ROOT, "profiles")
-
-
 # Issue slots of one (max,min) pair: two pairs take v_min, v_min, v_max3.
 PAIR_SLOTS = 1.5
 
@@ -121,15 +120,50 @@ def cpu_baseline(w, target_seconds: float, threads: int):
                       f"workload, {threads} OpenMP threads, {dt:.1f} s wall"}
 
 
+def replica_range_sizes(problem, cand):
+    """n_e per candidate: how many replica counts r put the candidate's cell
+    to use (t*r <= G and the per-replica load lands in the cell's level)."""
+    import numpy as np
+    T, B = problem.n_tp, problem.n_levels
+    sizes = np.zeros(len(cand), np.int64)
+    for j, cell in enumerate(cand):
+        b, ti, i = cell % B, (cell // B) % T, cell // (B * T)
+        t = int(problem.tp[ti])
+        n = 0
+        for r in range(1, problem.budget // t + 1):
+            u = np.float32(problem.demand[i]) / np.float32(r)
+            lv = np.nonzero(u <= problem.levels)[0]
+            n += int(len(lv) > 0 and lv[0] == b)
+        sizes[j] = n
+    return sizes
+
+
+def excl_work(problem, cand, live_tiles, S):
+    """Algorithmic work of one exclusion-scorer launch.
+    Per scenario, in VALU lane-slots: for each of the candidate's n_e replica
+    counts, the sampled ratio (multiply, quotient, min with 1: 2 + DIV_OPS)
+    and one (max,min) step into each realisation (2 x PAIR_SLOTS); then the
+    sampled tail test and two selects (3), the gap (two converts and a
+    subtract: 3) and one add of the pairwise sum (1).  Bytes: the two binary32
+    samples (8 B)."""
+    n_e = replica_range_sizes(problem, cand)
+    per_r = 2 + DIV_OPS + 2 * PAIR_SLOTS
+    slots = float(sum(S * (per_r * n_e[e] + 7) for (_, e) in live_tiles))
+    return slots, 8.0 * S * len(live_tiles), float(n_e.mean())
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=2, help="workload configuration (default 2)")
-    ap.add_argument("--kernel", type=int, default=0, help="0 auto, 1 wave per scenario, 2 lane per scenario")
+    ap.add_argument("--kernel", type=int, default=0,
+                    help="0 auto, 1 wave per scenario, 2 lane per scenario, 3 exclusion")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="wall budget of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-full-resolve", action="store_true",
+                    help="skip the second measurement with the full re-solve kernel")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (scales the HBM byte counters)")
     args = ap.parse_args()
@@ -164,51 +198,81 @@ def main():
     iv = fs.DeviceIntervals.from_host(w.intervals, dev)
     cand, cap_s, tail_s = t(w.cand), t(w.cap_s), t(w.tail_s)
     ctx = fs.Context(0)
-    ctx.set_score_kernel(args.kernel)
     ctx.set_option(fs.OPT_KERNEL_TIMING, 1)
     out = fs.ScoreOutput(torch.empty((O, E), dtype=torch.float64, device=dev),
                          torch.empty(O, dtype=torch.float64, device=dev),
                          torch.empty(O, dtype=torch.int32, device=dev), None)
     ws = ctx.workspace(fs.workspace_size(p, O, E, S))
     stream = torch.cuda.current_stream()
-    torch.cuda.synchronize()
-
-    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
-        fs.score_candidates(ctx, p, iv, cand, cap_s, tail_s, out=out, workspace=ws, stream=stream)
-    torch.cuda.synchronize()
-    ctx.kernel_timing()  # discard warm-up launches
-
-    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    ev0.record(stream)
-    for _ in range(args.steps):
-        fs.score_candidates(ctx, p, iv, cand, cap_s, tail_s, out=out, workspace=ws, stream=stream)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    total_ms = ev0.elapsed_time(ev1)
-    kernel_ms, launches = ctx.kernel_timing()
-    ms_per_step = total_ms / args.steps
 
     measured_cand = w.intervals.measured[:, w.cand].astype(bool)
-    scenarios = int((~measured_cand).sum()) * S
+    live_tiles = [(o, e) for o in range(O) for e in range(E) if not measured_cand[o, e]]
+    scenarios = len(live_tiles) * S
+
+    def run(kernel, steps, warmup):
+        ctx.set_score_kernel(kernel)
+        torch.cuda.synchronize()
+        for _ in range(warmup):
+            fs.score_candidates(ctx, p, iv, cand, cap_s, tail_s, out=out, workspace=ws, stream=stream)
+        torch.cuda.synchronize()
+        ctx.kernel_timing()  # discard warm-up launches
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for _ in range(steps):
+            fs.score_candidates(ctx, p, iv, cand, cap_s, tail_s, out=out, workspace=ws, stream=stream)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        kernel_ms, launches = ctx.kernel_timing()
+        return ev0.elapsed_time(ev1) / steps, kernel_ms / max(launches, 1), launches
+
+    lane_ok = p.floor_rps is None and [int(x) for x in p.tp] == [1, 2, 4, 8] and p.budget in (16, 32, 64)
+    kernel = args.kernel if args.kernel else (3 if p.floor_rps is None else 1)
+    print(f"[bench] kernel {kernel}: warmup {args.warmup}, timing {args.steps} steps", file=sys.stderr, flush=True)
+    ms_per_step, kernel_ms, launches = run(kernel, args.steps, args.warmup)
     value = scenarios / (ms_per_step / 1e3)
 
-    lane_ok = p.floor_rps is None and list(p.tp) == [1, 2, 4, 8] and p.budget in (16, 32, 64)
-    lane = args.kernel == 2 or (args.kernel == 0 and lane_ok)
-    kernel_name = f"k_score_lane<{p.budget}>" if lane else "k_score_wave"
-    roofline = None
-    if lane and launches:
-        ops = lane_work_per_scenario(p, existing_options(p))
-        kernel_avg_s = kernel_ms / launches / 1e3
-        achieved = ops * scenarios / kernel_avg_s
+    def roofline_of(kernel_id, kernel_ms_avg):
         tag = f"cfg{args.config}"
-        traffic = committed_traffic(f"k_score_lane{p.budget}", tag)
-        roofline = {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_OPS / 1e12,
-                    "unit": "TOP/s", "frac": achieved / VALU_PEAK_OPS, "traffic": traffic,
-                    "kernel": kernel_name, "op": "VALU lane-slot", "ops_per_scenario": ops,
-                    "kernel_ms_avg": kernel_ms / launches, "scenarios_per_launch": scenarios}
+        kernel_s = kernel_ms_avg / 1e3
+        if kernel_id == 3:
+            slots, nbytes, mean_ne = excl_work(p, w.cand, live_tiles, S)
+            t_alu, t_hbm = slots / VALU_PEAK_OPS, nbytes / HBM_PEAK_BYTES
+            name = "k_score_excl<4>"
+            extra = {"mean_replica_range": mean_ne}
+            if t_hbm >= t_alu:
+                achieved = nbytes / kernel_s
+                return dict(bound="hbm", achieved=achieved / 1e9, peak=HBM_PEAK_BYTES / 1e9, unit="GB/s",
+                            frac=achieved / HBM_PEAK_BYTES,
+                            traffic=committed_traffic("k_score_excl", tag), kernel=name,
+                            bytes_per_scenario=8.0, slots_per_scenario=slots / scenarios,
+                            alu_frac=slots / kernel_s / VALU_PEAK_OPS, kernel_ms_avg=kernel_ms_avg,
+                            scenarios_per_launch=scenarios, **extra)
+            achieved = slots / kernel_s
+            return dict(bound="alu", achieved=achieved / 1e12, peak=VALU_PEAK_OPS / 1e12, unit="TOP/s",
+                        frac=achieved / VALU_PEAK_OPS, traffic=committed_traffic("k_score_excl", tag),
+                        kernel=name, op="VALU lane-slot", slots_per_scenario=slots / scenarios,
+                        hbm_frac=nbytes / kernel_s / HBM_PEAK_BYTES, kernel_ms_avg=kernel_ms_avg,
+                        scenarios_per_launch=scenarios, **extra)
+        if kernel_id == 2:
+            ops = lane_work_per_scenario(p, existing_options(p))
+            achieved = ops * scenarios / kernel_s
+            return dict(bound="alu", achieved=achieved / 1e12, peak=VALU_PEAK_OPS / 1e12, unit="TOP/s",
+                        frac=achieved / VALU_PEAK_OPS,
+                        traffic=committed_traffic(f"k_score_lane{p.budget}", tag),
+                        kernel=f"k_score_lane<{p.budget}>", op="VALU lane-slot", slots_per_scenario=ops,
+                        kernel_ms_avg=kernel_ms_avg, scenarios_per_launch=scenarios)
+        return None
+
+    roofline = roofline_of(kernel, kernel_ms) if launches else None
+    kernel_name = {1: "k_score_wave", 2: f"k_score_lane<{p.budget}>", 3: "k_score_excl<4>"}[kernel]
+
+    full = None
+    if not args.no_full_resolve and kernel != 2 and lane_ok:
+        print("[bench] full re-solve kernel (lane per scenario)", file=sys.stderr, flush=True)
+        f_ms, f_kms, f_n = run(2, 5, 2)
+        full = {"kernel": f"k_score_lane<{p.budget}>", "value": scenarios / (f_ms / 1e3),
+                "ms_per_step": f_ms, "roofline": roofline_of(2, f_kms) if f_n else None}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -228,7 +292,7 @@ def main():
                    "scenarios_per_step": scenarios, "scenarios_in_config": O * E * S,
                    "measured_candidates_skipped": int(measured_cand.sum()) * S,
                    "kernel": kernel_name, "parallelism": "single GPU"},
-        "roofline": roofline, "cpu_baseline": cpu,
+        "roofline": roofline, "cpu_baseline": cpu, "full_resolve": full,
     }
     print(json.dumps(line), flush=True)
     ctx.close()

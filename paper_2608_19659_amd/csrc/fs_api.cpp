@@ -15,7 +15,7 @@
 
 struct fs_context {
   int device;
-  int score_kernel;  // 0 auto, 1 wave per scenario, 2 lane per scenario
+  int score_kernel;  // 0 auto, 1 wave per scenario, 2 lane per scenario, 3 exclusion
   int timing;        // record events around the scoring kernel
   std::vector<std::pair<hipEvent_t, hipEvent_t>> events;
 };
@@ -172,7 +172,7 @@ fs_status fs_context_kernel_timing(fs_context *ctx, double *total_ms, int64_t *l
 fs_status fs_context_set_option(fs_context *ctx, fs_option option, int64_t value) {
   if (!ctx) return fail(FS_ERR_INVALID_ARGUMENT, "context is NULL");
   if (option == FS_OPT_SCORE_KERNEL) {
-    if (value < 0 || value > 2) return fail(FS_ERR_INVALID_ARGUMENT, "score kernel must be 0, 1 or 2");
+    if (value < 0 || value > 3) return fail(FS_ERR_INVALID_ARGUMENT, "score kernel must be 0, 1, 2 or 3");
     ctx->score_kernel = (int)value;
     return FS_OK;
   }
@@ -219,14 +219,17 @@ fs_status fs_solve_batch(fs_context *ctx, const fs_problem *p, const float *d_ca
   DeviceGuard dg(ctx->device);
   if (dg.err != hipSuccess) return hip_fail(dg.err, "hipSetDevice");
   uint8_t *ws = (uint8_t *)d_workspace;
-  hipError_t e = fs::launch_setup(P, nullptr, 0, ws, L, stream);
-  if (e != hipSuccess) return hip_fail(e, "set-up launch");
+  hipError_t e;
   if (env_validate()) {
-    e = fs::launch_validate_cells(d_cap, d_tail, n_scenarios * (int64_t)P.N, (int32_t *)(ws + L.flag), stream);
+    int32_t *flag = (int32_t *)(ws + L.flag);
+    e = fs::launch_zero_flags(flag, stream);
+    if (e == hipSuccess) e = fs::launch_validate_cells(d_cap, d_tail, n_scenarios * (int64_t)P.N, flag, stream);
     if (e != hipSuccess) return hip_fail(e, "validation launch");
     st = read_flags(L, ws, stream, "fs_solve_batch");
     if (st != FS_OK) return st;
   }
+  e = fs::launch_setup(P, nullptr, 0, ws, L, stream);
+  if (e != hipSuccess) return hip_fail(e, "set-up launch");
   e = fs::launch_solve_batch(P, d_cap, d_tail, n_scenarios, to_out(out), ws, L, stream);
   if (e != hipSuccess) return hip_fail(e, "solve launch");
   return FS_OK;
@@ -250,10 +253,12 @@ fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals
   if (n_orders > 0 && n_cand > 0 && (!d_cand || !d_cap_s || !d_tail_s || !d_score))
     return fail(FS_ERR_INVALID_ARGUMENT, "candidate, sample or score arrays are NULL");
   int kernel = ctx->score_kernel;
-  if (kernel == 0) kernel = fs::lane_kernel_supported(P) ? 2 : 1;
+  if (kernel == 0) kernel = fs::excl_kernel_supported(P) ? 3 : 1;
   if (kernel == 2 && !fs::lane_kernel_supported(P))
     return fail(FS_ERR_UNSUPPORTED,
                 "lane-per-scenario scoring needs no floors, TP set {1,2,4,8} and budget 16, 32 or 64");
+  if (kernel == 3 && !fs::excl_kernel_supported(P))
+    return fail(FS_ERR_UNSUPPORTED, "exclusion scoring does not handle critical floors");
   const int32_t S = n_cand > 0 ? n_samples : 0;
   const fs::WsLayout L = fs::ws_layout(P, n_orders, n_cand, S);
   if (!d_workspace) return fail(FS_ERR_INVALID_ARGUMENT, "workspace is NULL");
@@ -263,18 +268,23 @@ fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals
   DeviceGuard dg(ctx->device);
   if (dg.err != hipSuccess) return hip_fail(dg.err, "hipSetDevice");
   uint8_t *ws = (uint8_t *)d_workspace;
-  hipError_t e = fs::launch_setup(P, d_cand, n_cand, ws, L, stream);
-  if (e != hipSuccess) return hip_fail(e, "set-up launch");
+  hipError_t e;
   if (env_validate()) {
     int32_t *flag = (int32_t *)(ws + L.flag);
     const int64_t cells = (int64_t)n_orders * P.N;
-    e = fs::launch_validate_cells(iv.cap_lo, iv.tail_lo, cells, flag, stream);
+    e = fs::launch_zero_flags(flag, stream);
+    if (e == hipSuccess) e = fs::launch_validate_cells(iv.cap_lo, iv.tail_lo, cells, flag, stream);
     if (e == hipSuccess) e = fs::launch_validate_cells(iv.cap_hi, iv.tail_hi, cells, flag, stream);
     if (e == hipSuccess && n_cand > 0)
       e = fs::launch_validate_cells(d_cap_s, d_tail_s, (int64_t)n_orders * n_cand * S, flag, stream);
+    if (e == hipSuccess) e = fs::launch_validate_cands(d_cand, n_cand, P.N, flag, stream);
     if (e != hipSuccess) return hip_fail(e, "validation launch");
     st = read_flags(L, ws, stream, "fs_score_candidates");
     if (st != FS_OK) return st;
+  }
+  if (kernel != 3) {
+    e = fs::launch_setup(P, d_cand, n_cand, ws, L, stream);
+    if (e != hipSuccess) return hip_fail(e, "set-up launch");
   }
   fs::ScoreArgs a{iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi, iv.measured, d_cand, d_cap_s, d_tail_s,
                   n_orders, n_cand, S, d_score, d_gap_now, d_best, d_tau_dump, ws, L, kernel,
@@ -309,17 +319,19 @@ fs_status fs_certify(fs_context *ctx, const fs_problem *p, fs_intervals iv, int3
   DeviceGuard dg(ctx->device);
   if (dg.err != hipSuccess) return hip_fail(dg.err, "hipSetDevice");
   uint8_t *ws = (uint8_t *)d_workspace;
-  hipError_t e = fs::launch_setup(P, nullptr, 0, ws, L, stream);
-  if (e != hipSuccess) return hip_fail(e, "set-up launch");
+  hipError_t e;
   if (env_validate()) {
     int32_t *flag = (int32_t *)(ws + L.flag);
     const int64_t cells = (int64_t)n_orders * P.N;
-    e = fs::launch_validate_cells(iv.cap_lo, iv.tail_lo, cells, flag, stream);
+    e = fs::launch_zero_flags(flag, stream);
+    if (e == hipSuccess) e = fs::launch_validate_cells(iv.cap_lo, iv.tail_lo, cells, flag, stream);
     if (e == hipSuccess) e = fs::launch_validate_cells(iv.cap_hi, iv.tail_hi, cells, flag, stream);
     if (e != hipSuccess) return hip_fail(e, "validation launch");
     st = read_flags(L, ws, stream, "fs_certify");
     if (st != FS_OK) return st;
   }
+  e = fs::launch_setup(P, nullptr, 0, ws, L, stream);
+  if (e != hipSuccess) return hip_fail(e, "set-up launch");
   e = fs::launch_certify(P, iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi, iv.measured, n_orders, eps,
                          d_state, to_out(cons), to_out(opt), d_gap, ws, L, stream);
   if (e != hipSuccess) return hip_fail(e, "certify launch");

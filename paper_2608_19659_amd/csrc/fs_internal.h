@@ -42,6 +42,18 @@ struct CandInfo {
   int32_t pad0, pad1;
 };
 
+// Per (order, candidate) constants of the exclusion scorer.  With H the
+// (max,min) convolution of every class except the candidate's, U the best
+// value reachable without the candidate's cell and f_r the ratio of r
+// replicas on the candidate's cell, a scenario's objective is
+//   tau = max(U, max_{r in [rlo, rhi]} min(f_r, H[G - t*r])).
+struct TileInfo {
+  int32_t cls, t, rlo, rhi;  // class, TP degree, replica range (rlo > rhi: unused cell)
+  int32_t u_m, u_p;          // U of the conservative / optimistic realisation (bits)
+  int32_t state;             // 0 = solve, 1 = measured, -1 = invalid candidate
+  int32_t ti;                // TP index
+};
+
 // Workspace layout; every region is 256-byte aligned.
 struct WsLayout {
   size_t bmap;     // int8  [K][G+1]   load level of r replicas (-1 = none)
@@ -49,6 +61,10 @@ struct WsLayout {
   size_t base;     // int32 [O][2]     base tau bits (conservative, optimistic)
   size_t opts;     // float [O][2][K][PP][2] option (cap, tail), lane kernel only
   size_t partial;  // double [O][E][ceil(S/64)]
+  size_t tiles;    // TileInfo [O][E]                       exclusion scorer
+  size_t tabB;     // int32 [O][2][K][G+1] per-class tables   exclusion scorer
+  size_t tabP;     // int32 [O][2][K][G+1] prefix convolutions
+  size_t tabH;     // int32 [O][2][K][G+1] all classes but one
   size_t flag;     // int32 [4]        validation / error flags
   size_t total;
   int64_t n_partial;  // ceil(S / 64)
@@ -60,6 +76,8 @@ WsLayout ws_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S);
 // Lane-per-scenario scoring supports these shapes.
 bool lane_kernel_supported(const DevProblem &P);
 int lane_kernel_options(int G);
+// Exclusion scoring supports every problem without critical floors.
+bool excl_kernel_supported(const DevProblem &P);
 
 // ---- launchers (fs_kernels.hip) --------------------------------------------
 struct ScoreArgs {
@@ -73,7 +91,7 @@ struct ScoreArgs {
   float *tau_dump;
   uint8_t *ws;
   WsLayout L;
-  int kernel;  // 1 = wave per scenario, 2 = lane per scenario
+  int kernel;  // 1 = wave per scenario, 2 = lane per scenario, 3 = exclusion
   hipEvent_t ev_begin, ev_end;  // recorded around the scoring kernel if set
 };
 
@@ -94,8 +112,11 @@ hipError_t launch_certify(const DevProblem &P, const float *cap_lo, const float 
                           const float *tail_lo, const float *tail_hi, const uint8_t *measured,
                           int32_t O, float eps, int32_t *state, AllocOut cons, AllocOut opt,
                           double *gap, uint8_t *ws, const WsLayout &L, hipStream_t s);
-// Device-side input checks (FS_VALIDATE=1): counts bad values into flag[0].
+// Device-side input checks (FS_VALIDATE=1): flag[0] counts bad cell values,
+// flag[1] candidate indices outside [0, N).  Zero the flags first.
+hipError_t launch_zero_flags(int32_t *flag, hipStream_t s);
 hipError_t launch_validate_cells(const float *cap, const float *tail, int64_t n, int32_t *flag,
                                  hipStream_t s);
+hipError_t launch_validate_cands(const int32_t *cand, int32_t E, int32_t N, int32_t *flag, hipStream_t s);
 
 }  // namespace fs

@@ -97,25 +97,26 @@ __device__ __forceinline__ int cell_of(const DevProblem &P, int k, int ti, int b
 // ---------------------------------------------------------------------------
 // Set-up: load level of every (class, replica count), and candidate info.
 // ---------------------------------------------------------------------------
-__global__ void k_setup_bucket(DevProblem P, int8_t *__restrict__ bmap, int32_t *__restrict__ flag) {
+// Load level of r replicas of class k: the offered load per replica is
+// lambda_k / r in binary32, and the replica runs in the smallest level that
+// is at least that load; -1 when no level is large enough.
+__device__ __forceinline__ int level_of(const DevProblem &P, int k, int r) {
+  const float per_replica = P.demand[k] / (float)r;
+  for (int j = 0; j < P.B; ++j)
+    if (per_replica <= P.levels[j]) return j;
+  return -1;
+}
+
+__global__ void k_setup_bucket(DevProblem P, int8_t *__restrict__ bmap) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx < 4) flag[idx] = 0;
   const int n = P.K * (P.G + 1);
   if (idx >= n) return;
   const int k = idx / (P.G + 1), r = idx % (P.G + 1);
-  int b = -1;
-  if (r >= 1) {
-    // offered load per replica, binary32; smallest level at least that load
-    const float per_replica = P.demand[k] / (float)r;
-    for (int j = 0; j < P.B; ++j)
-      if (per_replica <= P.levels[j]) { b = j; break; }
-  }
-  bmap[idx] = (int8_t)b;
+  bmap[idx] = (int8_t)(r >= 1 ? level_of(P, k, r) : -1);
 }
 
 __global__ void k_setup_cand(DevProblem P, const int32_t *__restrict__ cand, int32_t E,
-                             const int8_t *__restrict__ bmap, CandInfo *__restrict__ info,
-                             int32_t *__restrict__ flag) {
+                             const int8_t *__restrict__ bmap, CandInfo *__restrict__ info) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= E) return;
   const int cell = cand[e];
@@ -124,7 +125,6 @@ __global__ void k_setup_cand(DevProblem P, const int32_t *__restrict__ cand, int
   ci.pad0 = ci.pad1 = 0;
   if (cell < 0 || cell >= P.N) {
     ci.cls = -1; ci.ti = 0; ci.rlo = 1; ci.rhi = 0; ci.tp = 0;
-    atomicAdd(&flag[1], 1);
     info[e] = ci;
     return;
   }
@@ -554,13 +554,329 @@ __global__ __launch_bounds__(256) void k_score_lane(DevProblem P, const CandInfo
   __syncthreads();
   if (threadIdx.x == 0) {
     // 256 samples per block = four 64-sample blocks of the pairwise tree
-    const double sum = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
-    // a block covers 4 of the 64-sample partial slots; the first holds the
-    // sum, the other three hold zeros, which the final tree adds exactly
-    const int64_t slot = (int64_t)chunk * 4;
-    partial[tile * n_partial + slot] = sum;
-    for (int q = 1; q < 4 && slot + q < n_partial; ++q) partial[tile * n_partial + slot + q] = 0.0;
+    partial[tile * n_partial + chunk] = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
   }
+}
+
+
+// ---------------------------------------------------------------------------
+// Exclusion scorer.  The (max,min) convolution is associative and
+// commutative, so tau* = (B'_i (.) H_i)[G] where B'_i is the table of the
+// candidate's class i and H_i the convolution of every other class.  A
+// scenario changes only the candidate's cell, i.e. the options (t, r) with
+// r in [rlo, rhi].  With Bx the class-i table without those options and
+// f_r the sampled ratio of r replicas, distributivity of min over max gives
+//   tau = max( max_g min(Bx[g], H_i[G-g]),  max_r min(f_r, H_i[G - t*r]) )
+// (H_i is nondecreasing, so the best budget left for a sampled option of
+// cost t*r is all of G - t*r).  The first term, U, and every H_i[G - t*r]
+// are per (order, candidate); a scenario costs one ratio and two (max,min)
+// steps per replica count in [rlo, rhi].  The result is the same maximum
+// over the same binary32 values, so it is bit-identical to the full solve.
+// ---------------------------------------------------------------------------
+
+// Z[g] = max_{a <= g} min(X[g - a], Y[a]) for g = 0..G (all in LDS).
+__device__ void block_conv(const int *X, const int *Y, int *Z, int G) {
+  for (int g = threadIdx.x; g <= G; g += blockDim.x) {
+    int best = INT_MIN;
+    for (int a = 0; a <= g; ++a) best = max(best, min(X[g - a], Y[a]));
+    Z[g] = best;
+  }
+}
+
+__device__ void block_copy_in(int *dst, const int32_t *src, int n) {
+  for (int g = threadIdx.x; g < n; g += blockDim.x) dst[g] = src[g];
+}
+
+__device__ void block_copy_out(int32_t *dst, const int *src, int n) {
+  for (int g = threadIdx.x; g < n; g += blockDim.x) dst[g] = src[g];
+}
+
+// In-place prefix maximum of T[0..G] by wavefront 0 of the block.
+__device__ void block_prefix_max(int *T, int G) {
+  if (threadIdx.x < kWave) {
+    const int lane = threadIdx.x;
+    int carry = INT_MIN;
+    for (int base = 0; base <= G; base += kWave) {
+      const int g = base + lane;
+      int v = (g <= G) ? T[g] : INT_MIN;
+      v = max(wave_scan_max(v, lane), carry);
+      if (g <= G) T[g] = v;
+      carry = __shfl(v, kWave - 1, kWave);
+    }
+  }
+}
+
+// Best ratio of class k with at most g GPUs, for g = 0..G, into T (LDS).
+// Options whose cell is `skip_cell` are left out.
+__device__ void block_class_table(const DevProblem &P, int k, const float *cap, const float *tail,
+                                  int skip_cell, int *T) {
+  const int G = P.G;
+  for (int g = threadIdx.x; g <= G; g += blockDim.x) T[g] = 0;
+  __syncthreads();
+  for (int ti = 0; ti < P.NT; ++ti) {
+    const int t = P.tp[ti];
+    for (int r = 1 + threadIdx.x; t * r <= G; r += blockDim.x) {
+      const int b = level_of(P, k, r);
+      if (b < 0) continue;
+      const int cell = cell_of(P, k, ti, b);
+      if (cell == skip_cell) continue;
+      atomicMax(&T[t * r], ratio_bits(cap[cell], tail[cell], r, P.slo[k], P.rcp_demand[k]));
+    }
+  }
+  __syncthreads();
+  block_prefix_max(T, G);
+  __syncthreads();
+}
+
+// Per (realisation, order): class tables, prefix convolutions, the
+// all-but-one tables H_i and the base objective.
+__global__ __launch_bounds__(256) void k_tables(DevProblem P, const float *__restrict__ cap_lo,
+                                                const float *__restrict__ cap_hi,
+                                                const float *__restrict__ tail_lo,
+                                                const float *__restrict__ tail_hi,
+                                                int32_t *__restrict__ tabB, int32_t *__restrict__ tabP,
+                                                int32_t *__restrict__ tabH, int32_t *__restrict__ base) {
+  extern __shared__ int lds[];
+  const int R = blockIdx.x, o = blockIdx.y;
+  const int G = P.G, K = P.K, W = G + 1;
+  int *X = lds, *Y = lds + W, *Z = lds + 2 * W;
+  const size_t off = (size_t)o * P.N;
+  // Section 4.1: conservative = (low capacity, high tail); optimistic = (high, low).
+  const float *cap = (R == 0 ? cap_lo : cap_hi) + off;
+  const float *tail = (R == 0 ? tail_hi : tail_lo) + off;
+  const size_t tb = ((size_t)o * 2 + R) * K * W;
+  int32_t *Bt = tabB + tb, *Pt = tabP + tb, *Ht = tabH + tb;
+
+  for (int k = 0; k < K; ++k) {
+    block_class_table(P, k, cap, tail, -1, X);
+    block_copy_out(Bt + (size_t)k * W, X, W);
+    if (k == 0) block_copy_out(Pt, X, W);
+    __syncthreads();
+  }
+  if (K == 1) {
+    for (int g = threadIdx.x; g <= G; g += blockDim.x) Ht[g] = INT_MAX;  // empty convolution
+    if (threadIdx.x == 0) base[o * 2 + R] = Bt[G];
+    return;
+  }
+  // prefix: P_0 = B_0, P_k = P_{k-1} (.) B_k for k = 1..K-2
+  block_copy_in(X, Pt, W);
+  __syncthreads();
+  for (int k = 1; k <= K - 2; ++k) {
+    block_copy_in(Y, Bt + (size_t)k * W, W);
+    __syncthreads();
+    block_conv(X, Y, Z, G);
+    __syncthreads();
+    block_copy_out(Pt + (size_t)k * W, Z, W);
+    for (int g = threadIdx.x; g <= G; g += blockDim.x) X[g] = Z[g];
+    __syncthreads();
+  }
+  // suffix S_{i+1} in Y; H_i = P_{i-1} (.) S_{i+1}; H_{K-1} = P_{K-2}; H_0 = S_1
+  block_copy_out(Ht + (size_t)(K - 1) * W, X, W);  // X holds P_{K-2}
+  block_copy_in(Y, Bt + (size_t)(K - 1) * W, W);
+  __syncthreads();
+  for (int i = K - 2; i >= 1; --i) {
+    block_copy_in(X, Pt + (size_t)(i - 1) * W, W);
+    __syncthreads();
+    block_conv(X, Y, Z, G);
+    __syncthreads();
+    block_copy_out(Ht + (size_t)i * W, Z, W);
+    block_copy_in(X, Bt + (size_t)i * W, W);
+    __syncthreads();
+    block_conv(X, Y, Z, G);
+    __syncthreads();
+    for (int g = threadIdx.x; g <= G; g += blockDim.x) Y[g] = Z[g];
+    __syncthreads();
+  }
+  block_copy_out(Ht, Y, W);  // H_0 = S_1
+  // base objective = max_g min(B_0[g], H_0[G - g])
+  block_copy_in(X, Bt, W);
+  __syncthreads();
+  int best = INT_MIN;
+  for (int g = threadIdx.x; g <= G; g += blockDim.x) best = max(best, min(X[g], Y[G - g]));
+  best = wave_max(best);
+  __shared__ int wbest[4];
+  if ((threadIdx.x & (kWave - 1)) == 0) wbest[threadIdx.x >> 6] = best;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int v = wbest[0];
+    for (int w = 1; w < (int)(blockDim.x >> 6); ++w) v = max(v, wbest[w]);
+    base[o * 2 + R] = v;
+  }
+}
+
+// Per (candidate, order): the candidate's class, TP and replica range, and
+// U of both realisations.  One wavefront per tile; order-0 blocks also
+// record the candidate info used by the finalize step.
+__global__ __launch_bounds__(64) void k_tile_prep(DevProblem P, const int32_t *__restrict__ cand,
+                                                  int32_t E, const uint8_t *__restrict__ measured,
+                                                  const float *__restrict__ cap_lo,
+                                                  const float *__restrict__ cap_hi,
+                                                  const float *__restrict__ tail_lo,
+                                                  const float *__restrict__ tail_hi,
+                                                  const int32_t *__restrict__ tabH,
+                                                  TileInfo *__restrict__ tiles,
+                                                  CandInfo *__restrict__ info) {
+  extern __shared__ int T[];
+  const int e = blockIdx.x, o = blockIdx.y, lane = threadIdx.x;
+  const int G = P.G, W = G + 1;
+  const int cell = cand[e];
+  TileInfo tl;
+  tl.cls = 0; tl.t = 0; tl.rlo = 1; tl.rhi = 0; tl.u_m = 0; tl.u_p = 0; tl.ti = 0;
+  const size_t tile = (size_t)o * E + e;
+  if (cell < 0 || cell >= P.N) {
+    tl.state = -1;
+    if (lane == 0) {
+      tiles[tile] = tl;
+      if (o == 0) {
+        CandInfo ci;
+        ci.cls = -1; ci.ti = 0; ci.rlo = 1; ci.rhi = 0; ci.cell = cell; ci.tp = 0; ci.pad0 = ci.pad1 = 0;
+        info[e] = ci;
+      }
+    }
+    return;
+  }
+  const int b = cell % P.B;
+  const int ti = (cell / P.B) % P.NT;
+  const int k = cell / (P.B * P.NT);
+  const int t = P.tp[ti];
+  int rlo = INT_MAX, rhi = -1;
+  for (int r = 1 + lane; t * r <= G; r += kWave) {
+    if (level_of(P, k, r) == b) {
+      rlo = min(rlo, r);
+      rhi = max(rhi, r);
+    }
+  }
+  rlo = wave_min(rlo);
+  rhi = wave_max(rhi);
+  if (rhi < 0) { rlo = 1; rhi = 0; }
+  tl.cls = k; tl.t = t; tl.ti = ti; tl.rlo = rlo; tl.rhi = rhi;
+  const size_t off = (size_t)o * P.N;
+  tl.state = measured[off + cell] ? 1 : 0;
+  if (tl.state == 0) {
+    for (int R = 0; R < 2; ++R) {
+      const float *cap = (R == 0 ? cap_lo : cap_hi) + off;
+      const float *tail = (R == 0 ? tail_hi : tail_lo) + off;
+      block_class_table(P, k, cap, tail, cell, T);
+      const int32_t *H = tabH + (((size_t)o * 2 + R) * P.K + k) * W;
+      int best = INT_MIN;
+      for (int g = lane; g <= G; g += kWave) best = max(best, min(T[g], H[G - g]));
+      best = wave_max(best);
+      if (R == 0) tl.u_m = best;
+      else tl.u_p = best;
+      __syncthreads();
+    }
+  }
+  if (lane == 0) {
+    tiles[tile] = tl;
+    if (o == 0) {
+      CandInfo ci;
+      ci.cls = k; ci.ti = ti; ci.rlo = rlo; ci.rhi = rhi; ci.cell = cell; ci.tp = t;
+      ci.pad0 = ci.pad1 = 0;
+      info[e] = ci;
+    }
+  }
+}
+
+// Scenarios of the exclusion scorer: block (chunk, e, o) holds 256 lanes x
+// SPL consecutive samples; lane l owns samples [chunk*256*SPL + l*SPL, +SPL).
+template <int SPL>
+__global__ __launch_bounds__(256) void k_score_excl(DevProblem P, const TileInfo *__restrict__ tiles,
+                                                    const int32_t *__restrict__ tabH,
+                                                    const float *__restrict__ cap_s,
+                                                    const float *__restrict__ tail_s, int32_t E,
+                                                    int32_t S, const int32_t *__restrict__ base,
+                                                    double *__restrict__ partial, int64_t n_partial,
+                                                    float *__restrict__ tau_dump) {
+  constexpr int CHUNK = 256 * SPL;
+  extern __shared__ int Mlds[];
+  __shared__ double wsum[4];
+  const int chunk = blockIdx.x, e = blockIdx.y, o = blockIdx.z;
+  const size_t tile = (size_t)o * E + e;
+  const TileInfo tl = tiles[tile];
+  if (tl.state < 0) return;
+  const int s_first = chunk * CHUNK + threadIdx.x * SPL;
+  if (tl.state == 1) {
+    if (tau_dump) {
+      for (int q = 0; q < SPL; ++q) {
+        if (s_first + q < S) {
+          tau_dump[(tile * S + s_first + q) * 2 + 0] = __int_as_float(base[o * 2 + 0]);
+          tau_dump[(tile * S + s_first + q) * 2 + 1] = __int_as_float(base[o * 2 + 1]);
+        }
+      }
+    }
+    return;
+  }
+  const int G = P.G, W = G + 1;
+  const int nr = tl.rhi >= tl.rlo ? tl.rhi - tl.rlo + 1 : 0;
+  const int nr4 = (nr + 3) & ~3;
+  int *Mm = Mlds, *Mp = Mlds + nr4;
+  const int32_t *Hm = tabH + (((size_t)o * 2 + 0) * P.K + tl.cls) * W;
+  const int32_t *Hp = tabH + (((size_t)o * 2 + 1) * P.K + tl.cls) * W;
+  for (int j = threadIdx.x; j < nr4; j += blockDim.x) {
+    const int r = tl.rlo + j;
+    // padding entries are 0: min(f, 0) <= 0 <= U never raises the maximum
+    Mm[j] = j < nr ? Hm[G - tl.t * r] : 0;
+    Mp[j] = j < nr ? Hp[G - tl.t * r] : 0;
+  }
+  __syncthreads();
+
+  float cs[SPL], ls[SPL];
+  const size_t sbase = tile * S + s_first;
+  if (s_first + SPL <= S && (SPL == 4) && ((sbase & 3) == 0)) {
+    const float4 c4 = *reinterpret_cast<const float4 *>(cap_s + sbase);
+    const float4 l4 = *reinterpret_cast<const float4 *>(tail_s + sbase);
+    cs[0] = c4.x; cs[1] = c4.y; cs[2] = c4.z; cs[3] = c4.w;
+    ls[0] = l4.x; ls[1] = l4.y; ls[2] = l4.z; ls[3] = l4.w;
+  } else {
+#pragma unroll
+    for (int q = 0; q < SPL; ++q) {
+      const bool live = s_first + q < S;
+      cs[q] = live ? cap_s[sbase + q] : 0.0f;
+      ls[q] = live ? tail_s[sbase + q] : 0.0f;
+    }
+  }
+  const double rcp = P.rcp_demand[tl.cls];
+  int am[SPL], ap[SPL];
+#pragma unroll
+  for (int q = 0; q < SPL; ++q) { am[q] = tl.u_m; ap[q] = tl.u_p; }
+  for (int j = 0; j < nr4; j += 4) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float rf = (float)(tl.rlo + j + u);
+      const int mm = Mm[j + u], mp = Mp[j + u];
+#pragma unroll
+      for (int q = 0; q < SPL; ++q) {
+        const float capacity = rf * cs[q];
+        const int fb = __float_as_int(fminf((float)((double)capacity * rcp), 1.0f));
+        am[q] = max(am[q], min(fb, mm));
+        ap[q] = max(ap[q], min(fb, mp));
+      }
+    }
+  }
+  const float slo = P.slo[tl.cls];
+  double gq[SPL];
+#pragma unroll
+  for (int q = 0; q < SPL; ++q) {
+    // a sampled tail above the SLO makes every option on the cell worth 0
+    const bool tail_ok = ls[q] <= slo;
+    const int tm = tail_ok ? am[q] : tl.u_m;
+    const int tp = tail_ok ? ap[q] : tl.u_p;
+    const bool live = s_first + q < S;
+    gq[q] = live ? (double)__int_as_float(tp) - (double)__int_as_float(tm) : 0.0;
+    if (tau_dump && live) {
+      tau_dump[(sbase + q) * 2 + 0] = __int_as_float(tm);
+      tau_dump[(sbase + q) * 2 + 1] = __int_as_float(tp);
+    }
+  }
+  // pairwise tree: within the lane's SPL consecutive samples, then lanes
+  double v;
+  if (SPL == 4) v = (gq[0] + gq[1]) + (gq[2 % SPL] + gq[3 % SPL]);
+  else if (SPL == 2) v = gq[0] + gq[1 % SPL];
+  else v = gq[0];
+  v = wave_pairwise_sum(v);
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) partial[tile * n_partial + chunk] = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
 }
 
 // ---------------------------------------------------------------------------
@@ -679,6 +995,16 @@ __global__ __launch_bounds__(64) void k_certify(DevProblem P, const int8_t *__re
   state[o] = st;
 }
 
+__global__ void k_zero_flags(int32_t *__restrict__ flag) {
+  if (threadIdx.x < 4) flag[threadIdx.x] = 0;
+}
+
+__global__ void k_validate_cands(const int32_t *__restrict__ cand, int32_t E, int32_t N,
+                                 int32_t *__restrict__ flag) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e < E && (cand[e] < 0 || cand[e] >= N)) atomicAdd(&flag[1], 1);
+}
+
 __global__ void k_validate_cells(const float *__restrict__ cap, const float *__restrict__ tail,
                                  int64_t n, int32_t *__restrict__ flag) {
   int bad = 0;
@@ -707,6 +1033,8 @@ bool lane_kernel_supported(const DevProblem &P) {
 
 int lane_kernel_options(int G) { return G + G / 2 + G / 4 + G / 8; }
 
+bool excl_kernel_supported(const DevProblem &P) { return !P.has_floor; }
+
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 WsLayout ws_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
@@ -720,6 +1048,11 @@ WsLayout ws_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
   L.n_partial = S > 0 ? (S + kWave - 1) / kWave : 1;
   L.partial = at; at = align256(at + sizeof(double) * (size_t)O * (size_t)E * L.n_partial);
   L.flag = at; at = align256(at + sizeof(int32_t) * 4);
+  L.tiles = at; at = align256(at + sizeof(TileInfo) * (size_t)O * (size_t)E);
+  const size_t tab = excl_kernel_supported(P) ? sizeof(int32_t) * (size_t)O * 2 * P.K * (P.G + 1) : 0;
+  L.tabB = at; at = align256(at + tab);
+  L.tabP = at; at = align256(at + tab);
+  L.tabH = at; at = align256(at + tab);
   L.total = at;
   return L;
 }
@@ -727,33 +1060,59 @@ WsLayout ws_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
 hipError_t launch_setup(const DevProblem &P, const int32_t *cand, int32_t E, uint8_t *ws,
                         const WsLayout &L, hipStream_t s) {
   const int n = P.K * (P.G + 1);
-  k_setup_bucket<<<(n + 255) / 256, 256, 0, s>>>(P, (int8_t *)(ws + L.bmap), (int32_t *)(ws + L.flag));
+  k_setup_bucket<<<(n + 255) / 256, 256, 0, s>>>(P, (int8_t *)(ws + L.bmap));
   if (E > 0) {
     k_setup_cand<<<(E + 255) / 256, 256, 0, s>>>(P, cand, E, (const int8_t *)(ws + L.bmap),
-                                                (CandInfo *)(ws + L.cand), (int32_t *)(ws + L.flag));
+                                                (CandInfo *)(ws + L.cand));
   }
   return hipGetLastError();
 }
 
 hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) {
   const int8_t *bmap = (const int8_t *)(a.ws + a.L.bmap);
-  const CandInfo *info = (const CandInfo *)(a.ws + a.L.cand);
+  CandInfo *info = (CandInfo *)(a.ws + a.L.cand);
   int32_t *base = (int32_t *)(a.ws + a.L.base);
   double *partial = (double *)(a.ws + a.L.partial);
   const size_t lds = lds_bytes_solver(P, 0);
   if (a.O == 0) return hipSuccess;
+  if (a.kernel == 3) {
+    const int W = P.G + 1;
+    constexpr int kSpl = 4;
+    TileInfo *tiles = (TileInfo *)(a.ws + a.L.tiles);
+    int32_t *tabH = (int32_t *)(a.ws + a.L.tabH);
+    k_tables<<<dim3(2, a.O), 256, 3 * W * sizeof(int), s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
+                                                           (int32_t *)(a.ws + a.L.tabB),
+                                                           (int32_t *)(a.ws + a.L.tabP), tabH, base);
+    int64_t n_partial = 1;
+    if (a.E > 0) {
+      k_tile_prep<<<dim3(a.E, a.O), 64, W * sizeof(int), s>>>(P, a.cand, a.E, a.measured, a.cap_lo, a.cap_hi,
+                                                             a.tail_lo, a.tail_hi, tabH, tiles, info);
+      n_partial = (a.S + 256 * kSpl - 1) / (256 * kSpl);
+      const int max_nr4 = ((P.G / P.tp[0]) + 3) & ~3;
+      const size_t mlds = 2 * (size_t)max_nr4 * sizeof(int);
+      if (a.ev_begin) (void)hipEventRecord(a.ev_begin, s);
+      k_score_excl<kSpl><<<dim3((unsigned)n_partial, a.E, a.O), 256, mlds, s>>>(
+          P, tiles, tabH, a.cap_s, a.tail_s, a.E, a.S, base, partial, n_partial, a.tau_dump);
+      if (a.ev_end) (void)hipEventRecord(a.ev_end, s);
+    }
+    k_finalize<<<a.O, 64, 0, s>>>(P, info, a.measured, a.E, a.S, base, partial, n_partial, a.score,
+                                  a.gap_now, a.best);
+    return hipGetLastError();
+  }
   k_base<<<dim3(2, a.O), 64, lds, s>>>(P, bmap, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, base);
+  int64_t n_partial = a.L.n_partial;
   if (a.E > 0) {
     if (a.kernel == 2) {
       float *opts = (float *)(a.ws + a.L.opts);
       const dim3 grid((a.S + 255) / 256, a.E, a.O);
+      n_partial = (a.S + 255) / 256;
 #define FS_LANE_CASE(GG)                                                                         \
   case GG:                                                                                       \
     k_gather_options<GG><<<dim3(P.K, 2, a.O), 128, 0, s>>>(P, bmap, a.cap_lo, a.cap_hi,          \
                                                            a.tail_lo, a.tail_hi, opts);          \
     if (a.ev_begin) (void)hipEventRecord(a.ev_begin, s);                                         \
     k_score_lane<GG><<<grid, 256, 0, s>>>(P, info, a.measured, opts, a.cap_s, a.tail_s, a.E,     \
-                                          a.S, base, partial, a.L.n_partial, a.tau_dump);        \
+                                          a.S, base, partial, n_partial, a.tau_dump);            \
     if (a.ev_end) (void)hipEventRecord(a.ev_end, s);                                             \
     break;
       switch (P.G) {
@@ -767,13 +1126,14 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
     } else {
       const dim3 grid((a.S + kWave - 1) / kWave, a.E, a.O);
       if (a.ev_begin) (void)hipEventRecord(a.ev_begin, s);
+      n_partial = (a.S + kWave - 1) / kWave;
       k_score_wave<<<grid, 64, lds, s>>>(P, bmap, info, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
                                          a.measured, a.cap_s, a.tail_s, a.E, a.S, base, partial,
-                                         a.L.n_partial, a.tau_dump);
+                                         n_partial, a.tau_dump);
       if (a.ev_end) (void)hipEventRecord(a.ev_end, s);
     }
   }
-  k_finalize<<<a.O, 64, 0, s>>>(P, info, a.measured, a.E, a.S, base, partial, a.L.n_partial,
+  k_finalize<<<a.O, 64, 0, s>>>(P, info, a.measured, a.E, a.S, base, partial, n_partial,
                                 a.score, a.gap_now, a.best);
   return hipGetLastError();
 }
@@ -794,6 +1154,17 @@ hipError_t launch_certify(const DevProblem &P, const float *cap_lo, const float 
   k_certify<<<O, 64, lds_bytes_solver(P, 2), s>>>(P, (const int8_t *)(ws + L.bmap), cap_lo, cap_hi,
                                                   tail_lo, tail_hi, measured, eps, state, cons, opt,
                                                   gap);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_flags(int32_t *flag, hipStream_t s) {
+  k_zero_flags<<<1, 64, 0, s>>>(flag);
+  return hipGetLastError();
+}
+
+hipError_t launch_validate_cands(const int32_t *cand, int32_t E, int32_t N, int32_t *flag, hipStream_t s) {
+  if (E == 0) return hipSuccess;
+  k_validate_cands<<<(E + 255) / 256, 256, 0, s>>>(cand, E, N, flag);
   return hipGetLastError();
 }
 

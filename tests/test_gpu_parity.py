@@ -79,7 +79,7 @@ def assert_scores_equal(g, o, tile_mask=None):
             np.testing.assert_array_equal(dump[m].view(np.uint32), o.tau_dump[m].view(np.uint32))
 
 
-KERNELS = [1, 2]  # wave per scenario, lane per scenario
+KERNELS = [1, 2, 3]  # wave per scenario, lane per scenario, exclusion
 
 
 # ------------------------------------------------------ golden fixtures -----
@@ -142,14 +142,16 @@ def test_hw3_scores_and_certificates_on_gpu(env, orc):
     d = hw3["intervals"]
     iv = Intervals(*(np.array([d[k]], np.float32) for k in ("cap_lo", "cap_hi", "tail_lo", "tail_hi")),
                    np.array([d["measured"]], np.uint8))
-    note("hw3 scores")
-    score, gap, best, dump = gpu_score(env, p, iv, hw3["cand"], np.array([hw3["cap_s"]], np.float32),
-                                       np.array([hw3["tail_s"]], np.float32), kernel=1)
     ex = hw3["expect"]
-    assert gap[0] == ex["gap_now"]
-    np.testing.assert_array_equal(score[0], ex["score"])
-    assert best[0] == ex["best"]
-    np.testing.assert_array_equal(dump[0, :, :, 0], np.array(ex["tau_minus"], np.float32))
+    for kernel in (1, 3):
+        note(f"hw3 scores kernel {kernel}")
+        score, gap, best, dump = gpu_score(env, p, iv, hw3["cand"], np.array([hw3["cap_s"]], np.float32),
+                                           np.array([hw3["tail_s"]], np.float32), kernel=kernel)
+        assert gap[0] == ex["gap_now"]
+        np.testing.assert_array_equal(score[0], ex["score"])
+        assert best[0] == ex["best"]
+        np.testing.assert_array_equal(dump[0, :, :, 0], np.array(ex["tau_minus"], np.float32))
+        np.testing.assert_array_equal(dump[0, :, :, 1], np.array(ex["tau_plus"], np.float32))
     torch, fs, ctx = env
     states = {"UNDECIDED": 0, "CERTIFIED_FEASIBLE": 1, "CERTIFIED_INFEASIBLE": 2}
     for case in hw3["certificates"]:
@@ -228,21 +230,23 @@ def test_score_config2_tiles(env, orc, kernel):
     assert_scores_equal(g, o)
 
 
-def test_score_config3_subset(env, orc):
-    """Config 3 shape (K=8, G=256): wave-per-scenario kernel, 2 orders x 6
-    candidates, first 96 samples (a ragged 64-sample block)."""
+@pytest.mark.parametrize("kernel", [1, 3])
+def test_score_config3_subset(env, orc, kernel):
+    """Config 3 shape (K=8, G=256): 2 orders x 6 candidates, first 96
+    samples (a ragged block)."""
     w = make_workload(3, orders=[0, 5])
     sel = np.array([0, 31, 77, 128, 200, 255])
     S = 96
     cs = np.ascontiguousarray(w.cap_s[:, sel, :S])
     ts = np.ascontiguousarray(w.tail_s[:, sel, :S])
-    note("score cfg3 subset")
-    g = gpu_score(env, w.problem, w.intervals, w.cand[sel], cs, ts, kernel=1)
+    note(f"score cfg3 subset kernel {kernel}")
+    g = gpu_score(env, w.problem, w.intervals, w.cand[sel], cs, ts, kernel=kernel)
     o = orc.score(w.problem, w.intervals, w.cand[sel], cs, ts, n_threads=16)
     assert_scores_equal(g, o)
 
 
-def test_score_config4_subset(env, orc):
+@pytest.mark.parametrize("kernel", [1, 3])
+def test_score_config4_subset(env, orc, kernel):
     """Config 4 shape (K=16, TP up to 16, G=1024): 1 order x 3 candidates,
     first 24 samples."""
     w = make_workload(4, orders=[1], with_samples=True)
@@ -250,10 +254,38 @@ def test_score_config4_subset(env, orc):
     S = 24
     cs = np.ascontiguousarray(w.cap_s[:, sel, :S])
     ts = np.ascontiguousarray(w.tail_s[:, sel, :S])
-    note("score cfg4 subset")
-    g = gpu_score(env, w.problem, w.intervals, w.cand[sel], cs, ts, kernel=1)
+    note(f"score cfg4 subset kernel {kernel}")
+    g = gpu_score(env, w.problem, w.intervals, w.cand[sel], cs, ts, kernel=kernel)
     o = orc.score(w.problem, w.intervals, w.cand[sel], cs, ts, n_threads=16)
     assert_scores_equal(g, o)
+
+
+def test_score_config3_full_orders_exclusion(env, orc):
+    """Config 3 at its real sample count (4096) with the exclusion kernel:
+    all 256 candidates of one order, sampled scenarios re-solved by the
+    oracle one by one, and three whole tiles re-scored."""
+    w = make_workload(3, orders=[7])
+    note("score cfg3 one full order, exclusion")
+    score, gap, best, dump = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=3)
+    p, iv = w.problem, w.intervals
+    rng = np.random.default_rng(33)
+    E, S = w.n_cand, w.n_samples
+    for _ in range(60):
+        e, s = int(rng.integers(E)), int(rng.integers(S))
+        cell = w.cand[e]
+        if iv.measured[0, cell]:
+            continue
+        cm, tm = iv.cap_lo[0].copy(), iv.tail_hi[0].copy()
+        cp, tp = iv.cap_hi[0].copy(), iv.tail_lo[0].copy()
+        cm[cell] = cp[cell] = w.cap_s[0, e, s]
+        tm[cell] = tp[cell] = w.tail_s[0, e, s]
+        assert dump[0, e, s, 0] == orc.solve(p, cm, tm).tau, (e, s)
+        assert dump[0, e, s, 1] == orc.solve(p, cp, tp).tau, (e, s)
+    mask = np.zeros((1, E), np.uint8)
+    live = [e for e in range(E) if not iv.measured[0, w.cand[e]]]
+    mask[0, rng.choice(live, size=3, replace=False)] = 1
+    o_ref = orc.score(p, iv, w.cand, w.cap_s, w.tail_s, tile_mask=mask, n_threads=16)
+    assert_scores_equal((score, gap, best, dump), o_ref, tile_mask=mask)
 
 
 def test_score_config2_full_size_sampled(env, orc):
@@ -349,13 +381,15 @@ def test_single_class_problem(env, orc, kernel):
     assert_scores_equal(g, orc.score(p, iv, cand, cs, ts))
 
 
-def test_lane_and_wave_kernels_agree_and_are_deterministic(env, orc):
+def test_kernels_agree_and_are_deterministic(env, orc):
     w = make_workload(1, orders=[4, 9, 20])
     note("determinism")
     a = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=2)
     b = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=2)
     c = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=1)
-    for x, y in ((a, b), (a, c)):
+    d = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=3)
+    f = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=3)
+    for x, y in ((a, b), (a, c), (a, d), (d, f)):
         np.testing.assert_array_equal(x[0], y[0])
         np.testing.assert_array_equal(x[1], y[1])
         np.testing.assert_array_equal(x[2], y[2])
@@ -372,7 +406,31 @@ def test_lane_kernel_rejects_unsupported_shapes(env):
     with pytest.raises(fs.FleetSieveError) as ei:
         fs.score_candidates(ctx, w.problem, div, cand, cs, cs)
     assert ei.value.status == fs.FS_ERR_UNSUPPORTED
+    p = w.problem
+    pf = Problem(p.tp, p.levels, p.demand, p.slo, p.budget, floor_rps=np.full(p.n_classes, 1.0, np.float32))
+    ctx.set_score_kernel(3)
+    with pytest.raises(fs.FleetSieveError) as ei:
+        fs.score_candidates(ctx, pf, div, cand, cs, cs)
+    assert ei.value.status == fs.FS_ERR_UNSUPPORTED
     ctx.set_score_kernel(0)
+
+
+def test_score_with_floors_uses_wave_kernel(env, orc):
+    """Critical floors are scored by the wave-per-scenario kernel (the
+    automatic choice) and match the oracle, including negative gaps."""
+    w = make_workload(2, orders=[1, 2])
+    p = w.problem
+    fl = np.zeros(p.n_classes, np.float32)
+    fl[1], fl[3] = 3.0, 1.5
+    pf = Problem(p.tp, p.levels, p.demand, p.slo, p.budget, floor_rps=fl)
+    sel = np.array([3, 50, 90])
+    S = 70
+    cs = np.ascontiguousarray(w.cap_s[:, sel, :S])
+    ts = np.ascontiguousarray(w.tail_s[:, sel, :S])
+    note("score with floors")
+    g = gpu_score(env, pf, w.intervals, w.cand[sel], cs, ts, kernel=0)
+    o = orc.score(pf, w.intervals, w.cand[sel], cs, ts, n_threads=16)
+    assert_scores_equal(g, o)
 
 
 # --------------------------------------------------------- certificates -----
