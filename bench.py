@@ -161,6 +161,10 @@ def main():
     ap.add_argument("--kernel", type=int, default=0,
                     help="0 auto, 1 wave per scenario, 2 lane per scenario, 3 exclusion")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="wall budget of the oracle baseline")
+    ap.add_argument("--spl", type=int, default=0,
+                    help="exclusion scorer samples per lane (4, 8, 16; 0 = library default)")
+    ap.add_argument("--wpb", type=int, default=0,
+                    help="exclusion scorer wavefronts per block (1, 4; 0 = library default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-full-resolve", action="store_true",
                     help="skip the second measurement with the full re-solve kernel")
@@ -199,6 +203,8 @@ def main():
     cand, cap_s, tail_s = t(w.cand), t(w.cap_s), t(w.tail_s)
     ctx = fs.Context(0)
     ctx.set_option(fs.OPT_KERNEL_TIMING, 1)
+    ctx.set_option(fs.OPT_SAMPLES_PER_LANE, args.spl)
+    ctx.set_option(fs.OPT_WAVES_PER_BLOCK, args.wpb)
     out = fs.ScoreOutput(torch.empty((O, E), dtype=torch.float64, device=dev),
                          torch.empty(O, dtype=torch.float64, device=dev),
                          torch.empty(O, dtype=torch.int32, device=dev), None)
@@ -238,7 +244,7 @@ def main():
         if kernel_id == 3:
             slots, nbytes, mean_ne = excl_work(p, w.cand, live_tiles, S)
             t_alu, t_hbm = slots / VALU_PEAK_OPS, nbytes / HBM_PEAK_BYTES
-            name = "k_score_excl<4>"
+            name = "k_score_excl"
             extra = {"mean_replica_range": mean_ne}
             if t_hbm >= t_alu:
                 achieved = nbytes / kernel_s
@@ -265,7 +271,7 @@ def main():
         return None
 
     roofline = roofline_of(kernel, kernel_ms) if launches else None
-    kernel_name = {1: "k_score_wave", 2: f"k_score_lane<{p.budget}>", 3: "k_score_excl<4>"}[kernel]
+    kernel_name = {1: "k_score_wave", 2: f"k_score_lane<{p.budget}>", 3: "k_score_excl"}[kernel]
 
     full = None
     if not args.no_full_resolve and kernel != 2 and lane_ok:

@@ -112,14 +112,24 @@ typedef struct fs_context fs_context;
 
 /* Options for fs_context_set_option. */
 typedef enum fs_option {
-  /* Scoring kernel: 0 = automatic, 1 = one wavefront per scenario (any
-   * problem), 2 = one lane per scenario (no floors, TP set {1,2,4,8},
-   * budget 16, 32 or 64).  Both give identical bits. */
+  /* Scoring kernel: 0 = automatic (3 without critical floors, else 1),
+   * 1 = one wavefront per scenario, full solves (any problem),
+   * 2 = one lane per scenario, full solves (no floors, TP set {1,2,4,8},
+   *     budget 16, 32 or 64),
+   * 3 = exclusion scorer: per-order all-but-one tables, O(replica range) per
+   *     scenario (no floors).  All give identical bits. */
   FS_OPT_SCORE_KERNEL = 1,
   /* 1 = record a pair of HIP events on the caller's stream around every
    * launch of the scoring kernel (the per-scenario solve), for
    * fs_context_kernel_timing; 0 = off (default). */
-  FS_OPT_KERNEL_TIMING = 2
+  FS_OPT_KERNEL_TIMING = 2,
+  /* Exclusion scorer (kernel 3): samples each lane handles, 4, 8 or 16
+   * (0 = library default).  A launch-shape tuning knob; results are
+   * identical for every value. */
+  FS_OPT_SAMPLES_PER_LANE = 3,
+  /* Exclusion scorer: wavefronts per block, 1 or 4 (0 = library default).
+   * A launch-shape tuning knob; results are identical for every value. */
+  FS_OPT_WAVES_PER_BLOCK = 4
 } fs_option;
 
 /* Creates a context bound to HIP device `hip_device`.  One context per host

@@ -17,6 +17,8 @@ struct fs_context {
   int device;
   int score_kernel;  // 0 auto, 1 wave per scenario, 2 lane per scenario, 3 exclusion
   int timing;        // record events around the scoring kernel
+  int spl;           // exclusion scorer samples per lane (0 = default)
+  int wpb;           // exclusion scorer wavefronts per block (0 = default)
   std::vector<std::pair<hipEvent_t, hipEvent_t>> events;
 };
 
@@ -136,7 +138,7 @@ fs_status fs_context_create(int hip_device, fs_context **out) {
   if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
   if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
     return fail(FS_ERR_UNSUPPORTED, std::string("libfleetsieve is built for gfx950, device is ") + prop.gcnArchName);
-  *out = new fs_context{hip_device, 0, 0, {}};
+  *out = new fs_context{hip_device, 0, 0, 0, 0, {}};
   return FS_OK;
 }
 
@@ -174,6 +176,18 @@ fs_status fs_context_set_option(fs_context *ctx, fs_option option, int64_t value
   if (option == FS_OPT_SCORE_KERNEL) {
     if (value < 0 || value > 3) return fail(FS_ERR_INVALID_ARGUMENT, "score kernel must be 0, 1, 2 or 3");
     ctx->score_kernel = (int)value;
+    return FS_OK;
+  }
+  if (option == FS_OPT_SAMPLES_PER_LANE) {
+    if (value != 0 && value != 4 && value != 8 && value != 16)
+      return fail(FS_ERR_INVALID_ARGUMENT, "samples per lane must be 0, 4, 8 or 16");
+    ctx->spl = (int)value;
+    return FS_OK;
+  }
+  if (option == FS_OPT_WAVES_PER_BLOCK) {
+    if (value != 0 && value != 1 && value != 4)
+      return fail(FS_ERR_INVALID_ARGUMENT, "waves per block must be 0, 1 or 4");
+    ctx->wpb = (int)value;
     return FS_OK;
   }
   if (option == FS_OPT_KERNEL_TIMING) {
@@ -288,7 +302,7 @@ fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals
   }
   fs::ScoreArgs a{iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi, iv.measured, d_cand, d_cap_s, d_tail_s,
                   n_orders, n_cand, S, d_score, d_gap_now, d_best, d_tau_dump, ws, L, kernel,
-                  nullptr, nullptr};
+                  ctx->spl, ctx->wpb, nullptr, nullptr};
   if (ctx->timing && n_cand > 0) {
     e = hipEventCreate(&a.ev_begin);
     if (e == hipSuccess) e = hipEventCreate(&a.ev_end);

@@ -51,7 +51,7 @@ struct TileInfo {
   int32_t cls, t, rlo, rhi;  // class, TP degree, replica range (rlo > rhi: unused cell)
   int32_t u_m, u_p;          // U of the conservative / optimistic realisation (bits)
   int32_t state;             // 0 = solve, 1 = measured, -1 = invalid candidate
-  int32_t ti;                // TP index
+  int32_t cell;              // candidate cell index
 };
 
 // Workspace layout; every region is 256-byte aligned.
@@ -61,10 +61,9 @@ struct WsLayout {
   size_t base;     // int32 [O][2]     base tau bits (conservative, optimistic)
   size_t opts;     // float [O][2][K][PP][2] option (cap, tail), lane kernel only
   size_t partial;  // double [O][E][ceil(S/64)]
-  size_t tiles;    // TileInfo [O][E]                       exclusion scorer
-  size_t tabB;     // int32 [O][2][K][G+1] per-class tables   exclusion scorer
-  size_t tabP;     // int32 [O][2][K][G+1] prefix convolutions
-  size_t tabH;     // int32 [O][2][K][G+1] all classes but one
+  size_t tiles;      // TileInfo [O][E]                       exclusion scorer
+  size_t tabH;       // int32 [O][2][K][G+1] all classes but one
+  size_t tabB;       // int32 [O][2][4][K][G+1] set-up tables when LDS is too small
   size_t flag;     // int32 [4]        validation / error flags
   size_t total;
   int64_t n_partial;  // ceil(S / 64)
@@ -92,6 +91,8 @@ struct ScoreArgs {
   uint8_t *ws;
   WsLayout L;
   int kernel;  // 1 = wave per scenario, 2 = lane per scenario, 3 = exclusion
+  int spl;     // exclusion scorer: samples per lane (4, 8 or 16; 0 = default)
+  int wpb;     // exclusion scorer: wavefronts per block (1 or 4; 0 = default)
   hipEvent_t ev_begin, ev_end;  // recorded around the scoring kernel if set
 };
 

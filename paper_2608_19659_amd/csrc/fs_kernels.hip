@@ -574,314 +574,6 @@ __global__ __launch_bounds__(256) void k_score_lane(DevProblem P, const CandInfo
 // over the same binary32 values, so it is bit-identical to the full solve.
 // ---------------------------------------------------------------------------
 
-// Z[g] = max_{a <= g} min(X[g - a], Y[a]) for g = 0..G (all in LDS).
-__device__ void block_conv(const int *X, const int *Y, int *Z, int G) {
-  for (int g = threadIdx.x; g <= G; g += blockDim.x) {
-    int best = INT_MIN;
-    for (int a = 0; a <= g; ++a) best = max(best, min(X[g - a], Y[a]));
-    Z[g] = best;
-  }
-}
-
-__device__ void block_copy_in(int *dst, const int32_t *src, int n) {
-  for (int g = threadIdx.x; g < n; g += blockDim.x) dst[g] = src[g];
-}
-
-__device__ void block_copy_out(int32_t *dst, const int *src, int n) {
-  for (int g = threadIdx.x; g < n; g += blockDim.x) dst[g] = src[g];
-}
-
-// In-place prefix maximum of T[0..G] by wavefront 0 of the block.
-__device__ void block_prefix_max(int *T, int G) {
-  if (threadIdx.x < kWave) {
-    const int lane = threadIdx.x;
-    int carry = INT_MIN;
-    for (int base = 0; base <= G; base += kWave) {
-      const int g = base + lane;
-      int v = (g <= G) ? T[g] : INT_MIN;
-      v = max(wave_scan_max(v, lane), carry);
-      if (g <= G) T[g] = v;
-      carry = __shfl(v, kWave - 1, kWave);
-    }
-  }
-}
-
-// Best ratio of class k with at most g GPUs, for g = 0..G, into T (LDS).
-// Options whose cell is `skip_cell` are left out.
-__device__ void block_class_table(const DevProblem &P, int k, const float *cap, const float *tail,
-                                  int skip_cell, int *T) {
-  const int G = P.G;
-  for (int g = threadIdx.x; g <= G; g += blockDim.x) T[g] = 0;
-  __syncthreads();
-  for (int ti = 0; ti < P.NT; ++ti) {
-    const int t = P.tp[ti];
-    for (int r = 1 + threadIdx.x; t * r <= G; r += blockDim.x) {
-      const int b = level_of(P, k, r);
-      if (b < 0) continue;
-      const int cell = cell_of(P, k, ti, b);
-      if (cell == skip_cell) continue;
-      atomicMax(&T[t * r], ratio_bits(cap[cell], tail[cell], r, P.slo[k], P.rcp_demand[k]));
-    }
-  }
-  __syncthreads();
-  block_prefix_max(T, G);
-  __syncthreads();
-}
-
-// Per (realisation, order): class tables, prefix convolutions, the
-// all-but-one tables H_i and the base objective.
-__global__ __launch_bounds__(256) void k_tables(DevProblem P, const float *__restrict__ cap_lo,
-                                                const float *__restrict__ cap_hi,
-                                                const float *__restrict__ tail_lo,
-                                                const float *__restrict__ tail_hi,
-                                                int32_t *__restrict__ tabB, int32_t *__restrict__ tabP,
-                                                int32_t *__restrict__ tabH, int32_t *__restrict__ base) {
-  extern __shared__ int lds[];
-  const int R = blockIdx.x, o = blockIdx.y;
-  const int G = P.G, K = P.K, W = G + 1;
-  int *X = lds, *Y = lds + W, *Z = lds + 2 * W;
-  const size_t off = (size_t)o * P.N;
-  // Section 4.1: conservative = (low capacity, high tail); optimistic = (high, low).
-  const float *cap = (R == 0 ? cap_lo : cap_hi) + off;
-  const float *tail = (R == 0 ? tail_hi : tail_lo) + off;
-  const size_t tb = ((size_t)o * 2 + R) * K * W;
-  int32_t *Bt = tabB + tb, *Pt = tabP + tb, *Ht = tabH + tb;
-
-  for (int k = 0; k < K; ++k) {
-    block_class_table(P, k, cap, tail, -1, X);
-    block_copy_out(Bt + (size_t)k * W, X, W);
-    if (k == 0) block_copy_out(Pt, X, W);
-    __syncthreads();
-  }
-  if (K == 1) {
-    for (int g = threadIdx.x; g <= G; g += blockDim.x) Ht[g] = INT_MAX;  // empty convolution
-    if (threadIdx.x == 0) base[o * 2 + R] = Bt[G];
-    return;
-  }
-  // prefix: P_0 = B_0, P_k = P_{k-1} (.) B_k for k = 1..K-2
-  block_copy_in(X, Pt, W);
-  __syncthreads();
-  for (int k = 1; k <= K - 2; ++k) {
-    block_copy_in(Y, Bt + (size_t)k * W, W);
-    __syncthreads();
-    block_conv(X, Y, Z, G);
-    __syncthreads();
-    block_copy_out(Pt + (size_t)k * W, Z, W);
-    for (int g = threadIdx.x; g <= G; g += blockDim.x) X[g] = Z[g];
-    __syncthreads();
-  }
-  // suffix S_{i+1} in Y; H_i = P_{i-1} (.) S_{i+1}; H_{K-1} = P_{K-2}; H_0 = S_1
-  block_copy_out(Ht + (size_t)(K - 1) * W, X, W);  // X holds P_{K-2}
-  block_copy_in(Y, Bt + (size_t)(K - 1) * W, W);
-  __syncthreads();
-  for (int i = K - 2; i >= 1; --i) {
-    block_copy_in(X, Pt + (size_t)(i - 1) * W, W);
-    __syncthreads();
-    block_conv(X, Y, Z, G);
-    __syncthreads();
-    block_copy_out(Ht + (size_t)i * W, Z, W);
-    block_copy_in(X, Bt + (size_t)i * W, W);
-    __syncthreads();
-    block_conv(X, Y, Z, G);
-    __syncthreads();
-    for (int g = threadIdx.x; g <= G; g += blockDim.x) Y[g] = Z[g];
-    __syncthreads();
-  }
-  block_copy_out(Ht, Y, W);  // H_0 = S_1
-  // base objective = max_g min(B_0[g], H_0[G - g])
-  block_copy_in(X, Bt, W);
-  __syncthreads();
-  int best = INT_MIN;
-  for (int g = threadIdx.x; g <= G; g += blockDim.x) best = max(best, min(X[g], Y[G - g]));
-  best = wave_max(best);
-  __shared__ int wbest[4];
-  if ((threadIdx.x & (kWave - 1)) == 0) wbest[threadIdx.x >> 6] = best;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int v = wbest[0];
-    for (int w = 1; w < (int)(blockDim.x >> 6); ++w) v = max(v, wbest[w]);
-    base[o * 2 + R] = v;
-  }
-}
-
-// Per (candidate, order): the candidate's class, TP and replica range, and
-// U of both realisations.  One wavefront per tile; order-0 blocks also
-// record the candidate info used by the finalize step.
-__global__ __launch_bounds__(64) void k_tile_prep(DevProblem P, const int32_t *__restrict__ cand,
-                                                  int32_t E, const uint8_t *__restrict__ measured,
-                                                  const float *__restrict__ cap_lo,
-                                                  const float *__restrict__ cap_hi,
-                                                  const float *__restrict__ tail_lo,
-                                                  const float *__restrict__ tail_hi,
-                                                  const int32_t *__restrict__ tabH,
-                                                  TileInfo *__restrict__ tiles,
-                                                  CandInfo *__restrict__ info) {
-  extern __shared__ int T[];
-  const int e = blockIdx.x, o = blockIdx.y, lane = threadIdx.x;
-  const int G = P.G, W = G + 1;
-  const int cell = cand[e];
-  TileInfo tl;
-  tl.cls = 0; tl.t = 0; tl.rlo = 1; tl.rhi = 0; tl.u_m = 0; tl.u_p = 0; tl.ti = 0;
-  const size_t tile = (size_t)o * E + e;
-  if (cell < 0 || cell >= P.N) {
-    tl.state = -1;
-    if (lane == 0) {
-      tiles[tile] = tl;
-      if (o == 0) {
-        CandInfo ci;
-        ci.cls = -1; ci.ti = 0; ci.rlo = 1; ci.rhi = 0; ci.cell = cell; ci.tp = 0; ci.pad0 = ci.pad1 = 0;
-        info[e] = ci;
-      }
-    }
-    return;
-  }
-  const int b = cell % P.B;
-  const int ti = (cell / P.B) % P.NT;
-  const int k = cell / (P.B * P.NT);
-  const int t = P.tp[ti];
-  int rlo = INT_MAX, rhi = -1;
-  for (int r = 1 + lane; t * r <= G; r += kWave) {
-    if (level_of(P, k, r) == b) {
-      rlo = min(rlo, r);
-      rhi = max(rhi, r);
-    }
-  }
-  rlo = wave_min(rlo);
-  rhi = wave_max(rhi);
-  if (rhi < 0) { rlo = 1; rhi = 0; }
-  tl.cls = k; tl.t = t; tl.ti = ti; tl.rlo = rlo; tl.rhi = rhi;
-  const size_t off = (size_t)o * P.N;
-  tl.state = measured[off + cell] ? 1 : 0;
-  if (tl.state == 0) {
-    for (int R = 0; R < 2; ++R) {
-      const float *cap = (R == 0 ? cap_lo : cap_hi) + off;
-      const float *tail = (R == 0 ? tail_hi : tail_lo) + off;
-      block_class_table(P, k, cap, tail, cell, T);
-      const int32_t *H = tabH + (((size_t)o * 2 + R) * P.K + k) * W;
-      int best = INT_MIN;
-      for (int g = lane; g <= G; g += kWave) best = max(best, min(T[g], H[G - g]));
-      best = wave_max(best);
-      if (R == 0) tl.u_m = best;
-      else tl.u_p = best;
-      __syncthreads();
-    }
-  }
-  if (lane == 0) {
-    tiles[tile] = tl;
-    if (o == 0) {
-      CandInfo ci;
-      ci.cls = k; ci.ti = ti; ci.rlo = rlo; ci.rhi = rhi; ci.cell = cell; ci.tp = t;
-      ci.pad0 = ci.pad1 = 0;
-      info[e] = ci;
-    }
-  }
-}
-
-// Scenarios of the exclusion scorer: block (chunk, e, o) holds 256 lanes x
-// SPL consecutive samples; lane l owns samples [chunk*256*SPL + l*SPL, +SPL).
-template <int SPL>
-__global__ __launch_bounds__(256) void k_score_excl(DevProblem P, const TileInfo *__restrict__ tiles,
-                                                    const int32_t *__restrict__ tabH,
-                                                    const float *__restrict__ cap_s,
-                                                    const float *__restrict__ tail_s, int32_t E,
-                                                    int32_t S, const int32_t *__restrict__ base,
-                                                    double *__restrict__ partial, int64_t n_partial,
-                                                    float *__restrict__ tau_dump) {
-  constexpr int CHUNK = 256 * SPL;
-  extern __shared__ int Mlds[];
-  __shared__ double wsum[4];
-  const int chunk = blockIdx.x, e = blockIdx.y, o = blockIdx.z;
-  const size_t tile = (size_t)o * E + e;
-  const TileInfo tl = tiles[tile];
-  if (tl.state < 0) return;
-  const int s_first = chunk * CHUNK + threadIdx.x * SPL;
-  if (tl.state == 1) {
-    if (tau_dump) {
-      for (int q = 0; q < SPL; ++q) {
-        if (s_first + q < S) {
-          tau_dump[(tile * S + s_first + q) * 2 + 0] = __int_as_float(base[o * 2 + 0]);
-          tau_dump[(tile * S + s_first + q) * 2 + 1] = __int_as_float(base[o * 2 + 1]);
-        }
-      }
-    }
-    return;
-  }
-  const int G = P.G, W = G + 1;
-  const int nr = tl.rhi >= tl.rlo ? tl.rhi - tl.rlo + 1 : 0;
-  const int nr4 = (nr + 3) & ~3;
-  int *Mm = Mlds, *Mp = Mlds + nr4;
-  const int32_t *Hm = tabH + (((size_t)o * 2 + 0) * P.K + tl.cls) * W;
-  const int32_t *Hp = tabH + (((size_t)o * 2 + 1) * P.K + tl.cls) * W;
-  for (int j = threadIdx.x; j < nr4; j += blockDim.x) {
-    const int r = tl.rlo + j;
-    // padding entries are 0: min(f, 0) <= 0 <= U never raises the maximum
-    Mm[j] = j < nr ? Hm[G - tl.t * r] : 0;
-    Mp[j] = j < nr ? Hp[G - tl.t * r] : 0;
-  }
-  __syncthreads();
-
-  float cs[SPL], ls[SPL];
-  const size_t sbase = tile * S + s_first;
-  if (s_first + SPL <= S && (SPL == 4) && ((sbase & 3) == 0)) {
-    const float4 c4 = *reinterpret_cast<const float4 *>(cap_s + sbase);
-    const float4 l4 = *reinterpret_cast<const float4 *>(tail_s + sbase);
-    cs[0] = c4.x; cs[1] = c4.y; cs[2] = c4.z; cs[3] = c4.w;
-    ls[0] = l4.x; ls[1] = l4.y; ls[2] = l4.z; ls[3] = l4.w;
-  } else {
-#pragma unroll
-    for (int q = 0; q < SPL; ++q) {
-      const bool live = s_first + q < S;
-      cs[q] = live ? cap_s[sbase + q] : 0.0f;
-      ls[q] = live ? tail_s[sbase + q] : 0.0f;
-    }
-  }
-  const double rcp = P.rcp_demand[tl.cls];
-  int am[SPL], ap[SPL];
-#pragma unroll
-  for (int q = 0; q < SPL; ++q) { am[q] = tl.u_m; ap[q] = tl.u_p; }
-  for (int j = 0; j < nr4; j += 4) {
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const float rf = (float)(tl.rlo + j + u);
-      const int mm = Mm[j + u], mp = Mp[j + u];
-#pragma unroll
-      for (int q = 0; q < SPL; ++q) {
-        const float capacity = rf * cs[q];
-        const int fb = __float_as_int(fminf((float)((double)capacity * rcp), 1.0f));
-        am[q] = max(am[q], min(fb, mm));
-        ap[q] = max(ap[q], min(fb, mp));
-      }
-    }
-  }
-  const float slo = P.slo[tl.cls];
-  double gq[SPL];
-#pragma unroll
-  for (int q = 0; q < SPL; ++q) {
-    // a sampled tail above the SLO makes every option on the cell worth 0
-    const bool tail_ok = ls[q] <= slo;
-    const int tm = tail_ok ? am[q] : tl.u_m;
-    const int tp = tail_ok ? ap[q] : tl.u_p;
-    const bool live = s_first + q < S;
-    gq[q] = live ? (double)__int_as_float(tp) - (double)__int_as_float(tm) : 0.0;
-    if (tau_dump && live) {
-      tau_dump[(sbase + q) * 2 + 0] = __int_as_float(tm);
-      tau_dump[(sbase + q) * 2 + 1] = __int_as_float(tp);
-    }
-  }
-  // pairwise tree: within the lane's SPL consecutive samples, then lanes
-  double v;
-  if (SPL == 4) v = (gq[0] + gq[1]) + (gq[2 % SPL] + gq[3 % SPL]);
-  else if (SPL == 2) v = gq[0] + gq[1 % SPL];
-  else v = gq[0];
-  v = wave_pairwise_sum(v);
-  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = v;
-  __syncthreads();
-  if (threadIdx.x == 0) partial[tile * n_partial + chunk] = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
-}
-
-// ---------------------------------------------------------------------------
-// Finalize: score = Gamma_t - (pairwise sum of partials) / S, and the argmax.
-// ---------------------------------------------------------------------------
 struct Pick {
   double score;
   int tp, cell, e;  // e < 0: nothing
@@ -896,6 +588,483 @@ __device__ __forceinline__ bool better(const Pick &a, const Pick &b) {
   return a.e < b.e;
 }
 
+// Z[g] = max_{a <= g} min(X[g - a], Y[a]) for one target g.
+__device__ __forceinline__ int conv_at(const int *X, const int *Y, int g) {
+  int best = INT_MIN;
+  for (int a = 0; a <= g; ++a) best = max(best, min(X[g - a], Y[a]));
+  return best;
+}
+
+// The same target split over 4 consecutive lanes (lane j of the group takes
+// a = j, j + 4, ...); every lane of the group returns the full maximum.
+// All 64 lanes of the wavefront must call it.
+__device__ __forceinline__ int conv_at4(const int *X, const int *Y, int g, bool active) {
+  const int j = threadIdx.x & 3;
+  int best = INT_MIN;
+  if (active) {
+#pragma unroll 4
+    for (int a = j; a <= g; a += 4) best = max(best, min(X[g - a], Y[a]));
+  }
+  best = max(best, __shfl_xor(best, 1, kWave));
+  best = max(best, __shfl_xor(best, 2, kWave));
+  return best;
+}
+
+__device__ __forceinline__ double load_acquire(const double *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Pairwise tree over x[0..n), zero-padded to a power of two P2 <= 4096, by
+// one full wavefront: lane l first sums its aligned block of P2/64 values
+// (a balanced tree in registers), then the lanes combine by butterfly.
+__device__ double wave_tree_sum(const double *x, int64_t n) {
+  constexpr int kMaxL = 64;
+  const int lane = threadIdx.x & (kWave - 1);
+  int64_t p2 = 1;
+  while (p2 < n) p2 <<= 1;
+  const int L = p2 >= kWave ? (int)(p2 / kWave) : 1;
+  double v[kMaxL];
+#pragma unroll
+  for (int j = 0; j < kMaxL; ++j) {
+    const int64_t i = (int64_t)lane * L + j;
+    v[j] = (j < L && i < n) ? load_acquire(x + i) : 0.0;
+  }
+#pragma unroll
+  for (int w = 1; w < kMaxL; w <<= 1) {
+    if (w < L) {
+#pragma unroll
+      for (int j = 0; j + w < kMaxL; j += 2 * w) v[j] = v[j] + v[j + w];
+    }
+  }
+  return wave_pairwise_sum(v[0]);
+}
+
+// Decodes a flattened option index p (0 <= p < P = sum_t floor(G / t)) of
+// one class into (TP index, replicas); options are ordered by TP, then r.
+__device__ __forceinline__ void option_of(const DevProblem &P, int p, int *ti, int *r) {
+  int t = 0;
+  for (; t < P.NT - 1; ++t) {
+    const int n = P.G / P.tp[t];
+    if (p < n) break;
+    p -= n;
+  }
+  *ti = t;
+  *r = p + 1;
+}
+
+// Tables per (realisation, order).  Dynamic LDS holds the order's cells of
+// this realisation (cap, tail), the per-cell maxima, the replica range of
+// every cell, the load-level map and, when kLds, the class tables B, the
+// prefix convolutions P, the suffix convolutions S and the all-but-one
+// tables H (4 x K x (G+1) ints); otherwise those four live in `gtab`.
+//   B_k[g]  best ratio of class k with at most g GPUs
+//   P_k = B_0 (.) ... (.) B_k,   S_k = B_k (.) ... (.) B_{K-1}
+//   H_i = P_{i-1} (.) S_{i+1}    (the convolution of every class but i)
+// Then for every option o of class i, w_o = min(f_o, H_i[G - cost_o]): the
+// best objective of an allocation that gives class i exactly option o.  The
+// objective is max(0, max_o w_o) over the options of any one class, and
+// U(cell) is the same maximum without the options that use `cell`, i.e. the
+// best other cell of the class.
+template <bool kLds>
+__global__ __launch_bounds__(1024) void k_prep(DevProblem P, const float *__restrict__ cap_lo,
+                                              const float *__restrict__ cap_hi,
+                                              const float *__restrict__ tail_lo,
+                                              const float *__restrict__ tail_hi,
+                                              const uint8_t *__restrict__ measured,
+                                              const int32_t *__restrict__ cand, int32_t E,
+                                              int32_t *__restrict__ tabH, int32_t *__restrict__ gtab,
+                                              TileInfo *__restrict__ tiles, int32_t *__restrict__ base) {
+  extern __shared__ int lds[];
+  __shared__ int cls_best[kMaxClasses], cls_arg[kMaxClasses], cls_second[kMaxClasses];
+  const int R = blockIdx.x, o = blockIdx.y, tid = threadIdx.x, nth = blockDim.x;
+  const int G = P.G, K = P.K, W = G + 1, N = P.N;
+  const int KW = K * W;
+  float *ccap = (float *)lds;                // [N]
+  float *ctail = ccap + N;                   // [N]
+  int *mc = (int *)(ctail + N);              // [N] best w over the cell's options
+  int *rlo = mc + N, *rhi = rlo + N;         // [N] replica range using the cell
+  int8_t *lvl = (int8_t *)(rhi + N);         // [K][W]
+  int *tabs = kLds ? (int *)(lvl + ((KW + 15) & ~15)) : gtab + ((size_t)o * 2 + R) * 4 * KW;
+  int *Bt = tabs, *Pt = tabs + KW, *St = tabs + 2 * KW, *Ht = tabs + 3 * KW;
+  const size_t off = (size_t)o * N;
+  // Section 4.1: conservative = (low capacity, high tail); optimistic = (high, low).
+  const float *gcap = (R == 0 ? cap_lo : cap_hi) + off;
+  const float *gtail = (R == 0 ? tail_hi : tail_lo) + off;
+  int PPc = 0;  // options per class
+  for (int t = 0; t < P.NT; ++t) PPc += G / P.tp[t];
+
+  for (int c = tid; c < N; c += nth) {
+    ccap[c] = gcap[c];
+    ctail[c] = gtail[c];
+    mc[c] = INT_MIN;
+    rlo[c] = INT_MAX;
+    rhi[c] = -1;
+  }
+  for (int idx = tid; idx < KW; idx += nth) {
+    const int k = idx / W, r = idx - k * W;
+    lvl[idx] = (int8_t)(r >= 1 ? level_of(P, k, r) : -1);
+    Bt[idx] = 0;
+  }
+  __syncthreads();
+  // class tables: every option max-merged into its exact GPU count; also the
+  // replica range of every cell
+  for (int q = tid; q < K * PPc; q += nth) {
+    const int k = q / PPc;
+    int ti, r;
+    option_of(P, q - k * PPc, &ti, &r);
+    const int b = lvl[k * W + r];
+    if (b < 0) continue;
+    const int t = P.tp[ti];
+    const int cell = cell_of(P, k, ti, b);
+    atomicMax(&Bt[k * W + t * r], ratio_bits(ccap[cell], ctail[cell], r, P.slo[k], P.rcp_demand[k]));
+    atomicMin(&rlo[cell], r);
+    atomicMax(&rhi[cell], r);
+  }
+  __syncthreads();
+  // ... then best with at most g GPUs: prefix maximum, one class per wavefront
+  const int wave = tid >> 6, lane = tid & (kWave - 1), nw = nth >> 6;
+  for (int k = wave; k < K; k += nw) {
+    int *T = Bt + k * W;
+    int carry = INT_MIN;
+    for (int b0 = 0; b0 <= G; b0 += kWave) {
+      const int g = b0 + lane;
+      int v = (g <= G) ? T[g] : INT_MIN;
+      v = max(wave_scan_max(v, lane), carry);
+      if (g <= G) T[g] = v;
+      carry = __shfl(v, kWave - 1, kWave);
+    }
+  }
+  __syncthreads();
+  if (K == 1) {
+    for (int g = tid; g < W; g += nth) Ht[g] = INT_MAX;  // the empty convolution
+  } else {
+    for (int g = tid; g < W; g += nth) {
+      Pt[g] = Bt[g];
+      St[(K - 1) * W + g] = Bt[(K - 1) * W + g];
+    }
+    __syncthreads();
+    // prefix and suffix chains advance together, one step per pass; each
+    // target is shared by a group of 4 lanes
+    const int groups = nth / 4, grp = tid / 4;
+    for (int j = 1; j <= K - 2; ++j) {
+      const int ks = K - 1 - j;
+      for (int base_item = 0; base_item < 2 * W; base_item += groups) {
+        const int item = base_item + grp;
+        const bool act = item < 2 * W;
+        const bool pre = item < W;
+        const int g = pre ? item : item - W;
+        const int v = pre ? conv_at4(Pt + (j - 1) * W, Bt + j * W, g, act)
+                          : conv_at4(Bt + ks * W, St + (ks + 1) * W, act ? g : 0, act);
+        if (act && (tid & 3) == 0) {
+          if (pre) Pt[j * W + g] = v;
+          else St[ks * W + g] = v;
+        }
+      }
+      __syncthreads();
+    }
+    for (int base_item = 0; base_item < KW; base_item += groups) {
+      const int item = base_item + grp;
+      const bool act = item < KW;
+      const int i = act ? item / W : 0, g = act ? item - i * W : 0;
+      const bool mid = act && i > 0 && i < K - 1;
+      const int v = conv_at4(Pt + (mid ? i - 1 : 0) * W, St + (mid ? i + 1 : 0) * W, g, mid);
+      if (act && (tid & 3) == 0) {
+        if (i == 0) Ht[item] = St[W + g];
+        else if (i == K - 1) Ht[item] = Pt[(K - 2) * W + g];
+        else Ht[item] = v;
+      }
+    }
+  }
+  __syncthreads();
+  int32_t *Hg = tabH + ((size_t)o * 2 + R) * KW;
+  for (int idx = tid; idx < KW; idx += nth) Hg[idx] = Ht[idx];
+  // w_o per option, folded into its cell's maximum
+  for (int q = tid; q < K * PPc; q += nth) {
+    const int k = q / PPc;
+    int ti, r;
+    option_of(P, q - k * PPc, &ti, &r);
+    const int b = lvl[k * W + r];
+    if (b < 0) continue;
+    const int t = P.tp[ti];
+    const int cell = cell_of(P, k, ti, b);
+    const int f = ratio_bits(ccap[cell], ctail[cell], r, P.slo[k], P.rcp_demand[k]);
+    atomicMax(&mc[cell], min(f, Ht[k * W + G - t * r]));
+  }
+  __syncthreads();
+  // per class: best cell value, its cell, and the best of the other cells
+  const int per_class = P.NT * P.B;
+  for (int k = wave; k < K; k += nw) {
+    int best = INT_MIN;
+    for (int c = lane; c < per_class; c += kWave) best = max(best, mc[k * per_class + c]);
+    best = wave_max(best);
+    int arg = INT_MAX;
+    for (int c = lane; c < per_class; c += kWave)
+      if (mc[k * per_class + c] == best) arg = min(arg, c);
+    arg = wave_min(arg);
+    int second = INT_MIN;
+    for (int c = lane; c < per_class; c += kWave)
+      if (c != arg) second = max(second, mc[k * per_class + c]);
+    second = wave_max(second);
+    if (lane == 0) {
+      cls_best[k] = best;
+      cls_arg[k] = k * per_class + arg;
+      cls_second[k] = second;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) base[o * 2 + R] = max(0, cls_best[0]);  // 0: the empty allocation
+  // tile records
+  for (int e = tid; e < E; e += nth) {
+    TileInfo *tl = tiles + (size_t)o * E + e;
+    const int cell = cand[e];
+    if (cell < 0 || cell >= N) {
+      if (R == 0) {
+        tl->state = -1; tl->cell = cell; tl->cls = 0; tl->t = 0; tl->rlo = 1; tl->rhi = 0; tl->u_m = 0;
+      } else {
+        tl->u_p = 0;
+      }
+      continue;
+    }
+    const int k = cell / per_class;
+    const int u = max(0, cell == cls_arg[k] ? cls_second[k] : cls_best[k]);
+    if (R == 0) {
+      const int ti = (cell / P.B) % P.NT;
+      tl->cls = k; tl->t = P.tp[ti]; tl->cell = cell;
+      tl->rlo = rhi[cell] >= 0 ? rlo[cell] : 1;
+      tl->rhi = rhi[cell];
+      if (rhi[cell] < 0) tl->rhi = 0;
+      tl->state = measured[off + cell] ? 1 : 0;
+      tl->u_m = u;
+    } else {
+      tl->u_p = u;
+    }
+  }
+}
+
+// Scenarios of the exclusion scorer: block (chunk, e, o) holds 64*WPB lanes x
+// SPL consecutive samples; lane l owns samples [chunk*CHUNK + l*SPL, +SPL).
+template <int SPL, int WPB>
+__global__ __launch_bounds__(64 * WPB) void k_score_excl(DevProblem P, const TileInfo *__restrict__ tiles,
+                                                    const int32_t *__restrict__ tabH,
+                                                    const float *__restrict__ cap_s,
+                                                    const float *__restrict__ tail_s, int32_t E,
+                                                    int32_t S, const int32_t *__restrict__ base,
+                                                    double *__restrict__ partial, int64_t n_partial,
+                                                    float *__restrict__ tau_dump) {
+  constexpr int CHUNK = 64 * WPB * SPL;
+  extern __shared__ int Mlds[];
+  __shared__ double wsum[WPB];
+  const int chunk = blockIdx.x, e = blockIdx.y, o = blockIdx.z;
+  const size_t tile = (size_t)o * E + e;
+  const TileInfo tl = tiles[tile];
+  const int s_first = chunk * CHUNK + threadIdx.x * SPL;
+  const size_t sbase = tile * S + s_first;
+  double block_sum = 0.0;
+  if (tl.state == 1 && tau_dump) {
+    for (int q = 0; q < SPL; ++q) {
+      if (s_first + q < S) {
+        tau_dump[(sbase + q) * 2 + 0] = __int_as_float(base[o * 2 + 0]);
+        tau_dump[(sbase + q) * 2 + 1] = __int_as_float(base[o * 2 + 1]);
+      }
+    }
+  }
+  if (tl.state == 0) {
+    const int G = P.G, W = G + 1;
+    const int nr = tl.rhi >= tl.rlo ? tl.rhi - tl.rlo + 1 : 0;
+    const int nr4 = (nr + 3) & ~3;
+    float cs[SPL], ls[SPL];
+    // with no replica count on the cell the samples cannot matter
+    const bool need = nr > 0 || tau_dump;
+    if (need && s_first + SPL <= S && ((sbase & 3) == 0)) {
+#pragma unroll
+      for (int v4 = 0; v4 < SPL / 4; ++v4) {
+        const float4 c4 = *reinterpret_cast<const float4 *>(cap_s + sbase + 4 * v4);
+        const float4 l4 = *reinterpret_cast<const float4 *>(tail_s + sbase + 4 * v4);
+        cs[4 * v4 + 0] = c4.x; cs[4 * v4 + 1] = c4.y; cs[4 * v4 + 2] = c4.z; cs[4 * v4 + 3] = c4.w;
+        ls[4 * v4 + 0] = l4.x; ls[4 * v4 + 1] = l4.y; ls[4 * v4 + 2] = l4.z; ls[4 * v4 + 3] = l4.w;
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < SPL; ++q) {
+        const bool live = need && s_first + q < S;
+        cs[q] = live ? cap_s[sbase + q] : 0.0f;
+        ls[q] = live ? tail_s[sbase + q] : 0.0f;
+      }
+    }
+    int *Mm = Mlds, *Mp = Mlds + nr4;
+    const int32_t *Hm = tabH + (((size_t)o * 2 + 0) * P.K + tl.cls) * W;
+    const int32_t *Hp = tabH + (((size_t)o * 2 + 1) * P.K + tl.cls) * W;
+    for (int j = threadIdx.x; j < nr4; j += blockDim.x) {
+      const int r = tl.rlo + j;
+      // padding entries are 0: min(f, 0) <= 0 <= U never raises the maximum
+      Mm[j] = j < nr ? Hm[G - tl.t * r] : 0;
+      Mp[j] = j < nr ? Hp[G - tl.t * r] : 0;
+    }
+    __syncthreads();
+    const double rcp = P.rcp_demand[tl.cls];
+    int am[SPL], ap[SPL];
+#pragma unroll
+    for (int q = 0; q < SPL; ++q) { am[q] = tl.u_m; ap[q] = tl.u_p; }
+    for (int j = 0; j < nr4; j += 4) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float rf = (float)(tl.rlo + j + u);
+        const int mm = Mm[j + u], mp = Mp[j + u];
+#pragma unroll
+        for (int q = 0; q < SPL; ++q) {
+          const float capacity = rf * cs[q];
+          const int fb = __float_as_int(fminf((float)((double)capacity * rcp), 1.0f));
+          am[q] = max(am[q], min(fb, mm));
+          ap[q] = max(ap[q], min(fb, mp));
+        }
+      }
+    }
+    const float slo = P.slo[tl.cls];
+    double gq[SPL];
+#pragma unroll
+    for (int q = 0; q < SPL; ++q) {
+      // a sampled tail above the SLO makes every option on the cell worth 0
+      const bool tail_ok = ls[q] <= slo;
+      const int tm = tail_ok ? am[q] : tl.u_m;
+      const int tp = tail_ok ? ap[q] : tl.u_p;
+      const bool live = s_first + q < S;
+      gq[q] = live ? (double)__int_as_float(tp) - (double)__int_as_float(tm) : 0.0;
+      if (tau_dump && live) {
+        tau_dump[(sbase + q) * 2 + 0] = __int_as_float(tm);
+        tau_dump[(sbase + q) * 2 + 1] = __int_as_float(tp);
+      }
+    }
+    // pairwise tree: within the lane's SPL consecutive samples, then lanes
+#pragma unroll
+    for (int w = 1; w < SPL; w <<= 1) {
+#pragma unroll
+      for (int j = 0; j + w < SPL; j += 2 * w) gq[j] = gq[j] + gq[j + w];
+    }
+    double v = wave_pairwise_sum(gq[0]);
+    if (WPB == 1) {
+      block_sum = v;
+    } else {
+      if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = v;
+      __syncthreads();
+      block_sum = (wsum[0] + wsum[1 % WPB]) + (wsum[2 % WPB] + wsum[3 % WPB]);
+    }
+  }
+  if (tl.state == 0 && threadIdx.x == 0) partial[tile * n_partial + chunk] = block_sum;
+}
+// Scores and best candidate of the exclusion scorer: one block per order,
+// one thread per candidate.  Each tile's partials (at most 16 here) are
+// summed by the pairwise tree in registers.
+__global__ __launch_bounds__(256) void k_finalize_excl(const TileInfo *__restrict__ tiles, int32_t E,
+                                                       int32_t S, const int32_t *__restrict__ base,
+                                                       const double *__restrict__ partial,
+                                                       int64_t n_partial, double *__restrict__ score,
+                                                       double *__restrict__ gap_now,
+                                                       int32_t *__restrict__ best) {
+  __shared__ Pick s_pick[4];
+  const int o = blockIdx.x;
+  const double gap = (double)__int_as_float(base[o * 2 + 1]) - (double)__int_as_float(base[o * 2 + 0]);
+  int p2 = 1;
+  while (p2 < n_partial) p2 <<= 1;
+  Pick mine{0.0, 0, 0, -1};
+  for (int e = threadIdx.x; e < E; e += blockDim.x) {
+    const size_t tile = (size_t)o * E + e;
+    const TileInfo tl = tiles[tile];
+    double sc = 0.0;  // a revealed cell: nothing to learn
+    if (tl.state < 0) {
+      sc = __builtin_nan("");
+    } else if (tl.state == 0) {
+      const double *x = partial + tile * n_partial;
+      double v[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) v[j] = j < n_partial ? x[j] : 0.0;
+#pragma unroll
+      for (int w = 1; w < 16; w <<= 1) {
+        if (w < p2) {
+#pragma unroll
+          for (int j = 0; j + w < 16; j += 2 * w) v[j] = v[j] + v[j + w];
+        }
+      }
+      sc = gap - v[0] / (double)S;
+      const Pick c{sc, tl.t, tl.cell, e};
+      if (better(c, mine)) mine = c;
+    }
+    score[tile] = sc;
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    Pick other;
+    other.score = __shfl_xor(mine.score, off, kWave);
+    other.tp = __shfl_xor(mine.tp, off, kWave);
+    other.cell = __shfl_xor(mine.cell, off, kWave);
+    other.e = __shfl_xor(mine.e, off, kWave);
+    if (better(other, mine)) mine = other;
+  }
+  if ((threadIdx.x & 63) == 0) s_pick[threadIdx.x >> 6] = mine;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < (int)(blockDim.x >> 6); ++w)
+      if (better(s_pick[w], mine)) mine = s_pick[w];
+    if (best) best[o] = mine.e;
+    if (gap_now) gap_now[o] = gap;
+  }
+}
+
+// Scores and best candidate, many partials per tile: one wavefront per
+// candidate sums the tile's partials; then a second pass picks the best.
+__global__ __launch_bounds__(256) void k_tile_scores_wave(const TileInfo *__restrict__ tiles, int32_t E,
+                                                          int32_t S, const int32_t *__restrict__ base,
+                                                          const double *__restrict__ partial,
+                                                          int64_t n_partial, double *__restrict__ score) {
+  const int o = blockIdx.y;
+  const int e = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (e >= E) return;
+  const size_t tile = (size_t)o * E + e;
+  const TileInfo tl = tiles[tile];
+  double sc = 0.0;
+  if (tl.state < 0) sc = __builtin_nan("");
+  if (tl.state == 0) {
+    const double gap = (double)__int_as_float(base[o * 2 + 1]) - (double)__int_as_float(base[o * 2 + 0]);
+    sc = gap - wave_tree_sum(partial + tile * n_partial, n_partial) / (double)S;
+  }
+  if ((threadIdx.x & 63) == 0) score[tile] = sc;
+}
+
+__global__ __launch_bounds__(256) void k_pick_best(const TileInfo *__restrict__ tiles, int32_t E,
+                                                   const int32_t *__restrict__ base,
+                                                   const double *__restrict__ score,
+                                                   double *__restrict__ gap_now, int32_t *__restrict__ best) {
+  __shared__ Pick s_pick[4];
+  const int o = blockIdx.x;
+  Pick mine{0.0, 0, 0, -1};
+  for (int e = threadIdx.x; e < E; e += blockDim.x) {
+    const TileInfo tl = tiles[(size_t)o * E + e];
+    if (tl.state != 0) continue;
+    const Pick c{score[(size_t)o * E + e], tl.t, tl.cell, e};
+    if (better(c, mine)) mine = c;
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    Pick other;
+    other.score = __shfl_xor(mine.score, off, kWave);
+    other.tp = __shfl_xor(mine.tp, off, kWave);
+    other.cell = __shfl_xor(mine.cell, off, kWave);
+    other.e = __shfl_xor(mine.e, off, kWave);
+    if (better(other, mine)) mine = other;
+  }
+  if ((threadIdx.x & 63) == 0) s_pick[threadIdx.x >> 6] = mine;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < (int)(blockDim.x >> 6); ++w)
+      if (better(s_pick[w], mine)) mine = s_pick[w];
+    if (best) best[o] = mine.e;
+    if (gap_now)
+      gap_now[o] = (double)__int_as_float(base[o * 2 + 1]) - (double)__int_as_float(base[o * 2 + 0]);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Finalize: score = Gamma_t - (pairwise sum of partials) / S, and the argmax.
+// ---------------------------------------------------------------------------
 __global__ __launch_bounds__(64) void k_finalize(DevProblem P, const CandInfo *__restrict__ info,
                                                  const uint8_t *__restrict__ measured, int32_t E,
                                                  int32_t S, const int32_t *__restrict__ base,
@@ -1037,6 +1206,18 @@ bool excl_kernel_supported(const DevProblem &P) { return !P.has_floor; }
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Dynamic LDS the exclusion set-up kernel may request, and its block size
+// (its passes are short and latency-bound: width shortens them).
+constexpr size_t kPrepLdsLimit = 60 * 1024;
+constexpr int kPrepThreads = 1024;
+
+// LDS of the exclusion set-up besides its tables: cells (cap, tail), cell
+// maxima, replica ranges, and the level map.
+static size_t prep_lds_small(const DevProblem &P) {
+  const size_t KW = (size_t)P.K * (P.G + 1);
+  return 5 * sizeof(int) * (size_t)P.N + ((KW + 15) & ~(size_t)15);
+}
+
 WsLayout ws_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
   WsLayout L{};
   size_t at = 0;
@@ -1050,9 +1231,11 @@ WsLayout ws_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
   L.flag = at; at = align256(at + sizeof(int32_t) * 4);
   L.tiles = at; at = align256(at + sizeof(TileInfo) * (size_t)O * (size_t)E);
   const size_t tab = excl_kernel_supported(P) ? sizeof(int32_t) * (size_t)O * 2 * P.K * (P.G + 1) : 0;
-  L.tabB = at; at = align256(at + tab);
-  L.tabP = at; at = align256(at + tab);
   L.tabH = at; at = align256(at + tab);
+  // the exclusion set-up keeps B, P, S, H in LDS when they fit, else here
+  const size_t W = (size_t)P.G + 1, KW = (size_t)P.K * W;
+  const bool in_lds = prep_lds_small(P) + 4 * KW * sizeof(int) <= kPrepLdsLimit;
+  L.tabB = at; at = align256(at + (excl_kernel_supported(P) && !in_lds ? 4 * tab : 0));
   L.total = at;
   return L;
 }
@@ -1076,27 +1259,54 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
   const size_t lds = lds_bytes_solver(P, 0);
   if (a.O == 0) return hipSuccess;
   if (a.kernel == 3) {
-    const int W = P.G + 1;
+    const int W = P.G + 1, KW = P.K * W;
     constexpr int kSpl = 4;
     TileInfo *tiles = (TileInfo *)(a.ws + a.L.tiles);
     int32_t *tabH = (int32_t *)(a.ws + a.L.tabH);
-    k_tables<<<dim3(2, a.O), 256, 3 * W * sizeof(int), s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
-                                                           (int32_t *)(a.ws + a.L.tabB),
-                                                           (int32_t *)(a.ws + a.L.tabP), tabH, base);
-    int64_t n_partial = 1;
-    if (a.E > 0) {
-      k_tile_prep<<<dim3(a.E, a.O), 64, W * sizeof(int), s>>>(P, a.cand, a.E, a.measured, a.cap_lo, a.cap_hi,
-                                                             a.tail_lo, a.tail_hi, tabH, tiles, info);
-      n_partial = (a.S + 256 * kSpl - 1) / (256 * kSpl);
-      const int max_nr4 = ((P.G / P.tp[0]) + 3) & ~3;
-      const size_t mlds = 2 * (size_t)max_nr4 * sizeof(int);
-      if (a.ev_begin) (void)hipEventRecord(a.ev_begin, s);
-      k_score_excl<kSpl><<<dim3((unsigned)n_partial, a.E, a.O), 256, mlds, s>>>(
-          P, tiles, tabH, a.cap_s, a.tail_s, a.E, a.S, base, partial, n_partial, a.tau_dump);
-      if (a.ev_end) (void)hipEventRecord(a.ev_end, s);
+    const size_t small = prep_lds_small(P);
+    const size_t big = small + 4 * (size_t)KW * sizeof(int);
+    if (big <= kPrepLdsLimit)
+      k_prep<true><<<dim3(2, a.O), kPrepThreads, big, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured,
+                                                  a.cand, a.E, tabH, nullptr, tiles, base);
+    else
+      k_prep<false><<<dim3(2, a.O), kPrepThreads, small, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
+                                                     a.measured, a.cand, a.E, tabH,
+                                                     (int32_t *)(a.ws + a.L.tabB), tiles, base);
+    if (a.E == 0) {
+      k_finalize<<<a.O, 64, 0, s>>>(P, info, a.measured, 0, a.S, base, partial, 1, a.score, a.gap_now,
+                                    a.best);
+      return hipGetLastError();
     }
-    k_finalize<<<a.O, 64, 0, s>>>(P, info, a.measured, a.E, a.S, base, partial, n_partial, a.score,
-                                  a.gap_now, a.best);
+    const int spl = a.spl == 8 || a.spl == 16 ? a.spl : kSpl;
+    const int wpb = a.wpb == 4 ? 4 : 1;
+    const int64_t chunk = 64 * wpb * spl;
+    const int64_t n_partial = (a.S + chunk - 1) / chunk;
+    const int max_nr4 = ((P.G / P.tp[0]) + 3) & ~3;
+    const size_t mlds = 2 * (size_t)max_nr4 * sizeof(int);
+    const dim3 grid((unsigned)n_partial, a.E, a.O);
+    if (a.ev_begin) (void)hipEventRecord(a.ev_begin, s);
+#define FS_EXCL_LAUNCH(SP, WB)                                                                       \
+  k_score_excl<SP, WB><<<grid, 64 * WB, mlds, s>>>(P, tiles, tabH, a.cap_s, a.tail_s, a.E, a.S, base, \
+                                                   partial, n_partial, a.tau_dump)
+    if (wpb == 1) {
+      if (spl == 16) FS_EXCL_LAUNCH(16, 1);
+      else if (spl == 8) FS_EXCL_LAUNCH(8, 1);
+      else FS_EXCL_LAUNCH(4, 1);
+    } else {
+      if (spl == 16) FS_EXCL_LAUNCH(16, 4);
+      else if (spl == 8) FS_EXCL_LAUNCH(8, 4);
+      else FS_EXCL_LAUNCH(4, 4);
+    }
+#undef FS_EXCL_LAUNCH
+    if (a.ev_end) (void)hipEventRecord(a.ev_end, s);
+    if (n_partial <= 16) {
+      k_finalize_excl<<<a.O, 256, 0, s>>>(tiles, a.E, a.S, base, partial, n_partial, a.score, a.gap_now,
+                                          a.best);
+    } else {
+      k_tile_scores_wave<<<dim3((a.E + 3) / 4, a.O), 256, 0, s>>>(tiles, a.E, a.S, base, partial, n_partial,
+                                                                 a.score);
+      k_pick_best<<<a.O, 256, 0, s>>>(tiles, a.E, base, a.score, a.gap_now, a.best);
+    }
     return hipGetLastError();
   }
   k_base<<<dim3(2, a.O), 64, lds, s>>>(P, bmap, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, base);

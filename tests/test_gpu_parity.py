@@ -474,3 +474,29 @@ def test_validation_mode_rejects_bad_cells(env, monkeypatch):
                             torch.tensor([7], dtype=torch.int32, device="cuda:0"),
                             torch.ones((1, 1, 2), device="cuda:0"), torch.ones((1, 1, 2), device="cuda:0"))
     assert ei.value.status == fs.FS_ERR_INVALID_ARGUMENT
+
+
+@pytest.mark.parametrize("S", [70_000, 600_000, 1 << 20])
+def test_score_many_partials(env, orc, S):
+    """Large sample counts up to the maximum (2^20): many partial sums per
+    tile, reduced by the same pairwise tree as the oracle (exclusion and lane
+    kernels)."""
+    w = make_workload(1, orders=[2], with_samples=False)
+    p, iv = w.problem, w.intervals
+    live = [e for e in range(w.n_cand) if not iv.measured[0, w.cand[e]]]
+    sel = np.array(live[:2] if S < (1 << 20) else live[1:2])
+    rng = np.random.default_rng(S)
+    lo_c, hi_c = iv.cap_lo[0, w.cand[sel]], iv.cap_hi[0, w.cand[sel]]
+    lo_t, hi_t = iv.tail_lo[0, w.cand[sel]], iv.tail_hi[0, w.cand[sel]]
+    steps = np.rint((hi_c - lo_c) * 64).astype(np.int64)
+    n = len(sel)
+    cs = ((np.rint(lo_c * 64)[:, None] + rng.integers(0, steps[:, None] + 1, size=(n, S))) / 64).astype(np.float32)
+    ts = (lo_t[:, None] + rng.random((n, S)) * (hi_t - lo_t)[:, None]).astype(np.float32)
+    cs, ts = cs[None], ts[None]
+    o = orc.score(p, iv, w.cand[sel], cs, ts, dump=False, n_threads=2)
+    for kernel in (2, 3):
+        note(f"many partials S={S} kernel {kernel}")
+        score, gap, best, _ = gpu_score(env, p, iv, w.cand[sel], cs, ts, kernel, dump=False)
+        np.testing.assert_array_equal(score, o.score)
+        np.testing.assert_array_equal(gap, o.gap_now)
+        np.testing.assert_array_equal(best, o.best)
