@@ -163,8 +163,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="wall budget of the oracle baseline")
     ap.add_argument("--spl", type=int, default=0,
                     help="exclusion scorer samples per lane (4, 8, 16; 0 = library default)")
-    ap.add_argument("--wpb", type=int, default=0,
-                    help="exclusion scorer wavefronts per block (1, 4; 0 = library default)")
+    ap.add_argument("--cpw", type=int, default=0,
+                    help="exclusion scorer sample chunks per wavefront (1, 2, 4, 8; 0 = library default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-full-resolve", action="store_true",
                     help="skip the second measurement with the full re-solve kernel")
@@ -204,7 +204,7 @@ def main():
     ctx = fs.Context(0)
     ctx.set_option(fs.OPT_KERNEL_TIMING, 1)
     ctx.set_option(fs.OPT_SAMPLES_PER_LANE, args.spl)
-    ctx.set_option(fs.OPT_WAVES_PER_BLOCK, args.wpb)
+    ctx.set_option(fs.OPT_CHUNKS_PER_WAVE, args.cpw)
     out = fs.ScoreOutput(torch.empty((O, E), dtype=torch.float64, device=dev),
                          torch.empty(O, dtype=torch.float64, device=dev),
                          torch.empty(O, dtype=torch.int32, device=dev), None)

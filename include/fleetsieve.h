@@ -127,9 +127,10 @@ typedef enum fs_option {
    * (0 = library default).  A launch-shape tuning knob; results are
    * identical for every value. */
   FS_OPT_SAMPLES_PER_LANE = 3,
-  /* Exclusion scorer: wavefronts per block, 1 or 4 (0 = library default).
-   * A launch-shape tuning knob; results are identical for every value. */
-  FS_OPT_WAVES_PER_BLOCK = 4
+  /* Exclusion scorer: consecutive sample chunks each wavefront evaluates,
+   * 1, 2, 4 or 8 (0 = library default).  A launch-shape tuning knob;
+   * results are identical for every value. */
+  FS_OPT_CHUNKS_PER_WAVE = 4
 } fs_option;
 
 /* Creates a context bound to HIP device `hip_device`.  One context per host

@@ -18,7 +18,7 @@ struct fs_context {
   int score_kernel;  // 0 auto, 1 wave per scenario, 2 lane per scenario, 3 exclusion
   int timing;        // record events around the scoring kernel
   int spl;           // exclusion scorer samples per lane (0 = default)
-  int wpb;           // exclusion scorer wavefronts per block (0 = default)
+  int cpw;           // exclusion scorer sample chunks per wavefront (0 = default)
   std::vector<std::pair<hipEvent_t, hipEvent_t>> events;
 };
 
@@ -184,10 +184,10 @@ fs_status fs_context_set_option(fs_context *ctx, fs_option option, int64_t value
     ctx->spl = (int)value;
     return FS_OK;
   }
-  if (option == FS_OPT_WAVES_PER_BLOCK) {
-    if (value != 0 && value != 1 && value != 4)
-      return fail(FS_ERR_INVALID_ARGUMENT, "waves per block must be 0, 1 or 4");
-    ctx->wpb = (int)value;
+  if (option == FS_OPT_CHUNKS_PER_WAVE) {
+    if (value != 0 && value != 1 && value != 2 && value != 4 && value != 8)
+      return fail(FS_ERR_INVALID_ARGUMENT, "chunks per wavefront must be 0, 1, 2, 4 or 8");
+    ctx->cpw = (int)value;
     return FS_OK;
   }
   if (option == FS_OPT_KERNEL_TIMING) {
@@ -302,7 +302,7 @@ fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals
   }
   fs::ScoreArgs a{iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi, iv.measured, d_cand, d_cap_s, d_tail_s,
                   n_orders, n_cand, S, d_score, d_gap_now, d_best, d_tau_dump, ws, L, kernel,
-                  ctx->spl, ctx->wpb, nullptr, nullptr};
+                  ctx->spl, ctx->cpw, nullptr, nullptr};
   if (ctx->timing && n_cand > 0) {
     e = hipEventCreate(&a.ev_begin);
     if (e == hipSuccess) e = hipEventCreate(&a.ev_end);

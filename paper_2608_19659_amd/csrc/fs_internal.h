@@ -92,7 +92,7 @@ struct ScoreArgs {
   WsLayout L;
   int kernel;  // 1 = wave per scenario, 2 = lane per scenario, 3 = exclusion
   int spl;     // exclusion scorer: samples per lane (4, 8 or 16; 0 = default)
-  int wpb;     // exclusion scorer: wavefronts per block (1 or 4; 0 = default)
+  int cpw;     // exclusion scorer: sample chunks per wavefront (1, 2, 4, 8; 0 = default)
   hipEvent_t ev_begin, ev_end;  // recorded around the scoring kernel if set
 };
 

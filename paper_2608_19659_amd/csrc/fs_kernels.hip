@@ -841,85 +841,171 @@ __global__ __launch_bounds__(1024) void k_prep(DevProblem P, const float *__rest
   }
 }
 
-// Scenarios of the exclusion scorer: block (chunk, e, o) holds 64*WPB lanes x
-// SPL consecutive samples; lane l owns samples [chunk*CHUNK + l*SPL, +SPL).
-template <int SPL, int WPB>
-__global__ __launch_bounds__(64 * WPB) void k_score_excl(DevProblem P, const TileInfo *__restrict__ tiles,
-                                                    const int32_t *__restrict__ tabH,
-                                                    const float *__restrict__ cap_s,
-                                                    const float *__restrict__ tail_s, int32_t E,
-                                                    int32_t S, const int32_t *__restrict__ base,
-                                                    double *__restrict__ partial, int64_t n_partial,
-                                                    float *__restrict__ tau_dump) {
-  constexpr int CHUNK = 64 * WPB * SPL;
-  extern __shared__ int Mlds[];
-  __shared__ double wsum[WPB];
-  const int chunk = blockIdx.x, e = blockIdx.y, o = blockIdx.z;
-  const size_t tile = (size_t)o * E + e;
-  const TileInfo tl = tiles[tile];
-  const int s_first = chunk * CHUNK + threadIdx.x * SPL;
-  const size_t sbase = tile * S + s_first;
-  double block_sum = 0.0;
-  if (tl.state == 1 && tau_dump) {
+// Sampled ratio of r replicas: min(1, fl32(fl32(r * c) / lambda)) as bits.
+__device__ __forceinline__ int sampled_ratio(float rf, float cs, double rcp) {
+  const float capacity = rf * cs;
+  return __float_as_int(fminf((float)((double)capacity * rcp), 1.0f));
+}
+
+// Largest replica range handled by the unrolled scan; longer ranges use the
+// crossing search.
+constexpr int kScanMax = 16;
+
+// Scenarios of the exclusion scorer.  One wavefront handles CPW consecutive
+// chunks of 64 x SPL samples of one (order, candidate) tile; lane l owns
+// samples [chunk*64*SPL + l*SPL, +SPL) of each chunk, and the next chunk's
+// samples are loaded while the current one is evaluated.  Each chunk's sum
+// is written as one partial (a node of the pairwise tree over s).
+//
+// Per realisation, tau = max(U, max_r min(f_r, M_r)) with M_r = H[G - t*r].
+// Short replica ranges are scanned.  For long ones: f_r is nondecreasing in r
+// and M_r nonincreasing, so min(f_r, M_r) rises while f_r < M_r and falls
+// after; with r* the first r where f_r >= M_r, the maximum is
+// max(f_{r*-1}, M_{r*}), and r* is found by bisection.
+template <int SPL>
+__device__ __forceinline__ void load_samples(const float *__restrict__ cap_s, const float *__restrict__ tail_s,
+                                             size_t sbase, int s_first, int S, bool need, float (&cs)[SPL],
+                                             float (&ls)[SPL]) {
+  if (need && s_first + SPL <= S && ((sbase & 3) == 0)) {
+#pragma unroll
+    for (int v4 = 0; v4 < SPL / 4; ++v4) {
+      const float4 c4 = *reinterpret_cast<const float4 *>(cap_s + sbase + 4 * v4);
+      const float4 l4 = *reinterpret_cast<const float4 *>(tail_s + sbase + 4 * v4);
+      cs[4 * v4 + 0] = c4.x; cs[4 * v4 + 1] = c4.y; cs[4 * v4 + 2] = c4.z; cs[4 * v4 + 3] = c4.w;
+      ls[4 * v4 + 0] = l4.x; ls[4 * v4 + 1] = l4.y; ls[4 * v4 + 2] = l4.z; ls[4 * v4 + 3] = l4.w;
+    }
+  } else {
+#pragma unroll
     for (int q = 0; q < SPL; ++q) {
-      if (s_first + q < S) {
-        tau_dump[(sbase + q) * 2 + 0] = __int_as_float(base[o * 2 + 0]);
-        tau_dump[(sbase + q) * 2 + 1] = __int_as_float(base[o * 2 + 1]);
-      }
+      const bool live = need && s_first + q < S;
+      cs[q] = live ? cap_s[sbase + q] : 0.0f;
+      ls[q] = live ? tail_s[sbase + q] : 0.0f;
     }
   }
-  if (tl.state == 0) {
-    const int G = P.G, W = G + 1;
-    const int nr = tl.rhi >= tl.rlo ? tl.rhi - tl.rlo + 1 : 0;
-    const int nr4 = (nr + 3) & ~3;
-    float cs[SPL], ls[SPL];
-    // with no replica count on the cell the samples cannot matter
-    const bool need = nr > 0 || tau_dump;
-    if (need && s_first + SPL <= S && ((sbase & 3) == 0)) {
-#pragma unroll
-      for (int v4 = 0; v4 < SPL / 4; ++v4) {
-        const float4 c4 = *reinterpret_cast<const float4 *>(cap_s + sbase + 4 * v4);
-        const float4 l4 = *reinterpret_cast<const float4 *>(tail_s + sbase + 4 * v4);
-        cs[4 * v4 + 0] = c4.x; cs[4 * v4 + 1] = c4.y; cs[4 * v4 + 2] = c4.z; cs[4 * v4 + 3] = c4.w;
-        ls[4 * v4 + 0] = l4.x; ls[4 * v4 + 1] = l4.y; ls[4 * v4 + 2] = l4.z; ls[4 * v4 + 3] = l4.w;
-      }
-    } else {
-#pragma unroll
-      for (int q = 0; q < SPL; ++q) {
-        const bool live = need && s_first + q < S;
-        cs[q] = live ? cap_s[sbase + q] : 0.0f;
-        ls[q] = live ? tail_s[sbase + q] : 0.0f;
-      }
-    }
-    int *Mm = Mlds, *Mp = Mlds + nr4;
-    const int32_t *Hm = tabH + (((size_t)o * 2 + 0) * P.K + tl.cls) * W;
-    const int32_t *Hp = tabH + (((size_t)o * 2 + 1) * P.K + tl.cls) * W;
-    for (int j = threadIdx.x; j < nr4; j += blockDim.x) {
-      const int r = tl.rlo + j;
-      // padding entries are 0: min(f, 0) <= 0 <= U never raises the maximum
-      Mm[j] = j < nr ? Hm[G - tl.t * r] : 0;
-      Mp[j] = j < nr ? Hp[G - tl.t * r] : 0;
-    }
-    __syncthreads();
-    const double rcp = P.rcp_demand[tl.cls];
-    int am[SPL], ap[SPL];
-#pragma unroll
-    for (int q = 0; q < SPL; ++q) { am[q] = tl.u_m; ap[q] = tl.u_p; }
-    for (int j = 0; j < nr4; j += 4) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const float rf = (float)(tl.rlo + j + u);
-        const int mm = Mm[j + u], mp = Mp[j + u];
-#pragma unroll
+}
+
+template <int SPL, int CPW>
+__global__ __launch_bounds__(64) void k_score_excl(DevProblem P, const TileInfo *__restrict__ tiles,
+                                                   const int32_t *__restrict__ tabH,
+                                                   const float *__restrict__ cap_s,
+                                                   const float *__restrict__ tail_s, int32_t E,
+                                                   int32_t S, const int32_t *__restrict__ base,
+                                                   double *__restrict__ partial, int64_t n_partial,
+                                                   float *__restrict__ tau_dump) {
+  constexpr int CHUNK = 64 * SPL;
+  extern __shared__ int Mlds[];
+  const int e = blockIdx.y, o = blockIdx.z;
+  const int lane = threadIdx.x;
+  const size_t tile = (size_t)o * E + e;
+  const TileInfo tl = tiles[tile];
+  const int c0 = blockIdx.x * CPW;
+  if (tl.state == 1) {
+    if (tau_dump) {
+      for (int c = c0; c < c0 + CPW && c < n_partial; ++c) {
+        const int s_first = c * CHUNK + lane * SPL;
         for (int q = 0; q < SPL; ++q) {
-          const float capacity = rf * cs[q];
-          const int fb = __float_as_int(fminf((float)((double)capacity * rcp), 1.0f));
-          am[q] = max(am[q], min(fb, mm));
-          ap[q] = max(ap[q], min(fb, mp));
+          if (s_first + q < S) {
+            tau_dump[(tile * S + s_first + q) * 2 + 0] = __int_as_float(base[o * 2 + 0]);
+            tau_dump[(tile * S + s_first + q) * 2 + 1] = __int_as_float(base[o * 2 + 1]);
+          }
         }
       }
     }
-    const float slo = P.slo[tl.cls];
+    return;
+  }
+  if (tl.state != 0) return;
+  const int G = P.G, W = G + 1;
+  const int nr = tl.rhi >= tl.rlo ? tl.rhi - tl.rlo + 1 : 0;
+  // with no replica count on the cell the samples cannot matter
+  const bool need = nr > 0 || tau_dump;
+  const int32_t *Hm = tabH + (((size_t)o * 2 + 0) * P.K + tl.cls) * W + G;
+  const int32_t *Hp = tabH + (((size_t)o * 2 + 1) * P.K + tl.cls) * W + G;
+  const double rcp = P.rcp_demand[tl.cls];
+  const float slo = P.slo[tl.cls];
+  const bool scan = nr <= kScanMax;
+  int mm[kScanMax], mp[kScanMax];
+  int steps = 0;
+  if (scan) {
+#pragma unroll
+    for (int j = 0; j < kScanMax; ++j) {
+      const int r = tl.rlo + j;
+      mm[j] = j < nr ? Hm[-tl.t * r] : 0;
+      mp[j] = j < nr ? Hp[-tl.t * r] : 0;
+    }
+  } else {
+    for (int j = lane; j < nr; j += kWave) {
+      Mlds[j] = Hm[-tl.t * (tl.rlo + j)];
+      Mlds[nr + j] = Hp[-tl.t * (tl.rlo + j)];
+    }
+    __syncthreads();
+    while ((1 << steps) <= nr) ++steps;  // ceil(log2(nr + 1))
+  }
+  float cs[SPL], ls[SPL], ncs[SPL], nls[SPL];
+  {
+    const int s_first = c0 * CHUNK + lane * SPL;
+    load_samples<SPL>(cap_s, tail_s, tile * S + s_first, s_first, S, need && c0 < n_partial, cs, ls);
+  }
+#pragma unroll
+  for (int i = 0; i < CPW; ++i) {
+    const int c = c0 + i;
+    if (c >= n_partial) break;  // uniform
+    if (i + 1 < CPW) {
+      const int s_next = (c + 1) * CHUNK + lane * SPL;
+      load_samples<SPL>(cap_s, tail_s, tile * S + s_next, s_next, S, need && c + 1 < n_partial, ncs, nls);
+    }
+    const int s_first = c * CHUNK + lane * SPL;
+    int am[SPL], ap[SPL];
+#pragma unroll
+    for (int q = 0; q < SPL; ++q) { am[q] = tl.u_m; ap[q] = tl.u_p; }
+    if (scan) {
+#pragma unroll
+      for (int j = 0; j < kScanMax; j += 2) {
+        if (j < nr) {
+          const float r1 = (float)(tl.rlo + j), r2 = (float)(tl.rlo + j + 1);
+          const bool two = j + 1 < nr;
+#pragma unroll
+          for (int q = 0; q < SPL; ++q) {
+            const int f1 = sampled_ratio(r1, cs[q], rcp);
+            const int f2 = two ? sampled_ratio(r2, cs[q], rcp) : INT_MIN;
+            am[q] = max(am[q], max(min(f1, mm[j]), min(f2, mm[j + 1])));
+            ap[q] = max(ap[q], max(min(f1, mp[j]), min(f2, mp[j + 1])));
+          }
+        }
+      }
+    } else {
+      // all 2 x SPL searches advance together, so their LDS reads overlap
+      int lo[SPL][2], hi[SPL][2];
+#pragma unroll
+      for (int q = 0; q < SPL; ++q) {
+        lo[q][0] = lo[q][1] = 0;
+        hi[q][0] = hi[q][1] = nr;  // first j in [0, nr] with f >= M (nr: none)
+      }
+      for (int it = 0; it < steps; ++it) {
+#pragma unroll
+        for (int q = 0; q < SPL; ++q) {
+#pragma unroll
+          for (int side = 0; side < 2; ++side) {
+            const bool act = lo[q][side] < hi[q][side];
+            const int mid = min((lo[q][side] + hi[q][side]) >> 1, nr - 1);
+            const int f = sampled_ratio((float)(tl.rlo + mid), cs[q], rcp);
+            const bool take = act && f >= Mlds[side * nr + mid];
+            hi[q][side] = take ? mid : hi[q][side];
+            lo[q][side] = (act && !take) ? mid + 1 : lo[q][side];
+          }
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < SPL; ++q) {
+#pragma unroll
+        for (int side = 0; side < 2; ++side) {
+          const int j = lo[q][side];
+          int v = j > 0 ? sampled_ratio((float)(tl.rlo + j - 1), cs[q], rcp) : INT_MIN;
+          if (j < nr) v = max(v, Mlds[side * nr + j]);
+          if (side == 0) am[q] = max(am[q], v);
+          else ap[q] = max(ap[q], v);
+        }
+      }
+    }
     double gq[SPL];
 #pragma unroll
     for (int q = 0; q < SPL; ++q) {
@@ -930,8 +1016,8 @@ __global__ __launch_bounds__(64 * WPB) void k_score_excl(DevProblem P, const Til
       const bool live = s_first + q < S;
       gq[q] = live ? (double)__int_as_float(tp) - (double)__int_as_float(tm) : 0.0;
       if (tau_dump && live) {
-        tau_dump[(sbase + q) * 2 + 0] = __int_as_float(tm);
-        tau_dump[(sbase + q) * 2 + 1] = __int_as_float(tp);
+        tau_dump[(tile * S + s_first + q) * 2 + 0] = __int_as_float(tm);
+        tau_dump[(tile * S + s_first + q) * 2 + 1] = __int_as_float(tp);
       }
     }
     // pairwise tree: within the lane's SPL consecutive samples, then lanes
@@ -940,17 +1026,15 @@ __global__ __launch_bounds__(64 * WPB) void k_score_excl(DevProblem P, const Til
 #pragma unroll
       for (int j = 0; j + w < SPL; j += 2 * w) gq[j] = gq[j] + gq[j + w];
     }
-    double v = wave_pairwise_sum(gq[0]);
-    if (WPB == 1) {
-      block_sum = v;
-    } else {
-      if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = v;
-      __syncthreads();
-      block_sum = (wsum[0] + wsum[1 % WPB]) + (wsum[2 % WPB] + wsum[3 % WPB]);
+    const double v = wave_pairwise_sum(gq[0]);
+    if (lane == 0) partial[tile * n_partial + c] = v;
+    if (i + 1 < CPW) {
+#pragma unroll
+      for (int q = 0; q < SPL; ++q) { cs[q] = ncs[q]; ls[q] = nls[q]; }
     }
   }
-  if (tl.state == 0 && threadIdx.x == 0) partial[tile * n_partial + chunk] = block_sum;
 }
+
 // Scores and best candidate of the exclusion scorer: one block per order,
 // one thread per candidate.  Each tile's partials (at most 16 here) are
 // summed by the pairwise tree in registers.
@@ -1278,25 +1362,26 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
       return hipGetLastError();
     }
     const int spl = a.spl == 8 || a.spl == 16 ? a.spl : kSpl;
-    const int wpb = a.wpb == 4 ? 4 : 1;
-    const int64_t chunk = 64 * wpb * spl;
+    const int cpw = a.cpw == 2 ? 2 : (a.cpw == 4 ? 4 : (a.cpw == 8 ? 8 : 1));
+    const int64_t chunk = 64 * spl;
     const int64_t n_partial = (a.S + chunk - 1) / chunk;
-    const int max_nr4 = ((P.G / P.tp[0]) + 3) & ~3;
-    const size_t mlds = 2 * (size_t)max_nr4 * sizeof(int);
-    const dim3 grid((unsigned)n_partial, a.E, a.O);
+    const size_t mlds = 2 * (size_t)(P.G / P.tp[0] + 1) * sizeof(int);
+    const dim3 grid((unsigned)((n_partial + cpw - 1) / cpw), a.E, a.O);
     if (a.ev_begin) (void)hipEventRecord(a.ev_begin, s);
-#define FS_EXCL_LAUNCH(SP, WB)                                                                       \
-  k_score_excl<SP, WB><<<grid, 64 * WB, mlds, s>>>(P, tiles, tabH, a.cap_s, a.tail_s, a.E, a.S, base, \
-                                                   partial, n_partial, a.tau_dump)
-    if (wpb == 1) {
-      if (spl == 16) FS_EXCL_LAUNCH(16, 1);
-      else if (spl == 8) FS_EXCL_LAUNCH(8, 1);
-      else FS_EXCL_LAUNCH(4, 1);
-    } else {
-      if (spl == 16) FS_EXCL_LAUNCH(16, 4);
-      else if (spl == 8) FS_EXCL_LAUNCH(8, 4);
-      else FS_EXCL_LAUNCH(4, 4);
-    }
+#define FS_EXCL_LAUNCH(SP, CP)                                                                       \
+  k_score_excl<SP, CP><<<grid, 64, mlds, s>>>(P, tiles, tabH, a.cap_s, a.tail_s, a.E, a.S, base,     \
+                                              partial, n_partial, a.tau_dump)
+#define FS_EXCL_SPL(SP)                   \
+  switch (cpw) {                          \
+    case 4: FS_EXCL_LAUNCH(SP, 4); break; \
+    case 2: FS_EXCL_LAUNCH(SP, 2); break; \
+    case 8: FS_EXCL_LAUNCH(SP, 8); break; \
+    default: FS_EXCL_LAUNCH(SP, 1); break; \
+  }
+    if (spl == 16) { FS_EXCL_SPL(16) }
+    else if (spl == 8) { FS_EXCL_SPL(8) }
+    else { FS_EXCL_SPL(4) }
+#undef FS_EXCL_SPL
 #undef FS_EXCL_LAUNCH
     if (a.ev_end) (void)hipEventRecord(a.ev_end, s);
     if (n_partial <= 16) {
