@@ -52,6 +52,8 @@ struct TileInfo {
   int32_t u_m, u_p;          // U of the conservative / optimistic realisation (bits)
   int32_t state;             // 0 = solve, 1 = measured, -1 = invalid candidate
   int32_t cell;              // candidate cell index
+  int32_t toff;              // offset of the cell's capacity thresholds
+  int32_t pad[3];
 };
 
 // Workspace layout; every region is 256-byte aligned.
@@ -64,6 +66,8 @@ struct WsLayout {
   size_t tiles;      // TileInfo [O][E]                       exclusion scorer
   size_t tabH;       // int32 [O][2][K][G+1] all classes but one
   size_t tabB;       // int32 [O][2][4][K][G+1] set-up tables when LDS is too small
+  size_t thr;        // float [O][2][K*P] capacity thresholds of every cell's replica range
+  size_t perm;       // int32 [E] launch order of the candidates (longest range first)
   size_t flag;     // int32 [4]        validation / error flags
   size_t total;
   int64_t n_partial;  // ceil(S / 64)

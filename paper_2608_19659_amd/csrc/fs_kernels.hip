@@ -673,9 +673,12 @@ __global__ __launch_bounds__(1024) void k_prep(DevProblem P, const float *__rest
                                               const uint8_t *__restrict__ measured,
                                               const int32_t *__restrict__ cand, int32_t E,
                                               int32_t *__restrict__ tabH, int32_t *__restrict__ gtab,
-                                              TileInfo *__restrict__ tiles, int32_t *__restrict__ base) {
+                                              TileInfo *__restrict__ tiles, int32_t *__restrict__ base,
+                                              float *__restrict__ thr, int32_t n_thr,
+                                              int32_t *__restrict__ perm) {
   extern __shared__ int lds[];
   __shared__ int cls_best[kMaxClasses], cls_arg[kMaxClasses], cls_second[kMaxClasses];
+  __shared__ int bucket_count[32], bucket_start[32];
   const int R = blockIdx.x, o = blockIdx.y, tid = threadIdx.x, nth = blockDim.x;
   const int G = P.G, K = P.K, W = G + 1, N = P.N;
   const int KW = K * W;
@@ -683,7 +686,8 @@ __global__ __launch_bounds__(1024) void k_prep(DevProblem P, const float *__rest
   float *ctail = ccap + N;                   // [N]
   int *mc = (int *)(ctail + N);              // [N] best w over the cell's options
   int *rlo = mc + N, *rhi = rlo + N;         // [N] replica range using the cell
-  int8_t *lvl = (int8_t *)(rhi + N);         // [K][W]
+  int *toff = rhi + N;                       // [N] offset of the cell's thresholds
+  int8_t *lvl = (int8_t *)(toff + N);        // [K][W]
   int *tabs = kLds ? (int *)(lvl + ((KW + 15) & ~15)) : gtab + ((size_t)o * 2 + R) * 4 * KW;
   int *Bt = tabs, *Pt = tabs + KW, *St = tabs + 2 * KW, *Ht = tabs + 3 * KW;
   const size_t off = (size_t)o * N;
@@ -734,6 +738,22 @@ __global__ __launch_bounds__(1024) void k_prep(DevProblem P, const float *__rest
       carry = __shfl(v, kWave - 1, kWave);
     }
   }
+  // exclusive prefix sum of the replica-range lengths (wavefront 0)
+  if (wave == 0) {
+    int carry = 0;
+    for (int b0 = 0; b0 < N; b0 += kWave) {
+      const int c = b0 + lane;
+      const int len = (c < N && rhi[c] >= 0) ? rhi[c] - rlo[c] + 1 : 0;
+      int v = len;
+#pragma unroll
+      for (int d = 1; d < kWave; d <<= 1) {
+        const int u = __shfl_up(v, d, kWave);
+        if (lane >= d) v += u;
+      }
+      if (c < N) toff[c] = carry + v - len;
+      carry += __shfl(v, kWave - 1, kWave);
+    }
+  }
   __syncthreads();
   if (K == 1) {
     for (int g = tid; g < W; g += nth) Ht[g] = INT_MAX;  // the empty convolution
@@ -778,6 +798,46 @@ __global__ __launch_bounds__(1024) void k_prep(DevProblem P, const float *__rest
   __syncthreads();
   int32_t *Hg = tabH + ((size_t)o * 2 + R) * KW;
   for (int idx = tid; idx < KW; idx += nth) Hg[idx] = Ht[idx];
+  // Capacity thresholds: for cell c and replica count r in its range, the
+  // smallest binary32 capacity whose ratio reaches M = H_k[G - t*r].  The
+  // ratio is nondecreasing in the capacity and nonnegative binary32 values
+  // order like their bit patterns, so bisection over bit patterns finds it;
+  // a sampled capacity x then has f_r(x) >= M exactly when x >= threshold.
+  // NaN marks "never" (M above 1).
+  {
+    float *T = thr + ((size_t)o * 2 + R) * n_thr;
+    const int total = toff[N - 1] + (rhi[N - 1] >= 0 ? rhi[N - 1] - rlo[N - 1] + 1 : 0);
+    for (int it = tid; it < total; it += nth) {
+      int lo = 0, hi = N - 1;  // the cell whose offset block holds `it`
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (toff[mid] <= it) lo = mid;
+        else hi = mid - 1;
+      }
+      const int c = lo;
+      const int k = c / (P.NT * P.B), ti = (c / P.B) % P.NT;
+      const int r = rlo[c] + (it - toff[c]);
+      const int M = Ht[k * W + G - P.tp[ti] * r];
+      float th;
+      if (M <= 0) {
+        th = 0.0f;
+      } else if (M > __float_as_int(1.0f)) {
+        th = __builtin_nanf("");
+      } else {
+        unsigned blo = 0, bhi = 0x7F800000u;  // +inf reaches ratio 1 >= M
+        const float rf = (float)r;
+        while (blo < bhi) {
+          const unsigned mid = blo + ((bhi - blo) >> 1);
+          const float capacity = rf * __uint_as_float(mid);
+          const int f = __float_as_int(fminf((float)((double)capacity * P.rcp_demand[k]), 1.0f));
+          if (f >= M) bhi = mid;
+          else blo = mid + 1;
+        }
+        th = __uint_as_float(blo);
+      }
+      T[it] = th;
+    }
+  }
   // w_o per option, folded into its cell's maximum
   for (int q = tid; q < K * PPc; q += nth) {
     const int k = q / PPc;
@@ -813,6 +873,32 @@ __global__ __launch_bounds__(1024) void k_prep(DevProblem P, const float *__rest
   }
   __syncthreads();
   if (tid == 0) base[o * 2 + R] = max(0, cls_best[0]);  // 0: the empty allocation
+  // Launch order of the candidates for the scoring kernel: longest replica
+  // range first (bucketed by its bit length), so the heaviest wavefronts start
+  // first.  Any order gives the same results.
+  if (R == 0 && o == 0) {
+    if (tid < 32) bucket_count[tid] = 0;
+    __syncthreads();
+    for (int e = tid; e < E; e += nth) {
+      const int cell = cand[e];
+      const int len = (cell >= 0 && cell < N && rhi[cell] >= 0) ? rhi[cell] - rlo[cell] + 1 : 0;
+      atomicAdd(&bucket_count[31 - min(31, 32 - __clz(len))], 1);
+    }
+    __syncthreads();
+    if (tid == 0) {
+      int at = 0;
+      for (int bkt = 0; bkt < 32; ++bkt) {
+        bucket_start[bkt] = at;
+        at += bucket_count[bkt];
+      }
+    }
+    __syncthreads();
+    for (int e = tid; e < E; e += nth) {
+      const int cell = cand[e];
+      const int len = (cell >= 0 && cell < N && rhi[cell] >= 0) ? rhi[cell] - rlo[cell] + 1 : 0;
+      perm[atomicAdd(&bucket_start[31 - min(31, 32 - __clz(len))], 1)] = e;
+    }
+  }
   // tile records
   for (int e = tid; e < E; e += nth) {
     TileInfo *tl = tiles + (size_t)o * E + e;
@@ -834,6 +920,7 @@ __global__ __launch_bounds__(1024) void k_prep(DevProblem P, const float *__rest
       tl->rhi = rhi[cell];
       if (rhi[cell] < 0) tl->rhi = 0;
       tl->state = measured[off + cell] ? 1 : 0;
+      tl->toff = toff[cell];
       tl->u_m = u;
     } else {
       tl->u_p = u;
@@ -849,7 +936,7 @@ __device__ __forceinline__ int sampled_ratio(float rf, float cs, double rcp) {
 
 // Largest replica range handled by the unrolled scan; longer ranges use the
 // crossing search.
-constexpr int kScanMax = 16;
+constexpr int kScanMax = 8;
 
 // Scenarios of the exclusion scorer.  One wavefront handles CPW consecutive
 // chunks of 64 x SPL samples of one (order, candidate) tile; lane l owns
@@ -891,10 +978,11 @@ __global__ __launch_bounds__(64) void k_score_excl(DevProblem P, const TileInfo 
                                                    const float *__restrict__ tail_s, int32_t E,
                                                    int32_t S, const int32_t *__restrict__ base,
                                                    double *__restrict__ partial, int64_t n_partial,
-                                                   float *__restrict__ tau_dump) {
+                                                   float *__restrict__ tau_dump, const float *__restrict__ thr,
+                                                   int32_t n_thr, const int32_t *__restrict__ perm) {
   constexpr int CHUNK = 64 * SPL;
   extern __shared__ int Mlds[];
-  const int e = blockIdx.y, o = blockIdx.z;
+  const int o = blockIdx.y, e = perm[blockIdx.z];
   const int lane = threadIdx.x;
   const size_t tile = (size_t)o * E + e;
   const TileInfo tl = tiles[tile];
@@ -933,9 +1021,14 @@ __global__ __launch_bounds__(64) void k_score_excl(DevProblem P, const TileInfo 
       mp[j] = j < nr ? Hp[-tl.t * r] : 0;
     }
   } else {
+    const float *Tm = thr + ((size_t)o * 2 + 0) * n_thr + tl.toff;
+    const float *Tp = thr + ((size_t)o * 2 + 1) * n_thr + tl.toff;
+    float *Tl = (float *)(Mlds + 2 * nr);
     for (int j = lane; j < nr; j += kWave) {
       Mlds[j] = Hm[-tl.t * (tl.rlo + j)];
       Mlds[nr + j] = Hp[-tl.t * (tl.rlo + j)];
+      Tl[j] = Tm[j];
+      Tl[nr + j] = Tp[j];
     }
     __syncthreads();
     while ((1 << steps) <= nr) ++steps;  // ceil(log2(nr + 1))
@@ -973,7 +1066,9 @@ __global__ __launch_bounds__(64) void k_score_excl(DevProblem P, const TileInfo 
         }
       }
     } else {
-      // all 2 x SPL searches advance together, so their LDS reads overlap
+      // all 2 x SPL searches advance together, so their LDS reads overlap;
+      // the crossing is the first j whose threshold the sample reaches
+      const float *Tl = (const float *)(Mlds + 2 * nr);
       int lo[SPL][2], hi[SPL][2];
 #pragma unroll
       for (int q = 0; q < SPL; ++q) {
@@ -987,8 +1082,7 @@ __global__ __launch_bounds__(64) void k_score_excl(DevProblem P, const TileInfo 
           for (int side = 0; side < 2; ++side) {
             const bool act = lo[q][side] < hi[q][side];
             const int mid = min((lo[q][side] + hi[q][side]) >> 1, nr - 1);
-            const int f = sampled_ratio((float)(tl.rlo + mid), cs[q], rcp);
-            const bool take = act && f >= Mlds[side * nr + mid];
+            const bool take = act && cs[q] >= Tl[side * nr + mid];
             hi[q][side] = take ? mid : hi[q][side];
             lo[q][side] = (act && !take) ? mid + 1 : lo[q][side];
           }
@@ -1299,7 +1393,15 @@ constexpr int kPrepThreads = 1024;
 // maxima, replica ranges, and the level map.
 static size_t prep_lds_small(const DevProblem &P) {
   const size_t KW = (size_t)P.K * (P.G + 1);
-  return 5 * sizeof(int) * (size_t)P.N + ((KW + 15) & ~(size_t)15);
+  return 6 * sizeof(int) * (size_t)P.N + ((KW + 15) & ~(size_t)15);
+}
+
+// Upper bound of the threshold entries per (order, realisation): one per
+// (class, option).
+static int32_t excl_thresholds(const DevProblem &P) {
+  int per_class = 0;
+  for (int t = 0; t < P.NT; ++t) per_class += P.G / P.tp[t];
+  return P.K * per_class;
 }
 
 WsLayout ws_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
@@ -1320,6 +1422,8 @@ WsLayout ws_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
   const size_t W = (size_t)P.G + 1, KW = (size_t)P.K * W;
   const bool in_lds = prep_lds_small(P) + 4 * KW * sizeof(int) <= kPrepLdsLimit;
   L.tabB = at; at = align256(at + (excl_kernel_supported(P) && !in_lds ? 4 * tab : 0));
+  L.thr = at; at = align256(at + (excl_kernel_supported(P) ? sizeof(float) * (size_t)O * 2 * excl_thresholds(P) : 0));
+  L.perm = at; at = align256(at + sizeof(int32_t) * (size_t)(E > 0 ? E : 1));
   L.total = at;
   return L;
 }
@@ -1349,28 +1453,31 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
     int32_t *tabH = (int32_t *)(a.ws + a.L.tabH);
     const size_t small = prep_lds_small(P);
     const size_t big = small + 4 * (size_t)KW * sizeof(int);
+    float *thr = (float *)(a.ws + a.L.thr);
+    const int32_t n_thr = excl_thresholds(P);
+    int32_t *perm = (int32_t *)(a.ws + a.L.perm);
     if (big <= kPrepLdsLimit)
       k_prep<true><<<dim3(2, a.O), kPrepThreads, big, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured,
-                                                  a.cand, a.E, tabH, nullptr, tiles, base);
+                                                  a.cand, a.E, tabH, nullptr, tiles, base, thr, n_thr, perm);
     else
       k_prep<false><<<dim3(2, a.O), kPrepThreads, small, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
                                                      a.measured, a.cand, a.E, tabH,
-                                                     (int32_t *)(a.ws + a.L.tabB), tiles, base);
+                                                     (int32_t *)(a.ws + a.L.tabB), tiles, base, thr, n_thr, perm);
     if (a.E == 0) {
       k_finalize<<<a.O, 64, 0, s>>>(P, info, a.measured, 0, a.S, base, partial, 1, a.score, a.gap_now,
                                     a.best);
       return hipGetLastError();
     }
     const int spl = a.spl == 8 || a.spl == 16 ? a.spl : kSpl;
-    const int cpw = a.cpw == 2 ? 2 : (a.cpw == 4 ? 4 : (a.cpw == 8 ? 8 : 1));
+    const int cpw = a.cpw == 1 ? 1 : (a.cpw == 4 ? 4 : (a.cpw == 8 ? 8 : 2));
     const int64_t chunk = 64 * spl;
     const int64_t n_partial = (a.S + chunk - 1) / chunk;
-    const size_t mlds = 2 * (size_t)(P.G / P.tp[0] + 1) * sizeof(int);
-    const dim3 grid((unsigned)((n_partial + cpw - 1) / cpw), a.E, a.O);
+    const size_t mlds = 4 * (size_t)(P.G / P.tp[0] + 1) * sizeof(int);
+    const dim3 grid((unsigned)((n_partial + cpw - 1) / cpw), a.O, a.E);
     if (a.ev_begin) (void)hipEventRecord(a.ev_begin, s);
 #define FS_EXCL_LAUNCH(SP, CP)                                                                       \
   k_score_excl<SP, CP><<<grid, 64, mlds, s>>>(P, tiles, tabH, a.cap_s, a.tail_s, a.E, a.S, base,     \
-                                              partial, n_partial, a.tau_dump)
+                                              partial, n_partial, a.tau_dump, thr, n_thr, perm)
 #define FS_EXCL_SPL(SP)                   \
   switch (cpw) {                          \
     case 4: FS_EXCL_LAUNCH(SP, 4); break; \
