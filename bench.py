@@ -164,7 +164,9 @@ def main():
     ap.add_argument("--spl", type=int, default=0,
                     help="exclusion scorer samples per lane (4, 8, 16; 0 = library default)")
     ap.add_argument("--cpw", type=int, default=0,
-                    help="exclusion scorer sample chunks per wavefront (1, 2, 4, 8; 0 = library default)")
+                    help="exclusion scorer sample chunks per work item (1, 2, 4, 8; 0 = library default)")
+    ap.add_argument("--waves", type=int, default=0,
+                    help="exclusion scorer grid in wavefronts (0 = library default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-full-resolve", action="store_true",
                     help="skip the second measurement with the full re-solve kernel")
@@ -205,6 +207,7 @@ def main():
     ctx.set_option(fs.OPT_KERNEL_TIMING, 1)
     ctx.set_option(fs.OPT_SAMPLES_PER_LANE, args.spl)
     ctx.set_option(fs.OPT_CHUNKS_PER_WAVE, args.cpw)
+    ctx.set_option(fs.OPT_SCORER_WAVES, args.waves)
     out = fs.ScoreOutput(torch.empty((O, E), dtype=torch.float64, device=dev),
                          torch.empty(O, dtype=torch.float64, device=dev),
                          torch.empty(O, dtype=torch.int32, device=dev), None)

@@ -127,10 +127,14 @@ typedef enum fs_option {
    * (0 = library default).  A launch-shape tuning knob; results are
    * identical for every value. */
   FS_OPT_SAMPLES_PER_LANE = 3,
-  /* Exclusion scorer: consecutive sample chunks each wavefront evaluates,
-   * 1, 2, 4 or 8 (0 = library default).  A launch-shape tuning knob;
+  /* Exclusion scorer: consecutive sample chunks of one tile in each work
+   * item, 1, 2, 4 or 8 (0 = library default).  A launch-shape tuning knob;
    * results are identical for every value. */
-  FS_OPT_CHUNKS_PER_WAVE = 4
+  FS_OPT_CHUNKS_PER_WAVE = 4,
+  /* Exclusion scorer: wavefronts of its fixed grid, which stride over the
+   * work items, in [1, 2^20] (0 = library default).  A launch-shape tuning
+   * knob; results are identical for every value. */
+  FS_OPT_SCORER_WAVES = 5
 } fs_option;
 
 /* Creates a context bound to HIP device `hip_device`.  One context per host

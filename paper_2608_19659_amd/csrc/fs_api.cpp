@@ -18,7 +18,8 @@ struct fs_context {
   int score_kernel;  // 0 auto, 1 wave per scenario, 2 lane per scenario, 3 exclusion
   int timing;        // record events around the scoring kernel
   int spl;           // exclusion scorer samples per lane (0 = default)
-  int cpw;           // exclusion scorer sample chunks per wavefront (0 = default)
+  int cpw;           // exclusion scorer sample chunks per work item (0 = default)
+  int waves;         // exclusion scorer grid in wavefronts (0 = default)
   std::vector<std::pair<hipEvent_t, hipEvent_t>> events;
 };
 
@@ -138,7 +139,7 @@ fs_status fs_context_create(int hip_device, fs_context **out) {
   if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
   if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
     return fail(FS_ERR_UNSUPPORTED, std::string("libfleetsieve is built for gfx950, device is ") + prop.gcnArchName);
-  *out = new fs_context{hip_device, 0, 0, 0, 0, {}};
+  *out = new fs_context{hip_device, 0, 0, 0, 0, 0, {}};
   return FS_OK;
 }
 
@@ -186,8 +187,14 @@ fs_status fs_context_set_option(fs_context *ctx, fs_option option, int64_t value
   }
   if (option == FS_OPT_CHUNKS_PER_WAVE) {
     if (value != 0 && value != 1 && value != 2 && value != 4 && value != 8)
-      return fail(FS_ERR_INVALID_ARGUMENT, "chunks per wavefront must be 0, 1, 2, 4 or 8");
+      return fail(FS_ERR_INVALID_ARGUMENT, "chunks per work item must be 0, 1, 2, 4 or 8");
     ctx->cpw = (int)value;
+    return FS_OK;
+  }
+  if (option == FS_OPT_SCORER_WAVES) {
+    if (value < 0 || value > (1 << 20))
+      return fail(FS_ERR_INVALID_ARGUMENT, "scorer wavefronts must be in [0, 2^20]");
+    ctx->waves = (int)value;
     return FS_OK;
   }
   if (option == FS_OPT_KERNEL_TIMING) {
@@ -302,7 +309,7 @@ fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals
   }
   fs::ScoreArgs a{iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi, iv.measured, d_cand, d_cap_s, d_tail_s,
                   n_orders, n_cand, S, d_score, d_gap_now, d_best, d_tau_dump, ws, L, kernel,
-                  ctx->spl, ctx->cpw, nullptr, nullptr};
+                  ctx->spl, ctx->cpw, ctx->waves, nullptr, nullptr};
   if (ctx->timing && n_cand > 0) {
     e = hipEventCreate(&a.ev_begin);
     if (e == hipSuccess) e = hipEventCreate(&a.ev_end);

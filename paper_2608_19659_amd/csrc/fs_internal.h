@@ -52,7 +52,7 @@ struct TileInfo {
   int32_t u_m, u_p;          // U of the conservative / optimistic realisation (bits)
   int32_t state;             // 0 = solve, 1 = measured, -1 = invalid candidate
   int32_t cell;              // candidate cell index
-  int32_t toff;              // offset of the cell's capacity thresholds
+  int32_t toff;              // option index of (class, TP, rlo): M and thresholds of the range
   int32_t pad[3];
 };
 
@@ -64,10 +64,11 @@ struct WsLayout {
   size_t opts;     // float [O][2][K][PP][2] option (cap, tail), lane kernel only
   size_t partial;  // double [O][E][ceil(S/64)]
   size_t tiles;      // TileInfo [O][E]                       exclusion scorer
-  size_t tabH;       // int32 [O][2][K][G+1] all classes but one
-  size_t tabB;       // int32 [O][2][4][K][G+1] set-up tables when LDS is too small
-  size_t thr;        // float [O][2][K*P] capacity thresholds of every cell's replica range
-  size_t perm;       // int32 [E] launch order of the candidates (longest range first)
+  size_t tabB;       // int32 [O][2][K][3][K][G] set-up tables when LDS is too small
+  size_t mopt;       // int32 [O][2][K*P] M = H[G - t*r] of every option (class, TP, r)
+  size_t thr;        // float [O][2][K*P] capacity threshold of every option
+  size_t list;       // int4 [O][E] live tiles of each order, longest replica range first
+  size_t live;       // int32 [O] number of live tiles of each order
   size_t flag;     // int32 [4]        validation / error flags
   size_t total;
   int64_t n_partial;  // ceil(S / 64)
@@ -96,7 +97,8 @@ struct ScoreArgs {
   WsLayout L;
   int kernel;  // 1 = wave per scenario, 2 = lane per scenario, 3 = exclusion
   int spl;     // exclusion scorer: samples per lane (4, 8 or 16; 0 = default)
-  int cpw;     // exclusion scorer: sample chunks per wavefront (1, 2, 4, 8; 0 = default)
+  int cpw;     // exclusion scorer: sample chunks per work item (1, 2, 4, 8; 0 = default)
+  int waves;   // exclusion scorer: wavefronts of its grid (0 = default)
   hipEvent_t ev_begin, ev_end;  // recorded around the scoring kernel if set
 };
 

@@ -81,13 +81,31 @@ __device__ __forceinline__ int wave_scan_max(int v, int lane) {
   return v;
 }
 
-// Pairwise sum over the 64 lanes: after the step with offset 2^j every lane
-// holds the sum of its aligned block of 2^(j+1) lanes, so the association is
-// the balanced binary tree over lane order.
+// One DPP lane permutation of a binary64 value (both halves moved alike).
+template <int kCtrl>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const int lo = __builtin_amdgcn_mov_dpp(__double2loint(v), kCtrl, 0xF, 0xF, true);
+  const int hi = __builtin_amdgcn_mov_dpp(__double2hiint(v), kCtrl, 0xF, 0xF, true);
+  return __hiloint2double(hi, lo);
+}
+
+__device__ __forceinline__ double readlane_f64(double v, int l) {
+  return __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(v), l),
+                          __builtin_amdgcn_readlane(__double2loint(v), l));
+}
+
+// Pairwise sum over the 64 lanes, as the balanced binary tree over lane
+// order: after each step every lane holds the sum of its aligned block of
+// 2, 4, 8, 16 lanes (the partner block's value comes by a DPP permutation:
+// quad xor 1, quad xor 2, half-row mirror, row mirror; every lane of a block
+// holds the same sum, and a + b = b + a exactly), then the four row sums are
+// combined as (r0 + r1) + (r2 + r3).  The result is the same in every lane.
 __device__ __forceinline__ double wave_pairwise_sum(double v) {
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) v += __shfl_xor(v, off, kWave);
-  return v;
+  v = v + dpp_f64<0xB1>(v);   // quad_perm [1, 0, 3, 2]
+  v = v + dpp_f64<0x4E>(v);   // quad_perm [2, 3, 0, 1]
+  v = v + dpp_f64<0x141>(v);  // row_half_mirror
+  v = v + dpp_f64<0x140>(v);  // row_mirror
+  return (readlane_f64(v, 0) + readlane_f64(v, 16)) + (readlane_f64(v, 32) + readlane_f64(v, 48));
 }
 
 __device__ __forceinline__ int cell_of(const DevProblem &P, int k, int ti, int b) {
@@ -652,279 +670,377 @@ __device__ __forceinline__ void option_of(const DevProblem &P, int p, int *ti, i
   *r = p + 1;
 }
 
-// Tables per (realisation, order).  Dynamic LDS holds the order's cells of
-// this realisation (cap, tail), the per-cell maxima, the replica range of
-// every cell, the load-level map and, when kLds, the class tables B, the
-// prefix convolutions P, the suffix convolutions S and the all-but-one
-// tables H (4 x K x (G+1) ints); otherwise those four live in `gtab`.
-//   B_k[g]  best ratio of class k with at most g GPUs
-//   P_k = B_0 (.) ... (.) B_k,   S_k = B_k (.) ... (.) B_{K-1}
-//   H_i = P_{i-1} (.) S_{i+1}    (the convolution of every class but i)
-// Then for every option o of class i, w_o = min(f_o, H_i[G - cost_o]): the
-// best objective of an allocation that gives class i exactly option o.  The
-// objective is max(0, max_o w_o) over the options of any one class, and
-// U(cell) is the same maximum without the options that use `cell`, i.e. the
-// best other cell of the class.
+// Z[g] = max_{a <= g} min(X[g - a], Y[a]) for nondecreasing X and Y.  The
+// inner minimum follows Y while Y[a] < X[g - a] and X afterwards, so it rises
+// and then falls in a; with a* the first a where Y[a] >= X[g - a] (a
+// monotone predicate, found by bisection) the maximum is
+// max(Y[a* - 1], X[g - a*]).  `top` is a power of two with 2 * top > g + 1.
+__device__ __forceinline__ int conv_mono(const int *X, const int *Y, int g, int top) {
+  int pos = 0;
+  for (int step = top; step > 0; step >>= 1) {
+    const int a = min(pos + step - 1, g);
+    const bool below = Y[a] < X[g - a];
+    pos += (pos + step - 1 <= g && below) ? step : 0;
+  }
+  const int left = Y[max(pos - 1, 0)];
+  const int right = X[g - min(pos, g)];
+  return max(pos >= 1 ? left : INT_MIN, pos <= g ? right : INT_MIN);
+}
+
+// Smallest binary32 capacity x >= 0 at which r replicas reach ratio bits M,
+// i.e. min(1, fl32(fl32(r * x) / demand)) >= M.  The ratio is nondecreasing
+// in x and nonnegative binary32 values order like their bit patterns.  The
+// quotient M * demand / r lands within a few units in the last place; the
+// answer is then pinned by stepping until x reaches M and x - 1ulp does not,
+// with a bisection over bit patterns if that takes more than a few steps.
+// 0 when M <= 0 (always reached); NaN when M exceeds 1 (never reached).
+__device__ __forceinline__ float capacity_threshold(int r, int M, float demand, double rcp) {
+  if (M <= 0) return 0.0f;
+  if (M > __float_as_int(1.0f)) return __builtin_nanf("");
+  const float rf = (float)r;
+  auto reach = [&](unsigned xb) {
+    const float capacity = rf * __uint_as_float(xb);
+    return __float_as_int(fminf((float)((double)capacity * rcp), 1.0f)) >= M;
+  };
+  unsigned x = __float_as_uint(__int_as_float(M) * demand * __builtin_amdgcn_rcpf(rf));
+  int n = 0;
+  while (!reach(x) && n < 8) { ++x; ++n; }
+  while (x > 0 && reach(x - 1) && n < 16) { --x; ++n; }
+  if (reach(x) && (x == 0 || !reach(x - 1))) return __uint_as_float(x);
+  unsigned blo = 0, bhi = 0x7F800000u;  // +inf reaches ratio 1 >= M
+  while (blo < bhi) {
+    const unsigned mid = blo + ((bhi - blo) >> 1);
+    if (reach(mid)) bhi = mid;
+    else blo = mid + 1;
+  }
+  return __uint_as_float(blo);
+}
+
+// Candidates the exclusion set-up keeps in LDS (more are read from memory).
+constexpr int kPrepCandLds = 4096;
+
+// Bucket of a replica-range length for the heavy-first work order: longer
+// ranges (more work per scenario) get smaller bucket numbers.
+__device__ __forceinline__ int range_bucket(int len) { return 31 - min(31, 32 - __clz(len)); }
+
+// Problem constants the set-up reads in its inner loops, staged in LDS
+// (kernel arguments are reached through memory loads).
+struct PrepConsts {
+  float levels[kMaxLevels];
+  float demand[kMaxClasses];
+  float slo[kMaxClasses];
+  double rcp[kMaxClasses];
+  int tp[kMaxTp];
+  int optoff[kMaxTp + 1];  // first option of each TP among a class's options
+};
+
+// Replica range of cell (k, ti, b) from the load-level table: the level is
+// nonincreasing in r (with "none" above every level), so the r in
+// [1, G / t] at level b form the range [first r at level <= b,
+// first r at level <= b - 1, exclusive).
+__device__ __forceinline__ int first_r_at_most(const int8_t *lvlk, int rmax, int b, int B) {
+  int lo = 1, hi = rmax + 1;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    const int l = lvlk[mid - 1];
+    if ((l < 0 ? B : l) <= b) hi = mid;
+    else lo = mid + 1;
+  }
+  return lo;
+}
+
+__device__ __forceinline__ void cell_range(const int8_t *lvl, int G, int NT, int B, const int *tp, int cell,
+                                           int *rlo, int *rhi) {
+  const int k = cell / (NT * B), ti = (cell / B) % NT, b = cell % B;
+  const int rmax = G / tp[ti];
+  const int8_t *lvlk = lvl + (size_t)k * G;
+  *rlo = first_r_at_most(lvlk, rmax, b, B);
+  *rhi = b == 0 ? rmax : first_r_at_most(lvlk, rmax, b - 1, B) - 1;
+}
+
+// Set-up of the exclusion scorer, one block per (realisation R, order o,
+// class i); R = 0 is the conservative corner (low capacity, high tail) and
+// R = 1 the optimistic one (Section 4.1).  Tables over g in [0, G) (G itself
+// is never read):
+//   B_k[g]  best ratio of class k with at most g GPUs (nondecreasing)
+//   H_i     the (max,min) convolution of B_k over every k != i, by a tree
+// Every (max,min) target of nondecreasing tables is a crossing search.  Then,
+// per option o = (TP t, r) of class i on cell c: M_o = H_i[G - t r],
+// w_o = min(f_o, M_o), the capacity threshold of M_o, and the cell maximum of
+// w_o.  The objective is max(0, max_o w_o) over the options of any one class;
+// U(cell) is that maximum over the other cells of the cell's class.  Each
+// block writes the tile records of its class's candidates; block (0, o, 0)
+// also writes the order's list of tiles the scorer visits (longest replica
+// range first).
+//
+// Dynamic LDS: all cells (cap, tail) of this realisation; the class's cell
+// maxima and replica ranges; the candidates (up to kPrepCandLds); the
+// load-level table (K x G int8); the order's revealed flags; and, when kLds,
+// the tables (B and two tree buffers, 3 x K x G ints), else in gtab.
 template <bool kLds>
-__global__ __launch_bounds__(1024) void k_prep(DevProblem P, const float *__restrict__ cap_lo,
-                                              const float *__restrict__ cap_hi,
-                                              const float *__restrict__ tail_lo,
-                                              const float *__restrict__ tail_hi,
-                                              const uint8_t *__restrict__ measured,
-                                              const int32_t *__restrict__ cand, int32_t E,
-                                              int32_t *__restrict__ tabH, int32_t *__restrict__ gtab,
-                                              TileInfo *__restrict__ tiles, int32_t *__restrict__ base,
-                                              float *__restrict__ thr, int32_t n_thr,
-                                              int32_t *__restrict__ perm) {
+__global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restrict__ cap_lo,
+                                             const float *__restrict__ cap_hi,
+                                             const float *__restrict__ tail_lo,
+                                             const float *__restrict__ tail_hi,
+                                             const uint8_t *__restrict__ measured,
+                                             const int32_t *__restrict__ cand, int32_t E, int32_t dump,
+                                             int32_t *__restrict__ gtab, TileInfo *__restrict__ tiles,
+                                             int32_t *__restrict__ base, int32_t *__restrict__ mopt,
+                                             float *__restrict__ thr, int32_t n_thr,
+                                             int4 *__restrict__ list, int32_t *__restrict__ live_count) {
   extern __shared__ int lds[];
-  __shared__ int cls_best[kMaxClasses], cls_arg[kMaxClasses], cls_second[kMaxClasses];
-  __shared__ int bucket_count[32], bucket_start[32];
-  const int R = blockIdx.x, o = blockIdx.y, tid = threadIdx.x, nth = blockDim.x;
-  const int G = P.G, K = P.K, W = G + 1, N = P.N;
-  const int KW = K * W;
+  __shared__ PrepConsts C;
+  __shared__ int bucket_count[32], bucket_start[32], n_live;
+  const int R = blockIdx.x, o = blockIdx.y, ci = blockIdx.z;
+  const int tid = threadIdx.x, nth = blockDim.x;
+  const int wave = tid >> 6, lane = tid & (kWave - 1), nw = nth >> 6;
+  const int G = P.G, K = P.K, N = P.N, NT = P.NT, B = P.B, KG = K * G;
+  const int per_class = NT * B;
+  const bool lister = R == 0 && ci == 0;  // writes the work list and invalid records
   float *ccap = (float *)lds;                // [N]
   float *ctail = ccap + N;                   // [N]
-  int *mc = (int *)(ctail + N);              // [N] best w over the cell's options
-  int *rlo = mc + N, *rhi = rlo + N;         // [N] replica range using the cell
-  int *toff = rhi + N;                       // [N] offset of the cell's thresholds
-  int8_t *lvl = (int8_t *)(toff + N);        // [K][W]
-  int *tabs = kLds ? (int *)(lvl + ((KW + 15) & ~15)) : gtab + ((size_t)o * 2 + R) * 4 * KW;
-  int *Bt = tabs, *Pt = tabs + KW, *St = tabs + 2 * KW, *Ht = tabs + 3 * KW;
+  int *mc = (int *)(ctail + N);              // [per_class] cell maxima of class ci
+  int *crlo = mc + per_class;                // [per_class] replica ranges of class ci
+  int *crhi = crlo + per_class;              // [per_class]
+  const bool cand_lds = E <= kPrepCandLds;
+  int *candl = crhi + per_class;             // [E] candidates (when E <= kPrepCandLds)
+  int8_t *lvl = (int8_t *)(candl + (cand_lds ? E : 0));  // [K][G] level of r = g + 1 replicas
+  uint8_t *meas = (uint8_t *)(lvl + ((KG + 15) & ~15));  // [N] revealed cells of the order
+  int *tabs = kLds ? (int *)(meas + ((N + 15) & ~15)) : gtab + (((size_t)o * 2 + R) * K + ci) * 3 * KG;
+  int *Bt = tabs;                            // [K][G]
+  int *Xa = tabs + KG, *Xb = tabs + 2 * KG;  // tree buffers, [ceil((K-1)/2)][G] each
   const size_t off = (size_t)o * N;
-  // Section 4.1: conservative = (low capacity, high tail); optimistic = (high, low).
   const float *gcap = (R == 0 ? cap_lo : cap_hi) + off;
   const float *gtail = (R == 0 ? tail_hi : tail_lo) + off;
-  int PPc = 0;  // options per class
-  for (int t = 0; t < P.NT; ++t) PPc += G / P.tp[t];
+  const int PPc = n_thr / K;
+  int top = 1;
+  while (2 * top <= G) top <<= 1;  // 2 * top > G >= g + 1
 
+  // --- stage constants and cells
+  if (tid < B) C.levels[tid] = P.levels[tid];
+  if (tid < K) {
+    C.demand[tid] = P.demand[tid];
+    C.slo[tid] = P.slo[tid];
+    C.rcp[tid] = P.rcp_demand[tid];
+  }
+  if (tid < NT) C.tp[tid] = P.tp[tid];
+  if (tid == 0) {
+    int at = 0;
+    for (int t = 0; t < NT; ++t) {
+      C.optoff[t] = at;
+      at += G / P.tp[t];
+    }
+    C.optoff[NT] = at;
+  }
+  if (tid < 32) bucket_count[tid] = 0;
   for (int c = tid; c < N; c += nth) {
     ccap[c] = gcap[c];
     ctail[c] = gtail[c];
+    meas[c] = measured[off + c];
+  }
+  if (cand_lds)
+    for (int e = tid; e < E; e += nth) candl[e] = cand[e];
+  for (int c = tid; c < per_class; c += nth) {
     mc[c] = INT_MIN;
-    rlo[c] = INT_MAX;
-    rhi[c] = -1;
-  }
-  for (int idx = tid; idx < KW; idx += nth) {
-    const int k = idx / W, r = idx - k * W;
-    lvl[idx] = (int8_t)(r >= 1 ? level_of(P, k, r) : -1);
-    Bt[idx] = 0;
+    crlo[c] = INT_MAX;
+    crhi[c] = -1;
   }
   __syncthreads();
-  // class tables: every option max-merged into its exact GPU count; also the
-  // replica range of every cell
-  for (int q = tid; q < K * PPc; q += nth) {
-    const int k = q / PPc;
-    int ti, r;
-    option_of(P, q - k * PPc, &ti, &r);
-    const int b = lvl[k * W + r];
-    if (b < 0) continue;
-    const int t = P.tp[ti];
-    const int cell = cell_of(P, k, ti, b);
-    atomicMax(&Bt[k * W + t * r], ratio_bits(ccap[cell], ctail[cell], r, P.slo[k], P.rcp_demand[k]));
-    atomicMin(&rlo[cell], r);
-    atomicMax(&rhi[cell], r);
+
+  // --- load level of every (class, r): the smallest level holding demand / r
+  for (int idx = tid; idx < KG; idx += nth) {
+    const int k = idx / G, r = idx - k * G + 1;
+    const float per_replica = C.demand[k] / (float)r;
+    int lo = 0, hi = B;  // first level >= per_replica; B = none
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (per_replica <= C.levels[mid]) hi = mid;
+      else lo = mid + 1;
+    }
+    lvl[idx] = (int8_t)(lo < B ? lo : -1);
   }
   __syncthreads();
-  // ... then best with at most g GPUs: prefix maximum, one class per wavefront
-  const int wave = tid >> 6, lane = tid & (kWave - 1), nw = nth >> 6;
-  for (int k = wave; k < K; k += nw) {
-    int *T = Bt + k * W;
-    int carry = INT_MIN;
-    for (int b0 = 0; b0 <= G; b0 += kWave) {
-      const int g = b0 + lane;
-      int v = (g <= G) ? T[g] : INT_MIN;
-      v = max(wave_scan_max(v, lane), carry);
-      if (g <= G) T[g] = v;
-      carry = __shfl(v, kWave - 1, kWave);
-    }
-  }
-  // exclusive prefix sum of the replica-range lengths (wavefront 0)
-  if (wave == 0) {
-    int carry = 0;
-    for (int b0 = 0; b0 < N; b0 += kWave) {
-      const int c = b0 + lane;
-      const int len = (c < N && rhi[c] >= 0) ? rhi[c] - rlo[c] + 1 : 0;
-      int v = len;
-#pragma unroll
-      for (int d = 1; d < kWave; d <<= 1) {
-        const int u = __shfl_up(v, d, kWave);
-        if (lane >= d) v += u;
-      }
-      if (c < N) toff[c] = carry + v - len;
-      carry += __shfl(v, kWave - 1, kWave);
-    }
-  }
-  __syncthreads();
-  if (K == 1) {
-    for (int g = tid; g < W; g += nth) Ht[g] = INT_MAX;  // the empty convolution
-  } else {
-    for (int g = tid; g < W; g += nth) {
-      Pt[g] = Bt[g];
-      St[(K - 1) * W + g] = Bt[(K - 1) * W + g];
-    }
-    __syncthreads();
-    // prefix and suffix chains advance together, one step per pass; each
-    // target is shared by a group of 4 lanes
-    const int groups = nth / 4, grp = tid / 4;
-    for (int j = 1; j <= K - 2; ++j) {
-      const int ks = K - 1 - j;
-      for (int base_item = 0; base_item < 2 * W; base_item += groups) {
-        const int item = base_item + grp;
-        const bool act = item < 2 * W;
-        const bool pre = item < W;
-        const int g = pre ? item : item - W;
-        const int v = pre ? conv_at4(Pt + (j - 1) * W, Bt + j * W, g, act)
-                          : conv_at4(Bt + ks * W, St + (ks + 1) * W, act ? g : 0, act);
-        if (act && (tid & 3) == 0) {
-          if (pre) Pt[j * W + g] = v;
-          else St[ks * W + g] = v;
+
+  // --- B tables of the other classes, one wavefront per class: every option
+  // max-merged into its exact GPU count, then the prefix maximum.  Waves not
+  // needed there handle the order's work-list counts (block (0, o, 0)).
+  const int nbw = min(nw, K);  // wavefronts building tables
+  if (wave < nbw) {
+    for (int k = wave; k < K; k += nbw) {
+      if (k == ci) continue;
+      int *T = Bt + k * G;
+      for (int g = lane; g < G; g += kWave) T[g] = 0;  // no option: ratio 0
+      for (int ti = 0; ti < NT; ++ti) {
+        const int t = C.tp[ti];
+        for (int r = lane + 1; t * r < G; r += kWave) {
+          const int b = lvl[k * G + r - 1];
+          if (b < 0) continue;
+          const int cell = cell_of(P, k, ti, b);
+          atomicMax(&T[t * r], ratio_bits(ccap[cell], ctail[cell], r, C.slo[k], C.rcp[k]));
         }
+      }
+      const int L = (G + kWave - 1) / kWave;  // lane l owns [l * L, l * L + L)
+      int run = 0;
+      for (int j = 0; j < L; ++j) {
+        const int g = lane * L + j;
+        if (g < G) {
+          run = max(run, T[g]);
+          T[g] = run;
+        }
+      }
+      int carry = __shfl_up(wave_scan_max(run, lane), 1, kWave);
+      if (lane == 0) carry = 0;
+      for (int j = 0; j < L; ++j) {
+        const int g = lane * L + j;
+        if (g < G) T[g] = max(T[g], carry);
+      }
+    }
+  }
+  if (lister) {
+    const int span = (nw - nbw) * kWave;
+    const int first = wave < nbw ? -1 : tid - nbw * kWave;
+    for (int e = (span > 0 ? first : tid); e >= 0 && e < E; e += (span > 0 ? span : nth)) {
+      const int cell = cand_lds ? candl[e] : cand[e];
+      if (cell < 0 || cell >= N) continue;
+      int rlo, rhi;
+      cell_range(lvl, G, NT, B, C.tp, cell, &rlo, &rhi);
+      const int nr = rhi >= rlo ? rhi - rlo + 1 : 0;
+      if (dump || (!meas[cell] && nr > 0)) atomicAdd(&bucket_count[range_bucket(nr)], 1);
+    }
+  }
+  __syncthreads();
+
+  // --- H_ci: tree over the tables k != ci.  Level 0 reads B (logical table
+  // j is class j, or j + 1 from ci on); later levels alternate Xa / Xb.
+  const int n0 = K - 1;
+  const int *H;
+  if (K == 1) {
+    for (int g = tid; g < G; g += nth) Xa[g] = INT_MAX;  // the empty convolution
+    H = Xa;
+  } else if (n0 == 1) {
+    H = Bt + (ci == 0 ? 1 : 0) * G;
+  } else {
+    int n = n0;
+    int *src = nullptr, *dst = Xa;
+    while (n > 1) {
+      const int pairs = n >> 1, odd = n & 1;
+      for (int item = tid; item < (pairs + odd) * G; item += nth) {
+        const int p = item / G, g = item - p * G;
+        const int ja = 2 * p, jb = 2 * p + 1;
+        const int *X = src ? src + ja * G : Bt + (ja < ci ? ja : ja + 1) * G;
+        int v;
+        if (p < pairs) {
+          const int *Y = src ? src + jb * G : Bt + (jb < ci ? jb : jb + 1) * G;
+          v = conv_mono(X, Y, g, top);
+        } else {
+          v = X[g];  // the odd table passes through
+        }
+        dst[p * G + g] = v;
       }
       __syncthreads();
+      n = pairs + odd;
+      src = dst;
+      dst = dst == Xa ? Xb : Xa;
     }
-    for (int base_item = 0; base_item < KW; base_item += groups) {
-      const int item = base_item + grp;
-      const bool act = item < KW;
-      const int i = act ? item / W : 0, g = act ? item - i * W : 0;
-      const bool mid = act && i > 0 && i < K - 1;
-      const int v = conv_at4(Pt + (mid ? i - 1 : 0) * W, St + (mid ? i + 1 : 0) * W, g, mid);
-      if (act && (tid & 3) == 0) {
-        if (i == 0) Ht[item] = St[W + g];
-        else if (i == K - 1) Ht[item] = Pt[(K - 2) * W + g];
-        else Ht[item] = v;
-      }
+    H = src;
+  }
+  // work-list bucket offsets (block (0, o, 0), last wavefront)
+  if (lister && wave == nw - 1) {
+    const int cnt = lane < 32 ? bucket_count[lane] : 0;
+    int incl = cnt;
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+      const int u = __shfl_up(incl, d, kWave);
+      if (lane >= d) incl += u;
+    }
+    if (lane < 32) bucket_start[lane] = incl - cnt;
+    if (lane == 31) {
+      live_count[o] = incl;
+      n_live = incl;
     }
   }
-  __syncthreads();
-  int32_t *Hg = tabH + ((size_t)o * 2 + R) * KW;
-  for (int idx = tid; idx < KW; idx += nth) Hg[idx] = Ht[idx];
-  // Capacity thresholds: for cell c and replica count r in its range, the
-  // smallest binary32 capacity whose ratio reaches M = H_k[G - t*r].  The
-  // ratio is nondecreasing in the capacity and nonnegative binary32 values
-  // order like their bit patterns, so bisection over bit patterns finds it;
-  // a sampled capacity x then has f_r(x) >= M exactly when x >= threshold.
-  // NaN marks "never" (M above 1).
+  if (K == 1) __syncthreads();
+
+  // --- options of class ci: M, threshold, and w folded into the cell maximum
   {
-    float *T = thr + ((size_t)o * 2 + R) * n_thr;
-    const int total = toff[N - 1] + (rhi[N - 1] >= 0 ? rhi[N - 1] - rlo[N - 1] + 1 : 0);
-    for (int it = tid; it < total; it += nth) {
-      int lo = 0, hi = N - 1;  // the cell whose offset block holds `it`
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (toff[mid] <= it) lo = mid;
-        else hi = mid - 1;
+    int32_t *Mo = mopt + ((size_t)o * 2 + R) * n_thr + (size_t)ci * PPc;
+    float *To = thr + ((size_t)o * 2 + R) * n_thr + (size_t)ci * PPc;
+    for (int p = tid; p < PPc; p += nth) {
+      int ti = 0;
+      while (ti + 1 < NT && p >= C.optoff[ti + 1]) ++ti;
+      const int r = p - C.optoff[ti] + 1, t = C.tp[ti];
+      const int b = lvl[ci * G + r - 1];
+      if (b < 0) {
+        Mo[p] = INT_MIN;
+        To[p] = __builtin_nanf("");
+        continue;
       }
-      const int c = lo;
-      const int k = c / (P.NT * P.B), ti = (c / P.B) % P.NT;
-      const int r = rlo[c] + (it - toff[c]);
-      const int M = Ht[k * W + G - P.tp[ti] * r];
-      float th;
-      if (M <= 0) {
-        th = 0.0f;
-      } else if (M > __float_as_int(1.0f)) {
-        th = __builtin_nanf("");
-      } else {
-        unsigned blo = 0, bhi = 0x7F800000u;  // +inf reaches ratio 1 >= M
-        const float rf = (float)r;
-        while (blo < bhi) {
-          const unsigned mid = blo + ((bhi - blo) >> 1);
-          const float capacity = rf * __uint_as_float(mid);
-          const int f = __float_as_int(fminf((float)((double)capacity * P.rcp_demand[k]), 1.0f));
-          if (f >= M) bhi = mid;
-          else blo = mid + 1;
-        }
-        th = __uint_as_float(blo);
-      }
-      T[it] = th;
-    }
-  }
-  // w_o per option, folded into its cell's maximum
-  for (int q = tid; q < K * PPc; q += nth) {
-    const int k = q / PPc;
-    int ti, r;
-    option_of(P, q - k * PPc, &ti, &r);
-    const int b = lvl[k * W + r];
-    if (b < 0) continue;
-    const int t = P.tp[ti];
-    const int cell = cell_of(P, k, ti, b);
-    const int f = ratio_bits(ccap[cell], ctail[cell], r, P.slo[k], P.rcp_demand[k]);
-    atomicMax(&mc[cell], min(f, Ht[k * W + G - t * r]));
-  }
-  __syncthreads();
-  // per class: best cell value, its cell, and the best of the other cells
-  const int per_class = P.NT * P.B;
-  for (int k = wave; k < K; k += nw) {
-    int best = INT_MIN;
-    for (int c = lane; c < per_class; c += kWave) best = max(best, mc[k * per_class + c]);
-    best = wave_max(best);
-    int arg = INT_MAX;
-    for (int c = lane; c < per_class; c += kWave)
-      if (mc[k * per_class + c] == best) arg = min(arg, c);
-    arg = wave_min(arg);
-    int second = INT_MIN;
-    for (int c = lane; c < per_class; c += kWave)
-      if (c != arg) second = max(second, mc[k * per_class + c]);
-    second = wave_max(second);
-    if (lane == 0) {
-      cls_best[k] = best;
-      cls_arg[k] = k * per_class + arg;
-      cls_second[k] = second;
+      const int local = ti * B + b, cell = ci * per_class + local;
+      const int M = H[G - t * r];
+      const int f = ratio_bits(ccap[cell], ctail[cell], r, C.slo[ci], C.rcp[ci]);
+      atomicMax(&mc[local], min(f, M));
+      atomicMin(&crlo[local], r);
+      atomicMax(&crhi[local], r);
+      Mo[p] = M;
+      To[p] = capacity_threshold(r, M, C.demand[ci], C.rcp[ci]);
     }
   }
   __syncthreads();
-  if (tid == 0) base[o * 2 + R] = max(0, cls_best[0]);  // 0: the empty allocation
-  // Launch order of the candidates for the scoring kernel: longest replica
-  // range first (bucketed by its bit length), so the heaviest wavefronts start
-  // first.  Any order gives the same results.
-  if (R == 0 && o == 0) {
-    if (tid < 32) bucket_count[tid] = 0;
-    __syncthreads();
-    for (int e = tid; e < E; e += nth) {
-      const int cell = cand[e];
-      const int len = (cell >= 0 && cell < N && rhi[cell] >= 0) ? rhi[cell] - rlo[cell] + 1 : 0;
-      atomicAdd(&bucket_count[31 - min(31, 32 - __clz(len))], 1);
-    }
-    __syncthreads();
-    if (tid == 0) {
-      int at = 0;
-      for (int bkt = 0; bkt < 32; ++bkt) {
-        bucket_start[bkt] = at;
-        at += bucket_count[bkt];
-      }
-    }
-    __syncthreads();
-    for (int e = tid; e < E; e += nth) {
-      const int cell = cand[e];
-      const int len = (cell >= 0 && cell < N && rhi[cell] >= 0) ? rhi[cell] - rlo[cell] + 1 : 0;
-      perm[atomicAdd(&bucket_start[31 - min(31, 32 - __clz(len))], 1)] = e;
-    }
-  }
-  // tile records
+
+  // --- tile records of class ci's candidates, U, base, and the work list
   for (int e = tid; e < E; e += nth) {
+    const int cell = cand_lds ? candl[e] : cand[e];
     TileInfo *tl = tiles + (size_t)o * E + e;
-    const int cell = cand[e];
     if (cell < 0 || cell >= N) {
-      if (R == 0) {
-        tl->state = -1; tl->cell = cell; tl->cls = 0; tl->t = 0; tl->rlo = 1; tl->rhi = 0; tl->u_m = 0;
-      } else {
-        tl->u_p = 0;
+      if (lister) {
+        tl->state = -1; tl->cell = cell; tl->cls = 0; tl->t = 0; tl->rlo = 1; tl->rhi = 0;
+        tl->toff = 0; tl->u_m = 0; tl->u_p = 0;
       }
       continue;
     }
-    const int k = cell / per_class;
-    const int u = max(0, cell == cls_arg[k] ? cls_second[k] : cls_best[k]);
+    if (lister) {
+      int rlo, rhi;
+      cell_range(lvl, G, NT, B, C.tp, cell, &rlo, &rhi);
+      const int nr = rhi >= rlo ? rhi - rlo + 1 : 0;
+      if (dump || (!meas[cell] && nr > 0)) {
+        const int k = cell / per_class, ti = (cell / B) % NT, r0 = nr > 0 ? rlo : 1;
+        const int4 ent = make_int4(e, k * PPc + C.optoff[ti] + r0 - 1, r0 | (nr << 16),
+                                   k | ((meas[cell] ? 1 : 0) << 8));
+        list[(size_t)o * E + atomicAdd(&bucket_start[range_bucket(nr)], 1)] = ent;
+      }
+    }
+    if (cell / per_class != ci) continue;
+    const int local = cell - ci * per_class;
+    int u0 = 0, u1 = 0, u2 = 0, u3 = 0;  // the other cells' best, 4 chains
+    int c = 0;
+    for (; c + 4 <= per_class; c += 4) {
+      u0 = max(u0, c + 0 != local ? mc[c + 0] : 0);
+      u1 = max(u1, c + 1 != local ? mc[c + 1] : 0);
+      u2 = max(u2, c + 2 != local ? mc[c + 2] : 0);
+      u3 = max(u3, c + 3 != local ? mc[c + 3] : 0);
+    }
+    for (; c < per_class; ++c) u0 = max(u0, c != local ? mc[c] : 0);
+    const int u = max(max(u0, u1), max(u2, u3));
     if (R == 0) {
-      const int ti = (cell / P.B) % P.NT;
-      tl->cls = k; tl->t = P.tp[ti]; tl->cell = cell;
-      tl->rlo = rhi[cell] >= 0 ? rlo[cell] : 1;
-      tl->rhi = rhi[cell];
-      if (rhi[cell] < 0) tl->rhi = 0;
-      tl->state = measured[off + cell] ? 1 : 0;
-      tl->toff = toff[cell];
+      const int ti = local / B;
+      const int nr = crhi[local] >= crlo[local] ? crhi[local] - crlo[local] + 1 : 0;
+      tl->cls = ci; tl->t = C.tp[ti]; tl->cell = cell;
+      tl->rlo = nr > 0 ? crlo[local] : 1;
+      tl->rhi = nr > 0 ? crhi[local] : 0;
+      tl->state = meas[cell] ? 1 : 0;
+      tl->toff = ci * PPc + C.optoff[ti] + (nr > 0 ? crlo[local] : 1) - 1;
       tl->u_m = u;
     } else {
       tl->u_p = u;
     }
+  }
+  if (lister)
+    for (int z = n_live + tid; z < E; z += nth) list[(size_t)o * E + z] = make_int4(-1, 0, 0, 0);
+  if (ci == 0 && wave == 0) {
+    int v = 0;  // 0: the empty allocation
+    for (int c = lane; c < per_class; c += kWave) v = max(v, mc[c]);
+    v = wave_max(v);
+    if (lane == 0) base[o * 2 + R] = v;
   }
 }
 
@@ -938,17 +1054,21 @@ __device__ __forceinline__ int sampled_ratio(float rf, float cs, double rcp) {
 // crossing search.
 constexpr int kScanMax = 8;
 
-// Scenarios of the exclusion scorer.  One wavefront handles CPW consecutive
-// chunks of 64 x SPL samples of one (order, candidate) tile; lane l owns
-// samples [chunk*64*SPL + l*SPL, +SPL) of each chunk, and the next chunk's
-// samples are loaded while the current one is evaluated.  Each chunk's sum
-// is written as one partial (a node of the pairwise tree over s).
+// Scenarios of the exclusion scorer.  The work items are (order, live tile,
+// group of CPW consecutive chunks of 64 x SPL samples); item it has
+// z = it / (O * groups) -- the tile's place in its order's heavy-first list
+// -- then the order, then the group, so the longest replica ranges of every
+// order come first.  A fixed grid of single-wavefront blocks strides over the
+// items.  Lane l owns samples [chunk * 64 * SPL + l * SPL, +SPL) of each
+// chunk, and the next chunk's samples are loaded while the current one is
+// evaluated.  Each chunk's sum is written as one partial (a node of the
+// pairwise tree over s).
 //
 // Per realisation, tau = max(U, max_r min(f_r, M_r)) with M_r = H[G - t*r].
 // Short replica ranges are scanned.  For long ones: f_r is nondecreasing in r
 // and M_r nonincreasing, so min(f_r, M_r) rises while f_r < M_r and falls
-// after; with r* the first r where f_r >= M_r, the maximum is
-// max(f_{r*-1}, M_{r*}), and r* is found by bisection.
+// after; with r* the first r where f_r >= M_r -- the first r whose capacity
+// threshold the sample reaches -- the maximum is max(f_{r*-1}, M_{r*}).
 template <int SPL>
 __device__ __forceinline__ void load_samples(const float *__restrict__ cap_s, const float *__restrict__ tail_s,
                                              size_t sbase, int s_first, int S, bool need, float (&cs)[SPL],
@@ -971,162 +1091,260 @@ __device__ __forceinline__ void load_samples(const float *__restrict__ cap_s, co
   }
 }
 
+// Orders LDS accesses of one wavefront (its lanes' writes before their
+// reads); LDS executes one wavefront's instructions in issue order.
+__device__ __forceinline__ void wave_lds_fence() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Work-list entry of a tile (written by the set-up): candidate e (-1 past the
+// end of the order's list), option offset of rlo, rlo | nr << 16, and
+// class | state << 8.
+constexpr int kScorerWavesPerBlock = 1;
+
 template <int SPL, int CPW>
-__global__ __launch_bounds__(64) void k_score_excl(DevProblem P, const TileInfo *__restrict__ tiles,
-                                                   const int32_t *__restrict__ tabH,
-                                                   const float *__restrict__ cap_s,
-                                                   const float *__restrict__ tail_s, int32_t E,
-                                                   int32_t S, const int32_t *__restrict__ base,
-                                                   double *__restrict__ partial, int64_t n_partial,
-                                                   float *__restrict__ tau_dump, const float *__restrict__ thr,
-                                                   int32_t n_thr, const int32_t *__restrict__ perm) {
+__global__ __launch_bounds__(64 * kScorerWavesPerBlock) void k_score_excl(
+    DevProblem P, const TileInfo *__restrict__ tiles, const int32_t *__restrict__ mopt,
+    const float *__restrict__ thr, int32_t n_thr, const int4 *__restrict__ list,
+    const int32_t *__restrict__ live_count, const float *__restrict__ cap_s, const float *__restrict__ tail_s,
+    int32_t O, int32_t E, int32_t S, const int32_t *__restrict__ base, double *__restrict__ partial,
+    int64_t n_partial, float *__restrict__ tau_dump, int32_t lds_per_wave) {
   constexpr int CHUNK = 64 * SPL;
-  extern __shared__ int Mlds[];
-  const int o = blockIdx.y, e = perm[blockIdx.z];
-  const int lane = threadIdx.x;
-  const size_t tile = (size_t)o * E + e;
-  const TileInfo tl = tiles[tile];
-  const int c0 = blockIdx.x * CPW;
-  if (tl.state == 1) {
-    if (tau_dump) {
-      for (int c = c0; c < c0 + CPW && c < n_partial; ++c) {
-        const int s_first = c * CHUNK + lane * SPL;
-        for (int q = 0; q < SPL; ++q) {
-          if (s_first + q < S) {
-            tau_dump[(tile * S + s_first + q) * 2 + 0] = __int_as_float(base[o * 2 + 0]);
-            tau_dump[(tile * S + s_first + q) * 2 + 1] = __int_as_float(base[o * 2 + 1]);
-          }
-        }
+  extern __shared__ int lds[];
+  // the wavefront index is uniform: keep it (and all item bookkeeping) scalar
+  const int lane = threadIdx.x & (kWave - 1), wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  int *Mlds = lds + wave * lds_per_wave;
+  const int64_t workers = (int64_t)gridDim.x * kScorerWavesPerBlock;
+  const int groups = (int)((n_partial + CPW - 1) / CPW);
+  const int64_t per_z = (int64_t)O * groups;
+  // list entries are the same for every lane: keep them in scalar registers
+  auto uniform4 = [](int4 v) {
+    return make_int4(__builtin_amdgcn_readfirstlane(v.x), __builtin_amdgcn_readfirstlane(v.y),
+                     __builtin_amdgcn_readfirstlane(v.z), __builtin_amdgcn_readfirstlane(v.w));
+  };
+  // Item it is (z, o, g) with it = (z * O + o) * groups + g: place z in the
+  // order's list, order o, chunk group g.  A wavefront's items are `workers`
+  // apart, so the triple advances by a fixed step with carries (divisions
+  // only at start).
+  struct Pos { int z, o, g; };
+  auto split = [&](int64_t it) {
+    Pos q;
+    q.z = (int)(it / per_z);
+    const int64_t rem = it - (int64_t)q.z * per_z;
+    q.o = (int)(rem / groups);
+    q.g = (int)(rem - (int64_t)q.o * groups);
+    return q;
+  };
+  const Pos step = split(workers);
+  auto advance = [&](Pos q) {
+    q.g += step.g;
+    q.o += step.o;
+    q.z += step.z;
+    if (q.g >= groups) { q.g -= groups; ++q.o; }
+    if (q.o >= O) { q.o -= O; ++q.z; }
+    return q;
+  };
+  // items past the longest list are all empty; the bound is formed while the
+  // first item runs
+  int zl = 0;
+  for (int i = lane; i < O; i += kWave) zl = max(zl, live_count[i]);
+  int64_t n_items = (int64_t)E * per_z;
+  bool bounded = false;
+  // With the default grid most wavefronts take a single item, so the chain
+  // per item is kept short: list entry, then constants and samples together.
+  int64_t it = (int64_t)blockIdx.x * kScorerWavesPerBlock + wave;
+  Pos pos = split(it);
+  // Loads the values a scanned item needs besides its samples: U of both
+  // realisations and M over the replica range.
+  auto load_consts = [&](int oo, int4 en, int2 &uu, int (&m0)[kScanMax], int (&m1)[kScanMax]) {
+    const size_t tl = (size_t)oo * E + en.x;
+    const int nrr = en.z >> 16;
+    const int2 raw = *reinterpret_cast<const int2 *>(&tiles[tl].u_m);
+    uu = make_int2(__builtin_amdgcn_readfirstlane(raw.x), __builtin_amdgcn_readfirstlane(raw.y));
+    if (nrr <= kScanMax) {
+      const int32_t *M0 = mopt + ((size_t)oo * 2 + 0) * n_thr + en.y;
+      const int32_t *M1 = mopt + ((size_t)oo * 2 + 1) * n_thr + en.y;
+#pragma unroll
+      for (int j = 0; j < kScanMax; ++j) {
+        m0[j] = j < nrr ? __builtin_amdgcn_readfirstlane(M0[j]) : 0;
+        m1[j] = j < nrr ? __builtin_amdgcn_readfirstlane(M1[j]) : 0;
       }
     }
-    return;
-  }
-  if (tl.state != 0) return;
-  const int G = P.G, W = G + 1;
-  const int nr = tl.rhi >= tl.rlo ? tl.rhi - tl.rlo + 1 : 0;
-  // with no replica count on the cell the samples cannot matter
-  const bool need = nr > 0 || tau_dump;
-  const int32_t *Hm = tabH + (((size_t)o * 2 + 0) * P.K + tl.cls) * W + G;
-  const int32_t *Hp = tabH + (((size_t)o * 2 + 1) * P.K + tl.cls) * W + G;
-  const double rcp = P.rcp_demand[tl.cls];
-  const float slo = P.slo[tl.cls];
-  const bool scan = nr <= kScanMax;
-  int mm[kScanMax], mp[kScanMax];
-  int steps = 0;
-  if (scan) {
+  };
+  for (; it < n_items; it += workers, pos = advance(pos)) {
+    const int o = pos.o, c0 = pos.g * CPW;
+    const int4 ent = uniform4(list[(size_t)o * E + pos.z]);
+    if (ent.x >= 0) {
+      const int e = ent.x, toff = ent.y, rlo = ent.z & 0xFFFF, nr = ent.z >> 16;
+      const int cls = ent.w & 0xFF, state = ent.w >> 8;
+      const size_t tile = (size_t)o * E + e;
+      int2 u;
+      int mm[kScanMax], mp[kScanMax];
+      load_consts(o, ent, u, mm, mp);
+      if (state != 0 || nr == 0) {
+        // listed only when dumping: a revealed cell keeps the base values; a
+        // cell no replica count reaches leaves tau at U
+        const int vm = state != 0 ? base[o * 2 + 0] : u.x;
+        const int vp = state != 0 ? base[o * 2 + 1] : u.y;
+        for (int c = c0; c < c0 + CPW && c < n_partial; ++c) {
+          const int s_first = c * CHUNK + lane * SPL;
+          for (int q = 0; q < SPL; ++q) {
+            if (s_first + q < S) {
+              tau_dump[(tile * S + s_first + q) * 2 + 0] = __int_as_float(vm);
+              tau_dump[(tile * S + s_first + q) * 2 + 1] = __int_as_float(vp);
+            }
+          }
+        }
+      } else {
+        float cs[SPL], ls[SPL], ncs[SPL], nls[SPL];
+        {
+          const int s_first = c0 * CHUNK + lane * SPL;
+          load_samples<SPL>(cap_s, tail_s, tile * S + s_first, s_first, S, true, cs, ls);
+        }
+        const int32_t *Mm = mopt + ((size_t)o * 2 + 0) * n_thr + toff;
+        const int32_t *Mp = mopt + ((size_t)o * 2 + 1) * n_thr + toff;
+        const double rcp = P.rcp_demand[cls];
+        const float slo = P.slo[cls];
+        const bool scan = nr <= kScanMax;
+        int steps = 0;
+        if (!scan) {
+          const float *Tm = thr + ((size_t)o * 2 + 0) * n_thr + toff;
+          const float *Tp = thr + ((size_t)o * 2 + 1) * n_thr + toff;
+          float *Tl = (float *)(Mlds + 2 * nr);
+          wave_lds_fence();  // the previous item's reads of this wave's LDS are done
+          for (int j = lane; j < nr; j += kWave) {
+            Mlds[j] = Mm[j];
+            Mlds[nr + j] = Mp[j];
+            Tl[j] = Tm[j];
+            Tl[nr + j] = Tp[j];
+          }
+          wave_lds_fence();
+          while ((1 << steps) <= nr) ++steps;  // ceil(log2(nr + 1))
+        }
 #pragma unroll
-    for (int j = 0; j < kScanMax; ++j) {
-      const int r = tl.rlo + j;
-      mm[j] = j < nr ? Hm[-tl.t * r] : 0;
-      mp[j] = j < nr ? Hp[-tl.t * r] : 0;
-    }
-  } else {
-    const float *Tm = thr + ((size_t)o * 2 + 0) * n_thr + tl.toff;
-    const float *Tp = thr + ((size_t)o * 2 + 1) * n_thr + tl.toff;
-    float *Tl = (float *)(Mlds + 2 * nr);
-    for (int j = lane; j < nr; j += kWave) {
-      Mlds[j] = Hm[-tl.t * (tl.rlo + j)];
-      Mlds[nr + j] = Hp[-tl.t * (tl.rlo + j)];
-      Tl[j] = Tm[j];
-      Tl[nr + j] = Tp[j];
-    }
-    __syncthreads();
-    while ((1 << steps) <= nr) ++steps;  // ceil(log2(nr + 1))
-  }
-  float cs[SPL], ls[SPL], ncs[SPL], nls[SPL];
-  {
-    const int s_first = c0 * CHUNK + lane * SPL;
-    load_samples<SPL>(cap_s, tail_s, tile * S + s_first, s_first, S, need && c0 < n_partial, cs, ls);
-  }
+        for (int i = 0; i < CPW; ++i) {
+          const int c = c0 + i;
+          if (c >= n_partial) break;  // uniform
+          if (i + 1 < CPW && c + 1 < n_partial) {
+            const int s_next = (c + 1) * CHUNK + lane * SPL;
+            load_samples<SPL>(cap_s, tail_s, tile * S + s_next, s_next, S, true, ncs, nls);
+          }
+          const int s_first = c * CHUNK + lane * SPL;
+          int am[SPL], ap[SPL];
 #pragma unroll
-  for (int i = 0; i < CPW; ++i) {
-    const int c = c0 + i;
-    if (c >= n_partial) break;  // uniform
-    if (i + 1 < CPW) {
-      const int s_next = (c + 1) * CHUNK + lane * SPL;
-      load_samples<SPL>(cap_s, tail_s, tile * S + s_next, s_next, S, need && c + 1 < n_partial, ncs, nls);
-    }
-    const int s_first = c * CHUNK + lane * SPL;
-    int am[SPL], ap[SPL];
+          for (int q = 0; q < SPL; ++q) am[q] = ap[q] = INT_MIN;
+          if (scan) {
 #pragma unroll
-    for (int q = 0; q < SPL; ++q) { am[q] = tl.u_m; ap[q] = tl.u_p; }
-    if (scan) {
+            for (int j = 0; j < kScanMax; j += 2) {
+              if (j < nr) {
+                const float r1 = (float)(rlo + j), r2 = (float)(rlo + j + 1);
+                const bool two = j + 1 < nr;
 #pragma unroll
-      for (int j = 0; j < kScanMax; j += 2) {
-        if (j < nr) {
-          const float r1 = (float)(tl.rlo + j), r2 = (float)(tl.rlo + j + 1);
-          const bool two = j + 1 < nr;
+                for (int q = 0; q < SPL; ++q) {
+                  const int f1 = sampled_ratio(r1, cs[q], rcp);
+                  const int f2 = two ? sampled_ratio(r2, cs[q], rcp) : INT_MIN;
+                  am[q] = max(am[q], max(min(f1, mm[j]), min(f2, mm[j + 1])));
+                  ap[q] = max(ap[q], max(min(f1, mp[j]), min(f2, mp[j + 1])));
+                }
+              }
+            }
+          } else {
+            // All 2 x SPL searches advance together and every probe reads
+            // LDS unconditionally (index clamped), so the reads of one step
+            // are in flight at once.  pos counts the leading thresholds the
+            // sample does not reach (NaN is never reached); the predicate is
+            // monotone in j, so after the steps 2^(steps-1), ..., 1 pos is
+            // the first crossing.
+            const float *Tl = (const float *)(Mlds + 2 * nr);
+            int pos[SPL][2];
+#pragma unroll
+            for (int q = 0; q < SPL; ++q) pos[q][0] = pos[q][1] = 0;
+            for (int step = 1 << (steps - 1); step > 0; step >>= 1) {
+#pragma unroll
+              for (int q = 0; q < SPL; ++q) {
+#pragma unroll
+                for (int side = 0; side < 2; ++side) {
+                  const int idx = pos[q][side] + step - 1;
+                  const float th = Tl[side * nr + min(idx, nr - 1)];
+                  const bool below = !(cs[q] >= th);
+                  pos[q][side] += (idx < nr && below) ? step : 0;
+                }
+              }
+            }
+#pragma unroll
+            for (int q = 0; q < SPL; ++q) {
+#pragma unroll
+              for (int side = 0; side < 2; ++side) {
+                const int j = pos[q][side];
+                const int mj = Mlds[side * nr + min(j, nr - 1)];
+                const int fprev = sampled_ratio((float)(rlo + j - 1), cs[q], rcp);
+                const int v = max(j > 0 ? fprev : INT_MIN, j < nr ? mj : INT_MIN);
+                if (side == 0) am[q] = max(am[q], v);
+                else ap[q] = max(ap[q], v);
+              }
+            }
+          }
+          double gq[SPL];
 #pragma unroll
           for (int q = 0; q < SPL; ++q) {
-            const int f1 = sampled_ratio(r1, cs[q], rcp);
-            const int f2 = two ? sampled_ratio(r2, cs[q], rcp) : INT_MIN;
-            am[q] = max(am[q], max(min(f1, mm[j]), min(f2, mm[j + 1])));
-            ap[q] = max(ap[q], max(min(f1, mp[j]), min(f2, mp[j + 1])));
+            // tau = max(U, best over the cell's replica counts); a sampled
+            // tail above the SLO makes every option on the cell worth 0
+            const bool tail_ok = ls[q] <= slo;
+            const int tm = tail_ok ? max(am[q], u.x) : u.x;
+            const int tp = tail_ok ? max(ap[q], u.y) : u.y;
+            const bool live = s_first + q < S;
+            gq[q] = live ? (double)__int_as_float(tp) - (double)__int_as_float(tm) : 0.0;
+            if (tau_dump && live) {
+              tau_dump[(tile * S + s_first + q) * 2 + 0] = __int_as_float(tm);
+              tau_dump[(tile * S + s_first + q) * 2 + 1] = __int_as_float(tp);
+            }
+          }
+          // pairwise tree: within the lane's SPL consecutive samples, then lanes
+#pragma unroll
+          for (int w = 1; w < SPL; w <<= 1) {
+#pragma unroll
+            for (int j = 0; j + w < SPL; j += 2 * w) gq[j] = gq[j] + gq[j + w];
+          }
+          const double v = wave_pairwise_sum(gq[0]);
+          if (lane == 0) partial[tile * n_partial + c] = v;
+          if (i + 1 < CPW) {
+#pragma unroll
+            for (int q = 0; q < SPL; ++q) { cs[q] = ncs[q]; ls[q] = nls[q]; }
           }
         }
       }
-    } else {
-      // all 2 x SPL searches advance together, so their LDS reads overlap;
-      // the crossing is the first j whose threshold the sample reaches
-      const float *Tl = (const float *)(Mlds + 2 * nr);
-      int lo[SPL][2], hi[SPL][2];
-#pragma unroll
-      for (int q = 0; q < SPL; ++q) {
-        lo[q][0] = lo[q][1] = 0;
-        hi[q][0] = hi[q][1] = nr;  // first j in [0, nr] with f >= M (nr: none)
-      }
-      for (int it = 0; it < steps; ++it) {
-#pragma unroll
-        for (int q = 0; q < SPL; ++q) {
-#pragma unroll
-          for (int side = 0; side < 2; ++side) {
-            const bool act = lo[q][side] < hi[q][side];
-            const int mid = min((lo[q][side] + hi[q][side]) >> 1, nr - 1);
-            const bool take = act && cs[q] >= Tl[side * nr + mid];
-            hi[q][side] = take ? mid : hi[q][side];
-            lo[q][side] = (act && !take) ? mid + 1 : lo[q][side];
-          }
-        }
-      }
-#pragma unroll
-      for (int q = 0; q < SPL; ++q) {
-#pragma unroll
-        for (int side = 0; side < 2; ++side) {
-          const int j = lo[q][side];
-          int v = j > 0 ? sampled_ratio((float)(tl.rlo + j - 1), cs[q], rcp) : INT_MIN;
-          if (j < nr) v = max(v, Mlds[side * nr + j]);
-          if (side == 0) am[q] = max(am[q], v);
-          else ap[q] = max(ap[q], v);
-        }
-      }
     }
-    double gq[SPL];
-#pragma unroll
-    for (int q = 0; q < SPL; ++q) {
-      // a sampled tail above the SLO makes every option on the cell worth 0
-      const bool tail_ok = ls[q] <= slo;
-      const int tm = tail_ok ? am[q] : tl.u_m;
-      const int tp = tail_ok ? ap[q] : tl.u_p;
-      const bool live = s_first + q < S;
-      gq[q] = live ? (double)__int_as_float(tp) - (double)__int_as_float(tm) : 0.0;
-      if (tau_dump && live) {
-        tau_dump[(tile * S + s_first + q) * 2 + 0] = __int_as_float(tm);
-        tau_dump[(tile * S + s_first + q) * 2 + 1] = __int_as_float(tp);
-      }
-    }
-    // pairwise tree: within the lane's SPL consecutive samples, then lanes
-#pragma unroll
-    for (int w = 1; w < SPL; w <<= 1) {
-#pragma unroll
-      for (int j = 0; j + w < SPL; j += 2 * w) gq[j] = gq[j] + gq[j + w];
-    }
-    const double v = wave_pairwise_sum(gq[0]);
-    if (lane == 0) partial[tile * n_partial + c] = v;
-    if (i + 1 < CPW) {
-#pragma unroll
-      for (int q = 0; q < SPL; ++q) { cs[q] = ncs[q]; ls[q] = nls[q]; }
+    if (!bounded) {
+      n_items = (int64_t)__builtin_amdgcn_readfirstlane(wave_max(zl)) * per_z;
+      bounded = true;
     }
   }
+}
+
+// Pairwise sum (balanced tree over the sample order, zero-padded to a power
+// of two) of n copies of c.  Every full aligned block of 2^j copies sums to
+// 2^j c exactly, so the tree is its lowest set bit of n as one full block,
+// then one addition per higher set bit, innermost first.
+__device__ __forceinline__ double pairwise_run(double c, int64_t n) {
+  if (n <= 0) return 0.0;
+  int64_t low = n & -n;
+  double acc = (double)low * c;
+  for (int64_t rest = n - low; rest != 0; rest -= low) {
+    low = rest & -rest;
+    acc = (double)low * c + acc;
+  }
+  return acc;
+}
+
+// Tile score of the exclusion scorer: Gamma_t - (sum over s of the
+// scenario's gap) / S.  A tile with no replica count on its cell has the
+// same gap u_p - u_m in every scenario and was not visited by the scorer.
+__device__ __forceinline__ bool excl_constant_tile(const TileInfo &tl) { return tl.rhi < tl.rlo; }
+
+__device__ __forceinline__ double excl_constant_sum(const TileInfo &tl, int32_t S) {
+  return pairwise_run((double)__int_as_float(tl.u_p) - (double)__int_as_float(tl.u_m), S);
 }
 
 // Scores and best candidate of the exclusion scorer: one block per order,
@@ -1146,23 +1364,31 @@ __global__ __launch_bounds__(256) void k_finalize_excl(const TileInfo *__restric
   Pick mine{0.0, 0, 0, -1};
   for (int e = threadIdx.x; e < E; e += blockDim.x) {
     const size_t tile = (size_t)o * E + e;
+    // the partials are read together with the tile record (entries of tiles
+    // the scorer did not visit are not used)
+    const double *x = partial + tile * n_partial;
+    double v[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) v[j] = j < n_partial ? x[j] : 0.0;
     const TileInfo tl = tiles[tile];
     double sc = 0.0;  // a revealed cell: nothing to learn
     if (tl.state < 0) {
       sc = __builtin_nan("");
     } else if (tl.state == 0) {
-      const double *x = partial + tile * n_partial;
-      double v[16];
+      double sum;
+      if (excl_constant_tile(tl)) {
+        sum = excl_constant_sum(tl, S);
+      } else {
 #pragma unroll
-      for (int j = 0; j < 16; ++j) v[j] = j < n_partial ? x[j] : 0.0;
+        for (int w = 1; w < 16; w <<= 1) {
+          if (w < p2) {
 #pragma unroll
-      for (int w = 1; w < 16; w <<= 1) {
-        if (w < p2) {
-#pragma unroll
-          for (int j = 0; j + w < 16; j += 2 * w) v[j] = v[j] + v[j + w];
+            for (int j = 0; j + w < 16; j += 2 * w) v[j] = v[j] + v[j + w];
+          }
         }
+        sum = v[0];
       }
-      sc = gap - v[0] / (double)S;
+      sc = gap - sum / (double)S;
       const Pick c{sc, tl.t, tl.cell, e};
       if (better(c, mine)) mine = c;
     }
@@ -1202,7 +1428,9 @@ __global__ __launch_bounds__(256) void k_tile_scores_wave(const TileInfo *__rest
   if (tl.state < 0) sc = __builtin_nan("");
   if (tl.state == 0) {
     const double gap = (double)__int_as_float(base[o * 2 + 1]) - (double)__int_as_float(base[o * 2 + 0]);
-    sc = gap - wave_tree_sum(partial + tile * n_partial, n_partial) / (double)S;
+    const double sum = excl_constant_tile(tl) ? excl_constant_sum(tl, S)
+                                              : wave_tree_sum(partial + tile * n_partial, n_partial);
+    sc = gap - sum / (double)S;
   }
   if ((threadIdx.x & 63) == 0) score[tile] = sc;
 }
@@ -1387,17 +1615,22 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // Dynamic LDS the exclusion set-up kernel may request, and its block size
 // (its passes are short and latency-bound: width shortens them).
 constexpr size_t kPrepLdsLimit = 60 * 1024;
-constexpr int kPrepThreads = 1024;
+constexpr int kPrepThreads = 512;
 
-// LDS of the exclusion set-up besides its tables: cells (cap, tail), cell
-// maxima, replica ranges, and the level map.
-static size_t prep_lds_small(const DevProblem &P) {
-  const size_t KW = (size_t)P.K * (P.G + 1);
-  return 6 * sizeof(int) * (size_t)P.N + ((KW + 15) & ~(size_t)15);
+// LDS of the exclusion set-up besides its tables: cells (cap, tail), the
+// class's cell maxima and replica ranges, the candidates, the load-level
+// table and the revealed flags.
+static size_t prep_lds_small(const DevProblem &P, int64_t E) {
+  const size_t KG = (size_t)P.K * P.G;
+  const size_t cands = E <= kPrepCandLds ? (size_t)E : 0;
+  return sizeof(int) * (2 * (size_t)P.N + 3 * (size_t)P.NT * P.B + cands) + ((KG + 15) & ~(size_t)15) +
+         (((size_t)P.N + 15) & ~(size_t)15);
 }
 
-// Upper bound of the threshold entries per (order, realisation): one per
-// (class, option).
+// LDS of the set-up tables per block: B and two tree buffers, K x G each.
+static size_t prep_lds_tables(const DevProblem &P) { return 3 * sizeof(int) * (size_t)P.K * P.G; }
+
+// Options per (order, realisation): one per (class, TP, r).
 static int32_t excl_thresholds(const DevProblem &P) {
   int per_class = 0;
   for (int t = 0; t < P.NT; ++t) per_class += P.G / P.tp[t];
@@ -1416,14 +1649,15 @@ WsLayout ws_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
   L.partial = at; at = align256(at + sizeof(double) * (size_t)O * (size_t)E * L.n_partial);
   L.flag = at; at = align256(at + sizeof(int32_t) * 4);
   L.tiles = at; at = align256(at + sizeof(TileInfo) * (size_t)O * (size_t)E);
-  const size_t tab = excl_kernel_supported(P) ? sizeof(int32_t) * (size_t)O * 2 * P.K * (P.G + 1) : 0;
-  L.tabH = at; at = align256(at + tab);
+  const bool excl = excl_kernel_supported(P);
   // the exclusion set-up keeps B, P, S, H in LDS when they fit, else here
-  const size_t W = (size_t)P.G + 1, KW = (size_t)P.K * W;
-  const bool in_lds = prep_lds_small(P) + 4 * KW * sizeof(int) <= kPrepLdsLimit;
-  L.tabB = at; at = align256(at + (excl_kernel_supported(P) && !in_lds ? 4 * tab : 0));
-  L.thr = at; at = align256(at + (excl_kernel_supported(P) ? sizeof(float) * (size_t)O * 2 * excl_thresholds(P) : 0));
-  L.perm = at; at = align256(at + sizeof(int32_t) * (size_t)(E > 0 ? E : 1));
+  const bool in_lds = prep_lds_small(P, E) + prep_lds_tables(P) <= kPrepLdsLimit;
+  L.tabB = at; at = align256(at + (excl && !in_lds ? (size_t)O * 2 * P.K * prep_lds_tables(P) : 0));
+  const size_t n_opt = excl ? (size_t)O * 2 * excl_thresholds(P) : 0;
+  L.mopt = at; at = align256(at + sizeof(int32_t) * n_opt);
+  L.thr = at; at = align256(at + sizeof(float) * n_opt);
+  L.list = at; at = align256(at + sizeof(int4) * (size_t)O * (size_t)E);
+  L.live = at; at = align256(at + sizeof(int32_t) * (size_t)(O > 0 ? O : 1));
   L.total = at;
   return L;
 }
@@ -1447,22 +1681,24 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
   const size_t lds = lds_bytes_solver(P, 0);
   if (a.O == 0) return hipSuccess;
   if (a.kernel == 3) {
-    const int W = P.G + 1, KW = P.K * W;
     constexpr int kSpl = 4;
     TileInfo *tiles = (TileInfo *)(a.ws + a.L.tiles);
-    int32_t *tabH = (int32_t *)(a.ws + a.L.tabH);
-    const size_t small = prep_lds_small(P);
-    const size_t big = small + 4 * (size_t)KW * sizeof(int);
+    int32_t *mopt = (int32_t *)(a.ws + a.L.mopt);
     float *thr = (float *)(a.ws + a.L.thr);
+    int4 *list = (int4 *)(a.ws + a.L.list);
+    int32_t *live = (int32_t *)(a.ws + a.L.live);
     const int32_t n_thr = excl_thresholds(P);
-    int32_t *perm = (int32_t *)(a.ws + a.L.perm);
+    const int dump = a.tau_dump != nullptr;
+    const size_t small = prep_lds_small(P, a.E), big = small + prep_lds_tables(P);
     if (big <= kPrepLdsLimit)
-      k_prep<true><<<dim3(2, a.O), kPrepThreads, big, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured,
-                                                  a.cand, a.E, tabH, nullptr, tiles, base, thr, n_thr, perm);
+      k_prep<true><<<dim3(2, a.O, P.K), kPrepThreads, big, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
+                                                          a.measured, a.cand, a.E, dump, nullptr, tiles,
+                                                          base, mopt, thr, n_thr, list, live);
     else
-      k_prep<false><<<dim3(2, a.O), kPrepThreads, small, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
-                                                     a.measured, a.cand, a.E, tabH,
-                                                     (int32_t *)(a.ws + a.L.tabB), tiles, base, thr, n_thr, perm);
+      k_prep<false><<<dim3(2, a.O, P.K), kPrepThreads, small, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
+                                                             a.measured, a.cand, a.E, dump,
+                                                             (int32_t *)(a.ws + a.L.tabB), tiles, base, mopt,
+                                                             thr, n_thr, list, live);
     if (a.E == 0) {
       k_finalize<<<a.O, 64, 0, s>>>(P, info, a.measured, 0, a.S, base, partial, 1, a.score, a.gap_now,
                                     a.best);
@@ -1472,12 +1708,18 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
     const int cpw = a.cpw == 1 ? 1 : (a.cpw == 4 ? 4 : (a.cpw == 8 ? 8 : 2));
     const int64_t chunk = 64 * spl;
     const int64_t n_partial = (a.S + chunk - 1) / chunk;
-    const size_t mlds = 4 * (size_t)(P.G / P.tp[0] + 1) * sizeof(int);
-    const dim3 grid((unsigned)((n_partial + cpw - 1) / cpw), a.O, a.E);
+    const int32_t lds_per_wave = 4 * (P.G / P.tp[0] + 1);  // M and thresholds of the longest range
+    const size_t mlds = (size_t)kScorerWavesPerBlock * lds_per_wave * sizeof(int);
+    const int64_t groups = (n_partial + cpw - 1) / cpw;
+    const int64_t items = groups * a.O * a.E;  // upper bound of the live items
+    const int64_t waves = a.waves > 0 ? a.waves : 8192;
+    const int64_t blocks = ((items < waves ? items : waves) + kScorerWavesPerBlock - 1) / kScorerWavesPerBlock;
+    const unsigned grid = (unsigned)blocks;
     if (a.ev_begin) (void)hipEventRecord(a.ev_begin, s);
 #define FS_EXCL_LAUNCH(SP, CP)                                                                       \
-  k_score_excl<SP, CP><<<grid, 64, mlds, s>>>(P, tiles, tabH, a.cap_s, a.tail_s, a.E, a.S, base,     \
-                                              partial, n_partial, a.tau_dump, thr, n_thr, perm)
+  k_score_excl<SP, CP><<<grid, 64 * kScorerWavesPerBlock, mlds, s>>>(                             \
+      P, tiles, mopt, thr, n_thr, list, live, a.cap_s, a.tail_s, a.O, a.E, a.S, base, partial,      \
+      n_partial, a.tau_dump, lds_per_wave)
 #define FS_EXCL_SPL(SP)                   \
   switch (cpw) {                          \
     case 4: FS_EXCL_LAUNCH(SP, 4); break; \

@@ -399,7 +399,8 @@ def test_kernels_agree_and_are_deterministic(env, orc):
 @pytest.mark.parametrize("S", [4096, 1000])
 def test_exclusion_launch_shapes_agree(env, S):
     """Every launch shape of the exclusion scorer (samples per lane x chunks
-    per wavefront) gives the same bits as the lane kernel's full re-solve, on
+    per work item x grid size, down to one wavefront doing every item) gives
+    the same bits as the lane kernel's full re-solve, on
     two whole config-2 orders; S=1000 leaves a ragged last chunk and wavefronts
     with fewer chunks than the knob asks for."""
     torch, fs, ctx = env
@@ -409,15 +410,18 @@ def test_exclusion_launch_shapes_agree(env, S):
     try:
         for spl in (4, 8, 16):
             for cpw in (1, 2, 4, 8):
-                note(f"exclusion shape S={S} spl={spl} cpw={cpw}")
-                ctx.set_option(fs.OPT_SAMPLES_PER_LANE, spl)
-                ctx.set_option(fs.OPT_CHUNKS_PER_WAVE, cpw)
-                g = gpu_score(env, w.problem, w.intervals, w.cand, cs, ts, kernel=3)
-                for x, y in zip(g, ref):
-                    np.testing.assert_array_equal(x.view(np.uint32), y.view(np.uint32))
+                for waves in (0, 1, 333):
+                    note(f"exclusion shape S={S} spl={spl} cpw={cpw} waves={waves}")
+                    ctx.set_option(fs.OPT_SAMPLES_PER_LANE, spl)
+                    ctx.set_option(fs.OPT_CHUNKS_PER_WAVE, cpw)
+                    ctx.set_option(fs.OPT_SCORER_WAVES, waves)
+                    g = gpu_score(env, w.problem, w.intervals, w.cand, cs, ts, kernel=3)
+                    for x, y in zip(g, ref):
+                        np.testing.assert_array_equal(x.view(np.uint32), y.view(np.uint32))
     finally:
         ctx.set_option(fs.OPT_SAMPLES_PER_LANE, 0)
         ctx.set_option(fs.OPT_CHUNKS_PER_WAVE, 0)
+        ctx.set_option(fs.OPT_SCORER_WAVES, 0)
 
 
 def test_lane_kernel_rejects_unsupported_shapes(env):
