@@ -108,6 +108,14 @@ __device__ __forceinline__ double wave_pairwise_sum(double v) {
   return (readlane_f64(v, 0) + readlane_f64(v, 16)) + (readlane_f64(v, 32) + readlane_f64(v, 48));
 }
 
+// Orders LDS accesses of one wavefront (its lanes' writes before their
+// reads); LDS executes one wavefront's instructions in issue order.
+__device__ __forceinline__ void wave_lds_fence() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 __device__ __forceinline__ int cell_of(const DevProblem &P, int k, int ti, int b) {
   return (k * P.NT + ti) * P.B + b;
 }
@@ -716,52 +724,103 @@ __device__ __forceinline__ float capacity_threshold(int r, int M, float demand, 
   return __uint_as_float(blo);
 }
 
-// Candidates the exclusion set-up keeps in LDS (more are read from memory).
-constexpr int kPrepCandLds = 4096;
-
 // Bucket of a replica-range length for the heavy-first work order: longer
 // ranges (more work per scenario) get smaller bucket numbers.
 __device__ __forceinline__ int range_bucket(int len) { return 31 - min(31, 32 - __clz(len)); }
 
-// Problem constants the set-up reads in its inner loops, staged in LDS
-// (kernel arguments are reached through memory loads).
+// Problem constants the set-up indexes per lane, staged in LDS (kernel
+// arguments are reached through memory loads).
 struct PrepConsts {
   float levels[kMaxLevels];
   float demand[kMaxClasses];
-  float slo[kMaxClasses];
-  double rcp[kMaxClasses];
   int tp[kMaxTp];
   int optoff[kMaxTp + 1];  // first option of each TP among a class's options
 };
 
-// Replica range of cell (k, ti, b) from the load-level table: the level is
-// nonincreasing in r (with "none" above every level), so the r in
-// [1, G / t] at level b form the range [first r at level <= b,
-// first r at level <= b - 1, exclusive).
-__device__ __forceinline__ int first_r_at_most(const int8_t *lvlk, int rmax, int b, int B) {
+// Replica range of a cell: the r in [1, G / t] at the cell's level.  The
+// level is nonincreasing in r ("none" sits above every level), so the range
+// is [first r at level <= b, first r at level <= b - 1), both by bisection on
+// demand / r <= levels[j] (the four argument values are read once).
+__device__ __forceinline__ int first_r_at_most(float demand, float level, int rmax) {
   int lo = 1, hi = rmax + 1;
   while (lo < hi) {
     const int mid = (lo + hi) >> 1;
-    const int l = lvlk[mid - 1];
-    if ((l < 0 ? B : l) <= b) hi = mid;
+    if (demand / (float)mid <= level) hi = mid;
     else lo = mid + 1;
   }
   return lo;
 }
 
-__device__ __forceinline__ void cell_range(const int8_t *lvl, int G, int NT, int B, const int *tp, int cell,
-                                           int *rlo, int *rhi) {
-  const int k = cell / (NT * B), ti = (cell / B) % NT, b = cell % B;
-  const int rmax = G / tp[ti];
-  const int8_t *lvlk = lvl + (size_t)k * G;
-  *rlo = first_r_at_most(lvlk, rmax, b, B);
-  *rhi = b == 0 ? rmax : first_r_at_most(lvlk, rmax, b - 1, B) - 1;
+__device__ __forceinline__ void cell_range(const DevProblem &P, int cell, int *rlo, int *rhi) {
+  const int k = cell / (P.NT * P.B), ti = (cell / P.B) % P.NT, b = cell % P.B;
+  const int rmax = P.G / P.tp[ti];
+  const float demand = P.demand[k], lb = P.levels[b], lb1 = P.levels[b > 0 ? b - 1 : 0];
+  *rlo = first_r_at_most(demand, lb, rmax);
+  *rhi = b == 0 ? rmax : first_r_at_most(demand, lb1, rmax) - 1;
+}
+
+// Work list of one order (the set-up's extra block per order): the tiles the
+// scorer visits -- unrevealed candidates with a nonempty replica range, or
+// every valid candidate when dumping -- as self-contained entries (candidate,
+// option offset, rlo | nr << 16, class | state << 8), longest range first
+// (bucketed by bit length), then end markers.  Also the records of invalid
+// candidates.  Depends only on the problem and the revealed flags.
+__device__ void prep_list(const DevProblem &P, int o, const uint8_t *__restrict__ measured,
+                          const int32_t *__restrict__ cand, int E, int dump, int PPc, const PrepConsts &C,
+                          TileInfo *__restrict__ tiles, int4 *__restrict__ list,
+                          int32_t *__restrict__ live_count, int *bucket_count, int *bucket_start, int *n_live) {
+  const int tid = threadIdx.x, nth = blockDim.x, lane = tid & (kWave - 1);
+  const int N = P.N, per_class = P.NT * P.B;
+  const size_t off = (size_t)o * N;
+  for (int e = tid; e < E; e += nth) {
+    const int cell = cand[e];
+    if (cell < 0 || cell >= N) {
+      TileInfo *tl = tiles + (size_t)o * E + e;
+      tl->state = -1; tl->cell = cell; tl->cls = 0; tl->t = 0; tl->rlo = 1; tl->rhi = 0;
+      tl->toff = 0; tl->u_m = 0; tl->u_p = 0;
+      continue;
+    }
+    int rlo, rhi;
+    cell_range(P, cell, &rlo, &rhi);
+    const int nr = rhi >= rlo ? rhi - rlo + 1 : 0;
+    if (dump || (!measured[off + cell] && nr > 0)) atomicAdd(&bucket_count[range_bucket(nr)], 1);
+  }
+  __syncthreads();
+  if (tid < kWave) {
+    const int cnt = lane < 32 ? bucket_count[lane] : 0;
+    int incl = cnt;
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+      const int u = __shfl_up(incl, d, kWave);
+      if (lane >= d) incl += u;
+    }
+    if (lane < 32) bucket_start[lane] = incl - cnt;
+    if (lane == 31) {
+      live_count[o] = incl;
+      *n_live = incl;
+    }
+  }
+  __syncthreads();
+  for (int e = tid; e < E; e += nth) {
+    const int cell = cand[e];
+    if (cell < 0 || cell >= N) continue;
+    int rlo, rhi;
+    cell_range(P, cell, &rlo, &rhi);
+    const int nr = rhi >= rlo ? rhi - rlo + 1 : 0;
+    const bool meas = measured[off + cell] != 0;
+    if (dump || (!meas && nr > 0)) {
+      const int k = cell / per_class, ti = (cell / P.B) % P.NT, r0 = nr > 0 ? rlo : 1;
+      const int4 ent = make_int4(e, k * PPc + C.optoff[ti] + r0 - 1, r0 | (nr << 16), k | ((meas ? 1 : 0) << 8));
+      list[(size_t)o * E + atomicAdd(&bucket_start[range_bucket(nr)], 1)] = ent;
+    }
+  }
+  for (int z = *n_live + tid; z < E; z += nth) list[(size_t)o * E + z] = make_int4(-1, 0, 0, 0);
 }
 
 // Set-up of the exclusion scorer, one block per (realisation R, order o,
-// class i); R = 0 is the conservative corner (low capacity, high tail) and
-// R = 1 the optimistic one (Section 4.1).  Tables over g in [0, G) (G itself
-// is never read):
+// class i) plus one work-list block per order (i = K); R = 0 is the
+// conservative corner (low capacity, high tail) and R = 1 the optimistic one
+// (Section 4.1).  Tables over g in [0, G) (G itself is never read):
 //   B_k[g]  best ratio of class k with at most g GPUs (nondecreasing)
 //   H_i     the (max,min) convolution of B_k over every k != i, by a tree
 // Every (max,min) target of nondecreasing tables is a crossing search.  Then,
@@ -769,14 +828,11 @@ __device__ __forceinline__ void cell_range(const int8_t *lvl, int G, int NT, int
 // w_o = min(f_o, M_o), the capacity threshold of M_o, and the cell maximum of
 // w_o.  The objective is max(0, max_o w_o) over the options of any one class;
 // U(cell) is that maximum over the other cells of the cell's class.  Each
-// block writes the tile records of its class's candidates; block (0, o, 0)
-// also writes the order's list of tiles the scorer visits (longest replica
-// range first).
+// block writes the tile records of its class's candidates.
 //
 // Dynamic LDS: all cells (cap, tail) of this realisation; the class's cell
-// maxima and replica ranges; the candidates (up to kPrepCandLds); the
-// load-level table (K x G int8); the order's revealed flags; and, when kLds,
-// the tables (B and two tree buffers, 3 x K x G ints), else in gtab.
+// maxima and replica ranges; the load-level table (K x G int8); and, when
+// kLds, the tables (B and two tree buffers, 3 x K x G ints), else in gtab.
 template <bool kLds>
 __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restrict__ cap_lo,
                                              const float *__restrict__ cap_hi,
@@ -793,36 +849,10 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
   __shared__ int bucket_count[32], bucket_start[32], n_live;
   const int R = blockIdx.x, o = blockIdx.y, ci = blockIdx.z;
   const int tid = threadIdx.x, nth = blockDim.x;
-  const int wave = tid >> 6, lane = tid & (kWave - 1), nw = nth >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & (kWave - 1), nw = nth >> 6;
   const int G = P.G, K = P.K, N = P.N, NT = P.NT, B = P.B, KG = K * G;
   const int per_class = NT * B;
-  const bool lister = R == 0 && ci == 0;  // writes the work list and invalid records
-  float *ccap = (float *)lds;                // [N]
-  float *ctail = ccap + N;                   // [N]
-  int *mc = (int *)(ctail + N);              // [per_class] cell maxima of class ci
-  int *crlo = mc + per_class;                // [per_class] replica ranges of class ci
-  int *crhi = crlo + per_class;              // [per_class]
-  const bool cand_lds = E <= kPrepCandLds;
-  int *candl = crhi + per_class;             // [E] candidates (when E <= kPrepCandLds)
-  int8_t *lvl = (int8_t *)(candl + (cand_lds ? E : 0));  // [K][G] level of r = g + 1 replicas
-  uint8_t *meas = (uint8_t *)(lvl + ((KG + 15) & ~15));  // [N] revealed cells of the order
-  int *tabs = kLds ? (int *)(meas + ((N + 15) & ~15)) : gtab + (((size_t)o * 2 + R) * K + ci) * 3 * KG;
-  int *Bt = tabs;                            // [K][G]
-  int *Xa = tabs + KG, *Xb = tabs + 2 * KG;  // tree buffers, [ceil((K-1)/2)][G] each
-  const size_t off = (size_t)o * N;
-  const float *gcap = (R == 0 ? cap_lo : cap_hi) + off;
-  const float *gtail = (R == 0 ? tail_hi : tail_lo) + off;
   const int PPc = n_thr / K;
-  int top = 1;
-  while (2 * top <= G) top <<= 1;  // 2 * top > G >= g + 1
-
-  // --- stage constants and cells
-  if (tid < B) C.levels[tid] = P.levels[tid];
-  if (tid < K) {
-    C.demand[tid] = P.demand[tid];
-    C.slo[tid] = P.slo[tid];
-    C.rcp[tid] = P.rcp_demand[tid];
-  }
   if (tid < NT) C.tp[tid] = P.tp[tid];
   if (tid == 0) {
     int at = 0;
@@ -832,20 +862,45 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
     }
     C.optoff[NT] = at;
   }
-  if (tid < 32) bucket_count[tid] = 0;
+  if (ci == K) {  // the work-list block of order o
+    if (R != 0) return;
+    if (tid < 32) bucket_count[tid] = 0;
+    __syncthreads();
+    prep_list(P, o, measured, cand, E, dump, PPc, C, tiles, list, live_count, bucket_count, bucket_start,
+              &n_live);
+    return;
+  }
+  float *ccap = (float *)lds;                // [N]
+  float *ctail = ccap + N;                   // [N]
+  int *mc = (int *)(ctail + N);              // [per_class] cell maxima of class ci
+  int *crlo = mc + per_class;                // [per_class] replica ranges of class ci
+  int *crhi = crlo + per_class;              // [per_class]
+  int8_t *lvl = (int8_t *)(crhi + per_class);  // [K][G] load level of r = g + 1 replicas
+  int *tabs = kLds ? (int *)(lvl + ((KG + 15) & ~15)) : gtab + (((size_t)o * 2 + R) * K + ci) * 3 * KG;
+  int *Bt = tabs;                            // [K][G]
+  int *Xa = tabs + KG, *Xb = tabs + 2 * KG;  // tree buffers, [ceil((K-1)/2)][G] each
+  const size_t off = (size_t)o * N;
+  const float *gcap = (R == 0 ? cap_lo : cap_hi) + off;
+  const float *gtail = (R == 0 ? tail_hi : tail_lo) + off;
+  int top = 1;
+  while (2 * top <= G) top <<= 1;  // 2 * top > G >= g + 1
+
+  // --- stage the cells; each thread's first candidate is read now
   for (int c = tid; c < N; c += nth) {
     ccap[c] = gcap[c];
     ctail[c] = gtail[c];
-    meas[c] = measured[off + c];
   }
-  if (cand_lds)
-    for (int e = tid; e < E; e += nth) candl[e] = cand[e];
   for (int c = tid; c < per_class; c += nth) {
     mc[c] = INT_MIN;
     crlo[c] = INT_MAX;
     crhi[c] = -1;
   }
+  if (tid < B) C.levels[tid] = P.levels[tid];
+  if (tid < K) C.demand[tid] = P.demand[tid];
+  const int my_cell = tid < E ? cand[tid] : -1;
   __syncthreads();
+  const bool my_valid = my_cell >= 0 && my_cell < N;
+  const int my_meas = (R == 0 && my_valid && my_cell / per_class == ci) ? measured[off + my_cell] : 0;
 
   // --- load level of every (class, r): the smallest level holding demand / r
   for (int idx = tid; idx < KG; idx += nth) {
@@ -862,23 +917,26 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
   __syncthreads();
 
   // --- B tables of the other classes, one wavefront per class: every option
-  // max-merged into its exact GPU count, then the prefix maximum.  Waves not
-  // needed there handle the order's work-list counts (block (0, o, 0)).
-  const int nbw = min(nw, K);  // wavefronts building tables
+  // max-merged into its exact GPU count, then the prefix maximum
+  const int nbw = min(nw, K);
   if (wave < nbw) {
     for (int k = wave; k < K; k += nbw) {
       if (k == ci) continue;
       int *T = Bt + k * G;
       for (int g = lane; g < G; g += kWave) T[g] = 0;  // no option: ratio 0
+      wave_lds_fence();
+      const float slo = P.slo[k];
+      const double rcp = P.rcp_demand[k];
       for (int ti = 0; ti < NT; ++ti) {
-        const int t = C.tp[ti];
+        const int t = P.tp[ti];
         for (int r = lane + 1; t * r < G; r += kWave) {
           const int b = lvl[k * G + r - 1];
           if (b < 0) continue;
           const int cell = cell_of(P, k, ti, b);
-          atomicMax(&T[t * r], ratio_bits(ccap[cell], ctail[cell], r, C.slo[k], C.rcp[k]));
+          atomicMax(&T[t * r], ratio_bits(ccap[cell], ctail[cell], r, slo, rcp));
         }
       }
+      wave_lds_fence();
       const int L = (G + kWave - 1) / kWave;  // lane l owns [l * L, l * L + L)
       int run = 0;
       for (int j = 0; j < L; ++j) {
@@ -896,18 +954,6 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
       }
     }
   }
-  if (lister) {
-    const int span = (nw - nbw) * kWave;
-    const int first = wave < nbw ? -1 : tid - nbw * kWave;
-    for (int e = (span > 0 ? first : tid); e >= 0 && e < E; e += (span > 0 ? span : nth)) {
-      const int cell = cand_lds ? candl[e] : cand[e];
-      if (cell < 0 || cell >= N) continue;
-      int rlo, rhi;
-      cell_range(lvl, G, NT, B, C.tp, cell, &rlo, &rhi);
-      const int nr = rhi >= rlo ? rhi - rlo + 1 : 0;
-      if (dump || (!meas[cell] && nr > 0)) atomicAdd(&bucket_count[range_bucket(nr)], 1);
-    }
-  }
   __syncthreads();
 
   // --- H_ci: tree over the tables k != ci.  Level 0 reads B (logical table
@@ -917,6 +963,7 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
   if (K == 1) {
     for (int g = tid; g < G; g += nth) Xa[g] = INT_MAX;  // the empty convolution
     H = Xa;
+    __syncthreads();
   } else if (n0 == 1) {
     H = Bt + (ci == 0 ? 1 : 0) * G;
   } else {
@@ -944,27 +991,13 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
     }
     H = src;
   }
-  // work-list bucket offsets (block (0, o, 0), last wavefront)
-  if (lister && wave == nw - 1) {
-    const int cnt = lane < 32 ? bucket_count[lane] : 0;
-    int incl = cnt;
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-      const int u = __shfl_up(incl, d, kWave);
-      if (lane >= d) incl += u;
-    }
-    if (lane < 32) bucket_start[lane] = incl - cnt;
-    if (lane == 31) {
-      live_count[o] = incl;
-      n_live = incl;
-    }
-  }
-  if (K == 1) __syncthreads();
 
   // --- options of class ci: M, threshold, and w folded into the cell maximum
   {
     int32_t *Mo = mopt + ((size_t)o * 2 + R) * n_thr + (size_t)ci * PPc;
     float *To = thr + ((size_t)o * 2 + R) * n_thr + (size_t)ci * PPc;
+    const float slo = P.slo[ci], demand = P.demand[ci];
+    const double rcp = P.rcp_demand[ci];
     for (int p = tid; p < PPc; p += nth) {
       int ti = 0;
       while (ti + 1 < NT && p >= C.optoff[ti + 1]) ++ti;
@@ -976,40 +1009,24 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
         continue;
       }
       const int local = ti * B + b, cell = ci * per_class + local;
-      const int M = H[G - t * r];
-      const int f = ratio_bits(ccap[cell], ctail[cell], r, C.slo[ci], C.rcp[ci]);
+      // ratios never exceed 1, so M above 1 acts as 1 (min(f, M) and the
+      // crossing are unchanged) and the scorer can skip the clamp of f
+      const int M = min(H[G - t * r], __float_as_int(1.0f));
+      const int f = ratio_bits(ccap[cell], ctail[cell], r, slo, rcp);
       atomicMax(&mc[local], min(f, M));
       atomicMin(&crlo[local], r);
       atomicMax(&crhi[local], r);
       Mo[p] = M;
-      To[p] = capacity_threshold(r, M, C.demand[ci], C.rcp[ci]);
+      To[p] = capacity_threshold(r, M, demand, rcp);
     }
   }
   __syncthreads();
 
-  // --- tile records of class ci's candidates, U, base, and the work list
+  // --- tile records of class ci's candidates and U; the base objective
   for (int e = tid; e < E; e += nth) {
-    const int cell = cand_lds ? candl[e] : cand[e];
+    const int cell = e == tid ? my_cell : cand[e];
+    if (cell < 0 || cell >= N || cell / per_class != ci) continue;
     TileInfo *tl = tiles + (size_t)o * E + e;
-    if (cell < 0 || cell >= N) {
-      if (lister) {
-        tl->state = -1; tl->cell = cell; tl->cls = 0; tl->t = 0; tl->rlo = 1; tl->rhi = 0;
-        tl->toff = 0; tl->u_m = 0; tl->u_p = 0;
-      }
-      continue;
-    }
-    if (lister) {
-      int rlo, rhi;
-      cell_range(lvl, G, NT, B, C.tp, cell, &rlo, &rhi);
-      const int nr = rhi >= rlo ? rhi - rlo + 1 : 0;
-      if (dump || (!meas[cell] && nr > 0)) {
-        const int k = cell / per_class, ti = (cell / B) % NT, r0 = nr > 0 ? rlo : 1;
-        const int4 ent = make_int4(e, k * PPc + C.optoff[ti] + r0 - 1, r0 | (nr << 16),
-                                   k | ((meas[cell] ? 1 : 0) << 8));
-        list[(size_t)o * E + atomicAdd(&bucket_start[range_bucket(nr)], 1)] = ent;
-      }
-    }
-    if (cell / per_class != ci) continue;
     const int local = cell - ci * per_class;
     int u0 = 0, u1 = 0, u2 = 0, u3 = 0;  // the other cells' best, 4 chains
     int c = 0;
@@ -1024,18 +1041,17 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
     if (R == 0) {
       const int ti = local / B;
       const int nr = crhi[local] >= crlo[local] ? crhi[local] - crlo[local] + 1 : 0;
+      const int meas = e == tid ? my_meas : measured[off + cell];
       tl->cls = ci; tl->t = C.tp[ti]; tl->cell = cell;
       tl->rlo = nr > 0 ? crlo[local] : 1;
       tl->rhi = nr > 0 ? crhi[local] : 0;
-      tl->state = meas[cell] ? 1 : 0;
+      tl->state = meas ? 1 : 0;
       tl->toff = ci * PPc + C.optoff[ti] + (nr > 0 ? crlo[local] : 1) - 1;
       tl->u_m = u;
     } else {
       tl->u_p = u;
     }
   }
-  if (lister)
-    for (int z = n_live + tid; z < E; z += nth) list[(size_t)o * E + z] = make_int4(-1, 0, 0, 0);
   if (ci == 0 && wave == 0) {
     int v = 0;  // 0: the empty allocation
     for (int c = lane; c < per_class; c += kWave) v = max(v, mc[c]);
@@ -1048,6 +1064,13 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
 __device__ __forceinline__ int sampled_ratio(float rf, float cs, double rcp) {
   const float capacity = rf * cs;
   return __float_as_int(fminf((float)((double)capacity * rcp), 1.0f));
+}
+
+// The same quotient without the clamp at 1, for use as min(q, M) with M <= 1
+// (the clamp cannot change that minimum).
+__device__ __forceinline__ int sampled_quotient(float rf, float cs, double rcp) {
+  const float capacity = rf * cs;
+  return __float_as_int((float)((double)capacity * rcp));
 }
 
 // Largest replica range handled by the unrolled scan; longer ranges use the
@@ -1069,34 +1092,33 @@ constexpr int kScanMax = 8;
 // and M_r nonincreasing, so min(f_r, M_r) rises while f_r < M_r and falls
 // after; with r* the first r where f_r >= M_r -- the first r whose capacity
 // threshold the sample reaches -- the maximum is max(f_{r*-1}, M_{r*}).
-template <int SPL>
-__device__ __forceinline__ void load_samples(const float *__restrict__ cap_s, const float *__restrict__ tail_s,
-                                             size_t sbase, int s_first, int S, bool need, float (&cs)[SPL],
-                                             float (&ls)[SPL]) {
-  if (need && s_first + SPL <= S && ((sbase & 3) == 0)) {
+// Samples of one chunk.  VEC (S a multiple of 4): each group of 4 samples
+// of a lane lies wholly below S or wholly past it; every group is fetched by
+// one 16-byte load at an in-bounds address (a group past S reads the tile's
+// last 4 samples, values that are never used), so the loads are unconditional
+// and the compiler's wait counts stay exact.  Otherwise single loads,
+// predicated per sample.
+template <int SPL, bool VEC>
+__device__ __forceinline__ void load_chunk(const float *__restrict__ cap_s, const float *__restrict__ tail_s,
+                                           size_t tbase, int s_first, int S, float (&cs)[SPL],
+                                           float (&ls)[SPL]) {
+  if constexpr (VEC) {
 #pragma unroll
     for (int v4 = 0; v4 < SPL / 4; ++v4) {
-      const float4 c4 = *reinterpret_cast<const float4 *>(cap_s + sbase + 4 * v4);
-      const float4 l4 = *reinterpret_cast<const float4 *>(tail_s + sbase + 4 * v4);
+      const size_t at = tbase + (size_t)min(s_first + 4 * v4, S - 4);
+      const float4 c4 = *reinterpret_cast<const float4 *>(cap_s + at);
+      const float4 l4 = *reinterpret_cast<const float4 *>(tail_s + at);
       cs[4 * v4 + 0] = c4.x; cs[4 * v4 + 1] = c4.y; cs[4 * v4 + 2] = c4.z; cs[4 * v4 + 3] = c4.w;
       ls[4 * v4 + 0] = l4.x; ls[4 * v4 + 1] = l4.y; ls[4 * v4 + 2] = l4.z; ls[4 * v4 + 3] = l4.w;
     }
   } else {
 #pragma unroll
     for (int q = 0; q < SPL; ++q) {
-      const bool live = need && s_first + q < S;
-      cs[q] = live ? cap_s[sbase + q] : 0.0f;
-      ls[q] = live ? tail_s[sbase + q] : 0.0f;
+      const bool live = s_first + q < S;
+      cs[q] = live ? cap_s[tbase + s_first + q] : 0.0f;
+      ls[q] = live ? tail_s[tbase + s_first + q] : 0.0f;
     }
   }
-}
-
-// Orders LDS accesses of one wavefront (its lanes' writes before their
-// reads); LDS executes one wavefront's instructions in issue order.
-__device__ __forceinline__ void wave_lds_fence() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 // Work-list entry of a tile (written by the set-up): candidate e (-1 past the
@@ -1104,7 +1126,7 @@ __device__ __forceinline__ void wave_lds_fence() {
 // class | state << 8.
 constexpr int kScorerWavesPerBlock = 1;
 
-template <int SPL, int CPW>
+template <int SPL, int CPW, bool VEC>
 __global__ __launch_bounds__(64 * kScorerWavesPerBlock) void k_score_excl(
     DevProblem P, const TileInfo *__restrict__ tiles, const int32_t *__restrict__ mopt,
     const float *__restrict__ thr, int32_t n_thr, const int4 *__restrict__ list,
@@ -1199,10 +1221,7 @@ __global__ __launch_bounds__(64 * kScorerWavesPerBlock) void k_score_excl(
         }
       } else {
         float cs[SPL], ls[SPL], ncs[SPL], nls[SPL];
-        {
-          const int s_first = c0 * CHUNK + lane * SPL;
-          load_samples<SPL>(cap_s, tail_s, tile * S + s_first, s_first, S, true, cs, ls);
-        }
+        load_chunk<SPL, VEC>(cap_s, tail_s, tile * S, c0 * CHUNK + lane * SPL, S, cs, ls);
         const int32_t *Mm = mopt + ((size_t)o * 2 + 0) * n_thr + toff;
         const int32_t *Mp = mopt + ((size_t)o * 2 + 1) * n_thr + toff;
         const double rcp = P.rcp_demand[cls];
@@ -1227,9 +1246,9 @@ __global__ __launch_bounds__(64 * kScorerWavesPerBlock) void k_score_excl(
         for (int i = 0; i < CPW; ++i) {
           const int c = c0 + i;
           if (c >= n_partial) break;  // uniform
-          if (i + 1 < CPW && c + 1 < n_partial) {
-            const int s_next = (c + 1) * CHUNK + lane * SPL;
-            load_samples<SPL>(cap_s, tail_s, tile * S + s_next, s_next, S, true, ncs, nls);
+          if (i + 1 < CPW) {  // unconditional (clamped) so the waits stay exact
+            const int cn = c + 1 < n_partial ? c + 1 : c;
+            load_chunk<SPL, VEC>(cap_s, tail_s, tile * S, cn * CHUNK + lane * SPL, S, ncs, nls);
           }
           const int s_first = c * CHUNK + lane * SPL;
           int am[SPL], ap[SPL];
@@ -1239,12 +1258,13 @@ __global__ __launch_bounds__(64 * kScorerWavesPerBlock) void k_score_excl(
 #pragma unroll
             for (int j = 0; j < kScanMax; j += 2) {
               if (j < nr) {
+                // M <= 1 lets min(f, M) use the unclamped quotient; past the
+                // range M is 0, a term that cannot raise tau (U >= 0)
                 const float r1 = (float)(rlo + j), r2 = (float)(rlo + j + 1);
-                const bool two = j + 1 < nr;
 #pragma unroll
                 for (int q = 0; q < SPL; ++q) {
-                  const int f1 = sampled_ratio(r1, cs[q], rcp);
-                  const int f2 = two ? sampled_ratio(r2, cs[q], rcp) : INT_MIN;
+                  const int f1 = sampled_quotient(r1, cs[q], rcp);
+                  const int f2 = sampled_quotient(r2, cs[q], rcp);
                   am[q] = max(am[q], max(min(f1, mm[j]), min(f2, mm[j + 1])));
                   ap[q] = max(ap[q], max(min(f1, mp[j]), min(f2, mp[j + 1])));
                 }
@@ -1618,13 +1638,10 @@ constexpr size_t kPrepLdsLimit = 60 * 1024;
 constexpr int kPrepThreads = 512;
 
 // LDS of the exclusion set-up besides its tables: cells (cap, tail), the
-// class's cell maxima and replica ranges, the candidates, the load-level
-// table and the revealed flags.
-static size_t prep_lds_small(const DevProblem &P, int64_t E) {
+// class's cell maxima and replica ranges, and the load-level table.
+static size_t prep_lds_small(const DevProblem &P) {
   const size_t KG = (size_t)P.K * P.G;
-  const size_t cands = E <= kPrepCandLds ? (size_t)E : 0;
-  return sizeof(int) * (2 * (size_t)P.N + 3 * (size_t)P.NT * P.B + cands) + ((KG + 15) & ~(size_t)15) +
-         (((size_t)P.N + 15) & ~(size_t)15);
+  return sizeof(int) * (2 * (size_t)P.N + 3 * (size_t)P.NT * P.B) + ((KG + 15) & ~(size_t)15);
 }
 
 // LDS of the set-up tables per block: B and two tree buffers, K x G each.
@@ -1651,7 +1668,7 @@ WsLayout ws_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
   L.tiles = at; at = align256(at + sizeof(TileInfo) * (size_t)O * (size_t)E);
   const bool excl = excl_kernel_supported(P);
   // the exclusion set-up keeps B, P, S, H in LDS when they fit, else here
-  const bool in_lds = prep_lds_small(P, E) + prep_lds_tables(P) <= kPrepLdsLimit;
+  const bool in_lds = prep_lds_small(P) + prep_lds_tables(P) <= kPrepLdsLimit;
   L.tabB = at; at = align256(at + (excl && !in_lds ? (size_t)O * 2 * P.K * prep_lds_tables(P) : 0));
   const size_t n_opt = excl ? (size_t)O * 2 * excl_thresholds(P) : 0;
   L.mopt = at; at = align256(at + sizeof(int32_t) * n_opt);
@@ -1689,13 +1706,13 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
     int32_t *live = (int32_t *)(a.ws + a.L.live);
     const int32_t n_thr = excl_thresholds(P);
     const int dump = a.tau_dump != nullptr;
-    const size_t small = prep_lds_small(P, a.E), big = small + prep_lds_tables(P);
+    const size_t small = prep_lds_small(P), big = small + prep_lds_tables(P);
     if (big <= kPrepLdsLimit)
-      k_prep<true><<<dim3(2, a.O, P.K), kPrepThreads, big, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
+      k_prep<true><<<dim3(2, a.O, P.K + 1), kPrepThreads, big, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
                                                           a.measured, a.cand, a.E, dump, nullptr, tiles,
                                                           base, mopt, thr, n_thr, list, live);
     else
-      k_prep<false><<<dim3(2, a.O, P.K), kPrepThreads, small, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
+      k_prep<false><<<dim3(2, a.O, P.K + 1), kPrepThreads, small, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
                                                              a.measured, a.cand, a.E, dump,
                                                              (int32_t *)(a.ws + a.L.tabB), tiles, base, mopt,
                                                              thr, n_thr, list, live);
@@ -1716,10 +1733,15 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
     const int64_t blocks = ((items < waves ? items : waves) + kScorerWavesPerBlock - 1) / kScorerWavesPerBlock;
     const unsigned grid = (unsigned)blocks;
     if (a.ev_begin) (void)hipEventRecord(a.ev_begin, s);
-#define FS_EXCL_LAUNCH(SP, CP)                                                                       \
-  k_score_excl<SP, CP><<<grid, 64 * kScorerWavesPerBlock, mlds, s>>>(                             \
-      P, tiles, mopt, thr, n_thr, list, live, a.cap_s, a.tail_s, a.O, a.E, a.S, base, partial,      \
-      n_partial, a.tau_dump, lds_per_wave)
+#define FS_EXCL_LAUNCH(SP, CP)                                                                      \
+  if (a.S % 4 == 0)                                                                                  \
+    k_score_excl<SP, CP, true><<<grid, 64 * kScorerWavesPerBlock, mlds, s>>>(                        \
+        P, tiles, mopt, thr, n_thr, list, live, a.cap_s, a.tail_s, a.O, a.E, a.S, base, partial,    \
+        n_partial, a.tau_dump, lds_per_wave);                                                        \
+  else                                                                                               \
+    k_score_excl<SP, CP, false><<<grid, 64 * kScorerWavesPerBlock, mlds, s>>>(                       \
+        P, tiles, mopt, thr, n_thr, list, live, a.cap_s, a.tail_s, a.O, a.E, a.S, base, partial,    \
+        n_partial, a.tau_dump, lds_per_wave)
 #define FS_EXCL_SPL(SP)                   \
   switch (cpw) {                          \
     case 4: FS_EXCL_LAUNCH(SP, 4); break; \
