@@ -614,6 +614,47 @@ __device__ __forceinline__ bool better(const Pick &a, const Pick &b) {
   return a.e < b.e;
 }
 
+template <int kCtrl>
+__device__ __forceinline__ Pick dpp_pick(const Pick &p) {
+  Pick q;
+  q.score = dpp_f64<kCtrl>(p.score);
+  q.tp = __builtin_amdgcn_mov_dpp(p.tp, kCtrl, 0xF, 0xF, true);
+  q.cell = __builtin_amdgcn_mov_dpp(p.cell, kCtrl, 0xF, 0xF, true);
+  q.e = __builtin_amdgcn_mov_dpp(p.e, kCtrl, 0xF, 0xF, true);
+  return q;
+}
+
+__device__ __forceinline__ Pick readlane_pick(const Pick &p, int l) {
+  Pick q;
+  q.score = readlane_f64(p.score, l);
+  q.tp = __builtin_amdgcn_readlane(p.tp, l);
+  q.cell = __builtin_amdgcn_readlane(p.cell, l);
+  q.e = __builtin_amdgcn_readlane(p.e, l);
+  return q;
+}
+
+// Best pick of the wavefront (`better` is a strict total order on picks with
+// e >= 0, so the combination order does not matter): DPP steps within rows
+// of 16 lanes, then the four row winners.  The result is the same in every
+// lane.
+__device__ __forceinline__ Pick wave_best(Pick p) {
+  Pick q = dpp_pick<0xB1>(p);  // quad_perm [1, 0, 3, 2]
+  if (better(q, p)) p = q;
+  q = dpp_pick<0x4E>(p);  // quad_perm [2, 3, 0, 1]
+  if (better(q, p)) p = q;
+  q = dpp_pick<0x141>(p);  // row_half_mirror
+  if (better(q, p)) p = q;
+  q = dpp_pick<0x140>(p);  // row_mirror
+  if (better(q, p)) p = q;
+  Pick best = readlane_pick(p, 0);
+#pragma unroll
+  for (int r = 1; r < 4; ++r) {
+    q = readlane_pick(p, 16 * r);
+    if (better(q, best)) best = q;
+  }
+  return best;
+}
+
 // Z[g] = max_{a <= g} min(X[g - a], Y[a]) for one target g.
 __device__ __forceinline__ int conv_at(const int *X, const int *Y, int g) {
   int best = INT_MIN;
@@ -1414,15 +1455,7 @@ __global__ __launch_bounds__(256) void k_finalize_excl(const TileInfo *__restric
     }
     score[tile] = sc;
   }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    Pick other;
-    other.score = __shfl_xor(mine.score, off, kWave);
-    other.tp = __shfl_xor(mine.tp, off, kWave);
-    other.cell = __shfl_xor(mine.cell, off, kWave);
-    other.e = __shfl_xor(mine.e, off, kWave);
-    if (better(other, mine)) mine = other;
-  }
+  mine = wave_best(mine);
   if ((threadIdx.x & 63) == 0) s_pick[threadIdx.x >> 6] = mine;
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -1468,15 +1501,7 @@ __global__ __launch_bounds__(256) void k_pick_best(const TileInfo *__restrict__ 
     const Pick c{score[(size_t)o * E + e], tl.t, tl.cell, e};
     if (better(c, mine)) mine = c;
   }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    Pick other;
-    other.score = __shfl_xor(mine.score, off, kWave);
-    other.tp = __shfl_xor(mine.tp, off, kWave);
-    other.cell = __shfl_xor(mine.cell, off, kWave);
-    other.e = __shfl_xor(mine.e, off, kWave);
-    if (better(other, mine)) mine = other;
-  }
+  mine = wave_best(mine);
   if ((threadIdx.x & 63) == 0) s_pick[threadIdx.x >> 6] = mine;
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -1530,15 +1555,7 @@ __global__ __launch_bounds__(64) void k_finalize(DevProblem P, const CandInfo *_
     const Pick cand{sc, ci.tp, ci.cell, e};
     if (better(cand, mine)) mine = cand;
   }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    Pick other;
-    other.score = __shfl_xor(mine.score, off, kWave);
-    other.tp = __shfl_xor(mine.tp, off, kWave);
-    other.cell = __shfl_xor(mine.cell, off, kWave);
-    other.e = __shfl_xor(mine.e, off, kWave);
-    if (better(other, mine)) mine = other;
-  }
+  mine = wave_best(mine);
   if (lane == 0 && best) best[o] = mine.e;
 }
 
