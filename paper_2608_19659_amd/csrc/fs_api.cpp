@@ -92,11 +92,12 @@ fs_status make_problem(const fs_problem *p, fs::DevProblem *P) {
 }
 
 struct DeviceGuard {
-  int prev = -1;
+  int prev = -1;  // device to restore (-1: none, already current)
   hipError_t err = hipSuccess;
   explicit DeviceGuard(int dev) {
     err = hipGetDevice(&prev);
-    if (err == hipSuccess) err = hipSetDevice(dev);
+    if (err == hipSuccess && prev == dev) prev = -1;
+    else if (err == hipSuccess) err = hipSetDevice(dev);
   }
   ~DeviceGuard() {
     if (prev >= 0) (void)hipSetDevice(prev);

@@ -266,36 +266,50 @@ class ScoreOutput:
     tau_dump: object  # [O, E, S, 2] float32 or None
 
 
+class ScorePlan:
+    """One fs_score_candidates call with its arguments checked and
+    marshalled once.  run() enqueues the call again on the same device
+    buffers (whose contents may change between runs); every run executes the
+    whole scoring path on the GPU.  iv holds [O, N] device tensors, cand an
+    int32 [E] device tensor, cap_s / tail_s float32 [O, E, S] device tensors."""
+
+    def __init__(self, ctx: Context, problem, iv: DeviceIntervals, cand, cap_s, tail_s, dump: bool = False,
+                 stream=None, workspace=None, out: ScoreOutput | None = None):
+        torch = _torch()
+        self._ref = _ProblemRef(problem)
+        O = int(iv.cap_lo.shape[0])
+        E = int(cand.shape[0])
+        S = int(cap_s.shape[2]) if E > 0 else 0
+        dev = iv.cap_lo.device
+        self._ivs = _intervals_struct(iv, O, self._ref.N)
+        pcand = _dev_ptr(cand, torch.int32, (E,), "cand")
+        pcs = _dev_ptr(cap_s, torch.float32, (O, E, S), "cap_s")
+        pts = _dev_ptr(tail_s, torch.float32, (O, E, S), "tail_s")
+        if out is None:
+            out = ScoreOutput(torch.empty((O, E), dtype=torch.float64, device=dev),
+                              torch.empty(O, dtype=torch.float64, device=dev),
+                              torch.empty(O, dtype=torch.int32, device=dev),
+                              torch.empty((O, E, S, 2), dtype=torch.float32, device=dev) if dump else None)
+        ws_bytes = workspace_size(problem, O, E, S)
+        ws = workspace if workspace is not None else ctx.workspace(ws_bytes)
+        self.out, self._ws, self._keep = out, ws, (iv, cand, cap_s, tail_s)
+        self._fn = load_library().fs_score_candidates
+        self._args = (ctx.handle, self._ref.ptr, self._ivs, O, pcand, E, pcs, pts, S,
+                      _dev_ptr(out.score, torch.float64, (O, E), "score"),
+                      _dev_ptr(out.gap_now, torch.float64, (O,), "gap_now"),
+                      _dev_ptr(out.best, torch.int32, (O,), "best"),
+                      _dev_ptr(out.tau_dump, torch.float32, (O, E, S, 2), "tau_dump"),
+                      ws.data_ptr(), ws.numel(), _stream(dev, stream))
+
+    def run(self) -> ScoreOutput:
+        _check(self._fn(*self._args))
+        return self.out
+
+
 def score_candidates(ctx: Context, problem, iv: DeviceIntervals, cand, cap_s, tail_s, dump: bool = False,
                      stream=None, workspace=None, out: ScoreOutput | None = None) -> ScoreOutput:
-    """Acquisition scores (fs_score_candidates).  iv holds [O, N] device
-    tensors, cand an int32 [E] device tensor, cap_s / tail_s float32
-    [O, E, S] device tensors."""
-    torch = _torch()
-    ref = _ProblemRef(problem)
-    O = int(iv.cap_lo.shape[0])
-    E = int(cand.shape[0])
-    S = int(cap_s.shape[2]) if E > 0 else 0
-    dev = iv.cap_lo.device
-    ivs = _intervals_struct(iv, O, ref.N)
-    pcand = _dev_ptr(cand, torch.int32, (E,), "cand")
-    pcs = _dev_ptr(cap_s, torch.float32, (O, E, S), "cap_s")
-    pts = _dev_ptr(tail_s, torch.float32, (O, E, S), "tail_s")
-    if out is None:
-        out = ScoreOutput(torch.empty((O, E), dtype=torch.float64, device=dev),
-                          torch.empty(O, dtype=torch.float64, device=dev),
-                          torch.empty(O, dtype=torch.int32, device=dev),
-                          torch.empty((O, E, S, 2), dtype=torch.float32, device=dev) if dump else None)
-    ws_bytes = workspace_size(problem, O, E, S)
-    ws = workspace if workspace is not None else ctx.workspace(ws_bytes)
-    _check(load_library().fs_score_candidates(
-        ctx.handle, ref.ptr, ivs, O, pcand, E, pcs, pts, S,
-        _dev_ptr(out.score, torch.float64, (O, E), "score"),
-        _dev_ptr(out.gap_now, torch.float64, (O,), "gap_now"),
-        _dev_ptr(out.best, torch.int32, (O,), "best"),
-        _dev_ptr(out.tau_dump, torch.float32, (O, E, S, 2), "tau_dump"),
-        ws.data_ptr(), ws.numel(), _stream(dev, stream)))
-    return out
+    """Acquisition scores (fs_score_candidates), one call."""
+    return ScorePlan(ctx, problem, iv, cand, cap_s, tail_s, dump, stream, workspace, out).run()
 
 
 @dataclass
