@@ -37,6 +37,8 @@ DIV_OPS = 3
 PROFILE_GLOB = os.path.join(ROOT, "profiles")
 # Issue slots of one (max,min) pair: two pairs take v_min, v_min, v_max3.
 PAIR_SLOTS = 1.5
+# Back-to-back scorer launches per event pair in the kernel-duration pass.
+TIMING_REPEATS = 10
 
 
 def lane_work_per_scenario(problem, bmap_exists) -> float:
@@ -166,8 +168,6 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="wall budget of the oracle baseline")
     ap.add_argument("--spl", type=int, default=0,
                     help="exclusion scorer samples per lane (4, 8, 16; 0 = library default)")
-    ap.add_argument("--cpw", type=int, default=0,
-                    help="exclusion scorer sample chunks per work item (1, 2, 4, 8; 0 = library default)")
     ap.add_argument("--waves", type=int, default=0,
                     help="exclusion scorer grid in wavefronts (0 = library default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -208,7 +208,6 @@ def main():
     cand, cap_s, tail_s = t(w.cand), t(w.cap_s), t(w.tail_s)
     ctx = fs.Context(0)
     ctx.set_option(fs.OPT_SAMPLES_PER_LANE, args.spl)
-    ctx.set_option(fs.OPT_CHUNKS_PER_WAVE, args.cpw)
     ctx.set_option(fs.OPT_SCORER_WAVES, args.waves)
     out = fs.ScoreOutput(torch.empty((O, E), dtype=torch.float64, device=dev),
                          torch.empty(O, dtype=torch.float64, device=dev),
@@ -222,9 +221,10 @@ def main():
 
     def run(kernel, steps, warmup):
         """Time `steps` whole steps (set-up, scorer, finalize) with no timing
-        markers in the stream, then the same number of steps again with a
-        pair of HIP events around every scorer launch (the events add host and
-        queue work of their own, so the step time comes from the first pass)."""
+        markers in the stream; then the same number of steps again, each with
+        TIMING_REPEATS back-to-back launches of the scorer between a pair of
+        HIP events, for the scorer's mean launch duration (an event pair
+        around a single launch would add its own queue work to the span)."""
         ctx.set_score_kernel(kernel)
         ctx.set_option(fs.OPT_KERNEL_TIMING, 0)
         plan = fs.ScorePlan(ctx, p, iv, cand, cap_s, tail_s, out=out, workspace=ws, stream=stream)
@@ -239,7 +239,7 @@ def main():
         ev1.record(stream)
         torch.cuda.synchronize()
         ms_per_step = ev0.elapsed_time(ev1) / steps
-        ctx.set_option(fs.OPT_KERNEL_TIMING, 1)
+        ctx.set_option(fs.OPT_KERNEL_TIMING, TIMING_REPEATS)
         ctx.kernel_timing()  # nothing pending
         for _ in range(steps):
             plan.run()

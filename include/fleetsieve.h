@@ -119,18 +119,15 @@ typedef enum fs_option {
    * 3 = exclusion scorer: per-order all-but-one tables, O(replica range) per
    *     scenario (no floors).  All give identical bits. */
   FS_OPT_SCORE_KERNEL = 1,
-  /* 1 = record a pair of HIP events on the caller's stream around every
-   * launch of the scoring kernel (the per-scenario solve), for
-   * fs_context_kernel_timing; 0 = off (default). */
+  /* n in [1, 64]: in every scoring call, launch the scoring kernel (the
+   * per-scenario solves) n times back to back between a pair of HIP events
+   * on the caller's stream, for fs_context_kernel_timing.  The kernel is
+   * idempotent, so the outputs are those of one launch.  0 = off (default). */
   FS_OPT_KERNEL_TIMING = 2,
   /* Exclusion scorer (kernel 3): samples each lane handles, 4, 8 or 16
    * (0 = library default).  A launch-shape tuning knob; results are
    * identical for every value. */
   FS_OPT_SAMPLES_PER_LANE = 3,
-  /* Exclusion scorer: consecutive sample chunks of one tile in each work
-   * item, 1, 2, 4 or 8 (0 = library default).  A launch-shape tuning knob;
-   * results are identical for every value. */
-  FS_OPT_CHUNKS_PER_WAVE = 4,
   /* Exclusion scorer: wavefronts of its fixed grid, which stride over the
    * work items, in [1, 2^20] (0 = library default).  A launch-shape tuning
    * knob; results are identical for every value. */
@@ -144,8 +141,8 @@ void fs_context_destroy(fs_context *ctx);
 fs_status fs_context_set_option(fs_context *ctx, fs_option option, int64_t value);
 
 /* Waits for the events recorded under FS_OPT_KERNEL_TIMING, returns the
- * summed scoring-kernel time in milliseconds and the number of launches
- * timed, and forgets them. */
+ * summed time between each event pair in milliseconds and the number of
+ * scoring-kernel launches they enclose, and forgets them. */
 fs_status fs_context_kernel_timing(fs_context *ctx, double *total_ms, int64_t *launches);
 
 /* Thread-local description of the last failure in this thread. */
@@ -183,7 +180,10 @@ fs_status fs_solve_batch(fs_context *ctx, const fs_problem *p, const float *d_ca
  *   d_gap_now [n_orders] binary64 (may be NULL)
  *   d_best    [n_orders] int32 (may be NULL)
  *   d_tau_dump NULL or [n_orders][n_cand][n_samples][2] = (tau-, tau+); for a
- *             measured candidate it holds the order's base values. */
+ *             measured candidate it holds the order's base values.
+ * Limits: n_orders and n_cand in [0, 65535], n_samples in [1, 2^20]; the
+ * exclusion scorer (kernel 3) also needs n_orders * n_cand < 2^31 and
+ * returns FS_ERR_UNSUPPORTED otherwise. */
 fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals iv,
                               int32_t n_orders, const int32_t *d_cand, int32_t n_cand,
                               const float *d_cap_s, const float *d_tail_s, int32_t n_samples,

@@ -3,6 +3,7 @@
 // launches on the caller's stream.
 #include "fleetsieve.h"
 
+#include <climits>
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -16,11 +17,14 @@
 struct fs_context {
   int device;
   int score_kernel;  // 0 auto, 1 wave per scenario, 2 lane per scenario, 3 exclusion
-  int timing;        // record events around the scoring kernel
+  int timing;        // back-to-back scoring-kernel launches between timing events (0 = off)
   int spl;           // exclusion scorer samples per lane (0 = default)
-  int cpw;           // exclusion scorer sample chunks per work item (0 = default)
   int waves;         // exclusion scorer grid in wavefronts (0 = default)
-  std::vector<std::pair<hipEvent_t, hipEvent_t>> events;
+  struct Timed {
+    hipEvent_t begin, end;
+    int launches;
+  };
+  std::vector<Timed> events;
 };
 
 namespace {
@@ -140,15 +144,15 @@ fs_status fs_context_create(int hip_device, fs_context **out) {
   if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
   if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
     return fail(FS_ERR_UNSUPPORTED, std::string("libfleetsieve is built for gfx950, device is ") + prop.gcnArchName);
-  *out = new fs_context{hip_device, 0, 0, 0, 0, 0, {}};
+  *out = new fs_context{hip_device, 0, 0, 0, 0, {}};
   return FS_OK;
 }
 
 void fs_context_destroy(fs_context *ctx) {
   if (!ctx) return;
   for (auto &ev : ctx->events) {
-    (void)hipEventDestroy(ev.first);
-    (void)hipEventDestroy(ev.second);
+    (void)hipEventDestroy(ev.begin);
+    (void)hipEventDestroy(ev.end);
   }
   delete ctx;
 }
@@ -156,17 +160,19 @@ void fs_context_destroy(fs_context *ctx) {
 fs_status fs_context_kernel_timing(fs_context *ctx, double *total_ms, int64_t *launches) {
   if (!ctx || !total_ms || !launches) return fail(FS_ERR_INVALID_ARGUMENT, "NULL argument");
   double sum = 0.0;
+  int64_t n = 0;
   hipError_t err = hipSuccess;
   for (auto &ev : ctx->events) {
     float ms = 0.0f;
-    hipError_t e = hipEventSynchronize(ev.second);
-    if (e == hipSuccess) e = hipEventElapsedTime(&ms, ev.first, ev.second);
+    hipError_t e = hipEventSynchronize(ev.end);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, ev.begin, ev.end);
     if (e != hipSuccess && err == hipSuccess) err = e;
     sum += ms;
-    (void)hipEventDestroy(ev.first);
-    (void)hipEventDestroy(ev.second);
+    n += ev.launches;
+    (void)hipEventDestroy(ev.begin);
+    (void)hipEventDestroy(ev.end);
   }
-  *launches = (int64_t)ctx->events.size();
+  *launches = n;
   *total_ms = sum;
   ctx->events.clear();
   if (err != hipSuccess) return hip_fail(err, "kernel timing");
@@ -186,12 +192,6 @@ fs_status fs_context_set_option(fs_context *ctx, fs_option option, int64_t value
     ctx->spl = (int)value;
     return FS_OK;
   }
-  if (option == FS_OPT_CHUNKS_PER_WAVE) {
-    if (value != 0 && value != 1 && value != 2 && value != 4 && value != 8)
-      return fail(FS_ERR_INVALID_ARGUMENT, "chunks per work item must be 0, 1, 2, 4 or 8");
-    ctx->cpw = (int)value;
-    return FS_OK;
-  }
   if (option == FS_OPT_SCORER_WAVES) {
     if (value < 0 || value > (1 << 20))
       return fail(FS_ERR_INVALID_ARGUMENT, "scorer wavefronts must be in [0, 2^20]");
@@ -199,7 +199,7 @@ fs_status fs_context_set_option(fs_context *ctx, fs_option option, int64_t value
     return FS_OK;
   }
   if (option == FS_OPT_KERNEL_TIMING) {
-    if (value < 0 || value > 1) return fail(FS_ERR_INVALID_ARGUMENT, "kernel timing must be 0 or 1");
+    if (value < 0 || value > 64) return fail(FS_ERR_INVALID_ARGUMENT, "kernel timing must be in [0, 64]");
     ctx->timing = (int)value;
     return FS_OK;
   }
@@ -281,6 +281,8 @@ fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals
                 "lane-per-scenario scoring needs no floors, TP set {1,2,4,8} and budget 16, 32 or 64");
   if (kernel == 3 && !fs::excl_kernel_supported(P))
     return fail(FS_ERR_UNSUPPORTED, "exclusion scoring does not handle critical floors");
+  if (kernel == 3 && (int64_t)n_orders * n_cand > INT32_MAX)
+    return fail(FS_ERR_UNSUPPORTED, "exclusion scoring needs n_orders * n_cand < 2^31");
   const int32_t S = n_cand > 0 ? n_samples : 0;
   const fs::WsLayout L = fs::ws_layout(P, n_orders, n_cand, S);
   if (!d_workspace) return fail(FS_ERR_INVALID_ARGUMENT, "workspace is NULL");
@@ -310,12 +312,13 @@ fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals
   }
   fs::ScoreArgs a{iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi, iv.measured, d_cand, d_cap_s, d_tail_s,
                   n_orders, n_cand, S, d_score, d_gap_now, d_best, d_tau_dump, ws, L, kernel,
-                  ctx->spl, ctx->cpw, ctx->waves, nullptr, nullptr};
+                  ctx->spl, ctx->waves, nullptr, nullptr, 1};
   if (ctx->timing && n_cand > 0) {
     e = hipEventCreate(&a.ev_begin);
     if (e == hipSuccess) e = hipEventCreate(&a.ev_end);
     if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
-    ctx->events.emplace_back(a.ev_begin, a.ev_end);
+    a.timing_launches = ctx->timing;
+    ctx->events.push_back({a.ev_begin, a.ev_end, ctx->timing});
   }
   e = fs::launch_score(P, a, stream);
   if (e != hipSuccess) return hip_fail(e, "score launch");

@@ -67,8 +67,8 @@ struct WsLayout {
   size_t tabB;       // int32 [O][2][K][3][K][G] set-up tables when LDS is too small
   size_t mopt;       // int32 [O][2][K*P] M = H[G - t*r] of every option (class, TP, r)
   size_t thr;        // float [O][2][K*P] capacity threshold of every option
-  size_t list;       // int4 [O][E] live tiles of each order, longest replica range first
-  size_t live;       // int32 [O] number of live tiles of each order
+  size_t list;       // int4 [O * E] live tiles of every order, longest replica range first
+  size_t live;       // int32 [1] number of listed tiles
   size_t flag;     // int32 [4]        validation / error flags
   size_t total;
   int64_t n_partial;  // ceil(S / 64)
@@ -97,9 +97,9 @@ struct ScoreArgs {
   WsLayout L;
   int kernel;  // 1 = wave per scenario, 2 = lane per scenario, 3 = exclusion
   int spl;     // exclusion scorer: samples per lane (4, 8 or 16; 0 = default)
-  int cpw;     // exclusion scorer: sample chunks per work item (1, 2, 4, 8; 0 = default)
   int waves;   // exclusion scorer: wavefronts of its grid (0 = default)
-  hipEvent_t ev_begin, ev_end;  // recorded around the scoring kernel if set
+  hipEvent_t ev_begin, ev_end;  // recorded around the scoring kernel launches if set
+  int timing_launches;          // back-to-back launches of the scoring kernel between the events
 };
 
 struct AllocOut {

@@ -81,6 +81,21 @@ __device__ __forceinline__ int wave_scan_max(int v, int lane) {
   return v;
 }
 
+// Inclusive prefix sum across the 64 lanes by DPP: shifts by 1, 2, 4, 8
+// within each row of 16 lanes (lanes with no source add 0), then the last
+// lane of row 0 is added to row 1 and of row 2 to row 3 (row_bcast:15), and
+// the last lane of row 1 (the total of rows 0-1) to rows 2 and 3
+// (row_bcast:31).
+__device__ __forceinline__ int wave_scan_add(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return v;
+}
+
 // One DPP lane permutation of a binary64 value (both halves moved alike).
 template <int kCtrl>
 __device__ __forceinline__ double dpp_f64(double v) {
@@ -800,66 +815,89 @@ __device__ __forceinline__ void cell_range(const DevProblem &P, int cell, int *r
   *rhi = b == 0 ? rmax : first_r_at_most(demand, lb1, rmax) - 1;
 }
 
-// Work list of one order (the set-up's extra block per order): the tiles the
-// scorer visits -- unrevealed candidates with a nonempty replica range, or
-// every valid candidate when dumping -- as self-contained entries (candidate,
-// option offset, rlo | nr << 16, class | state << 8), longest range first
-// (bucketed by bit length), then end markers.  Also the records of invalid
-// candidates.  Depends only on the problem and the revealed flags.
-__device__ void prep_list(const DevProblem &P, int o, const uint8_t *__restrict__ measured,
+// The scorer's work list (built by one extra block of the set-up): every
+// tile the scorer visits -- unrevealed (order, candidate) pairs with a
+// nonempty replica range, or every valid pair when dumping -- over all
+// orders, longest range first (bucketed by bit length), then end markers up
+// to O x E entries.  An entry is self-contained: (candidate, option offset
+// of rlo, rlo | nr << 16, class | state << 6 | order << 8).  Also the tile
+// records of invalid candidates.  Depends only on the problem and the
+// revealed flags.  The order of entries within a bucket is arbitrary (it
+// decides only which wavefront evaluates a tile).
+__device__ void prep_list(const DevProblem &P, int O, const uint8_t *__restrict__ measured,
                           const int32_t *__restrict__ cand, int E, int dump, int PPc, const PrepConsts &C,
-                          TileInfo *__restrict__ tiles, int4 *__restrict__ list,
-                          int32_t *__restrict__ live_count, int *bucket_count, int *bucket_start, int *n_live) {
+                          TileInfo *__restrict__ tiles, int4 *__restrict__ list, int32_t *__restrict__ n_listed,
+                          int *bucket_count, int *bucket_start, int *n_live) {
   const int tid = threadIdx.x, nth = blockDim.x, lane = tid & (kWave - 1);
   const int N = P.N, per_class = P.NT * P.B;
-  const size_t off = (size_t)o * N;
-  for (int e = tid; e < E; e += nth) {
-    const int cell = cand[e];
-    if (cell < 0 || cell >= N) {
-      TileInfo *tl = tiles + (size_t)o * E + e;
-      tl->state = -1; tl->cell = cell; tl->cls = 0; tl->t = 0; tl->rlo = 1; tl->rhi = 0;
-      tl->toff = 0; tl->u_m = 0; tl->u_p = 0;
-      continue;
+  // Threads work candidate by candidate (the replica range is computed once
+  // per candidate); when there are fewer candidates than threads, g threads
+  // share a candidate and take every g-th order.  The revealed flags of a
+  // candidate's orders are independent loads.
+  const int g = E < nth ? nth / E : 1;
+  const int sub = E < nth ? tid / E : 0;
+  const int e_first = E < nth ? tid - sub * E : tid, e_step = E < nth ? E : nth;
+  const bool active = sub < g;
+  for (int pass = 0; pass < 2; ++pass) {
+    for (int e = e_first; active && e < E; e += e_step) {
+      const int cell = cand[e];
+      if (cell < 0 || cell >= N) {
+        if (pass == 0) {
+          for (int o = sub; o < O; o += g) {
+            TileInfo *tl = tiles + (size_t)o * E + e;
+            tl->state = -1; tl->cell = cell; tl->cls = 0; tl->t = 0; tl->rlo = 1; tl->rhi = 0;
+            tl->toff = 0; tl->u_m = 0; tl->u_p = 0;
+          }
+        }
+        continue;
+      }
+      int rlo, rhi;
+      cell_range(P, cell, &rlo, &rhi);
+      const int nr = rhi >= rlo ? rhi - rlo + 1 : 0;
+      if (!dump && nr == 0) continue;  // never visited
+      const int b = range_bucket(nr);
+      // this thread's listed tiles of candidate e
+      int n = 0;
+#pragma unroll 8
+      for (int o = sub; o < O; o += g) n += (dump || !measured[(size_t)o * N + cell]) ? 1 : 0;
+      if (n == 0) continue;
+      if (pass == 0) {
+        atomicAdd(&bucket_count[b], n);
+      } else {
+        int at = atomicAdd(&bucket_start[b], n);
+        const int k = cell / per_class, ti = (cell / P.B) % P.NT, r0 = nr > 0 ? rlo : 1;
+        const int toff = k * PPc + C.optoff[ti] + r0 - 1;
+        for (int o = sub; o < O; o += g) {
+          const bool meas = measured[(size_t)o * N + cell] != 0;
+          if (dump || !meas) list[at++] = make_int4(e, toff, r0 | (nr << 16), k | ((meas ? 1 : 0) << 6) | (o << 8));
+        }
+      }
     }
-    int rlo, rhi;
-    cell_range(P, cell, &rlo, &rhi);
-    const int nr = rhi >= rlo ? rhi - rlo + 1 : 0;
-    if (dump || (!measured[off + cell] && nr > 0)) atomicAdd(&bucket_count[range_bucket(nr)], 1);
-  }
-  __syncthreads();
-  if (tid < kWave) {
-    const int cnt = lane < 32 ? bucket_count[lane] : 0;
-    int incl = cnt;
+    __syncthreads();
+    if (pass == 0) {
+      if (tid < kWave) {
+        const int cnt = lane < 32 ? bucket_count[lane] : 0;
+        int incl = cnt;
 #pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-      const int u = __shfl_up(incl, d, kWave);
-      if (lane >= d) incl += u;
-    }
-    if (lane < 32) bucket_start[lane] = incl - cnt;
-    if (lane == 31) {
-      live_count[o] = incl;
-      *n_live = incl;
-    }
-  }
-  __syncthreads();
-  for (int e = tid; e < E; e += nth) {
-    const int cell = cand[e];
-    if (cell < 0 || cell >= N) continue;
-    int rlo, rhi;
-    cell_range(P, cell, &rlo, &rhi);
-    const int nr = rhi >= rlo ? rhi - rlo + 1 : 0;
-    const bool meas = measured[off + cell] != 0;
-    if (dump || (!meas && nr > 0)) {
-      const int k = cell / per_class, ti = (cell / P.B) % P.NT, r0 = nr > 0 ? rlo : 1;
-      const int4 ent = make_int4(e, k * PPc + C.optoff[ti] + r0 - 1, r0 | (nr << 16), k | ((meas ? 1 : 0) << 8));
-      list[(size_t)o * E + atomicAdd(&bucket_start[range_bucket(nr)], 1)] = ent;
+        for (int d = 1; d < kWave; d <<= 1) {
+          const int u = __shfl_up(incl, d, kWave);
+          if (lane >= d) incl += u;
+        }
+        if (lane < 32) bucket_start[lane] = incl - cnt;
+        if (lane == 31) {
+          *n_listed = incl;
+          *n_live = incl;
+        }
+      }
+      __syncthreads();
     }
   }
-  for (int z = *n_live + tid; z < E; z += nth) list[(size_t)o * E + z] = make_int4(-1, 0, 0, 0);
+  for (int z = *n_live + tid; z < O * E; z += nth) list[z] = make_int4(-1, 0, 0, 0);
 }
 
 // Set-up of the exclusion scorer, one block per (realisation R, order o,
-// class i) plus one work-list block per order (i = K); R = 0 is the
+// class i), plus blocks with i = K of which (R = 0, o = 0) builds the work
+// list of every order and the others return at once; R = 0 is the
 // conservative corner (low capacity, high tail) and R = 1 the optimistic one
 // (Section 4.1).  Tables over g in [0, G) (G itself is never read):
 //   B_k[g]  best ratio of class k with at most g GPUs (nondecreasing)
@@ -884,7 +922,7 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
                                              int32_t *__restrict__ gtab, TileInfo *__restrict__ tiles,
                                              int32_t *__restrict__ base, int32_t *__restrict__ mopt,
                                              float *__restrict__ thr, int32_t n_thr,
-                                             int4 *__restrict__ list, int32_t *__restrict__ live_count) {
+                                             int4 *__restrict__ list, int32_t *__restrict__ n_listed) {
   extern __shared__ int lds[];
   __shared__ PrepConsts C;
   __shared__ int bucket_count[32], bucket_start[32], n_live;
@@ -903,12 +941,12 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
     }
     C.optoff[NT] = at;
   }
-  if (ci == K) {  // the work-list block of order o
-    if (R != 0) return;
+  if (ci == K) {  // one block builds the work list of every order
+    if (R != 0 || o != 0) return;
     if (tid < 32) bucket_count[tid] = 0;
     __syncthreads();
-    prep_list(P, o, measured, cand, E, dump, PPc, C, tiles, list, live_count, bucket_count, bucket_start,
-              &n_live);
+    prep_list(P, (int)gridDim.y, measured, cand, E, dump, PPc, C, tiles, list, n_listed, bucket_count,
+              bucket_start, &n_live);
     return;
   }
   float *ccap = (float *)lds;                // [N]
@@ -1118,21 +1156,9 @@ __device__ __forceinline__ int sampled_quotient(float rf, float cs, double rcp) 
 // crossing search.
 constexpr int kScanMax = 8;
 
-// Scenarios of the exclusion scorer.  The work items are (order, live tile,
-// group of CPW consecutive chunks of 64 x SPL samples); item it has
-// z = it / (O * groups) -- the tile's place in its order's heavy-first list
-// -- then the order, then the group, so the longest replica ranges of every
-// order come first.  A fixed grid of single-wavefront blocks strides over the
-// items.  Lane l owns samples [chunk * 64 * SPL + l * SPL, +SPL) of each
-// chunk, and the next chunk's samples are loaded while the current one is
-// evaluated.  Each chunk's sum is written as one partial (a node of the
-// pairwise tree over s).
-//
-// Per realisation, tau = max(U, max_r min(f_r, M_r)) with M_r = H[G - t*r].
-// Short replica ranges are scanned.  For long ones: f_r is nondecreasing in r
-// and M_r nonincreasing, so min(f_r, M_r) rises while f_r < M_r and falls
-// after; with r* the first r where f_r >= M_r -- the first r whose capacity
-// threshold the sample reaches -- the maximum is max(f_{r*-1}, M_{r*}).
+// Default grid of the exclusion scorer: four wavefronts per SIMD (1024 SIMDs).
+constexpr int kScorerWaves = 4096;
+
 // Samples of one chunk.  VEC (S a multiple of 4): each group of 4 samples
 // of a lane lies wholly below S or wholly past it; every group is fetched by
 // one 16-byte load at an in-bounds address (a group past S reads the tile's
@@ -1141,7 +1167,7 @@ constexpr int kScanMax = 8;
 // predicated per sample.
 template <int SPL, bool VEC>
 __device__ __forceinline__ void load_chunk(const float *__restrict__ cap_s, const float *__restrict__ tail_s,
-                                           size_t tbase, int s_first, int S, float (&cs)[SPL],
+                                           size_t tbase, int s_first, int S, bool live, float (&cs)[SPL],
                                            float (&ls)[SPL]) {
   if constexpr (VEC) {
 #pragma unroll
@@ -1155,232 +1181,313 @@ __device__ __forceinline__ void load_chunk(const float *__restrict__ cap_s, cons
   } else {
 #pragma unroll
     for (int q = 0; q < SPL; ++q) {
-      const bool live = s_first + q < S;
-      cs[q] = live ? cap_s[tbase + s_first + q] : 0.0f;
-      ls[q] = live ? tail_s[tbase + s_first + q] : 0.0f;
+      const bool in = live && s_first + q < S;
+      cs[q] = in ? cap_s[tbase + s_first + q] : 0.0f;
+      ls[q] = in ? tail_s[tbase + s_first + q] : 0.0f;
     }
   }
 }
 
-// Work-list entry of a tile (written by the set-up): candidate e (-1 past the
-// end of the order's list), option offset of rlo, rlo | nr << 16, and
-// class | state << 8.
-constexpr int kScorerWavesPerBlock = 1;
+// Everything one work item reads: its work-list entry, the lane's samples,
+// U of both realisations, and M and the capacity threshold of option
+// rlo + min(lane, nr - 1) of both realisations (a scan reads M lane by lane,
+// the crossing search looks both up across lanes).
+template <int SPL>
+struct ScoreItem {
+  int4 ent;
+  float cs[SPL], ls[SPL];
+  int u0, u1;
+  int vm0, vm1;
+  float vt0, vt1;
+};
 
-template <int SPL, int CPW, bool VEC>
-__global__ __launch_bounds__(64 * kScorerWavesPerBlock) void k_score_excl(
+// Value of lane idx (0 <= idx < 64) of v, per lane.
+__device__ __forceinline__ int lane_lookup(int v, int idx) { return __builtin_amdgcn_ds_bpermute(idx << 2, v); }
+
+// Scenarios of the exclusion scorer.  A work item is one chunk of 64 x SPL
+// samples of one live tile; items are numbered over the live tiles only, so
+// every wavefront gets the same number of items to within one, and the
+// chunks of one tile are neighbours.  Each wavefront of the grid takes the
+// items it, it + W, it + 2W, ... (W wavefronts) and runs them as a
+// two-stage pipeline: the list entry of the
+// item after next, then the samples and constants of the next item, are in
+// flight while the current item is evaluated.  All of these are vector loads
+// at unconditional (clamped) addresses, so each wait covers exactly the item
+// it is for; the per-class constants sit in LDS.  Lane l owns samples
+// [c * 64 * SPL + l * SPL, + SPL) of the item's tile, and the chunk's sum
+// is written as one partial (a node of the pairwise tree over s).
+//
+// Per realisation, tau = max(U, max_r min(f_r, M_r)) with M_r = H[G - t*r].
+// Ranges of at most kScanMax replica counts are scanned.  For longer ones:
+// f_r is nondecreasing in r and M_r nonincreasing, so min(f_r, M_r) rises
+// while f_r < M_r and falls after; with r* the first r where f_r >= M_r --
+// the first r whose capacity threshold the sample reaches -- the maximum is
+// max(f_{r*-1}, M_{r*}).
+template <int SPL, bool VEC, bool DUMP>
+__global__ __launch_bounds__(64) void k_score_excl(
     DevProblem P, const TileInfo *__restrict__ tiles, const int32_t *__restrict__ mopt,
     const float *__restrict__ thr, int32_t n_thr, const int4 *__restrict__ list,
-    const int32_t *__restrict__ live_count, const float *__restrict__ cap_s, const float *__restrict__ tail_s,
-    int32_t O, int32_t E, int32_t S, const int32_t *__restrict__ base, double *__restrict__ partial,
-    int64_t n_partial, float *__restrict__ tau_dump, int32_t lds_per_wave) {
+    const float *__restrict__ cap_s, const float *__restrict__ tail_s, int32_t O, int32_t E, int32_t S,
+    const int32_t *__restrict__ base, double *__restrict__ partial, int32_t n_chunk,
+    float *__restrict__ tau_dump) {
   constexpr int CHUNK = 64 * SPL;
   extern __shared__ int lds[];
-  // the wavefront index is uniform: keep it (and all item bookkeeping) scalar
-  const int lane = threadIdx.x & (kWave - 1), wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  int *Mlds = lds + wave * lds_per_wave;
-  const int64_t workers = (int64_t)gridDim.x * kScorerWavesPerBlock;
-  const int groups = (int)((n_partial + CPW - 1) / CPW);
-  const int64_t per_z = (int64_t)O * groups;
-  // list entries are the same for every lane: keep them in scalar registers
+  const int lane = threadIdx.x;
+  // per-class constants in LDS; then, for ranges longer than a wavefront, M
+  // and the thresholds of the range
+  double *c_rcp = reinterpret_cast<double *>(lds);
+  float *c_slo = reinterpret_cast<float *>(c_rcp + P.K);
+  int *Mlds = reinterpret_cast<int *>(c_slo + P.K);
+  for (int k = lane; k < P.K; k += kWave) {
+    c_rcp[k] = P.rcp_demand[k];
+    c_slo[k] = P.slo[k];
+  }
+  wave_lds_fence();
+  // An opaque zero added to every address below: the loads stay vector
+  // loads.  (Scalar loads complete out of order, so a wait for any LDS
+  // result would also wait for every scalar load in flight, including the
+  // next item's.)
+  int vz;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(vz));
+  const int W = (int)gridDim.x;
+  // Item it = j * n_chunk + c: chunk c of the tile in place j of the work
+  // list (every order's live tiles, longest replica range first), so the
+  // wavefronts' first items are the heaviest.
+  struct Pos { int64_t j; int c; };
+  const int64_t n_list = (int64_t)O * E;
+  const int step_j = W / n_chunk, step_c = W - step_j * n_chunk;
+  auto advance = [&](Pos q) {
+    q.j += step_j;
+    q.c += step_c;
+    if (q.c >= n_chunk) { q.c -= n_chunk; ++q.j; }
+    return q;
+  };
   auto uniform4 = [](int4 v) {
     return make_int4(__builtin_amdgcn_readfirstlane(v.x), __builtin_amdgcn_readfirstlane(v.y),
                      __builtin_amdgcn_readfirstlane(v.z), __builtin_amdgcn_readfirstlane(v.w));
   };
-  // Item it is (z, o, g) with it = (z * O + o) * groups + g: place z in the
-  // order's list, order o, chunk group g.  A wavefront's items are `workers`
-  // apart, so the triple advances by a fixed step with carries (divisions
-  // only at start).
-  struct Pos { int z, o, g; };
-  auto split = [&](int64_t it) {
-    Pos q;
-    q.z = (int)(it / per_z);
-    const int64_t rem = it - (int64_t)q.z * per_z;
-    q.o = (int)(rem / groups);
-    q.g = (int)(rem - (int64_t)q.o * groups);
-    return q;
+  auto list_at = [&](const Pos &p) { return list[(p.j < n_list ? p.j : 0) + vz]; };
+  // Issues the loads of an item whose list entry is known.  Items without a
+  // tile read one line at the start of the arrays instead.
+  auto issue = [&](ScoreItem<SPL> &X, const Pos &p) {
+    const int4 en = X.ent;
+    const bool live = en.x >= 0;
+    const int nr = en.z >> 16, o = en.w >> 8;
+    const size_t tile = live ? (size_t)o * E + en.x : 0;
+    load_chunk<SPL, VEC>(cap_s, tail_s, tile * S, live ? p.c * CHUNK + lane * SPL : 0, S, live, X.cs, X.ls);
+    const size_t row0 = live ? (size_t)o * 2 * n_thr : 0, row1 = live ? row0 + n_thr : 0;
+    const int toff = live ? en.y : 0;
+    const int2 u = *reinterpret_cast<const int2 *>(&tiles[tile + vz].u_m);
+    X.u0 = u.x;
+    X.u1 = u.y;
+    const int at = toff + (live && nr > 0 ? min(lane, nr - 1) : 0);
+    X.vm0 = mopt[row0 + at];
+    X.vm1 = mopt[row1 + at];
+    X.vt0 = thr[row0 + at];
+    X.vt1 = thr[row1 + at];
   };
-  const Pos step = split(workers);
-  auto advance = [&](Pos q) {
-    q.g += step.g;
-    q.o += step.o;
-    q.z += step.z;
-    if (q.g >= groups) { q.g -= groups; ++q.o; }
-    if (q.o >= O) { q.o -= O; ++q.z; }
-    return q;
-  };
-  // items past the longest list are all empty; the bound is formed while the
-  // first item runs
-  int zl = 0;
-  for (int i = lane; i < O; i += kWave) zl = max(zl, live_count[i]);
-  int64_t n_items = (int64_t)E * per_z;
-  bool bounded = false;
-  // With the default grid most wavefronts take a single item, so the chain
-  // per item is kept short: list entry, then constants and samples together.
-  int64_t it = (int64_t)blockIdx.x * kScorerWavesPerBlock + wave;
-  Pos pos = split(it);
-  // Loads the values a scanned item needs besides its samples: U of both
-  // realisations and M over the replica range.
-  auto load_consts = [&](int oo, int4 en, int2 &uu, int (&m0)[kScanMax], int (&m1)[kScanMax]) {
-    const size_t tl = (size_t)oo * E + en.x;
-    const int nrr = en.z >> 16;
-    const int2 raw = *reinterpret_cast<const int2 *>(&tiles[tl].u_m);
-    uu = make_int2(__builtin_amdgcn_readfirstlane(raw.x), __builtin_amdgcn_readfirstlane(raw.y));
-    if (nrr <= kScanMax) {
-      const int32_t *M0 = mopt + ((size_t)oo * 2 + 0) * n_thr + en.y;
-      const int32_t *M1 = mopt + ((size_t)oo * 2 + 1) * n_thr + en.y;
-#pragma unroll
-      for (int j = 0; j < kScanMax; ++j) {
-        m0[j] = j < nrr ? __builtin_amdgcn_readfirstlane(M0[j]) : 0;
-        m1[j] = j < nrr ? __builtin_amdgcn_readfirstlane(M1[j]) : 0;
+  // Evaluates an item whose loads were issued.
+  auto evaluate = [&](const ScoreItem<SPL> &X, const Pos &p) {
+    const int4 en = X.ent;
+    if (en.x < 0) return;  // no tile (uniform)
+    const int e = en.x, toff = en.y, rlo = en.z & 0xFFFF, nr = en.z >> 16;
+    const int cls = en.w & 0x3F, state = (en.w >> 6) & 3, o = en.w >> 8;
+    const size_t tile = (size_t)o * E + e;
+    const int s_first = p.c * CHUNK + lane * SPL;
+    if (DUMP && (state != 0 || nr == 0)) {
+      // listed only when dumping: a revealed cell keeps the base values; a
+      // cell no replica count reaches leaves tau at U
+      const int vm = state != 0 ? base[o * 2 + 0] : X.u0;
+      const int vp = state != 0 ? base[o * 2 + 1] : X.u1;
+      for (int q = 0; q < SPL; ++q) {
+        if (s_first + q < S) {
+          tau_dump[(tile * S + s_first + q) * 2 + 0] = __int_as_float(vm);
+          tau_dump[(tile * S + s_first + q) * 2 + 1] = __int_as_float(vp);
+        }
       }
+      return;
     }
-  };
-  for (; it < n_items; it += workers, pos = advance(pos)) {
-    const int o = pos.o, c0 = pos.g * CPW;
-    const int4 ent = uniform4(list[(size_t)o * E + pos.z]);
-    if (ent.x >= 0) {
-      const int e = ent.x, toff = ent.y, rlo = ent.z & 0xFFFF, nr = ent.z >> 16;
-      const int cls = ent.w & 0xFF, state = ent.w >> 8;
-      const size_t tile = (size_t)o * E + e;
-      int2 u;
-      int mm[kScanMax], mp[kScanMax];
-      load_consts(o, ent, u, mm, mp);
-      if (state != 0 || nr == 0) {
-        // listed only when dumping: a revealed cell keeps the base values; a
-        // cell no replica count reaches leaves tau at U
-        const int vm = state != 0 ? base[o * 2 + 0] : u.x;
-        const int vp = state != 0 ? base[o * 2 + 1] : u.y;
-        for (int c = c0; c < c0 + CPW && c < n_partial; ++c) {
-          const int s_first = c * CHUNK + lane * SPL;
+    const double rcp = c_rcp[cls];
+    const float slo = c_slo[cls];
+    int am[SPL], ap[SPL];
+#pragma unroll
+    for (int q = 0; q < SPL; ++q) am[q] = ap[q] = INT_MIN;
+    if (nr <= kScanMax) {
+#pragma unroll
+      for (int j = 0; j < kScanMax; j += 2) {
+        if (j < nr) {
+          // M <= 1 lets min(f, M) use the unclamped quotient; past the range
+          // M is taken as 0, a term that cannot raise tau (U >= 0)
+          const int mm0 = __builtin_amdgcn_readlane(X.vm0, j), mp0 = __builtin_amdgcn_readlane(X.vm1, j);
+          const int mm1 = j + 1 < nr ? __builtin_amdgcn_readlane(X.vm0, j + 1) : 0;
+          const int mp1 = j + 1 < nr ? __builtin_amdgcn_readlane(X.vm1, j + 1) : 0;
+          const float r1 = (float)(rlo + j), r2 = (float)(rlo + j + 1);
+#pragma unroll
           for (int q = 0; q < SPL; ++q) {
-            if (s_first + q < S) {
-              tau_dump[(tile * S + s_first + q) * 2 + 0] = __int_as_float(vm);
-              tau_dump[(tile * S + s_first + q) * 2 + 1] = __int_as_float(vp);
+            const int f1 = sampled_quotient(r1, X.cs[q], rcp);
+            const int f2 = sampled_quotient(r2, X.cs[q], rcp);
+            am[q] = max(am[q], max(min(f1, mm0), min(f2, mm1)));
+            ap[q] = max(ap[q], max(min(f1, mp0), min(f2, mp1)));
+          }
+        }
+      }
+    } else {
+      // All 2 x SPL searches advance together.  pos counts the leading
+      // thresholds the sample does not reach (NaN is never reached); the
+      // predicate is monotone in the option, so after the steps
+      // 2^(steps-1), ..., 1 pos is the first crossing.
+      int steps = 0;
+      while ((1 << steps) <= nr) ++steps;  // ceil(log2(nr + 1))
+      int pos[SPL][2];
+#pragma unroll
+      for (int q = 0; q < SPL; ++q) pos[q][0] = pos[q][1] = 0;
+      if (nr <= kWave) {
+        // option rlo + j of the range sits in lane j.  Each step issues all
+        // 2 x SPL cross-lane lookups before the first compare (the
+        // scheduling barriers keep them together, so their latencies
+        // overlap instead of adding up).
+        const int t0 = __float_as_int(X.vt0), t1 = __float_as_int(X.vt1);
+        for (int stp = 1 << (steps - 1); stp > 0; stp >>= 1) {
+          int th[SPL][2];
+#pragma unroll
+          for (int q = 0; q < SPL; ++q) {
+            th[q][0] = lane_lookup(t0, min(pos[q][0] + stp - 1, nr - 1));
+            th[q][1] = lane_lookup(t1, min(pos[q][1] + stp - 1, nr - 1));
+          }
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int q = 0; q < SPL; ++q) {
+#pragma unroll
+            for (int side = 0; side < 2; ++side) {
+              const int idx = pos[q][side] + stp - 1;
+              const bool below = !(X.cs[q] >= __int_as_float(th[q][side]));
+              pos[q][side] += (idx < nr && below) ? stp : 0;
             }
+          }
+        }
+        int mj[SPL][2];
+#pragma unroll
+        for (int q = 0; q < SPL; ++q) {
+          mj[q][0] = lane_lookup(X.vm0, min(pos[q][0], nr - 1));
+          mj[q][1] = lane_lookup(X.vm1, min(pos[q][1], nr - 1));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int q = 0; q < SPL; ++q) {
+#pragma unroll
+          for (int side = 0; side < 2; ++side) {
+            const int j = pos[q][side];
+            const int fprev = sampled_ratio((float)(rlo + j - 1), X.cs[q], rcp);
+            const int v = max(j > 0 ? fprev : INT_MIN, j < nr ? mj[q][side] : INT_MIN);
+            if (side == 0) am[q] = max(am[q], v);
+            else ap[q] = max(ap[q], v);
           }
         }
       } else {
-        float cs[SPL], ls[SPL], ncs[SPL], nls[SPL];
-        load_chunk<SPL, VEC>(cap_s, tail_s, tile * S, c0 * CHUNK + lane * SPL, S, cs, ls);
-        const int32_t *Mm = mopt + ((size_t)o * 2 + 0) * n_thr + toff;
-        const int32_t *Mp = mopt + ((size_t)o * 2 + 1) * n_thr + toff;
-        const double rcp = P.rcp_demand[cls];
-        const float slo = P.slo[cls];
-        const bool scan = nr <= kScanMax;
-        int steps = 0;
-        if (!scan) {
-          const float *Tm = thr + ((size_t)o * 2 + 0) * n_thr + toff;
-          const float *Tp = thr + ((size_t)o * 2 + 1) * n_thr + toff;
-          float *Tl = (float *)(Mlds + 2 * nr);
-          wave_lds_fence();  // the previous item's reads of this wave's LDS are done
-          for (int j = lane; j < nr; j += kWave) {
-            Mlds[j] = Mm[j];
-            Mlds[nr + j] = Mp[j];
-            Tl[j] = Tm[j];
-            Tl[nr + j] = Tp[j];
-          }
-          wave_lds_fence();
-          while ((1 << steps) <= nr) ++steps;  // ceil(log2(nr + 1))
+        // a range longer than a wavefront: M and the thresholds go to LDS
+        const int32_t *Mm = mopt + (size_t)o * 2 * n_thr + toff, *Mp = Mm + n_thr;
+        const float *Tm = thr + (size_t)o * 2 * n_thr + toff, *Tp = Tm + n_thr;
+        float *Tl = reinterpret_cast<float *>(Mlds + 2 * nr);
+        wave_lds_fence();  // the previous item's reads of this LDS are done
+        for (int j = lane; j < nr; j += kWave) {
+          Mlds[j] = Mm[j];
+          Mlds[nr + j] = Mp[j];
+          Tl[j] = Tm[j];
+          Tl[nr + j] = Tp[j];
         }
-#pragma unroll
-        for (int i = 0; i < CPW; ++i) {
-          const int c = c0 + i;
-          if (c >= n_partial) break;  // uniform
-          if (i + 1 < CPW) {  // unconditional (clamped) so the waits stay exact
-            const int cn = c + 1 < n_partial ? c + 1 : c;
-            load_chunk<SPL, VEC>(cap_s, tail_s, tile * S, cn * CHUNK + lane * SPL, S, ncs, nls);
-          }
-          const int s_first = c * CHUNK + lane * SPL;
-          int am[SPL], ap[SPL];
-#pragma unroll
-          for (int q = 0; q < SPL; ++q) am[q] = ap[q] = INT_MIN;
-          if (scan) {
-#pragma unroll
-            for (int j = 0; j < kScanMax; j += 2) {
-              if (j < nr) {
-                // M <= 1 lets min(f, M) use the unclamped quotient; past the
-                // range M is 0, a term that cannot raise tau (U >= 0)
-                const float r1 = (float)(rlo + j), r2 = (float)(rlo + j + 1);
-#pragma unroll
-                for (int q = 0; q < SPL; ++q) {
-                  const int f1 = sampled_quotient(r1, cs[q], rcp);
-                  const int f2 = sampled_quotient(r2, cs[q], rcp);
-                  am[q] = max(am[q], max(min(f1, mm[j]), min(f2, mm[j + 1])));
-                  ap[q] = max(ap[q], max(min(f1, mp[j]), min(f2, mp[j + 1])));
-                }
-              }
-            }
-          } else {
-            // All 2 x SPL searches advance together and every probe reads
-            // LDS unconditionally (index clamped), so the reads of one step
-            // are in flight at once.  pos counts the leading thresholds the
-            // sample does not reach (NaN is never reached); the predicate is
-            // monotone in j, so after the steps 2^(steps-1), ..., 1 pos is
-            // the first crossing.
-            const float *Tl = (const float *)(Mlds + 2 * nr);
-            int pos[SPL][2];
-#pragma unroll
-            for (int q = 0; q < SPL; ++q) pos[q][0] = pos[q][1] = 0;
-            for (int step = 1 << (steps - 1); step > 0; step >>= 1) {
-#pragma unroll
-              for (int q = 0; q < SPL; ++q) {
-#pragma unroll
-                for (int side = 0; side < 2; ++side) {
-                  const int idx = pos[q][side] + step - 1;
-                  const float th = Tl[side * nr + min(idx, nr - 1)];
-                  const bool below = !(cs[q] >= th);
-                  pos[q][side] += (idx < nr && below) ? step : 0;
-                }
-              }
-            }
-#pragma unroll
-            for (int q = 0; q < SPL; ++q) {
-#pragma unroll
-              for (int side = 0; side < 2; ++side) {
-                const int j = pos[q][side];
-                const int mj = Mlds[side * nr + min(j, nr - 1)];
-                const int fprev = sampled_ratio((float)(rlo + j - 1), cs[q], rcp);
-                const int v = max(j > 0 ? fprev : INT_MIN, j < nr ? mj : INT_MIN);
-                if (side == 0) am[q] = max(am[q], v);
-                else ap[q] = max(ap[q], v);
-              }
-            }
-          }
-          double gq[SPL];
+        wave_lds_fence();
+        for (int stp = 1 << (steps - 1); stp > 0; stp >>= 1) {
+          float th[SPL][2];
 #pragma unroll
           for (int q = 0; q < SPL; ++q) {
-            // tau = max(U, best over the cell's replica counts); a sampled
-            // tail above the SLO makes every option on the cell worth 0
-            const bool tail_ok = ls[q] <= slo;
-            const int tm = tail_ok ? max(am[q], u.x) : u.x;
-            const int tp = tail_ok ? max(ap[q], u.y) : u.y;
-            const bool live = s_first + q < S;
-            gq[q] = live ? (double)__int_as_float(tp) - (double)__int_as_float(tm) : 0.0;
-            if (tau_dump && live) {
-              tau_dump[(tile * S + s_first + q) * 2 + 0] = __int_as_float(tm);
-              tau_dump[(tile * S + s_first + q) * 2 + 1] = __int_as_float(tp);
+            th[q][0] = Tl[min(pos[q][0] + stp - 1, nr - 1)];
+            th[q][1] = Tl[nr + min(pos[q][1] + stp - 1, nr - 1)];
+          }
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int q = 0; q < SPL; ++q) {
+#pragma unroll
+            for (int side = 0; side < 2; ++side) {
+              const int idx = pos[q][side] + stp - 1;
+              const bool below = !(X.cs[q] >= th[q][side]);
+              pos[q][side] += (idx < nr && below) ? stp : 0;
             }
           }
-          // pairwise tree: within the lane's SPL consecutive samples, then lanes
+        }
+        int mj[SPL][2];
 #pragma unroll
-          for (int w = 1; w < SPL; w <<= 1) {
+        for (int q = 0; q < SPL; ++q) {
+          mj[q][0] = Mlds[min(pos[q][0], nr - 1)];
+          mj[q][1] = Mlds[nr + min(pos[q][1], nr - 1)];
+        }
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int j = 0; j + w < SPL; j += 2 * w) gq[j] = gq[j] + gq[j + w];
-          }
-          const double v = wave_pairwise_sum(gq[0]);
-          if (lane == 0) partial[tile * n_partial + c] = v;
-          if (i + 1 < CPW) {
+        for (int q = 0; q < SPL; ++q) {
 #pragma unroll
-            for (int q = 0; q < SPL; ++q) { cs[q] = ncs[q]; ls[q] = nls[q]; }
+          for (int side = 0; side < 2; ++side) {
+            const int j = pos[q][side];
+            const int fprev = sampled_ratio((float)(rlo + j - 1), X.cs[q], rcp);
+            const int v = max(j > 0 ? fprev : INT_MIN, j < nr ? mj[q][side] : INT_MIN);
+            if (side == 0) am[q] = max(am[q], v);
+            else ap[q] = max(ap[q], v);
           }
         }
       }
     }
-    if (!bounded) {
-      n_items = (int64_t)__builtin_amdgcn_readfirstlane(wave_max(zl)) * per_z;
-      bounded = true;
+    double gq[SPL];
+#pragma unroll
+    for (int q = 0; q < SPL; ++q) {
+      // tau = max(U, best over the cell's replica counts); a sampled tail
+      // above the SLO makes every option on the cell worth 0
+      const bool tail_ok = X.ls[q] <= slo;
+      const int tm = tail_ok ? max(am[q], X.u0) : X.u0;
+      const int tp = tail_ok ? max(ap[q], X.u1) : X.u1;
+      const bool live = s_first + q < S;
+      gq[q] = live ? (double)__int_as_float(tp) - (double)__int_as_float(tm) : 0.0;
+      if (DUMP && live) {
+        tau_dump[(tile * S + s_first + q) * 2 + 0] = __int_as_float(tm);
+        tau_dump[(tile * S + s_first + q) * 2 + 1] = __int_as_float(tp);
+      }
     }
+    // pairwise tree: within the lane's SPL consecutive samples, then lanes
+#pragma unroll
+    for (int w = 1; w < SPL; w <<= 1) {
+#pragma unroll
+      for (int j = 0; j + w < SPL; j += 2 * w) gq[j] = gq[j] + gq[j + w];
+    }
+    const double v = wave_pairwise_sum(gq[0]);
+    if (lane == 0) partial[tile * n_chunk + p.c] = v;
+  };
+
+  Pos pa;
+  pa.j = blockIdx.x / n_chunk;
+  pa.c = blockIdx.x - (int)pa.j * n_chunk;
+  ScoreItem<SPL> A, B;
+  A.ent = uniform4(list_at(pa));
+  if (pa.j >= n_list) A.ent.x = -1;
+  issue(A, pa);
+  Pos pb = advance(pa);
+  int4 raw_b = list_at(pb);
+  // One pipeline stage: the list entry of the item after next is requested,
+  // the next item's loads are issued, the current item is evaluated.  The
+  // two item buffers alternate roles (no copies, so no early waits).  Places
+  // only grow, so the first end marker ends the wavefront's work.
+  auto stage = [&](ScoreItem<SPL> &cur, ScoreItem<SPL> &nxt) {
+    nxt.ent = uniform4(raw_b);
+    if (pb.j >= n_list) nxt.ent.x = -1;
+    const Pos pc = advance(pb);
+    const int4 raw_c = list_at(pc);
+    issue(nxt, pb);
+    evaluate(cur, pa);
+    pa = pb;
+    pb = pc;
+    raw_b = raw_c;
+  };
+  for (;;) {
+    if (A.ent.x < 0) break;
+    stage(A, B);
+    if (B.ent.x < 0) break;
+    stage(B, A);
   }
 }
 
@@ -1691,7 +1798,7 @@ WsLayout ws_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
   L.mopt = at; at = align256(at + sizeof(int32_t) * n_opt);
   L.thr = at; at = align256(at + sizeof(float) * n_opt);
   L.list = at; at = align256(at + sizeof(int4) * (size_t)O * (size_t)E);
-  L.live = at; at = align256(at + sizeof(int32_t) * (size_t)(O > 0 ? O : 1));
+  L.live = at; at = align256(at + sizeof(int32_t));
   L.total = at;
   return L;
 }
@@ -1715,7 +1822,7 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
   const size_t lds = lds_bytes_solver(P, 0);
   if (a.O == 0) return hipSuccess;
   if (a.kernel == 3) {
-    constexpr int kSpl = 4;
+    constexpr int kSpl = 8;
     TileInfo *tiles = (TileInfo *)(a.ws + a.L.tiles);
     int32_t *mopt = (int32_t *)(a.ws + a.L.mopt);
     float *thr = (float *)(a.ws + a.L.thr);
@@ -1738,39 +1845,38 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
                                     a.best);
       return hipGetLastError();
     }
-    const int spl = a.spl == 8 || a.spl == 16 ? a.spl : kSpl;
-    const int cpw = a.cpw == 1 ? 1 : (a.cpw == 4 ? 4 : (a.cpw == 8 ? 8 : 2));
+    const int spl = a.spl == 4 || a.spl == 8 || a.spl == 16 ? a.spl : kSpl;
     const int64_t chunk = 64 * spl;
     const int64_t n_partial = (a.S + chunk - 1) / chunk;
-    const int32_t lds_per_wave = 4 * (P.G / P.tp[0] + 1);  // M and thresholds of the longest range
-    const size_t mlds = (size_t)kScorerWavesPerBlock * lds_per_wave * sizeof(int);
-    const int64_t groups = (n_partial + cpw - 1) / cpw;
-    const int64_t items = groups * a.O * a.E;  // upper bound of the live items
-    const int64_t waves = a.waves > 0 ? a.waves : 8192;
-    const int64_t blocks = ((items < waves ? items : waves) + kScorerWavesPerBlock - 1) / kScorerWavesPerBlock;
-    const unsigned grid = (unsigned)blocks;
+    // LDS: per-class constants, then M and thresholds of a range longer
+    // than a wavefront (the longest range has G / tp[0] options)
+    const int32_t range_max = P.G / P.tp[0];
+    const size_t mlds = (size_t)P.K * (sizeof(double) + sizeof(float)) +
+                        (range_max > kWave ? 4 * sizeof(int) * (size_t)range_max : 0);
+    const int64_t items = n_partial * a.O * a.E;  // upper bound of the live items
+    const int64_t waves = a.waves > 0 ? a.waves : kScorerWaves;
+    const unsigned grid = (unsigned)(items < waves ? items : waves);
+    const int launches = a.ev_begin ? a.timing_launches : 1;
     if (a.ev_begin) (void)hipEventRecord(a.ev_begin, s);
-#define FS_EXCL_LAUNCH(SP, CP)                                                                      \
-  if (a.S % 4 == 0)                                                                                  \
-    k_score_excl<SP, CP, true><<<grid, 64 * kScorerWavesPerBlock, mlds, s>>>(                        \
-        P, tiles, mopt, thr, n_thr, list, live, a.cap_s, a.tail_s, a.O, a.E, a.S, base, partial,    \
-        n_partial, a.tau_dump, lds_per_wave);                                                        \
-  else                                                                                               \
-    k_score_excl<SP, CP, false><<<grid, 64 * kScorerWavesPerBlock, mlds, s>>>(                       \
-        P, tiles, mopt, thr, n_thr, list, live, a.cap_s, a.tail_s, a.O, a.E, a.S, base, partial,    \
-        n_partial, a.tau_dump, lds_per_wave)
-#define FS_EXCL_SPL(SP)                   \
-  switch (cpw) {                          \
-    case 4: FS_EXCL_LAUNCH(SP, 4); break; \
-    case 2: FS_EXCL_LAUNCH(SP, 2); break; \
-    case 8: FS_EXCL_LAUNCH(SP, 8); break; \
-    default: FS_EXCL_LAUNCH(SP, 1); break; \
+    for (int rep = 0; rep < launches; ++rep) {
+#define FS_EXCL_LAUNCH(SP, VEC, DUMP)                                                               \
+  k_score_excl<SP, VEC, DUMP><<<grid, kWave, mlds, s>>>(P, tiles, mopt, thr, n_thr, list, a.cap_s,       \
+                                                        a.tail_s, a.O, a.E, a.S, base, partial,     \
+                                                        (int32_t)n_partial, a.tau_dump)
+#define FS_EXCL_SPL(SP)                                         \
+  if (a.tau_dump) {                                             \
+    if (a.S % 4 == 0) FS_EXCL_LAUNCH(SP, true, true);           \
+    else FS_EXCL_LAUNCH(SP, false, true);                       \
+  } else {                                                      \
+    if (a.S % 4 == 0) FS_EXCL_LAUNCH(SP, true, false);          \
+    else FS_EXCL_LAUNCH(SP, false, false);                      \
   }
-    if (spl == 16) { FS_EXCL_SPL(16) }
-    else if (spl == 8) { FS_EXCL_SPL(8) }
-    else { FS_EXCL_SPL(4) }
+      if (spl == 16) { FS_EXCL_SPL(16) }
+      else if (spl == 8) { FS_EXCL_SPL(8) }
+      else { FS_EXCL_SPL(4) }
 #undef FS_EXCL_SPL
 #undef FS_EXCL_LAUNCH
+    }
     if (a.ev_end) (void)hipEventRecord(a.ev_end, s);
     if (n_partial <= 16) {
       k_finalize_excl<<<a.O, 256, 0, s>>>(tiles, a.E, a.S, base, partial, n_partial, a.score, a.gap_now,
@@ -1784,6 +1890,7 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
   }
   k_base<<<dim3(2, a.O), 64, lds, s>>>(P, bmap, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, base);
   int64_t n_partial = a.L.n_partial;
+  const int launches = a.ev_begin ? a.timing_launches : 1;
   if (a.E > 0) {
     if (a.kernel == 2) {
       float *opts = (float *)(a.ws + a.L.opts);
@@ -1794,8 +1901,9 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
     k_gather_options<GG><<<dim3(P.K, 2, a.O), 128, 0, s>>>(P, bmap, a.cap_lo, a.cap_hi,          \
                                                            a.tail_lo, a.tail_hi, opts);          \
     if (a.ev_begin) (void)hipEventRecord(a.ev_begin, s);                                         \
-    k_score_lane<GG><<<grid, 256, 0, s>>>(P, info, a.measured, opts, a.cap_s, a.tail_s, a.E,     \
-                                          a.S, base, partial, n_partial, a.tau_dump);            \
+    for (int rep = 0; rep < launches; ++rep)                                                     \
+      k_score_lane<GG><<<grid, 256, 0, s>>>(P, info, a.measured, opts, a.cap_s, a.tail_s, a.E,   \
+                                            a.S, base, partial, n_partial, a.tau_dump);          \
     if (a.ev_end) (void)hipEventRecord(a.ev_end, s);                                             \
     break;
       switch (P.G) {
@@ -1810,9 +1918,10 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
       const dim3 grid((a.S + kWave - 1) / kWave, a.E, a.O);
       if (a.ev_begin) (void)hipEventRecord(a.ev_begin, s);
       n_partial = (a.S + kWave - 1) / kWave;
-      k_score_wave<<<grid, 64, lds, s>>>(P, bmap, info, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
-                                         a.measured, a.cap_s, a.tail_s, a.E, a.S, base, partial,
-                                         n_partial, a.tau_dump);
+      for (int rep = 0; rep < launches; ++rep)
+        k_score_wave<<<grid, 64, lds, s>>>(P, bmap, info, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
+                                           a.measured, a.cap_s, a.tail_s, a.E, a.S, base, partial,
+                                           n_partial, a.tau_dump);
       if (a.ev_end) (void)hipEventRecord(a.ev_end, s);
     }
   }

@@ -24,7 +24,6 @@ TP_NONE = 0xFF
 OPT_SCORE_KERNEL = 1
 OPT_KERNEL_TIMING = 2
 OPT_SAMPLES_PER_LANE = 3
-OPT_CHUNKS_PER_WAVE = 4
 OPT_SCORER_WAVES = 5
 KERNEL_AUTO, KERNEL_WAVE, KERNEL_LANE, KERNEL_EXCLUSION = 0, 1, 2, 3
 
@@ -165,7 +164,8 @@ class Context:
 
     def kernel_timing(self):
         """(total milliseconds, launches) of the scoring kernel since the
-        last query; needs set_option(OPT_KERNEL_TIMING, 1)."""
+        last query; needs set_option(OPT_KERNEL_TIMING, n), which launches
+        it n times back to back between each pair of events."""
         ms, n = ctypes.c_double(), ctypes.c_int64()
         _check(load_library().fs_context_kernel_timing(self.handle, ctypes.byref(ms), ctypes.byref(n)))
         return float(ms.value), int(n.value)

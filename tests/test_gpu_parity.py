@@ -296,6 +296,11 @@ def test_score_config2_full_size_sampled(env, orc):
     w = make_workload(2)
     note("score cfg2 full size")
     score, gap, best, dump = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=0)
+    # the benchmark runs without the tau dump: same scores, bit for bit
+    s2, g2, b2, _ = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=0, dump=False)
+    np.testing.assert_array_equal(s2.view(np.uint64), score.view(np.uint64))
+    np.testing.assert_array_equal(g2, gap)
+    np.testing.assert_array_equal(b2, best)
     O, E, S = w.cap_s.shape
     p, iv = w.problem, w.intervals
     rng = np.random.default_rng(2)
@@ -398,29 +403,27 @@ def test_kernels_agree_and_are_deterministic(env, orc):
 
 @pytest.mark.parametrize("S", [4096, 1000])
 def test_exclusion_launch_shapes_agree(env, S):
-    """Every launch shape of the exclusion scorer (samples per lane x chunks
-    per work item x grid size, down to one wavefront doing every item) gives
-    the same bits as the lane kernel's full re-solve, on
-    two whole config-2 orders; S=1000 leaves a ragged last chunk and wavefronts
-    with fewer chunks than the knob asks for."""
+    """Every launch shape of the exclusion scorer (samples per lane x grid
+    size, down to one wavefront doing every item), with and without the tau
+    dump, gives the same bits as the lane kernel's full re-solve, on two
+    whole config-2 orders; S=1000 leaves a ragged last chunk."""
     torch, fs, ctx = env
     w = make_workload(2, orders=[1, 2])
     cs, ts = w.cap_s[:, :, :S], w.tail_s[:, :, :S]
     ref = gpu_score(env, w.problem, w.intervals, w.cand, cs, ts, kernel=2)
     try:
         for spl in (4, 8, 16):
-            for cpw in (1, 2, 4, 8):
-                for waves in (0, 1, 333):
-                    note(f"exclusion shape S={S} spl={spl} cpw={cpw} waves={waves}")
+            for waves in (0, 1, 333, 8192):
+                for dump in (True, False):
+                    note(f"exclusion shape S={S} spl={spl} waves={waves} dump={dump}")
                     ctx.set_option(fs.OPT_SAMPLES_PER_LANE, spl)
-                    ctx.set_option(fs.OPT_CHUNKS_PER_WAVE, cpw)
                     ctx.set_option(fs.OPT_SCORER_WAVES, waves)
-                    g = gpu_score(env, w.problem, w.intervals, w.cand, cs, ts, kernel=3)
+                    g = gpu_score(env, w.problem, w.intervals, w.cand, cs, ts, kernel=3, dump=dump)
                     for x, y in zip(g, ref):
-                        np.testing.assert_array_equal(x.view(np.uint32), y.view(np.uint32))
+                        if x is not None:
+                            np.testing.assert_array_equal(x.view(np.uint32), y.view(np.uint32))
     finally:
         ctx.set_option(fs.OPT_SAMPLES_PER_LANE, 0)
-        ctx.set_option(fs.OPT_CHUNKS_PER_WAVE, 0)
         ctx.set_option(fs.OPT_SCORER_WAVES, 0)
 
 
