@@ -131,7 +131,12 @@ typedef enum fs_option {
   /* Exclusion scorer: wavefronts of its fixed grid, which stride over the
    * work items, in [1, 2^20] (0 = library default).  A launch-shape tuning
    * knob; results are identical for every value. */
-  FS_OPT_SCORER_WAVES = 5
+  FS_OPT_SCORER_WAVES = 5,
+  /* Exclusion scorer set-up: 0 = automatic (one block per order and
+   * realisation when the budget is at most 64 GPUs, there are at most 16
+   * classes and its LDS fits), 1 = the general set-up (one block per order,
+   * realisation and class; any problem).  Results are identical. */
+  FS_OPT_SETUP = 6
 } fs_option;
 
 /* Creates a context bound to HIP device `hip_device`.  One context per host

@@ -20,6 +20,7 @@ struct fs_context {
   int timing;        // back-to-back scoring-kernel launches between timing events (0 = off)
   int spl;           // exclusion scorer samples per lane (0 = default)
   int waves;         // exclusion scorer grid in wavefronts (0 = default)
+  int setup;         // exclusion scorer set-up: 0 automatic, 1 general
   struct Timed {
     hipEvent_t begin, end;
     int launches;
@@ -70,6 +71,8 @@ fs_status make_problem(const fs_problem *p, fs::DevProblem *P) {
     P->tp[t] = p->tp[t];
   }
   if (p->budget < p->tp[0]) return fail(FS_ERR_INVALID_ARGUMENT, "budget is below the smallest TP degree");
+  P->optoff[0] = 0;
+  for (int t = 0; t < p->n_tp; ++t) P->optoff[t + 1] = P->optoff[t] + p->budget / p->tp[t];
   for (int b = 0; b < p->n_levels; ++b) {
     const float v = p->levels[b];
     if (!(v > 0.0f) || !std::isfinite(v)) return fail(FS_ERR_INVALID_ARGUMENT, "levels must be finite and > 0");
@@ -144,7 +147,7 @@ fs_status fs_context_create(int hip_device, fs_context **out) {
   if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
   if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
     return fail(FS_ERR_UNSUPPORTED, std::string("libfleetsieve is built for gfx950, device is ") + prop.gcnArchName);
-  *out = new fs_context{hip_device, 0, 0, 0, 0, {}};
+  *out = new fs_context{hip_device, 0, 0, 0, 0, 0, {}};
   return FS_OK;
 }
 
@@ -196,6 +199,11 @@ fs_status fs_context_set_option(fs_context *ctx, fs_option option, int64_t value
     if (value < 0 || value > (1 << 20))
       return fail(FS_ERR_INVALID_ARGUMENT, "scorer wavefronts must be in [0, 2^20]");
     ctx->waves = (int)value;
+    return FS_OK;
+  }
+  if (option == FS_OPT_SETUP) {
+    if (value != 0 && value != 1) return fail(FS_ERR_INVALID_ARGUMENT, "set-up must be 0 or 1");
+    ctx->setup = (int)value;
     return FS_OK;
   }
   if (option == FS_OPT_KERNEL_TIMING) {
@@ -312,7 +320,7 @@ fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals
   }
   fs::ScoreArgs a{iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi, iv.measured, d_cand, d_cap_s, d_tail_s,
                   n_orders, n_cand, S, d_score, d_gap_now, d_best, d_tau_dump, ws, L, kernel,
-                  ctx->spl, ctx->waves, nullptr, nullptr, 1};
+                  ctx->spl, ctx->waves, ctx->setup, nullptr, nullptr, 1};
   if (ctx->timing && n_cand > 0) {
     e = hipEventCreate(&a.ev_begin);
     if (e == hipSuccess) e = hipEventCreate(&a.ev_end);

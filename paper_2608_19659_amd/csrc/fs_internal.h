@@ -30,6 +30,10 @@ struct DevProblem {
   // 2^-52 relative, is below the distance from any binary32 rounding
   // midpoint, at least 2^-50 relative).
   double rcp_demand[kMaxClasses];
+  // First option of each TP degree among one class's options, which are
+  // ordered by TP, then replicas: optoff[t] = sum over t' < t of G / tp[t'];
+  // optoff[NT] is the number of options per class.
+  int32_t optoff[kMaxTp + 1];
 };
 
 // Where a candidate cell enters the allocation: its class, TP index, load
@@ -98,6 +102,7 @@ struct ScoreArgs {
   int kernel;  // 1 = wave per scenario, 2 = lane per scenario, 3 = exclusion
   int spl;     // exclusion scorer: samples per lane (4, 8 or 16; 0 = default)
   int waves;   // exclusion scorer: wavefronts of its grid (0 = default)
+  int setup;   // exclusion scorer set-up: 0 automatic, 1 general
   hipEvent_t ev_begin, ev_end;  // recorded around the scoring kernel launches if set
   int timing_launches;          // back-to-back launches of the scoring kernel between the events
 };

@@ -96,6 +96,56 @@ __device__ __forceinline__ int wave_scan_add(int v) {
   return v;
 }
 
+// Maximum / minimum over the 64 lanes: DPP permutations within each row of
+// 16 lanes (quad xor 1, quad xor 2, half-row mirror, row mirror), then the
+// four row results by readlane.  Wave-uniform result; every lane must be
+// active.
+__device__ __forceinline__ int wave_max_dpp(int v) {
+  v = max(v, __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, true));
+  v = max(v, __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, true));
+  v = max(v, __builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, true));
+  v = max(v, __builtin_amdgcn_mov_dpp(v, 0x140, 0xF, 0xF, true));
+  return max(max(__builtin_amdgcn_readlane(v, 0), __builtin_amdgcn_readlane(v, 16)),
+             max(__builtin_amdgcn_readlane(v, 32), __builtin_amdgcn_readlane(v, 48)));
+}
+
+__device__ __forceinline__ int wave_min_dpp(int v) {
+  v = min(v, __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, true));
+  v = min(v, __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, true));
+  v = min(v, __builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, true));
+  v = min(v, __builtin_amdgcn_mov_dpp(v, 0x140, 0xF, 0xF, true));
+  return min(min(__builtin_amdgcn_readlane(v, 0), __builtin_amdgcn_readlane(v, 16)),
+             min(__builtin_amdgcn_readlane(v, 32), __builtin_amdgcn_readlane(v, 48)));
+}
+
+// Inclusive prefix maximum of nonnegative values across the 64 lanes: DPP
+// shifts by 1, 2, 4, 8 within each row (a lane with no source takes 0), then
+// every row takes the totals of the rows before it (by readlane).
+__device__ __forceinline__ int wave_scan_max_nonneg(int v, int lane) {
+  v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false));  // row_shr:1
+  v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false));  // row_shr:2
+  v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false));  // row_shr:4
+  v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false));  // row_shr:8
+  const int r0 = __builtin_amdgcn_readlane(v, 15), r1 = __builtin_amdgcn_readlane(v, 31);
+  const int r2 = __builtin_amdgcn_readlane(v, 47);
+  const int row = lane >> 4;
+  const int before = row == 0 ? 0 : row == 1 ? r0 : row == 2 ? max(r0, r1) : max(max(r0, r1), r2);
+  return max(v, before);
+}
+
+// Inclusive prefix sum across the 64 lanes: the same DPP shifts within rows,
+// then the totals of the rows before.
+__device__ __forceinline__ int wave_scan_add_rows(int v, int lane) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);
+  const int r0 = __builtin_amdgcn_readlane(v, 15), r1 = __builtin_amdgcn_readlane(v, 31);
+  const int r2 = __builtin_amdgcn_readlane(v, 47);
+  const int row = lane >> 4;
+  return v + (row == 0 ? 0 : row == 1 ? r0 : row == 2 ? r0 + r1 : r0 + r1 + r2);
+}
+
 // One DPP lane permutation of a binary64 value (both halves moved alike).
 template <int kCtrl>
 __device__ __forceinline__ double dpp_f64(double v) {
@@ -1139,6 +1189,333 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
   }
 }
 
+// ---------------------------------------------------------------------------
+// Set-up of the exclusion scorer for budgets of at most one wavefront.
+// ---------------------------------------------------------------------------
+// Largest budget and class count of the one-block-per-order set-up.
+constexpr int kPrepOrderMaxG = kWave;
+constexpr int kPrepOrderMaxK = 16;
+
+// The scorer's work list, built by one block from staged inputs: the
+// candidates' cells and every order's revealed flags are read into LDS in
+// one round trip, during which the block finds, for every (class, level),
+// the first and last replica count r in [1, G] whose per-replica load lands
+// in that level (the level is nonincreasing in r, so these form a range; a
+// cell of TP t keeps the part with t r <= G).  The list holds every tile the
+// scorer visits -- an unrevealed (order, candidate) pair whose cell some
+// replica count reaches, or every valid pair when dumping -- over all
+// orders, longest range first (bucketed by bit length), then end markers up
+// to O x E entries.  An entry is self-contained: (candidate, option offset
+// of rlo, rlo | nr << 16, class | revealed << 6 | order << 8).  The order of
+// entries within a bucket is arbitrary: it decides only which wavefront
+// evaluates a tile.  Also writes the tile records of invalid candidates.
+//
+// LDS: bucket counters and starts (2 x 32 + 4), the level ranges (2 x K x B),
+// per candidate its cell and range code (2 x E), the revealed flags (O x N
+// bytes).
+__device__ void prep_list_staged(const DevProblem &P, int O, const uint8_t *__restrict__ measured,
+                                 const int32_t *__restrict__ cand, int E, int dump, int PPc,
+                                 TileInfo *__restrict__ tiles, int4 *__restrict__ list,
+                                 int32_t *__restrict__ n_listed, int *lds) {
+  const int tid = threadIdx.x, nth = blockDim.x, lane = tid & (kWave - 1);
+  const int N = P.N, G = P.G, K = P.K, B = P.B, per_class = P.NT * P.B;
+  int *bucket_count = lds, *bucket_start = lds + 32, *n_live = lds + 64;
+  int *lv_first = lds + 68, *lv_last = lv_first + K * B;
+  int *c_cell = lv_last + K * B, *c_code = c_cell + E;
+  uint8_t *meas = reinterpret_cast<uint8_t *>(c_code + E);
+  __shared__ int c_tp[kMaxTp], c_optoff[kMaxTp + 1];
+  if (tid < P.NT) c_tp[tid] = P.tp[tid];
+  if (tid <= P.NT) c_optoff[tid] = P.optoff[tid];
+  if (tid < 32) bucket_count[tid] = 0;
+  for (int x = tid; x < K * B; x += nth) {
+    lv_first[x] = INT_MAX;
+    lv_last[x] = 0;
+  }
+  for (int x = tid; x < O * N; x += nth) meas[x] = measured[x];
+  for (int e = tid; e < E; e += nth) c_cell[e] = cand[e];
+  __syncthreads();  // the counters are set; the loads are still in flight
+  for (int k = 0; k < K; ++k) {  // problem constants are read at uniform indices
+    const float demand = P.demand[k];
+    for (int r = tid + 1; r <= G; r += nth) {
+      const float per_replica = demand / (float)r;
+      int b = 0;
+      for (int j = 0; j < B; ++j) b += P.levels[j] < per_replica ? 1 : 0;
+      if (b < B) {
+        atomicMin(&lv_first[k * B + b], r);
+        atomicMax(&lv_last[k * B + b], r);
+      }
+    }
+  }
+  __syncthreads();
+  // range code of a candidate: -1 invalid cell, -2 never visited (no replica
+  // count reaches the cell and nothing is dumped), else r0 | nr << 16
+  for (int e = tid; e < E; e += nth) {
+    const int cell = c_cell[e];
+    int code = -1;
+    if (cell >= 0 && cell < N) {
+      const int k = cell / per_class, ti = (cell / B) % P.NT, b = cell % B;
+      const int rlo = lv_first[k * B + b], rhi = min(lv_last[k * B + b], G / c_tp[ti]);
+      const int nr = rhi >= rlo ? rhi - rlo + 1 : 0;
+      code = (!dump && nr == 0) ? -2 : ((nr > 0 ? rlo : 1) | (nr << 16));
+    }
+    c_code[e] = code;
+  }
+  __syncthreads();
+  // Threads work candidate by candidate; when there are fewer candidates
+  // than threads, g threads share a candidate and take every g-th order.
+  const int g = E < nth ? nth / E : 1;
+  const int sub = E < nth ? tid / E : 0;
+  const int e_first = E < nth ? tid - sub * E : tid, e_step = E < nth ? E : nth;
+  const bool active = sub < g;
+  for (int pass = 0; pass < 2; ++pass) {
+    for (int e = e_first; active && e < E; e += e_step) {
+      const int code = c_code[e], cell = c_cell[e];
+      if (code == -1) {
+        if (pass == 0) {
+          for (int o = sub; o < O; o += g) {
+            TileInfo *tl = tiles + (size_t)o * E + e;
+            tl->state = -1; tl->cell = cell; tl->cls = 0; tl->t = 0; tl->rlo = 1; tl->rhi = 0;
+            tl->toff = 0; tl->u_m = 0; tl->u_p = 0;
+          }
+        }
+        continue;
+      }
+      if (code == -2) continue;
+      const int nr = code >> 16, b = range_bucket(nr);
+      int n = 0;
+      for (int o = sub; o < O; o += g) n += (dump || !meas[o * N + cell]) ? 1 : 0;
+      if (n == 0) continue;
+      if (pass == 0) {
+        atomicAdd(&bucket_count[b], n);
+      } else {
+        int at = atomicAdd(&bucket_start[b], n);
+        const int k = cell / per_class, ti = (cell / B) % P.NT;
+        const int toff = k * PPc + c_optoff[ti] + (code & 0xFFFF) - 1;
+        for (int o = sub; o < O; o += g) {
+          const bool rev = meas[o * N + cell] != 0;
+          if (dump || !rev) list[at++] = make_int4(e, toff, code, k | ((rev ? 1 : 0) << 6) | (o << 8));
+        }
+      }
+    }
+    __syncthreads();
+    if (pass == 0) {
+      if (tid < kWave) {
+        const int cnt = lane < 32 ? bucket_count[lane] : 0;
+        const int incl = wave_scan_add_rows(cnt, lane);
+        if (lane < 32) bucket_start[lane] = incl - cnt;
+        if (lane == 31) {
+          *n_listed = incl;
+          *n_live = incl;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  for (int z = *n_live + tid; z < O * E; z += nth) list[z] = make_int4(-1, 0, 0, 0);
+}
+
+// Set-up of the exclusion scorer when the budget fits one wavefront
+// (G <= 64) and K <= 16: one block per (order o, realisation R) --
+// block 2 o + R -- with one wavefront per class, and block 2 O builds the
+// work list.  R = 0 is the conservative corner (low capacity, high tail),
+// R = 1 the optimistic one (Section 4.1).  The same quantities as the
+// general set-up, with fewer barriers:
+//   1. all threads: the order's cells and candidates into LDS; the load
+//      level of every (class, r) (the count of grid levels below
+//      lambda / r is the index of the smallest level holding it)
+//   2. wavefront k: B_k, the best ratio of class k with at most g GPUs, by
+//      max-merging every option into its exact GPU count, then a prefix max
+//   3. wavefront i, on its own: H_i, the (max,min) convolution of the other
+//      classes' tables (a chain of crossing searches over nondecreasing
+//      tables); per option of class i, M = H_i[G - t r] clamped at 1, the
+//      capacity threshold of M and w = min(f, M) folded into its cell's
+//      maximum; U of each of its candidates from the two largest cell
+//      maxima; tile records; the base objective (class 0).
+// Tables cover g in [0, G) (option costs t r >= 1 read H at G - t r < G).
+//
+// LDS of a class block: cells (2N floats), the B tables (K x G), the
+// candidates (E), per wavefront 2G + 3 NT B ints (convolution buffers, cell
+// maxima, replica ranges), the order's revealed flags (N bytes, padded to 4)
+// and the load levels (K x G bytes).
+__global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *__restrict__ cap_lo,
+                                                     const float *__restrict__ cap_hi,
+                                                     const float *__restrict__ tail_lo,
+                                                     const float *__restrict__ tail_hi,
+                                                     const uint8_t *__restrict__ measured,
+                                                     const int32_t *__restrict__ cand, int32_t E, int32_t O,
+                                                     int32_t dump, TileInfo *__restrict__ tiles,
+                                                     int32_t *__restrict__ base, int32_t *__restrict__ mopt,
+                                                     float *__restrict__ thr, int32_t n_thr,
+                                                     int4 *__restrict__ list, int32_t *__restrict__ n_listed) {
+  extern __shared__ int lds[];
+  const int tid = threadIdx.x, nth = blockDim.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int G = P.G, K = P.K, N = P.N, NT = P.NT, B = P.B, per_class = NT * B;
+  const int PPc = n_thr / K;
+  if ((int)blockIdx.x == 2 * O) {
+    prep_list_staged(P, O, measured, cand, E, dump, PPc, tiles, list, n_listed, lds);
+    return;
+  }
+  const int o = blockIdx.x >> 1, R = blockIdx.x & 1;
+  float *ccap = reinterpret_cast<float *>(lds);
+  float *ctail = ccap + N;
+  int *Bt = reinterpret_cast<int *>(ctail + N);  // [K][G]
+  int *ccand = Bt + K * G;                       // [E]
+  const int wstride = 2 * G + 3 * per_class;
+  int *wbase = ccand + E;                        // [K][wstride]
+  uint8_t *mrow = reinterpret_cast<uint8_t *>(wbase + K * wstride);  // [N]
+  int8_t *lvl = reinterpret_cast<int8_t *>(mrow + ((N + 3) & ~3));   // [K][G]
+  int *Xa = wbase + wave * wstride, *Xb = Xa + G;
+  int *mc = Xb + G, *crlo = mc + per_class, *crhi = crlo + per_class;
+  const size_t off = (size_t)o * N;
+  const float *gcap = (R == 0 ? cap_lo : cap_hi) + off;
+  const float *gtail = (R == 0 ? tail_hi : tail_lo) + off;
+
+  // --- 1. stage the order; load levels while the loads are in flight
+  __shared__ int c_tp[kMaxTp], c_optoff[kMaxTp + 1];
+  if (tid < NT) c_tp[tid] = P.tp[tid];
+  if (tid <= NT) c_optoff[tid] = P.optoff[tid];
+  for (int c = tid; c < N; c += nth) {
+    ccap[c] = gcap[c];
+    ctail[c] = gtail[c];
+    if (R == 0) mrow[c] = measured[off + c];
+  }
+  for (int e = tid; e < E; e += nth) ccand[e] = cand[e];
+  if (lane < G) {  // wavefront k: the levels of class k, r = lane + 1
+    const float per_replica = P.demand[wave] / (float)(lane + 1);
+    int b = 0;
+    for (int j = 0; j < B; ++j) b += P.levels[j] < per_replica ? 1 : 0;
+    lvl[wave * G + lane] = (int8_t)(b < B ? b : -1);
+  }
+  for (int c = lane; c < per_class; c += kWave) {
+    mc[c] = INT_MIN;
+    crlo[c] = INT_MAX;
+    crhi[c] = -1;
+  }
+  __syncthreads();
+
+  // --- 2. wavefront k: B_k (options cost t r < G <= 64, so r < 64: one
+  // lane per replica count)
+  {
+    const int k = wave;
+    int *T = Bt + k * G;
+    if (lane < G) T[lane] = 0;  // no option: ratio 0
+    wave_lds_fence();
+    const float slo = P.slo[k];
+    const double rcp = P.rcp_demand[k];
+    const int r = lane + 1;
+    for (int ti = 0; ti < NT; ++ti) {
+      const int t = P.tp[ti];
+      if (t * r < G) {
+        const int b = lvl[k * G + r - 1];
+        if (b >= 0) {
+          const int cell = (k * NT + ti) * B + b;
+          atomicMax(&T[t * r], ratio_bits(ccap[cell], ctail[cell], r, slo, rcp));
+        }
+      }
+    }
+    wave_lds_fence();
+    const int v = wave_scan_max_nonneg(lane < G ? T[lane] : 0, lane);
+    if (lane < G) T[lane] = v;
+  }
+  __syncthreads();
+
+  // --- 3. wavefront i on its own from here
+  const int i = wave;
+  int top = 1;
+  while (2 * top <= G) top <<= 1;  // 2 * top > G >= g + 1
+  const int *H;
+  if (K == 1) {
+    if (lane < G) Xa[lane] = INT_MAX;  // the empty convolution
+    wave_lds_fence();
+    H = Xa;
+  } else {
+    const int k0 = i == 0 ? 1 : 0;
+    const int *X = Bt + k0 * G;
+    int *dst = Xa;
+    for (int k = k0 + 1; k < K; ++k) {
+      if (k == i) continue;
+      if (lane < G) dst[lane] = conv_mono(X, Bt + k * G, lane, top);
+      wave_lds_fence();
+      X = dst;
+      dst = dst == Xa ? Xb : Xa;
+    }
+    H = X;
+  }
+  {
+    int32_t *Mo = mopt + ((size_t)o * 2 + R) * n_thr + (size_t)i * PPc;
+    float *To = thr + ((size_t)o * 2 + R) * n_thr + (size_t)i * PPc;
+    const float slo = P.slo[i], demand = P.demand[i];
+    const double rcp = P.rcp_demand[i];
+    for (int p = lane; p < PPc; p += kWave) {
+      int ti = 0, first = 0, t = P.tp[0];
+      for (int t2 = 1; t2 < NT; ++t2) {
+        if (p >= P.optoff[t2]) {
+          ti = t2;
+          first = P.optoff[t2];
+          t = P.tp[t2];
+        }
+      }
+      const int r = p - first + 1;
+      const int b = lvl[i * G + r - 1];
+      if (b < 0) {
+        Mo[p] = INT_MIN;
+        To[p] = __builtin_nanf("");
+        continue;
+      }
+      const int local = ti * B + b, cell = i * per_class + local;
+      // ratios never exceed 1, so M above 1 acts as 1 (min(f, M) and the
+      // crossing are unchanged) and the scorer can skip the clamp of f
+      const int M = min(H[G - t * r], __float_as_int(1.0f));
+      const int f = ratio_bits(ccap[cell], ctail[cell], r, slo, rcp);
+      atomicMax(&mc[local], min(f, M));
+      atomicMin(&crlo[local], r);
+      atomicMax(&crhi[local], r);
+      Mo[p] = M;
+      To[p] = capacity_threshold(r, M, demand, rcp);
+    }
+  }
+  wave_lds_fence();
+  // U of a cell is the largest maximum among the class's other cells (or 0):
+  // the largest maximum m1 at its lowest index c1, and the largest m2 over
+  // every other cell, give it for every cell at once
+  int m1 = INT_MIN, c1 = INT_MAX;
+  for (int c = lane; c < per_class; c += kWave) {
+    const int v = mc[c];
+    if (v > m1) {
+      m1 = v;
+      c1 = c;
+    }
+  }
+  const int wm1 = wave_max_dpp(m1);
+  const int wc1 = wave_min_dpp(m1 == wm1 ? c1 : INT_MAX);
+  int m2 = INT_MIN;
+  for (int c = lane; c < per_class; c += kWave) m2 = max(m2, c != wc1 ? mc[c] : INT_MIN);
+  const int wm2 = wave_max_dpp(m2);
+  for (int e = lane; e < E; e += kWave) {
+    const int cell = ccand[e];
+    if (cell < 0 || cell >= N || cell / per_class != i) continue;
+    TileInfo *tl = tiles + (size_t)o * E + e;
+    const int local = cell - i * per_class;
+    const int u = max(0, local == wc1 ? wm2 : wm1);
+    if (R == 0) {
+      const int ti = local / B;
+      const int t = c_tp[ti], first = c_optoff[ti];
+      const int lo = crlo[local], hi = crhi[local];
+      const int nr = hi >= lo ? hi - lo + 1 : 0;
+      tl->cls = i; tl->t = t; tl->cell = cell;
+      tl->rlo = nr > 0 ? lo : 1;
+      tl->rhi = nr > 0 ? hi : 0;
+      tl->state = mrow[cell] ? 1 : 0;
+      tl->toff = i * PPc + first + (nr > 0 ? lo : 1) - 1;
+      tl->u_m = u;
+    } else {
+      tl->u_p = u;
+    }
+  }
+  if (i == 0 && lane == 0) base[o * 2 + R] = max(0, wm1);  // 0: the empty allocation
+}
+
 // Sampled ratio of r replicas: min(1, fl32(fl32(r * c) / lambda)) as bits.
 __device__ __forceinline__ int sampled_ratio(float rf, float cs, double rcp) {
   const float capacity = rf * cs;
@@ -1771,6 +2148,19 @@ static size_t prep_lds_small(const DevProblem &P) {
 // LDS of the set-up tables per block: B and two tree buffers, K x G each.
 static size_t prep_lds_tables(const DevProblem &P) { return 3 * sizeof(int) * (size_t)P.K * P.G; }
 
+// LDS of the one-block-per-order set-up: the larger of a class block's and
+// the work-list block's.
+static size_t prep_order_lds(const DevProblem &P, int64_t O, int64_t E) {
+  const size_t K = P.K, G = P.G, N = P.N, pc = (size_t)P.NT * P.B;
+  const size_t cls = 4 * (2 * N + K * G + (size_t)E + K * (2 * G + 3 * pc)) + ((N + 3) & ~(size_t)3) + K * G;
+  const size_t lst = 4 * (68 + 2 * K * (size_t)P.B + 2 * (size_t)E) + (size_t)O * N;
+  return cls > lst ? cls : lst;
+}
+
+static bool prep_order_fits(const DevProblem &P, int64_t O, int64_t E) {
+  return P.G <= kPrepOrderMaxG && P.K <= kPrepOrderMaxK && prep_order_lds(P, O, E) <= kPrepLdsLimit;
+}
+
 // Options per (order, realisation): one per (class, TP, r).
 static int32_t excl_thresholds(const DevProblem &P) {
   int per_class = 0;
@@ -1831,7 +2221,11 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
     const int32_t n_thr = excl_thresholds(P);
     const int dump = a.tau_dump != nullptr;
     const size_t small = prep_lds_small(P), big = small + prep_lds_tables(P);
-    if (big <= kPrepLdsLimit)
+    if (a.setup == 0 && prep_order_fits(P, a.O, a.E))
+      k_prep_order<<<2 * a.O + 1, P.K * kWave, prep_order_lds(P, a.O, a.E), s>>>(
+          P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured, a.cand, a.E, a.O, dump, tiles, base, mopt,
+          thr, n_thr, list, live);
+    else if (big <= kPrepLdsLimit)
       k_prep<true><<<dim3(2, a.O, P.K + 1), kPrepThreads, big, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
                                                           a.measured, a.cand, a.E, dump, nullptr, tiles,
                                                           base, mopt, thr, n_thr, list, live);

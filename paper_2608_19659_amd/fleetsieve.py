@@ -25,6 +25,7 @@ OPT_SCORE_KERNEL = 1
 OPT_KERNEL_TIMING = 2
 OPT_SAMPLES_PER_LANE = 3
 OPT_SCORER_WAVES = 5
+OPT_SETUP = 6
 KERNEL_AUTO, KERNEL_WAVE, KERNEL_LANE, KERNEL_EXCLUSION = 0, 1, 2, 3
 
 EXPORTED = ("fs_context_create", "fs_context_destroy", "fs_context_set_option", "fs_context_kernel_timing",

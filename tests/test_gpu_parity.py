@@ -427,6 +427,30 @@ def test_exclusion_launch_shapes_agree(env, S):
         ctx.set_option(fs.OPT_SCORER_WAVES, 0)
 
 
+@pytest.mark.parametrize("cfg,orders", [(0, None), (1, [0, 5, 17]), (2, [1, 2])])
+def test_setup_paths_agree(env, cfg, orders):
+    """The one-block-per-order set-up (budgets up to 64 GPUs) and the general
+    set-up give the same bits: scores, gaps, best candidates and every tau of
+    the dump, with and without the dump (the work list differs then)."""
+    torch, fs, ctx = env
+    w = make_workload(cfg, orders=orders)
+    S = min(w.cap_s.shape[2], 1024)
+    cs, ts = w.cap_s[:, :, :S], w.tail_s[:, :, :S]
+    try:
+        for dump in (True, False):
+            res = []
+            for setup in (0, 1):
+                note(f"set-up path cfg={cfg} setup={setup} dump={dump}")
+                ctx.set_option(fs.OPT_SETUP, setup)
+                res.append(gpu_score(env, w.problem, w.intervals, w.cand, cs, ts, kernel=3, dump=dump))
+            for x, y in zip(*res):
+                if x is not None:
+                    np.testing.assert_array_equal(x.view(np.uint32) if x.dtype != np.int32 else x,
+                                                  y.view(np.uint32) if y.dtype != np.int32 else y)
+    finally:
+        ctx.set_option(fs.OPT_SETUP, 0)
+
+
 def test_lane_kernel_rejects_unsupported_shapes(env):
     torch, fs, ctx = env
     w = make_workload(3, orders=[0], with_samples=False)
