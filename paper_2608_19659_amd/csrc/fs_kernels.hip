@@ -1610,6 +1610,7 @@ __global__ __launch_bounds__(64) void k_score_excl(
   constexpr int CHUNK = 64 * SPL;
   extern __shared__ int lds[];
   const int lane = threadIdx.x;
+  const int wv = (int)blockIdx.x;
   // per-class constants in LDS; then, for ranges longer than a wavefront, M
   // and the thresholds of the range
   double *c_rcp = reinterpret_cast<double *>(lds);
@@ -1628,15 +1629,21 @@ __global__ __launch_bounds__(64) void k_score_excl(
   asm volatile("v_mov_b32 %0, 0" : "=v"(vz));
   const int W = (int)gridDim.x;
   // Item it = j * n_chunk + c: chunk c of the tile in place j of the work
-  // list (every order's live tiles, longest replica range first), so the
-  // wavefronts' first items are the heaviest.
-  struct Pos { int64_t j; int c; };
+  // list (every order's live tiles, longest replica range first).  Items go
+  // to the wavefronts in serpentine order: wavefront w takes items w,
+  // 2W - 1 - w, 2W + w, 4W - 1 - w, ..., so the wavefronts with the
+  // heaviest first items get the lightest second ones.  Positions carry the
+  // parity of their round; the two steps are kept as (places, chunks).
+  struct Pos { int64_t j; int c; int odd; };
   const int64_t n_list = (int64_t)O * E;
-  const int step_j = W / n_chunk, step_c = W - step_j * n_chunk;
+  const int64_t d_even = 2 * (int64_t)W - 1 - 2 * wv, d_odd = 2 * (int64_t)wv + 1;
+  const int64_t sj0 = d_even / n_chunk, sj1 = d_odd / n_chunk;
+  const int sc0 = (int)(d_even - sj0 * n_chunk), sc1 = (int)(d_odd - sj1 * n_chunk);
   auto advance = [&](Pos q) {
-    q.j += step_j;
-    q.c += step_c;
+    q.j += q.odd ? sj1 : sj0;
+    q.c += q.odd ? sc1 : sc0;
     if (q.c >= n_chunk) { q.c -= n_chunk; ++q.j; }
+    q.odd ^= 1;
     return q;
   };
   auto uniform4 = [](int4 v) {
@@ -1686,9 +1693,13 @@ __global__ __launch_bounds__(64) void k_score_excl(
     }
     const double rcp = c_rcp[cls];
     const float slo = c_slo[cls];
+    // the accumulators start at U: tau = max(U, best over the range)
     int am[SPL], ap[SPL];
 #pragma unroll
-    for (int q = 0; q < SPL; ++q) am[q] = ap[q] = INT_MIN;
+    for (int q = 0; q < SPL; ++q) {
+      am[q] = X.u0;
+      ap[q] = X.u1;
+    }
     if (nr <= kScanMax) {
 #pragma unroll
       for (int j = 0; j < kScanMax; j += 2) {
@@ -1812,18 +1823,34 @@ __global__ __launch_bounds__(64) void k_score_excl(
       }
     }
     double gq[SPL];
+    // a sampled tail above the SLO makes every option on the cell worth 0,
+    // leaving tau = U; samples past S add 0 (the chunk holds none of them
+    // unless it is the tile's last and S is not a multiple of its size)
+    const bool full = (p.c + 1) * CHUNK <= S;
+    if (full) {
 #pragma unroll
-    for (int q = 0; q < SPL; ++q) {
-      // tau = max(U, best over the cell's replica counts); a sampled tail
-      // above the SLO makes every option on the cell worth 0
-      const bool tail_ok = X.ls[q] <= slo;
-      const int tm = tail_ok ? max(am[q], X.u0) : X.u0;
-      const int tp = tail_ok ? max(ap[q], X.u1) : X.u1;
-      const bool live = s_first + q < S;
-      gq[q] = live ? (double)__int_as_float(tp) - (double)__int_as_float(tm) : 0.0;
-      if (DUMP && live) {
-        tau_dump[(tile * S + s_first + q) * 2 + 0] = __int_as_float(tm);
-        tau_dump[(tile * S + s_first + q) * 2 + 1] = __int_as_float(tp);
+      for (int q = 0; q < SPL; ++q) {
+        const bool tail_ok = X.ls[q] <= slo;
+        const int tm = tail_ok ? am[q] : X.u0;
+        const int tp = tail_ok ? ap[q] : X.u1;
+        gq[q] = (double)__int_as_float(tp) - (double)__int_as_float(tm);
+        if (DUMP) {
+          tau_dump[(tile * S + s_first + q) * 2 + 0] = __int_as_float(tm);
+          tau_dump[(tile * S + s_first + q) * 2 + 1] = __int_as_float(tp);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < SPL; ++q) {
+        const bool tail_ok = X.ls[q] <= slo;
+        const int tm = tail_ok ? am[q] : X.u0;
+        const int tp = tail_ok ? ap[q] : X.u1;
+        const bool live = s_first + q < S;
+        gq[q] = live ? (double)__int_as_float(tp) - (double)__int_as_float(tm) : 0.0;
+        if (DUMP && live) {
+          tau_dump[(tile * S + s_first + q) * 2 + 0] = __int_as_float(tm);
+          tau_dump[(tile * S + s_first + q) * 2 + 1] = __int_as_float(tp);
+        }
       }
     }
     // pairwise tree: within the lane's SPL consecutive samples, then lanes
@@ -1837,8 +1864,9 @@ __global__ __launch_bounds__(64) void k_score_excl(
   };
 
   Pos pa;
-  pa.j = blockIdx.x / n_chunk;
-  pa.c = blockIdx.x - (int)pa.j * n_chunk;
+  pa.j = wv / n_chunk;
+  pa.c = wv - (int)pa.j * n_chunk;
+  pa.odd = 0;
   ScoreItem<SPL> A, B;
   A.ent = uniform4(list_at(pa));
   if (pa.j >= n_list) A.ent.x = -1;
