@@ -28,6 +28,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "allocation scenarios/sec on 1 MI355X; % of VALU/HBM roofline; oracle-exact"
+# The measured workload: 4 classes, TP {1, 2, 4, 8}, G = 64, 8 load levels,
+# 128 candidates x 4096 samples x 16 reveal orders.
+BENCH_WORKLOAD = "4class-G64"
 # 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz: one 32-bit VALU operation per lane per clock.
 VALU_PEAK_OPS = 256 * 4 * 16 * 2.4e9
 HBM_PEAK_BYTES = 8.0e12
@@ -162,7 +165,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=2, help="workload configuration (default 2)")
+    ap.add_argument("--workload", default=BENCH_WORKLOAD,
+                    help=f"synthetic workload name (default {BENCH_WORKLOAD})")
     ap.add_argument("--kernel", type=int, default=0,
                     help="0 auto, 1 wave per scenario, 2 lane per scenario, 3 exclusion")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="wall budget of the oracle baseline")
@@ -196,11 +200,14 @@ def main():
         return
 
     from paper_2608_19659_amd import fleetsieve as fs
-    from paper_2608_19659_amd.synth import CONFIGS, make_workload
+    from paper_2608_19659_amd.synth import WORKLOADS, make_workload
 
     dev = "cuda:0"
-    print(f"[bench] generating workload config {args.config}", file=sys.stderr, flush=True)
-    w = make_workload(args.config)
+    if args.workload not in WORKLOADS:
+        print(f"unknown workload {args.workload}; choose from {list(WORKLOADS)}", file=sys.stderr)
+        sys.exit(2)
+    print(f"[bench] generating workload {args.workload}", file=sys.stderr, flush=True)
+    w = make_workload(args.workload)
     p = w.problem
     O, E, S = w.cap_s.shape
     t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
@@ -255,7 +262,7 @@ def main():
     value = scenarios / (ms_per_step / 1e3)
 
     def roofline_of(kernel_id, kernel_ms_avg):
-        tag = f"cfg{args.config}"
+        tag = args.workload
         kernel_s = kernel_ms_avg / 1e3
         if kernel_id == 3:
             slots, nbytes, mean_ne, sampled = excl_work(p, w.cand, live_tiles, S)
@@ -302,16 +309,15 @@ def main():
         print(f"[bench] cpu baseline ({threads} threads)", file=sys.stderr, flush=True)
         cpu = cpu_baseline(w, args.cpu_seconds, threads)
 
-    c = CONFIGS[args.config]
     line = {
         "metric": METRIC, "value": value, "unit": "scenarios/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": f"config {args.config} ({c['name']}): {p.n_classes} classes, "
+        "config": {"workload": f"{args.workload}: {p.n_classes} classes, "
                                f"TP {[int(x) for x in p.tp]}, "
                                f"G={p.budget}, {p.n_levels} load levels, {E} candidates x {S} samples x "
                                f"{O} reveal orders",
-                   "scenarios_per_step": scenarios, "scenarios_in_config": O * E * S,
+                   "scenarios_per_step": scenarios, "scenarios_in_workload": O * E * S,
                    "measured_candidates_skipped": int(measured_cand.sum()) * S,
                    "kernel": kernel_name, "parallelism": "single GPU"},
         "roofline": roofline, "cpu_baseline": cpu, "full_resolve": full,

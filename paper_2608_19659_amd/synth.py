@@ -100,7 +100,7 @@ class Intervals:
 @dataclass
 class Workload:
     name: str
-    cfg: int
+    seed: int
     problem: Problem
     intervals: Intervals          # [O][N]
     cand: np.ndarray              # [E] int32 cell indices
@@ -108,7 +108,7 @@ class Workload:
     tail_s: np.ndarray | None     # [O][E][S] float32
     truth_cap: np.ndarray         # [N] hidden truth used for reveals
     truth_tail: np.ndarray
-    orders: np.ndarray            # which order indices of the full config these are
+    orders: np.ndarray            # which of the workload's reveal orders these are
     n_samples: int
     recipe: dict = field(default_factory=dict)
 
@@ -125,13 +125,14 @@ def _geometric(start: float, n: int) -> list:
     return [start * (2.0 ** k) for k in range(n)]
 
 
-CONFIGS = {
-    0: dict(name="tiny-2class-G16", K=2, tp=[1, 2, 4, 8], G=16, levels=[0.5, 1.0, 2.0],
+# The seeded synthetic workloads, by name.  Each has its own seed.
+WORKLOADS = {
+    "tiny-2class-G16": dict(seed=1000, K=2, tp=[1, 2, 4, 8], G=16, levels=[0.5, 1.0, 2.0],
             demand=("fixed", [4.0, 2.0]), slo=("fixed", [30.0, 30.0]),
             cap_range=(0.2, 3.0), cap_width=(0.05, 0.3), tail_sigma=0.4, tail_alpha=1.0,
             tail_tp_factor=False, tail_width=(0.1, 0.4), orders=1, reveal=False,
             cand=("subset", 8), samples=64),
-    1: dict(name="paper-shaped-2class-G16", K=2, tp=[1, 2, 4, 8], G=16,
+    "paper-shaped-2class-G16": dict(seed=1001, K=2, tp=[1, 2, 4, 8], G=16,
             levels=[0.25, 0.5, 1.0, 2.0, 4.0, 8.0],
             # code at 3 req/s (not 2) so the 16-GPU budget binds and decision
             # gaps stay open; at 4 / 2 req/s every realisation serves both fully
@@ -139,26 +140,22 @@ CONFIGS = {
             cap_range=(0.2, 3.0), cap_width=(0.05, 0.3), tail_sigma=0.4, tail_alpha=1.5,
             tail_tp_factor=True, tail_width=(0.1, 0.4), orders=200, reveal=True,
             cand=("all",), samples=1024),
-    2: dict(name="4class-G64", K=4, tp=[1, 2, 4, 8], G=64, levels=_geometric(0.125, 8),
+    "4class-G64": dict(seed=1002, K=4, tp=[1, 2, 4, 8], G=64, levels=_geometric(0.125, 8),
             demand=("uniform", 1.0, 20.0), slo=("fixed", [30.0, 20.0, 2.0, 300.0]),
             cap_range=(0.1, 5.0), cap_width=(0.05, 0.3), tail_sigma=0.5, tail_alpha=1.0,
             tail_tp_factor=True, tail_width=(0.1, 0.4), orders=16, reveal=True,
             cand=("all",), samples=4096),
-    3: dict(name="8class-G256", K=8, tp=[1, 2, 4, 8], G=256, levels=_geometric(0.125, 8),
+    "8class-G256": dict(seed=1003, K=8, tp=[1, 2, 4, 8], G=256, levels=_geometric(0.125, 8),
             demand=("uniform", 0.5, 50.0), slo=("choice", SLO_CHOICES),
             cap_range=(0.1, 5.0), cap_width=(0.02, 0.5), tail_sigma=0.5, tail_alpha=1.0,
             tail_tp_factor=True, tail_width=(0.02, 0.5), orders=64, reveal=True,
             cand=("all",), samples=4096),
-    4: dict(name="16class-G1024", K=16, tp=[1, 2, 4, 8, 16], G=1024, levels=_geometric(0.0625, 12),
+    "16class-G1024": dict(seed=1004, K=16, tp=[1, 2, 4, 8, 16], G=1024, levels=_geometric(0.0625, 12),
             demand=("uniform", 1.0, 200.0), slo=("choice", SLO_CHOICES),
             cap_range=(0.1, 5.0), cap_width=(0.02, 0.5), tail_sigma=0.5, tail_alpha=1.0,
             tail_tp_factor=True, tail_width=(0.02, 0.5), orders=4, reveal=True,
             cand=("all",), samples=256),
 }
-
-
-def seed_of(cfg: int) -> int:
-    return 1000 + cfg
 
 
 def q64(x):
@@ -183,8 +180,8 @@ def _knee_capacities(rng, tp, lo, hi, max_tries=10000):
     raise RuntimeError("capacity draw could not place the knee at TP4")
 
 
-def _problem_for(cfg: int, rng) -> Problem:
-    c = CONFIGS[cfg]
+def _problem_for(name: str, rng) -> Problem:
+    c = WORKLOADS[name]
     K = c["K"]
     kind = c["demand"][0]
     if kind == "fixed":
@@ -200,9 +197,9 @@ def _problem_for(cfg: int, rng) -> Problem:
                    slo=slo.astype(np.float32), budget=c["G"], floor_rps=None)
 
 
-def _initial_intervals(cfg: int, problem: Problem, rng):
+def _initial_intervals(name: str, problem: Problem, rng):
     """Initial interval per cell: [c_lo, c_hi] and [l_lo, l_hi], float64."""
-    c = CONFIGS[cfg]
+    c = WORKLOADS[name]
     K, T, B = problem.n_classes, problem.n_tp, problem.n_levels
     N = problem.n_cells
     cap_lo = np.zeros(N)
@@ -247,16 +244,16 @@ def _draw_inside(rng, cap_lo, cap_hi, tail_lo, tail_hi, shape=None):
     return cap.astype(np.float32), tail.astype(np.float32)
 
 
-def make_workload(cfg: int, orders=None, with_samples: bool = True) -> Workload:
-    """Build configuration ``cfg`` (0..4).  ``orders`` selects a subset of the
-    configuration's reveal orders (each order has its own seeded stream, so a
+def make_workload(name: str, orders=None, with_samples: bool = True) -> Workload:
+    """Build the workload ``name`` (a key of WORKLOADS).  ``orders`` selects a
+    subset of its reveal orders (each order has its own seeded stream, so a
     subset is identical to the same rows of the full build)."""
-    c = CONFIGS[cfg]
-    seed = seed_of(cfg)
+    c = WORKLOADS[name]
+    seed = c["seed"]
     rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 0])))
-    problem = _problem_for(cfg, rng)
+    problem = _problem_for(name, rng)
     N = problem.n_cells
-    cap_lo0, cap_hi0, tail_lo0, tail_hi0 = _initial_intervals(cfg, problem, rng)
+    cap_lo0, cap_hi0, tail_lo0, tail_hi0 = _initial_intervals(name, problem, rng)
     truth_cap, truth_tail = _draw_inside(rng, cap_lo0, cap_hi0, tail_lo0, tail_hi0)
     if c["cand"][0] == "subset":
         cand = np.sort(rng.choice(N, size=c["cand"][1], replace=False)).astype(np.int32)
@@ -290,7 +287,7 @@ def make_workload(cfg: int, orders=None, with_samples: bool = True) -> Workload:
             cs, ts = _draw_inside(srng, cl[cand], ch[cand], tl[cand], th[cand], shape=(E, S))
             cap_s[j], tail_s[j] = cs, ts
     iv = Intervals(cap_lo, cap_hi, tail_lo, tail_hi, measured)
-    return Workload(c["name"], cfg, problem, iv, cand, cap_s, tail_s,
+    return Workload(name, seed, problem, iv, cand, cap_s, tail_s,
                     truth_cap.astype(np.float32), truth_tail.astype(np.float32), sel, S, dict(c))
 
 

@@ -199,73 +199,73 @@ def test_dense_large_budget_waterfilling_shape(env, orc):
 
 # -------------------------------------------------- scores vs oracle --------
 @pytest.mark.parametrize("kernel", KERNELS)
-def test_score_config0_full(env, orc, kernel):
-    w = make_workload(0)
-    note(f"score cfg0 kernel {kernel}")
+def test_score_tiny_full(env, orc, kernel):
+    w = make_workload("tiny-2class-G16")
+    note(f"score tiny-2class-G16 kernel {kernel}")
     g = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel)
     o = orc.score(w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, n_threads=8)
     assert_scores_equal(g, o)
 
 
 @pytest.mark.parametrize("kernel", KERNELS)
-def test_score_config1_orders(env, orc, kernel):
-    w = make_workload(1, orders=[0, 2, 5, 7, 11, 13])
-    note(f"score cfg1 6 orders kernel {kernel}")
+def test_score_paper_shaped_orders(env, orc, kernel):
+    w = make_workload("paper-shaped-2class-G16", orders=[0, 2, 5, 7, 11, 13])
+    note(f"score paper-shaped-2class-G16 6 orders kernel {kernel}")
     g = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel)
     o = orc.score(w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, n_threads=16)
     assert_scores_equal(g, o)
 
 
 @pytest.mark.parametrize("kernel", KERNELS)
-def test_score_config2_tiles(env, orc, kernel):
+def test_score_4class_g64_tiles(env, orc, kernel):
     """Config 2 shape (K=4, G=64) on a few orders and candidates, all 4096
     samples: several 256-sample blocks per tile."""
-    w = make_workload(2, orders=[1, 2, 3])
+    w = make_workload("4class-G64", orders=[1, 2, 3])
     cand_sel = np.array([3, 17, 40, 64, 77, 100, 126])
     cand = w.cand[cand_sel]
     cs, ts = w.cap_s[:, cand_sel], w.tail_s[:, cand_sel]
-    note(f"score cfg2 3x7 tiles kernel {kernel}")
+    note(f"score 4class-G64 3x7 tiles kernel {kernel}")
     g = gpu_score(env, w.problem, w.intervals, cand, cs, ts, kernel)
     o = orc.score(w.problem, w.intervals, cand, cs, ts, n_threads=16)
     assert_scores_equal(g, o)
 
 
 @pytest.mark.parametrize("kernel", [1, 3])
-def test_score_config3_subset(env, orc, kernel):
+def test_score_8class_g256_subset(env, orc, kernel):
     """Config 3 shape (K=8, G=256): 2 orders x 6 candidates, first 96
     samples (a ragged block)."""
-    w = make_workload(3, orders=[0, 5])
+    w = make_workload("8class-G256", orders=[0, 5])
     sel = np.array([0, 31, 77, 128, 200, 255])
     S = 96
     cs = np.ascontiguousarray(w.cap_s[:, sel, :S])
     ts = np.ascontiguousarray(w.tail_s[:, sel, :S])
-    note(f"score cfg3 subset kernel {kernel}")
+    note(f"score 8class-G256 subset kernel {kernel}")
     g = gpu_score(env, w.problem, w.intervals, w.cand[sel], cs, ts, kernel=kernel)
     o = orc.score(w.problem, w.intervals, w.cand[sel], cs, ts, n_threads=16)
     assert_scores_equal(g, o)
 
 
 @pytest.mark.parametrize("kernel", [1, 3])
-def test_score_config4_subset(env, orc, kernel):
+def test_score_16class_g1024_subset(env, orc, kernel):
     """Config 4 shape (K=16, TP up to 16, G=1024): 1 order x 3 candidates,
     first 24 samples."""
-    w = make_workload(4, orders=[1], with_samples=True)
+    w = make_workload("16class-G1024", orders=[1], with_samples=True)
     sel = np.array([5, 480, 959])
     S = 24
     cs = np.ascontiguousarray(w.cap_s[:, sel, :S])
     ts = np.ascontiguousarray(w.tail_s[:, sel, :S])
-    note(f"score cfg4 subset kernel {kernel}")
+    note(f"score 16class-G1024 subset kernel {kernel}")
     g = gpu_score(env, w.problem, w.intervals, w.cand[sel], cs, ts, kernel=kernel)
     o = orc.score(w.problem, w.intervals, w.cand[sel], cs, ts, n_threads=16)
     assert_scores_equal(g, o)
 
 
-def test_score_config3_full_orders_exclusion(env, orc):
+def test_score_8class_g256_full_order_exclusion(env, orc):
     """Config 3 at its real sample count (4096) with the exclusion kernel:
     all 256 candidates of one order, sampled scenarios re-solved by the
     oracle one by one, and three whole tiles re-scored."""
-    w = make_workload(3, orders=[7])
-    note("score cfg3 one full order, exclusion")
+    w = make_workload("8class-G256", orders=[7])
+    note("score 8class-G256 one full order, exclusion")
     score, gap, best, dump = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=3)
     p, iv = w.problem, w.intervals
     rng = np.random.default_rng(33)
@@ -288,13 +288,13 @@ def test_score_config3_full_orders_exclusion(env, orc):
     assert_scores_equal((score, gap, best, dump), o_ref, tile_mask=mask)
 
 
-def test_score_config2_full_size_sampled(env, orc):
-    """The benchmark configuration at full size (16 orders x 128 candidates x
+def test_score_4class_g64_full_size_sampled(env, orc):
+    """The 4-class G=64 workload at full size (16 orders x 128 candidates x
     4096 samples) in the benchmark's launch configuration: sampled scenarios
     re-solved one by one by the oracle, two whole tiles re-scored, and the
     invariants of the realisations checked everywhere."""
-    w = make_workload(2)
-    note("score cfg2 full size")
+    w = make_workload("4class-G64")
+    note("score 4class-G64 full size")
     score, gap, best, dump = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=0)
     # the benchmark runs without the tau dump: same scores, bit for bit
     s2, g2, b2, _ = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=0, dump=False)
@@ -341,7 +341,7 @@ def test_score_config2_full_size_sampled(env, orc):
 @pytest.mark.parametrize("kernel", KERNELS)
 @pytest.mark.parametrize("S", [1, 65, 300])
 def test_score_ragged_samples(env, orc, kernel, S):
-    w = make_workload(1, orders=[0, 3])
+    w = make_workload("paper-shaped-2class-G16", orders=[0, 3])
     cs = np.ascontiguousarray(w.cap_s[:, :, :S])
     ts = np.ascontiguousarray(w.tail_s[:, :, :S])
     note(f"ragged S={S} kernel {kernel}")
@@ -351,7 +351,7 @@ def test_score_ragged_samples(env, orc, kernel, S):
 
 
 def test_score_no_candidates_and_all_measured(env, orc):
-    w = make_workload(1, orders=[0, 1])
+    w = make_workload("paper-shaped-2class-G16", orders=[0, 1])
     note("no candidates")
     score, gap, best, _ = gpu_score(env, w.problem, w.intervals, np.zeros(0, np.int32),
                                     np.zeros((2, 0, 0), np.float32), np.zeros((2, 0, 0), np.float32),
@@ -387,7 +387,7 @@ def test_single_class_problem(env, orc, kernel):
 
 
 def test_kernels_agree_and_are_deterministic(env, orc):
-    w = make_workload(1, orders=[4, 9, 20])
+    w = make_workload("paper-shaped-2class-G16", orders=[4, 9, 20])
     note("determinism")
     a = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=2)
     b = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=2)
@@ -406,9 +406,9 @@ def test_exclusion_launch_shapes_agree(env, S):
     """Every launch shape of the exclusion scorer (samples per lane x grid
     size, down to one wavefront doing every item), with and without the tau
     dump, gives the same bits as the lane kernel's full re-solve, on two
-    whole config-2 orders; S=1000 leaves a ragged last chunk."""
+    whole orders of the 4-class G=64 workload; S=1000 leaves a ragged last chunk."""
     torch, fs, ctx = env
-    w = make_workload(2, orders=[1, 2])
+    w = make_workload("4class-G64", orders=[1, 2])
     cs, ts = w.cap_s[:, :, :S], w.tail_s[:, :, :S]
     ref = gpu_score(env, w.problem, w.intervals, w.cand, cs, ts, kernel=2)
     try:
@@ -427,20 +427,21 @@ def test_exclusion_launch_shapes_agree(env, S):
         ctx.set_option(fs.OPT_SCORER_WAVES, 0)
 
 
-@pytest.mark.parametrize("cfg,orders", [(0, None), (1, [0, 5, 17]), (2, [1, 2])])
-def test_setup_paths_agree(env, cfg, orders):
+@pytest.mark.parametrize("name,orders", [("tiny-2class-G16", None), ("paper-shaped-2class-G16", [0, 5, 17]),
+                                         ("4class-G64", [1, 2])])
+def test_setup_paths_agree(env, name, orders):
     """The one-block-per-order set-up (budgets up to 64 GPUs) and the general
     set-up give the same bits: scores, gaps, best candidates and every tau of
     the dump, with and without the dump (the work list differs then)."""
     torch, fs, ctx = env
-    w = make_workload(cfg, orders=orders)
+    w = make_workload(name, orders=orders)
     S = min(w.cap_s.shape[2], 1024)
     cs, ts = w.cap_s[:, :, :S], w.tail_s[:, :, :S]
     try:
         for dump in (True, False):
             res = []
             for setup in (0, 1):
-                note(f"set-up path cfg={cfg} setup={setup} dump={dump}")
+                note(f"set-up path {name} setup={setup} dump={dump}")
                 ctx.set_option(fs.OPT_SETUP, setup)
                 res.append(gpu_score(env, w.problem, w.intervals, w.cand, cs, ts, kernel=3, dump=dump))
             for x, y in zip(*res):
@@ -453,7 +454,7 @@ def test_setup_paths_agree(env, cfg, orders):
 
 def test_lane_kernel_rejects_unsupported_shapes(env):
     torch, fs, ctx = env
-    w = make_workload(3, orders=[0], with_samples=False)
+    w = make_workload("8class-G256", orders=[0], with_samples=False)
     ctx.set_score_kernel(2)
     div = fs.DeviceIntervals.from_host(w.intervals, "cuda:0")
     cand = torch.zeros(1, dtype=torch.int32, device="cuda:0")
@@ -473,7 +474,7 @@ def test_lane_kernel_rejects_unsupported_shapes(env):
 def test_score_with_floors_uses_wave_kernel(env, orc):
     """Critical floors are scored by the wave-per-scenario kernel (the
     automatic choice) and match the oracle, including negative gaps."""
-    w = make_workload(2, orders=[1, 2])
+    w = make_workload("4class-G64", orders=[1, 2])
     p = w.problem
     fl = np.zeros(p.n_classes, np.float32)
     fl[1], fl[3] = 3.0, 1.5
@@ -491,14 +492,15 @@ def test_score_with_floors_uses_wave_kernel(env, orc):
 # --------------------------------------------------------- certificates -----
 def test_certify_random_orders(env, orc):
     torch, fs, ctx = env
-    for cfg, floors in ((1, False), (2, False), (2, True), (3, False)):
-        w = make_workload(cfg, orders=list(range(12)), with_samples=False)
+    for name, floors in (("paper-shaped-2class-G16", False), ("4class-G64", False), ("4class-G64", True),
+                        ("8class-G256", False)):
+        w = make_workload(name, orders=list(range(12)), with_samples=False)
         p = w.problem
         if floors:
             fl = np.zeros(p.n_classes, np.float32)
             fl[0], fl[2] = 2.0, 0.5
             p = Problem(p.tp, p.levels, p.demand, p.slo, p.budget, floor_rps=fl)
-        note(f"certify cfg{cfg} floors={floors}")
+        note(f"certify {name} floors={floors}")
         r = fs.certify(ctx, p, fs.DeviceIntervals.from_host(w.intervals, "cuda:0"), eps=0.05)
         torch.cuda.synchronize()
         o = orc.certify(p, w.intervals, eps=0.05)
@@ -507,8 +509,8 @@ def test_certify_random_orders(env, orc):
         g_cons = {k: v.cpu().numpy() for k, v in r.cons.items()}
         g_opt = {k: v.cpu().numpy() for k, v in r.opt.items()}
         for j in range(w.n_orders):
-            assert_alloc_equal(p, g_cons, j, o.cons[j], f"cfg{cfg} cons {j}")
-            assert_alloc_equal(p, g_opt, j, o.opt[j], f"cfg{cfg} opt {j}")
+            assert_alloc_equal(p, g_cons, j, o.cons[j], f"{name} cons {j}")
+            assert_alloc_equal(p, g_opt, j, o.opt[j], f"{name} opt {j}")
 
 
 # ------------------------------------------------------------ validation ----
@@ -536,7 +538,7 @@ def test_score_many_partials(env, orc, S):
     """Large sample counts up to the maximum (2^20): many partial sums per
     tile, reduced by the same pairwise tree as the oracle (exclusion and lane
     kernels)."""
-    w = make_workload(1, orders=[2], with_samples=False)
+    w = make_workload("paper-shaped-2class-G16", orders=[2], with_samples=False)
     p, iv = w.problem, w.intervals
     live = [e for e in range(w.n_cand) if not iv.measured[0, w.cand[e]]]
     sel = np.array(live[:2] if S < (1 << 20) else live[1:2])

@@ -125,7 +125,7 @@ def test_pairwise_sum_order(orc):
 def test_invariants_on_paper_shaped_workload(orc):
     """tau- <= tau+, 0 <= Gamma(o,e,s) <= Gamma_t, score in [0, Gamma_t] and a
     measured candidate scores exactly 0 (samples lie inside the intervals)."""
-    w = make_workload(1, orders=[0, 1, 2, 3])
+    w = make_workload("paper-shaped-2class-G16", orders=[0, 1, 2, 3])
     E = w.n_cand
     mask = np.zeros((w.n_orders, E), np.uint8)
     mask[:, ::6] = 1
@@ -142,7 +142,7 @@ def test_invariants_on_paper_shaped_workload(orc):
 
 
 def test_point_intervals_give_zero_scores(orc):
-    w = make_workload(0)
+    w = make_workload("tiny-2class-G16")
     tc, tt = w.truth_cap[None], w.truth_tail[None]
     iv = Intervals(tc, tc, tt, tt, np.zeros_like(w.intervals.measured))
     cs = np.broadcast_to(w.truth_cap[w.cand][None, :, None], w.cap_s.shape).copy()
@@ -152,13 +152,13 @@ def test_point_intervals_give_zero_scores(orc):
     assert np.all(r.score == 0.0)
 
 
-@pytest.mark.parametrize("cfg,n_orders", [(1, 24), (2, 6)])
-def test_health_gates(orc, cfg, n_orders):
+@pytest.mark.parametrize("name,n_orders", [("paper-shaped-2class-G16", 24), ("4class-G64", 6)])
+def test_health_gates(orc, name, n_orders):
     """The synthetic workloads are not degenerate: at least 30% of orders have
     an open gap, every such order has a candidate with a positive score (there
     is something decision-critical to measure), and at least 1% of all
     scenarios close part of the gap."""
-    w = make_workload(cfg, orders=list(range(n_orders)))
+    w = make_workload(name, orders=list(range(n_orders)))
     S = 16
     r = orc.score(w.problem, w.intervals, w.cand, w.cap_s[:, :, :S], w.tail_s[:, :, :S],
                   n_threads=8)

@@ -5,7 +5,7 @@ import hashlib
 import numpy as np
 import pytest
 
-from paper_2608_19659_amd.synth import CONFIGS, make_workload
+from paper_2608_19659_amd.synth import WORKLOADS, make_workload
 
 
 def _digest(w):
@@ -17,13 +17,13 @@ def _digest(w):
 
 
 def test_deterministic():
-    assert _digest(make_workload(0)) == _digest(make_workload(0))
-    assert _digest(make_workload(1, orders=[3, 7])) == _digest(make_workload(1, orders=[3, 7]))
+    assert _digest(make_workload("tiny-2class-G16")) == _digest(make_workload("tiny-2class-G16"))
+    assert _digest(make_workload("paper-shaped-2class-G16", orders=[3, 7])) == _digest(make_workload("paper-shaped-2class-G16", orders=[3, 7]))
 
 
 def test_order_subset_matches_full_rows():
-    full = make_workload(1, orders=list(range(6)))
-    sub = make_workload(1, orders=[2, 5])
+    full = make_workload("paper-shaped-2class-G16", orders=list(range(6)))
+    sub = make_workload("paper-shaped-2class-G16", orders=[2, 5])
     for j, o in enumerate([2, 5]):
         np.testing.assert_array_equal(sub.intervals.cap_lo[j], full.intervals.cap_lo[o])
         np.testing.assert_array_equal(sub.intervals.measured[j], full.intervals.measured[o])
@@ -31,11 +31,11 @@ def test_order_subset_matches_full_rows():
         np.testing.assert_array_equal(sub.tail_s[j], full.tail_s[o])
 
 
-@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
-def test_structure(cfg):
-    w = make_workload(cfg, orders=[0, 1], with_samples=(cfg < 3))
+@pytest.mark.parametrize("name", list(WORKLOADS))
+def test_structure(name):
+    c = WORKLOADS[name]
+    w = make_workload(name, orders=[0, 1], with_samples=(c["G"] <= 64))
     p, iv = w.problem, w.intervals
-    c = CONFIGS[cfg]
     assert p.n_classes == c["K"] and p.budget == c["G"] and list(p.tp) == c["tp"]
     assert iv.cap_lo.shape == (2, p.n_cells)
     for a in (iv.cap_lo, iv.cap_hi):
