@@ -246,3 +246,137 @@ def certify(problem, intervals, eps: float = 0.05) -> CertifyResult:
 def pairwise_sum(x) -> float:
     x = np.ascontiguousarray(x, dtype=np.float64)
     return float(_load().orc_pairwise_sum(_ptr(x, ctypes.c_double), len(x)))
+
+
+# ---------------------------------------------------------- profiling loop --
+# Duration of one profiling cell; a reveal costs this times the cell's TP
+# degree in GPU-seconds (Section 5: 300-second cells, cost = duration x GPUs).
+CELL_SECONDS = 300.0
+POLICY_SCORE, POLICY_ORDER = 0, 1
+
+
+@dataclass
+class LoopResult:
+    state: np.ndarray        # [O] int32 certificate state when the loop ended
+    finished: np.ndarray     # [O] uint8: 1 = certified, or no unmeasured candidate was left
+    rounds: np.ndarray       # [O] int32 reveals made
+    gpu_seconds: np.ndarray  # [O] float64: CELL_SECONDS x TP summed over the reveals
+    reveals: np.ndarray      # [O][max_rounds] int32 candidate revealed in each round, -1 after the end
+    final: list              # [O] Alloc returned (the conservative allocation A-)
+    tau_truth: np.ndarray    # [O] float32: the returned allocation's objective on the true table
+    tau_oracle: np.ndarray   # [O] float32: the optimum of the true table
+    regret: np.ndarray       # [O] float64: tau_oracle - tau_truth
+
+
+def value_on_table(problem, alloc: Alloc, cap, tail) -> np.float32:
+    """Objective level (2) of a fixed allocation on a point table: the
+    smallest fulfillment over the classes, an empty class counting 0."""
+    ref = _ProblemRef(problem)
+    K, T, B = len(ref.demand), len(ref.tp), len(ref.levels)
+    v = np.float32(np.inf)
+    for i in range(K):
+        r = alloc.replicas[i]
+        if r == 0:
+            return np.float32(0.0)
+        b = bucket(problem, i, r)
+        cell = (i * T + alloc.tp_index[i]) * B + b
+        v = min(v, fulfillment(problem, i, float(cap[cell]), float(tail[cell]), r))
+    return np.float32(v)
+
+
+def profile_loop(problem, intervals, truth_cap, truth_tail, cand, cap_s, tail_s, eps: float = 0.05,
+                 policy: int = POLICY_SCORE, order=None, max_rounds: int = None,
+                 n_threads: int = 1) -> LoopResult:
+    """Algorithm 1 (the profiling loop) for O independent trajectories, each
+    starting from its own row of ``intervals`` (the common initial design).
+    Per round, for every trajectory still running: the conservative and
+    optimistic allocations and the certificate (Section 4.2); a certified
+    state (feasible or infeasible) ends the trajectory and returns A-;
+    otherwise one unmeasured candidate is revealed -- its cell's intervals
+    collapse to the true values truth_cap[o][cell], truth_tail[o][cell] and
+    it becomes measured -- at a cost of CELL_SECONDS x TP GPU-seconds.  The
+    revealed candidate is the score's argmax (Section 4.3; POLICY_SCORE) or,
+    for the comparison, the first unmeasured one in order[o] (POLICY_ORDER,
+    e.g. a uniform random permutation).  A trajectory with no unmeasured
+    candidate left returns A- undecided (the certificate of its final
+    intervals is evaluated first, so a last reveal can still certify).  The
+    allocation's value on the true table gives the decision regret against
+    the true optimum.  The intervals are not refitted
+    between rounds; the samples of a candidate stay valid because its
+    intervals only change when it is revealed.  After max_rounds reveals
+    (default: the number of candidates) the trajectory stops undecided."""
+    ref = _ProblemRef(problem)
+    N = ref.n_cells
+    cl = np.array(intervals.cap_lo, dtype=np.float32).reshape(-1, N)
+    O = cl.shape[0]
+    ch = np.array(intervals.cap_hi, dtype=np.float32).reshape(O, N)
+    tl = np.array(intervals.tail_lo, dtype=np.float32).reshape(O, N)
+    th = np.array(intervals.tail_hi, dtype=np.float32).reshape(O, N)
+    ms = np.array(intervals.measured, dtype=np.uint8).reshape(O, N)
+    tc = np.asarray(truth_cap, dtype=np.float32).reshape(O, N)
+    tt = np.asarray(truth_tail, dtype=np.float32).reshape(O, N)
+    cand = np.asarray(cand, dtype=np.int32)
+    E = len(cand)
+    R = E if max_rounds is None else int(max_rounds)
+    state = np.zeros(O, np.int32)
+    finished = np.zeros(O, np.uint8)
+    rounds = np.zeros(O, np.int32)
+    gpu_s = np.zeros(O, np.float64)
+    reveals = np.full((O, R), -1, np.int32)
+    final = [None] * O
+    running = np.ones(O, bool)
+
+    class _Rows:  # the running trajectories' intervals, for the primitives
+        def __init__(self, idx):
+            self.cap_lo, self.cap_hi, self.tail_lo, self.tail_hi = cl[idx], ch[idx], tl[idx], th[idx]
+            self.measured = ms[idx]
+
+    for rnd in range(R + 1):
+        idx = np.nonzero(running)[0]
+        if len(idx) == 0:
+            break
+        cert = certify(problem, _Rows(idx), eps)
+        for j, o in enumerate(idx):
+            state[o] = cert.state[j]
+            final[o] = cert.cons[j]
+            if cert.state[j] != UNDECIDED:
+                finished[o] = 1
+                running[o] = False
+            elif all(ms[o, c] for c in cand):  # no unmeasured candidate: A- undecided
+                finished[o] = 1
+                running[o] = False
+        if rnd == R:
+            break
+        idx = np.nonzero(running)[0]
+        if len(idx) == 0:
+            break
+        if policy == POLICY_SCORE:
+            sc = score(problem, _Rows(idx), cand, np.asarray(cap_s)[idx], np.asarray(tail_s)[idx],
+                       dump=False, n_threads=n_threads)
+            picks = [int(b) for b in sc.best]
+        else:
+            picks = []
+            for o in idx:
+                pick = -1
+                for e in order[o]:
+                    if not ms[o, cand[e]]:
+                        pick = int(e)
+                        break
+                picks.append(pick)
+        for o, e in zip(idx, picks):
+            cell = int(cand[e])
+            cl[o, cell] = ch[o, cell] = tc[o, cell]
+            tl[o, cell] = th[o, cell] = tt[o, cell]
+            ms[o, cell] = 1
+            t = int(ref.tp[(cell // len(ref.levels)) % len(ref.tp)])
+            gpu_s[o] += CELL_SECONDS * t
+            reveals[o, rounds[o]] = e
+            rounds[o] += 1
+
+    tau_truth = np.zeros(O, np.float32)
+    tau_oracle = np.zeros(O, np.float32)
+    for o in range(O):
+        tau_oracle[o] = np.float32(solve(problem, tc[o], tt[o]).tau)
+        tau_truth[o] = value_on_table(problem, final[o], tc[o], tt[o])
+    regret = tau_oracle.astype(np.float64) - tau_truth.astype(np.float64)
+    return LoopResult(state, finished, rounds, gpu_s, reveals, final, tau_truth, tau_oracle, regret)
