@@ -209,6 +209,72 @@ fs_status fs_certify(fs_context *ctx, const fs_problem *p, fs_intervals iv, int3
                      float eps, int32_t *d_state, fs_alloc cons, fs_alloc opt, double *d_gap,
                      void *d_workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* Reveal rule of fs_profile_loop. */
+typedef enum fs_policy {
+  FS_POLICY_SCORE = 0,  /* the candidate with the largest score (Section 4.3, Algorithm 1) */
+  FS_POLICY_ORDER = 1   /* the first unmeasured candidate of a caller-given order
+                         * (for comparisons, e.g. a uniform random permutation) */
+} fs_policy;
+
+/* Duration of one profiling cell in seconds: a reveal costs this times the
+ * cell's TP degree in GPU-seconds (Section 5). */
+#define FS_CELL_SECONDS 300.0
+
+/* Outputs of fs_profile_loop, device memory, one entry per trajectory. */
+typedef struct fs_loop_out {
+  int32_t *state;       /* [O] certificate state when the trajectory ended (fs_cert)       */
+  uint8_t *finished;    /* [O] 1 = certified, or no unmeasured candidate was left;
+                         *     0 = stopped by the round limit                               */
+  int32_t *rounds;      /* [O] reveals made                                                 */
+  double *gpu_seconds;  /* [O] FS_CELL_SECONDS x TP degree summed over the reveals          */
+  int32_t *reveals;     /* [O][max_rounds] candidate revealed in each round, -1 after the
+                         * end; or NULL                                                     */
+  fs_alloc final_alloc; /* [O] the returned allocation: the conservative allocation A- of
+                         * the trajectory's last certificate (any field may be NULL)         */
+  float *tau_truth;     /* [O] objective level (2) of the returned allocation on the true
+                         * table (smallest fulfillment over the classes, an unserved class
+                         * counting 0); or NULL                                             */
+  float *tau_oracle;    /* [O] optimum of the true table (fs_solve_batch); or NULL           */
+} fs_loop_out;
+
+/* Workspace bytes for fs_profile_loop with these sizes. */
+fs_status fs_loop_workspace_size(const fs_problem *p, int32_t n_orders, int32_t n_cand,
+                                 int32_t n_samples, size_t *bytes);
+
+/* The profiling loop (Algorithm 1) for n_orders independent trajectories.
+ * Trajectory o starts from row o of iv (its initial design; iv is read only,
+ * the loop works on a copy in the workspace).  Each round, for every
+ * trajectory still running:
+ *   1. the certificate (as fs_certify, tolerance eps);  a certified state
+ *      (feasible or infeasible) ends the trajectory and returns A-;
+ *   2. if no candidate is left unmeasured, the trajectory ends undecided and
+ *      returns A-;
+ *   3. otherwise one candidate is revealed: under FS_POLICY_SCORE the argmax
+ *      of fs_score_candidates on the current intervals (same tie rule),
+ *      under FS_POLICY_ORDER the first unmeasured candidate of
+ *      d_order[o][0..n_cand) (entries outside [0, n_cand) are skipped).  Its
+ *      cell's capacity and tail intervals collapse to the true values
+ *      d_truth_cap[o][cell], d_truth_tail[o][cell] ([n_orders][N]), the cell
+ *      becomes measured, and the trajectory is charged FS_CELL_SECONDS x TP.
+ * After max_rounds reveals a trajectory gets one more certificate (steps 1-2)
+ * and then stops (finished = 0 if still undecided).  The intervals are not
+ * refitted between rounds: the samples d_cap_s, d_tail_s
+ * ([n_orders][n_cand][n_samples], drawn inside the initial intervals) stay
+ * valid, since a candidate's intervals change only when it is revealed.
+ * check_every > 0: every check_every rounds the call waits for the stream
+ * and returns early once no trajectory is running (the call then returns
+ * with the stream idle); check_every = 0: exactly max_rounds rounds are
+ * enqueued without waiting.  Limits as fs_score_candidates; max_rounds in
+ * [0, 65535]; critical floors are supported (the scorer then solves every
+ * scenario in full). */
+fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders,
+                          const float *d_truth_cap, const float *d_truth_tail,
+                          const int32_t *d_cand, int32_t n_cand, const float *d_cap_s,
+                          const float *d_tail_s, int32_t n_samples, float eps, fs_policy policy,
+                          const int32_t *d_order, int32_t max_rounds, int32_t check_every,
+                          fs_loop_out out, void *d_workspace, size_t workspace_bytes,
+                          hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

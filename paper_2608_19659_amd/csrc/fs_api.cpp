@@ -21,6 +21,7 @@ struct fs_context {
   int spl;           // exclusion scorer samples per lane (0 = default)
   int waves;         // exclusion scorer grid in wavefronts (0 = default)
   int setup;         // exclusion scorer set-up: 0 automatic, 1 general
+  int32_t *pinned;   // pinned host word: running trajectories read back by fs_profile_loop
   struct Timed {
     hipEvent_t begin, end;
     int launches;
@@ -147,12 +148,17 @@ fs_status fs_context_create(int hip_device, fs_context **out) {
   if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
   if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
     return fail(FS_ERR_UNSUPPORTED, std::string("libfleetsieve is built for gfx950, device is ") + prop.gcnArchName);
-  *out = new fs_context{hip_device, 0, 0, 0, 0, 0, {}};
+  int32_t *pinned = nullptr;
+  e = hipSetDevice(hip_device);
+  if (e == hipSuccess) e = hipHostMalloc((void **)&pinned, 64, hipHostMallocDefault);
+  if (e != hipSuccess) return hip_fail(e, "hipHostMalloc");
+  *out = new fs_context{hip_device, 0, 0, 0, 0, 0, pinned, {}};
   return FS_OK;
 }
 
 void fs_context_destroy(fs_context *ctx) {
   if (!ctx) return;
+  if (ctx->pinned) (void)hipHostFree(ctx->pinned);
   for (auto &ev : ctx->events) {
     (void)hipEventDestroy(ev.begin);
     (void)hipEventDestroy(ev.end);
@@ -330,6 +336,114 @@ fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals
   }
   e = fs::launch_score(P, a, stream);
   if (e != hipSuccess) return hip_fail(e, "score launch");
+  return FS_OK;
+}
+
+fs_status fs_loop_workspace_size(const fs_problem *p, int32_t n_orders, int32_t n_cand, int32_t n_samples,
+                                 size_t *bytes) {
+  if (!bytes) return fail(FS_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  if (n_orders < 0 || n_cand < 0 || n_samples < 0) return fail(FS_ERR_INVALID_ARGUMENT, "sizes must be >= 0");
+  fs::DevProblem P;
+  fs_status st = make_problem(p, &P);
+  if (st != FS_OK) return st;
+  *bytes = fs::loop_layout(P, n_orders, n_cand, n_cand > 0 ? n_samples : 0).total;
+  return FS_OK;
+}
+
+fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders,
+                          const float *d_truth_cap, const float *d_truth_tail, const int32_t *d_cand,
+                          int32_t n_cand, const float *d_cap_s, const float *d_tail_s, int32_t n_samples,
+                          float eps, fs_policy policy, const int32_t *d_order, int32_t max_rounds,
+                          int32_t check_every, fs_loop_out out, void *d_workspace, size_t workspace_bytes,
+                          hipStream_t stream) {
+  if (!ctx) return fail(FS_ERR_INVALID_ARGUMENT, "context is NULL");
+  fs::DevProblem P;
+  fs_status st = make_problem(p, &P);
+  if (st != FS_OK) return st;
+  if (n_orders < 0 || n_orders > 65535) return fail(FS_ERR_INVALID_ARGUMENT, "n_orders must be in [0, 65535]");
+  if (n_cand < 0 || n_cand > 65535) return fail(FS_ERR_INVALID_ARGUMENT, "n_cand must be in [0, 65535]");
+  if (max_rounds < 0 || max_rounds > 65535) return fail(FS_ERR_INVALID_ARGUMENT, "max_rounds must be in [0, 65535]");
+  if (check_every < 0) return fail(FS_ERR_INVALID_ARGUMENT, "check_every must be >= 0");
+  if (std::isnan(eps)) return fail(FS_ERR_INVALID_ARGUMENT, "eps must not be NaN");
+  if (policy != FS_POLICY_SCORE && policy != FS_POLICY_ORDER)
+    return fail(FS_ERR_INVALID_ARGUMENT, "policy must be FS_POLICY_SCORE or FS_POLICY_ORDER");
+  if (policy == FS_POLICY_SCORE && n_cand > 0 && (n_samples < 1 || n_samples > FS_MAX_SAMPLES))
+    return fail(FS_ERR_INVALID_ARGUMENT, "n_samples must be in [1, 2^20]");
+  if (n_orders > 0 && (!iv.cap_lo || !iv.cap_hi || !iv.tail_lo || !iv.tail_hi || !iv.measured))
+    return fail(FS_ERR_INVALID_ARGUMENT, "interval arrays are NULL");
+  if (n_orders > 0 && (!d_truth_cap || !d_truth_tail))
+    return fail(FS_ERR_INVALID_ARGUMENT, "true tables are NULL");
+  if (n_orders > 0 && n_cand > 0 && !d_cand) return fail(FS_ERR_INVALID_ARGUMENT, "candidates are NULL");
+  if (n_orders > 0 && n_cand > 0 && policy == FS_POLICY_SCORE && (!d_cap_s || !d_tail_s))
+    return fail(FS_ERR_INVALID_ARGUMENT, "sample arrays are NULL");
+  if (n_orders > 0 && n_cand > 0 && policy == FS_POLICY_ORDER && !d_order)
+    return fail(FS_ERR_INVALID_ARGUMENT, "the reveal order is NULL");
+  if (n_orders > 0 && (!out.state || !out.finished || !out.rounds || !out.gpu_seconds))
+    return fail(FS_ERR_INVALID_ARGUMENT, "state, finished, rounds and gpu_seconds outputs are required");
+  int kernel = ctx->score_kernel;
+  if (kernel == 0) kernel = fs::excl_kernel_supported(P) ? 3 : 1;
+  if (kernel == 2 && !fs::lane_kernel_supported(P))
+    return fail(FS_ERR_UNSUPPORTED,
+                "lane-per-scenario scoring needs no floors, TP set {1,2,4,8} and budget 16, 32 or 64");
+  if (kernel == 3 && !fs::excl_kernel_supported(P))
+    return fail(FS_ERR_UNSUPPORTED, "exclusion scoring does not handle critical floors");
+  const int32_t S = (n_cand > 0 && policy == FS_POLICY_SCORE) ? n_samples : 0;
+  const fs::LoopLayout LL = fs::loop_layout(P, n_orders, n_cand, S);
+  if (!d_workspace) return fail(FS_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  if (workspace_bytes < LL.total)
+    return fail(FS_ERR_WORKSPACE_TOO_SMALL, "workspace needs " + std::to_string(LL.total) + " bytes");
+  if (n_orders == 0) return FS_OK;
+  DeviceGuard dg(ctx->device);
+  if (dg.err != hipSuccess) return hip_fail(dg.err, "hipSetDevice");
+  uint8_t *ws = (uint8_t *)d_workspace;
+  fs::LoopDev D = fs::loop_dev(LL, ws, n_orders);
+  D.state = out.state;
+  D.finished = out.finished;
+  D.rounds = out.rounds;
+  D.gpu_seconds = out.gpu_seconds;
+  D.reveals = out.reveals;
+  D.max_rounds = max_rounds;
+  const size_t cells = (size_t)n_orders * P.N;
+  hipError_t e = hipMemcpyAsync(D.cap_lo, iv.cap_lo, 4 * cells, hipMemcpyDeviceToDevice, stream);
+  if (e == hipSuccess) e = hipMemcpyAsync(D.cap_hi, iv.cap_hi, 4 * cells, hipMemcpyDeviceToDevice, stream);
+  if (e == hipSuccess) e = hipMemcpyAsync(D.tail_lo, iv.tail_lo, 4 * cells, hipMemcpyDeviceToDevice, stream);
+  if (e == hipSuccess) e = hipMemcpyAsync(D.tail_hi, iv.tail_hi, 4 * cells, hipMemcpyDeviceToDevice, stream);
+  if (e == hipSuccess) e = hipMemcpyAsync(D.measured, iv.measured, cells, hipMemcpyDeviceToDevice, stream);
+  if (e != hipSuccess) return hip_fail(e, "interval copy");
+  e = fs::launch_setup(P, d_cand, n_cand, ws, LL.score, stream);
+  if (e == hipSuccess) e = fs::launch_loop_init(D, n_orders, stream);
+  if (e != hipSuccess) return hip_fail(e, "loop set-up launch");
+  const fs::AllocOut none{nullptr, nullptr, nullptr, nullptr, nullptr};
+  for (int32_t rnd = 0; rnd <= max_rounds; ++rnd) {
+    e = fs::launch_certify(P, D.cap_lo, D.cap_hi, D.tail_lo, D.tail_hi, D.measured, n_orders, eps, D.cert_state,
+                           D.cons, none, nullptr, ws, LL.score, stream);
+    if (e == hipSuccess) e = fs::launch_loop_decide(P, D, d_cand, n_cand, n_orders, stream);
+    if (e != hipSuccess) return hip_fail(e, "loop certificate launch");
+    if (rnd == max_rounds) break;
+    if (check_every > 0 && rnd > 0 && rnd % check_every == 0) {
+      e = hipMemcpyAsync(ctx->pinned, D.n_running, sizeof(int32_t), hipMemcpyDeviceToHost, stream);
+      if (e == hipSuccess) e = hipStreamSynchronize(stream);
+      if (e != hipSuccess) return hip_fail(e, "loop progress read-back");
+      if (*ctx->pinned == 0) break;
+    }
+    if (policy == FS_POLICY_SCORE && n_cand > 0) {
+      fs::ScoreArgs a{D.cap_lo, D.cap_hi, D.tail_lo, D.tail_hi, D.measured, d_cand, d_cap_s, d_tail_s,
+                      n_orders, n_cand, S, D.score, D.gap_now, D.best, nullptr, ws, LL.score, kernel,
+                      ctx->spl, ctx->waves, ctx->setup, nullptr, nullptr, 1};
+      e = fs::launch_score(P, a, stream);
+      if (e != hipSuccess) return hip_fail(e, "loop score launch");
+    }
+    e = fs::launch_loop_reveal(P, D, d_truth_cap, d_truth_tail, d_cand, n_cand, n_orders, (int32_t)policy,
+                               d_order, stream);
+    if (e != hipSuccess) return hip_fail(e, "loop reveal launch");
+  }
+  e = fs::launch_loop_output(P, D, ws, LL.score, d_truth_cap, d_truth_tail, n_orders, to_out(out.final_alloc),
+                             out.tau_truth, stream);
+  if (e == hipSuccess && out.tau_oracle)
+    e = fs::launch_solve_batch(P, d_truth_cap, d_truth_tail, n_orders,
+                               fs::AllocOut{out.tau_oracle, nullptr, nullptr, nullptr, nullptr}, ws, LL.score,
+                               stream);
+  if (e != hipSuccess) return hip_fail(e, "loop output launch");
   return FS_OK;
 }
 

@@ -124,6 +124,56 @@ hipError_t launch_certify(const DevProblem &P, const float *cap_lo, const float 
                           const float *tail_lo, const float *tail_hi, const uint8_t *measured,
                           int32_t O, float eps, int32_t *state, AllocOut cons, AllocOut opt,
                           double *gap, uint8_t *ws, const WsLayout &L, hipStream_t s);
+// ---- profiling loop (Algorithm 1) -------------------------------------------
+// Device state of fs_profile_loop: a working copy of the intervals, this
+// round's certificate and scores, the allocation each trajectory returns so
+// far, and the caller's per-trajectory outputs.
+struct LoopDev {
+  float *cap_lo, *cap_hi, *tail_lo, *tail_hi;  // [O][N] working intervals
+  uint8_t *measured;                           // [O][N]
+  int32_t *cert_state;                         // [O] this round's certificate
+  AllocOut cons;                               // [O] this round's conservative allocation
+  AllocOut fin;                                // [O] the allocation returned so far
+  double *score, *gap_now;                     // [O][E], [O] this round's scores
+  int32_t *best;                               // [O]
+  uint8_t *running;                            // [O] 1 while the trajectory continues
+  int32_t *n_running;                          // [1] running trajectories after the last decision
+  int32_t *state;                              // [O] caller outputs (fs_loop_out)
+  uint8_t *finished;
+  int32_t *rounds;
+  double *gpu_seconds;
+  int32_t *reveals;                            // [O][max_rounds] or NULL
+  int32_t max_rounds;
+};
+
+// Workspace of fs_profile_loop: the scorer's layout, then the loop's own
+// regions (offsets from the workspace start).
+struct LoopLayout {
+  WsLayout score;
+  size_t cap_lo, cap_hi, tail_lo, tail_hi, measured, cert_state, cons_obj, cons_tp, cons_rep, cons_fm,
+      cons_gp, fin_obj, fin_tp, fin_rep, fin_fm, fin_gp, scores, gap_now, best, running, n_running;
+  size_t total;
+};
+
+LoopLayout loop_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S);
+LoopDev loop_dev(const LoopLayout &L, uint8_t *ws, int64_t O);
+
+hipError_t launch_loop_init(const LoopDev &L, int32_t O, hipStream_t s);
+// After a certificate: trajectories that certified or have no unmeasured
+// candidate end (their candidates are then marked measured, so the scorer
+// skips them); every running trajectory takes A- as its allocation so far.
+hipError_t launch_loop_decide(const DevProblem &P, const LoopDev &L, const int32_t *cand, int32_t E,
+                              int32_t O, hipStream_t s);
+// Reveals one candidate of every running trajectory (policy 0: best[o],
+// policy 1: the first unmeasured one of order[o]).
+hipError_t launch_loop_reveal(const DevProblem &P, const LoopDev &L, const float *truth_cap,
+                              const float *truth_tail, const int32_t *cand, int32_t E, int32_t O,
+                              int32_t policy, const int32_t *order, hipStream_t s);
+// Copies the returned allocations out and evaluates them on the true table.
+hipError_t launch_loop_output(const DevProblem &P, const LoopDev &L, const uint8_t *ws, const WsLayout &SL,
+                              const float *truth_cap, const float *truth_tail, int32_t O, AllocOut out,
+                              float *tau_truth, hipStream_t s);
+
 // Device-side input checks (FS_VALIDATE=1): flag[0] counts bad cell values,
 // flag[1] candidate indices outside [0, N).  Zero the flags first.
 hipError_t launch_zero_flags(int32_t *flag, hipStream_t s);

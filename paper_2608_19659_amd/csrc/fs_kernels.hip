@@ -118,6 +118,13 @@ __device__ __forceinline__ int wave_min_dpp(int v) {
              min(__builtin_amdgcn_readlane(v, 32), __builtin_amdgcn_readlane(v, 48)));
 }
 
+// Sum over the 64 lanes (wave-uniform result; every lane must be active).
+__device__ __forceinline__ int wave_sum_int(int v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
 // Inclusive prefix maximum of nonnegative values across the 64 lanes: DPP
 // shifts by 1, 2, 4, 8 within each row (a lane with no source takes 0), then
 // every row takes the totals of the rows before it (by readlane).
@@ -2119,6 +2126,131 @@ __global__ __launch_bounds__(64) void k_certify(DevProblem P, const int8_t *__re
   state[o] = st;
 }
 
+// ---------------------------------------------------------------------------
+// Profiling loop (Algorithm 1): per-trajectory bookkeeping between the
+// certificate and scoring launches.
+// ---------------------------------------------------------------------------
+// Seconds one profiling cell runs (Section 5); a reveal costs this x TP.
+constexpr double kCellSeconds = 300.0;
+
+__global__ void k_loop_init(LoopDev L, int32_t O) {
+  const int o = blockIdx.x * blockDim.x + threadIdx.x;
+  if (o >= O) return;
+  L.running[o] = 1;
+  L.state[o] = 0;
+  L.finished[o] = 0;
+  L.rounds[o] = 0;
+  L.gpu_seconds[o] = 0.0;
+  if (L.reveals)
+    for (int j = 0; j < L.max_rounds; ++j) L.reveals[(size_t)o * L.max_rounds + j] = -1;
+}
+
+// One block strides over the trajectories and counts those still running.
+__global__ __launch_bounds__(256) void k_loop_decide(DevProblem P, LoopDev L, const int32_t *__restrict__ cand,
+                                                     int32_t E, int32_t O) {
+  __shared__ int s_count[4];
+  int count = 0;
+  for (int o = threadIdx.x; o < O; o += blockDim.x) {
+    if (!L.running[o]) continue;
+    const size_t off = (size_t)o * P.N;
+    const int st = L.cert_state[o];
+    L.state[o] = st;
+    L.fin.objective[o] = L.cons.objective[o];
+    L.fin.floors_met[o] = L.cons.floors_met[o];
+    L.fin.goodput[o] = L.cons.goodput[o];
+    for (int k = 0; k < P.K; ++k) {
+      L.fin.tp_index[(size_t)o * P.K + k] = L.cons.tp_index[(size_t)o * P.K + k];
+      L.fin.replicas[(size_t)o * P.K + k] = L.cons.replicas[(size_t)o * P.K + k];
+    }
+    bool end = st != 0;  // certified feasible or infeasible
+    if (!end) {          // else: no unmeasured candidate left
+      end = true;
+      for (int e = 0; e < E && end; ++e) {
+        const int c = cand[e];
+        if (c >= 0 && c < P.N && !L.measured[off + c]) end = false;
+      }
+    }
+    if (end) {
+      L.finished[o] = 1;
+      L.running[o] = 0;
+      for (int e = 0; e < E; ++e) {
+        const int c = cand[e];
+        if (c >= 0 && c < P.N) L.measured[off + c] = 1;
+      }
+    } else {
+      ++count;
+    }
+  }
+  count = wave_sum_int(count);
+  if ((threadIdx.x & (kWave - 1)) == 0) s_count[threadIdx.x >> 6] = count;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int total = 0;
+    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) total += s_count[w];
+    *L.n_running = total;
+  }
+}
+
+__global__ void k_loop_reveal(DevProblem P, LoopDev L, const float *__restrict__ truth_cap,
+                              const float *__restrict__ truth_tail, const int32_t *__restrict__ cand, int32_t E,
+                              int32_t O, int32_t policy, const int32_t *__restrict__ order) {
+  const int o = blockIdx.x * blockDim.x + threadIdx.x;
+  if (o >= O || !L.running[o]) return;
+  const size_t off = (size_t)o * P.N;
+  int pick = -1;
+  if (policy == 0) {
+    pick = L.best[o];
+  } else {
+    for (int j = 0; j < E; ++j) {
+      const int e = order[(size_t)o * E + j];
+      if (e < 0 || e >= E) continue;
+      const int c = cand[e];
+      if (c >= 0 && c < P.N && !L.measured[off + c]) {
+        pick = e;
+        break;
+      }
+    }
+  }
+  if (pick < 0 || pick >= E) return;
+  const int cell = cand[pick];
+  if (cell < 0 || cell >= P.N) return;
+  L.cap_lo[off + cell] = L.cap_hi[off + cell] = truth_cap[off + cell];
+  L.tail_lo[off + cell] = L.tail_hi[off + cell] = truth_tail[off + cell];
+  L.measured[off + cell] = 1;
+  L.gpu_seconds[o] += kCellSeconds * (double)P.tp[(cell / P.B) % P.NT];
+  if (L.reveals && L.rounds[o] < L.max_rounds) L.reveals[(size_t)o * L.max_rounds + L.rounds[o]] = pick;
+  L.rounds[o] += 1;
+}
+
+// The returned allocation's objective level (2) on the true table: the
+// smallest fulfillment over the classes, an unserved class counting 0.
+__global__ void k_loop_output(DevProblem P, LoopDev L, const int8_t *__restrict__ bmap,
+                              const float *__restrict__ truth_cap, const float *__restrict__ truth_tail,
+                              int32_t O, AllocOut out, float *__restrict__ tau_truth) {
+  const int o = blockIdx.x * blockDim.x + threadIdx.x;
+  if (o >= O) return;
+  const size_t off = (size_t)o * P.N;
+  if (out.objective) out.objective[o] = L.fin.objective[o];
+  if (out.floors_met) out.floors_met[o] = L.fin.floors_met[o];
+  if (out.goodput) out.goodput[o] = L.fin.goodput[o];
+  float v = __builtin_inff();
+  bool unserved = false;
+  for (int k = 0; k < P.K; ++k) {
+    const int ti = L.fin.tp_index[(size_t)o * P.K + k];
+    const int r = L.fin.replicas[(size_t)o * P.K + k];
+    if (out.tp_index) out.tp_index[(size_t)o * P.K + k] = (uint8_t)ti;
+    if (out.replicas) out.replicas[(size_t)o * P.K + k] = (uint16_t)r;
+    if (r == 0) {
+      unserved = true;
+      continue;
+    }
+    const int cell = cell_of(P, k, ti, bmap[k * (P.G + 1) + r]);
+    v = fminf(v, __int_as_float(ratio_bits(truth_cap[off + cell], truth_tail[off + cell], r, P.slo[k],
+                                           P.rcp_demand[k])));
+  }
+  if (tau_truth) tau_truth[o] = unserved ? 0.0f : v;
+}
+
 __global__ void k_zero_flags(int32_t *__restrict__ flag) {
   if (threadIdx.x < 4) flag[threadIdx.x] = 0;
 }
@@ -2368,6 +2500,91 @@ hipError_t launch_certify(const DevProblem &P, const float *cap_lo, const float 
   k_certify<<<O, 64, lds_bytes_solver(P, 2), s>>>(P, (const int8_t *)(ws + L.bmap), cap_lo, cap_hi,
                                                   tail_lo, tail_hi, measured, eps, state, cons, opt,
                                                   gap);
+  return hipGetLastError();
+}
+
+LoopLayout loop_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
+  LoopLayout L{};
+  L.score = ws_layout(P, O, E, S);
+  size_t at = L.score.total;
+  const size_t ON = (size_t)O * P.N, OK = (size_t)O * P.K;
+  auto take = [&](size_t bytes) {
+    const size_t here = at;
+    at = align256(at + (bytes > 0 ? bytes : 1));
+    return here;
+  };
+  L.cap_lo = take(4 * ON);
+  L.cap_hi = take(4 * ON);
+  L.tail_lo = take(4 * ON);
+  L.tail_hi = take(4 * ON);
+  L.measured = take(ON);
+  L.cert_state = take(4 * (size_t)O);
+  L.cons_obj = take(4 * (size_t)O);
+  L.cons_tp = take(OK);
+  L.cons_rep = take(2 * OK);
+  L.cons_fm = take((size_t)O);
+  L.cons_gp = take(4 * (size_t)O);
+  L.fin_obj = take(4 * (size_t)O);
+  L.fin_tp = take(OK);
+  L.fin_rep = take(2 * OK);
+  L.fin_fm = take((size_t)O);
+  L.fin_gp = take(4 * (size_t)O);
+  L.scores = take(8 * (size_t)O * (size_t)E);
+  L.gap_now = take(8 * (size_t)O);
+  L.best = take(4 * (size_t)O);
+  L.running = take((size_t)O);
+  L.n_running = take(4);
+  L.total = at;
+  return L;
+}
+
+LoopDev loop_dev(const LoopLayout &L, uint8_t *ws, int64_t O) {
+  (void)O;
+  LoopDev d{};
+  d.cap_lo = (float *)(ws + L.cap_lo);
+  d.cap_hi = (float *)(ws + L.cap_hi);
+  d.tail_lo = (float *)(ws + L.tail_lo);
+  d.tail_hi = (float *)(ws + L.tail_hi);
+  d.measured = ws + L.measured;
+  d.cert_state = (int32_t *)(ws + L.cert_state);
+  d.cons = AllocOut{(float *)(ws + L.cons_obj), ws + L.cons_tp, (uint16_t *)(ws + L.cons_rep), ws + L.cons_fm,
+                    (float *)(ws + L.cons_gp)};
+  d.fin = AllocOut{(float *)(ws + L.fin_obj), ws + L.fin_tp, (uint16_t *)(ws + L.fin_rep), ws + L.fin_fm,
+                   (float *)(ws + L.fin_gp)};
+  d.score = (double *)(ws + L.scores);
+  d.gap_now = (double *)(ws + L.gap_now);
+  d.best = (int32_t *)(ws + L.best);
+  d.running = ws + L.running;
+  d.n_running = (int32_t *)(ws + L.n_running);
+  return d;
+}
+
+hipError_t launch_loop_init(const LoopDev &L, int32_t O, hipStream_t s) {
+  if (O == 0) return hipSuccess;
+  k_loop_init<<<(O + 255) / 256, 256, 0, s>>>(L, O);
+  return hipGetLastError();
+}
+
+hipError_t launch_loop_decide(const DevProblem &P, const LoopDev &L, const int32_t *cand, int32_t E,
+                              int32_t O, hipStream_t s) {
+  k_loop_decide<<<1, 256, 0, s>>>(P, L, cand, E, O);
+  return hipGetLastError();
+}
+
+hipError_t launch_loop_reveal(const DevProblem &P, const LoopDev &L, const float *truth_cap,
+                              const float *truth_tail, const int32_t *cand, int32_t E, int32_t O,
+                              int32_t policy, const int32_t *order, hipStream_t s) {
+  if (O == 0) return hipSuccess;
+  k_loop_reveal<<<(O + 63) / 64, 64, 0, s>>>(P, L, truth_cap, truth_tail, cand, E, O, policy, order);
+  return hipGetLastError();
+}
+
+hipError_t launch_loop_output(const DevProblem &P, const LoopDev &L, const uint8_t *ws, const WsLayout &SL,
+                              const float *truth_cap, const float *truth_tail, int32_t O, AllocOut out,
+                              float *tau_truth, hipStream_t s) {
+  if (O == 0) return hipSuccess;
+  k_loop_output<<<(O + 63) / 64, 64, 0, s>>>(P, L, (const int8_t *)(ws + SL.bmap), truth_cap, truth_tail, O,
+                                             out, tau_truth);
   return hipGetLastError();
 }
 

@@ -31,7 +31,9 @@ KERNEL_AUTO, KERNEL_WAVE, KERNEL_LANE, KERNEL_EXCLUSION = 0, 1, 2, 3
 EXPORTED = ("fs_context_create", "fs_context_destroy", "fs_context_set_option", "fs_context_kernel_timing",
             "fs_last_error",
             "fs_validate_problem", "fs_workspace_size", "fs_solve_batch", "fs_score_candidates",
-            "fs_certify")
+            "fs_certify", "fs_loop_workspace_size", "fs_profile_loop")
+POLICY_SCORE, POLICY_ORDER = 0, 1
+CELL_SECONDS = 300.0
 
 
 class FleetSieveError(RuntimeError):
@@ -60,6 +62,12 @@ class _Alloc(ctypes.Structure):
                 ("goodput", ctypes.c_void_p)]
 
 
+class _LoopOut(ctypes.Structure):
+    _fields_ = [("state", ctypes.c_void_p), ("finished", ctypes.c_void_p), ("rounds", ctypes.c_void_p),
+                ("gpu_seconds", ctypes.c_void_p), ("reveals", ctypes.c_void_p), ("final_alloc", _Alloc),
+                ("tau_truth", ctypes.c_void_p), ("tau_oracle", ctypes.c_void_p)]
+
+
 _lib = None
 
 
@@ -85,6 +93,9 @@ def load_library():
     lib.fs_score_candidates.argtypes = [vp, P, _Intervals, i32, vp, i32, vp, vp, i32, vp, vp, vp, vp,
                                         vp, sz, vp]
     lib.fs_certify.argtypes = [vp, P, _Intervals, i32, ctypes.c_float, vp, _Alloc, _Alloc, vp, vp, sz, vp]
+    lib.fs_loop_workspace_size.argtypes = [P, i32, i32, i32, ctypes.POINTER(sz)]
+    lib.fs_profile_loop.argtypes = [vp, P, _Intervals, i32, vp, vp, vp, i32, vp, vp, i32, ctypes.c_float,
+                                    ctypes.c_int, vp, i32, i32, _LoopOut, vp, sz, vp]
     for name in EXPORTED:
         if name != "fs_context_destroy":
             getattr(lib, name).restype = ctypes.c_int
@@ -338,3 +349,59 @@ def certify(ctx: Context, problem, iv: DeviceIntervals, eps: float = 0.05, strea
                                      _alloc_struct(cons), _alloc_struct(opt), gap.data_ptr(), ws.data_ptr(),
                                      ws.numel(), _stream(dev, stream)))
     return CertifyOutput(state, gap, cons, opt)
+
+
+def loop_workspace_size(problem, n_orders: int, n_cand: int, n_samples: int) -> int:
+    ref = _ProblemRef(problem)
+    out = ctypes.c_size_t()
+    _check(load_library().fs_loop_workspace_size(ref.ptr, int(n_orders), int(n_cand), int(n_samples),
+                                                 ctypes.byref(out)))
+    return int(out.value)
+
+
+@dataclass
+class LoopOutput:
+    state: object        # [O] int32
+    finished: object     # [O] uint8
+    rounds: object       # [O] int32
+    gpu_seconds: object  # [O] float64
+    reveals: object      # [O, max_rounds] int32
+    final: dict          # [O] allocation tensors (objective, tp_index, replicas, floors_met, goodput)
+    tau_truth: object    # [O] float32
+    tau_oracle: object   # [O] float32
+
+
+def profile_loop(ctx: Context, problem, iv: DeviceIntervals, truth_cap, truth_tail, cand, cap_s, tail_s,
+                 eps: float = 0.05, policy: int = POLICY_SCORE, order=None, max_rounds: int | None = None,
+                 check_every: int = 4, stream=None, workspace=None) -> LoopOutput:
+    """The profiling loop (fs_profile_loop) for O trajectories.  iv holds
+    the initial designs [O, N]; truth_cap / truth_tail are float32 [O, N]
+    device tensors; order is an int32 [O, E] device tensor (policy
+    POLICY_ORDER) or None.  max_rounds defaults to E."""
+    torch = _torch()
+    ref = _ProblemRef(problem)
+    O = int(iv.cap_lo.shape[0])
+    E = int(cand.shape[0])
+    S = int(cap_s.shape[2]) if (E > 0 and policy == POLICY_SCORE) else 0
+    R = E if max_rounds is None else int(max_rounds)
+    dev = iv.cap_lo.device
+    ivs = _intervals_struct(iv, O, ref.N)
+    ptc = _dev_ptr(truth_cap, torch.float32, (O, ref.N), "truth_cap")
+    ptt = _dev_ptr(truth_tail, torch.float32, (O, ref.N), "truth_tail")
+    pcand = _dev_ptr(cand, torch.int32, (E,), "cand")
+    pcs = _dev_ptr(cap_s, torch.float32, (O, E, S), "cap_s") if S else None
+    pts = _dev_ptr(tail_s, torch.float32, (O, E, S), "tail_s") if S else None
+    pord = _dev_ptr(order, torch.int32, (O, E), "order") if order is not None else None
+    out = LoopOutput(torch.empty(O, dtype=torch.int32, device=dev), torch.empty(O, dtype=torch.uint8, device=dev),
+                     torch.empty(O, dtype=torch.int32, device=dev), torch.empty(O, dtype=torch.float64, device=dev),
+                     torch.empty((O, R), dtype=torch.int32, device=dev), _alloc_tensors(O, ref.K, dev),
+                     torch.empty(O, dtype=torch.float32, device=dev), torch.empty(O, dtype=torch.float32, device=dev))
+    lo = _LoopOut(out.state.data_ptr(), out.finished.data_ptr(), out.rounds.data_ptr(), out.gpu_seconds.data_ptr(),
+                  out.reveals.data_ptr() if R > 0 else None, _alloc_struct(out.final), out.tau_truth.data_ptr(),
+                  out.tau_oracle.data_ptr())
+    ws_bytes = loop_workspace_size(problem, O, E, S)
+    ws = workspace if workspace is not None else ctx.workspace(ws_bytes)
+    _check(load_library().fs_profile_loop(ctx.handle, ref.ptr, ivs, O, ptc, ptt, pcand, E, pcs, pts, S,
+                                          float(eps), int(policy), pord, R, int(check_every), lo, ws.data_ptr(),
+                                          ws.numel(), _stream(dev, stream)))
+    return out
