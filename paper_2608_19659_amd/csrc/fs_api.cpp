@@ -421,7 +421,9 @@ fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv,
     if (e != hipSuccess) return hip_fail(e, "loop certificate launch");
     if (rnd == max_rounds) break;
     if (check_every > 0 && rnd > 0 && rnd % check_every == 0) {
-      e = hipMemcpyAsync(ctx->pinned, D.n_running, sizeof(int32_t), hipMemcpyDeviceToHost, stream);
+      e = fs::launch_loop_count(D, n_orders, stream);
+      if (e == hipSuccess)
+        e = hipMemcpyAsync(ctx->pinned, D.n_running, sizeof(int32_t), hipMemcpyDeviceToHost, stream);
       if (e == hipSuccess) e = hipStreamSynchronize(stream);
       if (e != hipSuccess) return hip_fail(e, "loop progress read-back");
       if (*ctx->pinned == 0) break;

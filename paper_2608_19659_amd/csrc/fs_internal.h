@@ -137,7 +137,7 @@ struct LoopDev {
   double *score, *gap_now;                     // [O][E], [O] this round's scores
   int32_t *best;                               // [O]
   uint8_t *running;                            // [O] 1 while the trajectory continues
-  int32_t *n_running;                          // [1] running trajectories after the last decision
+  int32_t *n_running;                          // [1] running trajectories (launch_loop_count)
   int32_t *state;                              // [O] caller outputs (fs_loop_out)
   uint8_t *finished;
   int32_t *rounds;
@@ -164,6 +164,8 @@ hipError_t launch_loop_init(const LoopDev &L, int32_t O, hipStream_t s);
 // skips them); every running trajectory takes A- as its allocation so far.
 hipError_t launch_loop_decide(const DevProblem &P, const LoopDev &L, const int32_t *cand, int32_t E,
                               int32_t O, hipStream_t s);
+// Counts the running trajectories into n_running.
+hipError_t launch_loop_count(const LoopDev &L, int32_t O, hipStream_t s);
 // Reveals one candidate of every running trajectory (policy 0: best[o],
 // policy 1: the first unmeasured one of order[o]).
 hipError_t launch_loop_reveal(const DevProblem &P, const LoopDev &L, const float *truth_cap,

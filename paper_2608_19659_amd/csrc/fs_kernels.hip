@@ -1202,6 +1202,10 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
 // Largest budget and class count of the one-block-per-order set-up.
 constexpr int kPrepOrderMaxG = kWave;
 constexpr int kPrepOrderMaxK = 16;
+// Wavefronts per block of the per-order set-up: one per class, and at least
+// this many so the work-list block has threads enough (a class block's
+// wavefronts beyond K only help stage the order).
+constexpr int kPrepOrderMinWaves = 8;
 
 // The scorer's work list, built by one block from staged inputs: the
 // candidates' cells and every order's revealed flags are read into LDS in
@@ -1323,9 +1327,10 @@ __device__ void prep_list_staged(const DevProblem &P, int O, const uint8_t *__re
 
 // Set-up of the exclusion scorer when the budget fits one wavefront
 // (G <= 64) and K <= 16: one block per (order o, realisation R) --
-// block 2 o + R -- with one wavefront per class, and block 2 O builds the
-// work list.  R = 0 is the conservative corner (low capacity, high tail),
-// R = 1 the optimistic one (Section 4.1).  The same quantities as the
+// block 2 o + R -- with one wavefront per class (and idle ones up to
+// kPrepOrderMinWaves), and block 2 O builds the work list.  R = 0 is the
+// conservative corner (low capacity, high tail), R = 1 the optimistic one
+// (Section 4.1).  The same quantities as the
 // general set-up, with fewer barriers:
 //   1. all threads: the order's cells and candidates into LDS; the load
 //      level of every (class, r) (the count of grid levels below
@@ -1388,13 +1393,13 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
     if (R == 0) mrow[c] = measured[off + c];
   }
   for (int e = tid; e < E; e += nth) ccand[e] = cand[e];
-  if (lane < G) {  // wavefront k: the levels of class k, r = lane + 1
+  if (wave < K && lane < G) {  // wavefront k: the levels of class k, r = lane + 1
     const float per_replica = P.demand[wave] / (float)(lane + 1);
     int b = 0;
     for (int j = 0; j < B; ++j) b += P.levels[j] < per_replica ? 1 : 0;
     lvl[wave * G + lane] = (int8_t)(b < B ? b : -1);
   }
-  for (int c = lane; c < per_class; c += kWave) {
+  for (int c = lane; wave < K && c < per_class; c += kWave) {
     mc[c] = INT_MIN;
     crlo[c] = INT_MAX;
     crhi[c] = -1;
@@ -1403,7 +1408,7 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
 
   // --- 2. wavefront k: B_k (options cost t r < G <= 64, so r < 64: one
   // lane per replica count)
-  {
+  if (wave < K) {
     const int k = wave;
     int *T = Bt + k * G;
     if (lane < G) T[lane] = 0;  // no option: ratio 0
@@ -1428,6 +1433,7 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
   __syncthreads();
 
   // --- 3. wavefront i on its own from here
+  if (wave >= K) return;
   const int i = wave;
   int top = 1;
   while (2 * top <= G) top <<= 1;  // 2 * top > G >= g + 1
@@ -2145,73 +2151,77 @@ __global__ void k_loop_init(LoopDev L, int32_t O) {
     for (int j = 0; j < L.max_rounds; ++j) L.reveals[(size_t)o * L.max_rounds + j] = -1;
 }
 
-// One block strides over the trajectories and counts those still running.
-__global__ __launch_bounds__(256) void k_loop_decide(DevProblem P, LoopDev L, const int32_t *__restrict__ cand,
-                                                     int32_t E, int32_t O) {
-  __shared__ int s_count[4];
-  int count = 0;
-  for (int o = threadIdx.x; o < O; o += blockDim.x) {
-    if (!L.running[o]) continue;
-    const size_t off = (size_t)o * P.N;
-    const int st = L.cert_state[o];
+// One wavefront per trajectory: the lanes look at 64 candidates at a time.
+__global__ __launch_bounds__(64) void k_loop_decide(DevProblem P, LoopDev L, const int32_t *__restrict__ cand,
+                                                    int32_t E, int32_t O) {
+  const int o = blockIdx.x, lane = threadIdx.x;
+  if (!L.running[o]) return;
+  const size_t off = (size_t)o * P.N;
+  const int st = L.cert_state[o];
+  if (lane == 0) {
     L.state[o] = st;
     L.fin.objective[o] = L.cons.objective[o];
     L.fin.floors_met[o] = L.cons.floors_met[o];
     L.fin.goodput[o] = L.cons.goodput[o];
-    for (int k = 0; k < P.K; ++k) {
-      L.fin.tp_index[(size_t)o * P.K + k] = L.cons.tp_index[(size_t)o * P.K + k];
-      L.fin.replicas[(size_t)o * P.K + k] = L.cons.replicas[(size_t)o * P.K + k];
-    }
-    bool end = st != 0;  // certified feasible or infeasible
-    if (!end) {          // else: no unmeasured candidate left
-      end = true;
-      for (int e = 0; e < E && end; ++e) {
-        const int c = cand[e];
-        if (c >= 0 && c < P.N && !L.measured[off + c]) end = false;
-      }
-    }
-    if (end) {
-      L.finished[o] = 1;
-      L.running[o] = 0;
-      for (int e = 0; e < E; ++e) {
-        const int c = cand[e];
-        if (c >= 0 && c < P.N) L.measured[off + c] = 1;
-      }
-    } else {
-      ++count;
-    }
   }
-  count = wave_sum_int(count);
-  if ((threadIdx.x & (kWave - 1)) == 0) s_count[threadIdx.x >> 6] = count;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int total = 0;
-    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) total += s_count[w];
-    *L.n_running = total;
+  for (int k = lane; k < P.K; k += kWave) {
+    L.fin.tp_index[(size_t)o * P.K + k] = L.cons.tp_index[(size_t)o * P.K + k];
+    L.fin.replicas[(size_t)o * P.K + k] = L.cons.replicas[(size_t)o * P.K + k];
+  }
+  bool end = st != 0;  // certified feasible or infeasible
+  if (!end) {          // else: no unmeasured candidate left
+    bool open = false;
+    for (int e0 = 0; e0 < E && !open; e0 += kWave) {
+      const int e = e0 + lane;
+      const int c = e < E ? cand[e] : -1;
+      open = __ballot(c >= 0 && c < P.N && !L.measured[off + c]) != 0;
+    }
+    end = !open;
+  }
+  if (!end) return;
+  if (lane == 0) {
+    L.finished[o] = 1;
+    L.running[o] = 0;
+  }
+  for (int e = lane; e < E; e += kWave) {  // the scorer skips a finished trajectory
+    const int c = cand[e];
+    if (c >= 0 && c < P.N) L.measured[off + c] = 1;
   }
 }
 
-__global__ void k_loop_reveal(DevProblem P, LoopDev L, const float *__restrict__ truth_cap,
-                              const float *__restrict__ truth_tail, const int32_t *__restrict__ cand, int32_t E,
-                              int32_t O, int32_t policy, const int32_t *__restrict__ order) {
-  const int o = blockIdx.x * blockDim.x + threadIdx.x;
-  if (o >= O || !L.running[o]) return;
+// Running trajectories, for the host's early-exit check.
+__global__ __launch_bounds__(256) void k_loop_count(LoopDev L, int32_t O) {
+  __shared__ int s_count[4];
+  int count = 0;
+  for (int o = threadIdx.x; o < O; o += blockDim.x) count += L.running[o] ? 1 : 0;
+  count = wave_sum_int(count);
+  if ((threadIdx.x & (kWave - 1)) == 0) s_count[threadIdx.x >> 6] = count;
+  __syncthreads();
+  if (threadIdx.x == 0) *L.n_running = s_count[0] + s_count[1] + s_count[2] + s_count[3];
+}
+
+// One wavefront per trajectory; under a fixed order the lanes look at 64
+// entries of the order at a time and the first unmeasured one wins.
+__global__ __launch_bounds__(64) void k_loop_reveal(DevProblem P, LoopDev L, const float *__restrict__ truth_cap,
+                                                    const float *__restrict__ truth_tail,
+                                                    const int32_t *__restrict__ cand, int32_t E, int32_t O,
+                                                    int32_t policy, const int32_t *__restrict__ order) {
+  const int o = blockIdx.x, lane = threadIdx.x;
+  if (!L.running[o]) return;
   const size_t off = (size_t)o * P.N;
   int pick = -1;
   if (policy == 0) {
     pick = L.best[o];
   } else {
-    for (int j = 0; j < E; ++j) {
-      const int e = order[(size_t)o * E + j];
-      if (e < 0 || e >= E) continue;
-      const int c = cand[e];
-      if (c >= 0 && c < P.N && !L.measured[off + c]) {
-        pick = e;
-        break;
-      }
+    for (int j0 = 0; j0 < E && pick < 0; j0 += kWave) {
+      const int j = j0 + lane;
+      const int e = j < E ? order[(size_t)o * E + j] : -1;
+      const int c = (e >= 0 && e < E) ? cand[e] : -1;
+      const uint64_t m = __ballot(c >= 0 && c < P.N && !L.measured[off + c]);
+      if (m) pick = __shfl(e, __builtin_ctzll(m), kWave);
     }
   }
-  if (pick < 0 || pick >= E) return;
+  if (lane != 0 || pick < 0 || pick >= E) return;
   const int cell = cand[pick];
   if (cell < 0 || cell >= P.N) return;
   L.cap_lo[off + cell] = L.cap_hi[off + cell] = truth_cap[off + cell];
@@ -2382,7 +2392,8 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
     const int dump = a.tau_dump != nullptr;
     const size_t small = prep_lds_small(P), big = small + prep_lds_tables(P);
     if (a.setup == 0 && prep_order_fits(P, a.O, a.E))
-      k_prep_order<<<2 * a.O + 1, P.K * kWave, prep_order_lds(P, a.O, a.E), s>>>(
+      k_prep_order<<<2 * a.O + 1, (P.K > kPrepOrderMinWaves ? P.K : kPrepOrderMinWaves) * kWave,
+                     prep_order_lds(P, a.O, a.E), s>>>(
           P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured, a.cand, a.E, a.O, dump, tiles, base, mopt,
           thr, n_thr, list, live);
     else if (big <= kPrepLdsLimit)
@@ -2567,7 +2578,13 @@ hipError_t launch_loop_init(const LoopDev &L, int32_t O, hipStream_t s) {
 
 hipError_t launch_loop_decide(const DevProblem &P, const LoopDev &L, const int32_t *cand, int32_t E,
                               int32_t O, hipStream_t s) {
-  k_loop_decide<<<1, 256, 0, s>>>(P, L, cand, E, O);
+  if (O == 0) return hipSuccess;
+  k_loop_decide<<<O, kWave, 0, s>>>(P, L, cand, E, O);
+  return hipGetLastError();
+}
+
+hipError_t launch_loop_count(const LoopDev &L, int32_t O, hipStream_t s) {
+  k_loop_count<<<1, 256, 0, s>>>(L, O);
   return hipGetLastError();
 }
 
@@ -2575,7 +2592,7 @@ hipError_t launch_loop_reveal(const DevProblem &P, const LoopDev &L, const float
                               const float *truth_tail, const int32_t *cand, int32_t E, int32_t O,
                               int32_t policy, const int32_t *order, hipStream_t s) {
   if (O == 0) return hipSuccess;
-  k_loop_reveal<<<(O + 63) / 64, 64, 0, s>>>(P, L, truth_cap, truth_tail, cand, E, O, policy, order);
+  k_loop_reveal<<<O, kWave, 0, s>>>(P, L, truth_cap, truth_tail, cand, E, O, policy, order);
   return hipGetLastError();
 }
 
