@@ -1202,10 +1202,15 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
 // Largest budget and class count of the one-block-per-order set-up.
 constexpr int kPrepOrderMaxG = kWave;
 constexpr int kPrepOrderMaxK = 16;
-// Wavefronts per block of the per-order set-up: one per class, and at least
-// this many so the work-list block has threads enough (a class block's
-// wavefronts beyond K only help stage the order).
-constexpr int kPrepOrderMinWaves = 8;
+// Wavefronts per block of the per-order set-up: one per class, and one per
+// 1024 listed tiles (at most 16) so the work-list block has threads enough
+// for large lists; a class block's wavefronts beyond K only help stage the
+// order (extra wavefronts make its barriers slower, so small lists keep K).
+static int prep_order_waves(const DevProblem &P, int64_t O, int64_t E) {
+  const int64_t by_list = (O * E + 1023) / 1024;
+  const int64_t w = by_list > P.K ? by_list : P.K;
+  return (int)(w < 16 ? w : 16);
+}
 
 // The scorer's work list, built by one block from staged inputs: the
 // candidates' cells and every order's revealed flags are read into LDS in
@@ -1327,8 +1332,8 @@ __device__ void prep_list_staged(const DevProblem &P, int O, const uint8_t *__re
 
 // Set-up of the exclusion scorer when the budget fits one wavefront
 // (G <= 64) and K <= 16: one block per (order o, realisation R) --
-// block 2 o + R -- with one wavefront per class (and idle ones up to
-// kPrepOrderMinWaves), and block 2 O builds the work list.  R = 0 is the
+// block 2 o + R -- with one wavefront per class (and idle ones when the
+// list is large), and block 2 O builds the work list.  R = 0 is the
 // conservative corner (low capacity, high tail), R = 1 the optimistic one
 // (Section 4.1).  The same quantities as the
 // general set-up, with fewer barriers:
@@ -2392,8 +2397,7 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
     const int dump = a.tau_dump != nullptr;
     const size_t small = prep_lds_small(P), big = small + prep_lds_tables(P);
     if (a.setup == 0 && prep_order_fits(P, a.O, a.E))
-      k_prep_order<<<2 * a.O + 1, (P.K > kPrepOrderMinWaves ? P.K : kPrepOrderMinWaves) * kWave,
-                     prep_order_lds(P, a.O, a.E), s>>>(
+      k_prep_order<<<2 * a.O + 1, prep_order_waves(P, a.O, a.E) * kWave, prep_order_lds(P, a.O, a.E), s>>>(
           P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured, a.cand, a.E, a.O, dump, tiles, base, mopt,
           thr, n_thr, list, live);
     else if (big <= kPrepLdsLimit)
