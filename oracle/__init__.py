@@ -380,3 +380,85 @@ def profile_loop(problem, intervals, truth_cap, truth_tail, cand, cap_s, tail_s,
         tau_truth[o] = value_on_table(problem, final[o], tc[o], tt[o])
     regret = tau_oracle.astype(np.float64) - tau_truth.astype(np.float64)
     return LoopResult(state, finished, rounds, gpu_s, reveals, final, tau_truth, tau_oracle, regret)
+
+
+# ------------------------------------------------ multi-metric feasibility --
+@dataclass
+class Policy:
+    """Class policy of Eq. 5 in full: a configuration is feasible only if
+    every tail metric m is within limit[i][m] and (when given) its success
+    probability is at least success_min[i].  limit [K][M] (+inf = no limit),
+    success_min [K] or None."""
+    limit: np.ndarray
+    success_min: np.ndarray = None
+
+    @property
+    def n_metrics(self) -> int:
+        return int(np.asarray(self.limit).shape[1])
+
+
+def feasible_cells(problem, policy: Policy, tails, success=None) -> np.ndarray:
+    """Feasibility of each cell under the class policy (Eq. 5): tails is
+    [..., N, M] (metric fastest), success [..., N] or None.  Binary32
+    comparisons, inclusive limits."""
+    ref = _ProblemRef(problem)
+    K, T, B = len(ref.demand), len(ref.tp), len(ref.levels)
+    lim = np.asarray(policy.limit, np.float32).reshape(K, -1)
+    cls = np.repeat(np.arange(K), T * B)
+    tails = np.asarray(tails, np.float32)
+    ok = np.all(tails <= lim[cls], axis=-1)
+    if policy.success_min is not None:
+        smin = np.asarray(policy.success_min, np.float32)
+        ok &= np.asarray(success, np.float32) >= smin[cls]
+    return ok
+
+
+def pseudo_tail(ok) -> np.ndarray:
+    """A single tail value per cell that carries the policy: 0 when the cell
+    is feasible, +inf when it is not; a problem with every SLO at 0 then
+    tests exactly the policy."""
+    return np.where(ok, np.float32(0.0), np.float32(np.inf)).astype(np.float32)
+
+
+def reduce_intervals(problem, policy: Policy, intervals, tail_lo_m, tail_hi_m, succ_lo=None, succ_hi=None):
+    """Single-metric intervals equivalent to multi-metric ones: the
+    conservative side (upper tail bounds, lower success bound) becomes
+    tail_hi, the optimistic side (lower tails, upper success) tail_lo."""
+    from types import SimpleNamespace
+    hi = pseudo_tail(feasible_cells(problem, policy, tail_hi_m, succ_lo))
+    lo = pseudo_tail(feasible_cells(problem, policy, tail_lo_m, succ_hi))
+    return SimpleNamespace(cap_lo=intervals.cap_lo, cap_hi=intervals.cap_hi, tail_lo=lo, tail_hi=hi,
+                           measured=intervals.measured)
+
+
+def solve_policy_brute(problem, policy: Policy, cap, tails, success=None) -> float:
+    """Max-min fulfillment with the full policy applied option by option,
+    by enumeration (tiny problems only; objective level (2) without floors):
+    each class takes one option (TP t, r replicas) on cell (i, t, bucket(r))
+    or nothing, Sum t r <= G."""
+    import itertools
+    ref = _ProblemRef(problem)
+    K, T, B, G = len(ref.demand), len(ref.tp), len(ref.levels), int(problem.budget)
+    lim = np.asarray(policy.limit, np.float32).reshape(K, -1)
+    tails = np.asarray(tails, np.float32).reshape(K * T * B, -1)
+    opts = []
+    for i in range(K):
+        o = [(0, np.float32(0.0))]
+        for t in range(T):
+            for r in range(1, G // int(ref.tp[t]) + 1):
+                b = bucket(problem, i, r)
+                if b < 0:
+                    continue
+                cell = (i * T + t) * B + b
+                ok = bool(np.all(tails[cell] <= lim[i]))
+                if policy.success_min is not None:
+                    ok = ok and np.float32(success[cell]) >= np.float32(policy.success_min[i])
+                cap_r = np.float32(np.float32(r) * np.float32(cap[cell]))
+                f = min(np.float32(1.0), np.float32(cap_r / np.float32(ref.demand[i]))) if ok else np.float32(0.0)
+                o.append((int(ref.tp[t]) * r, np.float32(f)))
+        opts.append(o)
+    best = np.float32(0.0)
+    for combo in itertools.product(*opts):
+        if sum(c for c, _ in combo) <= G:
+            best = max(best, min(f for _, f in combo))
+    return float(best)

@@ -312,3 +312,81 @@ def random_problem(seed: int, K: int, tp, G: int, n_levels: int, critical: bool 
     if critical:
         floor = np.where(rng.random(K) < 0.5, np.rint(rng.uniform(0.25, 4.0, size=K) * 4) / 4, 0.0)
     return Problem(tp=tp, levels=levels, demand=demand, slo=slo, budget=G, floor_rps=floor)
+
+
+# --------------------------------------------- several metrics per cell --
+@dataclass
+class PolicyInputs:
+    """A second tail metric (TTFT-p99) and a success probability per cell
+    for a workload, with the class policy that bounds them (Section 5: chat
+    success >= 99%, TTFT-p99 <= 2 s, completion-p99 <= 30 s; code success
+    >= 99%, TTFT-p99 <= 5 s).  Metric 0 is the workload's own tail
+    (completion), metric 1 the TTFT.  Revealed cells hold the hidden truth."""
+    limit: np.ndarray        # [K][2] per-class limits (completion, TTFT)
+    success_min: np.ndarray  # [K]
+    tail_lo: np.ndarray      # [O][N][2]
+    tail_hi: np.ndarray      # [O][N][2]
+    succ_lo: np.ndarray      # [O][N]
+    succ_hi: np.ndarray      # [O][N]
+    truth_tail: np.ndarray   # [N][2]
+    truth_succ: np.ndarray   # [N]
+    tail_s: np.ndarray       # [O][E][S][2] or None
+    succ_s: np.ndarray       # [O][E][S] or None
+
+
+def make_policy_inputs(w: Workload, with_samples: bool = True) -> PolicyInputs:
+    """TTFT intervals (lognormal around a third of the class's TTFT limit,
+    growing with load, shrinking with TP like the completion tail) and
+    success intervals near the 99% floor, drawn with the workload's seed."""
+    p = w.problem
+    K, T, B, N = p.n_classes, p.n_tp, p.n_levels, p.n_cells
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([w.seed, 5])))
+    if K == 2:
+        ttft_limit = np.array([2.0, 5.0], np.float32)
+    else:
+        ttft_limit = (np.asarray(p.slo, np.float32) / 10.0).astype(np.float32)
+    limit = np.stack([np.asarray(p.slo, np.float32), ttft_limit], axis=1)
+    success_min = np.full(K, 0.99, np.float32)
+    ttft_lo0 = np.zeros(N, np.float32)
+    ttft_hi0 = np.zeros(N, np.float32)
+    succ_lo0 = np.zeros(N, np.float32)
+    succ_hi0 = np.zeros(N, np.float32)
+    for i in range(K):
+        for t in range(T):
+            rho = TAIL_TP_FACTOR[int(p.tp[t])]
+            for b in range(B):
+                cell = p.cell(i, t, b)
+                med = (float(ttft_limit[i]) / 3.0) * (1.0 + float(p.levels[b])) ** 0.5 * rho
+                lo = np.float32(med * np.exp(0.4 * rng.standard_normal()))
+                ttft_lo0[cell] = lo
+                ttft_hi0[cell] = np.float32(float(lo) * (1.0 + rng.uniform(0.1, 0.4)))
+                hi = np.float32(1.0 - 10.0 ** (-rng.uniform(1.8, 4.0)))
+                succ_hi0[cell] = hi
+                succ_lo0[cell] = np.float32(max(0.0, float(hi) - rng.uniform(0.0, 0.02)))
+    truth_ttft = np.clip(ttft_lo0 + rng.random(N).astype(np.float32) * (ttft_hi0 - ttft_lo0),
+                         ttft_lo0, ttft_hi0).astype(np.float32)
+    truth_succ = np.clip(succ_lo0 + rng.random(N).astype(np.float32) * (succ_hi0 - succ_lo0),
+                         succ_lo0, succ_hi0).astype(np.float32)
+    O = w.n_orders
+    m = w.intervals.measured.astype(bool)
+    ttft_lo = np.where(m, truth_ttft, ttft_lo0).astype(np.float32)
+    ttft_hi = np.where(m, truth_ttft, ttft_hi0).astype(np.float32)
+    succ_lo = np.where(m, truth_succ, succ_lo0).astype(np.float32)
+    succ_hi = np.where(m, truth_succ, succ_hi0).astype(np.float32)
+    tail_lo = np.stack([w.intervals.tail_lo, ttft_lo], axis=-1).astype(np.float32)
+    tail_hi = np.stack([w.intervals.tail_hi, ttft_hi], axis=-1).astype(np.float32)
+    truth_tail = np.stack([w.truth_tail, truth_ttft], axis=-1).astype(np.float32)
+    tail_s = succ_s = None
+    if with_samples and w.cap_s is not None:
+        E, S = len(w.cand), w.n_samples
+        tail_s = np.zeros((O, E, S, 2), np.float32)
+        succ_s = np.zeros((O, E, S), np.float32)
+        tail_s[..., 0] = w.tail_s
+        for j, o in enumerate(w.orders):
+            srng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([w.seed, 6, int(o)])))
+            lo, hi = ttft_lo[j][w.cand][:, None], ttft_hi[j][w.cand][:, None]
+            tail_s[j, :, :, 1] = np.clip(lo + srng.random((E, S)).astype(np.float32) * (hi - lo), lo, hi)
+            lo, hi = succ_lo[j][w.cand][:, None], succ_hi[j][w.cand][:, None]
+            succ_s[j] = np.clip(lo + srng.random((E, S)).astype(np.float32) * (hi - lo), lo, hi)
+    return PolicyInputs(limit, success_min, tail_lo, tail_hi, succ_lo, succ_hi, truth_tail, truth_succ,
+                        tail_s, succ_s)
