@@ -420,6 +420,28 @@ def pseudo_tail(ok) -> np.ndarray:
     return np.where(ok, np.float32(0.0), np.float32(np.inf)).astype(np.float32)
 
 
+def feasible_samples(problem, policy: Policy, cand, tail_s, succ_s=None) -> np.ndarray:
+    """Feasibility of candidate samples, each judged by its candidate cell's
+    class (Eq. 5): tail_s [O][E][S][M], succ_s [O][E][S] or None.  A
+    candidate outside the cell range is infeasible."""
+    ref = _ProblemRef(problem)
+    K, T, B = len(ref.demand), len(ref.tp), len(ref.levels)
+    N = K * T * B
+    lim = np.asarray(policy.limit, np.float32).reshape(K, -1)
+    tail_s = np.asarray(tail_s, np.float32)
+    O, E, S, M = tail_s.shape
+    out = np.zeros((O, E, S), bool)
+    for e, c in enumerate(np.asarray(cand, np.int64)):
+        if c < 0 or c >= N:
+            continue
+        i = int(c) // (T * B)
+        ok = np.all(tail_s[:, e] <= lim[i], axis=-1)
+        if policy.success_min is not None:
+            ok &= np.asarray(succ_s, np.float32)[:, e] >= np.float32(policy.success_min[i])
+        out[:, e] = ok
+    return out
+
+
 def reduce_intervals(problem, policy: Policy, intervals, tail_lo_m, tail_hi_m, succ_lo=None, succ_hi=None):
     """Single-metric intervals equivalent to multi-metric ones: the
     conservative side (upper tail bounds, lower success bound) becomes

@@ -335,7 +335,7 @@ class PolicyInputs:
 
 
 def make_policy_inputs(w: Workload, with_samples: bool = True) -> PolicyInputs:
-    """TTFT intervals (lognormal around a third of the class's TTFT limit,
+    """TTFT intervals (lognormal around a quarter of the class's TTFT limit,
     growing with load, shrinking with TP like the completion tail) and
     success intervals near the 99% floor, drawn with the workload's seed."""
     p = w.problem
@@ -356,13 +356,13 @@ def make_policy_inputs(w: Workload, with_samples: bool = True) -> PolicyInputs:
             rho = TAIL_TP_FACTOR[int(p.tp[t])]
             for b in range(B):
                 cell = p.cell(i, t, b)
-                med = (float(ttft_limit[i]) / 3.0) * (1.0 + float(p.levels[b])) ** 0.5 * rho
+                med = (float(ttft_limit[i]) / 4.0) * (1.0 + float(p.levels[b])) ** 0.5 * rho
                 lo = np.float32(med * np.exp(0.4 * rng.standard_normal()))
                 ttft_lo0[cell] = lo
                 ttft_hi0[cell] = np.float32(float(lo) * (1.0 + rng.uniform(0.1, 0.4)))
-                hi = np.float32(1.0 - 10.0 ** (-rng.uniform(1.8, 4.0)))
+                hi = np.float32(1.0 - 10.0 ** (-rng.uniform(2.0, 4.0)))
                 succ_hi0[cell] = hi
-                succ_lo0[cell] = np.float32(max(0.0, float(hi) - rng.uniform(0.0, 0.02)))
+                succ_lo0[cell] = np.float32(max(0.0, float(hi) - rng.uniform(0.0, 0.005)))
     truth_ttft = np.clip(ttft_lo0 + rng.random(N).astype(np.float32) * (ttft_hi0 - ttft_lo0),
                          ttft_lo0, ttft_hi0).astype(np.float32)
     truth_succ = np.clip(succ_lo0 + rng.random(N).astype(np.float32) * (succ_hi0 - succ_lo0),

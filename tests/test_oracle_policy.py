@@ -62,3 +62,30 @@ def test_single_metric_policy_is_the_slo_test():
         a = oracle.solve(p, cap[j], tail[j])
         b = oracle.solve(_zero_slo(p), cap[j], oracle.pseudo_tail(ok))
         assert a.tau == b.tau and a.tp_index == b.tp_index and a.replicas == b.replicas
+
+
+def test_sample_feasibility_is_cell_feasibility_at_the_candidate():
+    """A sample of candidate c is judged exactly as cell c would be with the
+    sample's metrics in its place; limits are inclusive, NaN fails, and a
+    candidate outside the cell range is infeasible."""
+    rng = np.random.default_rng(21)
+    p = random_problem(5, K=3, tp=[1, 2, 4], G=12, n_levels=2)
+    N, M, O, S = p.n_cells, 2, 2, 5
+    lim = np.array([[3.0, 1.0], [np.inf, 2.0], [5.0, np.inf]], np.float32)
+    pol = oracle.Policy(limit=lim, success_min=np.array([0.99, 0.95, 0.9], np.float32))
+    cand = np.array([0, 7, N - 1, 12, N, -1], np.int32)
+    tail_s = rng.uniform(0.0, 6.0, size=(O, len(cand), S, M)).astype(np.float32)
+    succ_s = rng.uniform(0.85, 1.0, size=(O, len(cand), S)).astype(np.float32)
+    tail_s[0, 0, 0] = lim[0]           # exactly at the limits: feasible if success passes
+    succ_s[0, 0, 0] = np.float32(0.99)
+    tail_s[0, 1, 1, 1] = np.nan
+    got = oracle.feasible_samples(p, pol, cand, tail_s, succ_s)
+    assert got[0, 0, 0] and not got[0, 1, 1]
+    assert not got[:, 4:].any()
+    for o in range(O):
+        for e, c in enumerate(cand[:4]):
+            for s in range(S):
+                tails = np.zeros((N, M), np.float32)
+                succ = np.ones(N, np.float32)
+                tails[c], succ[c] = tail_s[o, e, s], succ_s[o, e, s]
+                assert got[o, e, s] == oracle.feasible_cells(p, pol, tails, succ)[c]
