@@ -255,6 +255,127 @@ def loop_bench(args):
     ctx.close()
 
 
+def policy_bench(args):
+    """Class policies with several metrics (Eq. 5 in full) on a workload:
+    a step reduces the conservative and optimistic interval sides (one
+    launch) and every candidate sample (completion-p99, TTFT-p99 and a success probability per
+    cell, under per-class limits and a 99% success floor) to pseudo-tails,
+    then scores the batch with every SLO at 0.  The roofline object reports
+    the sample reduction, an HBM-bound element-wise kernel; the CPU baseline
+    is the oracle (reduction and score) on a bounded sample of tiles."""
+    import numpy as np
+    import torch
+    from types import SimpleNamespace
+    from paper_2608_19659_amd import fleetsieve as fs
+    from paper_2608_19659_amd.synth import WORKLOADS, Intervals, Problem, make_policy_inputs, make_workload
+
+    name = args.workload
+    if name not in WORKLOADS:
+        print(f"unknown workload {name}; choose from {list(WORKLOADS)}", file=sys.stderr)
+        sys.exit(2)
+    dev = "cuda:0"
+    print(f"[bench] policy workload {name}", file=sys.stderr, flush=True)
+    w = make_workload(name)
+    pi = make_policy_inputs(w)
+    p = w.problem
+    p0 = Problem(p.tp, p.levels, p.demand, np.zeros(p.n_classes, np.float32), p.budget)
+    pol = SimpleNamespace(limit=pi.limit, success_min=pi.success_min)
+    O, E, S = w.cap_s.shape
+    M = int(pi.limit.shape[1])
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    # both interval sides in one launch: row block 0 is the conservative side, 1 the optimistic
+    sides_m = t(np.stack([pi.tail_hi, pi.tail_lo]).reshape(2 * O, p.n_cells, -1))
+    sides_s = t(np.stack([pi.succ_lo, pi.succ_hi]).reshape(2 * O, p.n_cells))
+    sides = torch.empty((2, O, p.n_cells), dtype=torch.float32, device=dev)
+    ts_m, ss = t(pi.tail_s), t(pi.succ_s)
+    cand, cap_s = t(w.cand), t(w.cap_s)
+    ctx = fs.Context(0)
+    stream = torch.cuda.current_stream()
+    ctx.set_score_kernel(3 if p.floor_rps is None else 1)
+    iv = fs.DeviceIntervals(t(w.intervals.cap_lo), t(w.intervals.cap_hi), sides[1], sides[0],
+                            t(w.intervals.measured))
+    ts = torch.empty((O, E, S), dtype=torch.float32, device=dev)
+    out = fs.ScoreOutput(torch.empty((O, E), dtype=torch.float64, device=dev),
+                         torch.empty(O, dtype=torch.float64, device=dev),
+                         torch.empty(O, dtype=torch.int32, device=dev), None)
+    ws = ctx.workspace(fs.workspace_size(p0, O, E, S))
+    plan = fs.ScorePlan(ctx, p0, iv, cand, cap_s, ts, out=out, workspace=ws, stream=stream)
+
+    red_iv = fs.ReducePlan.cells(ctx, p, pol, sides_m, sides_s, out=sides.view(2 * O, p.n_cells), stream=stream)
+    red_s = fs.ReducePlan.samples(ctx, p, pol, cand, ts_m, ss, out=ts, stream=stream)
+
+    def step():
+        red_iv.run()
+        red_s.run()
+        plan.run()
+
+    for _ in range(args.warmup):
+        step()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = ev0.elapsed_time(ev1) / args.steps
+    # the sample reduction alone: TIMING_REPEATS back-to-back launches per event pair
+    red_ms = []
+    for _ in range(args.steps):
+        ev0.record(stream)
+        for _ in range(TIMING_REPEATS):
+            red_s.run()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        red_ms.append(ev0.elapsed_time(ev1) / TIMING_REPEATS)
+    red_ms = float(np.mean(red_ms))
+    step()
+    torch.cuda.synchronize()
+
+    import oracle
+    o_pol = oracle.Policy(limit=pi.limit, success_min=pi.success_min)
+    o_iv = oracle.reduce_intervals(p, o_pol, w.intervals, pi.tail_lo, pi.tail_hi, pi.succ_lo, pi.succ_hi)
+    o_ts = oracle.pseudo_tail(oracle.feasible_samples(p, o_pol, w.cand, pi.tail_s, pi.succ_s))
+    reduction_exact = bool(np.array_equal(ts.cpu().numpy().view(np.uint32), o_ts.view(np.uint32))
+                           and np.array_equal(iv.tail_hi.cpu().numpy(), o_iv.tail_hi)
+                           and np.array_equal(iv.tail_lo.cpu().numpy(), o_iv.tail_lo))
+
+    measured_cand = w.intervals.measured[:, w.cand].astype(bool)
+    scenarios = int((~measured_cand).sum()) * S
+    n_samples = O * E * S
+    bytes_per_sample = 4 * M + 4 + 4  # M tail metrics and a success value read, one pseudo-tail written
+    achieved = n_samples * bytes_per_sample / (red_ms / 1e3)
+    cpu = None
+    if not args.no_cpu_baseline:
+        threads = min(os.cpu_count() or 1, 16)
+        print(f"[bench] cpu baseline ({threads} threads)", file=sys.stderr, flush=True)
+        t0 = time.perf_counter()
+        oracle.feasible_samples(p, o_pol, w.cand, pi.tail_s, pi.succ_s)
+        t_red = time.perf_counter() - t0
+        w2 = SimpleNamespace(problem=p0, intervals=Intervals(w.intervals.cap_lo, w.intervals.cap_hi, o_iv.tail_lo,
+                                                             o_iv.tail_hi, w.intervals.measured),
+                             cand=w.cand, cap_s=w.cap_s, tail_s=o_ts)
+        cpu = cpu_baseline(w2, args.cpu_seconds, threads)
+        cpu["sample"] += f"; the oracle's sample reduction over all {n_samples} samples took {t_red:.2f} s"
+    line = {
+        "metric": "allocation scenarios/sec under multi-metric class policies (Eq. 5) on 1 MI355X; oracle-exact",
+        "value": scenarios / (ms_per_step / 1e3), "unit": "scenarios/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"{name} with {M} tail metrics (completion-p99, TTFT-p99) and a success floor: "
+                               f"{p.n_classes} classes, G={p.budget}, {E} candidates x {S} samples x {O} orders",
+                   "scenarios_per_step": scenarios, "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK_BYTES / 1e9, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_BYTES, "traffic": committed_traffic("k_reduce_samples", name),
+                     "kernel": "k_reduce_samples", "bytes_per_sample": bytes_per_sample,
+                     "samples_per_launch": n_samples, "kernel_ms_avg": red_ms},
+        "reduction_matches_oracle": reduction_exact,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    ctx.close()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -277,6 +398,9 @@ def main():
                          "score's argmax against uniform random reveal orders, and the loop's wall time")
     ap.add_argument("--loop-workload", default="paper-shaped-2class-G16",
                     help="workload of --loop (default paper-shaped-2class-G16: 200 reveal orders)")
+    ap.add_argument("--policy", action="store_true",
+                    help="score under multi-metric class policies (completion-p99, TTFT-p99, success floor), "
+                         "reducing intervals and samples on the GPU first")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (scales the HBM byte counters)")
     args = ap.parse_args()
@@ -301,6 +425,9 @@ def main():
 
     if args.loop:
         loop_bench(args)
+        return
+    if args.policy:
+        policy_bench(args)
         return
 
     from paper_2608_19659_amd import fleetsieve as fs

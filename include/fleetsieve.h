@@ -209,6 +209,42 @@ fs_status fs_certify(fs_context *ctx, const fs_problem *p, fs_intervals iv, int3
                      float eps, int32_t *d_state, fs_alloc cons, fs_alloc opt, double *d_gap,
                      void *d_workspace, size_t workspace_bytes, hipStream_t stream);
 
+#define FS_MAX_METRICS 8
+
+/* Class policy with several tail metrics and a success floor (Section 3,
+ * Eq. 5 in full: a selected configuration must keep every tail metric within
+ * its limit and its success probability at least s_min; Section 5 gives chat
+ * success >= 99%, TTFT-p99 <= 2 s, completion-p99 <= 30 s).  Host memory. */
+typedef struct fs_slo_policy {
+  int32_t n_metrics;         /* M in [1, FS_MAX_METRICS]: tail metrics per cell        */
+  const float *limit;        /* [K][M] limit of metric m for class i; +inf = none; not NaN */
+  const float *success_min;  /* [K] success floor, or NULL (no success requirement)      */
+} fs_slo_policy;
+
+/* Feasibility of cells under a policy, as the single tail value every other
+ * call tests: d_out[j][c] = 0 when every tail metric of cell c is within its
+ * class's limit and (when floors are given) its success is at least the
+ * floor, +inf otherwise (a NaN metric fails).  Given the problem with every
+ * slo[i] = 0, the other calls then apply the policy exactly (0 <= 0 holds,
+ * +inf <= 0 does not).  For intervals, reduce the conservative side (upper
+ * tail bounds with the lower success bound) into tail_hi and the optimistic
+ * side (lower tail bounds with the upper success bound) into tail_lo.
+ *   d_tails   [n_rows][N][M] (metric fastest)
+ *   d_success [n_rows][N] or NULL
+ *   d_out     [n_rows][N] */
+fs_status fs_reduce_cells(fs_context *ctx, const fs_problem *p, const fs_slo_policy *pol, const float *d_tails,
+                          const float *d_success, int64_t n_rows, float *d_out, hipStream_t stream);
+
+/* The same for candidate samples, each judged by its candidate's class:
+ *   d_tail_s [n_orders][n_cand][n_samples][M], d_succ_s [n_orders][n_cand][n_samples] or NULL,
+ *   d_out    [n_orders][n_cand][n_samples] (+inf for a candidate outside [0, N)).
+ * n_orders and n_cand at most 65535, n_samples at most FS_MAX_SAMPLES.  With
+ * n_samples a multiple of 4 and 16-byte aligned arrays the kernel moves 4
+ * samples per 16-byte access. */
+fs_status fs_reduce_samples(fs_context *ctx, const fs_problem *p, const fs_slo_policy *pol, const int32_t *d_cand,
+                            int32_t n_cand, const float *d_tail_s, const float *d_succ_s, int32_t n_orders,
+                            int32_t n_samples, float *d_out, hipStream_t stream);
+
 /* Reveal rule of fs_profile_loop. */
 typedef enum fs_policy {
   FS_POLICY_SCORE = 0,  /* the candidate with the largest score (Section 4.3, Algorithm 1) */

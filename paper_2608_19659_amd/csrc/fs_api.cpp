@@ -449,6 +449,79 @@ fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv,
   return FS_OK;
 }
 
+// Checks a policy and fills its kernel-side form.
+static fs_status make_policy(const fs::DevProblem &P, const fs_slo_policy *pol, fs::DevPolicy *Q) {
+  if (!pol) return fail(FS_ERR_INVALID_ARGUMENT, "policy is NULL");
+  if (pol->n_metrics < 1 || pol->n_metrics > FS_MAX_METRICS)
+    return fail(FS_ERR_INVALID_ARGUMENT, "n_metrics must be in [1, 8]");
+  if (!pol->limit) return fail(FS_ERR_INVALID_ARGUMENT, "policy limits are NULL");
+  std::memset(Q, 0, sizeof(*Q));
+  Q->M = pol->n_metrics;
+  Q->per_class = P.NT * P.B;
+  Q->N = P.N;
+  for (int i = 0; i < P.K * Q->M; ++i) {
+    if (std::isnan(pol->limit[i])) return fail(FS_ERR_INVALID_ARGUMENT, "policy limits must not be NaN");
+    Q->limit[i] = pol->limit[i];
+  }
+  if (pol->success_min) {
+    Q->has_success = 1;
+    for (int i = 0; i < P.K; ++i) {
+      if (std::isnan(pol->success_min[i])) return fail(FS_ERR_INVALID_ARGUMENT, "success floors must not be NaN");
+      Q->success_min[i] = pol->success_min[i];
+    }
+  }
+  return FS_OK;
+}
+
+fs_status fs_reduce_cells(fs_context *ctx, const fs_problem *p, const fs_slo_policy *pol, const float *d_tails,
+                          const float *d_success, int64_t n_rows, float *d_out, hipStream_t stream) {
+  if (!ctx) return fail(FS_ERR_INVALID_ARGUMENT, "context is NULL");
+  fs::DevProblem P;
+  fs_status st = make_problem(p, &P);
+  if (st != FS_OK) return st;
+  fs::DevPolicy Q;
+  st = make_policy(P, pol, &Q);
+  if (st != FS_OK) return st;
+  if (n_rows < 0 || n_rows > (int64_t)1 << 40) return fail(FS_ERR_INVALID_ARGUMENT, "n_rows out of range");
+  if (n_rows > 0 && (!d_tails || !d_out)) return fail(FS_ERR_INVALID_ARGUMENT, "tail or output array is NULL");
+  if (n_rows > 0 && Q.has_success && !d_success)
+    return fail(FS_ERR_INVALID_ARGUMENT, "the policy has success floors but the success array is NULL");
+  if (n_rows == 0) return FS_OK;
+  DeviceGuard dg(ctx->device);
+  if (dg.err != hipSuccess) return hip_fail(dg.err, "hipSetDevice");
+  const hipError_t e = fs::launch_reduce_cells(Q, d_tails, d_success, n_rows, d_out, stream);
+  if (e != hipSuccess) return hip_fail(e, "reduce launch");
+  return FS_OK;
+}
+
+fs_status fs_reduce_samples(fs_context *ctx, const fs_problem *p, const fs_slo_policy *pol, const int32_t *d_cand,
+                            int32_t n_cand, const float *d_tail_s, const float *d_succ_s, int32_t n_orders,
+                            int32_t n_samples, float *d_out, hipStream_t stream) {
+  if (!ctx) return fail(FS_ERR_INVALID_ARGUMENT, "context is NULL");
+  fs::DevProblem P;
+  fs_status st = make_problem(p, &P);
+  if (st != FS_OK) return st;
+  fs::DevPolicy Q;
+  st = make_policy(P, pol, &Q);
+  if (st != FS_OK) return st;
+  if (n_orders < 0 || n_orders > 65535) return fail(FS_ERR_INVALID_ARGUMENT, "n_orders must be in [0, 65535]");
+  if (n_cand < 0 || n_cand > 65535) return fail(FS_ERR_INVALID_ARGUMENT, "n_cand must be in [0, 65535]");
+  if (n_samples < 0 || n_samples > FS_MAX_SAMPLES)
+    return fail(FS_ERR_INVALID_ARGUMENT, "n_samples must be in [0, FS_MAX_SAMPLES]");
+  const int64_t n = (int64_t)n_orders * n_cand * n_samples;
+  if (n > 0 && (!d_cand || !d_tail_s || !d_out))
+    return fail(FS_ERR_INVALID_ARGUMENT, "candidate, sample or output array is NULL");
+  if (n > 0 && Q.has_success && !d_succ_s)
+    return fail(FS_ERR_INVALID_ARGUMENT, "the policy has success floors but the success samples are NULL");
+  if (n == 0) return FS_OK;
+  DeviceGuard dg(ctx->device);
+  if (dg.err != hipSuccess) return hip_fail(dg.err, "hipSetDevice");
+  const hipError_t e =
+      fs::launch_reduce_samples(Q, d_cand, n_cand, d_tail_s, d_succ_s, n_orders, n_samples, d_out, stream);
+  if (e != hipSuccess) return hip_fail(e, "reduce launch");
+  return FS_OK;
+}
+
 fs_status fs_certify(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders, float eps,
                      int32_t *d_state, fs_alloc cons, fs_alloc opt, double *d_gap, void *d_workspace,
                      size_t workspace_bytes, hipStream_t stream) {

@@ -176,6 +176,25 @@ hipError_t launch_loop_output(const DevProblem &P, const LoopDev &L, const uint8
                               const float *truth_cap, const float *truth_tail, int32_t O, AllocOut out,
                               float *tau_truth, hipStream_t s);
 
+// ---- class policies with several metrics (Eq. 5 in full) -----------------------
+constexpr int kMaxMetrics = 8;
+
+struct DevPolicy {
+  int32_t M;            // tail metrics per cell
+  int32_t has_success;  // success floors given
+  int32_t per_class;    // cells per class (NT * B)
+  int32_t N;            // cells
+  float limit[kMaxClasses * kMaxMetrics];  // [K][M]
+  float success_min[kMaxClasses];
+};
+
+// out[j] = 0 if cell (j mod N) passes its class's policy, else +inf.
+hipError_t launch_reduce_cells(const DevPolicy &Q, const float *tails, const float *success, int64_t rows,
+                               float *out, hipStream_t s);
+// out[o][e][s] = 0 if the sample passes the policy of cand[e]'s class, else +inf.
+hipError_t launch_reduce_samples(const DevPolicy &Q, const int32_t *cand, int32_t E, const float *tail_s,
+                                 const float *succ_s, int32_t O, int32_t S, float *out, hipStream_t s);
+
 // Device-side input checks (FS_VALIDATE=1): flag[0] counts bad cell values,
 // flag[1] candidate indices outside [0, N).  Zero the flags first.
 hipError_t launch_zero_flags(int32_t *flag, hipStream_t s);

@@ -2266,6 +2266,124 @@ __global__ void k_loop_output(DevProblem P, LoopDev L, const int8_t *__restrict_
   if (tau_truth) tau_truth[o] = unserved ? 0.0f : v;
 }
 
+// ---------------------------------------------------------------------------
+// Class policies with several tail metrics and a success floor (Eq. 5 in
+// full): each cell's (or sample's) metric vector becomes the single tail
+// value the other kernels test against an SLO of 0.  Element-wise and bound
+// by HBM: every block covers one row of cells or one run of a tile's
+// samples, so the class -- and with it the limits, read from the kernel
+// arguments at a uniform offset -- is known per block, and the hot loop does
+// no integer division.
+// ---------------------------------------------------------------------------
+constexpr int kReduceThreads = 256;
+constexpr int kReducePerThread = 4;  // samples per thread
+constexpr int kReduceRun = kReduceThreads * kReducePerThread;
+
+// Metric count: MC > 0 fixed at compile time, MC = 0 read from Q.M.
+template <int MC>
+__device__ __forceinline__ int policy_metrics(const DevPolicy &Q) {
+  return MC > 0 ? MC : Q.M;
+}
+
+// Every metric of t within class k's limits (inclusive; NaN fails).  The
+// tests are combined without short-circuit, so no branch splits the loads.
+template <int MC>
+__device__ __forceinline__ bool metrics_pass(const DevPolicy &Q, int k, const float *__restrict__ t) {
+  const int M = policy_metrics<MC>(Q);
+  bool ok = true;
+#pragma unroll
+  for (int m = 0; m < (MC > 0 ? MC : kMaxMetrics); ++m)
+    if (MC > 0 || m < M) ok &= t[m] <= Q.limit[k * M + m];
+  return ok;
+}
+
+// Cells: blockIdx.y walks the rows, blockIdx.x the 256-cell runs of a row.
+template <int MC>
+__global__ __launch_bounds__(kReduceThreads) void k_reduce_cells(DevPolicy Q, const float *__restrict__ tails,
+                                                                 const float *__restrict__ success, int64_t rows,
+                                                                 float *__restrict__ out) {
+  const int M = policy_metrics<MC>(Q);
+  const int c = (int)blockIdx.x * kReduceThreads + (int)threadIdx.x;
+  if (c >= Q.N) return;
+  const int k = c / Q.per_class;
+  for (int64_t row = blockIdx.y; row < rows; row += gridDim.y) {
+    const size_t j = (size_t)row * Q.N + c;
+    bool ok = metrics_pass<MC>(Q, k, tails + j * M);
+    if (Q.has_success) ok &= success[j] >= Q.success_min[k];
+    out[j] = ok ? 0.0f : __builtin_inff();
+  }
+}
+
+// Samples: blockIdx.y walks the (order, candidate) tiles, blockIdx.x the
+// runs of kReduceRun samples of a tile; the class is that of the tile's
+// candidate.  VEC (S a multiple of 4, arrays 16-byte aligned): a thread owns
+// 4 consecutive samples and moves them with 16-byte loads and stores
+// (M of them for the metrics, which are contiguous per sample).  Otherwise a
+// thread takes samples threadIdx.x, + 256, + 512, + 768 of the run.
+template <int MC, bool VEC>
+__global__ __launch_bounds__(kReduceThreads) void k_reduce_samples(DevPolicy Q, const int32_t *__restrict__ cand,
+                                                                   int32_t E, const float *__restrict__ tail_s,
+                                                                   const float *__restrict__ succ_s, int32_t S,
+                                                                   uint32_t tiles, float *__restrict__ out) {
+  const int M = policy_metrics<MC>(Q);
+  const float inf = __builtin_inff();
+  for (uint32_t tile = blockIdx.y; tile < tiles; tile += gridDim.y) {
+    const int cell = cand[tile % (uint32_t)E];
+    const int k = (cell >= 0 && cell < Q.N) ? cell / Q.per_class : -1;
+    const size_t base = (size_t)tile * S;
+    if constexpr (VEC) {
+      const int s = (int)blockIdx.x * kReduceRun + (int)threadIdx.x * kReducePerThread;
+      if (s >= S) continue;  // S % 4 == 0: samples s .. s + 3 all exist
+      float4 r = make_float4(inf, inf, inf, inf);
+      if (k >= 0) {
+        bool ok[kReducePerThread];
+        // the success values first, so that their load is in flight with the metrics'
+        float4 sc = make_float4(1.0f, 1.0f, 1.0f, 1.0f);
+        float f = 0.0f;
+        if (Q.has_success) {
+          sc = *reinterpret_cast<const float4 *>(succ_s + base + s);
+          f = Q.success_min[k];
+        }
+        if constexpr (MC > 0) {
+          float t[kReducePerThread * MC], lim[MC];
+          const float4 *src = reinterpret_cast<const float4 *>(tail_s + (base + s) * MC);
+#pragma unroll
+          for (int q = 0; q < MC; ++q) {
+            const float4 v = src[q];
+            t[4 * q + 0] = v.x; t[4 * q + 1] = v.y; t[4 * q + 2] = v.z; t[4 * q + 3] = v.w;
+            lim[q] = Q.limit[k * MC + q];
+          }
+#pragma unroll
+          for (int v = 0; v < kReducePerThread; ++v) {
+            ok[v] = true;
+#pragma unroll
+            for (int m = 0; m < MC; ++m) ok[v] &= t[v * MC + m] <= lim[m];
+          }
+        } else {
+#pragma unroll
+          for (int v = 0; v < kReducePerThread; ++v) ok[v] = metrics_pass<0>(Q, k, tail_s + (base + s + v) * M);
+        }
+        if (Q.has_success) {
+          ok[0] &= sc.x >= f; ok[1] &= sc.y >= f;
+          ok[2] &= sc.z >= f; ok[3] &= sc.w >= f;
+        }
+        r = make_float4(ok[0] ? 0.0f : inf, ok[1] ? 0.0f : inf, ok[2] ? 0.0f : inf, ok[3] ? 0.0f : inf);
+      }
+      *reinterpret_cast<float4 *>(out + base + s) = r;
+    } else {
+#pragma unroll
+      for (int v = 0; v < kReducePerThread; ++v) {
+        const int s = (int)blockIdx.x * kReduceRun + v * kReduceThreads + (int)threadIdx.x;
+        if (s >= S) break;
+        bool ok = k >= 0;
+        if (ok) ok = metrics_pass<0>(Q, k, tail_s + (base + s) * M);
+        if (ok && Q.has_success) ok = succ_s[base + s] >= Q.success_min[k];
+        out[base + s] = ok ? 0.0f : inf;
+      }
+    }
+  }
+}
+
 __global__ void k_zero_flags(int32_t *__restrict__ flag) {
   if (threadIdx.x < 4) flag[threadIdx.x] = 0;
 }
@@ -2606,6 +2724,44 @@ hipError_t launch_loop_output(const DevProblem &P, const LoopDev &L, const uint8
   if (O == 0) return hipSuccess;
   k_loop_output<<<(O + 63) / 64, 64, 0, s>>>(P, L, (const int8_t *)(ws + SL.bmap), truth_cap, truth_tail, O,
                                              out, tau_truth);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_cells(const DevPolicy &Q, const float *tails, const float *success, int64_t rows,
+                               float *out, hipStream_t s) {
+  if (rows == 0 || Q.N == 0) return hipSuccess;
+  const dim3 grid((unsigned)((Q.N + kReduceThreads - 1) / kReduceThreads),
+                  (unsigned)(rows < 65535 ? rows : 65535));
+  switch (Q.M) {
+    case 1: k_reduce_cells<1><<<grid, kReduceThreads, 0, s>>>(Q, tails, success, rows, out); break;
+    case 2: k_reduce_cells<2><<<grid, kReduceThreads, 0, s>>>(Q, tails, success, rows, out); break;
+    case 3: k_reduce_cells<3><<<grid, kReduceThreads, 0, s>>>(Q, tails, success, rows, out); break;
+    case 4: k_reduce_cells<4><<<grid, kReduceThreads, 0, s>>>(Q, tails, success, rows, out); break;
+    default: k_reduce_cells<0><<<grid, kReduceThreads, 0, s>>>(Q, tails, success, rows, out); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_samples(const DevPolicy &Q, const int32_t *cand, int32_t E, const float *tail_s,
+                                 const float *succ_s, int32_t O, int32_t S, float *out, hipStream_t s) {
+  const uint32_t tiles = (uint32_t)O * (uint32_t)E;  // O, E <= 65535
+  if (tiles == 0 || S == 0) return hipSuccess;
+  const dim3 grid((unsigned)((S + kReduceRun - 1) / kReduceRun), tiles < 65535 ? tiles : 65535u);
+  auto aligned = [](const void *q) { return ((uintptr_t)q & 15) == 0; };
+  const bool vec = S % 4 == 0 && aligned(tail_s) && aligned(out) && (!Q.has_success || aligned(succ_s));
+#define FS_RED_S(MC, V) k_reduce_samples<MC, V><<<grid, kReduceThreads, 0, s>>>(Q, cand, E, tail_s, succ_s, S, tiles, out)
+  if (!vec) {
+    FS_RED_S(0, false);
+  } else {
+    switch (Q.M) {
+      case 1: FS_RED_S(1, true); break;
+      case 2: FS_RED_S(2, true); break;
+      case 3: FS_RED_S(3, true); break;
+      case 4: FS_RED_S(4, true); break;
+      default: FS_RED_S(0, true); break;
+    }
+  }
+#undef FS_RED_S
   return hipGetLastError();
 }
 

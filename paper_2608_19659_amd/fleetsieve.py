@@ -31,7 +31,7 @@ KERNEL_AUTO, KERNEL_WAVE, KERNEL_LANE, KERNEL_EXCLUSION = 0, 1, 2, 3
 EXPORTED = ("fs_context_create", "fs_context_destroy", "fs_context_set_option", "fs_context_kernel_timing",
             "fs_last_error",
             "fs_validate_problem", "fs_workspace_size", "fs_solve_batch", "fs_score_candidates",
-            "fs_certify", "fs_loop_workspace_size", "fs_profile_loop")
+            "fs_certify", "fs_loop_workspace_size", "fs_profile_loop", "fs_reduce_cells", "fs_reduce_samples")
 POLICY_SCORE, POLICY_ORDER = 0, 1
 CELL_SECONDS = 300.0
 
@@ -60,6 +60,10 @@ class _Alloc(ctypes.Structure):
     _fields_ = [("objective", ctypes.c_void_p), ("tp_index", ctypes.c_void_p),
                 ("replicas", ctypes.c_void_p), ("floors_met", ctypes.c_void_p),
                 ("goodput", ctypes.c_void_p)]
+
+
+class _SloPolicy(ctypes.Structure):
+    _fields_ = [("n_metrics", ctypes.c_int32), ("limit", ctypes.c_void_p), ("success_min", ctypes.c_void_p)]
 
 
 class _LoopOut(ctypes.Structure):
@@ -96,6 +100,9 @@ def load_library():
     lib.fs_loop_workspace_size.argtypes = [P, i32, i32, i32, ctypes.POINTER(sz)]
     lib.fs_profile_loop.argtypes = [vp, P, _Intervals, i32, vp, vp, vp, i32, vp, vp, i32, ctypes.c_float,
                                     ctypes.c_int, vp, i32, i32, _LoopOut, vp, sz, vp]
+    Q = ctypes.POINTER(_SloPolicy)
+    lib.fs_reduce_cells.argtypes = [vp, P, Q, vp, vp, i64, vp, vp]
+    lib.fs_reduce_samples.argtypes = [vp, P, Q, vp, i32, vp, vp, i32, i32, vp, vp]
     for name in EXPORTED:
         if name != "fs_context_destroy":
             getattr(lib, name).restype = ctypes.c_int
@@ -405,3 +412,80 @@ def profile_loop(ctx: Context, problem, iv: DeviceIntervals, truth_cap, truth_ta
                                           float(eps), int(policy), pord, R, int(check_every), lo, ws.data_ptr(),
                                           ws.numel(), _stream(dev, stream)))
     return out
+
+
+class _PolicyRef:
+    """Host copy of a class policy (limit [K][M], success_min [K] or None)."""
+
+    def __init__(self, policy, K):
+        self.limit = np.ascontiguousarray(np.asarray(policy.limit, dtype=np.float32).reshape(K, -1))
+        sm = getattr(policy, "success_min", None)
+        self.smin = None if sm is None else np.ascontiguousarray(sm, dtype=np.float32)
+        self.M = int(self.limit.shape[1])
+        self.s = _SloPolicy(self.M, self.limit.ctypes.data, None if self.smin is None else self.smin.ctypes.data)
+
+    @property
+    def ptr(self):
+        return ctypes.byref(self.s)
+
+
+class ReducePlan:
+    """One fs_reduce_cells or fs_reduce_samples call with its arguments
+    checked and marshalled once; run() enqueues it again on the same device
+    buffers."""
+
+    def __init__(self, fn, args, out, keep):
+        self._fn, self._args, self.out, self._keep = fn, args, out, keep
+
+    def run(self):
+        _check(self._fn(*self._args))
+        return self.out
+
+    @staticmethod
+    def cells(ctx: Context, problem, policy, tails, success=None, out=None, stream=None) -> "ReducePlan":
+        """tails float32 [R, N, M], success float32 [R, N] or None, out [R, N]."""
+        torch = _torch()
+        ref = _ProblemRef(problem)
+        pol = _PolicyRef(policy, ref.K)
+        R = int(tails.shape[0])
+        dev = tails.device
+        pt = _dev_ptr(tails, torch.float32, (R, ref.N, pol.M), "tails")
+        ps = _dev_ptr(success, torch.float32, (R, ref.N), "success") if success is not None else None
+        if out is None:
+            out = torch.empty((R, ref.N), dtype=torch.float32, device=dev)
+        po = _dev_ptr(out, torch.float32, (R, ref.N), "out")
+        return ReducePlan(load_library().fs_reduce_cells,
+                          (ctx.handle, ref.ptr, pol.ptr, pt, ps, R, po, _stream(dev, stream)),
+                          out, (ref, pol, tails, success))
+
+    @staticmethod
+    def samples(ctx: Context, problem, policy, cand, tail_s, succ_s=None, out=None, stream=None) -> "ReducePlan":
+        """cand int32 [E], tail_s float32 [O, E, S, M], succ_s [O, E, S] or None, out [O, E, S]."""
+        torch = _torch()
+        ref = _ProblemRef(problem)
+        pol = _PolicyRef(policy, ref.K)
+        O, E, S = (int(x) for x in tail_s.shape[:3])
+        dev = tail_s.device
+        pc = _dev_ptr(cand, torch.int32, (E,), "cand")
+        pt = _dev_ptr(tail_s, torch.float32, (O, E, S, pol.M), "tail_s")
+        ps = _dev_ptr(succ_s, torch.float32, (O, E, S), "succ_s") if succ_s is not None else None
+        if out is None:
+            out = torch.empty((O, E, S), dtype=torch.float32, device=dev)
+        po = _dev_ptr(out, torch.float32, (O, E, S), "out")
+        return ReducePlan(load_library().fs_reduce_samples,
+                          (ctx.handle, ref.ptr, pol.ptr, pc, E, pt, ps, O, S, po, _stream(dev, stream)),
+                          out, (ref, pol, cand, tail_s, succ_s))
+
+
+def reduce_cells(ctx: Context, problem, policy, tails, success=None, out=None, stream=None):
+    """Pseudo-tails of cells under a class policy (fs_reduce_cells): tails is
+    a float32 [R, N, M] device tensor, success float32 [R, N] or None;
+    returns float32 [R, N] holding 0 (feasible) or +inf."""
+    return ReducePlan.cells(ctx, problem, policy, tails, success, out, stream).run()
+
+
+def reduce_samples(ctx: Context, problem, policy, cand, tail_s, succ_s=None, out=None, stream=None):
+    """Pseudo-tails of candidate samples (fs_reduce_samples): tail_s is a
+    float32 [O, E, S, M] device tensor, succ_s float32 [O, E, S] or None;
+    returns float32 [O, E, S]."""
+    return ReducePlan.samples(ctx, problem, policy, cand, tail_s, succ_s, out, stream).run()
