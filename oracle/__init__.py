@@ -63,6 +63,7 @@ class Alloc:
     goodput: float
     tp_index: list   # -1 = empty
     replicas: list
+    goodput64: float = None  # whole objective only: level (3)'s binary64 total
 
     def tp(self, problem) -> list:
         """GPUs per replica per class (0 = empty)."""
@@ -92,6 +93,10 @@ def _load():
                                   fp, fp, ctypes.c_int32, f64p, f64p, i32p, fp, u8p, ctypes.c_int]
         lib.orc_certify.argtypes = [P, ctypes.c_int32, fp, fp, fp, fp, u8p, ctypes.c_float,
                                     i32p, A, A, f64p]
+        for name in ("orc_solve_lex", "orc_solve_lex_brute"):
+            getattr(lib, name).argtypes = [P, fp, fp, A, f64p]
+        lib.orc_certify_lex.argtypes = [P, ctypes.c_int32, fp, fp, fp, fp, u8p, ctypes.c_float,
+                                        i32p, A, A, f64p, f64p]
         lib.orc_pairwise_sum.argtypes = [f64p, ctypes.c_int64]
         lib.orc_pairwise_sum.restype = ctypes.c_double
         _lib = lib
@@ -140,12 +145,25 @@ def fulfillment(problem, i: int, cap: float, tail: float, r: int) -> np.float32:
 
 
 def solve(problem, cap, tail, method: str = "dp") -> Alloc:
-    """Solve the allocation on one point realisation (cap[N], tail[N])."""
+    """Solve the allocation on one point realisation (cap[N], tail[N]).
+    Methods dp / brute / threshold: objective levels (1)-(2) with the
+    fewer-GPUs, smaller-TP tie-breaks; lex / lex_brute: the whole objective,
+    levels (1)-(4)."""
     ref = _ProblemRef(problem)
     cap = np.ascontiguousarray(cap, dtype=np.float32)
     tail = np.ascontiguousarray(tail, dtype=np.float32)
     assert cap.shape == (ref.n_cells,) and tail.shape == (ref.n_cells,)
     out = _Alloc()
+    if method in ("lex", "lex_brute"):
+        gp = ctypes.c_double()
+        fn = "orc_solve_lex" if method == "lex" else "orc_solve_lex_brute"
+        rc = getattr(_load(), fn)(ctypes.byref(ref.s), _ptr(cap, ctypes.c_float), _ptr(tail, ctypes.c_float),
+                                  ctypes.byref(out), ctypes.byref(gp))
+        if rc != 0:
+            raise ValueError(f"oracle {method} solve failed ({rc})")
+        a = _alloc_out(out, len(ref.demand))
+        a.goodput64 = float(gp.value)
+        return a
     fn = {"dp": "orc_solve_dp", "brute": "orc_solve_brute", "threshold": "orc_solve_threshold"}[method]
     rc = getattr(_load(), fn)(ctypes.byref(ref.s), _ptr(cap, ctypes.c_float), _ptr(tail, ctypes.c_float),
                               ctypes.byref(out))
@@ -241,6 +259,42 @@ def certify(problem, intervals, eps: float = 0.05) -> CertifyResult:
     k = len(ref.demand)
     return CertifyResult(state, gap, [_alloc_out(cons[o], k) for o in range(O)],
                          [_alloc_out(opt[o], k) for o in range(O)])
+
+
+@dataclass
+class CertifyLexResult:
+    state: np.ndarray   # [O] int32
+    gap_mm: np.ndarray  # [O] float64, tau+ - tau-
+    gap_gp: np.ndarray  # [O] float64, |gp+ - gp-| / max(gp+, gp-)
+    cons: list          # [O] Alloc under the whole objective (A-)
+    opt: list           # [O] Alloc (A+)
+
+
+def certify_lex(problem, intervals, eps: float = 0.05) -> CertifyLexResult:
+    """Certificate with the stage-wise gap (Section 4.2) under the whole
+    lexicographic objective."""
+    ref = _ProblemRef(problem)
+    N = ref.n_cells
+    cl = np.ascontiguousarray(intervals.cap_lo, dtype=np.float32).reshape(-1, N)
+    O = cl.shape[0]
+    ch = np.ascontiguousarray(intervals.cap_hi, dtype=np.float32).reshape(O, N)
+    tl = np.ascontiguousarray(intervals.tail_lo, dtype=np.float32).reshape(O, N)
+    th = np.ascontiguousarray(intervals.tail_hi, dtype=np.float32).reshape(O, N)
+    ms = np.ascontiguousarray(intervals.measured, dtype=np.uint8).reshape(O, N)
+    state = np.zeros(O, dtype=np.int32)
+    gmm = np.zeros(O, dtype=np.float64)
+    ggp = np.zeros(O, dtype=np.float64)
+    cons = (_Alloc * max(O, 1))()
+    opt = (_Alloc * max(O, 1))()
+    rc = _load().orc_certify_lex(ctypes.byref(ref.s), O, _ptr(cl, ctypes.c_float), _ptr(ch, ctypes.c_float),
+                                 _ptr(tl, ctypes.c_float), _ptr(th, ctypes.c_float), _ptr(ms, ctypes.c_uint8),
+                                 float(eps), _ptr(state, ctypes.c_int32), cons, opt, _ptr(gmm, ctypes.c_double),
+                                 _ptr(ggp, ctypes.c_double))
+    if rc != 0:
+        raise ValueError("oracle certify failed")
+    k = len(ref.demand)
+    return CertifyLexResult(state, gmm, ggp, [_alloc_out(cons[o], k) for o in range(O)],
+                            [_alloc_out(opt[o], k) for o in range(O)])
 
 
 def pairwise_sum(x) -> float:

@@ -14,9 +14,9 @@
  *   - the lexicographic objective stated after Eq. (5): (1) critical floors
  *     whenever they can be met, (2) maximise the minimum satisfaction ratio
  *     r_i = x_i / lambda_i; ties go to fewer GPUs, then to the
- *     lexicographically smaller TP vector (levels (3)-(4) of the paper's
- *     objective are replaced by these tie-breaks; see the readings in the
- *     design notes);
+ *     lexicographically smaller TP vector (the solvers orc_solve_*); and the
+ *     whole objective with (3) maximum served goodput and (4) fewest GPUs
+ *     (orc_solve_lex*, orc_certify_lex);
  *   - the conservative / optimistic realisations of Section 4.1;
  *   - the three-state certificate of Section 4.2;
  *   - the acquisition score of Section 4.3, score(e) = E[Gamma_t -
@@ -636,6 +636,256 @@ int orc_certify(const orc_problem *p, int32_t n_orders, const float *cap_lo, con
       else if (!(tail_hi[(size_t)o * N + cell] <= p->slo[i])) ok = 0;
     }
     if (ok && gap[o] <= (double)eps) state[o] = ORC_CERTIFIED_FEASIBLE;
+    else state[o] = ORC_UNDECIDED;
+  }
+  free(buf);
+  return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* The whole lexicographic objective, levels (1)-(4).                   */
+/* ------------------------------------------------------------------ */
+
+/* Served goodput of an option: failed requests are not goodput, so a
+ * configuration whose tail breaks the SLO serves 0. */
+static float orc_goodput_served(const orc_problem *p, int i, float cap, float tail, int r) {
+  if (!(tail <= p->slo[i])) return 0.0f;
+  return orc_served(p, i, cap, r);
+}
+
+/* Key of the residual tie-break: (TP degree, replicas) of class i, empty =
+ * (0, 0). */
+static int orc_lex_cmp(const orc_problem *p, const int *tpi_a, const int *r_a, const int *tpi_b,
+                       const int *r_b) {
+  for (int i = 0; i < p->n_classes; ++i) {
+    const int ta = tpi_a[i] < 0 ? 0 : p->tp[tpi_a[i]], tb = tpi_b[i] < 0 ? 0 : p->tp[tpi_b[i]];
+    if (ta != tb) return ta < tb ? -1 : 1;
+    if (r_a[i] != r_b[i]) return r_a[i] < r_b[i] ? -1 : 1;
+  }
+  return 0;
+}
+
+int orc_solve_lex_brute(const orc_problem *p, const float *cap, const float *tail, orc_alloc *out,
+                        double *goodput64) {
+  if (orc_check_problem(p)) return -1;
+  const int K = p->n_classes;
+  const int maxo = orc_max_options(p);
+  orc_option *opt = (orc_option *)malloc(sizeof(orc_option) * (size_t)maxo * K);
+  int nopt[ORC_MAX_CLASSES];
+  double combos = 1.0;
+  for (int i = 0; i < K; ++i) {
+    nopt[i] = orc_class_options(p, i, opt + (size_t)i * maxo);
+    combos *= (double)(nopt[i] + 1);
+  }
+  if (combos > 2.0e8) {
+    free(opt);
+    return -2;
+  }
+  const int has_crit = orc_has_critical(p);
+  int choice[ORC_MAX_CLASSES];
+  int floors_feasible = 0, best_found = 0, best_gpus = 0;
+  float best_tau = 0.0f;
+  double best_gp = 0.0;
+  int best_tpi[ORC_MAX_CLASSES], best_r[ORC_MAX_CLASSES];
+  for (int pass = 0; pass < 2; ++pass) {
+    if (pass == 0 && !has_crit) continue;
+    const int restrict_to_floors = has_crit && floors_feasible;
+    for (int i = 0; i < K; ++i) choice[i] = 0;
+    for (;;) {
+      int gpus = 0, floors_ok = 1;
+      float tau = 1.0f;
+      int tpi[ORC_MAX_CLASSES], rr[ORC_MAX_CLASSES];
+      float served[ORC_MAX_CLASSES];
+      for (int i = 0; i < K; ++i) {
+        float f = 0.0f;
+        served[i] = 0.0f;
+        tpi[i] = -1;
+        rr[i] = 0;
+        if (choice[i] == 0) {
+          if (orc_is_critical(p, i)) floors_ok = 0;
+        } else {
+          const orc_option *o = &opt[(size_t)i * maxo + choice[i] - 1];
+          const float c = cap[o->cell], l = tail[o->cell];
+          gpus += o->cost;
+          f = orc_fulfillment(p, i, c, l, o->r);
+          served[i] = orc_goodput_served(p, i, c, l, o->r);
+          tpi[i] = o->t_idx;
+          rr[i] = o->r;
+          if (orc_is_critical(p, i) && !orc_floor_valid(p, i, c, l, o->r)) floors_ok = 0;
+        }
+        if (f < tau) tau = f;
+      }
+      if (gpus <= p->budget) {
+        if (pass == 0) {
+          if (floors_ok) floors_feasible = 1;
+        } else if (!restrict_to_floors || floors_ok) {
+          double gp = 0.0;
+          for (int i = K - 1; i >= 0; --i) gp = (double)served[i] + gp;
+          int better = 0;
+          if (!best_found) better = 1;
+          else if (tau != best_tau) better = tau > best_tau;
+          else if (gp != best_gp) better = gp > best_gp;
+          else if (gpus != best_gpus) better = gpus < best_gpus;
+          else better = orc_lex_cmp(p, tpi, rr, best_tpi, best_r) < 0;
+          if (better) {
+            best_found = 1;
+            best_tau = tau;
+            best_gp = gp;
+            best_gpus = gpus;
+            memcpy(best_tpi, tpi, sizeof(int) * K);
+            memcpy(best_r, rr, sizeof(int) * K);
+          }
+        }
+      }
+      int i = 0;
+      while (i < K) {
+        if (++choice[i] <= nopt[i]) break;
+        choice[i] = 0;
+        ++i;
+      }
+      if (i == K) break;
+    }
+  }
+  memset(out, 0, sizeof(*out));
+  out->tau = best_tau;
+  out->floors_met = has_crit ? floors_feasible : 1;
+  for (int i = 0; i < K; ++i) {
+    out->tp_index[i] = best_tpi[i];
+    out->replicas[i] = best_r[i];
+  }
+  orc_fill_goodput(p, cap, out);
+  if (goodput64) *goodput64 = best_gp;
+  free(opt);
+  return 0;
+}
+
+/* Levels (3)-(4) as a knapsack over the budget, classes taken from the
+ * last to the first:
+ *   V_K[g] = (0, 0 GPUs) for every g;
+ *   V_k[g] = best over the allowed options o of class k with cost <= g of
+ *            (served_o + V_{k+1}[g - cost].goodput, cost + V_{k+1}[g - cost].gpus),
+ * best = larger goodput, then fewer GPUs.  Allowed: ratio >= tau* (level 2),
+ * floor-meeting for a critical class when the floors are enforced (level
+ * 1), and the empty option only for an unrestricted class when tau* = 0.
+ * The allocation is then read in class order: class k takes the first
+ * allowed option, in (TP, replicas) order with empty first, that keeps the
+ * optimum of V_k at the remaining budget. */
+int orc_solve_lex(const orc_problem *p, const float *cap, const float *tail, orc_alloc *out,
+                  double *goodput64) {
+  if (orc_check_problem(p)) return -1;
+  orc_alloc base;
+  int err = orc_solve_dp(p, cap, tail, &base);
+  if (err) return err;
+  const int K = p->n_classes, G = p->budget;
+  const float tau = base.tau;
+  const int has_crit = orc_has_critical(p);
+  const int maxo = orc_max_options(p);
+  orc_option *opt = (orc_option *)malloc(sizeof(orc_option) * (size_t)maxo * K);
+  int *allowed = (int *)malloc(sizeof(int) * (size_t)maxo * K);
+  float *served = (float *)malloc(sizeof(float) * (size_t)maxo * K);
+  int nopt[ORC_MAX_CLASSES], empty_ok[ORC_MAX_CLASSES];
+  for (int i = 0; i < K; ++i) {
+    const int restricted = has_crit && base.floors_met && orc_is_critical(p, i);
+    empty_ok[i] = !restricted && tau <= 0.0f;
+    nopt[i] = orc_class_options(p, i, opt + (size_t)i * maxo);
+    for (int j = 0; j < nopt[i]; ++j) {
+      const orc_option *o = &opt[(size_t)i * maxo + j];
+      const float c = cap[o->cell], l = tail[o->cell];
+      int ok = orc_fulfillment(p, i, c, l, o->r) >= tau;
+      if (restricted && !orc_floor_valid(p, i, c, l, o->r)) ok = 0;
+      allowed[(size_t)i * maxo + j] = ok;
+      served[(size_t)i * maxo + j] = orc_goodput_served(p, i, c, l, o->r);
+    }
+  }
+  /* layer k at offset k * (G + 1); gpus < 0 marks "no allowed completion" */
+  double *vgp = (double *)malloc(sizeof(double) * (size_t)(K + 1) * (G + 1));
+  int *vgpus = (int *)malloc(sizeof(int) * (size_t)(K + 1) * (G + 1));
+  for (int g = 0; g <= G; ++g) {
+    vgp[(size_t)K * (G + 1) + g] = 0.0;
+    vgpus[(size_t)K * (G + 1) + g] = 0;
+  }
+  for (int k = K - 1; k >= 0; --k) {
+    const double *ngp = vgp + (size_t)(k + 1) * (G + 1);
+    const int *ngpus = vgpus + (size_t)(k + 1) * (G + 1);
+    for (int g = 0; g <= G; ++g) {
+      double bgp = 0.0;
+      int bgpus = -1;
+      if (empty_ok[k] && ngpus[g] >= 0) {
+        bgp = ngp[g];
+        bgpus = ngpus[g];
+      }
+      for (int j = 0; j < nopt[k]; ++j) {
+        const orc_option *o = &opt[(size_t)k * maxo + j];
+        if (!allowed[(size_t)k * maxo + j] || o->cost > g || ngpus[g - o->cost] < 0) continue;
+        const double cgp = (double)served[(size_t)k * maxo + j] + ngp[g - o->cost];
+        const int cgpus = o->cost + ngpus[g - o->cost];
+        if (bgpus < 0 || cgp > bgp || (cgp == bgp && cgpus < bgpus)) {
+          bgp = cgp;
+          bgpus = cgpus;
+        }
+      }
+      vgp[(size_t)k * (G + 1) + g] = bgp;
+      vgpus[(size_t)k * (G + 1) + g] = bgpus;
+    }
+  }
+  memset(out, 0, sizeof(*out));
+  out->tau = tau;
+  out->floors_met = base.floors_met;
+  int rem = G;
+  for (int k = 0; k < K; ++k) {
+    const double want_gp = vgp[(size_t)k * (G + 1) + rem];
+    const int want_gpus = vgpus[(size_t)k * (G + 1) + rem];
+    const double *ngp = vgp + (size_t)(k + 1) * (G + 1);
+    const int *ngpus = vgpus + (size_t)(k + 1) * (G + 1);
+    out->tp_index[k] = -1;
+    out->replicas[k] = 0;
+    if (empty_ok[k] && ngpus[rem] >= 0 && ngp[rem] == want_gp && ngpus[rem] == want_gpus) continue;
+    /* options are listed by TP index, then replicas: (TP degree, r) order */
+    for (int j = 0; j < nopt[k]; ++j) {
+      const orc_option *o = &opt[(size_t)k * maxo + j];
+      if (!allowed[(size_t)k * maxo + j] || o->cost > rem || ngpus[rem - o->cost] < 0) continue;
+      if ((double)served[(size_t)k * maxo + j] + ngp[rem - o->cost] != want_gp) continue;
+      if (o->cost + ngpus[rem - o->cost] != want_gpus) continue;
+      out->tp_index[k] = o->t_idx;
+      out->replicas[k] = o->r;
+      rem -= o->cost;
+      break;
+    }
+  }
+  orc_fill_goodput(p, cap, out);
+  if (goodput64) *goodput64 = vgp[G];
+  free(opt); free(allowed); free(served); free(vgp); free(vgpus);
+  return 0;
+}
+
+int orc_certify_lex(const orc_problem *p, int32_t n_orders, const float *cap_lo, const float *cap_hi,
+                    const float *tail_lo, const float *tail_hi, const uint8_t *measured, float eps,
+                    int32_t *state, orc_alloc *cons, orc_alloc *opt, double *gap_mm, double *gap_gp) {
+  if (orc_check_problem(p)) return -1;
+  const int64_t N = orc_n_cells(p);
+  const int has_crit = orc_has_critical(p);
+  float *buf = (float *)malloc(sizeof(float) * (size_t)N * 4);
+  for (int o = 0; o < n_orders; ++o) {
+    double gp_m = 0.0, gp_p = 0.0;
+    orc_realisations(N, o, cap_lo, cap_hi, tail_lo, tail_hi, buf, buf + N, buf + 2 * N, buf + 3 * N);
+    orc_solve_lex(p, buf, buf + N, &cons[o], &gp_m);
+    orc_solve_lex(p, buf + 2 * N, buf + 3 * N, &opt[o], &gp_p);
+    gap_mm[o] = (double)opt[o].tau - (double)cons[o].tau;
+    const double top = gp_p > gp_m ? gp_p : gp_m;
+    gap_gp[o] = top > 0.0 ? fabs(gp_p - gp_m) / top : 0.0;
+    if (has_crit && !opt[o].floors_met) {
+      state[o] = ORC_CERTIFIED_INFEASIBLE;
+      continue;
+    }
+    int ok = cons[o].floors_met;
+    for (int i = 0; i < p->n_classes && ok; ++i) {
+      if (cons[o].replicas[i] == 0) continue;
+      const int r = cons[o].replicas[i];
+      const int cell = orc_cell(p, i, cons[o].tp_index[i], orc_bucket(p, i, r));
+      if (!measured[(size_t)o * N + cell]) ok = 0;
+      else if (!(tail_hi[(size_t)o * N + cell] <= p->slo[i])) ok = 0;
+    }
+    if (ok && gap_mm[o] <= (double)eps && gap_gp[o] <= (double)eps) state[o] = ORC_CERTIFIED_FEASIBLE;
     else state[o] = ORC_UNDECIDED;
   }
   free(buf);

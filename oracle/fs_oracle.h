@@ -97,6 +97,31 @@ int orc_certify(const orc_problem *p, int32_t n_orders,
                 const float *tail_lo, const float *tail_hi, const uint8_t *measured,
                 float eps, int32_t *state, orc_alloc *cons, orc_alloc *opt, double *gap);
 
+/* The paper's whole lexicographic objective (Section 3): levels (1) floors
+ * and (2) max-min fulfillment as above, then (3) the largest total served
+ * goodput among allocations that keep every class's ratio at least tau*
+ * (and the floors), then (4) the fewest GPUs; remaining ties go to the
+ * lexicographically smallest (t_0, r_0, t_1, r_1, ...) in class order with
+ * t the TP degree and empty = (0, 0).  A class's served goodput is
+ * min(lambda, fl32(r c)) when its tail is within the SLO, else 0; the total
+ * compared at level (3) is their binary64 sum accumulated from the last
+ * class to the first, returned in *goodput64 (may be NULL).
+ *   lex_brute: every combination, keys compared literally (tiny inputs);
+ *   lex:       levels (1)-(2) by orc_solve_dp, then a suffix knapsack over
+ *              the budget and a greedy reconstruction in class order. */
+int orc_solve_lex_brute(const orc_problem *p, const float *cap, const float *tail, orc_alloc *out,
+                        double *goodput64);
+int orc_solve_lex(const orc_problem *p, const float *cap, const float *tail, orc_alloc *out,
+                  double *goodput64);
+
+/* Certificate with the stage-wise gap (Section 4.2): both allocations under
+ * the whole objective; gap_mm = tau+ - tau-, gap_gp = |gp+ - gp-| /
+ * max(gp+, gp-) (0 when both are 0) in binary64; CERTIFIED_FEASIBLE needs
+ * both stages within eps. */
+int orc_certify_lex(const orc_problem *p, int32_t n_orders, const float *cap_lo, const float *cap_hi,
+                    const float *tail_lo, const float *tail_hi, const uint8_t *measured, float eps,
+                    int32_t *state, orc_alloc *cons, orc_alloc *opt, double *gap_mm, double *gap_gp);
+
 /* Pairwise sum of x[0..n) zero-padded to the next power of two. */
 double orc_pairwise_sum(const double *x, int64_t n);
 
