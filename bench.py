@@ -376,6 +376,98 @@ def policy_bench(args):
     ctx.close()
 
 
+def lex_work_per_scenario(problem) -> float:
+    """Algorithmic work of one solve under the whole objective, in VALU
+    lane-slots: levels (1)-(2) as one solve of the lane work model, then per
+    class and budget g the candidates of level (3)'s knapsack, one per
+    existing option with cost <= g: a binary64 add (2 slots at half rate),
+    two compares and a select (3)."""
+    import numpy as np
+    G, K = problem.budget, problem.n_classes
+    ex = existing_options(problem).reshape(K, -1)
+    costs = np.concatenate([np.arange(1, G // int(t) + 1) * int(t) for t in problem.tp])
+    per_g = np.array([[(costs[ex[k] > 0] <= g).sum() for g in range(G + 1)] for k in range(K)])
+    return lane_work_per_scenario(problem, existing_options(problem)) / 2.0 + 5.0 * float(per_g.sum())
+
+
+def lex_bench(args):
+    """Dense solves under the whole lexicographic objective (fs_solve_batch_lex)
+    on point realisations drawn inside the workload's intervals, against the
+    max-min solve (fs_solve_batch) on the same inputs.  The roofline object
+    reports k_solve_dense_lex against the VALU peak (the call's launch pair
+    also holds a set-up kernel of a few microseconds).  The CPU baseline is
+    the oracle's knapsack on a bounded sample of the same realisations."""
+    import numpy as np
+    import torch
+    from paper_2608_19659_amd import fleetsieve as fs
+    from paper_2608_19659_amd.synth import WORKLOADS, interval_realisations, make_workload
+
+    name = args.workload
+    if name not in WORKLOADS:
+        print(f"unknown workload {name}; choose from {list(WORKLOADS)}", file=sys.stderr)
+        sys.exit(2)
+    dev = "cuda:0"
+    n = args.lex_scenarios
+    print(f"[bench] whole-objective solves on {name}: {n} realisations", file=sys.stderr, flush=True)
+    w = make_workload(name, with_samples=False)
+    p = w.problem
+    cap_h, tail_h = interval_realisations(w, n)
+    cap = torch.from_numpy(cap_h).to(dev)
+    tail = torch.from_numpy(tail_h).to(dev)
+    ctx = fs.Context(0)
+    ws = ctx.workspace(fs.workspace_size(p))
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            r = fn()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for _ in range(args.steps):
+            r = fn()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        return r, ev0.elapsed_time(ev1) / args.steps
+
+    r_lex, ms_lex = timed(lambda: fs.solve_batch_lex(ctx, p, cap, tail, stream=stream, workspace=ws))
+    _, ms_mm = timed(lambda: fs.solve_batch(ctx, p, cap, tail, stream=stream, workspace=ws))
+    slots = lex_work_per_scenario(p)
+    achieved = slots * n / (ms_lex / 1e3)
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        got = {k: v.cpu().numpy() for k, v in r_lex.items()}
+        t0, j, same = time.perf_counter(), 0, True
+        while j < n and time.perf_counter() - t0 < 10.0:
+            a = oracle.solve(p, cap_h[j], tail_h[j], "lex")
+            same = same and got["goodput64"][j] == a.goodput64 and \
+                list(got["replicas"][j].view(np.uint16)) == a.replicas
+            j += 1
+        dt = time.perf_counter() - t0
+        cpu = {"value": j / dt, "unit": "scenarios/s", "cores": 1, "kind": "oracle",
+               "sample": f"the first {j} realisations, one thread, {dt:.1f} s wall",
+               "matches_gpu_on_sample": bool(same)}
+    line = {
+        "metric": "allocation solves/sec under the whole lexicographic objective (Section 3 levels 1-4) on 1 MI355X; "
+                  "oracle-exact",
+        "value": n / (ms_lex / 1e3), "unit": "scenarios/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_lex, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32+f64", "data": "synthetic",
+        "config": {"workload": f"{name}: {p.n_classes} classes, TP {[int(x) for x in p.tp]}, G={p.budget}; "
+                               f"{n} point realisations drawn inside its intervals",
+                   "parallelism": "single GPU"},
+        "maxmin_only": {"value": n / (ms_mm / 1e3), "ms_per_step": ms_mm},
+        "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_OPS / 1e12, "unit": "TOP/s",
+                     "frac": achieved / VALU_PEAK_OPS, "traffic": None, "kernel": "k_solve_dense_lex",
+                     "op": "VALU lane-slot", "slots_per_scenario": slots, "scenarios_per_launch": n,
+                     "kernel_ms_avg": ms_lex},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    ctx.close()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -401,6 +493,10 @@ def main():
     ap.add_argument("--policy", action="store_true",
                     help="score under multi-metric class policies (completion-p99, TTFT-p99, success floor), "
                          "reducing intervals and samples on the GPU first")
+    ap.add_argument("--lex", action="store_true",
+                    help="dense solves under the whole lexicographic objective (levels 1-4) on point realisations "
+                         "of the workload, against the max-min solve")
+    ap.add_argument("--lex-scenarios", type=int, default=65536, help="realisations per --lex step")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (scales the HBM byte counters)")
     args = ap.parse_args()
@@ -428,6 +524,9 @@ def main():
         return
     if args.policy:
         policy_bench(args)
+        return
+    if args.lex:
+        lex_bench(args)
         return
 
     from paper_2608_19659_amd import fleetsieve as fs

@@ -209,6 +209,39 @@ fs_status fs_certify(fs_context *ctx, const fs_problem *p, fs_intervals iv, int3
                      float eps, int32_t *d_state, fs_alloc cons, fs_alloc opt, double *d_gap,
                      void *d_workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* The paper's whole lexicographic objective (Section 3, after Eq. 5):
+ * (1) critical floors whenever they can be met, (2) max-min fulfillment,
+ * (3) the largest total served goodput among allocations that keep every
+ * class's ratio at least tau* (and the floors), (4) the fewest GPUs; the
+ * remaining ties go to the smallest (TP degree, replicas) of each class in
+ * class order, an unserved class first.  A class's served goodput is
+ * min(lambda, fl32(r c)) when the cell's tail is within the SLO, else 0;
+ * level (3) compares their binary64 sum taken from the last class to the
+ * first (exact while the nonzero served rates lie within a factor 2^23 of
+ * each other).  fs_solve_batch and fs_certify use levels (1)-(2) with the
+ * tie-breaks fewer GPUs, then smaller TP degrees.
+ *
+ * Supported while the solve's LDS fits 64 KiB: about (12 + 2K)(G + 1) + 6 x
+ * (options of one class) + 1 KiB (with TP {1, 2, 4, 8}: K = 4 up to
+ * G = 2063, K = 16 up to G = 1166, K = 64 up to G = 425);
+ * FS_ERR_UNSUPPORTED otherwise.
+ *
+ * Dense batch under the whole objective: out as in fs_solve_batch (objective
+ * = tau*, goodput = the binary32 class-order sum of the chosen allocation);
+ * d_goodput64 [n] (or NULL) receives level (3)'s binary64 total. */
+fs_status fs_solve_batch_lex(fs_context *ctx, const fs_problem *p, const float *d_cap, const float *d_tail,
+                             int64_t n_scenarios, fs_alloc out, double *d_goodput64, void *d_workspace,
+                             size_t workspace_bytes, hipStream_t stream);
+
+/* Certificate with the stage-wise allocation gap (Section 4.2; Fig. 4a
+ * tracks both stages): A- and A+ under the whole objective; the max-min
+ * stage tau+ - tau- and the goodput stage |gp+ - gp-| / max(gp+, gp-) (0
+ * when both are 0), binary64, each [n_orders] or NULL.  CERTIFIED_FEASIBLE
+ * needs both stages within eps; the other conditions are fs_certify's. */
+fs_status fs_certify_lex(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders, float eps,
+                         int32_t *d_state, fs_alloc cons, fs_alloc opt, double *d_gap_maxmin,
+                         double *d_gap_goodput, void *d_workspace, size_t workspace_bytes, hipStream_t stream);
+
 #define FS_MAX_METRICS 8
 
 /* Class policy with several tail metrics and a success floor (Section 3,

@@ -271,6 +271,52 @@ fs_status fs_solve_batch(fs_context *ctx, const fs_problem *p, const float *d_ca
   return FS_OK;
 }
 
+// Shared checks of the whole-objective calls: the stage's LDS must fit.
+static fs_status lex_supported(const fs::DevProblem &P, int n_alloc) {
+  const size_t need = fs::lds_bytes_lex(P, n_alloc);
+  if (need > fs::kLexLdsLimit)
+    return fail(FS_ERR_UNSUPPORTED, "the whole objective needs " + std::to_string(need) +
+                                        " bytes of LDS for this problem (at most 65536: about (12 + 2 K)(G + 1) "
+                                        "+ 6 x options per class + 1 KiB)");
+  return FS_OK;
+}
+
+fs_status fs_solve_batch_lex(fs_context *ctx, const fs_problem *p, const float *d_cap, const float *d_tail,
+                             int64_t n_scenarios, fs_alloc out, double *d_goodput64, void *d_workspace,
+                             size_t workspace_bytes, hipStream_t stream) {
+  if (!ctx) return fail(FS_ERR_INVALID_ARGUMENT, "context is NULL");
+  fs::DevProblem P;
+  fs_status st = make_problem(p, &P);
+  if (st != FS_OK) return st;
+  st = lex_supported(P, 1);
+  if (st != FS_OK) return st;
+  if (n_scenarios < 0 || n_scenarios > 0x7fffffff)
+    return fail(FS_ERR_INVALID_ARGUMENT, "n_scenarios must be in [0, 2^31)");
+  if (n_scenarios > 0 && (!d_cap || !d_tail)) return fail(FS_ERR_INVALID_ARGUMENT, "cell arrays are NULL");
+  const fs::WsLayout L = fs::ws_layout(P, 0, 0, 0);
+  if (!d_workspace) return fail(FS_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  if (workspace_bytes < L.total)
+    return fail(FS_ERR_WORKSPACE_TOO_SMALL, "workspace needs " + std::to_string(L.total) + " bytes");
+  if (n_scenarios == 0) return FS_OK;
+  DeviceGuard dg(ctx->device);
+  if (dg.err != hipSuccess) return hip_fail(dg.err, "hipSetDevice");
+  uint8_t *ws = (uint8_t *)d_workspace;
+  hipError_t e;
+  if (env_validate()) {
+    int32_t *flag = (int32_t *)(ws + L.flag);
+    e = fs::launch_zero_flags(flag, stream);
+    if (e == hipSuccess) e = fs::launch_validate_cells(d_cap, d_tail, n_scenarios * (int64_t)P.N, flag, stream);
+    if (e != hipSuccess) return hip_fail(e, "validation launch");
+    st = read_flags(L, ws, stream, "fs_solve_batch_lex");
+    if (st != FS_OK) return st;
+  }
+  e = fs::launch_setup(P, nullptr, 0, ws, L, stream);
+  if (e != hipSuccess) return hip_fail(e, "set-up launch");
+  e = fs::launch_solve_batch_lex(P, d_cap, d_tail, n_scenarios, to_out(out), d_goodput64, ws, L, stream);
+  if (e != hipSuccess) return hip_fail(e, "solve launch");
+  return FS_OK;
+}
+
 fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders,
                               const int32_t *d_cand, int32_t n_cand, const float *d_cap_s,
                               const float *d_tail_s, int32_t n_samples, double *d_score,
@@ -556,6 +602,46 @@ fs_status fs_certify(fs_context *ctx, const fs_problem *p, fs_intervals iv, int3
   if (e != hipSuccess) return hip_fail(e, "set-up launch");
   e = fs::launch_certify(P, iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi, iv.measured, n_orders, eps,
                          d_state, to_out(cons), to_out(opt), d_gap, ws, L, stream);
+  if (e != hipSuccess) return hip_fail(e, "certify launch");
+  return FS_OK;
+}
+
+fs_status fs_certify_lex(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders, float eps,
+                         int32_t *d_state, fs_alloc cons, fs_alloc opt, double *d_gap_maxmin,
+                         double *d_gap_goodput, void *d_workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!ctx) return fail(FS_ERR_INVALID_ARGUMENT, "context is NULL");
+  fs::DevProblem P;
+  fs_status st = make_problem(p, &P);
+  if (st != FS_OK) return st;
+  st = lex_supported(P, 2);
+  if (st != FS_OK) return st;
+  if (n_orders < 0 || n_orders > 0x7fffffff) return fail(FS_ERR_INVALID_ARGUMENT, "n_orders must be >= 0");
+  if (std::isnan(eps)) return fail(FS_ERR_INVALID_ARGUMENT, "eps must not be NaN");
+  if (n_orders > 0 && (!iv.cap_lo || !iv.cap_hi || !iv.tail_lo || !iv.tail_hi || !iv.measured || !d_state))
+    return fail(FS_ERR_INVALID_ARGUMENT, "interval or state arrays are NULL");
+  const fs::WsLayout L = fs::ws_layout(P, 0, 0, 0);
+  if (!d_workspace) return fail(FS_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  if (workspace_bytes < L.total)
+    return fail(FS_ERR_WORKSPACE_TOO_SMALL, "workspace needs " + std::to_string(L.total) + " bytes");
+  if (n_orders == 0) return FS_OK;
+  DeviceGuard dg(ctx->device);
+  if (dg.err != hipSuccess) return hip_fail(dg.err, "hipSetDevice");
+  uint8_t *ws = (uint8_t *)d_workspace;
+  hipError_t e;
+  if (env_validate()) {
+    int32_t *flag = (int32_t *)(ws + L.flag);
+    const int64_t cells = (int64_t)n_orders * P.N;
+    e = fs::launch_zero_flags(flag, stream);
+    if (e == hipSuccess) e = fs::launch_validate_cells(iv.cap_lo, iv.tail_lo, cells, flag, stream);
+    if (e == hipSuccess) e = fs::launch_validate_cells(iv.cap_hi, iv.tail_hi, cells, flag, stream);
+    if (e != hipSuccess) return hip_fail(e, "validation launch");
+    st = read_flags(L, ws, stream, "fs_certify_lex");
+    if (st != FS_OK) return st;
+  }
+  e = fs::launch_setup(P, nullptr, 0, ws, L, stream);
+  if (e != hipSuccess) return hip_fail(e, "set-up launch");
+  e = fs::launch_certify_lex(P, iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi, iv.measured, n_orders, eps, d_state,
+                             to_out(cons), to_out(opt), d_gap_maxmin, d_gap_goodput, ws, L, stream);
   if (e != hipSuccess) return hip_fail(e, "certify launch");
   return FS_OK;
 }

@@ -120,6 +120,16 @@ hipError_t launch_setup(const DevProblem &P, const int32_t *cand, int32_t E, uin
 hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s);
 hipError_t launch_solve_batch(const DevProblem &P, const float *cap, const float *tail, int64_t n,
                               AllocOut out, uint8_t *ws, const WsLayout &L, hipStream_t s);
+// The whole lexicographic objective (levels 1-4): LDS of a solve block with
+// n_alloc allocations, and the launches.
+size_t lds_bytes_lex(const DevProblem &P, int n_alloc);
+constexpr size_t kLexLdsLimit = 64 * 1024;
+hipError_t launch_solve_batch_lex(const DevProblem &P, const float *cap, const float *tail, int64_t n,
+                                  AllocOut out, double *gp64, uint8_t *ws, const WsLayout &L, hipStream_t s);
+hipError_t launch_certify_lex(const DevProblem &P, const float *cap_lo, const float *cap_hi, const float *tail_lo,
+                              const float *tail_hi, const uint8_t *measured, int32_t O, float eps, int32_t *state,
+                              AllocOut cons, AllocOut opt, double *gap_mm, double *gap_gp, uint8_t *ws,
+                              const WsLayout &L, hipStream_t s);
 hipError_t launch_certify(const DevProblem &P, const float *cap_lo, const float *cap_hi,
                           const float *tail_lo, const float *tail_hi, const uint8_t *measured,
                           int32_t O, float eps, int32_t *state, AllocOut cons, AllocOut opt,

@@ -2092,6 +2092,28 @@ __global__ __launch_bounds__(64) void k_finalize(DevProblem P, const CandInfo *_
 // ---------------------------------------------------------------------------
 // Certificate: one wavefront per order.
 // ---------------------------------------------------------------------------
+// State of one order (Section 4.2) given both allocations and whether the
+// gap is within eps: 2 when a class is critical and even the optimistic
+// allocation misses a floor; 1 when the conservative allocation meets the
+// floors, every cell it commits to is measured with its tail upper bound
+// within the SLO, and the gap is within eps; 0 otherwise.
+__device__ __forceinline__ int certificate_state(const DevProblem &P, const int8_t *__restrict__ bmap,
+                                                 const uint8_t *__restrict__ measured,
+                                                 const float *__restrict__ tail_hi, size_t off, int fm_m,
+                                                 int fm_p, const int *tm_index, const int *tm_rep,
+                                                 bool gap_ok) {
+  if (P.has_floor && !fm_p) return 2;
+  bool ok = fm_m != 0;
+  for (int k = 0; k < P.K && ok; ++k) {
+    const int r = tm_rep[k];
+    if (r == 0) continue;
+    const int cell = cell_of(P, k, tm_index[k], bmap[k * (P.G + 1) + r]);
+    if (!measured[off + cell]) ok = false;
+    else if (!(tail_hi[off + cell] <= P.slo[k])) ok = false;
+  }
+  return (ok && gap_ok) ? 1 : 0;
+}
+
 __global__ __launch_bounds__(64) void k_certify(DevProblem P, const int8_t *__restrict__ bmap,
                                                 const float *__restrict__ cap_lo,
                                                 const float *__restrict__ cap_hi,
@@ -2119,22 +2141,227 @@ __global__ __launch_bounds__(64) void k_certify(DevProblem P, const int8_t *__re
   if (lane != 0) return;
   const double gap = (double)__int_as_float(tau_p) - (double)__int_as_float(tau_m);
   if (gap_out) gap_out[o] = gap;
-  int st;
-  if (P.has_floor && !fm_p) {
-    st = 2;  // even the optimistic allocation misses a critical floor
-  } else {
-    bool ok = fm_m != 0;
-    for (int k = 0; k < P.K && ok; ++k) {
-      const int r = tm_rep[k];
-      if (r == 0) continue;
-      const int cell = cell_of(P, k, tm_index[k], bmap[k * (P.G + 1) + r]);
-      // every committed tail upper bound must be known and within the SLO
-      if (!measured[off + cell]) ok = false;
-      else if (!(tail_hi[off + cell] <= P.slo[k])) ok = false;
+  state[o] = certificate_state(P, bmap, measured, tail_hi, off, fm_m, fm_p, tm_index, tm_rep,
+                               gap <= (double)eps);
+}
+
+// ---------------------------------------------------------------------------
+// The whole lexicographic objective (Section 3): after levels (1) floors and
+// (2) max-min fulfillment, (3) the largest served goodput over allocations
+// that keep every ratio at least tau* (and the floors), then (4) the fewest
+// GPUs; remaining ties go to the smallest (TP, replicas) of each class in
+// class order, empty first.  Served goodput of an option is min(lambda,
+// fl32(r c)) when its tail is within the SLO, else 0; totals are binary64
+// sums taken from the last class to the first:
+//   V_K[g] = (0, 0 GPUs);  V_k[g] = best over allowed options o of class k
+//   with cost <= g of (served_o + V_{k+1}[g - cost], cost + GPUs of it),
+// best = larger goodput, then fewer GPUs, then the earlier option.  One
+// wavefront: lanes over the budgets g, the class's options in a uniform
+// loop; the choice of every (class, budget) is kept, and the allocation is
+// read in class order from the full budget.
+// ---------------------------------------------------------------------------
+struct LexLds {
+  double *vgp;      // [G + 1] goodput of the layer, updated in place
+  int *vn;          // [G + 1] GPUs, -1 = no allowed completion
+  int16_t *choice;  // [K][G + 1] option index, -1 = empty, -2 = none
+  float *oserved;   // [options of a class] served goodput
+  int16_t *ocost;   // [options of a class] cost, -1 = not allowed
+};
+
+// Options of a class are numbered by TP index, then replicas:
+// q = optoff[t] + r - 1.  TP index, degree and replicas of option q.
+__device__ __forceinline__ void option_of(const DevProblem &P, int q, int *ti, int *t, int *r) {
+  int i = 0, first = 0, deg = P.tp[0];
+  for (int t2 = 1; t2 < P.NT; ++t2) {
+    if (q >= P.optoff[t2]) {  // uniform loads, per-lane selects
+      i = t2;
+      first = P.optoff[t2];
+      deg = P.tp[t2];
     }
-    st = (ok && gap <= (double)eps) ? 1 : 0;
   }
-  state[o] = st;
+  *ti = i;
+  *t = deg;
+  *r = q - first + 1;
+}
+
+// One layer suffices: V_k[g] reads V_{k+1} at budgets <= g only, so the
+// budgets are rewritten from the top down, 64 at a time, every lane's reads
+// of a group before its writes.
+__device__ void wave_lex_stage(const DevProblem &P, const int8_t *__restrict__ bmap, const Realisation &R,
+                               int tau, int floors_met, const LexLds &X, const WaveAlloc &alloc,
+                               float *goodput, double *goodput64) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int K = P.K, G = P.G, PO = P.optoff[P.NT];
+  for (int g = lane; g <= G; g += kWave) {
+    X.vgp[g] = 0.0;
+    X.vn[g] = 0;
+  }
+  for (int k = K - 1; k >= 0; --k) {
+    const bool restricted = P.has_floor && floors_met && (P.floor_rps[k] > 0.0f);
+    const bool empty_ok = !restricted && tau <= 0;
+    const float slo = P.slo[k], demand = P.demand[k], fl = P.floor_rps[k];
+    const double rcp = P.rcp_demand[k];
+    for (int q = lane; q < PO; q += kWave) {
+      int ti, t, r;
+      option_of(P, q, &ti, &t, &r);
+      const int b = bmap[k * (G + 1) + r];
+      int cost = -1;
+      float served = 0.0f;
+      if (b >= 0) {
+        const int cell = cell_of(P, k, ti, b);
+        const float c = R.c(cell), l = R.l(cell);
+        bool ok = ratio_bits(c, l, r, slo, rcp) >= tau;
+        if (restricted && !floor_ok(c, l, r, slo, demand, fl)) ok = false;
+        if (ok) cost = t * r;
+        served = (l <= slo) ? served_rps(c, r, demand) : 0.0f;
+      }
+      X.ocost[q] = (int16_t)cost;
+      X.oserved[q] = served;
+    }
+    __syncthreads();
+    for (int base = (G / kWave) * kWave; base >= 0; base -= kWave) {
+      const int g = base + lane;
+      double bgp = 0.0;
+      int bn = -1, bc = -2;
+      if (g <= G) {
+        if (empty_ok && X.vn[g] >= 0) {
+          bgp = X.vgp[g];
+          bn = X.vn[g];
+          bc = -1;
+        }
+        for (int q = 0; q < PO; ++q) {
+          const int c = X.ocost[q];
+          if (c < 0 || c > g) continue;
+          const int n2 = X.vn[g - c];
+          if (n2 < 0) continue;
+          const double v = (double)X.oserved[q] + X.vgp[g - c];
+          const int vn = c + n2;
+          if (bn < 0 || v > bgp || (v == bgp && vn < bn)) {
+            bgp = v;
+            bn = vn;
+            bc = q;
+          }
+        }
+      }
+      wave_lds_fence();
+      if (g <= G) {
+        X.vgp[g] = bgp;
+        X.vn[g] = bn;
+        X.choice[k * (G + 1) + g] = (int16_t)bc;
+      }
+      wave_lds_fence();
+    }
+    __syncthreads();
+  }
+  if (lane == 0) {
+    int rem = G;
+    float gp = 0.0f;
+    for (int k = 0; k < K; ++k) {
+      const int q = X.choice[k * (G + 1) + rem];
+      int ti_sel = -1, r_sel = 0;
+      if (q >= 0) {
+        int t;
+        option_of(P, q, &ti_sel, &t, &r_sel);
+        rem -= t * r_sel;
+        const int cell = cell_of(P, k, ti_sel, bmap[k * (G + 1) + r_sel]);
+        gp += served_rps(R.c(cell), r_sel, P.demand[k]);
+      }
+      alloc.tp_index[k] = ti_sel;
+      alloc.replicas[k] = r_sel;
+    }
+    *goodput = gp;
+    *goodput64 = X.vgp[G];
+  }
+  __syncthreads();
+}
+
+// Work area of a lexicographic solve, shared in turn by the max-min solver
+// (3 (G + 1) ints) and the stage: the layer, the choices and one class's
+// option table, from an 8-byte aligned start.
+__device__ __host__ inline size_t lex_work_bytes(int K, int G, int PO) {
+  const size_t g1 = (size_t)G + 1;
+  size_t b = g1 * (sizeof(double) + sizeof(int)) + (size_t)PO * sizeof(float);
+  b += ((size_t)K * g1 + (size_t)PO) * sizeof(int16_t);
+  const size_t solver = 3 * g1 * sizeof(int);
+  return 8 + (b > solver ? b : solver);  // 8: aligning the start
+}
+
+__device__ __forceinline__ LexLds lex_lds(const DevProblem &P, void *start) {
+  const size_t g1 = (size_t)P.G + 1;
+  char *base = reinterpret_cast<char *>(((uintptr_t)start + 7) & ~(uintptr_t)7);
+  LexLds X;
+  X.vgp = reinterpret_cast<double *>(base);
+  X.vn = reinterpret_cast<int *>(X.vgp + g1);
+  X.oserved = reinterpret_cast<float *>(X.vn + g1);
+  X.choice = reinterpret_cast<int16_t *>(X.oserved + P.optoff[P.NT]);
+  X.ocost = X.choice + (size_t)P.K * g1;
+  return X;
+}
+
+// Dense batch under the whole objective: one wavefront per scenario.
+__global__ __launch_bounds__(64) void k_solve_dense_lex(DevProblem P, const int8_t *__restrict__ bmap,
+                                                        const float *__restrict__ cap,
+                                                        const float *__restrict__ tail, int64_t n,
+                                                        AllocOut out, double *__restrict__ gp64_out) {
+  extern __shared__ int lds[];
+  const int64_t j = blockIdx.x;
+  if (j >= n) return;
+  int *tp_index = lds;
+  int *replicas = tp_index + kMaxClasses;
+  int *work = replicas + kMaxClasses;
+  WaveAlloc wa{tp_index, replicas};
+  const LexLds X = lex_lds(P, work);
+  Realisation R{cap + j * P.N, tail + j * P.N, -1, 0.0f, 0.0f};
+  int fm;
+  float gp;
+  double gp64;
+  const int tau = wave_solve(P, bmap, R, work, &fm, nullptr, nullptr);
+  wave_lex_stage(P, bmap, R, tau, fm, X, wa, &gp, &gp64);
+  write_alloc(out, j, P.K, tau, fm, gp, wa);
+  if (gp64_out && threadIdx.x == 0) gp64_out[j] = gp64;
+}
+
+// Certificate with the stage-wise gap: both allocations under the whole
+// objective; max-min gap tau+ - tau-, goodput gap |gp+ - gp-| / max(gp+,
+// gp-) (0 when both are 0); within eps means both stages are.
+__global__ __launch_bounds__(64) void k_certify_lex(DevProblem P, const int8_t *__restrict__ bmap,
+                                                    const float *__restrict__ cap_lo,
+                                                    const float *__restrict__ cap_hi,
+                                                    const float *__restrict__ tail_lo,
+                                                    const float *__restrict__ tail_hi,
+                                                    const uint8_t *__restrict__ measured, float eps,
+                                                    int32_t *__restrict__ state, AllocOut cons, AllocOut opt,
+                                                    double *__restrict__ gap_mm_out,
+                                                    double *__restrict__ gap_gp_out) {
+  extern __shared__ int lds[];
+  const int o = blockIdx.x, lane = threadIdx.x;
+  const size_t off = (size_t)o * P.N;
+  int *tm_index = lds;
+  int *tm_rep = tm_index + kMaxClasses;
+  int *tp_index = tm_rep + kMaxClasses;
+  int *tp_rep = tp_index + kMaxClasses;
+  int *work = tp_rep + kMaxClasses;
+  WaveAlloc am{tm_index, tm_rep}, ap{tp_index, tp_rep};
+  const LexLds X = lex_lds(P, work);
+  int fm_m, fm_p;
+  float gp_m, gp_p;
+  double g64_m, g64_p;
+  Realisation rm{cap_lo + off, tail_hi + off, -1, 0.0f, 0.0f};
+  const int tau_m = wave_solve(P, bmap, rm, work, &fm_m, nullptr, nullptr);
+  wave_lex_stage(P, bmap, rm, tau_m, fm_m, X, am, &gp_m, &g64_m);
+  Realisation rp{cap_hi + off, tail_lo + off, -1, 0.0f, 0.0f};
+  const int tau_p = wave_solve(P, bmap, rp, work, &fm_p, nullptr, nullptr);
+  wave_lex_stage(P, bmap, rp, tau_p, fm_p, X, ap, &gp_p, &g64_p);
+  write_alloc(cons, o, P.K, tau_m, fm_m, gp_m, am);
+  write_alloc(opt, o, P.K, tau_p, fm_p, gp_p, ap);
+  if (lane != 0) return;
+  const double gap_mm = (double)__int_as_float(tau_p) - (double)__int_as_float(tau_m);
+  const double top = g64_p > g64_m ? g64_p : g64_m;
+  const double gap_gp = top > 0.0 ? fabs(g64_p - g64_m) / top : 0.0;
+  if (gap_mm_out) gap_mm_out[o] = gap_mm;
+  if (gap_gp_out) gap_gp_out[o] = gap_gp;
+  state[o] = certificate_state(P, bmap, measured, tail_hi, off, fm_m, fm_p, tm_index, tm_rep,
+                               gap_mm <= (double)eps && gap_gp <= (double)eps);
 }
 
 // ---------------------------------------------------------------------------
@@ -2622,6 +2849,28 @@ hipError_t launch_solve_batch(const DevProblem &P, const float *cap, const float
   if (n == 0) return hipSuccess;
   k_solve_dense<<<(unsigned)n, 64, lds_bytes_solver(P, 1), s>>>(P, (const int8_t *)(ws + L.bmap),
                                                                 cap, tail, n, out);
+  return hipGetLastError();
+}
+
+size_t lds_bytes_lex(const DevProblem &P, int n_alloc) {
+  return sizeof(int) * (size_t)n_alloc * 2 * kMaxClasses + lex_work_bytes(P.K, P.G, P.optoff[P.NT]);
+}
+
+hipError_t launch_solve_batch_lex(const DevProblem &P, const float *cap, const float *tail, int64_t n,
+                                  AllocOut out, double *gp64, uint8_t *ws, const WsLayout &L, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  k_solve_dense_lex<<<(unsigned)n, 64, lds_bytes_lex(P, 1), s>>>(P, (const int8_t *)(ws + L.bmap), cap, tail, n,
+                                                                 out, gp64);
+  return hipGetLastError();
+}
+
+hipError_t launch_certify_lex(const DevProblem &P, const float *cap_lo, const float *cap_hi, const float *tail_lo,
+                              const float *tail_hi, const uint8_t *measured, int32_t O, float eps, int32_t *state,
+                              AllocOut cons, AllocOut opt, double *gap_mm, double *gap_gp, uint8_t *ws,
+                              const WsLayout &L, hipStream_t s) {
+  if (O == 0) return hipSuccess;
+  k_certify_lex<<<O, 64, lds_bytes_lex(P, 2), s>>>(P, (const int8_t *)(ws + L.bmap), cap_lo, cap_hi, tail_lo,
+                                                   tail_hi, measured, eps, state, cons, opt, gap_mm, gap_gp);
   return hipGetLastError();
 }
 

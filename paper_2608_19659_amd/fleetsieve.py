@@ -31,7 +31,8 @@ KERNEL_AUTO, KERNEL_WAVE, KERNEL_LANE, KERNEL_EXCLUSION = 0, 1, 2, 3
 EXPORTED = ("fs_context_create", "fs_context_destroy", "fs_context_set_option", "fs_context_kernel_timing",
             "fs_last_error",
             "fs_validate_problem", "fs_workspace_size", "fs_solve_batch", "fs_score_candidates",
-            "fs_certify", "fs_loop_workspace_size", "fs_profile_loop", "fs_reduce_cells", "fs_reduce_samples")
+            "fs_certify", "fs_loop_workspace_size", "fs_profile_loop", "fs_reduce_cells", "fs_reduce_samples",
+            "fs_solve_batch_lex", "fs_certify_lex")
 POLICY_SCORE, POLICY_ORDER = 0, 1
 CELL_SECONDS = 300.0
 
@@ -100,6 +101,8 @@ def load_library():
     lib.fs_loop_workspace_size.argtypes = [P, i32, i32, i32, ctypes.POINTER(sz)]
     lib.fs_profile_loop.argtypes = [vp, P, _Intervals, i32, vp, vp, vp, i32, vp, vp, i32, ctypes.c_float,
                                     ctypes.c_int, vp, i32, i32, _LoopOut, vp, sz, vp]
+    lib.fs_solve_batch_lex.argtypes = [vp, P, vp, vp, i64, _Alloc, vp, vp, sz, vp]
+    lib.fs_certify_lex.argtypes = [vp, P, _Intervals, i32, ctypes.c_float, vp, _Alloc, _Alloc, vp, vp, vp, sz, vp]
     Q = ctypes.POINTER(_SloPolicy)
     lib.fs_reduce_cells.argtypes = [vp, P, Q, vp, vp, i64, vp, vp]
     lib.fs_reduce_samples.argtypes = [vp, P, Q, vp, i32, vp, vp, i32, i32, vp, vp]
@@ -253,6 +256,25 @@ def solve_batch(ctx: Context, problem, cap, tail, stream=None, workspace=None):
     return out
 
 
+def solve_batch_lex(ctx: Context, problem, cap, tail, stream=None, workspace=None):
+    """Dense batch solve under the whole lexicographic objective (levels
+    1-4, fs_solve_batch_lex).  As solve_batch, plus goodput64: level (3)'s
+    binary64 total per scenario."""
+    torch = _torch()
+    ref = _ProblemRef(problem)
+    n = int(cap.shape[0]) if cap.dim() == 2 else 0
+    pc = _dev_ptr(cap, torch.float32, (n, ref.N), "cap")
+    pt = _dev_ptr(tail, torch.float32, (n, ref.N), "tail")
+    out = _alloc_tensors(n, ref.K, cap.device)
+    out["goodput64"] = torch.empty(n, dtype=torch.float64, device=cap.device)
+    ws_bytes = workspace_size(problem)
+    ws = workspace if workspace is not None else ctx.workspace(ws_bytes)
+    _check(load_library().fs_solve_batch_lex(ctx.handle, ref.ptr, pc, pt, n, _alloc_struct(out),
+                                             out["goodput64"].data_ptr(), ws.data_ptr(), ws.numel(),
+                                             _stream(cap.device, stream)))
+    return out
+
+
 @dataclass
 class DeviceIntervals:
     cap_lo: object
@@ -356,6 +378,37 @@ def certify(ctx: Context, problem, iv: DeviceIntervals, eps: float = 0.05, strea
                                      _alloc_struct(cons), _alloc_struct(opt), gap.data_ptr(), ws.data_ptr(),
                                      ws.numel(), _stream(dev, stream)))
     return CertifyOutput(state, gap, cons, opt)
+
+
+@dataclass
+class CertifyLexOutput:
+    state: object
+    gap_maxmin: object   # [O] float64, tau+ - tau-
+    gap_goodput: object  # [O] float64, |gp+ - gp-| / max(gp+, gp-)
+    cons: dict
+    opt: dict
+
+
+def certify_lex(ctx: Context, problem, iv: DeviceIntervals, eps: float = 0.05, stream=None,
+                workspace=None) -> CertifyLexOutput:
+    """Certificate with the stage-wise gap under the whole objective
+    (fs_certify_lex)."""
+    torch = _torch()
+    ref = _ProblemRef(problem)
+    O = int(iv.cap_lo.shape[0])
+    dev = iv.cap_lo.device
+    ivs = _intervals_struct(iv, O, ref.N)
+    state = torch.empty(O, dtype=torch.int32, device=dev)
+    gmm = torch.empty(O, dtype=torch.float64, device=dev)
+    ggp = torch.empty(O, dtype=torch.float64, device=dev)
+    cons = _alloc_tensors(O, ref.K, dev)
+    opt = _alloc_tensors(O, ref.K, dev)
+    ws_bytes = workspace_size(problem)
+    ws = workspace if workspace is not None else ctx.workspace(ws_bytes)
+    _check(load_library().fs_certify_lex(ctx.handle, ref.ptr, ivs, O, float(eps), state.data_ptr(),
+                                         _alloc_struct(cons), _alloc_struct(opt), gmm.data_ptr(), ggp.data_ptr(),
+                                         ws.data_ptr(), ws.numel(), _stream(dev, stream)))
+    return CertifyLexOutput(state, gmm, ggp, cons, opt)
 
 
 def loop_workspace_size(problem, n_orders: int, n_cand: int, n_samples: int) -> int:

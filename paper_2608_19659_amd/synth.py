@@ -390,3 +390,19 @@ def make_policy_inputs(w: Workload, with_samples: bool = True) -> PolicyInputs:
             succ_s[j] = np.clip(lo + srng.random((E, S)).astype(np.float32) * (hi - lo), lo, hi)
     return PolicyInputs(limit, success_min, tail_lo, tail_hi, succ_lo, succ_hi, truth_tail, truth_succ,
                         tail_s, succ_s)
+
+
+def interval_realisations(w: Workload, n: int, seed: int = 11):
+    """n point realisations of a workload's uncertainty: realisation j draws
+    every cell of order j mod O uniformly inside its intervals (capacity on
+    the 1/64 req/s grid, tail in binary32).  Returns cap, tail [n][N]."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([w.seed, seed, 8])))
+    iv = w.intervals
+    O, N = iv.cap_lo.shape
+    rows = np.arange(n) % O
+    lo, hi = iv.cap_lo[rows], iv.cap_hi[rows]
+    k = np.floor(rng.random((n, N)) * (np.rint((hi - lo) * 64.0) + 1.0))
+    cap = (lo + k / 64.0).astype(np.float32)
+    tl, th = iv.tail_lo[rows], iv.tail_hi[rows]
+    tail = np.clip(tl + rng.random((n, N)).astype(np.float32) * (th - tl), tl, th).astype(np.float32)
+    return cap, tail

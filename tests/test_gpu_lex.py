@@ -1,0 +1,150 @@
+"""The whole lexicographic objective (Section 3, levels 1-4) and the
+stage-wise certificate (Section 4.2) on the GPU, through the C ABI
+(fs_solve_batch_lex, fs_certify_lex), against the hand-derived cases and
+the oracle bit for bit: tau*, floors, allocation, binary32 goodput, level
+(3)'s binary64 total, states and both gaps."""
+import sys
+from types import SimpleNamespace
+
+import numpy as np
+import pytest
+
+import oracle
+from conftest import load_golden
+from paper_2608_19659_amd.synth import Intervals, Problem, make_workload, random_point_tables, random_problem
+from test_oracle_lex import STATES, hw1_tables
+
+pytestmark = pytest.mark.gpu
+
+
+def note(msg):
+    print(f"[gpu] {msg}", file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def env():
+    import torch
+    from paper_2608_19659_amd import fleetsieve as fs
+    if not torch.cuda.is_available():
+        pytest.skip("no ROCm device")
+    return torch, fs, fs.Context(0)
+
+
+def _t(env, a):
+    return env[0].from_numpy(np.ascontiguousarray(a)).to("cuda:0")
+
+
+def gpu_solve_lex(env, p, cap, tail):
+    torch, fs, ctx = env
+    out = fs.solve_batch_lex(ctx, p, _t(env, cap), _t(env, tail))
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in out.items()}
+
+
+def assert_lex_equal(p, g, j, a, what=""):
+    assert g["objective"][j].view(np.uint32) == np.float32(a.tau).view(np.uint32), (what, g["objective"][j], a.tau)
+    assert int(g["floors_met"][j]) == a.floors_met, what
+    assert list(g["tp_index"][j]) == [255 if t < 0 else t for t in a.tp_index], (what, list(g["tp_index"][j]),
+                                                                                 a.tp_index)
+    assert list(g["replicas"][j].view(np.uint16)) == a.replicas, (what, a.replicas)
+    assert g["goodput"][j].view(np.uint32) == np.float32(a.goodput).view(np.uint32), what
+    assert g["goodput64"][j] == a.goodput64, (what, g["goodput64"][j], a.goodput64)
+
+
+@pytest.mark.parametrize("case", range(len(load_golden("lex_objective.json")["solves"])))
+def test_hand_derived_solves_on_gpu(env, case):
+    g = load_golden("lex_objective.json")
+    c = g["solves"][case]
+    note(f"lex golden solve: {c['what']}")
+    p, cap, tail = hw1_tables(g, c["budget"], c.get("floor"), c.get("code_tail"), c.get("tail_override", ()))
+    r = gpu_solve_lex(env, p, cap[None], tail[None])
+    assert r["objective"][0] == np.float32(c["tau"])
+    assert [0 if t == 255 else int(p.tp[t]) for t in r["tp_index"][0]] == c["tp"]
+    assert list(r["replicas"][0].view(np.uint16)) == c["replicas"]
+    assert r["goodput64"][0] == c["goodput"] and r["goodput"][0] == np.float32(c["goodput"])
+
+
+@pytest.mark.parametrize("case", range(len(load_golden("lex_objective.json")["certificates"])))
+def test_hand_derived_certificates_on_gpu(env, case):
+    torch, fs, ctx = env
+    g = load_golden("lex_objective.json")
+    c = g["certificates"][case]
+    note(f"lex golden certificate: {c['what']}")
+    p, cap, tail = hw1_tables(g, c["budget"])
+    lo, hi = cap.copy(), cap.copy()
+    lo[c["cell"]] = c["cap_lo"]
+    if c["measured_cell"]:
+        hi[c["cell"]] = c["cap_lo"]
+    meas = np.ones(p.n_cells, np.uint8)
+    meas[c["cell"]] = c["measured_cell"]
+    iv = Intervals(lo[None], hi[None], tail[None], tail[None], meas[None])
+    r = fs.certify_lex(ctx, p, fs.DeviceIntervals.from_host(iv, "cuda:0"), eps=c["eps"])
+    torch.cuda.synchronize()
+    assert r.state.item() == STATES[c["state"]]
+    assert r.gap_maxmin.item() == c["gap_mm"]
+    assert r.gap_goodput.item() == c["gap_gp_num"] / c["gap_gp_den"]
+    cons_tp = [0 if t == 255 else int(p.tp[t]) for t in r.cons["tp_index"][0].cpu().numpy()]
+    assert cons_tp == c["cons_tp"] and list(r.cons["replicas"][0].cpu().numpy()) == c["cons_replicas"]
+
+
+@pytest.mark.parametrize("critical", [False, True])
+def test_random_problems_match_oracle(env, critical):
+    rng = np.random.default_rng(15 + critical)
+    for inst in range(24):
+        tp = [[1, 2, 4, 8], [2, 4, 8], [1], [1, 3, 5], [2, 4]][inst % 5]
+        K = int(rng.integers(1, 6))
+        G = int(rng.integers(tp[0], 40 if inst % 3 else 150))
+        p = random_problem(seed=3000 + inst, K=K, tp=tp, G=G, n_levels=int(rng.integers(1, 6)), critical=critical)
+        cap, tail = random_point_tables(p, 16, seed=inst, cap_range=(0.0, 3.0), tail_range=(5.0, 45.0))
+        note(f"lex dense inst {inst} K={K} G={G} tp={tp} critical={critical}")
+        g = gpu_solve_lex(env, p, cap, tail)
+        for j in range(cap.shape[0]):
+            assert_lex_equal(p, g, j, oracle.solve(p, cap[j], tail[j], "lex"), f"inst {inst} row {j}")
+
+
+@pytest.mark.parametrize("name,n", [("paper-shaped-2class-G16", 64), ("4class-G64", 32), ("8class-G256", 8),
+                                    ("16class-G1024", 2)])
+def test_workload_realisations_match_oracle(env, name, n):
+    """Both corners of the workloads' intervals, the 16-class G=1024 case at
+    the largest budget the stage's LDS holds for it."""
+    w = make_workload(name, orders=list(range(min(n, 4))), with_samples=False)
+    p = w.problem
+    iv = w.intervals
+    cap = np.concatenate([iv.cap_lo, iv.cap_hi])[:n]
+    tail = np.concatenate([iv.tail_hi, iv.tail_lo])[:n]
+    note(f"lex dense {name} x {cap.shape[0]}")
+    g = gpu_solve_lex(env, p, cap, tail)
+    for j in range(cap.shape[0]):
+        assert_lex_equal(p, g, j, oracle.solve(p, cap[j], tail[j], "lex"), f"{name} row {j}")
+
+
+@pytest.mark.parametrize("name,orders", [("paper-shaped-2class-G16", list(range(12))), ("4class-G64", [0, 1, 2, 3]),
+                                         ("8class-G256", [0, 1])])
+def test_certificates_match_oracle(env, name, orders):
+    torch, fs, ctx = env
+    w = make_workload(name, orders=orders, with_samples=False)
+    note(f"lex certify {name} orders={orders}")
+    r = fs.certify_lex(ctx, w.problem, fs.DeviceIntervals.from_host(w.intervals, "cuda:0"), eps=0.05)
+    torch.cuda.synchronize()
+    o = oracle.certify_lex(w.problem, w.intervals, eps=0.05)
+    np.testing.assert_array_equal(r.state.cpu().numpy(), o.state)
+    np.testing.assert_array_equal(r.gap_maxmin.cpu().numpy(), o.gap_mm)
+    np.testing.assert_array_equal(r.gap_goodput.cpu().numpy(), o.gap_gp)
+    c = {k: v.cpu().numpy() for k, v in r.cons.items()}
+    op = {k: v.cpu().numpy() for k, v in r.opt.items()}
+    for j in range(len(orders)):
+        for got, a in ((c, o.cons[j]), (op, o.opt[j])):
+            assert list(got["tp_index"][j]) == [255 if t < 0 else t for t in a.tp_index], (name, j)
+            assert list(got["replicas"][j].view(np.uint16)) == a.replicas, (name, j)
+            assert got["goodput"][j].view(np.uint32) == np.float32(a.goodput).view(np.uint32), (name, j)
+    assert (o.gap_gp > 0).any()
+
+
+def test_unsupported_sizes_are_rejected(env):
+    torch, fs, ctx = env
+    p = random_problem(seed=5, K=64, tp=[1, 2, 4, 8], G=512, n_levels=2)
+    note("lex K=64 G=512: rejected before any launch")
+    cap = torch.zeros((1, p.n_cells), device="cuda:0")
+    with pytest.raises(fs.FleetSieveError) as e:
+        fs.solve_batch_lex(ctx, p, cap, cap)
+    assert e.value.status == fs.FS_ERR_UNSUPPORTED

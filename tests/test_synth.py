@@ -60,3 +60,16 @@ def test_structure(name):
         lo = iv.tail_lo[:, w.cand][:, :, None]
         hi = iv.tail_hi[:, w.cand][:, :, None]
         assert np.all((w.tail_s >= lo) & (w.tail_s <= hi))
+
+
+def test_interval_realisations_stay_inside():
+    from paper_2608_19659_amd.synth import interval_realisations
+    w = make_workload("4class-G64", with_samples=False)
+    cap, tail = interval_realisations(w, 100)
+    iv = w.intervals
+    rows = np.arange(100) % iv.cap_lo.shape[0]
+    assert (cap >= iv.cap_lo[rows]).all() and (cap <= iv.cap_hi[rows]).all()
+    assert (tail >= iv.tail_lo[rows]).all() and (tail <= iv.tail_hi[rows]).all()
+    assert np.array_equal(np.rint(cap * 64.0), cap * 64.0)
+    c2, t2 = interval_realisations(w, 100)
+    assert np.array_equal(cap, c2) and np.array_equal(tail, t2)
