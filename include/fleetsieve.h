@@ -136,8 +136,16 @@ typedef enum fs_option {
    * realisation when the budget is at most 64 GPUs, there are at most 16
    * classes and its LDS fits), 1 = the general set-up (one block per order,
    * realisation and class; any problem).  Results are identical. */
-  FS_OPT_SETUP = 6
+  FS_OPT_SETUP = 6,
+  /* Certificate of fs_profile_loop: FS_OBJECTIVE_MAXMIN (default; objective
+   * levels 1-2 and the max-min gap, as fs_certify) or
+   * FS_OBJECTIVE_LEXICOGRAPHIC (the whole objective and the stage-wise gap,
+   * as fs_certify_lex; FS_ERR_UNSUPPORTED where that does not fit).  The
+   * score stays the max-min stage's either way. */
+  FS_OPT_LOOP_OBJECTIVE = 7
 } fs_option;
+
+typedef enum fs_objective { FS_OBJECTIVE_MAXMIN = 0, FS_OBJECTIVE_LEXICOGRAPHIC = 1 } fs_objective;
 
 /* Creates a context bound to HIP device `hip_device`.  One context per host
  * thread; a context is not thread-safe. */

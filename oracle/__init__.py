@@ -340,7 +340,7 @@ def value_on_table(problem, alloc: Alloc, cap, tail) -> np.float32:
 
 def profile_loop(problem, intervals, truth_cap, truth_tail, cand, cap_s, tail_s, eps: float = 0.05,
                  policy: int = POLICY_SCORE, order=None, max_rounds: int = None,
-                 n_threads: int = 1) -> LoopResult:
+                 n_threads: int = 1, objective: str = "maxmin") -> LoopResult:
     """Algorithm 1 (the profiling loop) for O independent trajectories, each
     starting from its own row of ``intervals`` (the common initial design).
     Per round, for every trajectory still running: the conservative and
@@ -353,7 +353,9 @@ def profile_loop(problem, intervals, truth_cap, truth_tail, cand, cap_s, tail_s,
     for the comparison, the first unmeasured one in order[o] (POLICY_ORDER,
     e.g. a uniform random permutation).  A trajectory with no unmeasured
     candidate left returns A- undecided (the certificate of its final
-    intervals is evaluated first, so a last reveal can still certify).  The
+    intervals is evaluated first, so a last reveal can still certify).  With
+    objective="lex" the certificate is the stage-wise one under the whole
+    objective (certify_lex) and A- is that objective's allocation.  The
     allocation's value on the true table gives the decision regret against
     the true optimum.  The intervals are not refitted
     between rounds; the samples of a candidate stay valid because its
@@ -389,7 +391,7 @@ def profile_loop(problem, intervals, truth_cap, truth_tail, cand, cap_s, tail_s,
         idx = np.nonzero(running)[0]
         if len(idx) == 0:
             break
-        cert = certify(problem, _Rows(idx), eps)
+        cert = certify(problem, _Rows(idx), eps) if objective == "maxmin" else certify_lex(problem, _Rows(idx), eps)
         for j, o in enumerate(idx):
             state[o] = cert.state[j]
             final[o] = cert.cons[j]

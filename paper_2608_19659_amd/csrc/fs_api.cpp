@@ -21,6 +21,7 @@ struct fs_context {
   int spl;           // exclusion scorer samples per lane (0 = default)
   int waves;         // exclusion scorer grid in wavefronts (0 = default)
   int setup;         // exclusion scorer set-up: 0 automatic, 1 general
+  int loop_objective;  // profiling loop certificate: 0 max-min, 1 whole objective
   int32_t *pinned;   // pinned host word: running trajectories read back by fs_profile_loop
   struct Timed {
     hipEvent_t begin, end;
@@ -152,7 +153,7 @@ fs_status fs_context_create(int hip_device, fs_context **out) {
   e = hipSetDevice(hip_device);
   if (e == hipSuccess) e = hipHostMalloc((void **)&pinned, 64, hipHostMallocDefault);
   if (e != hipSuccess) return hip_fail(e, "hipHostMalloc");
-  *out = new fs_context{hip_device, 0, 0, 0, 0, 0, pinned, {}};
+  *out = new fs_context{hip_device, 0, 0, 0, 0, 0, 0, pinned, {}};
   return FS_OK;
 }
 
@@ -205,6 +206,12 @@ fs_status fs_context_set_option(fs_context *ctx, fs_option option, int64_t value
     if (value < 0 || value > (1 << 20))
       return fail(FS_ERR_INVALID_ARGUMENT, "scorer wavefronts must be in [0, 2^20]");
     ctx->waves = (int)value;
+    return FS_OK;
+  }
+  if (option == FS_OPT_LOOP_OBJECTIVE) {
+    if (value != FS_OBJECTIVE_MAXMIN && value != FS_OBJECTIVE_LEXICOGRAPHIC)
+      return fail(FS_ERR_INVALID_ARGUMENT, "loop objective must be FS_OBJECTIVE_MAXMIN or FS_OBJECTIVE_LEXICOGRAPHIC");
+    ctx->loop_objective = (int)value;
     return FS_OK;
   }
   if (option == FS_OPT_SETUP) {
@@ -433,6 +440,11 @@ fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv,
                 "lane-per-scenario scoring needs no floors, TP set {1,2,4,8} and budget 16, 32 or 64");
   if (kernel == 3 && !fs::excl_kernel_supported(P))
     return fail(FS_ERR_UNSUPPORTED, "exclusion scoring does not handle critical floors");
+  const bool lex = ctx->loop_objective == FS_OBJECTIVE_LEXICOGRAPHIC;
+  if (lex) {
+    st = lex_supported(P, 2);
+    if (st != FS_OK) return st;
+  }
   const int32_t S = (n_cand > 0 && policy == FS_POLICY_SCORE) ? n_samples : 0;
   const fs::LoopLayout LL = fs::loop_layout(P, n_orders, n_cand, S);
   if (!d_workspace) return fail(FS_ERR_INVALID_ARGUMENT, "workspace is NULL");
@@ -461,8 +473,10 @@ fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv,
   if (e != hipSuccess) return hip_fail(e, "loop set-up launch");
   const fs::AllocOut none{nullptr, nullptr, nullptr, nullptr, nullptr};
   for (int32_t rnd = 0; rnd <= max_rounds; ++rnd) {
-    e = fs::launch_certify(P, D.cap_lo, D.cap_hi, D.tail_lo, D.tail_hi, D.measured, n_orders, eps, D.cert_state,
-                           D.cons, none, nullptr, ws, LL.score, stream);
+    e = lex ? fs::launch_certify_lex(P, D.cap_lo, D.cap_hi, D.tail_lo, D.tail_hi, D.measured, n_orders, eps,
+                                     D.cert_state, D.cons, none, nullptr, nullptr, ws, LL.score, stream)
+            : fs::launch_certify(P, D.cap_lo, D.cap_hi, D.tail_lo, D.tail_hi, D.measured, n_orders, eps,
+                                 D.cert_state, D.cons, none, nullptr, ws, LL.score, stream);
     if (e == hipSuccess) e = fs::launch_loop_decide(P, D, d_cand, n_cand, n_orders, stream);
     if (e != hipSuccess) return hip_fail(e, "loop certificate launch");
     if (rnd == max_rounds) break;

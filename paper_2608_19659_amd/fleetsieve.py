@@ -26,6 +26,8 @@ OPT_KERNEL_TIMING = 2
 OPT_SAMPLES_PER_LANE = 3
 OPT_SCORER_WAVES = 5
 OPT_SETUP = 6
+OPT_LOOP_OBJECTIVE = 7
+OBJECTIVE_MAXMIN, OBJECTIVE_LEXICOGRAPHIC = 0, 1
 KERNEL_AUTO, KERNEL_WAVE, KERNEL_LANE, KERNEL_EXCLUSION = 0, 1, 2, 3
 
 EXPORTED = ("fs_context_create", "fs_context_destroy", "fs_context_set_option", "fs_context_kernel_timing",

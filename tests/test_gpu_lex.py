@@ -148,3 +148,60 @@ def test_unsupported_sizes_are_rejected(env):
     with pytest.raises(fs.FleetSieveError) as e:
         fs.solve_batch_lex(ctx, p, cap, cap)
     assert e.value.status == fs.FS_ERR_UNSUPPORTED
+
+
+def _gpu_loop(env, p, iv, tc, tt, cand, cs, ts, eps, objective, max_rounds=None):
+    torch, fs, ctx = env
+    ctx.set_option(fs.OPT_LOOP_OBJECTIVE, objective)
+    try:
+        r = fs.profile_loop(ctx, p, fs.DeviceIntervals.from_host(iv, "cuda:0"), _t(env, tc), _t(env, tt),
+                            _t(env, np.asarray(cand, np.int32)), _t(env, cs), _t(env, ts), eps=eps,
+                            max_rounds=max_rounds)
+        torch.cuda.synchronize()
+    finally:
+        ctx.set_option(fs.OPT_LOOP_OBJECTIVE, fs.OBJECTIVE_MAXMIN)
+    return {k: (v.cpu().numpy() if hasattr(v, "cpu") else {kk: vv.cpu().numpy() for kk, vv in v.items()})
+            for k, v in vars(r).items()}
+
+
+@pytest.mark.parametrize("objective", ["lex", "maxmin"])
+def test_hand_derived_loop_on_gpu(env, objective):
+    from test_oracle_lex import _loop_inputs
+    torch, fs, ctx = env
+    g = load_golden("lex_objective.json")
+    c = g["loop"]
+    p, iv, tc, tt, cand, cs, ts = _loop_inputs(g, c)
+    note(f"lex golden loop, {objective}")
+    code = fs.OBJECTIVE_LEXICOGRAPHIC if objective == "lex" else fs.OBJECTIVE_MAXMIN
+    r = _gpu_loop(env, p, iv, tc, tt, cand, cs, ts, c["eps"], code)
+    want = c[objective]
+    assert r["state"][0] == STATES[want["state"]] and r["rounds"][0] == want["rounds"]
+    assert list(r["reveals"][0][: want["rounds"]]) == want["reveals"]
+    assert r["gpu_seconds"][0] == want["gpu_seconds"]
+    assert [0 if t == 255 else int(p.tp[t]) for t in r["final"]["tp_index"][0]] == want["final_tp"]
+    assert list(r["final"]["replicas"][0].view(np.uint16)) == want["final_replicas"]
+    assert r["tau_truth"][0] == np.float32(want["tau_truth"])
+
+
+@pytest.mark.parametrize("name,orders,S,max_rounds", [("paper-shaped-2class-G16", list(range(8)), 64, None),
+                                                      ("4class-G64", [1, 2], 256, 12)])
+def test_loop_under_whole_objective_matches_oracle(env, name, orders, S, max_rounds):
+    torch, fs, ctx = env
+    w = make_workload(name, orders=orders)
+    O = len(orders)
+    tc = np.repeat(w.truth_cap[None], O, axis=0)
+    tt = np.repeat(w.truth_tail[None], O, axis=0)
+    cs, ts = np.ascontiguousarray(w.cap_s[:, :, :S]), np.ascontiguousarray(w.tail_s[:, :, :S])
+    note(f"lex loop {name} orders={orders} S={S}")
+    o = oracle.profile_loop(w.problem, w.intervals, tc, tt, w.cand, cs, ts, eps=0.05, max_rounds=max_rounds,
+                            n_threads=8, objective="lex")
+    r = _gpu_loop(env, w.problem, w.intervals, tc, tt, w.cand, cs, ts, 0.05, fs.OBJECTIVE_LEXICOGRAPHIC,
+                  max_rounds)
+    np.testing.assert_array_equal(r["state"], o.state)
+    np.testing.assert_array_equal(r["rounds"], o.rounds)
+    np.testing.assert_array_equal(r["reveals"], o.reveals)
+    np.testing.assert_array_equal(r["gpu_seconds"], o.gpu_seconds)
+    np.testing.assert_array_equal(r["tau_truth"], o.tau_truth)
+    for j, a in enumerate(o.final):
+        assert list(r["final"]["replicas"][j].view(np.uint16)) == a.replicas, j
+        assert list(r["final"]["tp_index"][j]) == [255 if t < 0 else t for t in a.tp_index], j

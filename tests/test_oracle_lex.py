@@ -135,3 +135,32 @@ def test_certificate_stages():
     pt = SimpleNamespace(cap_lo=cap, cap_hi=cap, tail_lo=tail, tail_hi=tail, measured=np.ones(cap.shape, np.uint8))
     r = oracle.certify_lex(p, pt, 0.0)
     assert (r.gap_mm == 0).all() and (r.gap_gp == 0).all() and (r.state == 1).all()
+
+
+def _loop_inputs(g, c):
+    p, cap, tail = hw1_tables(g, c["budget"])
+    cell = c["cand"][0]
+    lo, hi, truth = cap.copy(), cap.copy(), cap.copy()
+    lo[cell] = min(c["cap_s"])
+    hi[cell] = max(c["cap_s"])
+    truth[cell] = c["truth_cap"]
+    meas = np.ones(p.n_cells, np.uint8)
+    meas[cell] = 0
+    iv = SimpleNamespace(cap_lo=lo[None], cap_hi=hi[None], tail_lo=tail[None], tail_hi=tail[None],
+                         measured=meas[None])
+    cs = np.array([[c["cap_s"]]], np.float32)
+    ts = np.full_like(cs, g["tail"])
+    return p, iv, truth[None], tail[None], np.array(c["cand"], np.int32), cs, ts
+
+
+@pytest.mark.parametrize("objective", ["lex", "maxmin"])
+def test_hand_derived_loop(objective):
+    g = load_golden("lex_objective.json")
+    c = g["loop"]
+    p, iv, tc, tt, cand, cs, ts = _loop_inputs(g, c)
+    r = oracle.profile_loop(p, iv, tc, tt, cand, cs, ts, eps=c["eps"], objective=objective)
+    want = c[objective]
+    assert r.state[0] == STATES[want["state"]] and r.rounds[0] == want["rounds"]
+    assert list(r.reveals[0][: want["rounds"]]) == want["reveals"] and r.gpu_seconds[0] == want["gpu_seconds"]
+    assert r.final[0].tp(p) == want["final_tp"] and r.final[0].replicas == want["final_replicas"]
+    assert r.tau_truth[0] == np.float32(want["tau_truth"]) and r.regret[0] == 0.0
