@@ -340,7 +340,7 @@ def value_on_table(problem, alloc: Alloc, cap, tail) -> np.float32:
 
 def profile_loop(problem, intervals, truth_cap, truth_tail, cand, cap_s, tail_s, eps: float = 0.05,
                  policy: int = POLICY_SCORE, order=None, max_rounds: int = None,
-                 n_threads: int = 1, objective: str = "maxmin") -> LoopResult:
+                 n_threads: int = 1, objective: str = "maxmin", refit: bool = False) -> LoopResult:
     """Algorithm 1 (the profiling loop) for O independent trajectories, each
     starting from its own row of ``intervals`` (the common initial design).
     Per round, for every trajectory still running: the conservative and
@@ -355,7 +355,11 @@ def profile_loop(problem, intervals, truth_cap, truth_tail, cand, cap_s, tail_s,
     candidate left returns A- undecided (the certificate of its final
     intervals is evaluated first, so a last reveal can still certify).  With
     objective="lex" the certificate is the stage-wise one under the whole
-    objective (certify_lex) and A- is that objective's allocation.  The
+    objective (certify_lex) and A- is that objective's allocation.  With
+    refit=True every round starts with refit_intervals (Algorithm 1's fit
+    step) of the trajectory's initial intervals with its revealed cells, the
+    certificate and score use the refitted intervals, and the score's
+    samples are clamped into them.  The
     allocation's value on the true table gives the decision regret against
     the true optimum.  The intervals are not refitted
     between rounds; the samples of a candidate stay valid because its
@@ -391,7 +395,11 @@ def profile_loop(problem, intervals, truth_cap, truth_tail, cand, cap_s, tail_s,
         idx = np.nonzero(running)[0]
         if len(idx) == 0:
             break
-        cert = certify(problem, _Rows(idx), eps) if objective == "maxmin" else certify_lex(problem, _Rows(idx), eps)
+        # the refit is a function of the initial intervals and the revealed
+        # cells, recomputed every round (the trajectory's own arrays keep the
+        # unrefitted intervals)
+        rows = refit_intervals(problem, _Rows(idx)) if refit else _Rows(idx)
+        cert = certify(problem, rows, eps) if objective == "maxmin" else certify_lex(problem, rows, eps)
         for j, o in enumerate(idx):
             state[o] = cert.state[j]
             final[o] = cert.cons[j]
@@ -407,8 +415,12 @@ def profile_loop(problem, intervals, truth_cap, truth_tail, cand, cap_s, tail_s,
         if len(idx) == 0:
             break
         if policy == POLICY_SCORE:
-            sc = score(problem, _Rows(idx), cand, np.asarray(cap_s)[idx], np.asarray(tail_s)[idx],
-                       dump=False, n_threads=n_threads)
+            cs, ts = np.asarray(cap_s)[idx], np.asarray(tail_s)[idx]
+            rows = _Rows(idx)
+            if refit:
+                rows = refit_intervals(problem, rows)
+                cs, ts = clamp_samples(rows, cand, cs, ts)
+            sc = score(problem, rows, cand, cs, ts, dump=False, n_threads=n_threads)
             picks = [int(b) for b in sc.best]
         else:
             picks = []
@@ -436,6 +448,93 @@ def profile_loop(problem, intervals, truth_cap, truth_tail, cand, cap_s, tail_s,
         tau_truth[o] = value_on_table(problem, final[o], tc[o], tt[o])
     regret = tau_oracle.astype(np.float64) - tau_truth.astype(np.float64)
     return LoopResult(state, finished, rounds, gpu_s, reveals, final, tau_truth, tau_oracle, regret)
+
+
+# ------------------------------------------------------- interval refit --
+def _round_down_f32(x: float) -> np.float32:
+    """The largest binary32 value not above the binary64 value x."""
+    v = np.float32(x)
+    if float(v) > x:
+        v = np.nextafter(v, np.float32(-np.inf))
+    return np.float32(v)
+
+
+def refit_intervals(problem, intervals):
+    """Interval refit of Algorithm 1's fit step under a structural prior
+    (Section 4.1: an interior-knee prior combined with the measured cells).
+    The prior, as read here: for every class and load level, the capacity
+    per GPU (c / t) is unimodal over the TP degrees in ascending order (it
+    rises to the knee and falls after it), and for every class and TP degree
+    the tail is nondecreasing in the load level.  Consequences drawn from the
+    measured cells (their point values), for every unmeasured cell:
+      capacity: for measured TP degrees t_a < t < t_b at the same class and
+        level, c(t) / t >= min(c(t_a) / t_a, c(t_b) / t_b), so
+        cap_lo >= t * min(...) (binary64, rounded down to binary32);
+      tail: tail_lo >= the largest measured tail at a lower level of the same
+        class and TP, tail_hi <= the smallest measured tail at a higher level.
+    A bound that would empty the interval contradicts the prior; that
+    quantity keeps its interval.  Measured cells are unchanged.  Returns new
+    [O][N] arrays (cap_lo, cap_hi, tail_lo, tail_hi, measured)."""
+    from types import SimpleNamespace
+    ref = _ProblemRef(problem)
+    K, T, B = len(ref.demand), len(ref.tp), len(ref.levels)
+    N = K * T * B
+    cl = np.array(intervals.cap_lo, dtype=np.float32).reshape(-1, N)
+    O = cl.shape[0]
+    ch = np.array(intervals.cap_hi, dtype=np.float32).reshape(O, N)
+    tl = np.array(intervals.tail_lo, dtype=np.float32).reshape(O, N)
+    th = np.array(intervals.tail_hi, dtype=np.float32).reshape(O, N)
+    ms = np.array(intervals.measured, dtype=np.uint8).reshape(O, N)
+    out_cl, out_tl, out_th = cl.copy(), tl.copy(), th.copy()
+    cell = lambda i, t, b: (i * T + t) * B + b
+    for o in range(O):
+        for i in range(K):
+            for b in range(B):
+                for t in range(T):
+                    c = cell(i, t, b)
+                    if ms[o, c]:
+                        continue
+                    lo = cl[o, c]
+                    for a in range(t):
+                        for z in range(t + 1, T):
+                            ca, cz = cell(i, a, b), cell(i, z, b)
+                            if not (ms[o, ca] and ms[o, cz]):
+                                continue
+                            per_gpu = min(float(cl[o, ca]) / float(ref.tp[a]), float(cl[o, cz]) / float(ref.tp[z]))
+                            lo = max(lo, _round_down_f32(float(ref.tp[t]) * per_gpu))
+                    if lo <= ch[o, c]:
+                        out_cl[o, c] = lo
+            for t in range(T):
+                for b in range(B):
+                    c = cell(i, t, b)
+                    if ms[o, c]:
+                        continue
+                    lo, hi = tl[o, c], th[o, c]
+                    for b2 in range(B):
+                        c2 = cell(i, t, b2)
+                        if not ms[o, c2]:
+                            continue
+                        if b2 < b:
+                            lo = max(lo, tl[o, c2])
+                        elif b2 > b:
+                            hi = min(hi, tl[o, c2])
+                    if lo <= hi:
+                        out_tl[o, c], out_th[o, c] = lo, hi
+    return SimpleNamespace(cap_lo=out_cl, cap_hi=ch.copy(), tail_lo=out_tl, tail_hi=out_th, measured=ms.copy())
+
+
+def clamp_samples(intervals, cand, cap_s, tail_s):
+    """Samples of each candidate moved into its current intervals
+    (min(max(x, lo), hi)); used after a refit."""
+    cl = np.asarray(intervals.cap_lo, np.float32)
+    O = cl.shape[0]
+    cand = np.asarray(cand, np.int64)
+    lo_c, hi_c = cl[:, cand][:, :, None], np.asarray(intervals.cap_hi, np.float32)[:, cand][:, :, None]
+    lo_t = np.asarray(intervals.tail_lo, np.float32)[:, cand][:, :, None]
+    hi_t = np.asarray(intervals.tail_hi, np.float32)[:, cand][:, :, None]
+    cs = np.minimum(np.maximum(np.asarray(cap_s, np.float32).reshape(O, len(cand), -1), lo_c), hi_c)
+    ts = np.minimum(np.maximum(np.asarray(tail_s, np.float32).reshape(O, len(cand), -1), lo_t), hi_t)
+    return cs.astype(np.float32), ts.astype(np.float32)
 
 
 # ------------------------------------------------ multi-metric feasibility --

@@ -155,6 +155,19 @@ WORKLOADS = {
             cap_range=(0.1, 5.0), cap_width=(0.02, 0.5), tail_sigma=0.5, tail_alpha=1.0,
             tail_tp_factor=True, tail_width=(0.02, 0.5), orders=4, reveal=True,
             cand=("all",), samples=256),
+    # Truth drawn first with the structure the interval refit assumes
+    # (capacity per GPU unimodal over TP with its knee at TP4, tail
+    # nondecreasing in the load), intervals around it.
+    "paper-shaped-2class-G16-knee": dict(seed=1005, K=2, tp=[1, 2, 4, 8], G=16,
+            levels=[0.25, 0.5, 1.0, 2.0, 4.0, 8.0], demand=("fixed", [4.0, 3.0]), slo=("fixed", [30.0, 30.0]),
+            cap_range=(0.2, 3.0), cap_width=(0.05, 0.3), tail_sigma=0.4, tail_alpha=1.5,
+            tail_tp_factor=True, tail_width=(0.1, 0.4), orders=200, reveal=True,
+            cand=("all",), samples=1024, structure=True),
+    "4class-G64-knee": dict(seed=1006, K=4, tp=[1, 2, 4, 8], G=64, levels=_geometric(0.125, 8),
+            demand=("uniform", 1.0, 20.0), slo=("fixed", [30.0, 20.0, 2.0, 300.0]),
+            cap_range=(0.1, 5.0), cap_width=(0.05, 0.3), tail_sigma=0.5, tail_alpha=1.0,
+            tail_tp_factor=True, tail_width=(0.1, 0.4), orders=16, reveal=True,
+            cand=("all",), samples=4096, structure=True),
 }
 
 
@@ -228,6 +241,58 @@ def _initial_intervals(name: str, problem: Problem, rng):
     return cap_lo, cap_hi, tail_lo, tail_hi
 
 
+def _structured_truth(name: str, problem: Problem, rng):
+    """Truth with the refit's structure, then intervals containing it.
+    Per (class, level): capacity per GPU at the knee (TP4) drawn from the
+    workload's range over 4, each step away from the knee keeping a factor
+    U[0.55, 0.95] of its neighbour; per-replica values on the 1/64 grid
+    (redrawn until the per-GPU values stay unimodal after rounding).  Per
+    (class, TP): tails as in the generic workloads, then a running maximum
+    over increasing load.  Intervals: capacity [q64(c (1 - w)), q64(c (1 +
+    w'))] and tail [l / (1 + u), l (1 + u')], w, w', u, u' from the widths."""
+    c = WORKLOADS[name]
+    K, T, B = problem.n_classes, problem.n_tp, problem.n_levels
+    N = problem.n_cells
+    tp = [int(x) for x in problem.tp]
+    knee = tp.index(4)
+    truth_cap = np.zeros(N)
+    truth_tail = np.zeros(N, np.float32)
+    for i in range(K):
+        for b in range(B):
+            while True:
+                g = np.zeros(T)
+                g[knee] = rng.uniform(*c["cap_range"]) / 4.0
+                for t in range(knee - 1, -1, -1):
+                    g[t] = g[t + 1] * rng.uniform(0.55, 0.95)
+                for t in range(knee + 1, T):
+                    g[t] = g[t - 1] * rng.uniform(0.55, 0.95)
+                caps = q64(g * np.array(tp, float))
+                per_gpu = caps / np.array(tp, float)
+                if np.all(np.diff(per_gpu[:knee + 1]) >= 0) and np.all(np.diff(per_gpu[knee:]) <= 0):
+                    break
+            for t in range(T):
+                truth_cap[problem.cell(i, t, b)] = caps[t]
+    for i in range(K):
+        for t in range(T):
+            rho = TAIL_TP_FACTOR[int(problem.tp[t])] if c["tail_tp_factor"] else 1.0
+            run = np.float32(0.0)
+            for b in range(B):
+                load = float(problem.levels[b])
+                median = (float(problem.slo[i]) / 3.0) * (1.0 + load) ** c["tail_alpha"] * rho
+                run = max(run, np.float32(median * np.exp(c["tail_sigma"] * rng.standard_normal())))
+                truth_tail[problem.cell(i, t, b)] = run
+    w_lo = rng.uniform(*c["cap_width"], size=N)
+    w_hi = rng.uniform(*c["cap_width"], size=N)
+    cap_lo = np.minimum(q64(truth_cap * (1.0 - w_lo)), truth_cap)
+    cap_hi = np.maximum(q64(truth_cap * (1.0 + w_hi)), truth_cap)
+    u_lo = rng.uniform(*c["tail_width"], size=N)
+    u_hi = rng.uniform(*c["tail_width"], size=N)
+    tail_lo = np.minimum((truth_tail / (1.0 + u_lo)).astype(np.float32), truth_tail)
+    tail_hi = np.maximum((truth_tail * (1.0 + u_hi)).astype(np.float32), truth_tail)
+    return (cap_lo, cap_hi, tail_lo.astype(np.float64), tail_hi.astype(np.float64),
+            truth_cap.astype(np.float32), truth_tail)
+
+
 def _draw_inside(rng, cap_lo, cap_hi, tail_lo, tail_hi, shape=None):
     """Uniform draw inside intervals: capacity on the 1/64 grid, tail fp32."""
     steps = np.rint((np.asarray(cap_hi) - np.asarray(cap_lo)) * 64.0).astype(np.int64)
@@ -253,8 +318,11 @@ def make_workload(name: str, orders=None, with_samples: bool = True) -> Workload
     rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 0])))
     problem = _problem_for(name, rng)
     N = problem.n_cells
-    cap_lo0, cap_hi0, tail_lo0, tail_hi0 = _initial_intervals(name, problem, rng)
-    truth_cap, truth_tail = _draw_inside(rng, cap_lo0, cap_hi0, tail_lo0, tail_hi0)
+    if c.get("structure"):
+        cap_lo0, cap_hi0, tail_lo0, tail_hi0, truth_cap, truth_tail = _structured_truth(name, problem, rng)
+    else:
+        cap_lo0, cap_hi0, tail_lo0, tail_hi0 = _initial_intervals(name, problem, rng)
+        truth_cap, truth_tail = _draw_inside(rng, cap_lo0, cap_hi0, tail_lo0, tail_hi0)
     if c["cand"][0] == "subset":
         cand = np.sort(rng.choice(N, size=c["cand"][1], replace=False)).astype(np.int32)
     else:

@@ -46,12 +46,24 @@ def test_structure(name):
     # interior knee: per-GPU lower capacity of the initial intervals is largest
     # at TP4 in every (class, load); revealed cells hold the hidden truth instead
     k4 = list(p.tp).index(4)
-    for i in range(p.n_classes):
-        for b in range(p.n_levels):
-            if any(iv.measured[0][p.cell(i, t, b)] for t in range(p.n_tp)):
-                continue
-            per_gpu = [iv.cap_lo[0][p.cell(i, t, b)] / p.tp[t] for t in range(p.n_tp)]
-            assert all(per_gpu[k4] > v for t, v in enumerate(per_gpu) if t != k4)
+    if c.get("structure"):
+        # the truth has the refit's structure: per-GPU capacity unimodal over TP
+        # with its knee at TP4, tail nondecreasing in the load; it lies inside
+        for i in range(p.n_classes):
+            for b in range(p.n_levels):
+                per_gpu = np.array([w.truth_cap[p.cell(i, t, b)] / p.tp[t] for t in range(p.n_tp)])
+                assert np.all(np.diff(per_gpu[:k4 + 1]) >= 0) and np.all(np.diff(per_gpu[k4:]) <= 0)
+            for t in range(p.n_tp):
+                assert np.all(np.diff([w.truth_tail[p.cell(i, t, b)] for b in range(p.n_levels)]) >= 0)
+        assert np.all((iv.cap_lo <= w.truth_cap) & (w.truth_cap <= iv.cap_hi))
+        assert np.all((iv.tail_lo <= w.truth_tail) & (w.truth_tail <= iv.tail_hi))
+    else:
+        for i in range(p.n_classes):
+            for b in range(p.n_levels):
+                if any(iv.measured[0][p.cell(i, t, b)] for t in range(p.n_tp)):
+                    continue
+                per_gpu = [iv.cap_lo[0][p.cell(i, t, b)] / p.tp[t] for t in range(p.n_tp)]
+                assert all(per_gpu[k4] > v for t, v in enumerate(per_gpu) if t != k4)
     if w.cap_s is not None:
         lo = iv.cap_lo[:, w.cand][:, :, None]
         hi = iv.cap_hi[:, w.cand][:, :, None]
