@@ -192,29 +192,47 @@ def loop_bench(args):
     rng = np.random.default_rng(4242)
     order = t(np.stack([rng.permutation(E) for _ in range(O)]).astype(np.int32))
     ctx = fs.Context(0)
-    ws = ctx.workspace(fs.loop_workspace_size(p, O, E, S))
+    ws = ctx.workspace(fs.loop_refit_workspace_size(p, O, E, S) if args.refit else fs.loop_workspace_size(p, O, E, S))
 
-    def run(policy, reps):
+    def run(policy, reps, refit=False):
         ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         fs.profile_loop(ctx, p, iv, tc, tt, cand, cap_s, tail_s, eps, policy,
-                        order if policy == fs.POLICY_ORDER else None, workspace=ws)
+                        order if policy == fs.POLICY_ORDER else None, workspace=ws, refit=refit)
         torch.cuda.synchronize()
         ev0.record()
         for _ in range(reps):
             r = fs.profile_loop(ctx, p, iv, tc, tt, cand, cap_s, tail_s, eps, policy,
-                                order if policy == fs.POLICY_ORDER else None, workspace=ws)
+                                order if policy == fs.POLICY_ORDER else None, workspace=ws, refit=refit)
         ev1.record()
         torch.cuda.synchronize()
         return r, ev0.elapsed_time(ev1) / reps
 
     r_fs, ms_fs = run(fs.POLICY_SCORE, max(args.steps // 4, 1))
     r_rd, ms_rd = run(fs.POLICY_ORDER, max(args.steps // 4, 1))
+    r_rf = r_rdf = None
+    if args.refit:
+        r_rf, ms_rf = run(fs.POLICY_SCORE, max(args.steps // 4, 1), refit=True)
+        r_rdf, ms_rdf = run(fs.POLICY_ORDER, max(args.steps // 4, 1), refit=True)
     c = lambda x: x.cpu().numpy()
     gs_fs, gs_rd = c(r_fs.gpu_seconds), c(r_rd.gpu_seconds)
     st_fs, st_rd = c(r_fs.state), c(r_rd.state)
     reg = lambda r: (c(r.tau_oracle).astype(np.float64) - c(r.tau_truth).astype(np.float64))
     reg_fs, reg_rd = reg(r_fs), reg(r_rd)
     rounds_fs = c(r_fs.rounds)
+    refit_line = None
+    if r_rf is not None:
+        gs_rf = c(r_rf.gpu_seconds)
+        reg_rf = reg(r_rf)
+        refit_line = {"ms_per_loop": ms_rf, "gpu_seconds_mean": float(gs_rf.mean()),
+                      "saving_vs_no_refit": float(1.0 - gs_rf.mean() / gs_fs.mean()),
+                      "per_order_win_rate": float(np.mean(gs_rf < gs_fs)),
+                      "per_order_loss_rate": float(np.mean(gs_rf > gs_fs)),
+                      "certified_feasible_fraction": float(np.mean(c(r_rf.state) == 1)),
+                      "max_regret": float(reg_rf.max()), "rounds_mean": float(c(r_rf.rounds).mean()),
+                      "uniform_random": {"ms_per_loop": ms_rdf, "gpu_seconds_mean": float(c(r_rdf.gpu_seconds).mean()),
+                                         "saving_vs_no_refit": float(1.0 - c(r_rdf.gpu_seconds).mean() / gs_rd.mean()),
+                                         "max_regret": float(reg(r_rdf).max()),
+                                         "certified_feasible_fraction": float(np.mean(c(r_rdf.state) == 1))}}
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
@@ -249,6 +267,7 @@ def loop_bench(args):
         "certified_feasible_fraction": {"score_argmax": float(np.mean(st_fs == 1)),
                                         "uniform_random": float(np.mean(st_rd == 1))},
         "max_regret": {"score_argmax": float(reg_fs.max()), "uniform_random": float(reg_rd.max())},
+        "refit": refit_line,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
@@ -488,6 +507,9 @@ def main():
     ap.add_argument("--loop", action="store_true",
                     help="run the profiling loop (Algorithm 1) instead: GPU-seconds to certificate of the "
                          "score's argmax against uniform random reveal orders, and the loop's wall time")
+    ap.add_argument("--refit", action="store_true",
+                    help="with --loop: also run the score policy with Algorithm 1's fit step (interval refit) "
+                         "every round, on the same trajectories")
     ap.add_argument("--loop-workload", default="paper-shaped-2class-G16",
                     help="workload of --loop (default paper-shaped-2class-G16: 200 reveal orders)")
     ap.add_argument("--policy", action="store_true",

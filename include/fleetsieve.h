@@ -142,7 +142,13 @@ typedef enum fs_option {
    * FS_OBJECTIVE_LEXICOGRAPHIC (the whole objective and the stage-wise gap,
    * as fs_certify_lex; FS_ERR_UNSUPPORTED where that does not fit).  The
    * score stays the max-min stage's either way. */
-  FS_OPT_LOOP_OBJECTIVE = 7
+  FS_OPT_LOOP_OBJECTIVE = 7,
+  /* 1: fs_profile_loop starts every round with Algorithm 1's fit step,
+   * fs_refit_intervals of each trajectory's initial intervals with its
+   * revealed cells; the certificate and the score use the refitted
+   * intervals and the samples clamped into them.  Needs the workspace of
+   * fs_loop_refit_workspace_size.  0 (default): no refit. */
+  FS_OPT_LOOP_REFIT = 8
 } fs_option;
 
 typedef enum fs_objective { FS_OBJECTIVE_MAXMIN = 0, FS_OBJECTIVE_LEXICOGRAPHIC = 1 } fs_objective;
@@ -286,6 +292,25 @@ fs_status fs_reduce_samples(fs_context *ctx, const fs_problem *p, const fs_slo_p
                             int32_t n_cand, const float *d_tail_s, const float *d_succ_s, int32_t n_orders,
                             int32_t n_samples, float *d_out, hipStream_t stream);
 
+/* Interval refit, Algorithm 1's fit step (Section 4.1: the intervals combine
+ * an interior-knee structural prior with the measured cells).  The prior, as
+ * read here: for every class and load level the capacity per GPU (c / t) is
+ * unimodal over the TP degrees in ascending order, and for every class and
+ * TP degree the tail does not fall as the load level rises.  For every
+ * unmeasured cell (measured = point intervals, never written):
+ *   cap_lo' = max(cap_lo, t * min(best measured c / t below t, best measured
+ *             c / t above t)), binary64 rounded down to binary32, when
+ *             measured TP degrees exist on both sides at the same class and
+ *             level;
+ *   tail_lo' = max(tail_lo, measured tails at lower levels, same class and TP),
+ *   tail_hi' = min(tail_hi, measured tails at higher levels);
+ * a bound that would empty the interval is dropped (the prior does not hold
+ * there) and that quantity keeps its interval.  cap_hi and measured are
+ * unchanged.  Outputs [n_orders][N] device arrays; each may alias its input
+ * (cap_lo_out = iv.cap_lo etc. refits in place). */
+fs_status fs_refit_intervals(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders,
+                             float *d_cap_lo_out, float *d_tail_lo_out, float *d_tail_hi_out, hipStream_t stream);
+
 /* Reveal rule of fs_profile_loop. */
 typedef enum fs_policy {
   FS_POLICY_SCORE = 0,  /* the candidate with the largest score (Section 4.3, Algorithm 1) */
@@ -315,6 +340,11 @@ typedef struct fs_loop_out {
 } fs_loop_out;
 
 /* Workspace bytes for fs_profile_loop with these sizes. */
+/* Workspace of fs_profile_loop with FS_OPT_LOOP_REFIT = 1 (the loop's plus
+ * the refitted intervals and two clamped copies of the samples). */
+fs_status fs_loop_refit_workspace_size(const fs_problem *p, int32_t n_orders, int32_t n_cand, int32_t n_samples,
+                                       size_t *bytes);
+
 fs_status fs_loop_workspace_size(const fs_problem *p, int32_t n_orders, int32_t n_cand,
                                  int32_t n_samples, size_t *bytes);
 

@@ -22,6 +22,7 @@ struct fs_context {
   int waves;         // exclusion scorer grid in wavefronts (0 = default)
   int setup;         // exclusion scorer set-up: 0 automatic, 1 general
   int loop_objective;  // profiling loop certificate: 0 max-min, 1 whole objective
+  int loop_refit;      // profiling loop fit step: 0 off, 1 interval refit every round
   int32_t *pinned;   // pinned host word: running trajectories read back by fs_profile_loop
   struct Timed {
     hipEvent_t begin, end;
@@ -153,7 +154,7 @@ fs_status fs_context_create(int hip_device, fs_context **out) {
   e = hipSetDevice(hip_device);
   if (e == hipSuccess) e = hipHostMalloc((void **)&pinned, 64, hipHostMallocDefault);
   if (e != hipSuccess) return hip_fail(e, "hipHostMalloc");
-  *out = new fs_context{hip_device, 0, 0, 0, 0, 0, 0, pinned, {}};
+  *out = new fs_context{hip_device, 0, 0, 0, 0, 0, 0, 0, pinned, {}};
   return FS_OK;
 }
 
@@ -206,6 +207,11 @@ fs_status fs_context_set_option(fs_context *ctx, fs_option option, int64_t value
     if (value < 0 || value > (1 << 20))
       return fail(FS_ERR_INVALID_ARGUMENT, "scorer wavefronts must be in [0, 2^20]");
     ctx->waves = (int)value;
+    return FS_OK;
+  }
+  if (option == FS_OPT_LOOP_REFIT) {
+    if (value != 0 && value != 1) return fail(FS_ERR_INVALID_ARGUMENT, "loop refit must be 0 or 1");
+    ctx->loop_refit = (int)value;
     return FS_OK;
   }
   if (option == FS_OPT_LOOP_OBJECTIVE) {
@@ -403,6 +409,39 @@ fs_status fs_loop_workspace_size(const fs_problem *p, int32_t n_orders, int32_t 
   return FS_OK;
 }
 
+fs_status fs_loop_refit_workspace_size(const fs_problem *p, int32_t n_orders, int32_t n_cand, int32_t n_samples,
+                                       size_t *bytes) {
+  if (!bytes) return fail(FS_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  if (n_orders < 0 || n_cand < 0 || n_samples < 0) return fail(FS_ERR_INVALID_ARGUMENT, "sizes must be >= 0");
+  fs::DevProblem P;
+  fs_status st = make_problem(p, &P);
+  if (st != FS_OK) return st;
+  const int32_t S = n_cand > 0 ? n_samples : 0;
+  const size_t base = fs::loop_layout(P, n_orders, n_cand, S).total;
+  *bytes = fs::refit_layout(P, n_orders, n_cand, S, base).total;
+  return FS_OK;
+}
+
+fs_status fs_refit_intervals(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders,
+                             float *d_cap_lo_out, float *d_tail_lo_out, float *d_tail_hi_out, hipStream_t stream) {
+  if (!ctx) return fail(FS_ERR_INVALID_ARGUMENT, "context is NULL");
+  fs::DevProblem P;
+  fs_status st = make_problem(p, &P);
+  if (st != FS_OK) return st;
+  if (n_orders < 0 || n_orders > 0x7fffffff) return fail(FS_ERR_INVALID_ARGUMENT, "n_orders must be >= 0");
+  if (n_orders > 0 && (!iv.cap_lo || !iv.cap_hi || !iv.tail_lo || !iv.tail_hi || !iv.measured))
+    return fail(FS_ERR_INVALID_ARGUMENT, "interval arrays are NULL");
+  if (n_orders > 0 && (!d_cap_lo_out || !d_tail_lo_out || !d_tail_hi_out))
+    return fail(FS_ERR_INVALID_ARGUMENT, "output arrays are NULL");
+  if (n_orders == 0) return FS_OK;
+  DeviceGuard dg(ctx->device);
+  if (dg.err != hipSuccess) return hip_fail(dg.err, "hipSetDevice");
+  const hipError_t e = fs::launch_refit(P, iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi, iv.measured, n_orders,
+                                        d_cap_lo_out, d_tail_lo_out, d_tail_hi_out, stream);
+  if (e != hipSuccess) return hip_fail(e, "refit launch");
+  return FS_OK;
+}
+
 fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders,
                           const float *d_truth_cap, const float *d_truth_tail, const int32_t *d_cand,
                           int32_t n_cand, const float *d_cap_s, const float *d_tail_s, int32_t n_samples,
@@ -447,9 +486,13 @@ fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv,
   }
   const int32_t S = (n_cand > 0 && policy == FS_POLICY_SCORE) ? n_samples : 0;
   const fs::LoopLayout LL = fs::loop_layout(P, n_orders, n_cand, S);
+  const bool refit = ctx->loop_refit != 0;
+  const fs::RefitLayout RL = fs::refit_layout(P, n_orders, n_cand, S, LL.total);
+  const size_t need = refit ? RL.total : LL.total;
   if (!d_workspace) return fail(FS_ERR_INVALID_ARGUMENT, "workspace is NULL");
-  if (workspace_bytes < LL.total)
-    return fail(FS_ERR_WORKSPACE_TOO_SMALL, "workspace needs " + std::to_string(LL.total) + " bytes");
+  if (workspace_bytes < need)
+    return fail(FS_ERR_WORKSPACE_TOO_SMALL, "workspace needs " + std::to_string(need) + " bytes" +
+                                                (refit ? " (fs_loop_refit_workspace_size)" : ""));
   if (n_orders == 0) return FS_OK;
   DeviceGuard dg(ctx->device);
   if (dg.err != hipSuccess) return hip_fail(dg.err, "hipSetDevice");
@@ -472,10 +515,23 @@ fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv,
   if (e == hipSuccess) e = fs::launch_loop_init(D, n_orders, stream);
   if (e != hipSuccess) return hip_fail(e, "loop set-up launch");
   const fs::AllocOut none{nullptr, nullptr, nullptr, nullptr, nullptr};
+  // With the fit step, the trajectories' own intervals (D.*) keep the initial
+  // ones with the revealed cells collapsed; every round the certificate and
+  // the score see their refit (R_*) and the samples clamped into it.
+  float *R_cap_lo = refit ? (float *)(ws + RL.cap_lo) : D.cap_lo;
+  float *R_tail_lo = refit ? (float *)(ws + RL.tail_lo) : D.tail_lo;
+  float *R_tail_hi = refit ? (float *)(ws + RL.tail_hi) : D.tail_hi;
+  float *R_cap_s = refit ? (float *)(ws + RL.cap_s) : nullptr;
+  float *R_tail_s = refit ? (float *)(ws + RL.tail_s) : nullptr;
   for (int32_t rnd = 0; rnd <= max_rounds; ++rnd) {
-    e = lex ? fs::launch_certify_lex(P, D.cap_lo, D.cap_hi, D.tail_lo, D.tail_hi, D.measured, n_orders, eps,
+    if (refit) {
+      e = fs::launch_refit(P, D.cap_lo, D.cap_hi, D.tail_lo, D.tail_hi, D.measured, n_orders, R_cap_lo, R_tail_lo,
+                           R_tail_hi, stream);
+      if (e != hipSuccess) return hip_fail(e, "loop refit launch");
+    }
+    e = lex ? fs::launch_certify_lex(P, R_cap_lo, D.cap_hi, R_tail_lo, R_tail_hi, D.measured, n_orders, eps,
                                      D.cert_state, D.cons, none, nullptr, nullptr, ws, LL.score, stream)
-            : fs::launch_certify(P, D.cap_lo, D.cap_hi, D.tail_lo, D.tail_hi, D.measured, n_orders, eps,
+            : fs::launch_certify(P, R_cap_lo, D.cap_hi, R_tail_lo, R_tail_hi, D.measured, n_orders, eps,
                                  D.cert_state, D.cons, none, nullptr, ws, LL.score, stream);
     if (e == hipSuccess) e = fs::launch_loop_decide(P, D, d_cand, n_cand, n_orders, stream);
     if (e != hipSuccess) return hip_fail(e, "loop certificate launch");
@@ -489,7 +545,15 @@ fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv,
       if (*ctx->pinned == 0) break;
     }
     if (policy == FS_POLICY_SCORE && n_cand > 0) {
-      fs::ScoreArgs a{D.cap_lo, D.cap_hi, D.tail_lo, D.tail_hi, D.measured, d_cand, d_cap_s, d_tail_s,
+      const float *cs = d_cap_s, *ts = d_tail_s;
+      if (refit) {
+        e = fs::launch_clamp_samples(P, d_cand, n_cand, R_cap_lo, D.cap_hi, R_tail_lo, R_tail_hi, d_cap_s,
+                                     d_tail_s, n_orders, S, R_cap_s, R_tail_s, stream);
+        if (e != hipSuccess) return hip_fail(e, "loop sample clamp launch");
+        cs = R_cap_s;
+        ts = R_tail_s;
+      }
+      fs::ScoreArgs a{R_cap_lo, D.cap_hi, R_tail_lo, R_tail_hi, D.measured, d_cand, cs, ts,
                       n_orders, n_cand, S, D.score, D.gap_now, D.best, nullptr, ws, LL.score, kernel,
                       ctx->spl, ctx->waves, ctx->setup, nullptr, nullptr, 1};
       e = fs::launch_score(P, a, stream);

@@ -166,6 +166,22 @@ struct LoopLayout {
 };
 
 LoopLayout loop_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S);
+
+// Interval refit and sample clamping (Algorithm 1's fit step).  The refit
+// outputs may alias its inputs.
+hipError_t launch_refit(const DevProblem &P, const float *cap_lo, const float *cap_hi, const float *tail_lo,
+                        const float *tail_hi, const uint8_t *measured, int32_t O, float *cap_lo_out,
+                        float *tail_lo_out, float *tail_hi_out, hipStream_t s);
+hipError_t launch_clamp_samples(const DevProblem &P, const int32_t *cand, int32_t E, const float *cap_lo,
+                                const float *cap_hi, const float *tail_lo, const float *tail_hi, const float *cap_s,
+                                const float *tail_s, int32_t O, int32_t S, float *cs_out, float *ts_out,
+                                hipStream_t s);
+// Extra workspace of a loop with the fit step, after LoopLayout::total:
+// refitted cap_lo, tail_lo, tail_hi [O][N] and clamped samples [O][E][S] x 2.
+struct RefitLayout {
+  size_t cap_lo, tail_lo, tail_hi, cap_s, tail_s, total;
+};
+RefitLayout refit_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S, size_t start);
 LoopDev loop_dev(const LoopLayout &L, uint8_t *ws, int64_t O);
 
 hipError_t launch_loop_init(const LoopDev &L, int32_t O, hipStream_t s);

@@ -242,6 +242,23 @@ __global__ void k_setup_cand(DevProblem P, const int32_t *__restrict__ cand, int
   info[e] = ci;
 }
 
+// Z[g] = max_{a <= g} min(X[g - a], Y[a]) for nondecreasing X and Y.  The
+// inner minimum follows Y while Y[a] < X[g - a] and X afterwards, so it rises
+// and then falls in a; with a* the first a where Y[a] >= X[g - a] (a
+// monotone predicate, found by bisection) the maximum is
+// max(Y[a* - 1], X[g - a*]).  `top` is a power of two with 2 * top > g + 1.
+__device__ __forceinline__ int conv_mono(const int *X, const int *Y, int g, int top) {
+  int pos = 0;
+  for (int step = top; step > 0; step >>= 1) {
+    const int a = min(pos + step - 1, g);
+    const bool below = Y[a] < X[g - a];
+    pos += (pos + step - 1 <= g && below) ? step : 0;
+  }
+  const int left = Y[max(pos - 1, 0)];
+  const int right = X[g - min(pos, g)];
+  return max(pos >= 1 ? left : INT_MIN, pos <= g ? right : INT_MIN);
+}
+
 // ---------------------------------------------------------------------------
 // Wave-per-scenario solver.
 // ---------------------------------------------------------------------------
@@ -298,6 +315,8 @@ __device__ int wave_solve(const DevProblem &P, const int8_t *__restrict__ bmap,
   *floors_met_out = floors_met;
 
   int *D = lds, *T = lds + (G + 1), *Dn = lds + 2 * (G + 1);
+  int top = 1;
+  while (2 * top <= G + 1) top <<= 1;  // 2 top > G + 1 >= g + 1: the crossing search covers [0, g]
   int tau = 0;
   for (int k = 0; k < K; ++k) {
     const bool restricted = P.has_floor && floors_met && (P.floor_rps[k] > 0.0f);
@@ -329,17 +348,13 @@ __device__ int wave_solve(const DevProblem &P, const int8_t *__restrict__ bmap,
     if (k == 0) {
       int *tmp = D; D = T; T = tmp;
     } else if (k + 1 < K) {
-      for (int g = lane; g <= G; g += kWave) {
-        int best = INT_MIN;
-        for (int a = 0; a <= g; ++a) best = max(best, min(D[g - a], T[a]));
-        Dn[g] = best;
-      }
+      // both tables are nondecreasing in the budget (prefix maxima, and
+      // (max,min) convolutions of such), so every target is a crossing search
+      for (int g = lane; g <= G; g += kWave) Dn[g] = conv_mono(D, T, g, top);
       __syncthreads();
       int *tmp = D; D = Dn; Dn = tmp;
     } else {
-      int best = INT_MIN;
-      for (int a = lane; a <= G; a += kWave) best = max(best, min(D[G - a], T[a]));
-      tau = wave_max(best);
+      tau = conv_mono(D, T, G, top);
     }
     __syncthreads();
   }
@@ -401,12 +416,55 @@ __device__ __forceinline__ void write_alloc(const AllocOut &out, int64_t j, int 
 }
 
 // ---------------------------------------------------------------------------
+// LDS staging of a wave solve's inputs.  The solver looks up the bucket map
+// and the realisation's cells inside its loops; from global memory every
+// lookup is a dependent round trip.  When they fit, the kernels copy the
+// bucket map (K (G + 1) bytes) and the realisation's cells (2 N floats)
+// into LDS once, with the whole wavefront, and the solver reads them there.
+// ---------------------------------------------------------------------------
+constexpr size_t kStageLimit = 48 * 1024;  // LDS a staged solve block may use
+
+__device__ __host__ inline size_t stage_bytes(const DevProblem &P) {  // 16: aligning the start
+  return 16 + (((size_t)P.K * (P.G + 1) + 3) & ~(size_t)3) + 2 * sizeof(float) * (size_t)P.N;
+}
+
+// Whether a solve block stages its inputs: its LDS with the staging area
+// stays within kStageLimit.
+inline bool stage_fits(size_t lds) { return lds <= kStageLimit; }
+
+struct StageArea {
+  int8_t *bmap;
+  float *cap, *tail;
+};
+
+__device__ __forceinline__ StageArea stage_area(const DevProblem &P, void *start) {
+  StageArea A;
+  A.bmap = reinterpret_cast<int8_t *>(((uintptr_t)start + 15) & ~(uintptr_t)15);
+  A.cap = reinterpret_cast<float *>(A.bmap + (((size_t)P.K * (P.G + 1) + 3) & ~(size_t)3));
+  A.tail = A.cap + P.N;
+  return A;
+}
+
+__device__ __forceinline__ void stage_copy_bmap(const DevProblem &P, const int8_t *__restrict__ g, int8_t *d) {
+  const int n = P.K * (P.G + 1);
+  for (int x = threadIdx.x; x < n; x += blockDim.x) d[x] = g[x];
+}
+
+__device__ __forceinline__ void stage_copy_cells(const DevProblem &P, const float *__restrict__ gc,
+                                                 const float *__restrict__ gt, float *dc, float *dt) {
+  for (int x = threadIdx.x; x < P.N; x += blockDim.x) {
+    dc[x] = gc[x];
+    dt[x] = gt[x];
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Dense batch solve: one wavefront per scenario.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(64) void k_solve_dense(DevProblem P, const int8_t *__restrict__ bmap,
                                                     const float *__restrict__ cap,
                                                     const float *__restrict__ tail, int64_t n,
-                                                    AllocOut out) {
+                                                    AllocOut out, int stage) {
   extern __shared__ int lds[];
   const int64_t j = blockIdx.x;
   if (j >= n) return;
@@ -414,6 +472,15 @@ __global__ __launch_bounds__(64) void k_solve_dense(DevProblem P, const int8_t *
   int *replicas = tp_index + kMaxClasses;
   WaveAlloc wa{tp_index, replicas};
   Realisation R{cap + j * P.N, tail + j * P.N, -1, 0.0f, 0.0f};
+  if (stage) {
+    const StageArea A = stage_area(P, replicas + kMaxClasses);
+    stage_copy_bmap(P, bmap, A.bmap);
+    stage_copy_cells(P, R.cap, R.tail, A.cap, A.tail);
+    bmap = A.bmap;
+    R.cap = A.cap;
+    R.tail = A.tail;
+    __syncthreads();
+  }
   int fm;
   float gp;
   const int tau = wave_solve(P, bmap, R, lds, &fm, &wa, &gp);
@@ -789,23 +856,6 @@ __device__ __forceinline__ void option_of(const DevProblem &P, int p, int *ti, i
   }
   *ti = t;
   *r = p + 1;
-}
-
-// Z[g] = max_{a <= g} min(X[g - a], Y[a]) for nondecreasing X and Y.  The
-// inner minimum follows Y while Y[a] < X[g - a] and X afterwards, so it rises
-// and then falls in a; with a* the first a where Y[a] >= X[g - a] (a
-// monotone predicate, found by bisection) the maximum is
-// max(Y[a* - 1], X[g - a*]).  `top` is a power of two with 2 * top > g + 1.
-__device__ __forceinline__ int conv_mono(const int *X, const int *Y, int g, int top) {
-  int pos = 0;
-  for (int step = top; step > 0; step >>= 1) {
-    const int a = min(pos + step - 1, g);
-    const bool below = Y[a] < X[g - a];
-    pos += (pos + step - 1 <= g && below) ? step : 0;
-  }
-  const int left = Y[max(pos - 1, 0)];
-  const int right = X[g - min(pos, g)];
-  return max(pos >= 1 ? left : INT_MIN, pos <= g ? right : INT_MIN);
 }
 
 // Smallest binary32 capacity x >= 0 at which r replicas reach ratio bits M,
@@ -2121,7 +2171,7 @@ __global__ __launch_bounds__(64) void k_certify(DevProblem P, const int8_t *__re
                                                 const float *__restrict__ tail_hi,
                                                 const uint8_t *__restrict__ measured, float eps,
                                                 int32_t *__restrict__ state, AllocOut cons,
-                                                AllocOut opt, double *__restrict__ gap_out) {
+                                                AllocOut opt, double *__restrict__ gap_out, int stage) {
   extern __shared__ int lds[];
   const int o = blockIdx.x, lane = threadIdx.x;
   const size_t off = (size_t)o * P.N;
@@ -2130,12 +2180,26 @@ __global__ __launch_bounds__(64) void k_certify(DevProblem P, const int8_t *__re
   int *tp_index = tm_rep + kMaxClasses;
   int *tp_rep = tp_index + kMaxClasses;
   WaveAlloc am{tm_index, tm_rep}, ap{tp_index, tp_rep};
+  const StageArea A = stage_area(P, tp_rep + kMaxClasses);
+  const int8_t *bm = bmap;
   int fm_m, fm_p;
   float gp_m, gp_p;
   Realisation rm{cap_lo + off, tail_hi + off, -1, 0.0f, 0.0f};
-  const int tau_m = wave_solve(P, bmap, rm, lds, &fm_m, &am, &gp_m);
+  if (stage) {
+    stage_copy_bmap(P, bmap, A.bmap);
+    stage_copy_cells(P, rm.cap, rm.tail, A.cap, A.tail);
+    bm = A.bmap;
+    rm = Realisation{A.cap, A.tail, -1, 0.0f, 0.0f};
+    __syncthreads();
+  }
+  const int tau_m = wave_solve(P, bm, rm, lds, &fm_m, &am, &gp_m);
   Realisation rp{cap_hi + off, tail_lo + off, -1, 0.0f, 0.0f};
-  const int tau_p = wave_solve(P, bmap, rp, lds, &fm_p, &ap, &gp_p);
+  if (stage) {
+    stage_copy_cells(P, rp.cap, rp.tail, A.cap, A.tail);
+    rp = Realisation{A.cap, A.tail, -1, 0.0f, 0.0f};
+    __syncthreads();
+  }
+  const int tau_p = wave_solve(P, bm, rp, lds, &fm_p, &ap, &gp_p);
   write_alloc(cons, o, P.K, tau_m, fm_m, gp_m, am);
   write_alloc(opt, o, P.K, tau_p, fm_p, gp_p, ap);
   if (lane != 0) return;
@@ -2302,7 +2366,8 @@ __device__ __forceinline__ LexLds lex_lds(const DevProblem &P, void *start) {
 __global__ __launch_bounds__(64) void k_solve_dense_lex(DevProblem P, const int8_t *__restrict__ bmap,
                                                         const float *__restrict__ cap,
                                                         const float *__restrict__ tail, int64_t n,
-                                                        AllocOut out, double *__restrict__ gp64_out) {
+                                                        AllocOut out, double *__restrict__ gp64_out,
+                                                        int stage) {
   extern __shared__ int lds[];
   const int64_t j = blockIdx.x;
   if (j >= n) return;
@@ -2312,6 +2377,15 @@ __global__ __launch_bounds__(64) void k_solve_dense_lex(DevProblem P, const int8
   WaveAlloc wa{tp_index, replicas};
   const LexLds X = lex_lds(P, work);
   Realisation R{cap + j * P.N, tail + j * P.N, -1, 0.0f, 0.0f};
+  if (stage) {
+    const StageArea A = stage_area(P, reinterpret_cast<char *>(work) + lex_work_bytes(P.K, P.G, P.optoff[P.NT]));
+    stage_copy_bmap(P, bmap, A.bmap);
+    stage_copy_cells(P, R.cap, R.tail, A.cap, A.tail);
+    bmap = A.bmap;
+    R.cap = A.cap;
+    R.tail = A.tail;
+    __syncthreads();
+  }
   int fm;
   float gp;
   double gp64;
@@ -2332,7 +2406,7 @@ __global__ __launch_bounds__(64) void k_certify_lex(DevProblem P, const int8_t *
                                                     const uint8_t *__restrict__ measured, float eps,
                                                     int32_t *__restrict__ state, AllocOut cons, AllocOut opt,
                                                     double *__restrict__ gap_mm_out,
-                                                    double *__restrict__ gap_gp_out) {
+                                                    double *__restrict__ gap_gp_out, int stage) {
   extern __shared__ int lds[];
   const int o = blockIdx.x, lane = threadIdx.x;
   const size_t off = (size_t)o * P.N;
@@ -2343,15 +2417,29 @@ __global__ __launch_bounds__(64) void k_certify_lex(DevProblem P, const int8_t *
   int *work = tp_rep + kMaxClasses;
   WaveAlloc am{tm_index, tm_rep}, ap{tp_index, tp_rep};
   const LexLds X = lex_lds(P, work);
+  const StageArea A = stage_area(P, reinterpret_cast<char *>(work) + lex_work_bytes(P.K, P.G, P.optoff[P.NT]));
+  const int8_t *bm = bmap;
   int fm_m, fm_p;
   float gp_m, gp_p;
   double g64_m, g64_p;
   Realisation rm{cap_lo + off, tail_hi + off, -1, 0.0f, 0.0f};
-  const int tau_m = wave_solve(P, bmap, rm, work, &fm_m, nullptr, nullptr);
-  wave_lex_stage(P, bmap, rm, tau_m, fm_m, X, am, &gp_m, &g64_m);
+  if (stage) {
+    stage_copy_bmap(P, bmap, A.bmap);
+    stage_copy_cells(P, rm.cap, rm.tail, A.cap, A.tail);
+    bm = A.bmap;
+    rm = Realisation{A.cap, A.tail, -1, 0.0f, 0.0f};
+    __syncthreads();
+  }
+  const int tau_m = wave_solve(P, bm, rm, work, &fm_m, nullptr, nullptr);
+  wave_lex_stage(P, bm, rm, tau_m, fm_m, X, am, &gp_m, &g64_m);
   Realisation rp{cap_hi + off, tail_lo + off, -1, 0.0f, 0.0f};
-  const int tau_p = wave_solve(P, bmap, rp, work, &fm_p, nullptr, nullptr);
-  wave_lex_stage(P, bmap, rp, tau_p, fm_p, X, ap, &gp_p, &g64_p);
+  if (stage) {
+    stage_copy_cells(P, rp.cap, rp.tail, A.cap, A.tail);
+    rp = Realisation{A.cap, A.tail, -1, 0.0f, 0.0f};
+    __syncthreads();
+  }
+  const int tau_p = wave_solve(P, bm, rp, work, &fm_p, nullptr, nullptr);
+  wave_lex_stage(P, bm, rp, tau_p, fm_p, X, ap, &gp_p, &g64_p);
   write_alloc(cons, o, P.K, tau_m, fm_m, gp_m, am);
   write_alloc(opt, o, P.K, tau_p, fm_p, gp_p, ap);
   if (lane != 0) return;
@@ -2362,6 +2450,96 @@ __global__ __launch_bounds__(64) void k_certify_lex(DevProblem P, const int8_t *
   if (gap_gp_out) gap_gp_out[o] = gap_gp;
   state[o] = certificate_state(P, bmap, measured, tail_hi, off, fm_m, fm_p, tm_index, tm_rep,
                                gap_mm <= (double)eps && gap_gp <= (double)eps);
+}
+
+// ---------------------------------------------------------------------------
+// Interval refit (Algorithm 1's fit step) under a structural prior: per
+// class and load level, capacity per GPU is unimodal over the TP degrees in
+// ascending order; per class and TP degree, the tail does not fall as the
+// load level rises.  From the measured cells of the same row or column, an
+// unmeasured cell gets
+//   cap_lo >= t * min(max_{a < t measured} c_a / t_a, max_{z > t measured} c_z / t_z)
+// (binary64, rounded down to binary32), and tail bounds from the nearest
+// measured loads below and above; a bound that would empty the interval is
+// dropped (the prior does not hold there).  One block per order, a thread
+// per cell; measured cells are copied, or left alone when an output aliases
+// its input (the refit reads only measured cells of other threads).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float round_down_f32(double x) {
+  float v = (float)x;
+  if ((double)v > x) v = nextafterf(v, -__builtin_inff());
+  return v;
+}
+
+__global__ __launch_bounds__(256) void k_refit(DevProblem P, const float *__restrict__ cap_lo,
+                                               const float *__restrict__ cap_hi, const float *__restrict__ tail_lo,
+                                               const float *__restrict__ tail_hi,
+                                               const uint8_t *__restrict__ measured, float *cap_lo_out,
+                                               float *tail_lo_out, float *tail_hi_out) {
+  const size_t off = (size_t)blockIdx.x * P.N;
+  const int NT = P.NT, B = P.B;
+  for (int c = threadIdx.x; c < P.N; c += blockDim.x) {
+    if (measured[off + c]) {  // unchanged: copied unless refitting in place
+      if (cap_lo_out != cap_lo) cap_lo_out[off + c] = cap_lo[off + c];
+      if (tail_lo_out != tail_lo) tail_lo_out[off + c] = tail_lo[off + c];
+      if (tail_hi_out != tail_hi) tail_hi_out[off + c] = tail_hi[off + c];
+      continue;
+    }
+    const int b = c % B, t = (c / B) % NT, row = c - b - t * B;  // row: the class's first cell
+    // capacity: best measured per-GPU value on each side of t at level b
+    double left = -1.0, right = -1.0;
+    for (int a = 0; a < NT; ++a) {
+      const int ca = row + a * B + b;
+      if (a == t || !measured[off + ca]) continue;
+      const double q = (double)cap_lo[off + ca] / (double)P.tp[a];
+      if (a < t) left = fmax(left, q);
+      else right = fmax(right, q);
+    }
+    float lo = cap_lo[off + c];
+    if (left >= 0.0 && right >= 0.0) lo = fmaxf(lo, round_down_f32((double)P.tp[t] * fmin(left, right)));
+    if (lo <= cap_hi[off + c]) cap_lo_out[off + c] = lo;
+    else if (cap_lo_out != cap_lo) cap_lo_out[off + c] = cap_lo[off + c];
+    // tail: measured loads below bound it from below, above from above
+    float tl = tail_lo[off + c], th = tail_hi[off + c];
+    for (int b2 = 0; b2 < B; ++b2) {
+      const int c2 = row + t * B + b2;
+      if (b2 == b || !measured[off + c2]) continue;
+      const float v = tail_lo[off + c2];
+      if (b2 < b) tl = fmaxf(tl, v);
+      else th = fminf(th, v);
+    }
+    if (tl <= th) {
+      tail_lo_out[off + c] = tl;
+      tail_hi_out[off + c] = th;
+    } else {
+      if (tail_lo_out != tail_lo) tail_lo_out[off + c] = tail_lo[off + c];
+      if (tail_hi_out != tail_hi) tail_hi_out[off + c] = tail_hi[off + c];
+    }
+  }
+}
+
+// Samples of every (order, candidate) moved into the candidate's current
+// intervals: min(max(x, lo), hi).  Block (run of 1024, tile).
+__global__ __launch_bounds__(256) void k_clamp_samples(int32_t N, const int32_t *__restrict__ cand, int32_t E,
+                                                       const float *__restrict__ cap_lo,
+                                                       const float *__restrict__ cap_hi,
+                                                       const float *__restrict__ tail_lo,
+                                                       const float *__restrict__ tail_hi,
+                                                       const float *__restrict__ cap_s,
+                                                       const float *__restrict__ tail_s, int32_t S, uint32_t tiles,
+                                                       float *__restrict__ cs_out, float *__restrict__ ts_out) {
+  for (uint32_t tile = blockIdx.y; tile < tiles; tile += gridDim.y) {
+    const uint32_t o = tile / (uint32_t)E, e = tile % (uint32_t)E;
+    const int cell = cand[e];
+    if (cell < 0 || cell >= N) continue;  // never scored
+    const size_t ci = (size_t)o * N + cell;
+    const float cl = cap_lo[ci], ch = cap_hi[ci], tl = tail_lo[ci], th = tail_hi[ci];
+    const size_t base = (size_t)tile * S;
+    for (int s = (int)blockIdx.x * 1024 + (int)threadIdx.x; s < S && s < ((int)blockIdx.x + 1) * 1024; s += 256) {
+      cs_out[base + s] = fminf(fmaxf(cap_s[base + s], cl), ch);
+      ts_out[base + s] = fminf(fmaxf(tail_s[base + s], tl), th);
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -2847,8 +3025,10 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
 hipError_t launch_solve_batch(const DevProblem &P, const float *cap, const float *tail, int64_t n,
                               AllocOut out, uint8_t *ws, const WsLayout &L, hipStream_t s) {
   if (n == 0) return hipSuccess;
-  k_solve_dense<<<(unsigned)n, 64, lds_bytes_solver(P, 1), s>>>(P, (const int8_t *)(ws + L.bmap),
-                                                                cap, tail, n, out);
+  const size_t base = lds_bytes_solver(P, 1), staged = base + stage_bytes(P);
+  const int stage = stage_fits(staged) ? 1 : 0;
+  k_solve_dense<<<(unsigned)n, 64, stage ? staged : base, s>>>(P, (const int8_t *)(ws + L.bmap), cap, tail, n,
+                                                               out, stage);
   return hipGetLastError();
 }
 
@@ -2859,8 +3039,10 @@ size_t lds_bytes_lex(const DevProblem &P, int n_alloc) {
 hipError_t launch_solve_batch_lex(const DevProblem &P, const float *cap, const float *tail, int64_t n,
                                   AllocOut out, double *gp64, uint8_t *ws, const WsLayout &L, hipStream_t s) {
   if (n == 0) return hipSuccess;
-  k_solve_dense_lex<<<(unsigned)n, 64, lds_bytes_lex(P, 1), s>>>(P, (const int8_t *)(ws + L.bmap), cap, tail, n,
-                                                                 out, gp64);
+  const size_t base = lds_bytes_lex(P, 1), staged = base + stage_bytes(P);
+  const int stage = stage_fits(staged) ? 1 : 0;
+  k_solve_dense_lex<<<(unsigned)n, 64, stage ? staged : base, s>>>(P, (const int8_t *)(ws + L.bmap), cap, tail,
+                                                                   n, out, gp64, stage);
   return hipGetLastError();
 }
 
@@ -2869,8 +3051,11 @@ hipError_t launch_certify_lex(const DevProblem &P, const float *cap_lo, const fl
                               AllocOut cons, AllocOut opt, double *gap_mm, double *gap_gp, uint8_t *ws,
                               const WsLayout &L, hipStream_t s) {
   if (O == 0) return hipSuccess;
-  k_certify_lex<<<O, 64, lds_bytes_lex(P, 2), s>>>(P, (const int8_t *)(ws + L.bmap), cap_lo, cap_hi, tail_lo,
-                                                   tail_hi, measured, eps, state, cons, opt, gap_mm, gap_gp);
+  const size_t base = lds_bytes_lex(P, 2), staged = base + stage_bytes(P);
+  const int stage = stage_fits(staged) ? 1 : 0;
+  k_certify_lex<<<O, 64, stage ? staged : base, s>>>(P, (const int8_t *)(ws + L.bmap), cap_lo, cap_hi, tail_lo,
+                                                     tail_hi, measured, eps, state, cons, opt, gap_mm, gap_gp,
+                                                     stage);
   return hipGetLastError();
 }
 
@@ -2879,9 +3064,10 @@ hipError_t launch_certify(const DevProblem &P, const float *cap_lo, const float 
                           int32_t O, float eps, int32_t *state, AllocOut cons, AllocOut opt,
                           double *gap, uint8_t *ws, const WsLayout &L, hipStream_t s) {
   if (O == 0) return hipSuccess;
-  k_certify<<<O, 64, lds_bytes_solver(P, 2), s>>>(P, (const int8_t *)(ws + L.bmap), cap_lo, cap_hi,
-                                                  tail_lo, tail_hi, measured, eps, state, cons, opt,
-                                                  gap);
+  const size_t base = lds_bytes_solver(P, 2), staged = base + stage_bytes(P);
+  const int stage = stage_fits(staged) ? 1 : 0;
+  k_certify<<<O, 64, stage ? staged : base, s>>>(P, (const int8_t *)(ws + L.bmap), cap_lo, cap_hi, tail_lo,
+                                                 tail_hi, measured, eps, state, cons, opt, gap, stage);
   return hipGetLastError();
 }
 
@@ -2920,6 +3106,24 @@ LoopLayout loop_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
   return L;
 }
 
+RefitLayout refit_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S, size_t start) {
+  RefitLayout L{};
+  size_t at = align256(start);
+  auto take = [&](size_t bytes) {
+    const size_t here = at;
+    at = align256(at + (bytes > 0 ? bytes : 1));
+    return here;
+  };
+  const size_t ON = (size_t)O * P.N, OES = (size_t)O * (size_t)E * (size_t)S;
+  L.cap_lo = take(4 * ON);
+  L.tail_lo = take(4 * ON);
+  L.tail_hi = take(4 * ON);
+  L.cap_s = take(4 * OES);
+  L.tail_s = take(4 * OES);
+  L.total = at;
+  return L;
+}
+
 LoopDev loop_dev(const LoopLayout &L, uint8_t *ws, int64_t O) {
   (void)O;
   LoopDev d{};
@@ -2939,6 +3143,26 @@ LoopDev loop_dev(const LoopLayout &L, uint8_t *ws, int64_t O) {
   d.running = ws + L.running;
   d.n_running = (int32_t *)(ws + L.n_running);
   return d;
+}
+
+hipError_t launch_refit(const DevProblem &P, const float *cap_lo, const float *cap_hi, const float *tail_lo,
+                        const float *tail_hi, const uint8_t *measured, int32_t O, float *cap_lo_out,
+                        float *tail_lo_out, float *tail_hi_out, hipStream_t s) {
+  if (O == 0) return hipSuccess;
+  k_refit<<<O, 256, 0, s>>>(P, cap_lo, cap_hi, tail_lo, tail_hi, measured, cap_lo_out, tail_lo_out, tail_hi_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_clamp_samples(const DevProblem &P, const int32_t *cand, int32_t E, const float *cap_lo,
+                                const float *cap_hi, const float *tail_lo, const float *tail_hi, const float *cap_s,
+                                const float *tail_s, int32_t O, int32_t S, float *cs_out, float *ts_out,
+                                hipStream_t s) {
+  const uint32_t tiles = (uint32_t)O * (uint32_t)E;
+  if (tiles == 0 || S == 0) return hipSuccess;
+  const dim3 grid((unsigned)((S + 1023) / 1024), tiles < 65535 ? tiles : 65535u);
+  k_clamp_samples<<<grid, 256, 0, s>>>(P.N, cand, E, cap_lo, cap_hi, tail_lo, tail_hi, cap_s, tail_s, S, tiles,
+                                       cs_out, ts_out);
+  return hipGetLastError();
 }
 
 hipError_t launch_loop_init(const LoopDev &L, int32_t O, hipStream_t s) {

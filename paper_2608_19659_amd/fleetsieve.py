@@ -27,6 +27,7 @@ OPT_SAMPLES_PER_LANE = 3
 OPT_SCORER_WAVES = 5
 OPT_SETUP = 6
 OPT_LOOP_OBJECTIVE = 7
+OPT_LOOP_REFIT = 8
 OBJECTIVE_MAXMIN, OBJECTIVE_LEXICOGRAPHIC = 0, 1
 KERNEL_AUTO, KERNEL_WAVE, KERNEL_LANE, KERNEL_EXCLUSION = 0, 1, 2, 3
 
@@ -34,7 +35,7 @@ EXPORTED = ("fs_context_create", "fs_context_destroy", "fs_context_set_option", 
             "fs_last_error",
             "fs_validate_problem", "fs_workspace_size", "fs_solve_batch", "fs_score_candidates",
             "fs_certify", "fs_loop_workspace_size", "fs_profile_loop", "fs_reduce_cells", "fs_reduce_samples",
-            "fs_solve_batch_lex", "fs_certify_lex")
+            "fs_solve_batch_lex", "fs_certify_lex", "fs_refit_intervals", "fs_loop_refit_workspace_size")
 POLICY_SCORE, POLICY_ORDER = 0, 1
 CELL_SECONDS = 300.0
 
@@ -103,6 +104,8 @@ def load_library():
     lib.fs_loop_workspace_size.argtypes = [P, i32, i32, i32, ctypes.POINTER(sz)]
     lib.fs_profile_loop.argtypes = [vp, P, _Intervals, i32, vp, vp, vp, i32, vp, vp, i32, ctypes.c_float,
                                     ctypes.c_int, vp, i32, i32, _LoopOut, vp, sz, vp]
+    lib.fs_refit_intervals.argtypes = [vp, P, _Intervals, i32, vp, vp, vp, vp]
+    lib.fs_loop_refit_workspace_size.argtypes = [P, i32, i32, i32, ctypes.POINTER(sz)]
     lib.fs_solve_batch_lex.argtypes = [vp, P, vp, vp, i64, _Alloc, vp, vp, sz, vp]
     lib.fs_certify_lex.argtypes = [vp, P, _Intervals, i32, ctypes.c_float, vp, _Alloc, _Alloc, vp, vp, vp, sz, vp]
     Q = ctypes.POINTER(_SloPolicy)
@@ -413,6 +416,29 @@ def certify_lex(ctx: Context, problem, iv: DeviceIntervals, eps: float = 0.05, s
     return CertifyLexOutput(state, gmm, ggp, cons, opt)
 
 
+def refit_intervals(ctx: Context, problem, iv: DeviceIntervals, stream=None) -> DeviceIntervals:
+    """Algorithm 1's fit step (fs_refit_intervals) on [O, N] device
+    intervals; returns new intervals (cap_hi and measured shared with iv)."""
+    torch = _torch()
+    ref = _ProblemRef(problem)
+    O = int(iv.cap_lo.shape[0])
+    ivs = _intervals_struct(iv, O, ref.N)
+    out = DeviceIntervals(torch.empty_like(iv.cap_lo), iv.cap_hi, torch.empty_like(iv.tail_lo),
+                          torch.empty_like(iv.tail_hi), iv.measured)
+    _check(load_library().fs_refit_intervals(ctx.handle, ref.ptr, ivs, O, out.cap_lo.data_ptr(),
+                                             out.tail_lo.data_ptr(), out.tail_hi.data_ptr(),
+                                             _stream(iv.cap_lo.device, stream)))
+    return out
+
+
+def loop_refit_workspace_size(problem, n_orders: int, n_cand: int, n_samples: int) -> int:
+    ref = _ProblemRef(problem)
+    out = ctypes.c_size_t()
+    _check(load_library().fs_loop_refit_workspace_size(ref.ptr, int(n_orders), int(n_cand), int(n_samples),
+                                                       ctypes.byref(out)))
+    return int(out.value)
+
+
 def loop_workspace_size(problem, n_orders: int, n_cand: int, n_samples: int) -> int:
     ref = _ProblemRef(problem)
     out = ctypes.c_size_t()
@@ -435,7 +461,7 @@ class LoopOutput:
 
 def profile_loop(ctx: Context, problem, iv: DeviceIntervals, truth_cap, truth_tail, cand, cap_s, tail_s,
                  eps: float = 0.05, policy: int = POLICY_SCORE, order=None, max_rounds: int | None = None,
-                 check_every: int = 4, stream=None, workspace=None) -> LoopOutput:
+                 check_every: int = 4, stream=None, workspace=None, refit: bool = False) -> LoopOutput:
     """The profiling loop (fs_profile_loop) for O trajectories.  iv holds
     the initial designs [O, N]; truth_cap / truth_tail are float32 [O, N]
     device tensors; order is an int32 [O, E] device tensor (policy
@@ -461,8 +487,9 @@ def profile_loop(ctx: Context, problem, iv: DeviceIntervals, truth_cap, truth_ta
     lo = _LoopOut(out.state.data_ptr(), out.finished.data_ptr(), out.rounds.data_ptr(), out.gpu_seconds.data_ptr(),
                   out.reveals.data_ptr() if R > 0 else None, _alloc_struct(out.final), out.tau_truth.data_ptr(),
                   out.tau_oracle.data_ptr())
-    ws_bytes = loop_workspace_size(problem, O, E, S)
+    ws_bytes = (loop_refit_workspace_size if refit else loop_workspace_size)(problem, O, E, S)
     ws = workspace if workspace is not None else ctx.workspace(ws_bytes)
+    ctx.set_option(OPT_LOOP_REFIT, 1 if refit else 0)
     _check(load_library().fs_profile_loop(ctx.handle, ref.ptr, ivs, O, ptc, ptt, pcand, E, pcs, pts, S,
                                           float(eps), int(policy), pord, R, int(check_every), lo, ws.data_ptr(),
                                           ws.numel(), _stream(dev, stream)))
