@@ -97,6 +97,8 @@ def _load():
             getattr(lib, name).argtypes = [P, fp, fp, A, f64p]
         lib.orc_certify_lex.argtypes = [P, ctypes.c_int32, fp, fp, fp, fp, u8p, ctypes.c_float,
                                         i32p, A, A, f64p, f64p]
+        lib.orc_score_lex.argtypes = [P, ctypes.c_int32, fp, fp, fp, fp, u8p, i32p, ctypes.c_int32,
+                                      fp, fp, ctypes.c_int32, f64p, f64p, f64p, f64p, i32p, u8p, ctypes.c_int]
         lib.orc_pairwise_sum.argtypes = [f64p, ctypes.c_int64]
         lib.orc_pairwise_sum.restype = ctypes.c_double
         _lib = lib
@@ -295,6 +297,48 @@ def certify_lex(problem, intervals, eps: float = 0.05) -> CertifyLexResult:
     k = len(ref.demand)
     return CertifyLexResult(state, gmm, ggp, [_alloc_out(cons[o], k) for o in range(O)],
                             [_alloc_out(opt[o], k) for o in range(O)])
+
+
+@dataclass
+class ScoreLexResult:
+    score_mm: np.ndarray  # [O][E] expected max-min stage reduction
+    score_gp: np.ndarray  # [O][E] expected goodput stage reduction
+    gap_mm: np.ndarray    # [O]
+    gap_gp: np.ndarray    # [O]
+    best: np.ndarray      # [O]
+
+
+def score_lex(problem, intervals, cand, cap_s, tail_s, tile_mask=None, n_threads: int = 1) -> ScoreLexResult:
+    """Acquisition scores with the stage-wise gap under the whole objective
+    (orc_score_lex); tiles outside tile_mask are left 0."""
+    ref = _ProblemRef(problem)
+    N = ref.n_cells
+    cl = np.ascontiguousarray(intervals.cap_lo, dtype=np.float32).reshape(-1, N)
+    O = cl.shape[0]
+    ch = np.ascontiguousarray(intervals.cap_hi, dtype=np.float32).reshape(O, N)
+    tl = np.ascontiguousarray(intervals.tail_lo, dtype=np.float32).reshape(O, N)
+    th = np.ascontiguousarray(intervals.tail_hi, dtype=np.float32).reshape(O, N)
+    ms = np.ascontiguousarray(intervals.measured, dtype=np.uint8).reshape(O, N)
+    cand = np.ascontiguousarray(cand, dtype=np.int32)
+    E = len(cand)
+    cs = np.ascontiguousarray(cap_s, dtype=np.float32).reshape(O, E, -1)
+    ts = np.ascontiguousarray(tail_s, dtype=np.float32).reshape(O, E, -1)
+    S = cs.shape[2]
+    smm = np.zeros((O, E), np.float64)
+    sgp = np.zeros((O, E), np.float64)
+    gmm = np.zeros(O, np.float64)
+    ggp = np.zeros(O, np.float64)
+    best = np.zeros(O, np.int32)
+    mask = None if tile_mask is None else np.ascontiguousarray(tile_mask, dtype=np.uint8).reshape(O, E)
+    rc = _load().orc_score_lex(ctypes.byref(ref.s), O, _ptr(cl, ctypes.c_float), _ptr(ch, ctypes.c_float),
+                               _ptr(tl, ctypes.c_float), _ptr(th, ctypes.c_float), _ptr(ms, ctypes.c_uint8),
+                               _ptr(cand, ctypes.c_int32), E, _ptr(cs, ctypes.c_float), _ptr(ts, ctypes.c_float), S,
+                               _ptr(smm, ctypes.c_double), _ptr(sgp, ctypes.c_double), _ptr(gmm, ctypes.c_double),
+                               _ptr(ggp, ctypes.c_double), _ptr(best, ctypes.c_int32),
+                               None if mask is None else _ptr(mask, ctypes.c_uint8), int(n_threads))
+    if rc != 0:
+        raise ValueError("oracle score failed")
+    return ScoreLexResult(smm, sgp, gmm, ggp, best)
 
 
 def pairwise_sum(x) -> float:

@@ -891,3 +891,95 @@ int orc_certify_lex(const orc_problem *p, int32_t n_orders, const float *cap_lo,
   free(buf);
   return 0;
 }
+
+/* Stage-wise gap of one pair of allocations under the whole objective:
+ * max-min stage tau+ - tau-, goodput stage |gp+ - gp-| / max(gp+, gp-). */
+static void orc_stage_gaps(const orc_alloc *am, const orc_alloc *ap, double gm, double gp, double *mm,
+                           double *gg) {
+  *mm = (double)ap->tau - (double)am->tau;
+  const double top = gp > gm ? gp : gm;
+  *gg = top > 0.0 ? fabs(gp - gm) / top : 0.0;
+}
+
+int orc_score_lex(const orc_problem *p, int32_t n_orders, const float *cap_lo, const float *cap_hi,
+                  const float *tail_lo, const float *tail_hi, const uint8_t *measured, const int32_t *cand,
+                  int32_t n_cand, const float *cap_s, const float *tail_s, int32_t n_samples, double *score_mm,
+                  double *score_gp, double *gap_mm, double *gap_gp, int32_t *best, const uint8_t *tile_mask,
+                  int n_threads) {
+  if (orc_check_problem(p)) return -1;
+  if (n_orders < 0 || n_cand < 0 || n_samples < 1) return -1;
+  const int64_t N = orc_n_cells(p);
+  const int64_t E = n_cand, S = n_samples;
+  for (int e = 0; e < n_cand; ++e)
+    if (cand[e] < 0 || cand[e] >= N) return -1;
+  int err = 0;
+#ifdef _OPENMP
+#pragma omp parallel for schedule(dynamic, 1) num_threads(n_threads > 0 ? n_threads : 1)
+#endif
+  for (int o = 0; o < n_orders; ++o) {
+    float *buf = (float *)malloc(sizeof(float) * (size_t)N * 4);
+    orc_alloc am, ap;
+    double gm = 0.0, gp = 0.0;
+    orc_realisations(N, o, cap_lo, cap_hi, tail_lo, tail_hi, buf, buf + N, buf + 2 * N, buf + 3 * N);
+    if (orc_solve_lex(p, buf, buf + N, &am, &gm) || orc_solve_lex(p, buf + 2 * N, buf + 3 * N, &ap, &gp)) err = -1;
+    orc_stage_gaps(&am, &ap, gm, gp, &gap_mm[o], &gap_gp[o]);
+    free(buf);
+  }
+  const int64_t tiles = (int64_t)n_orders * E;
+#ifdef _OPENMP
+#pragma omp parallel for schedule(dynamic, 1) num_threads(n_threads > 0 ? n_threads : 1)
+#endif
+  for (int64_t tile = 0; tile < tiles; ++tile) {
+    if (tile_mask && !tile_mask[tile]) continue;
+    const int o = (int)(tile / E);
+    const int e = (int)(tile % E);
+    const int cell = cand[e];
+    if (measured[(size_t)o * N + cell]) {
+      score_mm[tile] = 0.0;
+      score_gp[tile] = 0.0;
+      continue;
+    }
+    float *buf = (float *)malloc(sizeof(float) * (size_t)N * 4);
+    double *gmm = (double *)malloc(sizeof(double) * (size_t)S);
+    double *ggp = (double *)malloc(sizeof(double) * (size_t)S);
+    float *cap_m = buf, *tail_m = buf + N, *cap_p = buf + 2 * N, *tail_p = buf + 3 * N;
+    orc_realisations(N, o, cap_lo, cap_hi, tail_lo, tail_hi, cap_m, tail_m, cap_p, tail_p);
+    for (int64_t s = 0; s < S; ++s) {
+      const float cs = cap_s[tile * S + s], ts = tail_s[tile * S + s];
+      cap_m[cell] = cs; tail_m[cell] = ts;
+      cap_p[cell] = cs; tail_p[cell] = ts;
+      orc_alloc am, ap;
+      double gm = 0.0, gp = 0.0;
+      if (orc_solve_lex(p, cap_m, tail_m, &am, &gm) || orc_solve_lex(p, cap_p, tail_p, &ap, &gp)) err = -1;
+      orc_stage_gaps(&am, &ap, gm, gp, &gmm[s], &ggp[s]);
+    }
+    score_mm[tile] = gap_mm[o] - orc_pairwise_sum(gmm, S) / (double)S;
+    score_gp[tile] = gap_gp[o] - orc_pairwise_sum(ggp, S) / (double)S;
+    free(buf);
+    free(gmm);
+    free(ggp);
+  }
+  /* the larger expected max-min reduction, then the larger expected
+   * goodput-stage reduction, then the cheaper cell, the smaller cell, the
+   * earlier candidate */
+  for (int o = 0; o < n_orders; ++o) {
+    int b = -1;
+    for (int e = 0; e < n_cand; ++e) {
+      const int cell = cand[e];
+      if (measured[(size_t)o * N + cell]) continue;
+      if (b < 0) { b = e; continue; }
+      const double me = score_mm[(size_t)o * E + e], mb = score_mm[(size_t)o * E + b];
+      const double ge = score_gp[(size_t)o * E + e], gb = score_gp[(size_t)o * E + b];
+      const int te = p->tp[(cell / p->n_levels) % p->n_tp];
+      const int tb = p->tp[(cand[b] / p->n_levels) % p->n_tp];
+      int better;
+      if (me != mb) better = me > mb;
+      else if (ge != gb) better = ge > gb;
+      else if (te != tb) better = te < tb;
+      else better = cell < cand[b];
+      if (better) b = e;
+    }
+    best[o] = b;
+  }
+  return err;
+}

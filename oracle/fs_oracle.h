@@ -122,6 +122,19 @@ int orc_certify_lex(const orc_problem *p, int32_t n_orders, const float *cap_lo,
                     const float *tail_lo, const float *tail_hi, const uint8_t *measured, float eps,
                     int32_t *state, orc_alloc *cons, orc_alloc *opt, double *gap_mm, double *gap_gp);
 
+/* Acquisition score with the stage-wise gap (Section 4.3 with Section 4.2's
+ * stages) under the whole objective: per (order, candidate) the expected
+ * reduction of each stage, score_mm = gap_mm - mean Gamma_mm(s) and score_gp
+ * = gap_gp - mean Gamma_gp(s) (pairwise sums over the samples), gap_* the
+ * order's current stages; best = the larger score_mm, then the larger
+ * score_gp, then the smaller TP, cell index, candidate.  Measured candidates
+ * score (0, 0) and are never picked. */
+int orc_score_lex(const orc_problem *p, int32_t n_orders, const float *cap_lo, const float *cap_hi,
+                  const float *tail_lo, const float *tail_hi, const uint8_t *measured, const int32_t *cand,
+                  int32_t n_cand, const float *cap_s, const float *tail_s, int32_t n_samples, double *score_mm,
+                  double *score_gp, double *gap_mm, double *gap_gp, int32_t *best, const uint8_t *tile_mask,
+                  int n_threads);
+
 /* Pairwise sum of x[0..n) zero-padded to the next power of two. */
 double orc_pairwise_sum(const double *x, int64_t n);
 

@@ -164,3 +164,51 @@ def test_hand_derived_loop(objective):
     assert list(r.reveals[0][: want["rounds"]]) == want["reveals"] and r.gpu_seconds[0] == want["gpu_seconds"]
     assert r.final[0].tp(p) == want["final_tp"] and r.final[0].replicas == want["final_replicas"]
     assert r.tau_truth[0] == np.float32(want["tau_truth"]) and r.regret[0] == 0.0
+
+
+def _score_inputs(g, c):
+    p, cap, tail = hw1_tables(g, c["budget"])
+    lo, hi = cap.copy(), cap.copy()
+    meas = np.ones(p.n_cells, np.uint8)
+    for k, v in c["cap_lo"].items():
+        lo[int(k)] = v
+        meas[int(k)] = 0
+    for k, v in c["cap_hi"].items():
+        hi[int(k)] = v
+    iv = SimpleNamespace(cap_lo=lo[None], cap_hi=hi[None], tail_lo=tail[None], tail_hi=tail[None],
+                         measured=meas[None])
+    cs = np.array([c["cap_s"]], np.float32)
+    return p, iv, np.array(c["cand"], np.int32), cs, np.full_like(cs, g["tail"])
+
+
+def test_hand_derived_stagewise_score():
+    g = load_golden("lex_objective.json")
+    c = g["score"]
+    p, iv, cand, cs, ts = _score_inputs(g, c)
+    r = oracle.score_lex(p, iv, cand, cs, ts)
+    assert list(r.score_mm[0]) == c["score_mm"]
+    assert list(r.score_gp[0]) == [x / c["score_gp_den"] for x in c["score_gp_num"]]
+    assert r.gap_gp[0] == c["gap_gp_num"] / c["score_gp_den"] and r.best[0] == c["best"]
+    assert oracle.score(p, iv, cand, cs, ts).best[0] == c["maxmin_best"]
+
+
+@pytest.mark.parametrize("name,orders", [("paper-shaped-2class-G16", [0, 3, 5]), ("4class-G64", [1])])
+def test_stagewise_score_keeps_the_maxmin_stage(name, orders):
+    """The max-min stage of the stage-wise score is the plain score, bit for
+    bit (tau* is the same under both objectives), and measured candidates
+    score (0, 0) and are never picked."""
+    from paper_2608_19659_amd.synth import make_workload
+    w = make_workload(name, orders=orders)
+    S = 16
+    cs, ts = np.ascontiguousarray(w.cap_s[:, :, :S]), np.ascontiguousarray(w.tail_s[:, :, :S])
+    mask = np.zeros((len(orders), len(w.cand)), np.uint8)
+    mask[:, ::7] = 1
+    r = oracle.score_lex(w.problem, w.intervals, w.cand, cs, ts, tile_mask=mask, n_threads=8)
+    m = oracle.score(w.problem, w.intervals, w.cand, cs, ts, tile_mask=mask, dump=False, n_threads=8)
+    sel = mask.astype(bool)
+    np.testing.assert_array_equal(r.score_mm[sel], m.score[sel])
+    np.testing.assert_array_equal(r.gap_mm, m.gap_now)
+    meas = w.intervals.measured[:, w.cand].astype(bool)
+    assert (r.score_mm[meas & sel] == 0).all() and (r.score_gp[meas & sel] == 0).all()
+    for o in range(len(orders)):
+        assert r.best[o] < 0 or not meas[o, r.best[o]]
