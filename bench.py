@@ -451,6 +451,18 @@ def lex_bench(args):
 
     r_lex, ms_lex = timed(lambda: fs.solve_batch_lex(ctx, p, cap, tail, stream=stream, workspace=ws))
     _, ms_mm = timed(lambda: fs.solve_batch(ctx, p, cap, tail, stream=stream, workspace=ws))
+    # the stage-wise score (every scenario solved in full) on the workload's first
+    # args.lex_score_samples samples, against the max-min score on the same inputs
+    ws_full = make_workload(name)
+    Sx = min(args.lex_score_samples, ws_full.cap_s.shape[2])
+    O, E = ws_full.cap_s.shape[:2]
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    div = fs.DeviceIntervals.from_host(ws_full.intervals, dev)
+    cand_d, cs_d, ts_d = t(ws_full.cand), t(ws_full.cap_s[:, :, :Sx]), t(ws_full.tail_s[:, :, :Sx])
+    wsl = ctx.workspace(fs.score_lex_workspace_size(p, O, E, Sx))
+    _, ms_sl = timed(lambda: fs.score_candidates_lex(ctx, p, div, cand_d, cs_d, ts_d, stream=stream, workspace=wsl))
+    _, ms_sm = timed(lambda: fs.score_candidates(ctx, p, div, cand_d, cs_d, ts_d, stream=stream))
+    live = int((~ws_full.intervals.measured[:, ws_full.cand].astype(bool)).sum()) * Sx
     slots = lex_work_per_scenario(p)
     achieved = slots * n / (ms_lex / 1e3)
     cpu = None
@@ -477,6 +489,9 @@ def lex_bench(args):
                                f"{n} point realisations drawn inside its intervals",
                    "parallelism": "single GPU"},
         "maxmin_only": {"value": n / (ms_mm / 1e3), "ms_per_step": ms_mm},
+        "stagewise_score": {"samples": Sx, "scenarios_per_call": live, "ms_per_call": ms_sl,
+                            "value": live / (ms_sl / 1e3), "unit": "scenarios/s",
+                            "maxmin_score_ms_per_call": ms_sm},
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_OPS / 1e12, "unit": "TOP/s",
                      "frac": achieved / VALU_PEAK_OPS, "traffic": None, "kernel": "k_solve_dense_lex",
                      "op": "VALU lane-slot", "slots_per_scenario": slots, "scenarios_per_launch": n,
@@ -519,6 +534,8 @@ def main():
                     help="dense solves under the whole lexicographic objective (levels 1-4) on point realisations "
                          "of the workload, against the max-min solve")
     ap.add_argument("--lex-scenarios", type=int, default=65536, help="realisations per --lex step")
+    ap.add_argument("--lex-score-samples", type=int, default=64,
+                    help="samples per candidate for the stage-wise score timed by --lex")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (scales the HBM byte counters)")
     args = ap.parse_args()

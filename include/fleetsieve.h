@@ -137,11 +137,12 @@ typedef enum fs_option {
    * classes and its LDS fits), 1 = the general set-up (one block per order,
    * realisation and class; any problem).  Results are identical. */
   FS_OPT_SETUP = 6,
-  /* Certificate of fs_profile_loop: FS_OBJECTIVE_MAXMIN (default; objective
-   * levels 1-2 and the max-min gap, as fs_certify) or
-   * FS_OBJECTIVE_LEXICOGRAPHIC (the whole objective and the stage-wise gap,
-   * as fs_certify_lex; FS_ERR_UNSUPPORTED where that does not fit).  The
-   * score stays the max-min stage's either way. */
+  /* Objective of fs_profile_loop: FS_OBJECTIVE_MAXMIN (default; objective
+   * levels 1-2, the max-min gap and score, as fs_certify and
+   * fs_score_candidates) or FS_OBJECTIVE_LEXICOGRAPHIC (the whole objective:
+   * the stage-wise certificate of fs_certify_lex and the stage-wise score of
+   * fs_score_candidates_lex, which solves every scenario in full;
+   * FS_ERR_UNSUPPORTED where that does not fit). */
   FS_OPT_LOOP_OBJECTIVE = 7,
   /* 1: fs_profile_loop starts every round with Algorithm 1's fit step,
    * fs_refit_intervals of each trajectory's initial intervals with its
@@ -255,6 +256,30 @@ fs_status fs_solve_batch_lex(fs_context *ctx, const fs_problem *p, const float *
 fs_status fs_certify_lex(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders, float eps,
                          int32_t *d_state, fs_alloc cons, fs_alloc opt, double *d_gap_maxmin,
                          double *d_gap_goodput, void *d_workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Acquisition score with the stage-wise gap under the whole objective
+ * (Section 4.3's score over Section 4.2's stages): per scenario (order o,
+ * candidate e, sample s) both allocations under the whole objective, the
+ * max-min stage Gamma_mm = tau+ - tau- and the goodput stage Gamma_gp =
+ * |gp+ - gp-| / max(gp+, gp-); per (o, e) the expected reduction of each,
+ *   d_score_maxmin[o][e]  = gap_maxmin[o]  - (pairwise sum over s of Gamma_mm) / S,
+ *   d_score_goodput[o][e] = gap_goodput[o] - (pairwise sum over s of Gamma_gp) / S;
+ * d_best[o] = the largest max-min score, then the largest goodput score,
+ * then the smaller TP, cell index, candidate (measured candidates score
+ * (0, 0) and are never picked; -1 when none is left).  d_gap_*[o] (or NULL)
+ * receive the order's current stages.  The max-min score equals
+ * fs_score_candidates' score bit for bit.  Every scenario is a full solve
+ * (two max-min solves and two knapsacks, one wavefront): far slower than
+ * fs_score_candidates.  Workspace: fs_score_lex_workspace_size; sizes as in
+ * fs_score_candidates; FS_ERR_UNSUPPORTED where the whole objective does not
+ * fit (see fs_solve_batch_lex). */
+fs_status fs_score_lex_workspace_size(const fs_problem *p, int32_t n_orders, int32_t n_cand, int32_t n_samples,
+                                      size_t *bytes);
+fs_status fs_score_candidates_lex(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders,
+                                  const int32_t *d_cand, int32_t n_cand, const float *d_cap_s, const float *d_tail_s,
+                                  int32_t n_samples, double *d_score_maxmin, double *d_score_goodput,
+                                  double *d_gap_maxmin, double *d_gap_goodput, int32_t *d_best, void *d_workspace,
+                                  size_t workspace_bytes, hipStream_t stream);
 
 #define FS_MAX_METRICS 8
 

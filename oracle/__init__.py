@@ -398,8 +398,9 @@ def profile_loop(problem, intervals, truth_cap, truth_tail, cand, cap_s, tail_s,
     e.g. a uniform random permutation).  A trajectory with no unmeasured
     candidate left returns A- undecided (the certificate of its final
     intervals is evaluated first, so a last reveal can still certify).  With
-    objective="lex" the certificate is the stage-wise one under the whole
-    objective (certify_lex) and A- is that objective's allocation.  With
+    objective="lex" the certificate and the score are the stage-wise ones
+    under the whole objective (certify_lex, score_lex) and A- is that
+    objective's allocation.  With
     refit=True every round starts with refit_intervals (Algorithm 1's fit
     step) of the trajectory's initial intervals with its revealed cells, the
     certificate and score use the refitted intervals, and the score's
@@ -464,7 +465,10 @@ def profile_loop(problem, intervals, truth_cap, truth_tail, cand, cap_s, tail_s,
             if refit:
                 rows = refit_intervals(problem, rows)
                 cs, ts = clamp_samples(rows, cand, cs, ts)
-            sc = score(problem, rows, cand, cs, ts, dump=False, n_threads=n_threads)
+            if objective == "maxmin":
+                sc = score(problem, rows, cand, cs, ts, dump=False, n_threads=n_threads)
+            else:
+                sc = score_lex(problem, rows, cand, cs, ts, n_threads=n_threads)
             picks = [int(b) for b in sc.best]
         else:
             picks = []

@@ -330,6 +330,55 @@ fs_status fs_solve_batch_lex(fs_context *ctx, const fs_problem *p, const float *
   return FS_OK;
 }
 
+fs_status fs_score_lex_workspace_size(const fs_problem *p, int32_t n_orders, int32_t n_cand, int32_t n_samples,
+                                      size_t *bytes) {
+  if (!bytes) return fail(FS_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  if (n_orders < 0 || n_cand < 0 || n_samples < 0) return fail(FS_ERR_INVALID_ARGUMENT, "sizes must be >= 0");
+  fs::DevProblem P;
+  fs_status st = make_problem(p, &P);
+  if (st != FS_OK) return st;
+  *bytes = fs::lex_score_layout(P, n_orders, n_cand, n_cand > 0 ? n_samples : 0).total;
+  return FS_OK;
+}
+
+fs_status fs_score_candidates_lex(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders,
+                                  const int32_t *d_cand, int32_t n_cand, const float *d_cap_s, const float *d_tail_s,
+                                  int32_t n_samples, double *d_score_maxmin, double *d_score_goodput,
+                                  double *d_gap_maxmin, double *d_gap_goodput, int32_t *d_best, void *d_workspace,
+                                  size_t workspace_bytes, hipStream_t stream) {
+  if (!ctx) return fail(FS_ERR_INVALID_ARGUMENT, "context is NULL");
+  fs::DevProblem P;
+  fs_status st = make_problem(p, &P);
+  if (st != FS_OK) return st;
+  st = lex_supported(P, 2);
+  if (st != FS_OK) return st;
+  if (n_orders < 0 || n_orders > 65535) return fail(FS_ERR_INVALID_ARGUMENT, "n_orders must be in [0, 65535]");
+  if (n_cand < 0 || n_cand > 65535) return fail(FS_ERR_INVALID_ARGUMENT, "n_cand must be in [0, 65535]");
+  if (n_cand > 0 && (n_samples < 1 || n_samples > FS_MAX_SAMPLES))
+    return fail(FS_ERR_INVALID_ARGUMENT, "n_samples must be in [1, 2^20]");
+  if (n_orders > 0 && (!iv.cap_lo || !iv.cap_hi || !iv.tail_lo || !iv.tail_hi || !iv.measured))
+    return fail(FS_ERR_INVALID_ARGUMENT, "interval arrays are NULL");
+  if (n_orders > 0 && n_cand > 0 &&
+      (!d_cand || !d_cap_s || !d_tail_s || !d_score_maxmin || !d_score_goodput))
+    return fail(FS_ERR_INVALID_ARGUMENT, "candidate, sample or score arrays are NULL");
+  const int32_t S = n_cand > 0 ? n_samples : 0;
+  const fs::LexScoreLayout L = fs::lex_score_layout(P, n_orders, n_cand, S);
+  if (!d_workspace) return fail(FS_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  if (workspace_bytes < L.total)
+    return fail(FS_ERR_WORKSPACE_TOO_SMALL, "workspace needs " + std::to_string(L.total) + " bytes");
+  if (n_orders == 0) return FS_OK;
+  DeviceGuard dg(ctx->device);
+  if (dg.err != hipSuccess) return hip_fail(dg.err, "hipSetDevice");
+  uint8_t *ws = (uint8_t *)d_workspace;
+  hipError_t e = fs::launch_setup(P, d_cand, n_cand, ws, L.score, stream);
+  if (e == hipSuccess)
+    e = fs::launch_score_lex(P, iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi, iv.measured, d_cap_s, d_tail_s,
+                             n_orders, n_cand, S, d_score_maxmin, d_score_goodput, d_gap_maxmin, d_gap_goodput,
+                             d_best, ws, L, stream);
+  if (e != hipSuccess) return hip_fail(e, "stage-wise score launch");
+  return FS_OK;
+}
+
 fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders,
                               const int32_t *d_cand, int32_t n_cand, const float *d_cap_s,
                               const float *d_tail_s, int32_t n_samples, double *d_score,
@@ -553,10 +602,21 @@ fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv,
         cs = R_cap_s;
         ts = R_tail_s;
       }
-      fs::ScoreArgs a{R_cap_lo, D.cap_hi, R_tail_lo, R_tail_hi, D.measured, d_cand, cs, ts,
-                      n_orders, n_cand, S, D.score, D.gap_now, D.best, nullptr, ws, LL.score, kernel,
-                      ctx->spl, ctx->waves, ctx->setup, nullptr, nullptr, 1};
-      e = fs::launch_score(P, a, stream);
+      if (lex) {  // the stage-wise score: the max-min stage first, then the goodput stage
+        fs::LexScoreLayout XL{};
+        XL.score = LL.score;
+        XL.part_gp = LL.part_gp;
+        XL.gap_mm = LL.gap_mm;
+        XL.gap_gp = LL.gap_gp;
+        XL.state = LL.lex_state;
+        e = fs::launch_score_lex(P, R_cap_lo, D.cap_hi, R_tail_lo, R_tail_hi, D.measured, cs, ts, n_orders, n_cand, S,
+                                 D.score, (double *)(ws + LL.scores_gp), nullptr, nullptr, D.best, ws, XL, stream);
+      } else {
+        fs::ScoreArgs a{R_cap_lo, D.cap_hi, R_tail_lo, R_tail_hi, D.measured, d_cand, cs, ts,
+                        n_orders, n_cand, S, D.score, D.gap_now, D.best, nullptr, ws, LL.score, kernel,
+                        ctx->spl, ctx->waves, ctx->setup, nullptr, nullptr, 1};
+        e = fs::launch_score(P, a, stream);
+      }
       if (e != hipSuccess) return hip_fail(e, "loop score launch");
     }
     e = fs::launch_loop_reveal(P, D, d_truth_cap, d_truth_tail, d_cand, n_cand, n_orders, (int32_t)policy,

@@ -162,10 +162,23 @@ struct LoopLayout {
   WsLayout score;
   size_t cap_lo, cap_hi, tail_lo, tail_hi, measured, cert_state, cons_obj, cons_tp, cons_rep, cons_fm,
       cons_gp, fin_obj, fin_tp, fin_rep, fin_fm, fin_gp, scores, gap_now, best, running, n_running;
+  size_t scores_gp, part_gp, gap_mm, gap_gp, lex_state;  // the stage-wise score (whole objective)
   size_t total;
 };
 
 LoopLayout loop_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S);
+
+// The stage-wise score under the whole objective: the scorer's layout plus a
+// second array of partials, the order's two stages and a scratch state.
+struct LexScoreLayout {
+  WsLayout score;
+  size_t part_gp, gap_mm, gap_gp, state, total;
+};
+LexScoreLayout lex_score_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S);
+hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const float *cap_hi, const float *tail_lo,
+                            const float *tail_hi, const uint8_t *measured, const float *cap_s, const float *tail_s,
+                            int32_t O, int32_t E, int32_t S, double *score_mm, double *score_gp, double *gap_mm,
+                            double *gap_gp, int32_t *best, uint8_t *ws, const LexScoreLayout &L, hipStream_t s);
 
 // Interval refit and sample clamping (Algorithm 1's fit step).  The refit
 // outputs may alias its inputs.

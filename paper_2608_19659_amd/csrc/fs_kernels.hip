@@ -2453,6 +2453,171 @@ __global__ __launch_bounds__(64) void k_certify_lex(DevProblem P, const int8_t *
 }
 
 // ---------------------------------------------------------------------------
+// The acquisition score with the stage-wise gap under the whole objective:
+// per scenario both allocations by the max-min solver and level (3)'s
+// knapsack, Gamma_mm = tau+ - tau- and Gamma_gp = |gp+ - gp-| / max(gp+,
+// gp-); the expected reduction of each stage per (order, candidate); the
+// argmax by the max-min stage, then the goodput stage, then the cost order.
+// Block (chunk, e, o) takes samples [64 chunk, 64 chunk + 64) one after
+// another with the whole wavefront; lane j keeps sample j's two gaps.
+// ---------------------------------------------------------------------------
+__device__ __host__ inline size_t stage2_bytes(const DevProblem &P) {  // bucket map + two realisations
+  return 16 + (((size_t)P.K * (P.G + 1) + 3) & ~(size_t)3) + 4 * sizeof(float) * (size_t)P.N;
+}
+
+__device__ __forceinline__ void stage_gaps(int tau_m, int tau_p, double gm, double gp, double *mm, double *gg) {
+  *mm = (double)__int_as_float(tau_p) - (double)__int_as_float(tau_m);
+  const double top = gp > gm ? gp : gm;
+  *gg = top > 0.0 ? fabs(gp - gm) / top : 0.0;
+}
+
+__global__ __launch_bounds__(64) void k_score_lex_wave(DevProblem P, const int8_t *__restrict__ bmap,
+                                                       const CandInfo *__restrict__ info,
+                                                       const float *__restrict__ cap_lo,
+                                                       const float *__restrict__ cap_hi,
+                                                       const float *__restrict__ tail_lo,
+                                                       const float *__restrict__ tail_hi,
+                                                       const uint8_t *__restrict__ measured,
+                                                       const float *__restrict__ cap_s,
+                                                       const float *__restrict__ tail_s, int32_t E, int32_t S,
+                                                       double *__restrict__ part_mm, double *__restrict__ part_gp,
+                                                       int64_t n_partial, int stage) {
+  extern __shared__ int lds[];
+  const int chunk = blockIdx.x, e = blockIdx.y, o = blockIdx.z;
+  const int lane = threadIdx.x;
+  const CandInfo ci = info[e];
+  const size_t tile = (size_t)o * E + e;
+  const size_t off = (size_t)o * P.N;
+  if (ci.cls < 0 || measured[off + ci.cell]) return;  // not scored (the finalize writes those)
+  int *tpi = lds;
+  int *rep = tpi + kMaxClasses;
+  int *work = rep + kMaxClasses;
+  WaveAlloc wa{tpi, rep};
+  const LexLds X = lex_lds(P, work);
+  const int8_t *bm = bmap;
+  const float *cm = cap_lo + off, *lm = tail_hi + off, *cp = cap_hi + off, *lp = tail_lo + off;
+  if (stage) {
+    char *st = reinterpret_cast<char *>(work) + lex_work_bytes(P.K, P.G, P.optoff[P.NT]);
+    int8_t *sb = reinterpret_cast<int8_t *>(((uintptr_t)st + 15) & ~(uintptr_t)15);
+    float *sc = reinterpret_cast<float *>(sb + (((size_t)P.K * (P.G + 1) + 3) & ~(size_t)3));
+    stage_copy_bmap(P, bmap, sb);
+    stage_copy_cells(P, cm, lm, sc, sc + P.N);
+    stage_copy_cells(P, cp, lp, sc + 2 * P.N, sc + 3 * P.N);
+    bm = sb;
+    cm = sc;
+    lm = sc + P.N;
+    cp = sc + 2 * P.N;
+    lp = sc + 3 * P.N;
+    __syncthreads();
+  }
+  double mine_mm = 0.0, mine_gp = 0.0;
+  const int s0 = chunk * kWave;
+  const int ns = min(kWave, S - s0);
+  for (int j = 0; j < ns; ++j) {
+    const float cs = cap_s[tile * S + s0 + j];
+    const float ts = tail_s[tile * S + s0 + j];
+    int fm;
+    float g32;
+    double gm, gp;
+    Realisation rm{cm, lm, ci.cell, cs, ts};
+    const int tm = wave_solve(P, bm, rm, work, &fm, nullptr, nullptr);
+    wave_lex_stage(P, bm, rm, tm, fm, X, wa, &g32, &gm);
+    Realisation rp{cp, lp, ci.cell, cs, ts};
+    const int tp = wave_solve(P, bm, rp, work, &fm, nullptr, nullptr);
+    wave_lex_stage(P, bm, rp, tp, fm, X, wa, &g32, &gp);
+    // the binary64 totals are in lane 0
+    gm = __hiloint2double(__builtin_amdgcn_readfirstlane(__double2hiint(gm)),
+                          __builtin_amdgcn_readfirstlane(__double2loint(gm)));
+    gp = __hiloint2double(__builtin_amdgcn_readfirstlane(__double2hiint(gp)),
+                          __builtin_amdgcn_readfirstlane(__double2loint(gp)));
+    double mm, gg;
+    stage_gaps(tm, tp, gm, gp, &mm, &gg);
+    if (lane == j) {
+      mine_mm = mm;
+      mine_gp = gg;
+    }
+  }
+  const double sum_mm = wave_pairwise_sum(mine_mm);
+  const double sum_gp = wave_pairwise_sum(mine_gp);
+  if (lane == 0) {
+    part_mm[tile * n_partial + chunk] = sum_mm;
+    part_gp[tile * n_partial + chunk] = sum_gp;
+  }
+}
+
+// Pairwise tree over n partials zero-padded to a power of two.
+__device__ __forceinline__ double partial_tree(const double *__restrict__ x, int64_t n) {
+  double stack[32];
+  int depth = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    double v = x[i];
+    for (int64_t m = i; m & 1; m >>= 1) v = stack[--depth] + v;
+    stack[depth++] = v;
+  }
+  double sum = stack[depth - 1];
+  for (int d = depth - 2; d >= 0; --d) sum = stack[d] + sum;
+  return sum;
+}
+
+struct PickLex {
+  double mm, gp;
+  int tp, cell, e;  // e < 0: nothing
+};
+
+__device__ __forceinline__ bool better_lex(const PickLex &a, const PickLex &b) {
+  if (a.e < 0) return false;
+  if (b.e < 0) return true;
+  if (a.mm != b.mm) return a.mm > b.mm;
+  if (a.gp != b.gp) return a.gp > b.gp;
+  if (a.tp != b.tp) return a.tp < b.tp;
+  if (a.cell != b.cell) return a.cell < b.cell;
+  return a.e < b.e;
+}
+
+// Scores of both stages and the lexicographic argmax: one wavefront per
+// order, lanes over the candidates, then a shuffle reduction.
+__global__ __launch_bounds__(64) void k_finalize_lex(DevProblem P, const CandInfo *__restrict__ info,
+                                                     const uint8_t *__restrict__ measured, int32_t E, int32_t S,
+                                                     const double *__restrict__ gap_mm,
+                                                     const double *__restrict__ gap_gp,
+                                                     const double *__restrict__ part_mm,
+                                                     const double *__restrict__ part_gp, int64_t n_partial,
+                                                     double *__restrict__ score_mm, double *__restrict__ score_gp,
+                                                     int32_t *__restrict__ best) {
+  const int o = blockIdx.x, lane = threadIdx.x;
+  PickLex mine{0.0, 0.0, 0, 0, -1};
+  for (int e = lane; e < E; e += kWave) {
+    const CandInfo ci = info[e];
+    const size_t tile = (size_t)o * E + e;
+    if (ci.cls < 0) {
+      score_mm[tile] = score_gp[tile] = __builtin_nan("");
+      continue;
+    }
+    if (measured[(size_t)o * P.N + ci.cell]) {
+      score_mm[tile] = score_gp[tile] = 0.0;
+      continue;
+    }
+    const double smm = gap_mm[o] - partial_tree(part_mm + tile * n_partial, n_partial) / (double)S;
+    const double sgp = gap_gp[o] - partial_tree(part_gp + tile * n_partial, n_partial) / (double)S;
+    score_mm[tile] = smm;
+    score_gp[tile] = sgp;
+    const PickLex c{smm, sgp, ci.tp, ci.cell, e};
+    if (better_lex(c, mine)) mine = c;
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    PickLex q;
+    q.mm = __shfl_xor(mine.mm, off, kWave);
+    q.gp = __shfl_xor(mine.gp, off, kWave);
+    q.tp = __shfl_xor(mine.tp, off, kWave);
+    q.cell = __shfl_xor(mine.cell, off, kWave);
+    q.e = __shfl_xor(mine.e, off, kWave);
+    if (better_lex(q, mine)) mine = q;
+  }
+  if (lane == 0 && best) best[o] = mine.e;
+}
+
+// ---------------------------------------------------------------------------
 // Interval refit (Algorithm 1's fit step) under a structural prior: per
 // class and load level, capacity per GPU is unimodal over the TP degrees in
 // ascending order; per class and TP degree, the tail does not fall as the
@@ -3102,6 +3267,11 @@ LoopLayout loop_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
   L.best = take(4 * (size_t)O);
   L.running = take((size_t)O);
   L.n_running = take(4);
+  L.scores_gp = take(8 * (size_t)O * (size_t)E);
+  L.part_gp = take(8 * (size_t)O * (size_t)E * L.score.n_partial);
+  L.gap_mm = take(8 * (size_t)O);
+  L.gap_gp = take(8 * (size_t)O);
+  L.lex_state = take(4 * (size_t)O);
   L.total = at;
   return L;
 }
@@ -3162,6 +3332,52 @@ hipError_t launch_clamp_samples(const DevProblem &P, const int32_t *cand, int32_
   const dim3 grid((unsigned)((S + 1023) / 1024), tiles < 65535 ? tiles : 65535u);
   k_clamp_samples<<<grid, 256, 0, s>>>(P.N, cand, E, cap_lo, cap_hi, tail_lo, tail_hi, cap_s, tail_s, S, tiles,
                                        cs_out, ts_out);
+  return hipGetLastError();
+}
+
+LexScoreLayout lex_score_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
+  LexScoreLayout L{};
+  L.score = ws_layout(P, O, E, S);
+  size_t at = L.score.total;
+  auto take = [&](size_t bytes) {
+    const size_t here = at;
+    at = align256(at + (bytes > 0 ? bytes : 1));
+    return here;
+  };
+  L.part_gp = take(sizeof(double) * (size_t)O * (size_t)E * L.score.n_partial);
+  L.gap_mm = take(sizeof(double) * (size_t)O);
+  L.gap_gp = take(sizeof(double) * (size_t)O);
+  L.state = take(sizeof(int32_t) * (size_t)O);
+  L.total = at;
+  return L;
+}
+
+hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const float *cap_hi, const float *tail_lo,
+                            const float *tail_hi, const uint8_t *measured, const float *cap_s, const float *tail_s,
+                            int32_t O, int32_t E, int32_t S, double *score_mm, double *score_gp, double *gap_mm,
+                            double *gap_gp, int32_t *best, uint8_t *ws, const LexScoreLayout &L, hipStream_t s) {
+  if (O == 0) return hipSuccess;
+  double *gmm = gap_mm ? gap_mm : (double *)(ws + L.gap_mm);
+  double *ggp = gap_gp ? gap_gp : (double *)(ws + L.gap_gp);
+  const AllocOut none{nullptr, nullptr, nullptr, nullptr, nullptr};
+  hipError_t e = launch_certify_lex(P, cap_lo, cap_hi, tail_lo, tail_hi, measured, O, 0.0f,
+                                    (int32_t *)(ws + L.state), none, none, gmm, ggp, ws, L.score, s);
+  if (e != hipSuccess || E == 0) return e;
+  const int64_t n_partial = L.score.n_partial;
+  double *pmm = (double *)(ws + L.score.partial), *pgp = (double *)(ws + L.part_gp);
+  const CandInfo *info = (const CandInfo *)(ws + L.score.cand);
+  if (S > 0) {
+    const size_t base = lds_bytes_lex(P, 1), staged = base + stage2_bytes(P);
+    const int stage = stage_fits(staged) ? 1 : 0;
+    const dim3 grid((unsigned)((S + kWave - 1) / kWave), (unsigned)E, (unsigned)O);
+    k_score_lex_wave<<<grid, 64, stage ? staged : base, s>>>(P, (const int8_t *)(ws + L.score.bmap), info, cap_lo,
+                                                             cap_hi, tail_lo, tail_hi, measured, cap_s, tail_s, E,
+                                                             S, pmm, pgp, n_partial, stage);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  k_finalize_lex<<<O, 64, 0, s>>>(P, info, measured, E, S, gmm, ggp, pmm, pgp, S > 0 ? n_partial : 0, score_mm,
+                                  score_gp, best);
   return hipGetLastError();
 }
 

@@ -35,7 +35,8 @@ EXPORTED = ("fs_context_create", "fs_context_destroy", "fs_context_set_option", 
             "fs_last_error",
             "fs_validate_problem", "fs_workspace_size", "fs_solve_batch", "fs_score_candidates",
             "fs_certify", "fs_loop_workspace_size", "fs_profile_loop", "fs_reduce_cells", "fs_reduce_samples",
-            "fs_solve_batch_lex", "fs_certify_lex", "fs_refit_intervals", "fs_loop_refit_workspace_size")
+            "fs_solve_batch_lex", "fs_certify_lex", "fs_refit_intervals", "fs_loop_refit_workspace_size",
+            "fs_score_lex_workspace_size", "fs_score_candidates_lex")
 POLICY_SCORE, POLICY_ORDER = 0, 1
 CELL_SECONDS = 300.0
 
@@ -104,6 +105,9 @@ def load_library():
     lib.fs_loop_workspace_size.argtypes = [P, i32, i32, i32, ctypes.POINTER(sz)]
     lib.fs_profile_loop.argtypes = [vp, P, _Intervals, i32, vp, vp, vp, i32, vp, vp, i32, ctypes.c_float,
                                     ctypes.c_int, vp, i32, i32, _LoopOut, vp, sz, vp]
+    lib.fs_score_lex_workspace_size.argtypes = [P, i32, i32, i32, ctypes.POINTER(sz)]
+    lib.fs_score_candidates_lex.argtypes = [vp, P, _Intervals, i32, vp, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp,
+                                            sz, vp]
     lib.fs_refit_intervals.argtypes = [vp, P, _Intervals, i32, vp, vp, vp, vp]
     lib.fs_loop_refit_workspace_size.argtypes = [P, i32, i32, i32, ctypes.POINTER(sz)]
     lib.fs_solve_batch_lex.argtypes = [vp, P, vp, vp, i64, _Alloc, vp, vp, sz, vp]
@@ -414,6 +418,51 @@ def certify_lex(ctx: Context, problem, iv: DeviceIntervals, eps: float = 0.05, s
                                          _alloc_struct(cons), _alloc_struct(opt), gmm.data_ptr(), ggp.data_ptr(),
                                          ws.data_ptr(), ws.numel(), _stream(dev, stream)))
     return CertifyLexOutput(state, gmm, ggp, cons, opt)
+
+
+@dataclass
+class ScoreLexOutput:
+    score_maxmin: object   # [O, E] float64
+    score_goodput: object  # [O, E] float64
+    gap_maxmin: object     # [O] float64
+    gap_goodput: object    # [O] float64
+    best: object           # [O] int32
+
+
+def score_lex_workspace_size(problem, n_orders: int, n_cand: int, n_samples: int) -> int:
+    ref = _ProblemRef(problem)
+    out = ctypes.c_size_t()
+    _check(load_library().fs_score_lex_workspace_size(ref.ptr, int(n_orders), int(n_cand), int(n_samples),
+                                                      ctypes.byref(out)))
+    return int(out.value)
+
+
+def score_candidates_lex(ctx: Context, problem, iv: DeviceIntervals, cand, cap_s, tail_s, stream=None,
+                         workspace=None) -> ScoreLexOutput:
+    """The stage-wise score under the whole objective
+    (fs_score_candidates_lex); shapes as in score_candidates."""
+    torch = _torch()
+    ref = _ProblemRef(problem)
+    O = int(iv.cap_lo.shape[0])
+    E = int(cand.shape[0])
+    S = int(cap_s.shape[2]) if E > 0 else 0
+    dev = iv.cap_lo.device
+    ivs = _intervals_struct(iv, O, ref.N)
+    pcand = _dev_ptr(cand, torch.int32, (E,), "cand")
+    pcs = _dev_ptr(cap_s, torch.float32, (O, E, S), "cap_s")
+    pts = _dev_ptr(tail_s, torch.float32, (O, E, S), "tail_s")
+    out = ScoreLexOutput(torch.empty((O, E), dtype=torch.float64, device=dev),
+                         torch.empty((O, E), dtype=torch.float64, device=dev),
+                         torch.empty(O, dtype=torch.float64, device=dev), torch.empty(O, dtype=torch.float64, device=dev),
+                         torch.empty(O, dtype=torch.int32, device=dev))
+    ws_bytes = score_lex_workspace_size(problem, O, E, S)
+    ws = workspace if workspace is not None else ctx.workspace(ws_bytes)
+    _check(load_library().fs_score_candidates_lex(ctx.handle, ref.ptr, ivs, O, pcand, E, pcs, pts, S,
+                                                  out.score_maxmin.data_ptr(), out.score_goodput.data_ptr(),
+                                                  out.gap_maxmin.data_ptr(), out.gap_goodput.data_ptr(),
+                                                  out.best.data_ptr(), ws.data_ptr(), ws.numel(),
+                                                  _stream(dev, stream)))
+    return out
 
 
 def refit_intervals(ctx: Context, problem, iv: DeviceIntervals, stream=None) -> DeviceIntervals:
