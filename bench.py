@@ -19,6 +19,7 @@ from __future__ import annotations
 import argparse
 import hashlib
 import json
+import math
 import os
 import re
 import sys
@@ -40,6 +41,8 @@ DIV_OPS = 3
 PROFILE_GLOB = os.path.join(ROOT, "profiles")
 # Issue slots of one (max,min) pair: two pairs take v_min, v_min, v_max3.
 PAIR_SLOTS = 1.5
+# Longest replica range the exclusion scorer scans; longer ones are searched.
+SCAN_MAX = 8
 # Back-to-back scorer launches per event pair in the kernel-duration pass.
 TIMING_REPEATS = 10
 
@@ -143,20 +146,37 @@ def replica_range_sizes(problem, cand):
     return sizes
 
 
+def excl_slots_per_scenario(n_e: int) -> float:
+    """VALU lane-slots of one scenario of the exclusion scorer, counted for
+    the algorithm the kernel runs on a replica range of n_e counts (max,
+    min, compare, select, convert, multiply = 1 slot; the exact quotient =
+    DIV_OPS; data movement, address arithmetic and loop control are not
+    counted):
+      n_e <= SCAN_MAX (the scan): per r the sampled quotient (multiply +
+        DIV_OPS) and one (max,min) step into each realisation
+        (2 x PAIR_SLOTS);
+      longer ranges (the crossing search): per realisation ceil(log2(n_e+1))
+        steps of a compare and a select, then the ratio of the last r below
+        the crossing (multiply, quotient, min with 1), two selects and a max,
+        and the max into the accumulator;
+    plus per scenario the sampled tail test and two selects (3), the gap (two
+    converts and a subtract: 3) and one add of the pairwise sum (1)."""
+    if n_e <= SCAN_MAX:
+        return n_e * (1 + DIV_OPS + 2 * PAIR_SLOTS) + 7
+    steps = math.ceil(math.log2(n_e + 1))
+    return 2 * (2 * steps + (2 + DIV_OPS) + 3 + 1) + 7
+
+
 def excl_work(problem, cand, live_tiles, S):
-    """Algorithmic work of one exclusion-scorer launch.
-    Per scenario, in VALU lane-slots: for each of the candidate's n_e replica
-    counts, the sampled ratio (multiply, quotient, min with 1: 2 + DIV_OPS)
-    and one (max,min) step into each realisation (2 x PAIR_SLOTS); then the
-    sampled tail test and two selects (3), the gap (two converts and a
-    subtract: 3) and one add of the pairwise sum (1).  Bytes: the two binary32
-    samples (8 B).  A tile whose cell no replica count reaches (n_e = 0) has
-    tau = U in every scenario: its samples cannot matter, so it contributes
-    neither slots nor bytes (its score is formed in closed form)."""
+    """Algorithmic work of one exclusion-scorer launch: VALU lane-slots
+    (excl_slots_per_scenario) and bytes (the two binary32 samples, 8 B) of
+    every scenario whose samples can matter.  A tile whose cell no replica
+    count reaches (n_e = 0) has tau = U in every scenario: its samples
+    cannot matter, so it contributes neither slots nor bytes (its score is
+    formed in closed form)."""
     n_e = replica_range_sizes(problem, cand)
-    per_r = 2 + DIV_OPS + 2 * PAIR_SLOTS
     used = [(o, e) for (o, e) in live_tiles if n_e[e] > 0]
-    slots = float(sum(S * (per_r * n_e[e] + 7) for (_, e) in used))
+    slots = float(sum(S * excl_slots_per_scenario(int(n_e[e])) for (_, e) in used))
     return slots, 8.0 * S * len(used), float(n_e.mean()), S * len(used)
 
 
@@ -397,16 +417,29 @@ def policy_bench(args):
 
 def lex_work_per_scenario(problem) -> float:
     """Algorithmic work of one solve under the whole objective, in VALU
-    lane-slots: levels (1)-(2) as one solve of the lane work model, then per
-    class and budget g the candidates of level (3)'s knapsack, one per
-    existing option with cost <= g: a binary64 add (2 slots at half rate),
-    two compares and a select (3)."""
+    lane-slots, for the algorithm k_solve_dense_lex runs: per existing option
+    its ratio (multiply, quotient, min with 1, tail compare, select, max into
+    its budget slot: 5 + DIV_OPS); per class the prefix maximum (G - 1);
+    each (max,min) target a crossing search (per step a compare and a
+    select, then two selects and a max) -- every budget of the K - 2 middle
+    classes and budget G of the last; then per class and budget g one
+    candidate of level (3)'s knapsack per existing option with cost <= g: a
+    binary64 add, two compares and a select (4; binary64 adds issue at the
+    full rate on gfx950)."""
     import numpy as np
     G, K = problem.budget, problem.n_classes
-    ex = existing_options(problem).reshape(K, -1)
+    ex = existing_options(problem)
+    per = int(ex.sum()) * (5 + DIV_OPS) + K * (G - 1)
+    if K >= 2:
+        top = 1
+        while 2 * top <= G + 1:
+            top *= 2
+        steps = int(math.log2(top)) + 1
+        per += ((K - 2) * (G + 1) + 1) * (2 * steps + 3)
+    ex = ex.reshape(K, -1)
     costs = np.concatenate([np.arange(1, G // int(t) + 1) * int(t) for t in problem.tp])
     per_g = np.array([[(costs[ex[k] > 0] <= g).sum() for g in range(G + 1)] for k in range(K)])
-    return lane_work_per_scenario(problem, existing_options(problem)) / 2.0 + 5.0 * float(per_g.sum())
+    return float(per) + 4.0 * float(per_g.sum())
 
 
 def lex_bench(args):
