@@ -42,7 +42,7 @@ PROFILE_GLOB = os.path.join(ROOT, "profiles")
 # Issue slots of one (max,min) pair: two pairs take v_min, v_min, v_max3.
 PAIR_SLOTS = 1.5
 # Longest replica range the exclusion scorer scans; longer ones are searched.
-SCAN_MAX = 8
+SCAN_MAX = 4
 # Back-to-back scorer launches per event pair in the kernel-duration pass.
 TIMING_REPEATS = 10
 
@@ -156,15 +156,15 @@ def excl_slots_per_scenario(n_e: int) -> float:
         DIV_OPS) and one (max,min) step into each realisation
         (2 x PAIR_SLOTS);
       longer ranges (the crossing search): per realisation ceil(log2(n_e+1))
-        steps of a compare and a select, then the ratio of the last r below
-        the crossing (multiply, quotient, min with 1), two selects and a max,
-        and the max into the accumulator;
+        steps of a compare and a select, then the ratio of the replica count
+        below the crossing (multiply and quotient) and the max of it, M at
+        the crossing and the accumulator (2);
     plus per scenario the sampled tail test and two selects (3), the gap (two
     converts and a subtract: 3) and one add of the pairwise sum (1)."""
     if n_e <= SCAN_MAX:
         return n_e * (1 + DIV_OPS + 2 * PAIR_SLOTS) + 7
     steps = math.ceil(math.log2(n_e + 1))
-    return 2 * (2 * steps + (2 + DIV_OPS) + 3 + 1) + 7
+    return 2 * (2 * steps + (1 + DIV_OPS) + 2) + 7
 
 
 def excl_work(problem, cand, live_tiles, S):

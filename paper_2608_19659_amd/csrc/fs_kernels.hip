@@ -205,6 +205,31 @@ __device__ __forceinline__ int level_of(const DevProblem &P, int k, int r) {
   return -1;
 }
 
+// Number of load levels below a per-replica load: the index of the smallest
+// level that holds it, B when none does.  The loop runs over the largest
+// level count, so the level values (kernel arguments) are fetched by a few
+// wide scalar loads ahead of the compares instead of one load per level.
+__device__ __forceinline__ int levels_below(const DevProblem &P, float per_replica) {
+  int b = 0;
+#pragma unroll
+  for (int j = 0; j < kMaxLevels; ++j) b += (j < P.B && P.levels[j] < per_replica) ? 1 : 0;
+  return b;
+}
+
+// Copies n bytes to LDS with all of a thread's loads (up to 8) issued before
+// its first LDS write, so their latencies overlap.
+__device__ __forceinline__ void stage_u8(uint8_t *__restrict__ dst, const uint8_t *__restrict__ src, int n,
+                                         int tid, int nth) {
+  for (int x0 = tid; x0 < n; x0 += 8 * nth) {
+    uint8_t v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = x0 + u * nth < n ? src[x0 + u * nth] : 0;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (x0 + u * nth < n) dst[x0 + u * nth] = v[u];
+  }
+}
+
 __global__ void k_setup_bucket(DevProblem P, int8_t *__restrict__ bmap) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   const int n = P.K * (P.G + 1);
@@ -1290,26 +1315,25 @@ __device__ void prep_list_staged(const DevProblem &P, int O, const uint8_t *__re
   int *c_cell = lv_last + K * B, *c_code = c_cell + E;
   uint8_t *meas = reinterpret_cast<uint8_t *>(c_code + E);
   __shared__ int c_tp[kMaxTp], c_optoff[kMaxTp + 1];
+  __shared__ float c_demand[kPrepOrderMaxK];
   if (tid < P.NT) c_tp[tid] = P.tp[tid];
   if (tid <= P.NT) c_optoff[tid] = P.optoff[tid];
+  if (tid < K) c_demand[tid] = P.demand[tid];
   if (tid < 32) bucket_count[tid] = 0;
   for (int x = tid; x < K * B; x += nth) {
     lv_first[x] = INT_MAX;
     lv_last[x] = 0;
   }
-  for (int x = tid; x < O * N; x += nth) meas[x] = measured[x];
+  stage_u8(meas, measured, O * N, tid, nth);
   for (int e = tid; e < E; e += nth) c_cell[e] = cand[e];
-  __syncthreads();  // the counters are set; the loads are still in flight
-  for (int k = 0; k < K; ++k) {  // problem constants are read at uniform indices
-    const float demand = P.demand[k];
-    for (int r = tid + 1; r <= G; r += nth) {
-      const float per_replica = demand / (float)r;
-      int b = 0;
-      for (int j = 0; j < B; ++j) b += P.levels[j] < per_replica ? 1 : 0;
-      if (b < B) {
-        atomicMin(&lv_first[k * B + b], r);
-        atomicMax(&lv_last[k * B + b], r);
-      }
+  __syncthreads();
+  // one thread per (class, replica count)
+  for (int x = tid; x < K * G; x += nth) {
+    const int k = x / G, r = x - k * G + 1;
+    const int b = levels_below(P, c_demand[k] / (float)r);
+    if (b < B) {
+      atomicMin(&lv_first[k * B + b], r);
+      atomicMax(&lv_last[k * B + b], r);
     }
   }
   __syncthreads();
@@ -1363,8 +1387,10 @@ __device__ void prep_list_staged(const DevProblem &P, int O, const uint8_t *__re
         }
       }
     }
-    __syncthreads();
+    // the end markers below need only the count from the first pass: no
+    // barrier (and no wait for the list's stores) after the second
     if (pass == 0) {
+      __syncthreads();
       if (tid < kWave) {
         const int cnt = lane < 32 ? bucket_count[lane] : 0;
         const int incl = wave_scan_add_rows(cnt, lane);
@@ -1449,9 +1475,7 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
   }
   for (int e = tid; e < E; e += nth) ccand[e] = cand[e];
   if (wave < K && lane < G) {  // wavefront k: the levels of class k, r = lane + 1
-    const float per_replica = P.demand[wave] / (float)(lane + 1);
-    int b = 0;
-    for (int j = 0; j < B; ++j) b += P.levels[j] < per_replica ? 1 : 0;
+    const int b = levels_below(P, P.demand[wave] / (float)(lane + 1));
     lvl[wave * G + lane] = (int8_t)(b < B ? b : -1);
   }
   for (int c = lane; wave < K && c < per_class; c += kWave) {
@@ -1472,7 +1496,7 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
     const double rcp = P.rcp_demand[k];
     const int r = lane + 1;
     for (int ti = 0; ti < NT; ++ti) {
-      const int t = P.tp[ti];
+      const int t = c_tp[ti];
       if (t * r < G) {
         const int b = lvl[k * G + r - 1];
         if (b >= 0) {
@@ -1516,12 +1540,13 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
     const float slo = P.slo[i], demand = P.demand[i];
     const double rcp = P.rcp_demand[i];
     for (int p = lane; p < PPc; p += kWave) {
-      int ti = 0, first = 0, t = P.tp[0];
+      int ti = 0, first = 0, t = c_tp[0];
       for (int t2 = 1; t2 < NT; ++t2) {
-        if (p >= P.optoff[t2]) {
+        const int f2 = c_optoff[t2];
+        if (p >= f2) {
           ti = t2;
-          first = P.optoff[t2];
-          t = P.tp[t2];
+          first = f2;
+          t = c_tp[t2];
         }
       }
       const int r = p - first + 1;
@@ -1599,7 +1624,7 @@ __device__ __forceinline__ int sampled_quotient(float rf, float cs, double rcp) 
 
 // Largest replica range handled by the unrolled scan; longer ranges use the
 // crossing search.
-constexpr int kScanMax = 8;
+constexpr int kScanMax = 4;
 
 // Default grid of the exclusion scorer: four wavefronts per SIMD (1024 SIMDs).
 constexpr int kScorerWaves = 4096;
@@ -1769,14 +1794,14 @@ __global__ __launch_bounds__(64) void k_score_excl(
       ap[q] = X.u1;
     }
     if (nr <= kScanMax) {
+      // pairs of replica counts, then a single one when nr is odd
 #pragma unroll
       for (int j = 0; j < kScanMax; j += 2) {
-        if (j < nr) {
-          // M <= 1 lets min(f, M) use the unclamped quotient; past the range
-          // M is taken as 0, a term that cannot raise tau (U >= 0)
+        if (j + 1 < nr) {
+          // M <= 1 lets min(f, M) use the unclamped quotient
           const int mm0 = __builtin_amdgcn_readlane(X.vm0, j), mp0 = __builtin_amdgcn_readlane(X.vm1, j);
-          const int mm1 = j + 1 < nr ? __builtin_amdgcn_readlane(X.vm0, j + 1) : 0;
-          const int mp1 = j + 1 < nr ? __builtin_amdgcn_readlane(X.vm1, j + 1) : 0;
+          const int mm1 = __builtin_amdgcn_readlane(X.vm0, j + 1);
+          const int mp1 = __builtin_amdgcn_readlane(X.vm1, j + 1);
           const float r1 = (float)(rlo + j), r2 = (float)(rlo + j + 1);
 #pragma unroll
           for (int q = 0; q < SPL; ++q) {
@@ -1784,6 +1809,15 @@ __global__ __launch_bounds__(64) void k_score_excl(
             const int f2 = sampled_quotient(r2, X.cs[q], rcp);
             am[q] = max(am[q], max(min(f1, mm0), min(f2, mm1)));
             ap[q] = max(ap[q], max(min(f1, mp0), min(f2, mp1)));
+          }
+        } else if (j < nr) {
+          const int mm0 = __builtin_amdgcn_readlane(X.vm0, j), mp0 = __builtin_amdgcn_readlane(X.vm1, j);
+          const float r1 = (float)(rlo + j);
+#pragma unroll
+          for (int q = 0; q < SPL; ++q) {
+            const int f1 = sampled_quotient(r1, X.cs[q], rcp);
+            am[q] = max(am[q], min(f1, mm0));
+            ap[q] = max(ap[q], min(f1, mp0));
           }
         }
       }
@@ -1794,53 +1828,66 @@ __global__ __launch_bounds__(64) void k_score_excl(
       // 2^(steps-1), ..., 1 pos is the first crossing.
       int steps = 0;
       while ((1 << steps) <= nr) ++steps;  // ceil(log2(nr + 1))
-      int pos[SPL][2];
+      if (nr < kWave) {
+        // Option rlo + j of the range sits in lane j.  The lanes past the
+        // range hold a threshold every sample reaches (-inf) and no option
+        // (M = INT_MIN), so the search never passes nr and needs no index
+        // clamp: a lookup index stays below 2^steps - 1 <= 63.  pos is kept
+        // in bytes (4 pos), the lane address of the lookups.  Lane j of rb
+        // holds the replica count below option j (0 for j = 0: its ratio,
+        // 0, cannot raise tau).  Each step issues all 2 x SPL cross-lane
+        // lookups before the first compare (the scheduling barriers keep
+        // them together, so their latencies overlap).
+        const bool in_range = lane < nr;
+        const int t0 = in_range ? __float_as_int(X.vt0) : (int)0xFF800000u;
+        const int t1 = in_range ? __float_as_int(X.vt1) : (int)0xFF800000u;
+        const int m0 = in_range ? X.vm0 : INT_MIN;
+        const int m1 = in_range ? X.vm1 : INT_MIN;
+        const int rb = __float_as_int(lane == 0 ? 0.0f : (float)(rlo + lane - 1));
+        int pb[SPL][2];
 #pragma unroll
-      for (int q = 0; q < SPL; ++q) pos[q][0] = pos[q][1] = 0;
-      if (nr <= kWave) {
-        // option rlo + j of the range sits in lane j.  Each step issues all
-        // 2 x SPL cross-lane lookups before the first compare (the
-        // scheduling barriers keep them together, so their latencies
-        // overlap instead of adding up).
-        const int t0 = __float_as_int(X.vt0), t1 = __float_as_int(X.vt1);
+        for (int q = 0; q < SPL; ++q) pb[q][0] = pb[q][1] = 0;
         for (int stp = 1 << (steps - 1); stp > 0; stp >>= 1) {
+          const int off = 4 * (stp - 1);
           int th[SPL][2];
 #pragma unroll
           for (int q = 0; q < SPL; ++q) {
-            th[q][0] = lane_lookup(t0, min(pos[q][0] + stp - 1, nr - 1));
-            th[q][1] = lane_lookup(t1, min(pos[q][1] + stp - 1, nr - 1));
+            th[q][0] = __builtin_amdgcn_ds_bpermute(pb[q][0] + off, t0);
+            th[q][1] = __builtin_amdgcn_ds_bpermute(pb[q][1] + off, t1);
           }
           __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
           for (int q = 0; q < SPL; ++q) {
 #pragma unroll
-            for (int side = 0; side < 2; ++side) {
-              const int idx = pos[q][side] + stp - 1;
-              const bool below = !(X.cs[q] >= __int_as_float(th[q][side]));
-              pos[q][side] += (idx < nr && below) ? stp : 0;
-            }
+            for (int side = 0; side < 2; ++side)
+              pb[q][side] += !(X.cs[q] >= __int_as_float(th[q][side])) ? 4 * stp : 0;
           }
         }
-        int mj[SPL][2];
+        // tau candidate: max(f of the replica count below the crossing,
+        // M at the crossing).  Below the crossing f < M <= 1, so the
+        // unclamped quotient is the ratio.
+        int mj[SPL][2], rj[SPL][2];
 #pragma unroll
         for (int q = 0; q < SPL; ++q) {
-          mj[q][0] = lane_lookup(X.vm0, min(pos[q][0], nr - 1));
-          mj[q][1] = lane_lookup(X.vm1, min(pos[q][1], nr - 1));
+          mj[q][0] = __builtin_amdgcn_ds_bpermute(pb[q][0], m0);
+          mj[q][1] = __builtin_amdgcn_ds_bpermute(pb[q][1], m1);
+          rj[q][0] = __builtin_amdgcn_ds_bpermute(pb[q][0], rb);
+          rj[q][1] = __builtin_amdgcn_ds_bpermute(pb[q][1], rb);
         }
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int q = 0; q < SPL; ++q) {
-#pragma unroll
-          for (int side = 0; side < 2; ++side) {
-            const int j = pos[q][side];
-            const int fprev = sampled_ratio((float)(rlo + j - 1), X.cs[q], rcp);
-            const int v = max(j > 0 ? fprev : INT_MIN, j < nr ? mj[q][side] : INT_MIN);
-            if (side == 0) am[q] = max(am[q], v);
-            else ap[q] = max(ap[q], v);
-          }
+          const int fm = sampled_quotient(__int_as_float(rj[q][0]), X.cs[q], rcp);
+          const int fp = sampled_quotient(__int_as_float(rj[q][1]), X.cs[q], rcp);
+          am[q] = max(am[q], max(fm, mj[q][0]));
+          ap[q] = max(ap[q], max(fp, mj[q][1]));
         }
       } else {
-        // a range longer than a wavefront: M and the thresholds go to LDS
+        // a range of a wavefront's length or more: M and the thresholds go
+        // to LDS
+        int pos[SPL][2];
+#pragma unroll
+        for (int q = 0; q < SPL; ++q) pos[q][0] = pos[q][1] = 0;
         const int32_t *Mm = mopt + (size_t)o * 2 * n_thr + toff, *Mp = Mm + n_thr;
         const float *Tm = thr + (size_t)o * 2 * n_thr + toff, *Tp = Tm + n_thr;
         float *Tl = reinterpret_cast<float *>(Mlds + 2 * nr);
@@ -3109,7 +3156,7 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
     // than a wavefront (the longest range has G / tp[0] options)
     const int32_t range_max = P.G / P.tp[0];
     const size_t mlds = (size_t)P.K * (sizeof(double) + sizeof(float)) +
-                        (range_max > kWave ? 4 * sizeof(int) * (size_t)range_max : 0);
+                        (range_max >= kWave ? 4 * sizeof(int) * (size_t)range_max : 0);
     const int64_t items = n_partial * a.O * a.E;  // upper bound of the live items
     const int64_t waves = a.waves > 0 ? a.waves : kScorerWaves;
     const unsigned grid = (unsigned)(items < waves ? items : waves);
