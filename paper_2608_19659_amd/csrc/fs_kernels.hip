@@ -886,10 +886,13 @@ __device__ __forceinline__ void option_of(const DevProblem &P, int p, int *ti, i
 // Smallest binary32 capacity x >= 0 at which r replicas reach ratio bits M,
 // i.e. min(1, fl32(fl32(r * x) / demand)) >= M.  The ratio is nondecreasing
 // in x and nonnegative binary32 values order like their bit patterns.  The
-// quotient M * demand / r lands within a few units in the last place; the
-// answer is then pinned by stepping until x reaches M and x - 1ulp does not,
-// with a bisection over bit patterns if that takes more than a few steps.
-// 0 when M <= 0 (always reached); NaN when M exceeds 1 (never reached).
+// quotient M * demand / r lands within a few units in the last place, so the
+// eight bit patterns from 3 below it are tested at once (independent
+// evaluations, whose latencies overlap): when the first does not reach M
+// (or is 0) and the last does, the answer is the first that does.  Otherwise
+// -- never seen, kept for safety -- the answer is pinned by stepping, then
+// by a bisection over bit patterns.  0 when M <= 0 (always reached); NaN when
+// M exceeds 1 (never reached).
 __device__ __forceinline__ float capacity_threshold(int r, int M, float demand, double rcp) {
   if (M <= 0) return 0.0f;
   if (M > __float_as_int(1.0f)) return __builtin_nanf("");
@@ -899,6 +902,13 @@ __device__ __forceinline__ float capacity_threshold(int r, int M, float demand, 
     return __float_as_int(fminf((float)((double)capacity * rcp), 1.0f)) >= M;
   };
   unsigned x = __float_as_uint(__int_as_float(M) * demand * __builtin_amdgcn_rcpf(rf));
+  {
+    const unsigned x0 = x > 3u ? x - 3u : 0u;
+    int below = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) below += reach(x0 + (unsigned)k) ? 0 : 1;
+    if (below < 8 && (below > 0 || x0 == 0u)) return __uint_as_float(x0 + (unsigned)below);
+  }
   int n = 0;
   while (!reach(x) && n < 8) { ++x; ++n; }
   while (x > 0 && reach(x - 1) && n < 16) { --x; ++n; }
@@ -1464,6 +1474,15 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
   const float *gcap = (R == 0 ? cap_lo : cap_hi) + off;
   const float *gtail = (R == 0 ? tail_hi : tail_lo) + off;
 
+  // the TP degrees and option offsets in registers: read unconditionally
+  // (a few wide scalar loads), so later loops over TP degrees touch no memory
+  int tpr[kMaxTp], ofr[kMaxTp];
+#pragma unroll
+  for (int j = 0; j < kMaxTp; ++j) {
+    tpr[j] = P.tp[j];
+    ofr[j] = P.optoff[j];
+  }
+
   // --- 1. stage the order; load levels while the loads are in flight
   __shared__ int c_tp[kMaxTp], c_optoff[kMaxTp + 1];
   if (tid < NT) c_tp[tid] = P.tp[tid];
@@ -1495,14 +1514,13 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
     const float slo = P.slo[k];
     const double rcp = P.rcp_demand[k];
     const int r = lane + 1;
-    for (int ti = 0; ti < NT; ++ti) {
-      const int t = c_tp[ti];
-      if (t * r < G) {
-        const int b = lvl[k * G + r - 1];
-        if (b >= 0) {
-          const int cell = (k * NT + ti) * B + b;
-          atomicMax(&T[t * r], ratio_bits(ccap[cell], ctail[cell], r, slo, rcp));
-        }
+    const int b = lane < G ? lvl[k * G + r - 1] : -1;
+#pragma unroll
+    for (int ti = 0; ti < kMaxTp; ++ti) {
+      const int t = tpr[ti];
+      if (ti < NT && t * r < G && b >= 0) {
+        const int cell = (k * NT + ti) * B + b;
+        atomicMax(&T[t * r], ratio_bits(ccap[cell], ctail[cell], r, slo, rcp));
       }
     }
     wave_lds_fence();
@@ -1539,33 +1557,50 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
     float *To = thr + ((size_t)o * 2 + R) * n_thr + (size_t)i * PPc;
     const float slo = P.slo[i], demand = P.demand[i];
     const double rcp = P.rcp_demand[i];
-    for (int p = lane; p < PPc; p += kWave) {
-      int ti = 0, first = 0, t = c_tp[0];
-      for (int t2 = 1; t2 < NT; ++t2) {
-        const int f2 = c_optoff[t2];
-        if (p >= f2) {
-          ti = t2;
-          first = f2;
-          t = c_tp[t2];
+    // Options two wavefronts' worth at a time: lane l takes options
+    // base + l and base + l + 64 together, so their LDS reads and threshold
+    // searches overlap (one pass when the class has at most 128 options).
+    for (int base = 0; base < PPc; base += 2 * kWave) {
+      int rr[2], Mv[2], fv[2], loc[2];
+      bool has[2], ok[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int p = base + lane + u * kWave;
+        int ti = 0, first = 0, t = tpr[0];
+#pragma unroll
+        for (int t2 = 1; t2 < kMaxTp; ++t2) {
+          const bool in = t2 < NT && p >= ofr[t2];
+          ti = in ? t2 : ti;
+          first = in ? ofr[t2] : first;
+          t = in ? tpr[t2] : t;
         }
+        has[u] = p < PPc;
+        const int r = has[u] ? p - first + 1 : 1;
+        const int b = has[u] ? lvl[i * G + r - 1] : -1;
+        ok[u] = b >= 0;
+        const int local = ti * B + (ok[u] ? b : 0), cell = i * per_class + local;
+        // ratios never exceed 1, so M above 1 acts as 1 (min(f, M) and the
+        // crossing are unchanged) and the scorer can skip the clamp of f
+        rr[u] = r;
+        loc[u] = local;
+        Mv[u] = ok[u] ? min(H[G - t * r], __float_as_int(1.0f)) : INT_MIN;
+        fv[u] = ok[u] ? ratio_bits(ccap[cell], ctail[cell], r, slo, rcp) : 0;
       }
-      const int r = p - first + 1;
-      const int b = lvl[i * G + r - 1];
-      if (b < 0) {
-        Mo[p] = INT_MIN;
-        To[p] = __builtin_nanf("");
-        continue;
+      float Tv[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) Tv[u] = ok[u] ? capacity_threshold(rr[u], Mv[u], demand, rcp) : __builtin_nanf("");
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        if (!has[u]) continue;
+        const int p = base + lane + u * kWave;
+        if (ok[u]) {
+          atomicMax(&mc[loc[u]], min(fv[u], Mv[u]));
+          atomicMin(&crlo[loc[u]], rr[u]);
+          atomicMax(&crhi[loc[u]], rr[u]);
+        }
+        Mo[p] = Mv[u];
+        To[p] = Tv[u];
       }
-      const int local = ti * B + b, cell = i * per_class + local;
-      // ratios never exceed 1, so M above 1 acts as 1 (min(f, M) and the
-      // crossing are unchanged) and the scorer can skip the clamp of f
-      const int M = min(H[G - t * r], __float_as_int(1.0f));
-      const int f = ratio_bits(ccap[cell], ctail[cell], r, slo, rcp);
-      atomicMax(&mc[local], min(f, M));
-      atomicMin(&crlo[local], r);
-      atomicMax(&crhi[local], r);
-      Mo[p] = M;
-      To[p] = capacity_threshold(r, M, demand, rcp);
     }
   }
   wave_lds_fence();
@@ -1626,8 +1661,11 @@ __device__ __forceinline__ int sampled_quotient(float rf, float cs, double rcp) 
 // crossing search.
 constexpr int kScanMax = 4;
 
-// Default grid of the exclusion scorer: four wavefronts per SIMD (1024 SIMDs).
-constexpr int kScorerWaves = 4096;
+// Default grid of the exclusion scorer: three wavefronts per SIMD (1024
+// SIMDs).  On the 4-class, G = 64 workload (about 7,100 items) three per
+// SIMD ran the scorer in 9.0-9.1 us against 9.5 us with four, 10.0 with 2.5
+// and 10.7-11.2 with two.
+constexpr int kScorerWaves = 3072;
 
 // Samples of one chunk.  VEC (S a multiple of 4): each group of 4 samples
 // of a lane lies wholly below S or wholly past it; every group is fetched by
