@@ -1382,8 +1382,22 @@ __device__ void prep_list_staged(const DevProblem &P, int O, const uint8_t *__re
       }
       if (code == -2) continue;
       const int nr = code >> 16, b = range_bucket(nr);
+      // the thread's orders o = sub, sub + g, ..., their revealed flags read
+      // eight at a time (the reads of a batch overlap)
+      auto flags = [&](int o0, uint8_t (&mv)[8]) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int o = o0 + u * g;
+          mv[u] = o < O ? meas[o * N + cell] : 1;
+        }
+      };
       int n = 0;
-      for (int o = sub; o < O; o += g) n += (dump || !meas[o * N + cell]) ? 1 : 0;
+      for (int o0 = sub; o0 < O; o0 += 8 * g) {
+        uint8_t mv[8];
+        flags(o0, mv);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) n += (o0 + u * g < O && (dump || !mv[u])) ? 1 : 0;
+      }
       if (n == 0) continue;
       if (pass == 0) {
         atomicAdd(&bucket_count[b], n);
@@ -1391,9 +1405,15 @@ __device__ void prep_list_staged(const DevProblem &P, int O, const uint8_t *__re
         int at = atomicAdd(&bucket_start[b], n);
         const int k = cell / per_class, ti = (cell / B) % P.NT;
         const int toff = k * PPc + c_optoff[ti] + (code & 0xFFFF) - 1;
-        for (int o = sub; o < O; o += g) {
-          const bool rev = meas[o * N + cell] != 0;
-          if (dump || !rev) list[at++] = make_int4(e, toff, code, k | ((rev ? 1 : 0) << 6) | (o << 8));
+        for (int o0 = sub; o0 < O; o0 += 8 * g) {
+          uint8_t mv[8];
+          flags(o0, mv);
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            const int o = o0 + u * g;
+            const bool rev = mv[u] != 0;
+            if (o < O && (dump || !rev)) list[at++] = make_int4(e, toff, code, k | ((rev ? 1 : 0) << 6) | (o << 8));
+          }
         }
       }
     }
@@ -2073,60 +2093,111 @@ __device__ __forceinline__ double excl_constant_sum(const TileInfo &tl, int32_t 
   return pairwise_run((double)__int_as_float(tl.u_p) - (double)__int_as_float(tl.u_m), S);
 }
 
-// Scores and best candidate of the exclusion scorer: one block per order,
-// one thread per candidate.  Each tile's partials (at most 16 here) are
-// summed by the pairwise tree in registers.
-__global__ __launch_bounds__(256) void k_finalize_excl(const TileInfo *__restrict__ tiles, int32_t E,
-                                                       int32_t S, const int32_t *__restrict__ base,
-                                                       const double *__restrict__ partial,
-                                                       int64_t n_partial, double *__restrict__ score,
-                                                       double *__restrict__ gap_now,
-                                                       int32_t *__restrict__ best) {
-  __shared__ Pick s_pick[4];
-  const int o = blockIdx.x;
+// Order-preserving key of a score: a larger score has a larger key, and
+// -0.0 counts as +0.0 (scores compare equal there).  Every number's key is
+// above 0, which stands for "no candidate".
+__device__ __forceinline__ uint64_t score_key(double x) {
+  const uint64_t b = (uint64_t)__double_as_longlong(x + 0.0);
+  return (b >> 63) ? ~b : (b | (1ull << 63));
+}
+
+// Tie-break key among equal scores (smaller wins): TP degree, then cell,
+// then candidate index (TP <= 4096 and cells < 2^16 by the problem limits).
+__device__ __forceinline__ uint64_t tie_key(int tp, int cell, int e) {
+  return ((uint64_t)(uint32_t)tp << 48) | ((uint64_t)(uint32_t)cell << 32) | (uint64_t)(uint32_t)e;
+}
+
+template <int kCtrl>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)v, kCtrl, 0xF, 0xF, true);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)(v >> 32), kCtrl, 0xF, 0xF, true);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int l) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Maximum (kMax) or minimum of a 64-bit key over the 64 lanes, by the same
+// DPP pattern as wave_max_dpp.  Wave-uniform result; every lane active.
+template <bool kMax>
+__device__ __forceinline__ uint64_t wave_ext_u64(uint64_t v) {
+  auto pick = [](uint64_t a, uint64_t b) { return kMax ? (a > b ? a : b) : (a < b ? a : b); };
+  v = pick(v, dpp_u64<0xB1>(v));
+  v = pick(v, dpp_u64<0x4E>(v));
+  v = pick(v, dpp_u64<0x141>(v));
+  v = pick(v, dpp_u64<0x140>(v));
+  return pick(pick(readlane_u64(v, 0), readlane_u64(v, 16)), pick(readlane_u64(v, 32), readlane_u64(v, 48)));
+}
+
+// Scores and best candidate of the exclusion scorer: one wavefront per
+// order, lane l taking candidates l, l + 64, ... two at a time (their loads
+// overlap).  Each tile's partials (at most 16 here) are summed by the
+// pairwise tree in registers.  The arg-max is two key reductions: the
+// largest score, then the smallest (TP, cell, index) among the lanes
+// holding it -- the order that `better` defines.
+__global__ __launch_bounds__(64) void k_finalize_excl(const TileInfo *__restrict__ tiles, int32_t E,
+                                                      int32_t S, const int32_t *__restrict__ base,
+                                                      const double *__restrict__ partial,
+                                                      int64_t n_partial, double *__restrict__ score,
+                                                      double *__restrict__ gap_now,
+                                                      int32_t *__restrict__ best) {
+  const int o = blockIdx.x, lane = threadIdx.x;
   const double gap = (double)__int_as_float(base[o * 2 + 1]) - (double)__int_as_float(base[o * 2 + 0]);
   int p2 = 1;
   while (p2 < n_partial) p2 <<= 1;
-  Pick mine{0.0, 0, 0, -1};
-  for (int e = threadIdx.x; e < E; e += blockDim.x) {
-    const size_t tile = (size_t)o * E + e;
-    // the partials are read together with the tile record (entries of tiles
-    // the scorer did not visit are not used)
-    const double *x = partial + tile * n_partial;
-    double v[16];
+  uint64_t kbest = 0, tbest = ~0ull;
+  for (int e0 = lane; e0 < E; e0 += 2 * kWave) {
+    double v[2][16];
+    TileInfo tl[2];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) v[j] = j < n_partial ? x[j] : 0.0;
-    const TileInfo tl = tiles[tile];
-    double sc = 0.0;  // a revealed cell: nothing to learn
-    if (tl.state < 0) {
-      sc = __builtin_nan("");
-    } else if (tl.state == 0) {
-      double sum;
-      if (excl_constant_tile(tl)) {
-        sum = excl_constant_sum(tl, S);
-      } else {
+    for (int u = 0; u < 2; ++u) {
+      // the partials are read together with the tile record (entries of
+      // tiles the scorer did not visit are not used)
+      const int e = e0 + u * kWave;
+      const size_t tile = (size_t)o * E + (e < E ? e : 0);
+      const double *x = partial + tile * n_partial;
 #pragma unroll
-        for (int w = 1; w < 16; w <<= 1) {
-          if (w < p2) {
-#pragma unroll
-            for (int j = 0; j + w < 16; j += 2 * w) v[j] = v[j] + v[j + w];
-          }
-        }
-        sum = v[0];
-      }
-      sc = gap - sum / (double)S;
-      const Pick c{sc, tl.t, tl.cell, e};
-      if (better(c, mine)) mine = c;
+      for (int j = 0; j < 16; ++j) v[u][j] = j < n_partial ? x[j] : 0.0;
+      tl[u] = tiles[tile];
     }
-    score[tile] = sc;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int e = e0 + u * kWave;
+      if (e >= E) continue;
+      double sc = 0.0;  // a revealed cell: nothing to learn
+      if (tl[u].state < 0) {
+        sc = __builtin_nan("");
+      } else if (tl[u].state == 0) {
+        double sum;
+        if (excl_constant_tile(tl[u])) {
+          sum = excl_constant_sum(tl[u], S);
+        } else {
+#pragma unroll
+          for (int w = 1; w < 16; w <<= 1) {
+            if (w < p2) {
+#pragma unroll
+              for (int j = 0; j + w < 16; j += 2 * w) v[u][j] = v[u][j] + v[u][j + w];
+            }
+          }
+          sum = v[u][0];
+        }
+        sc = gap - sum / (double)S;
+        const uint64_t k = score_key(sc), t = tie_key(tl[u].t, tl[u].cell, e);
+        if (k > kbest || (k == kbest && t < tbest)) {
+          kbest = k;
+          tbest = t;
+        }
+      }
+      score[(size_t)o * E + e] = sc;
+    }
   }
-  mine = wave_best(mine);
-  if ((threadIdx.x & 63) == 0) s_pick[threadIdx.x >> 6] = mine;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    for (int w = 1; w < (int)(blockDim.x >> 6); ++w)
-      if (better(s_pick[w], mine)) mine = s_pick[w];
-    if (best) best[o] = mine.e;
+  const uint64_t kmax = wave_ext_u64<true>(kbest);
+  const uint64_t tmin = wave_ext_u64<false>(kbest == kmax ? tbest : ~0ull);
+  if (lane == 0) {
+    if (best) best[o] = kmax != 0 ? (int32_t)(uint32_t)tmin : -1;
     if (gap_now) gap_now[o] = gap;
   }
 }
@@ -3221,7 +3292,7 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
     }
     if (a.ev_end) (void)hipEventRecord(a.ev_end, s);
     if (n_partial <= 16) {
-      k_finalize_excl<<<a.O, 256, 0, s>>>(tiles, a.E, a.S, base, partial, n_partial, a.score, a.gap_now,
+      k_finalize_excl<<<a.O, kWave, 0, s>>>(tiles, a.E, a.S, base, partial, n_partial, a.score, a.gap_now,
                                           a.best);
     } else {
       k_tile_scores_wave<<<dim3((a.E + 3) / 4, a.O), 256, 0, s>>>(tiles, a.E, a.S, base, partial, n_partial,
