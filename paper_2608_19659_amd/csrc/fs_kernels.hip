@@ -1844,12 +1844,18 @@ __global__ __launch_bounds__(64) void k_score_excl(
     }
     const double rcp = c_rcp[cls];
     const float slo = c_slo[cls];
-    // the accumulators start at U: tau = max(U, best over the range)
+    // the accumulators start at U: tau = max(U, best over the range).  A
+    // sampled tail above the SLO makes every option on the cell worth 0,
+    // leaving tau = U: the sample's capacity is taken as 0 instead, whose
+    // ratios (0) and crossings (M <= 0 where reached) cannot raise tau
+    // above U >= 0.
     int am[SPL], ap[SPL];
+    float cs[SPL];
 #pragma unroll
     for (int q = 0; q < SPL; ++q) {
       am[q] = X.u0;
       ap[q] = X.u1;
+      cs[q] = X.ls[q] <= slo ? X.cs[q] : 0.0f;
     }
     if (nr <= kScanMax) {
       // pairs of replica counts, then a single one when nr is odd
@@ -1863,8 +1869,8 @@ __global__ __launch_bounds__(64) void k_score_excl(
           const float r1 = (float)(rlo + j), r2 = (float)(rlo + j + 1);
 #pragma unroll
           for (int q = 0; q < SPL; ++q) {
-            const int f1 = sampled_quotient(r1, X.cs[q], rcp);
-            const int f2 = sampled_quotient(r2, X.cs[q], rcp);
+            const int f1 = sampled_quotient(r1, cs[q], rcp);
+            const int f2 = sampled_quotient(r2, cs[q], rcp);
             am[q] = max(am[q], max(min(f1, mm0), min(f2, mm1)));
             ap[q] = max(ap[q], max(min(f1, mp0), min(f2, mp1)));
           }
@@ -1873,7 +1879,7 @@ __global__ __launch_bounds__(64) void k_score_excl(
           const float r1 = (float)(rlo + j);
 #pragma unroll
           for (int q = 0; q < SPL; ++q) {
-            const int f1 = sampled_quotient(r1, X.cs[q], rcp);
+            const int f1 = sampled_quotient(r1, cs[q], rcp);
             am[q] = max(am[q], min(f1, mm0));
             ap[q] = max(ap[q], min(f1, mp0));
           }
@@ -1918,7 +1924,7 @@ __global__ __launch_bounds__(64) void k_score_excl(
           for (int q = 0; q < SPL; ++q) {
 #pragma unroll
             for (int side = 0; side < 2; ++side)
-              pb[q][side] += !(X.cs[q] >= __int_as_float(th[q][side])) ? 4 * stp : 0;
+              pb[q][side] += !(cs[q] >= __int_as_float(th[q][side])) ? 4 * stp : 0;
           }
         }
         // tau candidate: max(f of the replica count below the crossing,
@@ -1935,8 +1941,8 @@ __global__ __launch_bounds__(64) void k_score_excl(
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int q = 0; q < SPL; ++q) {
-          const int fm = sampled_quotient(__int_as_float(rj[q][0]), X.cs[q], rcp);
-          const int fp = sampled_quotient(__int_as_float(rj[q][1]), X.cs[q], rcp);
+          const int fm = sampled_quotient(__int_as_float(rj[q][0]), cs[q], rcp);
+          const int fp = sampled_quotient(__int_as_float(rj[q][1]), cs[q], rcp);
           am[q] = max(am[q], max(fm, mj[q][0]));
           ap[q] = max(ap[q], max(fp, mj[q][1]));
         }
@@ -1970,7 +1976,7 @@ __global__ __launch_bounds__(64) void k_score_excl(
 #pragma unroll
             for (int side = 0; side < 2; ++side) {
               const int idx = pos[q][side] + stp - 1;
-              const bool below = !(X.cs[q] >= th[q][side]);
+              const bool below = !(cs[q] >= th[q][side]);
               pos[q][side] += (idx < nr && below) ? stp : 0;
             }
           }
@@ -1987,7 +1993,7 @@ __global__ __launch_bounds__(64) void k_score_excl(
 #pragma unroll
           for (int side = 0; side < 2; ++side) {
             const int j = pos[q][side];
-            const int fprev = sampled_ratio((float)(rlo + j - 1), X.cs[q], rcp);
+            const int fprev = sampled_ratio((float)(rlo + j - 1), cs[q], rcp);
             const int v = max(j > 0 ? fprev : INT_MIN, j < nr ? mj[q][side] : INT_MIN);
             if (side == 0) am[q] = max(am[q], v);
             else ap[q] = max(ap[q], v);
@@ -1996,16 +2002,13 @@ __global__ __launch_bounds__(64) void k_score_excl(
       }
     }
     double gq[SPL];
-    // a sampled tail above the SLO makes every option on the cell worth 0,
-    // leaving tau = U; samples past S add 0 (the chunk holds none of them
-    // unless it is the tile's last and S is not a multiple of its size)
+    // samples past S add 0 (the chunk holds none of them unless it is the
+    // tile's last and S is not a multiple of its size)
     const bool full = (p.c + 1) * CHUNK <= S;
     if (full) {
 #pragma unroll
       for (int q = 0; q < SPL; ++q) {
-        const bool tail_ok = X.ls[q] <= slo;
-        const int tm = tail_ok ? am[q] : X.u0;
-        const int tp = tail_ok ? ap[q] : X.u1;
+        const int tm = am[q], tp = ap[q];
         gq[q] = (double)__int_as_float(tp) - (double)__int_as_float(tm);
         if (DUMP) {
           tau_dump[(tile * S + s_first + q) * 2 + 0] = __int_as_float(tm);
@@ -2015,9 +2018,7 @@ __global__ __launch_bounds__(64) void k_score_excl(
     } else {
 #pragma unroll
       for (int q = 0; q < SPL; ++q) {
-        const bool tail_ok = X.ls[q] <= slo;
-        const int tm = tail_ok ? am[q] : X.u0;
-        const int tp = tail_ok ? ap[q] : X.u1;
+        const int tm = am[q], tp = ap[q];
         const bool live = s_first + q < S;
         gq[q] = live ? (double)__int_as_float(tp) - (double)__int_as_float(tm) : 0.0;
         if (DUMP && live) {
