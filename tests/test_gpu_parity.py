@@ -386,6 +386,32 @@ def test_single_class_problem(env, orc, kernel):
     assert_scores_equal(g, orc.score(p, iv, cand, cs, ts))
 
 
+@pytest.mark.parametrize("budget", [62, 63, 64, 65, 128])
+@pytest.mark.parametrize("dump", [True, False])
+def test_exclusion_range_length_boundaries(env, orc, budget, dump):
+    """One load level holds every replica count, so the TP-1 cells' replica
+    ranges are the whole budget: 62 and 63 options take the exclusion
+    scorer's cross-lane search, 64 and more its LDS-staged search; the TP-2
+    cells' ranges (budget / 2) take the cross-lane search, and those of TP
+    16 and 32 (1 to 8 counts) the scan, odd lengths included."""
+    p = Problem(tp=[1, 2, 16, 32], levels=[20.0], demand=[3.0, 5.0], slo=[30.0, 25.0], budget=budget)
+    rng = np.random.default_rng(budget)
+    N, O, S = p.n_cells, 4, 300
+    # capacities put the crossing inside the TP-1 range (r * c / demand near
+    # the other class's best ratio for r around budget / 2); tails below the SLO
+    lo = (np.rint(rng.uniform(0.04, 0.2, (O, N)) * 1024) / 1024 * (64.0 / budget)).astype(np.float32)
+    hi = (lo * np.float32(1.5)).astype(np.float32)
+    tl = rng.uniform(5, 15, (O, N)).astype(np.float32)
+    th = (tl * 1.2).astype(np.float32)
+    iv = Intervals(lo, hi, tl, th, np.zeros((O, N), np.uint8))
+    cand = np.arange(N, dtype=np.int32)
+    cs = (lo[:, :, None] + (hi - lo)[:, :, None] * rng.uniform(0, 1, (O, N, S))).astype(np.float32)
+    ts = (tl[:, :, None] + (th - tl)[:, :, None] * rng.uniform(0, 1, (O, N, S))).astype(np.float32)
+    note(f"range boundaries budget {budget} dump {dump}")
+    g = gpu_score(env, p, iv, cand, cs, ts, kernel=3, dump=dump)
+    assert_scores_equal(g, orc.score(p, iv, cand, cs, ts))
+
+
 def test_kernels_agree_and_are_deterministic(env, orc):
     w = make_workload("paper-shaped-2class-G16", orders=[4, 9, 20])
     note("determinism")
