@@ -1383,12 +1383,14 @@ __device__ void prep_list_staged(const DevProblem &P, int O, const uint8_t *__re
       if (code == -2) continue;
       const int nr = code >> 16, b = range_bucket(nr);
       // the thread's orders o = sub, sub + g, ..., their revealed flags read
-      // eight at a time (the reads of a batch overlap)
+      // eight at a time: unconditional reads at clamped orders (an order
+      // past O counts as revealed), so the reads of a batch overlap
       auto flags = [&](int o0, uint8_t (&mv)[8]) {
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
           const int o = o0 + u * g;
-          mv[u] = o < O ? meas[o * N + cell] : 1;
+          const uint8_t f = meas[min(o, O - 1) * N + cell];
+          mv[u] = o < O ? f : 1;
         }
       };
       int n = 0;
@@ -1594,17 +1596,23 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
           first = in ? ofr[t2] : first;
           t = in ? tpr[t2] : t;
         }
+        // every read below is at a valid index whether or not the option
+        // exists (r = 1 past the last option; level 0 for an option with no
+        // level), so the reads are unconditional and overlap
         has[u] = p < PPc;
         const int r = has[u] ? p - first + 1 : 1;
-        const int b = has[u] ? lvl[i * G + r - 1] : -1;
+        const int bl = lvl[i * G + r - 1];
+        const int b = has[u] ? bl : -1;
         ok[u] = b >= 0;
         const int local = ti * B + (ok[u] ? b : 0), cell = i * per_class + local;
+        const int hv = H[G - t * r];
+        const float cc = ccap[cell], ct = ctail[cell];
         // ratios never exceed 1, so M above 1 acts as 1 (min(f, M) and the
         // crossing are unchanged) and the scorer can skip the clamp of f
         rr[u] = r;
         loc[u] = local;
-        Mv[u] = ok[u] ? min(H[G - t * r], __float_as_int(1.0f)) : INT_MIN;
-        fv[u] = ok[u] ? ratio_bits(ccap[cell], ctail[cell], r, slo, rcp) : 0;
+        Mv[u] = ok[u] ? min(hv, __float_as_int(1.0f)) : INT_MIN;
+        fv[u] = ok[u] ? ratio_bits(cc, ct, r, slo, rcp) : 0;
       }
       float Tv[2];
 #pragma unroll
@@ -1642,19 +1650,23 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
   const int wm2 = wave_max_dpp(m2);
   for (int e = lane; e < E; e += kWave) {
     const int cell = ccand[e];
-    if (cell < 0 || cell >= N || cell / per_class != i) continue;
+    const bool mine = cell >= 0 && cell < N && cell / per_class == i;
+    // the reads use a valid cell of class i for every candidate (so they
+    // are unconditional and overlap); other candidates' values are unused
+    const int local = mine ? cell - i * per_class : 0;
+    const int ti = local / B;
+    const int t = c_tp[ti], first = c_optoff[ti];
+    const int lo = crlo[local], hi = crhi[local];
+    const uint8_t rev = mrow[i * per_class + local];
+    if (!mine) continue;
     TileInfo *tl = tiles + (size_t)o * E + e;
-    const int local = cell - i * per_class;
     const int u = max(0, local == wc1 ? wm2 : wm1);
     if (R == 0) {
-      const int ti = local / B;
-      const int t = c_tp[ti], first = c_optoff[ti];
-      const int lo = crlo[local], hi = crhi[local];
       const int nr = hi >= lo ? hi - lo + 1 : 0;
       tl->cls = i; tl->t = t; tl->cell = cell;
       tl->rlo = nr > 0 ? lo : 1;
       tl->rhi = nr > 0 ? hi : 0;
-      tl->state = mrow[cell] ? 1 : 0;
+      tl->state = rev ? 1 : 0;
       tl->toff = i * PPc + first + (nr > 0 ? lo : 1) - 1;
       tl->u_m = u;
     } else {
