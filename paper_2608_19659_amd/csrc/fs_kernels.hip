@@ -1856,19 +1856,17 @@ __global__ __launch_bounds__(64) void k_score_excl(
     }
     const double rcp = c_rcp[cls];
     const float slo = c_slo[cls];
-    // the accumulators start at U: tau = max(U, best over the range).  A
-    // sampled tail above the SLO makes every option on the cell worth 0,
-    // leaving tau = U: the sample's capacity is taken as 0 instead, whose
-    // ratios (0) and crossings (M <= 0 where reached) cannot raise tau
-    // above U >= 0.
+    // tau = max(U, best over the range): U (uniform, in scalar registers)
+    // enters the accumulators with their first update -- every path below
+    // writes each accumulator (a listed tile has nr >= 1).  A sampled tail
+    // above the SLO makes every option on the cell worth 0, leaving tau = U:
+    // the sample's capacity is taken as 0 instead, whose ratios (0) and
+    // crossings (M <= 0 where reached) cannot raise tau above U >= 0.
+    const int u0 = __builtin_amdgcn_readfirstlane(X.u0), u1 = __builtin_amdgcn_readfirstlane(X.u1);
     int am[SPL], ap[SPL];
     float cs[SPL];
 #pragma unroll
-    for (int q = 0; q < SPL; ++q) {
-      am[q] = X.u0;
-      ap[q] = X.u1;
-      cs[q] = X.ls[q] <= slo ? X.cs[q] : 0.0f;
-    }
+    for (int q = 0; q < SPL; ++q) cs[q] = X.ls[q] <= slo ? X.cs[q] : 0.0f;
     if (nr <= kScanMax) {
       // pairs of replica counts, then a single one when nr is odd
 #pragma unroll
@@ -1883,8 +1881,8 @@ __global__ __launch_bounds__(64) void k_score_excl(
           for (int q = 0; q < SPL; ++q) {
             const int f1 = sampled_quotient(r1, cs[q], rcp);
             const int f2 = sampled_quotient(r2, cs[q], rcp);
-            am[q] = max(am[q], max(min(f1, mm0), min(f2, mm1)));
-            ap[q] = max(ap[q], max(min(f1, mp0), min(f2, mp1)));
+            am[q] = max(j == 0 ? u0 : am[q], max(min(f1, mm0), min(f2, mm1)));
+            ap[q] = max(j == 0 ? u1 : ap[q], max(min(f1, mp0), min(f2, mp1)));
           }
         } else if (j < nr) {
           const int mm0 = __builtin_amdgcn_readlane(X.vm0, j), mp0 = __builtin_amdgcn_readlane(X.vm1, j);
@@ -1892,8 +1890,8 @@ __global__ __launch_bounds__(64) void k_score_excl(
 #pragma unroll
           for (int q = 0; q < SPL; ++q) {
             const int f1 = sampled_quotient(r1, cs[q], rcp);
-            am[q] = max(am[q], min(f1, mm0));
-            ap[q] = max(ap[q], min(f1, mp0));
+            am[q] = max(j == 0 ? u0 : am[q], min(f1, mm0));
+            ap[q] = max(j == 0 ? u1 : ap[q], min(f1, mp0));
           }
         }
       }
@@ -1920,10 +1918,18 @@ __global__ __launch_bounds__(64) void k_score_excl(
         const int m0 = in_range ? X.vm0 : INT_MIN;
         const int m1 = in_range ? X.vm1 : INT_MIN;
         const int rb = __float_as_int(lane == 0 ? 0.0f : (float)(rlo + lane - 1));
+        // the first step probes one lane for every search (pos = 0): a
+        // uniform threshold, read into a scalar register
+        const int stp0 = 1 << (steps - 1);
+        const float f0m = __int_as_float(__builtin_amdgcn_readlane(t0, stp0 - 1));
+        const float f0p = __int_as_float(__builtin_amdgcn_readlane(t1, stp0 - 1));
         int pb[SPL][2];
 #pragma unroll
-        for (int q = 0; q < SPL; ++q) pb[q][0] = pb[q][1] = 0;
-        for (int stp = 1 << (steps - 1); stp > 0; stp >>= 1) {
+        for (int q = 0; q < SPL; ++q) {
+          pb[q][0] = !(cs[q] >= f0m) ? 4 * stp0 : 0;
+          pb[q][1] = !(cs[q] >= f0p) ? 4 * stp0 : 0;
+        }
+        for (int stp = stp0 >> 1; stp > 0; stp >>= 1) {
           const int off = 4 * (stp - 1);
           int th[SPL][2];
 #pragma unroll
@@ -1955,8 +1961,8 @@ __global__ __launch_bounds__(64) void k_score_excl(
         for (int q = 0; q < SPL; ++q) {
           const int fm = sampled_quotient(__int_as_float(rj[q][0]), cs[q], rcp);
           const int fp = sampled_quotient(__int_as_float(rj[q][1]), cs[q], rcp);
-          am[q] = max(am[q], max(fm, mj[q][0]));
-          ap[q] = max(ap[q], max(fp, mj[q][1]));
+          am[q] = max(u0, max(fm, mj[q][0]));
+          ap[q] = max(u1, max(fp, mj[q][1]));
         }
       } else {
         // a range of a wavefront's length or more: M and the thresholds go
@@ -2007,8 +2013,8 @@ __global__ __launch_bounds__(64) void k_score_excl(
             const int j = pos[q][side];
             const int fprev = sampled_ratio((float)(rlo + j - 1), cs[q], rcp);
             const int v = max(j > 0 ? fprev : INT_MIN, j < nr ? mj[q][side] : INT_MIN);
-            if (side == 0) am[q] = max(am[q], v);
-            else ap[q] = max(ap[q], v);
+            if (side == 0) am[q] = max(u0, v);
+            else ap[q] = max(u1, v);
           }
         }
       }
