@@ -1293,7 +1293,8 @@ constexpr int kPrepOrderMaxK = 16;
 // order (extra wavefronts make its barriers slower, so small lists keep K).
 static int prep_order_waves(const DevProblem &P, int64_t O, int64_t E) {
   const int64_t by_list = (O * E + 1023) / 1024;
-  const int64_t w = by_list > P.K ? by_list : P.K;
+  const int64_t by_class = 2 * P.K <= 16 ? 2 * P.K : P.K;
+  const int64_t w = by_list > by_class ? by_list : by_class;
   return (int)(w < 16 ? w : 16);
 }
 
@@ -1459,8 +1460,9 @@ __device__ void prep_list_staged(const DevProblem &P, int O, const uint8_t *__re
 // Tables cover g in [0, G) (option costs t r >= 1 read H at G - t r < G).
 //
 // LDS of a class block: cells (2N floats), the B tables (K x G), the
-// candidates (E), per wavefront 2G + 3 NT B ints (convolution buffers, cell
-// maxima, replica ranges), the order's revealed flags (N bytes, padded to 4)
+// candidates (E), per class wavefront (two per class when K <= 8) 2G + 3 NT B
+// ints (convolution buffers, cell maxima, replica ranges), the order's
+// revealed flags (N bytes, padded to 4)
 // and the load levels (K x G bytes).
 __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *__restrict__ cap_lo,
                                                      const float *__restrict__ cap_hi,
@@ -1487,8 +1489,11 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
   int *Bt = reinterpret_cast<int *>(ctail + N);  // [K][G]
   int *ccand = Bt + K * G;                       // [E]
   const int wstride = 2 * G + 3 * per_class;
-  int *wbase = ccand + E;                        // [K][wstride]
-  uint8_t *mrow = reinterpret_cast<uint8_t *>(wbase + K * wstride);  // [N]
+  // per-wavefront areas: one per class, two when a second wavefront per
+  // class computes the thresholds (at most 8 classes)
+  const int nwa = (int)(blockDim.x >> 6) >= 2 * K ? 2 * K : K;
+  int *wbase = ccand + E;                        // [nwa][wstride]
+  uint8_t *mrow = reinterpret_cast<uint8_t *>(wbase + nwa * wstride);  // [N]
   int8_t *lvl = reinterpret_cast<int8_t *>(mrow + ((N + 3) & ~3));   // [K][G]
   int *Xa = wbase + wave * wstride, *Xb = Xa + G;
   int *mc = Xb + G, *crlo = mc + per_class, *crhi = crlo + per_class;
@@ -1551,9 +1556,15 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
   }
   __syncthreads();
 
-  // --- 3. wavefront i on its own from here
-  if (wave >= K) return;
-  const int i = wave;
+  // --- 3. wavefront i on its own from here.  With at most 8 classes a
+  // second wavefront per class (K + i) computes the same H_i and only the
+  // capacity thresholds, which nothing else in the block needs, so the
+  // first one goes on to U and the records without them.
+  const bool split = (int)(blockDim.x >> 6) >= 2 * K;
+  if (wave >= (split ? 2 * K : K)) return;
+  const bool thr_wave = wave >= K;
+  const bool do_thr = !split || thr_wave, do_cells = !split || !thr_wave;
+  const int i = thr_wave ? wave - K : wave;
   int top = 1;
   while (2 * top <= G) top <<= 1;  // 2 * top > G >= g + 1
   const int *H;
@@ -1614,23 +1625,28 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
         Mv[u] = ok[u] ? min(hv, __float_as_int(1.0f)) : INT_MIN;
         fv[u] = ok[u] ? ratio_bits(cc, ct, r, slo, rcp) : 0;
       }
-      float Tv[2];
+      float Tv[2] = {0.0f, 0.0f};
+      if (do_thr) {
 #pragma unroll
-      for (int u = 0; u < 2; ++u) Tv[u] = ok[u] ? capacity_threshold(rr[u], Mv[u], demand, rcp) : __builtin_nanf("");
+        for (int u = 0; u < 2; ++u) Tv[u] = ok[u] ? capacity_threshold(rr[u], Mv[u], demand, rcp) : __builtin_nanf("");
+      }
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         if (!has[u]) continue;
         const int p = base + lane + u * kWave;
-        if (ok[u]) {
+        if (do_cells && ok[u]) {
           atomicMax(&mc[loc[u]], min(fv[u], Mv[u]));
           atomicMin(&crlo[loc[u]], rr[u]);
           atomicMax(&crhi[loc[u]], rr[u]);
         }
-        Mo[p] = Mv[u];
-        To[p] = Tv[u];
+        if (do_thr) {
+          Mo[p] = Mv[u];
+          To[p] = Tv[u];
+        }
       }
     }
   }
+  if (!do_cells) return;  // the threshold wavefront is done
   wave_lds_fence();
   // U of a cell is the largest maximum among the class's other cells (or 0):
   // the largest maximum m1 at its lowest index c1, and the largest m2 over
@@ -3190,7 +3206,8 @@ static size_t prep_lds_tables(const DevProblem &P) { return 3 * sizeof(int) * (s
 // the work-list block's.
 static size_t prep_order_lds(const DevProblem &P, int64_t O, int64_t E) {
   const size_t K = P.K, G = P.G, N = P.N, pc = (size_t)P.NT * P.B;
-  const size_t cls = 4 * (2 * N + K * G + (size_t)E + K * (2 * G + 3 * pc)) + ((N + 3) & ~(size_t)3) + K * G;
+  const size_t nw = 2 * K <= 16 ? 2 * K : K;  // wavefronts with a per-wavefront area
+  const size_t cls = 4 * (2 * N + K * G + (size_t)E + nw * (2 * G + 3 * pc)) + ((N + 3) & ~(size_t)3) + K * G;
   const size_t lst = 4 * (68 + 2 * K * (size_t)P.B + 2 * (size_t)E) + (size_t)O * N;
   return cls > lst ? cls : lst;
 }
