@@ -3,16 +3,24 @@
 
 A step is one fs_score_candidates call over the whole batch of the 4-class
 workload (TP {1,2,4,8}, G = 64 GPUs, 8 load levels, 128 candidate cells x
-4096 sampled outcomes x 16 reveal orders): base solves of every order, every
-scenario of every unmeasured candidate (two allocation solves each), scores
-and the argmax.  Inputs are synthetic (seeded) and resident in HBM before
-timing starts.
+4096 sampled outcomes x 16 reveal orders): per-order set-up (base solves and
+the all-but-one tables), every scenario of every unmeasured candidate (two
+allocation solves each), scores and the argmax.  Inputs are synthetic
+(seeded) and resident in HBM before timing starts.
+
+Two passes are timed: "warm" repeats the step on one copy of the samples
+(which then sit in the 256 MB Infinity Cache), "cold" rotates the step over
+enough copies of the samples that each step reads them from HBM.  The
+headline value is the cold step throughput.
 
 Prints one JSON line.  The roofline object reports the dominant kernel (the
-per-scenario solve) against the VALU issue peak; its duration is measured
-with HIP events recorded by the library on the same stream.  The CPU
-baseline is the plain oracle timed on a bounded sample of the same
-workload's tiles.
+per-scenario scorer) against the HBM bandwidth peak (the binding roofline of
+its work model): achieved = the algorithmic bytes per launch over the
+kernel's mean launch duration, measured with HIP events the library records
+on its stream; step_frac is the same bytes over the whole step.  After
+timing, the outputs of the timed steps are compared with the oracle's on
+the tiles its CPU baseline solved (bit for bit); a mismatch exits with
+status 1.
 """
 from __future__ import annotations
 
@@ -101,31 +109,92 @@ def committed_traffic(kernel: str, workload_tag: str):
     return float(m.group(1))
 
 
-def cpu_baseline(w, target_seconds: float, threads: int):
-    """The oracle, as is, on a bounded sample of the workload's tiles."""
-    import numpy as np
+def host_info() -> dict:
+    """The host the CPU baseline runs on: logical CPUs, the CPUs this
+    process may use, and the CPU model."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        allowed = len(os.sched_getaffinity(0))
+    except AttributeError:
+        allowed = os.cpu_count()
+    return {"nproc": os.cpu_count(), "cpus_allowed": allowed, "cpu_model": model}
+
+
+def baseline_threads() -> int:
+    """Oracle threads: the CPUs this process may use, at most 16 (a GPU's
+    share of the host on the GPU pool, whatever the host's CPU count)."""
+    return max(1, min(host_info()["cpus_allowed"] or 1, 16))
+
+
+def sha256_arrays(*arrays) -> str:
+    h = hashlib.sha256()
+    for a in arrays:
+        import numpy as np
+        h.update(np.ascontiguousarray(a).tobytes())
+    return h.hexdigest()
+
+
+def cpu_baseline(w, target_seconds: float, threads: int, seed: int = 1234):
+    """The oracle, as is, on a seeded sample of the workload's unmeasured
+    (order, candidate) tiles sized for about target_seconds on `threads`
+    OpenMP threads (every tile when they all fit), and on one thread for a
+    quarter of that.  Returns the record and the multi-thread run's result
+    and tile mask, for the parity check."""
     import oracle
+    from paper_2608_19659_amd.synth import seeded_tiles, tile_mask
     O, E, S = w.cap_s.shape
-    unmeasured = [(o, e) for o in range(O) for e in range(E) if not w.intervals.measured[o, w.cand[e]]]
-    rng = np.random.default_rng(1234)
-    order = rng.permutation(len(unmeasured))
+    n_live = int((~w.intervals.measured[:, w.cand].astype(bool)).sum())
 
     def run(n_tiles, n_threads):
-        mask = np.zeros((O, E), np.uint8)
-        for j in order[:n_tiles]:
-            mask[unmeasured[j]] = 1
+        mask = tile_mask(w, seeded_tiles(w, n_tiles, seed))
         t0 = time.perf_counter()
-        oracle.score(w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, tile_mask=mask, dump=False,
-                     n_threads=n_threads)
-        return time.perf_counter() - t0
+        res = oracle.score(w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, tile_mask=mask, dump=False,
+                           n_threads=n_threads)
+        return time.perf_counter() - t0, res, mask
 
     probe = max(threads, 1)
-    dt = run(probe, threads)
-    n_tiles = int(min(len(unmeasured), max(probe, probe * target_seconds / max(dt, 1e-3))))
-    dt = run(n_tiles, threads)
-    return {"value": n_tiles * S / dt, "unit": "scenarios/s", "cores": threads, "kind": "oracle",
-            "sample": f"{n_tiles} unmeasured (order, candidate) tiles x {S} samples of the benchmark "
-                      f"workload, {threads} OpenMP threads, {dt:.1f} s wall"}
+    dt, _, _ = run(probe, threads)
+    n_tiles = int(min(n_live, max(probe, probe * target_seconds / max(dt, 1e-3))))
+    dt, res, mask = run(n_tiles, threads)
+    # one thread, sized for a quarter of the budget
+    dt1, _, _ = run(1, 1)
+    n1 = int(min(n_live, max(1, 0.25 * target_seconds / max(dt1, 1e-3))))
+    dt1, _, _ = run(n1, 1)
+    rec = {"value": n_tiles * S / dt, "unit": "scenarios/s", "cores": threads, "kind": "oracle",
+           "sample": f"{n_tiles} of the {n_live} unmeasured (order, candidate) tiles x {S} samples of the "
+                     f"benchmark workload (seeded), {threads} OpenMP threads, {dt:.1f} s wall",
+           "one_core": {"value": n1 * S / dt1, "unit": "scenarios/s",
+                        "sample": f"{n1} tiles x {S} samples, 1 thread, {dt1:.1f} s wall"},
+           **host_info()}
+    return rec, res, mask
+
+
+def parity_check(w, out, o_res, mask) -> dict:
+    """The timed steps' outputs against the oracle on the tiles it solved:
+    scores of those tiles and every order's gap bit for bit, and the best
+    candidate of every order whose unmeasured tiles were all solved."""
+    import numpy as np
+    score = out.score.cpu().numpy()
+    gap = out.gap_now.cpu().numpy()
+    best = out.best.cpu().numpy()
+    m = mask.astype(bool)
+    meas = w.intervals.measured[:, w.cand].astype(bool)
+    ok_score = bool(np.array_equal(score[m].view(np.uint64), o_res.score[m].view(np.uint64)))
+    ok_gap = bool(np.array_equal(gap.view(np.uint64), o_res.gap_now.view(np.uint64)))
+    full_orders = [o for o in range(m.shape[0]) if np.all(m[o] | meas[o])]
+    ok_best = all(int(best[o]) == int(o_res.best[o]) for o in full_orders)
+    S = w.cap_s.shape[2]
+    return {"tiles": int(m.sum()), "scenarios": int(m.sum()) * S, "orders_best_checked": len(full_orders),
+            "scores_bit_exact": ok_score, "gaps_bit_exact": ok_gap, "best_equal": ok_best,
+            "bit_exact": ok_score and ok_gap and ok_best}
 
 
 def replica_range_sizes(problem, cand):
@@ -256,7 +325,7 @@ def loop_bench(args):
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
-        threads = min(os.cpu_count() or 1, 16)
+        threads = baseline_threads()
 
         # one trajectory at a time until about 10 s have passed
         dt, n, same = 0.0, 0, True
@@ -386,7 +455,7 @@ def policy_bench(args):
     achieved = n_samples * bytes_per_sample / (red_ms / 1e3)
     cpu = None
     if not args.no_cpu_baseline:
-        threads = min(os.cpu_count() or 1, 16)
+        threads = baseline_threads()
         print(f"[bench] cpu baseline ({threads} threads)", file=sys.stderr, flush=True)
         t0 = time.perf_counter()
         oracle.feasible_samples(p, o_pol, w.cand, pi.tail_s, pi.succ_s)
@@ -394,7 +463,7 @@ def policy_bench(args):
         w2 = SimpleNamespace(problem=p0, intervals=Intervals(w.intervals.cap_lo, w.intervals.cap_hi, o_iv.tail_lo,
                                                              o_iv.tail_hi, w.intervals.measured),
                              cand=w.cand, cap_s=w.cap_s, tail_s=o_ts)
-        cpu = cpu_baseline(w2, args.cpu_seconds, threads)
+        cpu, _, _ = cpu_baseline(w2, args.cpu_seconds, threads)
         cpu["sample"] += f"; the oracle's sample reduction over all {n_samples} samples took {t_red:.2f} s"
     line = {
         "metric": "allocation scenarios/sec under multi-metric class policies (Eq. 5) on 1 MI355X; oracle-exact",
@@ -569,6 +638,11 @@ def main():
     ap.add_argument("--lex-scenarios", type=int, default=65536, help="realisations per --lex step")
     ap.add_argument("--lex-score-samples", type=int, default=64,
                     help="samples per candidate for the stage-wise score timed by --lex")
+    ap.add_argument("--cold-copies", type=int, default=-1,
+                    help="sample copies the cold pass rotates over (-1: enough to exceed the Infinity Cache "
+                         "three times; 0 or 1: no cold pass)")
+    ap.add_argument("--warm-headline", action="store_true",
+                    help="report the warm pass (one sample copy, cached) as the headline instead of the cold one")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (scales the HBM byte counters)")
     args = ap.parse_args()
@@ -627,89 +701,128 @@ def main():
     measured_cand = w.intervals.measured[:, w.cand].astype(bool)
     live_tiles = [(o, e) for o in range(O) for e in range(E) if not measured_cand[o, e]]
     scenarios = len(live_tiles) * S
+    kernel = args.kernel if args.kernel else (3 if p.floor_rps is None else 1)
+    slots, nbytes, mean_ne, sampled = excl_work(p, w.cand, live_tiles, S)
 
-    def run(kernel, steps, warmup):
+    # Copies of the samples for the cold pass: enough that the samples one
+    # rotation reads exceed three times the 256 MB Infinity Cache, within 4 GB.
+    copies = args.cold_copies
+    if copies < 0:
+        copies = int(min(max(2, math.ceil(3 * 256e6 / max(nbytes, 1.0))), max(2, 4e9 // (8.0 * O * E * S))))
+    plans = [fs.ScorePlan(ctx, p, iv, cand, cap_s, tail_s, out=out, workspace=ws, stream=stream)]
+    keep = []
+    for _ in range(max(copies - 1, 0)):
+        c2, t2 = cap_s.clone(), tail_s.clone()
+        keep.append((c2, t2))
+        plans.append(fs.ScorePlan(ctx, p, iv, cand, c2, t2, out=out, workspace=ws, stream=stream))
+    torch.cuda.synchronize()
+
+    def timed(kernel_id, steps, warmup, rotate):
         """Time `steps` whole steps (set-up, scorer, finalize) with no timing
-        markers in the stream; then the same number of steps again, each with
-        TIMING_REPEATS back-to-back launches of the scorer between a pair of
-        HIP events, for the scorer's mean launch duration (an event pair
-        around a single launch would add its own queue work to the span)."""
-        ctx.set_score_kernel(kernel)
+        markers in the stream, rotating over the sample copies when asked;
+        then the same number of steps again with the library's HIP event
+        pair around the scorer: TIMING_REPEATS back-to-back launches per
+        step when warm (an event pair around one launch adds its own queue
+        work to the span), one launch per step when cold (a repeat would
+        read the samples from the cache)."""
+        ctx.set_score_kernel(kernel_id)
         ctx.set_option(fs.OPT_KERNEL_TIMING, 0)
-        plan = fs.ScorePlan(ctx, p, iv, cand, cap_s, tail_s, out=out, workspace=ws, stream=stream)
+        pl = plans if rotate else plans[:1]
         torch.cuda.synchronize()
-        for _ in range(warmup):
-            plan.run()
+        for j in range(warmup):
+            pl[j % len(pl)].run()
         ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         ev0.record(stream)
-        for _ in range(steps):
-            plan.run()
+        for j in range(steps):
+            pl[j % len(pl)].run()
         ev1.record(stream)
         torch.cuda.synchronize()
         ms_per_step = ev0.elapsed_time(ev1) / steps
-        ctx.set_option(fs.OPT_KERNEL_TIMING, TIMING_REPEATS)
+        ctx.set_option(fs.OPT_KERNEL_TIMING, 1 if rotate else TIMING_REPEATS)
         ctx.kernel_timing()  # nothing pending
-        for _ in range(steps):
-            plan.run()
+        for j in range(steps):
+            pl[j % len(pl)].run()
         torch.cuda.synchronize()
         kernel_ms, launches = ctx.kernel_timing()
         ctx.set_option(fs.OPT_KERNEL_TIMING, 0)
         return ms_per_step, kernel_ms / max(launches, 1), launches
 
-    lane_ok = p.floor_rps is None and [int(x) for x in p.tp] == [1, 2, 4, 8] and p.budget in (16, 32, 64)
-    kernel = args.kernel if args.kernel else (3 if p.floor_rps is None else 1)
-    print(f"[bench] kernel {kernel}: warmup {args.warmup}, timing {args.steps} steps", file=sys.stderr, flush=True)
-    ms_per_step, kernel_ms, launches = run(kernel, args.steps, args.warmup)
+    print(f"[bench] kernel {kernel}: warmup {args.warmup}, {args.steps} warm steps, {args.steps} cold steps over "
+          f"{copies} sample copies", file=sys.stderr, flush=True)
+    ms_warm, kms_warm, n_warm = timed(kernel, args.steps, args.warmup, False)
+    cold = None
+    if copies >= 2:
+        ms_cold, kms_cold, n_cold = timed(kernel, args.steps, args.warmup, True)
+        cold = {"ms_per_step": ms_cold, "value": scenarios / (ms_cold / 1e3), "kernel_ms_avg": kms_cold,
+                "sample_copies": copies, "bytes_per_rotation": nbytes * copies}
+    plans[0].run()  # the outputs checked below come from a step like every timed one
+    torch.cuda.synchronize()
+    headline_cold = cold is not None and not args.warm_headline
+    ms_per_step = cold["ms_per_step"] if headline_cold else ms_warm
+    kernel_ms = cold["kernel_ms_avg"] if headline_cold else kms_warm
     value = scenarios / (ms_per_step / 1e3)
 
-    def roofline_of(kernel_id, kernel_ms_avg):
+    def roofline_of(kernel_id, kernel_ms_avg, step_ms):
         tag = args.workload
         kernel_s = kernel_ms_avg / 1e3
         if kernel_id == 3:
-            slots, nbytes, mean_ne, sampled = excl_work(p, w.cand, live_tiles, S)
             t_alu, t_hbm = slots / VALU_PEAK_OPS, nbytes / HBM_PEAK_BYTES
             name = "k_score_excl"
-            extra = {"mean_replica_range": mean_ne, "scenarios_reading_samples": sampled}
+            extra = {"mean_replica_range": mean_ne, "scenarios_reading_samples": sampled,
+                     "bytes_per_launch": nbytes, "slots_per_launch": slots}
             if t_hbm >= t_alu:
                 achieved = nbytes / kernel_s
                 return dict(bound="hbm", achieved=achieved / 1e9, peak=HBM_PEAK_BYTES / 1e9, unit="GB/s",
                             frac=achieved / HBM_PEAK_BYTES,
                             traffic=committed_traffic("k_score_excl", tag), kernel=name,
+                            step_frac=nbytes / (step_ms / 1e3) / HBM_PEAK_BYTES,
                             bytes_per_scenario=8.0, slots_per_scenario=slots / scenarios,
                             alu_frac=slots / kernel_s / VALU_PEAK_OPS, kernel_ms_avg=kernel_ms_avg,
                             scenarios_per_launch=scenarios, **extra)
             achieved = slots / kernel_s
             return dict(bound="alu", achieved=achieved / 1e12, peak=VALU_PEAK_OPS / 1e12, unit="TOP/s",
                         frac=achieved / VALU_PEAK_OPS, traffic=committed_traffic("k_score_excl", tag),
-                        kernel=name, op="VALU lane-slot", slots_per_scenario=slots / scenarios,
+                        kernel=name, op="VALU lane-slot", step_frac=slots / (step_ms / 1e3) / VALU_PEAK_OPS,
+                        slots_per_scenario=slots / scenarios,
                         hbm_frac=nbytes / kernel_s / HBM_PEAK_BYTES, kernel_ms_avg=kernel_ms_avg,
                         scenarios_per_launch=scenarios, **extra)
         if kernel_id == 2:
             ops = lane_work_per_scenario(p, existing_options(p))
             achieved = ops * scenarios / kernel_s
             return dict(bound="alu", achieved=achieved / 1e12, peak=VALU_PEAK_OPS / 1e12, unit="TOP/s",
-                        frac=achieved / VALU_PEAK_OPS,
+                        frac=achieved / VALU_PEAK_OPS, step_frac=ops * scenarios / (step_ms / 1e3) / VALU_PEAK_OPS,
                         traffic=committed_traffic(f"k_score_lane{p.budget}", tag),
                         kernel=f"k_score_lane<{p.budget}>", op="VALU lane-slot", slots_per_scenario=ops,
                         kernel_ms_avg=kernel_ms_avg, scenarios_per_launch=scenarios)
         return None
 
-    roofline = roofline_of(kernel, kernel_ms) if launches else None
+    launches = n_cold if headline_cold else n_warm
+    roofline = roofline_of(kernel, kernel_ms, ms_per_step) if launches else None
+    if roofline is not None:
+        roofline["measured"] = "cold (sample copies rotated)" if headline_cold else "warm (one sample copy)"
+        warm_r = roofline_of(kernel, kms_warm, ms_warm) if n_warm else None
+        if headline_cold and warm_r is not None:
+            roofline["warm"] = {"frac": warm_r["frac"], "step_frac": warm_r["step_frac"], "kernel_ms_avg": kms_warm}
     kernel_name = {1: "k_score_wave", 2: f"k_score_lane<{p.budget}>", 3: "k_score_excl"}[kernel]
 
+    lane_ok = p.floor_rps is None and [int(x) for x in p.tp] == [1, 2, 4, 8] and p.budget in (16, 32, 64)
     full = None
     if not args.no_full_resolve and kernel != 2 and lane_ok:
         print("[bench] full re-solve kernel (lane per scenario)", file=sys.stderr, flush=True)
-        f_ms, f_kms, f_n = run(2, 5, 2)
+        f_ms, f_kms, f_n = timed(2, 5, 2, False)
         full = {"kernel": f"k_score_lane<{p.budget}>", "value": scenarios / (f_ms / 1e3),
-                "ms_per_step": f_ms, "roofline": roofline_of(2, f_kms) if f_n else None}
+                "ms_per_step": f_ms, "roofline": roofline_of(2, f_kms, f_ms) if f_n else None}
+        ctx.set_score_kernel(kernel)
+        plans[0].run()
+        torch.cuda.synchronize()
 
-    cpu = None
+    cpu = parity = None
     if not args.no_cpu_baseline:
-        threads = min(os.cpu_count() or 1, 16)
-        print(f"[bench] cpu baseline ({threads} threads)", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(w, args.cpu_seconds, threads)
+        threads = baseline_threads()
+        print(f"[bench] cpu baseline ({threads} threads) and parity", file=sys.stderr, flush=True)
+        cpu, o_res, mask = cpu_baseline(w, args.cpu_seconds, threads)
+        parity = parity_check(w, out, o_res, mask)
 
     line = {
         "metric": METRIC, "value": value, "unit": "scenarios/s", "n_gpus": 1, "steps": args.steps,
@@ -721,11 +834,20 @@ def main():
                                f"{O} reveal orders",
                    "scenarios_per_step": scenarios, "scenarios_in_workload": O * E * S,
                    "measured_candidates_skipped": int(measured_cand.sum()) * S,
-                   "kernel": kernel_name, "parallelism": "single GPU"},
-        "roofline": roofline, "cpu_baseline": cpu, "full_resolve": full,
+                   "kernel": kernel_name, "parallelism": "single GPU",
+                   "inputs_sha256": {"cap_s": sha256_arrays(w.cap_s), "tail_s": sha256_arrays(w.tail_s),
+                                     "intervals": sha256_arrays(w.intervals.cap_lo, w.intervals.cap_hi,
+                                                                w.intervals.tail_lo, w.intervals.tail_hi,
+                                                                w.intervals.measured, w.cand)}},
+        "warm": {"ms_per_step": ms_warm, "value": scenarios / (ms_warm / 1e3), "kernel_ms_avg": kms_warm},
+        "cold": cold,
+        "roofline": roofline, "parity": parity, "cpu_baseline": cpu, "full_resolve": full,
     }
     print(json.dumps(line), flush=True)
     ctx.close()
+    if parity is not None and not parity["bit_exact"]:
+        print("[bench] the timed run's outputs differ from the oracle", file=sys.stderr, flush=True)
+        sys.exit(1)
 
 
 if __name__ == "__main__":

@@ -149,7 +149,15 @@ typedef enum fs_option {
    * revealed cells; the certificate and the score use the refitted
    * intervals and the samples clamped into them.  Needs the workspace of
    * fs_loop_refit_workspace_size.  0 (default): no refit. */
-  FS_OPT_LOOP_REFIT = 8
+  FS_OPT_LOOP_REFIT = 8,
+  /* Exclusion scorer set-up: where the search for each option's capacity
+   * threshold (the smallest binary32 capacity at which the option reaches a
+   * given ratio) starts: 0 (default) = a window of eight bit patterns around
+   * the quotient estimate, then stepping, then a bisection over all bit
+   * patterns; 1 = stepping, then bisection; 2 = bisection only.  Every value
+   * gives identical results (a test knob for the later stages, which the
+   * window leaves unused on ordinary inputs). */
+  FS_OPT_THRESHOLD_SEARCH = 9
 } fs_option;
 
 typedef enum fs_objective { FS_OBJECTIVE_MAXMIN = 0, FS_OBJECTIVE_LEXICOGRAPHIC = 1 } fs_objective;
@@ -336,6 +344,19 @@ fs_status fs_reduce_samples(fs_context *ctx, const fs_problem *p, const fs_slo_p
 fs_status fs_refit_intervals(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders,
                              float *d_cap_lo_out, float *d_tail_lo_out, float *d_tail_hi_out, hipStream_t stream);
 
+/* The candidates' samples moved into the candidates' current intervals
+ * (Algorithm 1 refits the intervals every round; samples drawn once inside
+ * the initial intervals are clamped into the refitted ones before scoring):
+ *   cap_out[o][e][s]  = min(max(cap_s[o][e][s], cap_lo[o][c]), cap_hi[o][c]),
+ *   tail_out[o][e][s] = min(max(tail_s[o][e][s], tail_lo[o][c]), tail_hi[o][c]),
+ * with c = cand[e].  Arrays as in fs_score_candidates; each output
+ * [n_orders][n_cand][n_samples] may alias its input.  The samples of a
+ * candidate outside [0, N) are not written.  n_orders and n_cand in
+ * [0, 65535], n_samples in [0, 2^20]. */
+fs_status fs_clamp_samples(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders,
+                           const int32_t *d_cand, int32_t n_cand, const float *d_cap_s, const float *d_tail_s,
+                           int32_t n_samples, float *d_cap_out, float *d_tail_out, hipStream_t stream);
+
 /* Reveal rule of fs_profile_loop. */
 typedef enum fs_policy {
   FS_POLICY_SCORE = 0,  /* the candidate with the largest score (Section 4.3, Algorithm 1) */
@@ -356,8 +377,10 @@ typedef struct fs_loop_out {
   double *gpu_seconds;  /* [O] FS_CELL_SECONDS x TP degree summed over the reveals          */
   int32_t *reveals;     /* [O][max_rounds] candidate revealed in each round, -1 after the
                          * end; or NULL                                                     */
-  fs_alloc final_alloc; /* [O] the returned allocation: the conservative allocation A- of
-                         * the trajectory's last certificate (any field may be NULL)         */
+  fs_alloc final_alloc; /* [O] the returned allocation (any field may be NULL): A- of the
+                         * last certificate when the trajectory certified; otherwise
+                         * Algorithm 1's best measured feasible allocation, the optimum
+                         * of the table with every unmeasured cell infeasible            */
   float *tau_truth;     /* [O] objective level (2) of the returned allocation on the true
                          * table (smallest fulfillment over the classes, an unserved class
                          * counting 0); or NULL                                             */
@@ -380,7 +403,9 @@ fs_status fs_loop_workspace_size(const fs_problem *p, int32_t n_orders, int32_t 
  *   1. the certificate (as fs_certify, tolerance eps);  a certified state
  *      (feasible or infeasible) ends the trajectory and returns A-;
  *   2. if no candidate is left unmeasured, the trajectory ends undecided and
- *      returns A-;
+ *      returns the best measured feasible allocation: the solve (under the
+ *      loop's objective) of its table with every unmeasured cell infeasible
+ *      and every measured cell at its measured values;
  *   3. otherwise one candidate is revealed: under FS_POLICY_SCORE the argmax
  *      of fs_score_candidates on the current intervals (same tie rule),
  *      under FS_POLICY_ORDER the first unmeasured candidate of
@@ -389,7 +414,8 @@ fs_status fs_loop_workspace_size(const fs_problem *p, int32_t n_orders, int32_t 
  *      d_truth_cap[o][cell], d_truth_tail[o][cell] ([n_orders][N]), the cell
  *      becomes measured, and the trajectory is charged FS_CELL_SECONDS x TP.
  * After max_rounds reveals a trajectory gets one more certificate (steps 1-2)
- * and then stops (finished = 0 if still undecided).  The intervals are not
+ * and then stops (finished = 0 if still undecided, returning the best
+ * measured feasible allocation as in step 2).  The intervals are not
  * refitted between rounds: the samples d_cap_s, d_tail_s
  * ([n_orders][n_cand][n_samples], drawn inside the initial intervals) stay
  * valid, since a candidate's intervals change only when it is revealed.

@@ -360,7 +360,7 @@ class LoopResult:
     rounds: np.ndarray       # [O] int32 reveals made
     gpu_seconds: np.ndarray  # [O] float64: CELL_SECONDS x TP summed over the reveals
     reveals: np.ndarray      # [O][max_rounds] int32 candidate revealed in each round, -1 after the end
-    final: list              # [O] Alloc returned (the conservative allocation A-)
+    final: list              # [O] Alloc returned: A- when certified, else the best measured allocation
     tau_truth: np.ndarray    # [O] float32: the returned allocation's objective on the true table
     tau_oracle: np.ndarray   # [O] float32: the optimum of the true table
     regret: np.ndarray       # [O] float64: tau_oracle - tau_truth
@@ -396,8 +396,12 @@ def profile_loop(problem, intervals, truth_cap, truth_tail, cand, cap_s, tail_s,
     revealed candidate is the score's argmax (Section 4.3; POLICY_SCORE) or,
     for the comparison, the first unmeasured one in order[o] (POLICY_ORDER,
     e.g. a uniform random permutation).  A trajectory with no unmeasured
-    candidate left returns A- undecided (the certificate of its final
-    intervals is evaluated first, so a last reveal can still certify).  With
+    candidate left ends undecided (the certificate of its final intervals is
+    evaluated first, so a last reveal can still certify) and returns the best
+    measured feasible allocation (Algorithm 1's last line): the optimum of its
+    table with every unmeasured cell infeasible (tail +inf) and every measured
+    cell at its measured values; so does a trajectory stopped by the round
+    limit.  With
     objective="lex" the certificate and the score are the stage-wise ones
     under the whole objective (certify_lex, score_lex) and A- is that
     objective's allocation.  With
@@ -489,6 +493,14 @@ def profile_loop(problem, intervals, truth_cap, truth_tail, cand, cap_s, tail_s,
             reveals[o, rounds[o]] = e
             rounds[o] += 1
 
+    # A trajectory that ends without a certificate (no unmeasured candidate
+    # left, or the round limit) returns Algorithm 1's "best measured feasible
+    # allocation": the optimum of the table in which every unmeasured cell is
+    # infeasible and every measured cell takes its measured values.
+    for o in range(O):
+        if state[o] == UNDECIDED:
+            masked_tail = np.where(ms[o] != 0, th[o], np.float32(np.inf)).astype(np.float32)
+            final[o] = solve(problem, cl[o], masked_tail, "dp" if objective == "maxmin" else "lex")
     tau_truth = np.zeros(O, np.float32)
     tau_oracle = np.zeros(O, np.float32)
     for o in range(O):

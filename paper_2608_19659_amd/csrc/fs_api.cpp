@@ -23,6 +23,7 @@ struct fs_context {
   int setup;         // exclusion scorer set-up: 0 automatic, 1 general
   int loop_objective;  // profiling loop certificate: 0 max-min, 1 whole objective
   int loop_refit;      // profiling loop fit step: 0 off, 1 interval refit every round
+  int thr_search;      // exclusion set-up: capacity-threshold search start (0 window, 1 stepping, 2 bisection)
   int32_t *pinned;   // pinned host word: running trajectories read back by fs_profile_loop
   struct Timed {
     hipEvent_t begin, end;
@@ -154,7 +155,7 @@ fs_status fs_context_create(int hip_device, fs_context **out) {
   e = hipSetDevice(hip_device);
   if (e == hipSuccess) e = hipHostMalloc((void **)&pinned, 64, hipHostMallocDefault);
   if (e != hipSuccess) return hip_fail(e, "hipHostMalloc");
-  *out = new fs_context{hip_device, 0, 0, 0, 0, 0, 0, 0, pinned, {}};
+  *out = new fs_context{hip_device, 0, 0, 0, 0, 0, 0, 0, 0, pinned, {}};
   return FS_OK;
 }
 
@@ -218,6 +219,11 @@ fs_status fs_context_set_option(fs_context *ctx, fs_option option, int64_t value
     if (value != FS_OBJECTIVE_MAXMIN && value != FS_OBJECTIVE_LEXICOGRAPHIC)
       return fail(FS_ERR_INVALID_ARGUMENT, "loop objective must be FS_OBJECTIVE_MAXMIN or FS_OBJECTIVE_LEXICOGRAPHIC");
     ctx->loop_objective = (int)value;
+    return FS_OK;
+  }
+  if (option == FS_OPT_THRESHOLD_SEARCH) {
+    if (value < 0 || value > 2) return fail(FS_ERR_INVALID_ARGUMENT, "threshold search must be 0, 1 or 2");
+    ctx->thr_search = (int)value;
     return FS_OK;
   }
   if (option == FS_OPT_SETUP) {
@@ -434,7 +440,7 @@ fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals
   }
   fs::ScoreArgs a{iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi, iv.measured, d_cand, d_cap_s, d_tail_s,
                   n_orders, n_cand, S, d_score, d_gap_now, d_best, d_tau_dump, ws, L, kernel,
-                  ctx->spl, ctx->waves, ctx->setup, nullptr, nullptr, 1};
+                  ctx->spl, ctx->waves, ctx->setup, nullptr, nullptr, 1, ctx->thr_search};
   if (ctx->timing && n_cand > 0) {
     e = hipEventCreate(&a.ev_begin);
     if (e == hipSuccess) e = hipEventCreate(&a.ev_end);
@@ -491,6 +497,32 @@ fs_status fs_refit_intervals(fs_context *ctx, const fs_problem *p, fs_intervals 
   return FS_OK;
 }
 
+fs_status fs_clamp_samples(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders,
+                           const int32_t *d_cand, int32_t n_cand, const float *d_cap_s, const float *d_tail_s,
+                           int32_t n_samples, float *d_cap_out, float *d_tail_out, hipStream_t stream) {
+  if (!ctx) return fail(FS_ERR_INVALID_ARGUMENT, "context is NULL");
+  fs::DevProblem P;
+  fs_status st = make_problem(p, &P);
+  if (st != FS_OK) return st;
+  if (n_orders < 0 || n_orders > 65535) return fail(FS_ERR_INVALID_ARGUMENT, "n_orders must be in [0, 65535]");
+  if (n_cand < 0 || n_cand > 65535) return fail(FS_ERR_INVALID_ARGUMENT, "n_cand must be in [0, 65535]");
+  if (n_samples < 0 || n_samples > FS_MAX_SAMPLES)
+    return fail(FS_ERR_INVALID_ARGUMENT, "n_samples must be in [0, 2^20]");
+  const int64_t n = (int64_t)n_orders * n_cand * n_samples;
+  if (n > 0 && (!iv.cap_lo || !iv.cap_hi || !iv.tail_lo || !iv.tail_hi))
+    return fail(FS_ERR_INVALID_ARGUMENT, "interval arrays are NULL");
+  if (n > 0 && (!d_cand || !d_cap_s || !d_tail_s || !d_cap_out || !d_tail_out))
+    return fail(FS_ERR_INVALID_ARGUMENT, "candidate, sample or output arrays are NULL");
+  if (n == 0) return FS_OK;
+  DeviceGuard dg(ctx->device);
+  if (dg.err != hipSuccess) return hip_fail(dg.err, "hipSetDevice");
+  const hipError_t e = fs::launch_clamp_samples(P, d_cand, n_cand, iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi,
+                                                d_cap_s, d_tail_s, n_orders, n_samples, d_cap_out, d_tail_out,
+                                                stream);
+  if (e != hipSuccess) return hip_fail(e, "clamp launch");
+  return FS_OK;
+}
+
 fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders,
                           const float *d_truth_cap, const float *d_truth_tail, const int32_t *d_cand,
                           int32_t n_cand, const float *d_cap_s, const float *d_tail_s, int32_t n_samples,
@@ -510,6 +542,16 @@ fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv,
     return fail(FS_ERR_INVALID_ARGUMENT, "policy must be FS_POLICY_SCORE or FS_POLICY_ORDER");
   if (policy == FS_POLICY_SCORE && n_cand > 0 && (n_samples < 1 || n_samples > FS_MAX_SAMPLES))
     return fail(FS_ERR_INVALID_ARGUMENT, "n_samples must be in [1, 2^20]");
+  int kernel = ctx->score_kernel;
+  if (kernel == 0) kernel = fs::excl_kernel_supported(P) ? 3 : 1;
+  if (kernel == 2 && !fs::lane_kernel_supported(P))
+    return fail(FS_ERR_UNSUPPORTED,
+                "lane-per-scenario scoring needs no floors, TP set {1,2,4,8} and budget 16, 32 or 64");
+  if (kernel == 3 && !fs::excl_kernel_supported(P))
+    return fail(FS_ERR_UNSUPPORTED, "exclusion scoring does not handle critical floors");
+  // the exclusion scorer's work list indexes (order, candidate) pairs in int32
+  if (kernel == 3 && policy == FS_POLICY_SCORE && (int64_t)n_orders * n_cand > INT32_MAX)
+    return fail(FS_ERR_UNSUPPORTED, "exclusion scoring needs n_orders * n_cand < 2^31");
   if (n_orders > 0 && (!iv.cap_lo || !iv.cap_hi || !iv.tail_lo || !iv.tail_hi || !iv.measured))
     return fail(FS_ERR_INVALID_ARGUMENT, "interval arrays are NULL");
   if (n_orders > 0 && (!d_truth_cap || !d_truth_tail))
@@ -521,13 +563,6 @@ fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv,
     return fail(FS_ERR_INVALID_ARGUMENT, "the reveal order is NULL");
   if (n_orders > 0 && (!out.state || !out.finished || !out.rounds || !out.gpu_seconds))
     return fail(FS_ERR_INVALID_ARGUMENT, "state, finished, rounds and gpu_seconds outputs are required");
-  int kernel = ctx->score_kernel;
-  if (kernel == 0) kernel = fs::excl_kernel_supported(P) ? 3 : 1;
-  if (kernel == 2 && !fs::lane_kernel_supported(P))
-    return fail(FS_ERR_UNSUPPORTED,
-                "lane-per-scenario scoring needs no floors, TP set {1,2,4,8} and budget 16, 32 or 64");
-  if (kernel == 3 && !fs::excl_kernel_supported(P))
-    return fail(FS_ERR_UNSUPPORTED, "exclusion scoring does not handle critical floors");
   const bool lex = ctx->loop_objective == FS_OBJECTIVE_LEXICOGRAPHIC;
   if (lex) {
     st = lex_supported(P, 2);
@@ -546,6 +581,21 @@ fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv,
   DeviceGuard dg(ctx->device);
   if (dg.err != hipSuccess) return hip_fail(dg.err, "hipSetDevice");
   uint8_t *ws = (uint8_t *)d_workspace;
+  hipError_t e;
+  if (env_validate()) {
+    int32_t *flag = (int32_t *)(ws + LL.score.flag);
+    const int64_t cells = (int64_t)n_orders * P.N;
+    e = fs::launch_zero_flags(flag, stream);
+    if (e == hipSuccess) e = fs::launch_validate_cells(iv.cap_lo, iv.tail_lo, cells, flag, stream);
+    if (e == hipSuccess) e = fs::launch_validate_cells(iv.cap_hi, iv.tail_hi, cells, flag, stream);
+    if (e == hipSuccess) e = fs::launch_validate_cells(d_truth_cap, d_truth_tail, cells, flag, stream);
+    if (e == hipSuccess && S > 0)
+      e = fs::launch_validate_cells(d_cap_s, d_tail_s, (int64_t)n_orders * n_cand * S, flag, stream);
+    if (e == hipSuccess && n_cand > 0) e = fs::launch_validate_cands(d_cand, n_cand, P.N, flag, stream);
+    if (e != hipSuccess) return hip_fail(e, "validation launch");
+    st = read_flags(LL.score, ws, stream, "fs_profile_loop");
+    if (st != FS_OK) return st;
+  }
   fs::LoopDev D = fs::loop_dev(LL, ws, n_orders);
   D.state = out.state;
   D.finished = out.finished;
@@ -554,7 +604,7 @@ fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv,
   D.reveals = out.reveals;
   D.max_rounds = max_rounds;
   const size_t cells = (size_t)n_orders * P.N;
-  hipError_t e = hipMemcpyAsync(D.cap_lo, iv.cap_lo, 4 * cells, hipMemcpyDeviceToDevice, stream);
+  e = hipMemcpyAsync(D.cap_lo, iv.cap_lo, 4 * cells, hipMemcpyDeviceToDevice, stream);
   if (e == hipSuccess) e = hipMemcpyAsync(D.cap_hi, iv.cap_hi, 4 * cells, hipMemcpyDeviceToDevice, stream);
   if (e == hipSuccess) e = hipMemcpyAsync(D.tail_lo, iv.tail_lo, 4 * cells, hipMemcpyDeviceToDevice, stream);
   if (e == hipSuccess) e = hipMemcpyAsync(D.tail_hi, iv.tail_hi, 4 * cells, hipMemcpyDeviceToDevice, stream);
@@ -614,7 +664,7 @@ fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv,
       } else {
         fs::ScoreArgs a{R_cap_lo, D.cap_hi, R_tail_lo, R_tail_hi, D.measured, d_cand, cs, ts,
                         n_orders, n_cand, S, D.score, D.gap_now, D.best, nullptr, ws, LL.score, kernel,
-                        ctx->spl, ctx->waves, ctx->setup, nullptr, nullptr, 1};
+                        ctx->spl, ctx->waves, ctx->setup, nullptr, nullptr, 1, ctx->thr_search};
         e = fs::launch_score(P, a, stream);
       }
       if (e != hipSuccess) return hip_fail(e, "loop score launch");
@@ -623,8 +673,16 @@ fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv,
                                d_order, stream);
     if (e != hipSuccess) return hip_fail(e, "loop reveal launch");
   }
-  e = fs::launch_loop_output(P, D, ws, LL.score, d_truth_cap, d_truth_tail, n_orders, to_out(out.final_alloc),
-                             out.tau_truth, stream);
+  // Algorithm 1's last line for the trajectories that ended undecided: the
+  // best allocation over measured cells only, into this round's (no longer
+  // needed) conservative allocation
+  e = fs::launch_loop_measured_table(P, D, n_orders, stream);
+  if (e == hipSuccess)
+    e = lex ? fs::launch_solve_batch_lex(P, D.cap_lo, D.tail_lo, n_orders, D.cons, nullptr, ws, LL.score, stream)
+            : fs::launch_solve_batch(P, D.cap_lo, D.tail_lo, n_orders, D.cons, ws, LL.score, stream);
+  if (e == hipSuccess)
+    e = fs::launch_loop_output(P, D, D.cons, ws, LL.score, d_truth_cap, d_truth_tail, n_orders,
+                               to_out(out.final_alloc), out.tau_truth, stream);
   if (e == hipSuccess && out.tau_oracle)
     e = fs::launch_solve_batch(P, d_truth_cap, d_truth_tail, n_orders,
                                fs::AllocOut{out.tau_oracle, nullptr, nullptr, nullptr, nullptr}, ws, LL.score,

@@ -105,6 +105,8 @@ struct ScoreArgs {
   int setup;   // exclusion scorer set-up: 0 automatic, 1 general
   hipEvent_t ev_begin, ev_end;  // recorded around the scoring kernel launches if set
   int timing_launches;          // back-to-back launches of the scoring kernel between the events
+  int thr_search;               // exclusion set-up: where the capacity-threshold search starts
+                                // (0 window, 1 stepping, 2 bisection; identical results)
 };
 
 struct AllocOut {
@@ -210,10 +212,14 @@ hipError_t launch_loop_count(const LoopDev &L, int32_t O, hipStream_t s);
 hipError_t launch_loop_reveal(const DevProblem &P, const LoopDev &L, const float *truth_cap,
                               const float *truth_tail, const int32_t *cand, int32_t E, int32_t O,
                               int32_t policy, const int32_t *order, hipStream_t s);
-// Copies the returned allocations out and evaluates them on the true table.
-hipError_t launch_loop_output(const DevProblem &P, const LoopDev &L, const uint8_t *ws, const WsLayout &SL,
-                              const float *truth_cap, const float *truth_tail, int32_t O, AllocOut out,
-                              float *tau_truth, hipStream_t s);
+// Overwrites the working tail_lo with the measured-only table (unmeasured
+// cells +inf, measured cells their point tails) for the final solve.
+hipError_t launch_loop_measured_table(const DevProblem &P, const LoopDev &L, int32_t O, hipStream_t s);
+// Copies the returned allocations out (A- of a certified trajectory, meas of
+// one that ended undecided) and evaluates them on the true table.
+hipError_t launch_loop_output(const DevProblem &P, const LoopDev &L, const AllocOut &meas, const uint8_t *ws,
+                              const WsLayout &SL, const float *truth_cap, const float *truth_tail, int32_t O,
+                              AllocOut out, float *tau_truth, hipStream_t s);
 
 // ---- class policies with several metrics (Eq. 5 in full) -----------------------
 constexpr int kMaxMetrics = 8;

@@ -890,10 +890,12 @@ __device__ __forceinline__ void option_of(const DevProblem &P, int p, int *ti, i
 // eight bit patterns from 3 below it are tested at once (independent
 // evaluations, whose latencies overlap): when the first does not reach M
 // (or is 0) and the last does, the answer is the first that does.  Otherwise
-// -- never seen, kept for safety -- the answer is pinned by stepping, then
-// by a bisection over bit patterns.  0 when M <= 0 (always reached); NaN when
-// M exceeds 1 (never reached).
-__device__ __forceinline__ float capacity_threshold(int r, int M, float demand, double rcp) {
+// the answer is pinned by stepping from the estimate, then by a bisection
+// over all bit patterns.  `mode` selects where the search starts: 0 the
+// window, 1 the stepping, 2 the bisection (every mode returns the same
+// value; 1 and 2 exist so that the later stages can be tested).  0 when
+// M <= 0 (always reached); NaN when M exceeds 1 (never reached).
+__device__ __forceinline__ float capacity_threshold(int r, int M, float demand, double rcp, int mode) {
   if (M <= 0) return 0.0f;
   if (M > __float_as_int(1.0f)) return __builtin_nanf("");
   const float rf = (float)r;
@@ -902,17 +904,19 @@ __device__ __forceinline__ float capacity_threshold(int r, int M, float demand, 
     return __float_as_int(fminf((float)((double)capacity * rcp), 1.0f)) >= M;
   };
   unsigned x = __float_as_uint(__int_as_float(M) * demand * __builtin_amdgcn_rcpf(rf));
-  {
+  if (mode == 0) {
     const unsigned x0 = x > 3u ? x - 3u : 0u;
     int below = 0;
 #pragma unroll
     for (int k = 0; k < 8; ++k) below += reach(x0 + (unsigned)k) ? 0 : 1;
     if (below < 8 && (below > 0 || x0 == 0u)) return __uint_as_float(x0 + (unsigned)below);
   }
-  int n = 0;
-  while (!reach(x) && n < 8) { ++x; ++n; }
-  while (x > 0 && reach(x - 1) && n < 16) { --x; ++n; }
-  if (reach(x) && (x == 0 || !reach(x - 1))) return __uint_as_float(x);
+  if (mode <= 1) {
+    int n = 0;
+    while (!reach(x) && n < 8) { ++x; ++n; }
+    while (x > 0 && reach(x - 1) && n < 16) { --x; ++n; }
+    if (reach(x) && (x == 0 || !reach(x - 1))) return __uint_as_float(x);
+  }
   unsigned blo = 0, bhi = 0x7F800000u;  // +inf reaches ratio 1 >= M
   while (blo < bhi) {
     const unsigned mid = blo + ((bhi - blo) >> 1);
@@ -1064,7 +1068,8 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
                                              int32_t *__restrict__ gtab, TileInfo *__restrict__ tiles,
                                              int32_t *__restrict__ base, int32_t *__restrict__ mopt,
                                              float *__restrict__ thr, int32_t n_thr,
-                                             int4 *__restrict__ list, int32_t *__restrict__ n_listed) {
+                                             int4 *__restrict__ list, int32_t *__restrict__ n_listed,
+                                             int32_t thr_mode) {
   extern __shared__ int lds[];
   __shared__ PrepConsts C;
   __shared__ int bucket_count[32], bucket_start[32], n_live;
@@ -1238,7 +1243,7 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
       atomicMin(&crlo[local], r);
       atomicMax(&crhi[local], r);
       Mo[p] = M;
-      To[p] = capacity_threshold(r, M, demand, rcp);
+      To[p] = capacity_threshold(r, M, demand, rcp, thr_mode);
     }
   }
   __syncthreads();
@@ -1473,7 +1478,8 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
                                                      int32_t dump, TileInfo *__restrict__ tiles,
                                                      int32_t *__restrict__ base, int32_t *__restrict__ mopt,
                                                      float *__restrict__ thr, int32_t n_thr,
-                                                     int4 *__restrict__ list, int32_t *__restrict__ n_listed) {
+                                                     int4 *__restrict__ list, int32_t *__restrict__ n_listed,
+                                                     int32_t thr_mode) {
   extern __shared__ int lds[];
   const int tid = threadIdx.x, nth = blockDim.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1628,7 +1634,7 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
       float Tv[2] = {0.0f, 0.0f};
       if (do_thr) {
 #pragma unroll
-        for (int u = 0; u < 2; ++u) Tv[u] = ok[u] ? capacity_threshold(rr[u], Mv[u], demand, rcp) : __builtin_nanf("");
+        for (int u = 0; u < 2; ++u) Tv[u] = ok[u] ? capacity_threshold(rr[u], Mv[u], demand, rcp, thr_mode) : __builtin_nanf("");
       }
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
@@ -2998,22 +3004,36 @@ __global__ __launch_bounds__(64) void k_loop_reveal(DevProblem P, LoopDev L, con
   L.rounds[o] += 1;
 }
 
-// The returned allocation's objective level (2) on the true table: the
-// smallest fulfillment over the classes, an unserved class counting 0.
-__global__ void k_loop_output(DevProblem P, LoopDev L, const int8_t *__restrict__ bmap,
+// Algorithm 1's last line, the best measured feasible allocation: the
+// table of every trajectory with each unmeasured cell made infeasible (tail
+// +inf, written over the working tail_lo, which the loop no longer needs);
+// measured cells keep their point values.  The solve of (cap_lo, tail_lo)
+// then serves only measured cells.
+__global__ void k_loop_measured_table(LoopDev L, int64_t n) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= n) return;
+  L.tail_lo[j] = L.measured[j] ? L.tail_hi[j] : __builtin_inff();
+}
+
+// The returned allocation: A- of a certified trajectory, the best measured
+// feasible allocation (meas) of one that ended undecided; and its objective
+// level (2) on the true table: the smallest fulfillment over the classes, an
+// unserved class counting 0.
+__global__ void k_loop_output(DevProblem P, LoopDev L, AllocOut meas, const int8_t *__restrict__ bmap,
                               const float *__restrict__ truth_cap, const float *__restrict__ truth_tail,
                               int32_t O, AllocOut out, float *__restrict__ tau_truth) {
   const int o = blockIdx.x * blockDim.x + threadIdx.x;
   if (o >= O) return;
   const size_t off = (size_t)o * P.N;
-  if (out.objective) out.objective[o] = L.fin.objective[o];
-  if (out.floors_met) out.floors_met[o] = L.fin.floors_met[o];
-  if (out.goodput) out.goodput[o] = L.fin.goodput[o];
+  const AllocOut &A = L.state[o] == 0 ? meas : L.fin;
+  if (out.objective) out.objective[o] = A.objective[o];
+  if (out.floors_met) out.floors_met[o] = A.floors_met[o];
+  if (out.goodput) out.goodput[o] = A.goodput[o];
   float v = __builtin_inff();
   bool unserved = false;
   for (int k = 0; k < P.K; ++k) {
-    const int ti = L.fin.tp_index[(size_t)o * P.K + k];
-    const int r = L.fin.replicas[(size_t)o * P.K + k];
+    const int ti = A.tp_index[(size_t)o * P.K + k];
+    const int r = A.replicas[(size_t)o * P.K + k];
     if (out.tp_index) out.tp_index[(size_t)o * P.K + k] = (uint8_t)ti;
     if (out.replicas) out.replicas[(size_t)o * P.K + k] = (uint16_t)r;
     if (r == 0) {
@@ -3279,16 +3299,16 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
     if (a.setup == 0 && prep_order_fits(P, a.O, a.E))
       k_prep_order<<<2 * a.O + 1, prep_order_waves(P, a.O, a.E) * kWave, prep_order_lds(P, a.O, a.E), s>>>(
           P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured, a.cand, a.E, a.O, dump, tiles, base, mopt,
-          thr, n_thr, list, live);
+          thr, n_thr, list, live, a.thr_search);
     else if (big <= kPrepLdsLimit)
       k_prep<true><<<dim3(2, a.O, P.K + 1), kPrepThreads, big, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
                                                           a.measured, a.cand, a.E, dump, nullptr, tiles,
-                                                          base, mopt, thr, n_thr, list, live);
+                                                          base, mopt, thr, n_thr, list, live, a.thr_search);
     else
       k_prep<false><<<dim3(2, a.O, P.K + 1), kPrepThreads, small, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
                                                              a.measured, a.cand, a.E, dump,
                                                              (int32_t *)(a.ws + a.L.tabB), tiles, base, mopt,
-                                                             thr, n_thr, list, live);
+                                                             thr, n_thr, list, live, a.thr_search);
     if (a.E == 0) {
       k_finalize<<<a.O, 64, 0, s>>>(P, info, a.measured, 0, a.S, base, partial, 1, a.score, a.gap_now,
                                     a.best);
@@ -3599,11 +3619,18 @@ hipError_t launch_loop_reveal(const DevProblem &P, const LoopDev &L, const float
   return hipGetLastError();
 }
 
-hipError_t launch_loop_output(const DevProblem &P, const LoopDev &L, const uint8_t *ws, const WsLayout &SL,
-                              const float *truth_cap, const float *truth_tail, int32_t O, AllocOut out,
-                              float *tau_truth, hipStream_t s) {
+hipError_t launch_loop_measured_table(const DevProblem &P, const LoopDev &L, int32_t O, hipStream_t s) {
+  const int64_t n = (int64_t)O * P.N;
+  if (n == 0) return hipSuccess;
+  k_loop_measured_table<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(L, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_loop_output(const DevProblem &P, const LoopDev &L, const AllocOut &meas, const uint8_t *ws,
+                              const WsLayout &SL, const float *truth_cap, const float *truth_tail, int32_t O,
+                              AllocOut out, float *tau_truth, hipStream_t s) {
   if (O == 0) return hipSuccess;
-  k_loop_output<<<(O + 63) / 64, 64, 0, s>>>(P, L, (const int8_t *)(ws + SL.bmap), truth_cap, truth_tail, O,
+  k_loop_output<<<(O + 63) / 64, 64, 0, s>>>(P, L, meas, (const int8_t *)(ws + SL.bmap), truth_cap, truth_tail, O,
                                              out, tau_truth);
   return hipGetLastError();
 }

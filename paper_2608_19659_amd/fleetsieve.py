@@ -28,6 +28,7 @@ OPT_SCORER_WAVES = 5
 OPT_SETUP = 6
 OPT_LOOP_OBJECTIVE = 7
 OPT_LOOP_REFIT = 8
+OPT_THRESHOLD_SEARCH = 9
 OBJECTIVE_MAXMIN, OBJECTIVE_LEXICOGRAPHIC = 0, 1
 KERNEL_AUTO, KERNEL_WAVE, KERNEL_LANE, KERNEL_EXCLUSION = 0, 1, 2, 3
 
@@ -36,7 +37,7 @@ EXPORTED = ("fs_context_create", "fs_context_destroy", "fs_context_set_option", 
             "fs_validate_problem", "fs_workspace_size", "fs_solve_batch", "fs_score_candidates",
             "fs_certify", "fs_loop_workspace_size", "fs_profile_loop", "fs_reduce_cells", "fs_reduce_samples",
             "fs_solve_batch_lex", "fs_certify_lex", "fs_refit_intervals", "fs_loop_refit_workspace_size",
-            "fs_score_lex_workspace_size", "fs_score_candidates_lex")
+            "fs_score_lex_workspace_size", "fs_score_candidates_lex", "fs_clamp_samples")
 POLICY_SCORE, POLICY_ORDER = 0, 1
 CELL_SECONDS = 300.0
 
@@ -110,6 +111,7 @@ def load_library():
                                             sz, vp]
     lib.fs_refit_intervals.argtypes = [vp, P, _Intervals, i32, vp, vp, vp, vp]
     lib.fs_loop_refit_workspace_size.argtypes = [P, i32, i32, i32, ctypes.POINTER(sz)]
+    lib.fs_clamp_samples.argtypes = [vp, P, _Intervals, i32, vp, i32, vp, vp, i32, vp, vp, vp]
     lib.fs_solve_batch_lex.argtypes = [vp, P, vp, vp, i64, _Alloc, vp, vp, sz, vp]
     lib.fs_certify_lex.argtypes = [vp, P, _Intervals, i32, ctypes.c_float, vp, _Alloc, _Alloc, vp, vp, vp, sz, vp]
     Q = ctypes.POINTER(_SloPolicy)
@@ -478,6 +480,24 @@ def refit_intervals(ctx: Context, problem, iv: DeviceIntervals, stream=None) -> 
                                              out.tail_lo.data_ptr(), out.tail_hi.data_ptr(),
                                              _stream(iv.cap_lo.device, stream)))
     return out
+
+
+def clamp_samples(ctx: Context, problem, iv: DeviceIntervals, cand, cap_s, tail_s, stream=None):
+    """The candidates' samples clamped into their current intervals
+    (fs_clamp_samples); returns new (cap_s, tail_s) tensors [O, E, S]."""
+    torch = _torch()
+    ref = _ProblemRef(problem)
+    O = int(iv.cap_lo.shape[0])
+    E = int(cand.shape[0])
+    S = int(cap_s.shape[2]) if E > 0 else 0
+    ivs = _intervals_struct(iv, O, ref.N)
+    pcand = _dev_ptr(cand, torch.int32, (E,), "cand")
+    pcs = _dev_ptr(cap_s, torch.float32, (O, E, S), "cap_s")
+    pts = _dev_ptr(tail_s, torch.float32, (O, E, S), "tail_s")
+    cs_out, ts_out = torch.empty_like(cap_s), torch.empty_like(tail_s)
+    _check(load_library().fs_clamp_samples(ctx.handle, ref.ptr, ivs, O, pcand, E, pcs, pts, S, cs_out.data_ptr(),
+                                           ts_out.data_ptr(), _stream(iv.cap_lo.device, stream)))
+    return cs_out, ts_out
 
 
 def loop_refit_workspace_size(problem, n_orders: int, n_cand: int, n_samples: int) -> int:

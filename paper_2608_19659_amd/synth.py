@@ -155,6 +155,20 @@ WORKLOADS = {
             cap_range=(0.1, 5.0), cap_width=(0.02, 0.5), tail_sigma=0.5, tail_alpha=1.0,
             tail_tp_factor=True, tail_width=(0.02, 0.5), orders=4, reveal=True,
             cand=("all",), samples=256),
+    # Class counts between the two- and four-class shapes and the 16-class
+    # fleet at budgets of one wavefront or less: they exercise the set-up's
+    # wavefront layouts (two wavefronts per class up to 8 classes, one per
+    # class up to 16).
+    "6class-G32": dict(seed=1007, K=6, tp=[1, 2, 4, 8], G=32, levels=_geometric(0.125, 8),
+            demand=("uniform", 0.5, 3.0), slo=("choice", SLO_CHOICES),
+            cap_range=(0.1, 5.0), cap_width=(0.05, 0.3), tail_sigma=0.5, tail_alpha=1.0,
+            tail_tp_factor=True, tail_width=(0.1, 0.4), orders=8, reveal=True,
+            cand=("all",), samples=512),
+    "12class-G64": dict(seed=1008, K=12, tp=[1, 2, 4, 8], G=64, levels=_geometric(0.125, 8),
+            demand=("uniform", 1.0, 8.0), slo=("choice", SLO_CHOICES),
+            cap_range=(0.1, 5.0), cap_width=(0.05, 0.3), tail_sigma=0.5, tail_alpha=1.0,
+            tail_tp_factor=True, tail_width=(0.1, 0.4), orders=4, reveal=True,
+            cand=("all",), samples=256),
     # Truth drawn first with the structure the interval refit assumes
     # (capacity per GPU unimodal over TP with its knee at TP4, tail
     # nondecreasing in the load), intervals around it.
@@ -357,6 +371,27 @@ def make_workload(name: str, orders=None, with_samples: bool = True) -> Workload
     iv = Intervals(cap_lo, cap_hi, tail_lo, tail_hi, measured)
     return Workload(name, seed, problem, iv, cand, cap_s, tail_s,
                     truth_cap.astype(np.float32), truth_tail.astype(np.float32), sel, S, dict(c))
+
+
+def seeded_tiles(w: Workload, n: int, seed: int) -> list:
+    """n (order, candidate) tiles of a workload whose candidate is unmeasured
+    in that order, drawn by a seeded permutation (all of them when n is
+    larger); the subsets on which the large workloads are checked and timed
+    against the oracle."""
+    meas = np.asarray(w.intervals.measured)[:, np.asarray(w.cand)].astype(bool)
+    O, E = meas.shape
+    live = [(o, e) for o in range(O) for e in range(E) if not meas[o, e]]
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 5])))
+    pick = rng.permutation(len(live))[: min(n, len(live))]
+    return [live[j] for j in sorted(pick)]
+
+
+def tile_mask(w: Workload, tiles) -> np.ndarray:
+    """[O][E] uint8 mask of the given (order, candidate) tiles."""
+    m = np.zeros((np.asarray(w.intervals.measured).shape[0], len(w.cand)), np.uint8)
+    for o, e in tiles:
+        m[o, e] = 1
+    return m
 
 
 def random_point_tables(problem: Problem, n: int, seed: int, cap_range=(0.0, 4.0),

@@ -75,14 +75,16 @@ def test_hand_derived_trajectories_on_gpu(env, case):
                    np.array([d["measured"]], np.uint8))
     policy = 1 if c["policy"] == "order" else 0
     order = None if policy == 0 else [c["order"]]
-    r = gpu_loop(env, p, iv, [c["truth_cap"]], [c["truth_tail"]], g["cand"], [g["cap_s"]], [g["tail_s"]],
-                 c["eps"], policy, order, c.get("max_rounds"))
+    r = gpu_loop(env, p, iv, [c["truth_cap"]], [c["truth_tail"]], c.get("cand", g["cand"]),
+                 [c.get("cap_s", g["cap_s"])], [c.get("tail_s", g["tail_s"])], c["eps"], policy, order,
+                 c.get("max_rounds"))
     assert r["state"][0] == STATES[c["state"]]
     assert r["finished"][0] == c["finished"] and r["rounds"][0] == c["rounds"]
     assert list(r["reveals"][0][: c["rounds"]]) == c["reveals"]
     assert r["gpu_seconds"][0] == c["gpu_seconds"]
     if "final_replicas" in c:
-        assert list(r["replicas"][0]) == c["final_replicas"] and list(r["tp_index"][0]) == c["final_tp_index"]
+        assert list(r["replicas"][0]) == c["final_replicas"]
+        assert list(r["tp_index"][0]) == [255 if t < 0 else t for t in c["final_tp_index"]]
         assert r["objective"][0] == np.float32(c["final_tau"])
         assert r["tau_truth"][0] == np.float32(c["tau_truth"]) and r["tau_oracle"][0] == np.float32(c["tau_oracle"])
 
@@ -134,6 +136,19 @@ def test_floors_and_exhaustion_match_oracle(env):
     o = oracle.profile_loop(p, w.intervals, tc, tt, w.cand, cs, ts, eps=-1.0, n_threads=8)
     g = gpu_loop(env, p, w.intervals, tc, tt, w.cand, cs, ts, -1.0, 0)
     assert_loop_equal(g, o, "exhaustion")
+    # candidates a subset of the cells (8 of 24): at exhaustion the loop
+    # returns the best allocation over measured cells only
+    w, p, tc, tt, cs, ts = _inputs("tiny-2class-G16", [0], 64)
+    note("loop tiny-2class-G16 eps=-1 (candidate subset, exhaustion)")
+    o = oracle.profile_loop(p, w.intervals, tc, tt, w.cand, cs, ts, eps=-1.0, n_threads=8)
+    g = gpu_loop(env, p, w.intervals, tc, tt, w.cand, cs, ts, -1.0, 0)
+    assert_loop_equal(g, o, "candidate subset")
+    for name, rounds in (("tiny-2class-G16", 2), ("paper-shaped-2class-G16", 3)):
+        w, p, tc, tt, cs, ts = _inputs(name, [0, 1] if name != "tiny-2class-G16" else [0], 16)
+        note(f"loop {name} round limit {rounds}")
+        o = oracle.profile_loop(p, w.intervals, tc, tt, w.cand, cs, ts, eps=0.05, max_rounds=rounds, n_threads=8)
+        g = gpu_loop(env, p, w.intervals, tc, tt, w.cand, cs, ts, 0.05, 0, max_rounds=rounds)
+        assert_loop_equal(g, o, f"round limit {name}")
 
 
 def test_early_exit_checks_do_not_change_results(env):
@@ -145,3 +160,25 @@ def test_early_exit_checks_do_not_change_results(env):
     for r in res[1:]:
         for k in res[0]:
             np.testing.assert_array_equal(r[k], res[0][k], err_msg=k)
+
+
+def test_oversized_loop_is_rejected_before_any_launch(env):
+    """The exclusion scorer's work list indexes (order, candidate) pairs in
+    int32: 65535 orders x 65535 candidates is rejected with
+    FS_ERR_UNSUPPORTED by the host checks, before the pointer checks (every
+    device pointer here is NULL, so nothing could be launched)."""
+    import ctypes
+    torch, fs, ctx = env
+    lib = fs.load_library()
+    p = Problem(tp=[1, 2, 4, 8], levels=[0.5, 1.0, 2.0], demand=[4.0, 2.0], slo=[30.0, 30.0], budget=16)
+    ref = fs._ProblemRef(p)
+    note("oversized loop rejected")
+    st = lib.fs_profile_loop(ctx.handle, ref.ptr, fs._Intervals(), 65535, None, None, None, 65535, None, None, 64,
+                             ctypes.c_float(0.05), fs.POLICY_SCORE, None, 4, 0, fs._LoopOut(), None, 0, None)
+    assert st == fs.FS_ERR_UNSUPPORTED, lib.fs_last_error()
+    assert b"2^31" in lib.fs_last_error()
+    # the same sizes under a fixed reveal order never score, so the limit does not apply: the
+    # NULL arrays are then what is rejected
+    st = lib.fs_profile_loop(ctx.handle, ref.ptr, fs._Intervals(), 65535, None, None, None, 65535, None, None, 64,
+                             ctypes.c_float(0.05), fs.POLICY_ORDER, None, 4, 0, fs._LoopOut(), None, 0, None)
+    assert st == fs.FS_ERR_INVALID_ARGUMENT

@@ -9,7 +9,8 @@ import numpy as np
 import pytest
 
 from conftest import load_golden
-from paper_2608_19659_amd.synth import Intervals, Problem, make_workload, random_point_tables, random_problem
+from paper_2608_19659_amd.synth import (Intervals, Problem, make_workload, random_point_tables, random_problem,
+                                        seeded_tiles, tile_mask)
 
 pytestmark = pytest.mark.gpu
 
@@ -260,81 +261,73 @@ def test_score_16class_g1024_subset(env, orc, kernel):
     assert_scores_equal(g, o)
 
 
-def test_score_8class_g256_full_order_exclusion(env, orc):
-    """Config 3 at its real sample count (4096) with the exclusion kernel:
-    all 256 candidates of one order, sampled scenarios re-solved by the
-    oracle one by one, and three whole tiles re-scored."""
-    w = make_workload("8class-G256", orders=[7])
-    note("score 8class-G256 one full order, exclusion")
-    score, gap, best, dump = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=3)
-    p, iv = w.problem, w.intervals
-    rng = np.random.default_rng(33)
-    E, S = w.n_cand, w.n_samples
-    for _ in range(60):
-        e, s = int(rng.integers(E)), int(rng.integers(S))
-        cell = w.cand[e]
-        if iv.measured[0, cell]:
-            continue
-        cm, tm = iv.cap_lo[0].copy(), iv.tail_hi[0].copy()
-        cp, tp = iv.cap_hi[0].copy(), iv.tail_lo[0].copy()
-        cm[cell] = cp[cell] = w.cap_s[0, e, s]
-        tm[cell] = tp[cell] = w.tail_s[0, e, s]
-        assert dump[0, e, s, 0] == orc.solve(p, cm, tm).tau, (e, s)
-        assert dump[0, e, s, 1] == orc.solve(p, cp, tp).tau, (e, s)
-    mask = np.zeros((1, E), np.uint8)
-    live = [e for e in range(E) if not iv.measured[0, w.cand[e]]]
-    mask[0, rng.choice(live, size=3, replace=False)] = 1
-    o_ref = orc.score(p, iv, w.cand, w.cap_s, w.tail_s, tile_mask=mask, n_threads=16)
-    assert_scores_equal((score, gap, best, dump), o_ref, tile_mask=mask)
-
-
-def test_score_4class_g64_full_size_sampled(env, orc):
-    """The 4-class G=64 workload at full size (16 orders x 128 candidates x
-    4096 samples) in the benchmark's launch configuration: sampled scenarios
-    re-solved one by one by the oracle, two whole tiles re-scored, and the
-    invariants of the realisations checked everywhere."""
-    w = make_workload("4class-G64")
-    note("score 4class-G64 full size")
+def test_score_8class_g256_full_size_seeded_tiles(env, orc):
+    """The 8-class G=256 workload at full size (64 orders x 256 candidates x
+    4096 samples, 67 M scenarios) in the benchmark's launch configuration:
+    16 seeded tiles (65,536 scenarios) re-scored by the oracle, scores and
+    every tau of those tiles bit for bit; the invariants everywhere."""
+    w = make_workload("8class-G256")
+    note("score 8class-G256 full size")
     score, gap, best, dump = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=0)
-    # the benchmark runs without the tau dump: same scores, bit for bit
-    s2, g2, b2, _ = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=0, dump=False)
-    np.testing.assert_array_equal(s2.view(np.uint64), score.view(np.uint64))
-    np.testing.assert_array_equal(g2, gap)
-    np.testing.assert_array_equal(b2, best)
-    O, E, S = w.cap_s.shape
-    p, iv = w.problem, w.intervals
-    rng = np.random.default_rng(2)
-    for _ in range(400):
-        o, e, s = int(rng.integers(O)), int(rng.integers(E)), int(rng.integers(S))
-        cell = w.cand[e]
-        if iv.measured[o, cell]:
-            continue
-        cm, tm = iv.cap_lo[o].copy(), iv.tail_hi[o].copy()
-        cp, tp = iv.cap_hi[o].copy(), iv.tail_lo[o].copy()
-        cm[cell] = cp[cell] = w.cap_s[o, e, s]
-        tm[cell] = tp[cell] = w.tail_s[o, e, s]
-        assert dump[o, e, s, 0] == orc.solve(p, cm, tm).tau, (o, e, s)
-        assert dump[o, e, s, 1] == orc.solve(p, cp, tp).tau, (o, e, s)
-    mask = np.zeros((O, E), np.uint8)
-    unmeasured = [(o, e) for o in range(O) for e in range(E) if not iv.measured[o, w.cand[e]]]
-    for j in rng.choice(len(unmeasured), size=2, replace=False):
-        mask[unmeasured[j]] = 1
-    o_ref = orc.score(p, iv, w.cand, w.cap_s, w.tail_s, tile_mask=mask, n_threads=16)
+    tiles = seeded_tiles(w, 16, 1003)
+    mask = tile_mask(w, tiles)
+    note(f"oracle on {len(tiles)} tiles")
+    o_ref = orc.score(w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, tile_mask=mask, n_threads=16)
     assert_scores_equal((score, gap, best, dump), o_ref, tile_mask=mask)
     np.testing.assert_array_equal(gap, o_ref.gap_now)
-    # invariants everywhere
+    _check_invariants(w, score, gap, best, dump)
+
+
+def test_score_16class_g1024_full_size_seeded_tiles(env, orc):
+    """The 16-class G=1024 workload at full size (4 orders x 960 candidates
+    x 256 samples) through the general set-up with its tables in global
+    memory: 8 seeded tiles (2,048 scenarios) re-scored by the oracle, bit for
+    bit."""
+    w = make_workload("16class-G1024")
+    note("score 16class-G1024 full size")
+    score, gap, best, dump = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=0)
+    tiles = seeded_tiles(w, 8, 1004)
+    mask = tile_mask(w, tiles)
+    note(f"oracle on {len(tiles)} tiles")
+    o_ref = orc.score(w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, tile_mask=mask, n_threads=16)
+    assert_scores_equal((score, gap, best, dump), o_ref, tile_mask=mask)
+    np.testing.assert_array_equal(gap, o_ref.gap_now)
+    _check_invariants(w, score, gap, best, dump)
+
+
+def _check_invariants(w, score, gap, best, dump):
+    iv = w.intervals
     assert np.all(dump[..., 0] <= dump[..., 1])
     gam = dump[..., 1].astype(np.float64) - dump[..., 0]
     assert np.all(gam >= 0) and np.all(gam <= gap[:, None, None])
     assert np.all((score >= 0) & (score <= gap[:, None]))
     meas = iv.measured[:, w.cand].astype(bool)
     assert np.all(score[meas] == 0.0)
-    for o in range(O):
+    for o in range(len(gap)):
         if meas[o].all():
             assert best[o] == -1
         else:
             b = best[o]
             assert not meas[o, b] and score[o, b] == score[o][~meas[o]].max()
+
+
+def test_score_4class_g64_full_size(env, orc):
+    """The 4-class G=64 workload at full size (16 orders x 128 candidates x
+    4096 samples) in the benchmark's launch configuration, against the
+    oracle on every tile: every tau of the dump, every score, the gaps and
+    the best candidates bit for bit; the run without the dump (the
+    benchmark's) gives the same scores."""
+    w = make_workload("4class-G64")
+    note("score 4class-G64 full size")
+    score, gap, best, dump = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=0)
+    s2, g2, b2, _ = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=0, dump=False)
+    np.testing.assert_array_equal(s2.view(np.uint64), score.view(np.uint64))
+    np.testing.assert_array_equal(g2, gap)
+    np.testing.assert_array_equal(b2, best)
+    note("oracle on the whole launch")
+    o = orc.score(w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, n_threads=16)
+    assert_scores_equal((score, gap, best, dump), o)
+    _check_invariants(w, score, gap, best, dump)
 
 
 # ------------------------------------------------------------ edge cases ----
@@ -454,7 +447,7 @@ def test_exclusion_launch_shapes_agree(env, S):
 
 
 @pytest.mark.parametrize("name,orders", [("tiny-2class-G16", None), ("paper-shaped-2class-G16", [0, 5, 17]),
-                                         ("4class-G64", [1, 2])])
+                                         ("4class-G64", [1, 2]), ("6class-G32", None), ("12class-G64", None)])
 def test_setup_paths_agree(env, name, orders):
     """The one-block-per-order set-up (budgets up to 64 GPUs) and the general
     set-up give the same bits: scores, gaps, best candidates and every tau of
@@ -583,3 +576,40 @@ def test_score_many_partials(env, orc, S):
         np.testing.assert_array_equal(score, o.score)
         np.testing.assert_array_equal(gap, o.gap_now)
         np.testing.assert_array_equal(best, o.best)
+
+
+@pytest.mark.parametrize("name", ["6class-G32", "12class-G64"])
+def test_setup_wavefront_layouts_match_oracle(env, orc, name):
+    """The per-order set-up with two wavefronts per class (6 classes, 12
+    wavefronts) and with one per class (12 classes): every tau of the dump,
+    scores and best candidates equal the oracle's."""
+    w = make_workload(name)
+    S = min(w.n_samples, 256)
+    cs, ts = np.ascontiguousarray(w.cap_s[:, :, :S]), np.ascontiguousarray(w.tail_s[:, :, :S])
+    note(f"score {name} all orders, S={S}")
+    g = gpu_score(env, w.problem, w.intervals, w.cand, cs, ts, kernel=3)
+    o = orc.score(w.problem, w.intervals, w.cand, cs, ts, n_threads=16)
+    assert_scores_equal(g, o)
+    assert (o.gap_now > 0).any()
+
+
+@pytest.mark.parametrize("setup", [0, 1])
+def test_threshold_search_stages_match_oracle(env, orc, setup):
+    """The capacity-threshold search from each of its stages (the window of
+    eight bit patterns, stepping, bisection over all bit patterns) gives the
+    oracle's bits on the 4-class G=64 workload (3 orders x 7 candidates, 4096
+    samples), in both set-up kernels."""
+    torch, fs, ctx = env
+    w = make_workload("4class-G64", orders=[1, 2, 3])
+    sel = np.array([3, 17, 40, 64, 77, 100, 126])
+    cand, cs, ts = w.cand[sel], w.cap_s[:, sel], w.tail_s[:, sel]
+    o = orc.score(w.problem, w.intervals, cand, cs, ts, n_threads=16)
+    try:
+        ctx.set_option(fs.OPT_SETUP, setup)
+        for mode in (0, 1, 2):
+            note(f"threshold search mode {mode} set-up {setup}")
+            ctx.set_option(fs.OPT_THRESHOLD_SEARCH, mode)
+            assert_scores_equal(gpu_score(env, w.problem, w.intervals, cand, cs, ts, kernel=3), o)
+    finally:
+        ctx.set_option(fs.OPT_THRESHOLD_SEARCH, 0)
+        ctx.set_option(fs.OPT_SETUP, 0)

@@ -246,3 +246,19 @@ def test_profiling_loop_under_policy(env):
     np.testing.assert_array_equal(r.gpu_seconds.cpu().numpy(), o.gpu_seconds)
     np.testing.assert_array_equal(r.tau_truth.cpu().numpy(), o.tau_truth)
     np.testing.assert_array_equal(r.tau_oracle.cpu().numpy(), o.tau_oracle)
+
+
+def test_interval_sides_hand_derived_on_gpu(env):
+    """fs_reduce_cells on the hand-derived interval case
+    (tests/golden/policy_intervals.json): the conservative side (upper
+    tails, lower success) and the optimistic side (lower tails, upper
+    success) reduce to the hand-derived pseudo-tails."""
+    g = load_golden("policy_intervals.json")
+    p = Problem(tp=g["tp"], levels=g["levels"], demand=g["demand"], slo=g["slo"], budget=g["budget"])
+    pol = oracle.Policy(limit=np.array(g["limit"], np.float32), success_min=np.array(g["success_min"], np.float32))
+    note("policy interval sides golden case")
+    a = lambda k: np.array([g[k]], np.float32)
+    hi = gpu_cells(env, p, pol, a("tail_hi"), a("succ_lo"))
+    lo = gpu_cells(env, p, pol, a("tail_lo"), a("succ_hi"))
+    assert hi.tolist() == [g["conservative_tail_hi"]]
+    assert lo.tolist() == [g["optimistic_tail_lo"]]

@@ -117,3 +117,43 @@ def test_loop_with_refit_matches_oracle(env, name, orders, S, max_rounds, object
     reps = r.final["replicas"].cpu().numpy()
     for j, a in enumerate(o.final):
         assert list(reps[j].view(np.uint16)) == a.replicas, j
+
+
+def gpu_clamp(env, p, iv, cand, cs, ts):
+    torch, fs, ctx = env
+    c, t = fs.clamp_samples(ctx, p, fs.DeviceIntervals.from_host(iv, "cuda:0"),
+                            _t(env, np.asarray(cand, np.int32)), _t(env, cs), _t(env, ts))
+    torch.cuda.synchronize()
+    return c.cpu().numpy(), t.cpu().numpy()
+
+
+def test_clamp_hand_derived_on_gpu(env):
+    """fs_refit_intervals then fs_clamp_samples on the hand-derived case
+    (tests/golden/clamp_samples.json): the samples land in the refitted
+    intervals, exactly at the bounds where they fall outside."""
+    g = load_golden("clamp_samples.json")
+    note("clamp golden case")
+    p = Problem(tp=g["tp"], levels=g["levels"], demand=g["demand"], slo=g["slo"], budget=g["budget"])
+    r = gpu_refit(env, p, _iv(g["intervals"]))
+    for k in ("cap_lo", "cap_hi", "tail_lo", "tail_hi"):
+        assert list(r[k][0]) == g["refit"][k], k
+    f = Intervals(r["cap_lo"], r["cap_hi"], r["tail_lo"], r["tail_hi"], _iv(g["intervals"]).measured)
+    c, t = gpu_clamp(env, p, f, g["cand"], np.array([g["cap_s"]], np.float32), np.array([g["tail_s"]], np.float32))
+    assert c.tolist() == [g["clamped_cap_s"]] and t.tolist() == [g["clamped_tail_s"]]
+
+
+@pytest.mark.parametrize("name,seed,frac,S", [("4class-G64-knee", 3, 0.3, 4096), ("paper-shaped-2class-G16", 1, 0.3, 1000),
+                                              ("16class-G1024", 2, 0.4, 256)])
+def test_clamp_matches_oracle(env, name, seed, frac, S):
+    """k_clamp_samples against oracle.clamp_samples, bit for bit, on the
+    refit of a random measured state (ragged S included)."""
+    w0, iv = _random_state(name, seed, frac)
+    w = make_workload(name, orders=list(range(4)))
+    note(f"clamp {name} S={S}")
+    f = oracle.refit_intervals(w.problem, iv)
+    cs, ts = np.ascontiguousarray(w.cap_s[:, :, :S]), np.ascontiguousarray(w.tail_s[:, :, :S])
+    want_c, want_t = oracle.clamp_samples(f, w.cand, cs, ts)
+    got_c, got_t = gpu_clamp(env, w.problem, f, w.cand, cs, ts)
+    np.testing.assert_array_equal(got_c.view(np.uint32), want_c.view(np.uint32))
+    np.testing.assert_array_equal(got_t.view(np.uint32), want_t.view(np.uint32))
+    assert (want_c != cs).any() or (want_t != ts).any()

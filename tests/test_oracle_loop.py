@@ -38,8 +38,9 @@ def test_hand_derived_trajectories(case):
                 floor_rps=floor)
     iv = _intervals(c.get("intervals", g["intervals"]))
     policy = oracle.POLICY_ORDER if c["policy"] == "order" else oracle.POLICY_SCORE
-    r = oracle.profile_loop(p, iv, [c["truth_cap"]], [c["truth_tail"]], g["cand"],
-                            np.array([g["cap_s"]], np.float32), np.array([g["tail_s"]], np.float32),
+    r = oracle.profile_loop(p, iv, [c["truth_cap"]], [c["truth_tail"]], c.get("cand", g["cand"]),
+                            np.array([c.get("cap_s", g["cap_s"])], np.float32),
+                            np.array([c.get("tail_s", g["tail_s"])], np.float32),
                             eps=c["eps"], policy=policy, order=[c.get("order")], max_rounds=c.get("max_rounds"))
     assert r.state[0] == STATES[c["state"]], c["what"]
     assert r.finished[0] == c["finished"]

@@ -89,3 +89,24 @@ def test_sample_feasibility_is_cell_feasibility_at_the_candidate():
                 succ = np.ones(N, np.float32)
                 tails[c], succ[c] = tail_s[o, e, s], succ_s[o, e, s]
                 assert got[o, e, s] == oracle.feasible_cells(p, pol, tails, succ)[c]
+
+
+def test_interval_sides_hand_derived():
+    """The conservative side pairs the upper tail bounds with the LOWER
+    success bound, the optimistic side the lower tails with the upper
+    success bound (tests/golden/policy_intervals.json): a swapped pairing
+    flips cells 1 and 2."""
+    g = load_golden("policy_intervals.json")
+    p = Problem(tp=g["tp"], levels=g["levels"], demand=g["demand"], slo=g["slo"], budget=g["budget"])
+    pol = oracle.Policy(limit=np.array(g["limit"], np.float32), success_min=np.array(g["success_min"], np.float32))
+    N = p.n_cells
+    iv = SimpleNamespace(cap_lo=np.ones((1, N), np.float32), cap_hi=np.ones((1, N), np.float32),
+                         tail_lo=np.zeros((1, N), np.float32), tail_hi=np.zeros((1, N), np.float32),
+                         measured=np.zeros((1, N), np.uint8))
+    a = lambda k: np.array([g[k]], np.float32)
+    r = oracle.reduce_intervals(p, pol, iv, a("tail_lo"), a("tail_hi"), a("succ_lo"), a("succ_hi"))
+    assert r.tail_hi.tolist() == [g["conservative_tail_hi"]]
+    assert r.tail_lo.tolist() == [g["optimistic_tail_lo"]]
+    swapped = oracle.reduce_intervals(p, pol, iv, a("tail_lo"), a("tail_hi"), a("succ_hi"), a("succ_lo"))
+    assert swapped.tail_hi.tolist() != [g["conservative_tail_hi"]]
+    assert swapped.tail_lo.tolist() != [g["optimistic_tail_lo"]]

@@ -113,3 +113,39 @@ def test_loop_with_refit_on_structured_tables():
     b = oracle.profile_loop(w.problem, w.intervals, tc, tt, w.cand, cs, ts, eps=0.05, n_threads=8)
     assert (a.state == 1).all() and (a.regret == 0).all()
     assert a.gpu_seconds.sum() <= b.gpu_seconds.sum()
+
+
+def test_clamp_into_refitted_intervals_hand_derived():
+    """Samples are clamped into the refitted intervals (Algorithm 1 refits
+    before every score): below a raised cap_lo, above a lowered tail_hi, and
+    exactly at a bound (tests/golden/clamp_samples.json)."""
+    g = load_golden("clamp_samples.json")
+    p = Problem(tp=g["tp"], levels=g["levels"], demand=g["demand"], slo=g["slo"], budget=g["budget"])
+    iv = _iv(g["intervals"])
+    f = oracle.refit_intervals(p, iv)
+    for k in ("cap_lo", "cap_hi", "tail_lo", "tail_hi"):
+        assert list(getattr(f, k)[0]) == g["refit"][k], k
+    cs, ts = np.array([g["cap_s"]], np.float32), np.array([g["tail_s"]], np.float32)
+    c2, t2 = oracle.clamp_samples(f, g["cand"], cs, ts)
+    assert c2.tolist() == [g["clamped_cap_s"]] and t2.tolist() == [g["clamped_tail_s"]]
+    # the pin separates the refitted intervals from the initial ones
+    c0, t0 = oracle.clamp_samples(iv, g["cand"], cs, ts)
+    assert c0.tolist() != [g["clamped_cap_s"]] and t0.tolist() != [g["clamped_tail_s"]]
+
+
+def test_clamp_properties():
+    """On a workload: clamped samples lie inside the intervals, samples
+    already inside are unchanged, and clamping is idempotent."""
+    w, iv = _random_state("4class-G64-knee", 3, 0.3)
+    w = make_workload("4class-G64-knee", orders=list(range(4)))
+    f = oracle.refit_intervals(w.problem, iv)
+    cs, ts = oracle.clamp_samples(f, w.cand, w.cap_s[:, :, :256], w.tail_s[:, :, :256])
+    lo, hi = f.cap_lo[:, w.cand][:, :, None], f.cap_hi[:, w.cand][:, :, None]
+    assert np.all((cs >= lo) & (cs <= hi))
+    tl, th = f.tail_lo[:, w.cand][:, :, None], f.tail_hi[:, w.cand][:, :, None]
+    assert np.all((ts >= tl) & (ts <= th))
+    inside = (w.cap_s[:, :, :256] >= lo) & (w.cap_s[:, :, :256] <= hi)
+    assert np.array_equal(cs[inside], w.cap_s[:, :, :256][inside])
+    c2, t2 = oracle.clamp_samples(f, w.cand, cs, ts)
+    assert np.array_equal(c2, cs) and np.array_equal(t2, ts)
+    assert (cs != w.cap_s[:, :, :256]).any()  # the refit moved some samples
