@@ -219,6 +219,22 @@ fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals
                               float *d_tau_dump, void *d_workspace, size_t workspace_bytes,
                               hipStream_t stream);
 
+/* fs_score_candidates for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same arguments and results without the workspace, which
+ * is replaced by a static device array of FS_NOALLOC_SCRATCH_BYTES that the
+ * library holds on every GPU it runs on until the process ends.  Sizes whose
+ * fs_workspace_size exceeds it return FS_ERR_UNSUPPORTED.  Every call on one
+ * GPU uses the same array: calls that overlap on one GPU (other streams, other
+ * host threads) race and must be serialised by the caller.  The call makes
+ * no allocation; it ignores FS_OPT_KERNEL_TIMING and the FS_VALIDATE check. */
+#define FS_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+fs_status fs_score_candidates_noalloc(fs_context *ctx, const fs_problem *p, fs_intervals iv,
+                                      int32_t n_orders, const int32_t *d_cand, int32_t n_cand,
+                                      const float *d_cap_s, const float *d_tail_s, int32_t n_samples,
+                                      double *d_score, double *d_gap_now, int32_t *d_best,
+                                      float *d_tau_dump, hipStream_t stream);
+
 /* Three-state certificate (Section 4.2, Algorithm 1) per order:
  *   CERTIFIED_INFEASIBLE if some class is critical and even the optimistic
  *     allocation cannot meet every critical floor;

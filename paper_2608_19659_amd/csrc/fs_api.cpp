@@ -14,6 +14,8 @@
 
 #include "fs_internal.h"
 
+static_assert(fs::kNoAllocScratchBytes == FS_NOALLOC_SCRATCH_BYTES, "scratch size differs from the header");
+
 struct fs_context {
   int device;
   int score_kernel;  // 0 auto, 1 wave per scenario, 2 lane per scenario, 3 exclusion
@@ -25,6 +27,7 @@ struct fs_context {
   int loop_refit;      // profiling loop fit step: 0 off, 1 interval refit every round
   int thr_search;      // exclusion set-up: capacity-threshold search start (0 window, 1 stepping, 2 bisection)
   int32_t *pinned;   // pinned host word: running trajectories read back by fs_profile_loop
+  void *scratch;     // this device's address of the static scratch of fs_score_candidates_noalloc
   struct Timed {
     hipEvent_t begin, end;
     int launches;
@@ -155,7 +158,14 @@ fs_status fs_context_create(int hip_device, fs_context **out) {
   e = hipSetDevice(hip_device);
   if (e == hipSuccess) e = hipHostMalloc((void **)&pinned, 64, hipHostMallocDefault);
   if (e != hipSuccess) return hip_fail(e, "hipHostMalloc");
-  *out = new fs_context{hip_device, 0, 0, 0, 0, 0, 0, 0, 0, pinned, {}};
+  // the static scratch's address on this device (the device is current)
+  void *scratch = nullptr;
+  e = fs::scratch_address(&scratch);
+  if (e != hipSuccess) {
+    (void)hipHostFree(pinned);
+    return hip_fail(e, "hipGetSymbolAddress(scratch)");
+  }
+  *out = new fs_context{hip_device, 0, 0, 0, 0, 0, 0, 0, 0, pinned, scratch, {}};
   return FS_OK;
 }
 
@@ -385,11 +395,15 @@ fs_status fs_score_candidates_lex(fs_context *ctx, const fs_problem *p, fs_inter
   return FS_OK;
 }
 
-fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders,
-                              const int32_t *d_cand, int32_t n_cand, const float *d_cap_s,
-                              const float *d_tail_s, int32_t n_samples, double *d_score,
-                              double *d_gap_now, int32_t *d_best, float *d_tau_dump, void *d_workspace,
-                              size_t workspace_bytes, hipStream_t stream) {
+// fs_score_candidates and its variant without a workspace argument: with
+// noalloc set, the workspace is the library's static device scratch, and
+// neither the timing events (which create HIP events) nor the FS_VALIDATE
+// read-back are used.
+static fs_status score_candidates_impl(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders,
+                                       const int32_t *d_cand, int32_t n_cand, const float *d_cap_s,
+                                       const float *d_tail_s, int32_t n_samples, double *d_score,
+                                       double *d_gap_now, int32_t *d_best, float *d_tau_dump, void *d_workspace,
+                                       size_t workspace_bytes, hipStream_t stream, bool noalloc) {
   if (!ctx) return fail(FS_ERR_INVALID_ARGUMENT, "context is NULL");
   fs::DevProblem P;
   fs_status st = make_problem(p, &P);
@@ -398,10 +412,6 @@ fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals
   if (n_cand < 0 || n_cand > 65535) return fail(FS_ERR_INVALID_ARGUMENT, "n_cand must be in [0, 65535]");
   if (n_cand > 0 && (n_samples < 1 || n_samples > FS_MAX_SAMPLES))
     return fail(FS_ERR_INVALID_ARGUMENT, "n_samples must be in [1, 2^20]");
-  if (n_orders > 0 && (!iv.cap_lo || !iv.cap_hi || !iv.tail_lo || !iv.tail_hi || !iv.measured))
-    return fail(FS_ERR_INVALID_ARGUMENT, "interval arrays are NULL");
-  if (n_orders > 0 && n_cand > 0 && (!d_cand || !d_cap_s || !d_tail_s || !d_score))
-    return fail(FS_ERR_INVALID_ARGUMENT, "candidate, sample or score arrays are NULL");
   int kernel = ctx->score_kernel;
   if (kernel == 0) kernel = fs::excl_kernel_supported(P) ? 3 : 1;
   if (kernel == 2 && !fs::lane_kernel_supported(P))
@@ -413,15 +423,28 @@ fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals
     return fail(FS_ERR_UNSUPPORTED, "exclusion scoring needs n_orders * n_cand < 2^31");
   const int32_t S = n_cand > 0 ? n_samples : 0;
   const fs::WsLayout L = fs::ws_layout(P, n_orders, n_cand, S);
-  if (!d_workspace) return fail(FS_ERR_INVALID_ARGUMENT, "workspace is NULL");
-  if (workspace_bytes < L.total)
-    return fail(FS_ERR_WORKSPACE_TOO_SMALL, "workspace needs " + std::to_string(L.total) + " bytes");
+  // the scratch limit depends on the sizes alone: checked before the arrays
+  if (noalloc && L.total > workspace_bytes)
+    return fail(FS_ERR_UNSUPPORTED, "these sizes need " + std::to_string(L.total) +
+                                        " bytes of scratch; fs_score_candidates_noalloc has " +
+                                        std::to_string(workspace_bytes) + " (use fs_score_candidates)");
+  if (n_orders > 0 && (!iv.cap_lo || !iv.cap_hi || !iv.tail_lo || !iv.tail_hi || !iv.measured))
+    return fail(FS_ERR_INVALID_ARGUMENT, "interval arrays are NULL");
+  if (n_orders > 0 && n_cand > 0 && (!d_cand || !d_cap_s || !d_tail_s || !d_score))
+    return fail(FS_ERR_INVALID_ARGUMENT, "candidate, sample or score arrays are NULL");
+  if (noalloc) {
+    if (!d_workspace) return fail(FS_ERR_INTERNAL, "the device scratch address is unknown");
+  } else {
+    if (!d_workspace) return fail(FS_ERR_INVALID_ARGUMENT, "workspace is NULL");
+    if (workspace_bytes < L.total)
+      return fail(FS_ERR_WORKSPACE_TOO_SMALL, "workspace needs " + std::to_string(L.total) + " bytes");
+  }
   if (n_orders == 0) return FS_OK;
   DeviceGuard dg(ctx->device);
   if (dg.err != hipSuccess) return hip_fail(dg.err, "hipSetDevice");
   uint8_t *ws = (uint8_t *)d_workspace;
   hipError_t e;
-  if (env_validate()) {
+  if (!noalloc && env_validate()) {
     int32_t *flag = (int32_t *)(ws + L.flag);
     const int64_t cells = (int64_t)n_orders * P.N;
     e = fs::launch_zero_flags(flag, stream);
@@ -441,7 +464,7 @@ fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals
   fs::ScoreArgs a{iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi, iv.measured, d_cand, d_cap_s, d_tail_s,
                   n_orders, n_cand, S, d_score, d_gap_now, d_best, d_tau_dump, ws, L, kernel,
                   ctx->spl, ctx->waves, ctx->setup, nullptr, nullptr, 1, ctx->thr_search};
-  if (ctx->timing && n_cand > 0) {
+  if (!noalloc && ctx->timing && n_cand > 0) {
     e = hipEventCreate(&a.ev_begin);
     if (e == hipSuccess) e = hipEventCreate(&a.ev_end);
     if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
@@ -451,6 +474,26 @@ fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals
   e = fs::launch_score(P, a, stream);
   if (e != hipSuccess) return hip_fail(e, "score launch");
   return FS_OK;
+}
+
+fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders,
+                              const int32_t *d_cand, int32_t n_cand, const float *d_cap_s,
+                              const float *d_tail_s, int32_t n_samples, double *d_score,
+                              double *d_gap_now, int32_t *d_best, float *d_tau_dump, void *d_workspace,
+                              size_t workspace_bytes, hipStream_t stream) {
+  return score_candidates_impl(ctx, p, iv, n_orders, d_cand, n_cand, d_cap_s, d_tail_s, n_samples, d_score,
+                               d_gap_now, d_best, d_tau_dump, d_workspace, workspace_bytes, stream, false);
+}
+
+fs_status fs_score_candidates_noalloc(fs_context *ctx, const fs_problem *p, fs_intervals iv, int32_t n_orders,
+                                      const int32_t *d_cand, int32_t n_cand, const float *d_cap_s,
+                                      const float *d_tail_s, int32_t n_samples, double *d_score,
+                                      double *d_gap_now, int32_t *d_best, float *d_tau_dump,
+                                      hipStream_t stream) {
+  if (!ctx) return fail(FS_ERR_INVALID_ARGUMENT, "context is NULL");
+  return score_candidates_impl(ctx, p, iv, n_orders, d_cand, n_cand, d_cap_s, d_tail_s, n_samples, d_score,
+                               d_gap_now, d_best, d_tau_dump, ctx->scratch, fs::kNoAllocScratchBytes, stream,
+                               true);
 }
 
 fs_status fs_loop_workspace_size(const fs_problem *p, int32_t n_orders, int32_t n_cand, int32_t n_samples,

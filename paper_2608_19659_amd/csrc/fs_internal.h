@@ -81,6 +81,11 @@ struct WsLayout {
 
 WsLayout ws_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S);
 
+// Static device scratch of fs_score_candidates_noalloc (FS_NOALLOC_SCRATCH_BYTES
+// in the public header), and its address on the current device.
+constexpr size_t kNoAllocScratchBytes = (size_t)32 << 20;
+hipError_t scratch_address(void **ptr);
+
 // Lane-per-scenario scoring supports these shapes.
 bool lane_kernel_supported(const DevProblem &P);
 int lane_kernel_options(int G);

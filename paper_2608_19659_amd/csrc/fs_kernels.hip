@@ -3205,6 +3205,16 @@ int lane_kernel_options(int G) { return G + G / 2 + G / 4 + G / 8; }
 
 bool excl_kernel_supported(const DevProblem &P) { return !P.has_floor; }
 
+// Workspace of fs_score_candidates_noalloc, for callers that cannot
+// allocate: one copy per GPU the library runs on, held until the process
+// ends, shared by every such call on that GPU.  Host code must not pass the
+// name itself to a kernel (on the host it is a stand-in, not a device
+// address): it uses the address scratch_address() returns, taken once per
+// device when a context is created.
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+
+hipError_t scratch_address(void **ptr) { return hipGetSymbolAddress(ptr, HIP_SYMBOL(scratch)); }
+
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // Dynamic LDS the exclusion set-up kernel may request, and its block size

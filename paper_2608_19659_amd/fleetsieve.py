@@ -37,7 +37,8 @@ EXPORTED = ("fs_context_create", "fs_context_destroy", "fs_context_set_option", 
             "fs_validate_problem", "fs_workspace_size", "fs_solve_batch", "fs_score_candidates",
             "fs_certify", "fs_loop_workspace_size", "fs_profile_loop", "fs_reduce_cells", "fs_reduce_samples",
             "fs_solve_batch_lex", "fs_certify_lex", "fs_refit_intervals", "fs_loop_refit_workspace_size",
-            "fs_score_lex_workspace_size", "fs_score_candidates_lex", "fs_clamp_samples")
+            "fs_score_lex_workspace_size", "fs_score_candidates_lex", "fs_clamp_samples",
+            "fs_score_candidates_noalloc")
 POLICY_SCORE, POLICY_ORDER = 0, 1
 CELL_SECONDS = 300.0
 
@@ -112,6 +113,7 @@ def load_library():
     lib.fs_refit_intervals.argtypes = [vp, P, _Intervals, i32, vp, vp, vp, vp]
     lib.fs_loop_refit_workspace_size.argtypes = [P, i32, i32, i32, ctypes.POINTER(sz)]
     lib.fs_clamp_samples.argtypes = [vp, P, _Intervals, i32, vp, i32, vp, vp, i32, vp, vp, vp]
+    lib.fs_score_candidates_noalloc.argtypes = [vp, P, _Intervals, i32, vp, i32, vp, vp, i32, vp, vp, vp, vp, vp]
     lib.fs_solve_batch_lex.argtypes = [vp, P, vp, vp, i64, _Alloc, vp, vp, sz, vp]
     lib.fs_certify_lex.argtypes = [vp, P, _Intervals, i32, ctypes.c_float, vp, _Alloc, _Alloc, vp, vp, vp, sz, vp]
     Q = ctypes.POINTER(_SloPolicy)
@@ -356,6 +358,28 @@ class ScorePlan:
     def run(self) -> ScoreOutput:
         _check(self._fn(*self._args))
         return self.out
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20
+
+
+def score_candidates_noalloc(ctx: Context, problem, iv: DeviceIntervals, cand, cap_s, tail_s,
+                             out: "ScoreOutput", stream=None) -> "ScoreOutput":
+    """fs_score_candidates_noalloc: the scorer without a workspace (the
+    library's static device scratch); the caller passes the outputs."""
+    torch = _torch()
+    ref = _ProblemRef(problem)
+    O = int(iv.cap_lo.shape[0])
+    E = int(cand.shape[0])
+    S = int(cap_s.shape[2]) if E > 0 else 0
+    ivs = _intervals_struct(iv, O, ref.N)
+    _check(load_library().fs_score_candidates_noalloc(
+        ctx.handle, ref.ptr, ivs, O, _dev_ptr(cand, torch.int32, (E,), "cand"),
+        E, _dev_ptr(cap_s, torch.float32, (O, E, S), "cap_s"), _dev_ptr(tail_s, torch.float32, (O, E, S), "tail_s"),
+        S, _dev_ptr(out.score, torch.float64, (O, E), "score"), _dev_ptr(out.gap_now, torch.float64, (O,), "gap_now"),
+        _dev_ptr(out.best, torch.int32, (O,), "best"), _dev_ptr(out.tau_dump, torch.float32, (O, E, S, 2), "tau_dump"),
+        _stream(iv.cap_lo.device, stream)))
+    return out
 
 
 def score_candidates(ctx: Context, problem, iv: DeviceIntervals, cand, cap_s, tail_s, dump: bool = False,
