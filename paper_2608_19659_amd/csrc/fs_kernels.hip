@@ -1292,6 +1292,14 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
 // Largest budget and class count of the one-block-per-order set-up.
 constexpr int kPrepOrderMaxG = kWave;
 constexpr int kPrepOrderMaxK = 16;
+
+// Load level of every (class k, replica count r) for the set-up with one
+// block per order, from the problem statement alone (filled on the host,
+// passed by value): lvl[k * kPrepOrderMaxG + r - 1] is the smallest level
+// holding lambda_k / r (binary32), -1 when none does.
+struct PrepLevels {
+  int8_t lvl[kPrepOrderMaxK * kPrepOrderMaxG];
+};
 // Wavefronts per block of the per-order set-up: one per class, and one per
 // 1024 listed tiles (at most 16) so the work-list block has threads enough
 // for large lists; a class block's wavefronts beyond K only help stage the
@@ -1320,9 +1328,9 @@ static int prep_order_waves(const DevProblem &P, int64_t O, int64_t E) {
 // LDS: bucket counters and starts (2 x 32 + 4), the level ranges (2 x K x B),
 // per candidate its cell and range code (2 x E), the revealed flags (O x N
 // bytes).
-__device__ void prep_list_staged(const DevProblem &P, int O, const uint8_t *__restrict__ measured,
-                                 const int32_t *__restrict__ cand, int E, int dump, int PPc,
-                                 TileInfo *__restrict__ tiles, int4 *__restrict__ list,
+__device__ void prep_list_staged(const DevProblem &P, const PrepLevels &LV, int O,
+                                 const uint8_t *__restrict__ measured, const int32_t *__restrict__ cand, int E,
+                                 int dump, int PPc, TileInfo *__restrict__ tiles, int4 *__restrict__ list,
                                  int32_t *__restrict__ n_listed, int *lds) {
   const int tid = threadIdx.x, nth = blockDim.x, lane = tid & (kWave - 1);
   const int N = P.N, G = P.G, K = P.K, B = P.B, per_class = P.NT * P.B;
@@ -1331,10 +1339,8 @@ __device__ void prep_list_staged(const DevProblem &P, int O, const uint8_t *__re
   int *c_cell = lv_last + K * B, *c_code = c_cell + E;
   uint8_t *meas = reinterpret_cast<uint8_t *>(c_code + E);
   __shared__ int c_tp[kMaxTp], c_optoff[kMaxTp + 1];
-  __shared__ float c_demand[kPrepOrderMaxK];
   if (tid < P.NT) c_tp[tid] = P.tp[tid];
   if (tid <= P.NT) c_optoff[tid] = P.optoff[tid];
-  if (tid < K) c_demand[tid] = P.demand[tid];
   if (tid < 32) bucket_count[tid] = 0;
   for (int x = tid; x < K * B; x += nth) {
     lv_first[x] = INT_MAX;
@@ -1346,8 +1352,8 @@ __device__ void prep_list_staged(const DevProblem &P, int O, const uint8_t *__re
   // one thread per (class, replica count)
   for (int x = tid; x < K * G; x += nth) {
     const int k = x / G, r = x - k * G + 1;
-    const int b = levels_below(P, c_demand[k] / (float)r);
-    if (b < B) {
+    const int b = LV.lvl[k * kPrepOrderMaxG + r - 1];
+    if (b >= 0) {
       atomicMin(&lv_first[k * B + b], r);
       atomicMax(&lv_last[k * B + b], r);
     }
@@ -1454,21 +1460,22 @@ __device__ void prep_list_staged(const DevProblem &P, int O, const uint8_t *__re
 //   1. all threads: the order's cells and candidates into LDS; the load
 //      level of every (class, r) (the count of grid levels below
 //      lambda / r is the index of the smallest level holding it)
-//   2. wavefront k: B_k, the best ratio of class k with at most g GPUs, by
-//      max-merging every option into its exact GPU count, then a prefix max
-//   3. wavefront i, on its own: H_i, the (max,min) convolution of the other
-//      classes' tables (a chain of crossing searches over nondecreasing
-//      tables); per option of class i, M = H_i[G - t r] clamped at 1, the
-//      capacity threshold of M and w = min(f, M) folded into its cell's
-//      maximum; U of each of its candidates from the two largest cell
-//      maxima; tile records; the base objective (class 0).
+//   2. wavefront k: B_k, the best ratio of class k with at most g GPUs: per
+//      budget the options of exactly that cost, then a prefix maximum
+//   3. wavefront j: the rank of each value of B_j among the other tables,
+//      scattered into every H_i (i != j); H_i, the (max,min) convolution of
+//      the tables but B_i, is the prefix maximum of that scatter
+//   4. wavefront i, on its own: per option of class i, M = H_i[G - t r]
+//      clamped at 1, the capacity threshold of M and w = min(f, M) folded
+//      into its cell's maximum; U of each of its candidates from the two
+//      largest cell maxima; tile records; the base objective (class 0).
 // Tables cover g in [0, G) (option costs t r >= 1 read H at G - t r < G).
 //
-// LDS of a class block: cells (2N floats), the B tables (K x G), the
-// candidates (E), per class wavefront (two per class when K <= 8) 2G + 3 NT B
-// ints (convolution buffers, cell maxima, replica ranges), the order's
-// revealed flags (N bytes, padded to 4)
-// and the load levels (K x G bytes).
+// LDS of a class block: cells (2N floats), the B tables and the H scatter
+// (2 x K x G), the candidates (E), per class wavefront (two per class when
+// K <= 8) 3 NT B ints (cell maxima, replica ranges), the order's revealed
+// flags (N bytes, padded to 4) and the load levels (K x G bytes).
+template <int KP>
 __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *__restrict__ cap_lo,
                                                      const float *__restrict__ cap_hi,
                                                      const float *__restrict__ tail_lo,
@@ -1479,30 +1486,30 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
                                                      int32_t *__restrict__ base, int32_t *__restrict__ mopt,
                                                      float *__restrict__ thr, int32_t n_thr,
                                                      int4 *__restrict__ list, int32_t *__restrict__ n_listed,
-                                                     int32_t thr_mode) {
+                                                     int32_t thr_mode, const PrepLevels LV) {
   extern __shared__ int lds[];
   const int tid = threadIdx.x, nth = blockDim.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int G = P.G, K = P.K, N = P.N, NT = P.NT, B = P.B, per_class = NT * B;
   const int PPc = n_thr / K;
   if ((int)blockIdx.x == 2 * O) {
-    prep_list_staged(P, O, measured, cand, E, dump, PPc, tiles, list, n_listed, lds);
+    prep_list_staged(P, LV, O, measured, cand, E, dump, PPc, tiles, list, n_listed, lds);
     return;
   }
   const int o = blockIdx.x >> 1, R = blockIdx.x & 1;
   float *ccap = reinterpret_cast<float *>(lds);
   float *ctail = ccap + N;
-  int *Bt = reinterpret_cast<int *>(ctail + N);  // [K][G]
-  int *ccand = Bt + K * G;                       // [E]
-  const int wstride = 2 * G + 3 * per_class;
+  int *Bt = reinterpret_cast<int *>(ctail + N);  // [K][G] B tables
+  int *Hs = Bt + K * G;                          // [K][G] rank scatter of H
+  int *ccand = Hs + K * G;                       // [E]
+  const int wstride = 3 * per_class;
   // per-wavefront areas: one per class, two when a second wavefront per
   // class computes the thresholds (at most 8 classes)
   const int nwa = (int)(blockDim.x >> 6) >= 2 * K ? 2 * K : K;
   int *wbase = ccand + E;                        // [nwa][wstride]
   uint8_t *mrow = reinterpret_cast<uint8_t *>(wbase + nwa * wstride);  // [N]
   int8_t *lvl = reinterpret_cast<int8_t *>(mrow + ((N + 3) & ~3));   // [K][G]
-  int *Xa = wbase + wave * wstride, *Xb = Xa + G;
-  int *mc = Xb + G, *crlo = mc + per_class, *crhi = crlo + per_class;
+  int *mc = wbase + wave * wstride, *crlo = mc + per_class, *crhi = crlo + per_class;
   const size_t off = (size_t)o * N;
   const float *gcap = (R == 0 ? cap_lo : cap_hi) + off;
   const float *gtail = (R == 0 ? tail_hi : tail_lo) + off;
@@ -1510,10 +1517,12 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
   // the TP degrees and option offsets in registers: read unconditionally
   // (a few wide scalar loads), so later loops over TP degrees touch no memory
   int tpr[kMaxTp], ofr[kMaxTp];
+  float tpinv[kMaxTp];
 #pragma unroll
   for (int j = 0; j < kMaxTp; ++j) {
     tpr[j] = P.tp[j];
     ofr[j] = P.optoff[j];
+    tpinv[j] = tpr[j] > 0 ? 1.0f / (float)tpr[j] : 0.0f;
   }
 
   // --- 1. stage the order; load levels while the loads are in flight
@@ -1526,10 +1535,7 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
     if (R == 0) mrow[c] = measured[off + c];
   }
   for (int e = tid; e < E; e += nth) ccand[e] = cand[e];
-  if (wave < K && lane < G) {  // wavefront k: the levels of class k, r = lane + 1
-    const int b = levels_below(P, P.demand[wave] / (float)(lane + 1));
-    lvl[wave * G + lane] = (int8_t)(b < B ? b : -1);
-  }
+  if (wave < K && lane < G) lvl[wave * G + lane] = LV.lvl[wave * kPrepOrderMaxG + lane];  // r = lane + 1
   for (int c = lane; wave < K && c < per_class; c += kWave) {
     mc[c] = INT_MIN;
     crlo[c] = INT_MAX;
@@ -1537,32 +1543,105 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
   }
   __syncthreads();
 
-  // --- 2. wavefront k: B_k (options cost t r < G <= 64, so r < 64: one
-  // lane per replica count)
+  // --- 2. wavefront k: B_k, one lane per budget g < G.  The options of
+  // exact cost g are (t, g / t) for the TP degrees t dividing g; each reads
+  // its cell from LDS (all reads independent), then a prefix maximum over
+  // the lanes.  The table goes to LDS for the other wavefronts and stays in
+  // a register; the scatter targets of step 3 are cleared meanwhile.
+  int btab = 0;
   if (wave < K) {
     const int k = wave;
-    int *T = Bt + k * G;
-    if (lane < G) T[lane] = 0;  // no option: ratio 0
-    wave_lds_fence();
     const float slo = P.slo[k];
     const double rcp = P.rcp_demand[k];
-    const int r = lane + 1;
-    const int b = lane < G ? lvl[k * G + r - 1] : -1;
+    const int g = lane;
+    // all reads of a kind issued together: the levels of every (t, g / t),
+    // then their cells
+    int rr[kMaxTp], bb[kMaxTp];
+    bool ok[kMaxTp];
 #pragma unroll
     for (int ti = 0; ti < kMaxTp; ++ti) {
       const int t = tpr[ti];
-      if (ti < NT && t * r < G && b >= 0) {
-        const int cell = (k * NT + ti) * B + b;
-        atomicMax(&T[t * r], ratio_bits(ccap[cell], ctail[cell], r, slo, rcp));
-      }
+      // g / t, exact whenever t divides g (g < 64, t <= 4096: the float
+      // quotient is within 1/2 of it)
+      const int r = (int)((float)g * tpinv[ti] + 0.5f);
+      ok[ti] = ti < NT && g > 0 && g < G && r >= 1 && r * t == g;
+      rr[ti] = ok[ti] ? r : 1;
+      bb[ti] = lvl[k * G + rr[ti] - 1];
     }
-    wave_lds_fence();
-    const int v = wave_scan_max_nonneg(lane < G ? T[lane] : 0, lane);
-    if (lane < G) T[lane] = v;
+    __builtin_amdgcn_sched_barrier(0);
+    float cc[kMaxTp], ct[kMaxTp];
+#pragma unroll
+    for (int ti = 0; ti < kMaxTp; ++ti) {
+      const int cell = (k * NT + min(ti, NT - 1)) * B + max(bb[ti], 0);
+      cc[ti] = ccap[cell];
+      ct[ti] = ctail[cell];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    int best = 0;  // budget 0 and costs no option has: ratio 0
+#pragma unroll
+    for (int ti = 0; ti < kMaxTp; ++ti) {
+      const int f = ratio_bits(cc[ti], ct[ti], rr[ti], slo, rcp);
+      best = max(best, ok[ti] && bb[ti] >= 0 ? f : 0);
+    }
+    btab = wave_scan_max_nonneg(best, lane);
+    if (lane < G) {
+      Bt[k * G + lane] = btab;
+      Hs[k * G + lane] = 0;  // ratio 0: the smallest value a table holds
+    }
   }
   __syncthreads();
 
-  // --- 3. wavefront i on its own from here.  With at most 8 classes a
+  // --- 3. H_i, the (max,min) convolution of every table but B_i.  For
+  // nondecreasing tables the convolution of two is the first G entries of
+  // their sorted merge (H[g] >= v iff the entries below v, counted in both,
+  // number at most g), so H_i[g] is the entry of rank g in the union of the
+  // other classes' tables: every value v of B_j goes to H_i at index
+  // rank_i(v) = (entries below v in every table but B_i), with the largest
+  // value per index kept, and a prefix maximum fills the rest.  Wavefront j
+  // counts, for each v of its own table (first occurrences only), the
+  // entries below v in every table by a bisection over register copies of
+  // the tables (cross-lane reads by ds_bpermute, all K searches
+  // interleaved), and scatters v into the K - 1 targets.
+  if (wave < K && K > 1) {
+    const int j = wave;
+    // KP >= K tables, those past K empty (INT_MAX: never below v), so that
+    // the searches are straight-line code whatever K is
+    int tb[KP];
+#pragma unroll
+    for (int k = 0; k < KP; ++k) {
+      const int x = Bt[min(k, K - 1) * G + min(lane, G - 1)];
+      tb[k] = k < K && lane < G ? x : INT_MAX;
+    }
+    const int v = btab;
+    const int prev = __builtin_amdgcn_ds_bpermute(4 * (lane > 0 ? lane - 1 : 0), v);
+    const bool first = lane < G && (lane == 0 || prev != v);
+    int cnt[KP];
+#pragma unroll
+    for (int k = 0; k < KP; ++k) cnt[k] = 0;
+    // cnt counts the entries below v: after the steps 64, 32, ..., 1 it is
+    // the first index whose entry is not below v (entries past G are
+    // INT_MAX, never below)
+#pragma unroll
+    for (int step = kWave; step > 0; step >>= 1) {
+      int e[KP];
+#pragma unroll
+      for (int k = 0; k < KP; ++k) e[k] = __builtin_amdgcn_ds_bpermute(4 * min(cnt[k] + step - 1, kWave - 1), tb[k]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int k = 0; k < KP; ++k) cnt[k] += (cnt[k] + step - 1 < kWave && e[k] < v) ? step : 0;
+    }
+    int tot = 0;
+#pragma unroll
+    for (int k = 0; k < KP; ++k) tot += cnt[k];
+#pragma unroll
+    for (int k = 0; k < KP; ++k) {
+      const int rank = tot - cnt[k];
+      if (k < K && k != j && first && rank < G) atomicMax(&Hs[k * G + rank], v);
+    }
+  }
+  __syncthreads();
+
+  // --- 4. wavefront i on its own from here.  With at most 8 classes a
   // second wavefront per class (K + i) computes the same H_i and only the
   // capacity thresholds, which nothing else in the block needs, so the
   // first one goes on to U and the records without them.
@@ -1571,26 +1650,9 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
   const bool thr_wave = wave >= K;
   const bool do_thr = !split || thr_wave, do_cells = !split || !thr_wave;
   const int i = thr_wave ? wave - K : wave;
-  int top = 1;
-  while (2 * top <= G) top <<= 1;  // 2 * top > G >= g + 1
-  const int *H;
-  if (K == 1) {
-    if (lane < G) Xa[lane] = INT_MAX;  // the empty convolution
-    wave_lds_fence();
-    H = Xa;
-  } else {
-    const int k0 = i == 0 ? 1 : 0;
-    const int *X = Bt + k0 * G;
-    int *dst = Xa;
-    for (int k = k0 + 1; k < K; ++k) {
-      if (k == i) continue;
-      if (lane < G) dst[lane] = conv_mono(X, Bt + k * G, lane, top);
-      wave_lds_fence();
-      X = dst;
-      dst = dst == Xa ? Xb : Xa;
-    }
-    H = X;
-  }
+  // H_i in a register (lane g: H_i[g]); with one class, the empty
+  // convolution (no other class constrains the budget)
+  const int hreg = K == 1 ? INT_MAX : wave_scan_max_nonneg(lane < G ? Hs[i * G + lane] : 0, lane);
   {
     int32_t *Mo = mopt + ((size_t)o * 2 + R) * n_thr + (size_t)i * PPc;
     float *To = thr + ((size_t)o * 2 + R) * n_thr + (size_t)i * PPc;
@@ -1622,7 +1684,7 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
         const int b = has[u] ? bl : -1;
         ok[u] = b >= 0;
         const int local = ti * B + (ok[u] ? b : 0), cell = i * per_class + local;
-        const int hv = H[G - t * r];
+        const int hv = __builtin_amdgcn_ds_bpermute(4 * max(G - t * r, 0), hreg);
         const float cc = ccap[cell], ct = ctail[cell];
         // ratios never exceed 1, so M above 1 acts as 1 (min(f, M) and the
         // crossing are unchanged) and the scorer can skip the clamp of f
@@ -3237,7 +3299,7 @@ static size_t prep_lds_tables(const DevProblem &P) { return 3 * sizeof(int) * (s
 static size_t prep_order_lds(const DevProblem &P, int64_t O, int64_t E) {
   const size_t K = P.K, G = P.G, N = P.N, pc = (size_t)P.NT * P.B;
   const size_t nw = 2 * K <= 16 ? 2 * K : K;  // wavefronts with a per-wavefront area
-  const size_t cls = 4 * (2 * N + K * G + (size_t)E + nw * (2 * G + 3 * pc)) + ((N + 3) & ~(size_t)3) + K * G;
+  const size_t cls = 4 * (2 * N + 2 * K * G + (size_t)E + nw * 3 * pc) + ((N + 3) & ~(size_t)3) + K * G;
   const size_t lst = 4 * (68 + 2 * K * (size_t)P.B + 2 * (size_t)E) + (size_t)O * N;
   return cls > lst ? cls : lst;
 }
@@ -3306,11 +3368,28 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
     const int32_t n_thr = excl_thresholds(P);
     const int dump = a.tau_dump != nullptr;
     const size_t small = prep_lds_small(P), big = small + prep_lds_tables(P);
-    if (a.setup == 0 && prep_order_fits(P, a.O, a.E))
-      k_prep_order<<<2 * a.O + 1, prep_order_waves(P, a.O, a.E) * kWave, prep_order_lds(P, a.O, a.E), s>>>(
-          P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured, a.cand, a.E, a.O, dump, tiles, base, mopt,
-          thr, n_thr, list, live, a.thr_search);
-    else if (big <= kPrepLdsLimit)
+    if (a.setup == 0 && prep_order_fits(P, a.O, a.E)) {
+      // the smallest level holding lambda / r; it falls as r grows, so one
+      // pass over r per class moves it downwards only
+      PrepLevels LV{};
+      for (int k = 0; k < P.K; ++k) {
+        int b = P.B;
+        for (int r = 1; r <= P.G; ++r) {
+          const float u = P.demand[k] / (float)r;
+          while (b > 0 && !(P.levels[b - 1] < u)) --b;
+          LV.lvl[k * kPrepOrderMaxG + r - 1] = (int8_t)(b < P.B ? b : -1);
+        }
+      }
+      // the rank step's table count, rounded up to 4, 8 or 16
+#define FS_PREP_ORDER(KP)                                                                                         \
+  k_prep_order<KP><<<2 * a.O + 1, prep_order_waves(P, a.O, a.E) * kWave, prep_order_lds(P, a.O, a.E), s>>>(         \
+      P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured, a.cand, a.E, a.O, dump, tiles, base, mopt, thr,  \
+      n_thr, list, live, a.thr_search, LV)
+      if (P.K <= 4) FS_PREP_ORDER(4);
+      else if (P.K <= 8) FS_PREP_ORDER(8);
+      else FS_PREP_ORDER(16);
+#undef FS_PREP_ORDER
+    } else if (big <= kPrepLdsLimit)
       k_prep<true><<<dim3(2, a.O, P.K + 1), kPrepThreads, big, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
                                                           a.measured, a.cand, a.E, dump, nullptr, tiles,
                                                           base, mopt, thr, n_thr, list, live, a.thr_search);
