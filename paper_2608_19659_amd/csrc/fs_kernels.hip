@@ -1475,7 +1475,7 @@ __device__ void prep_list_staged(const DevProblem &P, const PrepLevels &LV, int 
 // (2 x K x G), the candidates (E), per class wavefront (two per class when
 // K <= 8) 3 NT B ints (cell maxima, replica ranges), the order's revealed
 // flags (N bytes, padded to 4) and the load levels (K x G bytes).
-template <int KP>
+template <int KP, int NTP>
 __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *__restrict__ cap_lo,
                                                      const float *__restrict__ cap_hi,
                                                      const float *__restrict__ tail_lo,
@@ -1516,10 +1516,10 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
 
   // the TP degrees and option offsets in registers: read unconditionally
   // (a few wide scalar loads), so later loops over TP degrees touch no memory
-  int tpr[kMaxTp], ofr[kMaxTp];
-  float tpinv[kMaxTp];
+  int tpr[NTP], ofr[NTP];
+  float tpinv[NTP];
 #pragma unroll
-  for (int j = 0; j < kMaxTp; ++j) {
+  for (int j = 0; j < NTP; ++j) {
     tpr[j] = P.tp[j];
     ofr[j] = P.optoff[j];
     tpinv[j] = tpr[j] > 0 ? 1.0f / (float)tpr[j] : 0.0f;
@@ -1556,10 +1556,10 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
     const int g = lane;
     // all reads of a kind issued together: the levels of every (t, g / t),
     // then their cells
-    int rr[kMaxTp], bb[kMaxTp];
-    bool ok[kMaxTp];
+    int rr[NTP], bb[NTP];
+    bool ok[NTP];
 #pragma unroll
-    for (int ti = 0; ti < kMaxTp; ++ti) {
+    for (int ti = 0; ti < NTP; ++ti) {
       const int t = tpr[ti];
       // g / t, exact whenever t divides g (g < 64, t <= 4096: the float
       // quotient is within 1/2 of it)
@@ -1569,9 +1569,9 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
       bb[ti] = lvl[k * G + rr[ti] - 1];
     }
     __builtin_amdgcn_sched_barrier(0);
-    float cc[kMaxTp], ct[kMaxTp];
+    float cc[NTP], ct[NTP];
 #pragma unroll
-    for (int ti = 0; ti < kMaxTp; ++ti) {
+    for (int ti = 0; ti < NTP; ++ti) {
       const int cell = (k * NT + min(ti, NT - 1)) * B + max(bb[ti], 0);
       cc[ti] = ccap[cell];
       ct[ti] = ctail[cell];
@@ -1579,7 +1579,7 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
     __builtin_amdgcn_sched_barrier(0);
     int best = 0;  // budget 0 and costs no option has: ratio 0
 #pragma unroll
-    for (int ti = 0; ti < kMaxTp; ++ti) {
+    for (int ti = 0; ti < NTP; ++ti) {
       const int f = ratio_bits(cc[ti], ct[ti], rr[ti], slo, rcp);
       best = max(best, ok[ti] && bb[ti] >= 0 ? f : 0);
     }
@@ -1669,7 +1669,7 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
         const int p = base + lane + u * kWave;
         int ti = 0, first = 0, t = tpr[0];
 #pragma unroll
-        for (int t2 = 1; t2 < kMaxTp; ++t2) {
+        for (int t2 = 1; t2 < NTP; ++t2) {
           const bool in = t2 < NT && p >= ofr[t2];
           ti = in ? t2 : ti;
           first = in ? ofr[t2] : first;
@@ -3380,14 +3380,22 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
           LV.lvl[k * kPrepOrderMaxG + r - 1] = (int8_t)(b < P.B ? b : -1);
         }
       }
-      // the rank step's table count, rounded up to 4, 8 or 16
-#define FS_PREP_ORDER(KP)                                                                                         \
-  k_prep_order<KP><<<2 * a.O + 1, prep_order_waves(P, a.O, a.E) * kWave, prep_order_lds(P, a.O, a.E), s>>>(         \
+      // compiled for the rank step's table count rounded up to 4, 8 or 16
+      // and for at most 4 or 8 TP degrees (loops over them are unrolled)
+#define FS_PREP_ORDER(KP, NTP)                                                                                    \
+  k_prep_order<KP, NTP><<<2 * a.O + 1, prep_order_waves(P, a.O, a.E) * kWave, prep_order_lds(P, a.O, a.E), s>>>(    \
       P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured, a.cand, a.E, a.O, dump, tiles, base, mopt, thr,  \
       n_thr, list, live, a.thr_search, LV)
-      if (P.K <= 4) FS_PREP_ORDER(4);
-      else if (P.K <= 8) FS_PREP_ORDER(8);
-      else FS_PREP_ORDER(16);
+#define FS_PREP_ORDER_K(NTP)                  \
+  if (P.K <= 4) FS_PREP_ORDER(4, NTP);        \
+  else if (P.K <= 8) FS_PREP_ORDER(8, NTP);   \
+  else FS_PREP_ORDER(16, NTP);
+      if (P.NT <= 4) {
+        FS_PREP_ORDER_K(4)
+      } else {
+        FS_PREP_ORDER_K(8)
+      }
+#undef FS_PREP_ORDER_K
 #undef FS_PREP_ORDER
     } else if (big <= kPrepLdsLimit)
       k_prep<true><<<dim3(2, a.O, P.K + 1), kPrepThreads, big, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
