@@ -20,7 +20,10 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "fs_oracle.c")
-_LIB = os.path.join(_HERE, "liboracle.so")
+# FLEETSIEVE_ORACLE_LIB selects another build of fs_oracle.c (for example
+# one compiled with sanitizers); the default is the one build() writes here.
+_BUILT = os.path.join(_HERE, "liboracle.so")
+_LIB = os.environ.get("FLEETSIEVE_ORACLE_LIB") or _BUILT
 
 MAX_CLASSES = 64
 UNDECIDED, CERTIFIED_FEASIBLE, CERTIFIED_INFEASIBLE = 0, 1, 2
@@ -28,14 +31,14 @@ UNDECIDED, CERTIFIED_FEASIBLE, CERTIFIED_INFEASIBLE = 0, 1, 2
 
 def build(force: bool = True) -> str:
     """Compile the oracle with gcc: binary32 arithmetic, no contraction."""
-    if force or not os.path.exists(_LIB):
-        tmp = _LIB + ".tmp"
+    if force or not os.path.exists(_BUILT):
+        tmp = _BUILT + ".tmp"
         cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp",
                "-ffp-contract=off", "-fno-fast-math", "-Wall", "-Wextra",
                "-o", tmp, _SRC, "-lm"]
         subprocess.run(cmd, check=True, cwd=_HERE)
-        os.replace(tmp, _LIB)
-    return _LIB
+        os.replace(tmp, _BUILT)
+    return _BUILT
 
 
 class _Problem(ctypes.Structure):

@@ -15,7 +15,9 @@ from dataclasses import dataclass
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libfleetsieve.so")
+# FLEETSIEVE_LIB selects another build of the library (for example one whose
+# host code is compiled with sanitizers); the default is the in-tree build.
+LIB_PATH = os.environ.get("FLEETSIEVE_LIB") or os.path.join(_HERE, "libfleetsieve.so")
 
 FS_OK, FS_ERR_INVALID_ARGUMENT, FS_ERR_UNSUPPORTED, FS_ERR_WORKSPACE_TOO_SMALL, FS_ERR_DEVICE, \
     FS_ERR_INTERNAL = range(6)

@@ -157,3 +157,35 @@ def test_clamp_matches_oracle(env, name, seed, frac, S):
     np.testing.assert_array_equal(got_c.view(np.uint32), want_c.view(np.uint32))
     np.testing.assert_array_equal(got_t.view(np.uint32), want_t.view(np.uint32))
     assert (want_c != cs).any() or (want_t != ts).any()
+
+
+@pytest.mark.parametrize("case", range(2))
+def test_fit_step_saves_a_reveal_on_gpu(env, case):
+    """The hand-derived loop of tests/golden/refit_loop.json on the GPU:
+    with the fit step the refitted tail closes the gap and the loop
+    certifies with no reveal; without it one reveal is paid."""
+    torch, fs, ctx = env
+    g = load_golden("refit_loop.json")
+    c = g["cases"][case]
+    p = Problem(tp=g["tp"], levels=g["levels"], demand=g["demand"], slo=g["slo"], budget=g["budget"])
+    d = g["intervals"]
+    iv = Intervals(*(np.array([d[k]], np.float32) for k in ("cap_lo", "cap_hi", "tail_lo", "tail_hi")),
+                   np.array([d["measured"]], np.uint8))
+    note(f"refit loop golden case refit={c['refit']}")
+    try:
+        r = fs.profile_loop(ctx, p, fs.DeviceIntervals.from_host(iv, "cuda:0"),
+                            _t(env, np.array([g["truth_cap"]], np.float32)),
+                            _t(env, np.array([g["truth_tail"]], np.float32)), _t(env, np.array(g["cand"], np.int32)),
+                            _t(env, np.array([g["cap_s"]], np.float32)), _t(env, np.array([g["tail_s"]], np.float32)),
+                            eps=g["eps"], refit=c["refit"])
+        torch.cuda.synchronize()
+    finally:
+        ctx.set_option(fs.OPT_LOOP_REFIT, 0)
+    assert int(r.state.cpu()[0]) == 1
+    assert int(r.rounds.cpu()[0]) == c["rounds"]
+    assert list(r.reveals.cpu().numpy()[0][: c["rounds"]]) == c["reveals"]
+    assert float(r.gpu_seconds.cpu()[0]) == c["gpu_seconds"]
+    assert list(r.final["tp_index"].cpu().numpy()[0]) == c["final_tp_index"]
+    assert list(r.final["replicas"].cpu().numpy()[0].view(np.uint16)) == c["final_replicas"]
+    assert float(r.final["objective"].cpu()[0]) == np.float32(c["final_tau"])
+    assert float(r.tau_truth.cpu()[0]) == np.float32(c["tau_truth"])

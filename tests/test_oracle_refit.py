@@ -149,3 +149,26 @@ def test_clamp_properties():
     c2, t2 = oracle.clamp_samples(f, w.cand, cs, ts)
     assert np.array_equal(c2, cs) and np.array_equal(t2, ts)
     assert (cs != w.cap_s[:, :, :256]).any()  # the refit moved some samples
+
+
+@pytest.mark.parametrize("case", range(2))
+def test_fit_step_saves_a_reveal_hand_derived(case):
+    """A loop in which the fit step decides (tests/golden/refit_loop.json):
+    the refitted tail of the only candidate lies above the SLO, the gap
+    closes and the loop certifies with no reveal, where the loop without
+    the fit step pays one reveal (300 GPU-s) for the same allocation."""
+    from paper_2608_19659_amd.synth import Intervals
+    g = load_golden("refit_loop.json")
+    c = g["cases"][case]
+    p = Problem(tp=g["tp"], levels=g["levels"], demand=g["demand"], slo=g["slo"], budget=g["budget"])
+    d = g["intervals"]
+    iv = Intervals(*(np.array([d[k]], np.float32) for k in ("cap_lo", "cap_hi", "tail_lo", "tail_hi")),
+                   np.array([d["measured"]], np.uint8))
+    r = oracle.profile_loop(p, iv, [g["truth_cap"]], [g["truth_tail"]], g["cand"], np.array([g["cap_s"]], np.float32),
+                            np.array([g["tail_s"]], np.float32), eps=g["eps"], refit=c["refit"])
+    assert r.state[0] == oracle.CERTIFIED_FEASIBLE
+    assert r.rounds[0] == c["rounds"] and list(r.reveals[0][: r.rounds[0]]) == c["reveals"]
+    assert r.gpu_seconds[0] == c["gpu_seconds"]
+    assert r.final[0].tp_index == c["final_tp_index"] and r.final[0].replicas == c["final_replicas"]
+    assert r.final[0].tau == np.float32(c["final_tau"])
+    assert r.tau_truth[0] == np.float32(c["tau_truth"]) and r.tau_oracle[0] == np.float32(c["tau_oracle"])
