@@ -930,6 +930,12 @@ __device__ __forceinline__ float capacity_threshold(int r, int M, float demand, 
 // ranges (more work per scenario) get smaller bucket numbers.
 __device__ __forceinline__ int range_bucket(int len) { return 31 - min(31, 32 - __clz(len)); }
 
+// Tables of the general set-up's convolution tree: B (K), the first level
+// (at least one table: the empty convolution of a single class) and the
+// second (the later levels reuse them).
+__device__ __host__ inline int prep_tree_a(int K) { return K - 1 > 2 ? (K - 1 + 1) / 2 : 1; }
+__device__ __host__ inline int prep_tree_b(int K) { return prep_tree_a(K) > 1 ? (prep_tree_a(K) + 1) / 2 : 1; }
+
 // Problem constants the set-up indexes per lane, staged in LDS (kernel
 // arguments are reached through memory loads).
 struct PrepConsts {
@@ -1058,6 +1064,11 @@ __device__ void prep_list(const DevProblem &P, int O, const uint8_t *__restrict_
 // Dynamic LDS: all cells (cap, tail) of this realisation; the class's cell
 // maxima and replica ranges; the load-level table (K x G int8); and, when
 // kLds, the tables (B and two tree buffers, 3 x K x G ints), else in gtab.
+__device__ void prep_list_staged(const DevProblem &P, const int8_t *lvl_tab, int lvl_stride, int O,
+                                 const uint8_t *__restrict__ measured, const int32_t *__restrict__ cand, int E,
+                                 int dump, int PPc, TileInfo *__restrict__ tiles, int4 *__restrict__ list,
+                                 int32_t *__restrict__ n_listed, int *lds);
+
 template <bool kLds>
 __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restrict__ cap_lo,
                                              const float *__restrict__ cap_hi,
@@ -1069,7 +1080,7 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
                                              int32_t *__restrict__ base, int32_t *__restrict__ mopt,
                                              float *__restrict__ thr, int32_t n_thr,
                                              int4 *__restrict__ list, int32_t *__restrict__ n_listed,
-                                             int32_t thr_mode) {
+                                             int32_t thr_mode, int32_t staged_list) {
   extern __shared__ int lds[];
   __shared__ PrepConsts C;
   __shared__ int bucket_count[32], bucket_start[32], n_live;
@@ -1090,6 +1101,25 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
   }
   if (ci == K) {  // one block builds the work list of every order
     if (R != 0 || o != 0) return;
+    if (staged_list) {
+      // the load level of every (class, r), then the list from staged inputs
+      int8_t *lvl_tab = reinterpret_cast<int8_t *>(lds);
+      for (int idx = tid; idx < KG; idx += nth) {
+        const int k = idx / G, r = idx - k * G + 1;
+        const float per_replica = P.demand[k] / (float)r;
+        int lo = 0, hi = B;  // first level >= per_replica; B = none
+        while (lo < hi) {
+          const int mid = (lo + hi) >> 1;
+          if (per_replica <= P.levels[mid]) hi = mid;
+          else lo = mid + 1;
+        }
+        lvl_tab[idx] = (int8_t)(lo < B ? lo : -1);
+      }
+      __syncthreads();
+      prep_list_staged(P, lvl_tab, G, (int)gridDim.y, measured, cand, E, dump, PPc, tiles, list, n_listed,
+                       lds + (KG + 15) / 16 * 4);
+      return;
+    }
     if (tid < 32) bucket_count[tid] = 0;
     __syncthreads();
     prep_list(P, (int)gridDim.y, measured, cand, E, dump, PPc, C, tiles, list, n_listed, bucket_count,
@@ -1104,7 +1134,9 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
   int8_t *lvl = (int8_t *)(crhi + per_class);  // [K][G] load level of r = g + 1 replicas
   int *tabs = kLds ? (int *)(lvl + ((KG + 15) & ~15)) : gtab + (((size_t)o * 2 + R) * K + ci) * 3 * KG;
   int *Bt = tabs;                            // [K][G]
-  int *Xa = tabs + KG, *Xb = tabs + 2 * KG;  // tree buffers, [ceil((K-1)/2)][G] each
+  // tree buffers: [ceil((K-1)/2)][G] and [ceil(ceil((K-1)/2)/2)][G] (the
+  // levels of the tree alternate between them, each no wider than the last)
+  int *Xa = tabs + KG, *Xb = Xa + prep_tree_a(K) * G;
   const size_t off = (size_t)o * N;
   const float *gcap = (R == 0 ? cap_lo : cap_hi) + off;
   const float *gtail = (R == 0 ? tail_hi : tail_lo) + off;
@@ -1328,7 +1360,7 @@ static int prep_order_waves(const DevProblem &P, int64_t O, int64_t E) {
 // LDS: bucket counters and starts (2 x 32 + 4), the level ranges (2 x K x B),
 // per candidate its cell and range code (2 x E), the revealed flags (O x N
 // bytes).
-__device__ void prep_list_staged(const DevProblem &P, const PrepLevels &LV, int O,
+__device__ void prep_list_staged(const DevProblem &P, const int8_t *lvl_tab, int lvl_stride, int O,
                                  const uint8_t *__restrict__ measured, const int32_t *__restrict__ cand, int E,
                                  int dump, int PPc, TileInfo *__restrict__ tiles, int4 *__restrict__ list,
                                  int32_t *__restrict__ n_listed, int *lds) {
@@ -1352,7 +1384,7 @@ __device__ void prep_list_staged(const DevProblem &P, const PrepLevels &LV, int 
   // one thread per (class, replica count)
   for (int x = tid; x < K * G; x += nth) {
     const int k = x / G, r = x - k * G + 1;
-    const int b = LV.lvl[k * kPrepOrderMaxG + r - 1];
+    const int b = lvl_tab[k * lvl_stride + r - 1];
     if (b >= 0) {
       atomicMin(&lv_first[k * B + b], r);
       atomicMax(&lv_last[k * B + b], r);
@@ -1493,7 +1525,7 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
   const int G = P.G, K = P.K, N = P.N, NT = P.NT, B = P.B, per_class = NT * B;
   const int PPc = n_thr / K;
   if ((int)blockIdx.x == 2 * O) {
-    prep_list_staged(P, LV, O, measured, cand, E, dump, PPc, tiles, list, n_listed, lds);
+    prep_list_staged(P, LV.lvl, kPrepOrderMaxG, O, measured, cand, E, dump, PPc, tiles, list, n_listed, lds);
     return;
   }
   const int o = blockIdx.x >> 1, R = blockIdx.x & 1;
@@ -3291,8 +3323,21 @@ static size_t prep_lds_small(const DevProblem &P) {
   return sizeof(int) * (2 * (size_t)P.N + 3 * (size_t)P.NT * P.B) + ((KG + 15) & ~(size_t)15);
 }
 
-// LDS of the set-up tables per block: B and two tree buffers, K x G each.
-static size_t prep_lds_tables(const DevProblem &P) { return 3 * sizeof(int) * (size_t)P.K * P.G; }
+// LDS of the set-up tables per block: B (K x G) and the two tree buffers.
+static size_t prep_lds_tables(const DevProblem &P) {
+  return sizeof(int) * (size_t)(P.K + prep_tree_a(P.K) + prep_tree_b(P.K)) * P.G;
+}
+
+// LDS of the general set-up's work-list block from staged inputs: the load
+// levels (K x G bytes), counters, level ranges, candidates, revealed flags.
+static size_t prep_list_lds(const DevProblem &P, int64_t O, int64_t E) {
+  const size_t KG = (size_t)P.K * P.G;
+  return ((KG + 15) & ~(size_t)15) + 4 * (68 + 2 * (size_t)P.K * P.B + 2 * (size_t)E) + (size_t)O * P.N;
+}
+
+// Dynamic LDS of one general set-up block: a workgroup may hold 160 KiB on
+// gfx950, less what the kernel declares statically.
+constexpr size_t kPrepGeneralLdsLimit = 156 * 1024;
 
 // LDS of the one-block-per-order set-up: the larger of a class block's and
 // the work-list block's.
@@ -3329,8 +3374,9 @@ WsLayout ws_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
   L.tiles = at; at = align256(at + sizeof(TileInfo) * (size_t)O * (size_t)E);
   const bool excl = excl_kernel_supported(P);
   // the exclusion set-up keeps B, P, S, H in LDS when they fit, else here
-  const bool in_lds = prep_lds_small(P) + prep_lds_tables(P) <= kPrepLdsLimit;
-  L.tabB = at; at = align256(at + (excl && !in_lds ? (size_t)O * 2 * P.K * prep_lds_tables(P) : 0));
+  const bool in_lds = prep_lds_small(P) + prep_lds_tables(P) <= kPrepGeneralLdsLimit;
+  L.tabB = at;
+  at = align256(at + (excl && !in_lds ? (size_t)O * 2 * P.K * 3 * sizeof(int) * P.K * P.G : 0));
   const size_t n_opt = excl ? (size_t)O * 2 * excl_thresholds(P) : 0;
   L.mopt = at; at = align256(at + sizeof(int32_t) * n_opt);
   L.thr = at; at = align256(at + sizeof(float) * n_opt);
@@ -3397,15 +3443,29 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
       }
 #undef FS_PREP_ORDER_K
 #undef FS_PREP_ORDER
-    } else if (big <= kPrepLdsLimit)
-      k_prep<true><<<dim3(2, a.O, P.K + 1), kPrepThreads, big, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
-                                                          a.measured, a.cand, a.E, dump, nullptr, tiles,
-                                                          base, mopt, thr, n_thr, list, live, a.thr_search);
-    else
-      k_prep<false><<<dim3(2, a.O, P.K + 1), kPrepThreads, small, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi,
-                                                             a.measured, a.cand, a.E, dump,
-                                                             (int32_t *)(a.ws + a.L.tabB), tiles, base, mopt,
-                                                             thr, n_thr, list, live, a.thr_search);
+    } else {
+      // the work-list block reads staged inputs when they fit; tables in
+      // LDS when they fit, else in the workspace
+      const size_t lst = prep_list_lds(P, a.O, a.E);
+      const int staged = lst <= kPrepGeneralLdsLimit;
+      const bool in_lds = big <= kPrepGeneralLdsLimit;
+      size_t lds = in_lds ? big : small;
+      if (staged && lst > lds) lds = lst;
+      const void *fn = in_lds ? reinterpret_cast<const void *>(&k_prep<true>)
+                              : reinterpret_cast<const void *>(&k_prep<false>);
+      if (lds > 64 * 1024) {
+        const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+      }
+      if (in_lds)
+        k_prep<true><<<dim3(2, a.O, P.K + 1), kPrepThreads, lds, s>>>(
+            P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured, a.cand, a.E, dump, nullptr, tiles, base, mopt,
+            thr, n_thr, list, live, a.thr_search, staged);
+      else
+        k_prep<false><<<dim3(2, a.O, P.K + 1), kPrepThreads, lds, s>>>(
+            P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured, a.cand, a.E, dump, (int32_t *)(a.ws + a.L.tabB),
+            tiles, base, mopt, thr, n_thr, list, live, a.thr_search, staged);
+    }
     if (a.E == 0) {
       k_finalize<<<a.O, 64, 0, s>>>(P, info, a.measured, 0, a.S, base, partial, 1, a.score, a.gap_now,
                                     a.best);
