@@ -387,10 +387,12 @@ fs_status fs_score_candidates_lex(fs_context *ctx, const fs_problem *p, fs_inter
   if (dg.err != hipSuccess) return hip_fail(dg.err, "hipSetDevice");
   uint8_t *ws = (uint8_t *)d_workspace;
   hipError_t e = fs::launch_setup(P, d_cand, n_cand, ws, L.score, stream);
+  // the goodput stage without full solves unless scoring kernel 1 (full
+  // solves) is asked for
   if (e == hipSuccess)
-    e = fs::launch_score_lex(P, iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi, iv.measured, d_cap_s, d_tail_s,
-                             n_orders, n_cand, S, d_score_maxmin, d_score_goodput, d_gap_maxmin, d_gap_goodput,
-                             d_best, ws, L, stream);
+    e = fs::launch_score_lex(P, iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi, iv.measured, d_cand, d_cap_s,
+                             d_tail_s, n_orders, n_cand, S, d_score_maxmin, d_score_goodput, d_gap_maxmin,
+                             d_gap_goodput, d_best, ws, L, ctx->score_kernel != 1, stream);
   if (e != hipSuccess) return hip_fail(e, "stage-wise score launch");
   return FS_OK;
 }
@@ -702,8 +704,10 @@ fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv,
         XL.gap_mm = LL.gap_mm;
         XL.gap_gp = LL.gap_gp;
         XL.state = LL.lex_state;
-        e = fs::launch_score_lex(P, R_cap_lo, D.cap_hi, R_tail_lo, R_tail_hi, D.measured, cs, ts, n_orders, n_cand, S,
-                                 D.score, (double *)(ws + LL.scores_gp), nullptr, nullptr, D.best, ws, XL, stream);
+        XL.fast = LL.lex_fast;
+        e = fs::launch_score_lex(P, R_cap_lo, D.cap_hi, R_tail_lo, R_tail_hi, D.measured, d_cand, cs, ts, n_orders,
+                                 n_cand, S, D.score, (double *)(ws + LL.scores_gp), nullptr, nullptr, D.best, ws, XL,
+                                 ctx->score_kernel != 1, stream);
       } else {
         fs::ScoreArgs a{R_cap_lo, D.cap_hi, R_tail_lo, R_tail_hi, D.measured, d_cand, cs, ts,
                         n_orders, n_cand, S, D.score, D.gap_now, D.best, nullptr, ws, LL.score, kernel,

@@ -163,6 +163,19 @@ struct LoopDev {
   int32_t max_rounds;
 };
 
+// The goodput stage of the stage-wise score without full solves (problems
+// without critical floors whose set-up fits): per (order, realisation)
+// every option's (ratio, served rate) and the sorted distinct ratios, and
+// per (order, realisation, class) and interval between them the knapsack
+// of the other classes (G + 1 binary64) and the class's best options (4
+// binary64).  fast = 0 when not available.
+struct LexExclRegions {
+  size_t opt, bp, nbp, V, W;
+  int32_t nbmax;  // breakpoints per (order, realisation) at most: K x options per class + 1
+  int fast;
+};
+LexExclRegions lex_excl_regions(const DevProblem &P, int64_t O, size_t *at);
+
 // Workspace of fs_profile_loop: the scorer's layout, then the loop's own
 // regions (offsets from the workspace start).
 struct LoopLayout {
@@ -170,6 +183,7 @@ struct LoopLayout {
   size_t cap_lo, cap_hi, tail_lo, tail_hi, measured, cert_state, cons_obj, cons_tp, cons_rep, cons_fm,
       cons_gp, fin_obj, fin_tp, fin_rep, fin_fm, fin_gp, scores, gap_now, best, running, n_running;
   size_t scores_gp, part_gp, gap_mm, gap_gp, lex_state;  // the stage-wise score (whole objective)
+  LexExclRegions lex_fast;
   size_t total;
 };
 
@@ -180,12 +194,16 @@ LoopLayout loop_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S);
 struct LexScoreLayout {
   WsLayout score;
   size_t part_gp, gap_mm, gap_gp, state, total;
+  LexExclRegions fast;
 };
 LexScoreLayout lex_score_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S);
+// fast: the goodput stage without full solves where the layout has it (else
+// every scenario is solved in full, as with fast = 0).
 hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const float *cap_hi, const float *tail_lo,
-                            const float *tail_hi, const uint8_t *measured, const float *cap_s, const float *tail_s,
-                            int32_t O, int32_t E, int32_t S, double *score_mm, double *score_gp, double *gap_mm,
-                            double *gap_gp, int32_t *best, uint8_t *ws, const LexScoreLayout &L, hipStream_t s);
+                            const float *tail_hi, const uint8_t *measured, const int32_t *cand, const float *cap_s,
+                            const float *tail_s, int32_t O, int32_t E, int32_t S, double *score_mm,
+                            double *score_gp, double *gap_mm, double *gap_gp, int32_t *best, uint8_t *ws,
+                            const LexScoreLayout &L, int fast, hipStream_t s);
 
 // Interval refit and sample clamping (Algorithm 1's fit step).  The refit
 // outputs may alias its inputs.

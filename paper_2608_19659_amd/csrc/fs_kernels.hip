@@ -2511,16 +2511,22 @@ __global__ __launch_bounds__(64) void k_certify(DevProblem P, const int8_t *__re
 //   V_K[g] = (0, 0 GPUs);  V_k[g] = best over allowed options o of class k
 //   with cost <= g of (served_o + V_{k+1}[g - cost], cost + GPUs of it),
 // best = larger goodput, then fewer GPUs, then the earlier option.  One
-// wavefront: lanes over the budgets g, the class's options in a uniform
-// loop; the choice of every (class, budget) is kept, and the allocation is
-// read in class order from the full budget.
+// wavefront.  Options of one cost reach the same budgets with the same
+// completion, so each class first merges its allowed options per cost c into
+// the largest served rate (the earliest option among equal ones) -- no other
+// option of that cost can be the best at any budget -- and the layer update
+// runs over costs, lanes over the budgets g:
+//   V_k[g] = best of (V_{k+1}[g] if empty allowed) and, for c = 1..g,
+//            (A_k[c] + V_{k+1}[g - c], c + GPUs of it),
+// equal (goodput, GPUs) going to the earlier option (the empty one first).
+// The choice of every (class, budget) is kept, and the allocation is read
+// in class order from the full budget.
 // ---------------------------------------------------------------------------
 struct LexLds {
   double *vgp;      // [G + 1] goodput of the layer, updated in place
+  int2 *aopt;       // [G + 1] per cost: (served rate bits, option index; -1 = none allowed)
   int *vn;          // [G + 1] GPUs, -1 = no allowed completion
   int16_t *choice;  // [K][G + 1] option index, -1 = empty, -2 = none
-  float *oserved;   // [options of a class] served goodput
-  int16_t *ocost;   // [options of a class] cost, -1 = not allowed
 };
 
 // Options of a class are numbered by TP index, then replicas:
@@ -2540,13 +2546,13 @@ __device__ __forceinline__ void option_of(const DevProblem &P, int q, int *ti, i
 }
 
 // One layer suffices: V_k[g] reads V_{k+1} at budgets <= g only, so the
-// budgets are rewritten from the top down, 64 at a time, every lane's reads
-// of a group before its writes.
+// budgets are rewritten from the top down, 64 at a time (lane l takes
+// g = top - l), every lane's reads of a group before its writes.
 __device__ void wave_lex_stage(const DevProblem &P, const int8_t *__restrict__ bmap, const Realisation &R,
                                int tau, int floors_met, const LexLds &X, const WaveAlloc &alloc,
                                float *goodput, double *goodput64) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int K = P.K, G = P.G, PO = P.optoff[P.NT];
+  const int K = P.K, G = P.G, NT = P.NT;
   for (int g = lane; g <= G; g += kWave) {
     X.vgp[g] = 0.0;
     X.vn[g] = 0;
@@ -2556,53 +2562,69 @@ __device__ void wave_lex_stage(const DevProblem &P, const int8_t *__restrict__ b
     const bool empty_ok = !restricted && tau <= 0;
     const float slo = P.slo[k], demand = P.demand[k], fl = P.floor_rps[k];
     const double rcp = P.rcp_demand[k];
-    for (int q = lane; q < PO; q += kWave) {
-      int ti, t, r;
-      option_of(P, q, &ti, &t, &r);
-      const int b = bmap[k * (G + 1) + r];
-      int cost = -1;
-      float served = 0.0f;
-      if (b >= 0) {
+    for (int c = lane + 1; c <= G; c += kWave) {
+      float best = 0.0f;
+      int bq = -1;
+      for (int ti = 0; ti < NT; ++ti) {  // options of cost c in (TP, replicas) order
+        const int t = P.tp[ti], r = c / t;
+        if (r * t != c) continue;
+        const int b = bmap[k * (G + 1) + r];
+        if (b < 0) continue;
         const int cell = cell_of(P, k, ti, b);
-        const float c = R.c(cell), l = R.l(cell);
-        bool ok = ratio_bits(c, l, r, slo, rcp) >= tau;
-        if (restricted && !floor_ok(c, l, r, slo, demand, fl)) ok = false;
-        if (ok) cost = t * r;
-        served = (l <= slo) ? served_rps(c, r, demand) : 0.0f;
+        const float cc = R.c(cell), l = R.l(cell);
+        bool ok = ratio_bits(cc, l, r, slo, rcp) >= tau;
+        if (restricted && !floor_ok(cc, l, r, slo, demand, fl)) ok = false;
+        if (!ok) continue;
+        const float sv = (l <= slo) ? served_rps(cc, r, demand) : 0.0f;
+        if (bq < 0 || sv > best) {
+          best = sv;
+          bq = P.optoff[ti] + r - 1;
+        }
       }
-      X.ocost[q] = (int16_t)cost;
-      X.oserved[q] = served;
+      X.aopt[c] = make_int2(__float_as_int(best), bq);
     }
     __syncthreads();
-    for (int base = (G / kWave) * kWave; base >= 0; base -= kWave) {
-      const int g = base + lane;
+    for (int top = G; top >= 0; top -= kWave) {
+      const int g = top - lane;
+      const int gs = g >= 0 ? g : 0;
       double bgp = 0.0;
-      int bn = -1, bc = -2;
-      if (g <= G) {
-        if (empty_ok && X.vn[g] >= 0) {
-          bgp = X.vgp[g];
-          bn = X.vn[g];
-          bc = -1;
+      int bn = -1, bq = -2;
+      if (empty_ok && X.vn[gs] >= 0) {
+        bgp = X.vgp[gs];
+        bn = X.vn[gs];
+        bq = -1;
+      }
+      auto take = [&](int c, int2 a, int n2, double v2) {
+        const double v = (double)__int_as_float(a.x) + v2;
+        const int vn = c + n2;
+        const bool ok = a.y >= 0 && gs >= c && n2 >= 0;
+        const bool better = bn < 0 || v > bgp || (v == bgp && (vn < bn || (vn == bn && a.y < bq)));
+        if (ok && better) {
+          bgp = v;
+          bn = vn;
+          bq = a.y;
         }
-        for (int q = 0; q < PO; ++q) {
-          const int c = X.ocost[q];
-          if (c < 0 || c > g) continue;
-          const int n2 = X.vn[g - c];
-          if (n2 < 0) continue;
-          const double v = (double)X.oserved[q] + X.vgp[g - c];
-          const int vn = c + n2;
-          if (bn < 0 || v > bgp || (v == bgp && vn < bn)) {
-            bgp = v;
-            bn = vn;
-            bc = q;
-          }
-        }
+      };
+      int c = 1;
+      for (; c + 3 <= top; c += 4) {
+        const int2 a0 = X.aopt[c], a1 = X.aopt[c + 1], a2 = X.aopt[c + 2], a3 = X.aopt[c + 3];
+        const int i0 = max(gs - c, 0), i1 = max(gs - c - 1, 0), i2 = max(gs - c - 2, 0), i3 = max(gs - c - 3, 0);
+        const int n0 = X.vn[i0], n1 = X.vn[i1], n2 = X.vn[i2], n3 = X.vn[i3];
+        const double v0 = X.vgp[i0], v1 = X.vgp[i1], v2 = X.vgp[i2], v3 = X.vgp[i3];
+        take(c, a0, n0, v0);
+        take(c + 1, a1, n1, v1);
+        take(c + 2, a2, n2, v2);
+        take(c + 3, a3, n3, v3);
+      }
+      for (; c <= top; ++c) {
+        const int i0 = max(gs - c, 0);
+        take(c, X.aopt[c], X.vn[i0], X.vgp[i0]);
       }
       wave_lds_fence();
-      if (g <= G) {
+      if (g >= 0) {
         X.vgp[g] = bgp;
         X.vn[g] = bn;
-        X.choice[k * (G + 1) + g] = (int16_t)bc;
+        X.choice[k * (G + 1) + g] = (int16_t)bq;
       }
       wave_lds_fence();
     }
@@ -2631,12 +2653,11 @@ __device__ void wave_lex_stage(const DevProblem &P, const int8_t *__restrict__ b
 }
 
 // Work area of a lexicographic solve, shared in turn by the max-min solver
-// (3 (G + 1) ints) and the stage: the layer, the choices and one class's
-// option table, from an 8-byte aligned start.
-__device__ __host__ inline size_t lex_work_bytes(int K, int G, int PO) {
+// (3 (G + 1) ints) and the stage: the layer, the per-cost options and the
+// choices, from an 8-byte aligned start.
+__device__ __host__ inline size_t lex_work_bytes(int K, int G) {
   const size_t g1 = (size_t)G + 1;
-  size_t b = g1 * (sizeof(double) + sizeof(int)) + (size_t)PO * sizeof(float);
-  b += ((size_t)K * g1 + (size_t)PO) * sizeof(int16_t);
+  const size_t b = g1 * (sizeof(double) + sizeof(int2) + sizeof(int)) + (size_t)K * g1 * sizeof(int16_t);
   const size_t solver = 3 * g1 * sizeof(int);
   return 8 + (b > solver ? b : solver);  // 8: aligning the start
 }
@@ -2646,10 +2667,9 @@ __device__ __forceinline__ LexLds lex_lds(const DevProblem &P, void *start) {
   char *base = reinterpret_cast<char *>(((uintptr_t)start + 7) & ~(uintptr_t)7);
   LexLds X;
   X.vgp = reinterpret_cast<double *>(base);
-  X.vn = reinterpret_cast<int *>(X.vgp + g1);
-  X.oserved = reinterpret_cast<float *>(X.vn + g1);
-  X.choice = reinterpret_cast<int16_t *>(X.oserved + P.optoff[P.NT]);
-  X.ocost = X.choice + (size_t)P.K * g1;
+  X.aopt = reinterpret_cast<int2 *>(X.vgp + g1);
+  X.vn = reinterpret_cast<int *>(X.aopt + g1);
+  X.choice = reinterpret_cast<int16_t *>(X.vn + g1);
   return X;
 }
 
@@ -2669,7 +2689,7 @@ __global__ __launch_bounds__(64) void k_solve_dense_lex(DevProblem P, const int8
   const LexLds X = lex_lds(P, work);
   Realisation R{cap + j * P.N, tail + j * P.N, -1, 0.0f, 0.0f};
   if (stage) {
-    const StageArea A = stage_area(P, reinterpret_cast<char *>(work) + lex_work_bytes(P.K, P.G, P.optoff[P.NT]));
+    const StageArea A = stage_area(P, reinterpret_cast<char *>(work) + lex_work_bytes(P.K, P.G));
     stage_copy_bmap(P, bmap, A.bmap);
     stage_copy_cells(P, R.cap, R.tail, A.cap, A.tail);
     bmap = A.bmap;
@@ -2708,7 +2728,7 @@ __global__ __launch_bounds__(64) void k_certify_lex(DevProblem P, const int8_t *
   int *work = tp_rep + kMaxClasses;
   WaveAlloc am{tm_index, tm_rep}, ap{tp_index, tp_rep};
   const LexLds X = lex_lds(P, work);
-  const StageArea A = stage_area(P, reinterpret_cast<char *>(work) + lex_work_bytes(P.K, P.G, P.optoff[P.NT]));
+  const StageArea A = stage_area(P, reinterpret_cast<char *>(work) + lex_work_bytes(P.K, P.G));
   const int8_t *bm = bmap;
   int fm_m, fm_p;
   float gp_m, gp_p;
@@ -2788,7 +2808,7 @@ __global__ __launch_bounds__(64) void k_score_lex_wave(DevProblem P, const int8_
   const int8_t *bm = bmap;
   const float *cm = cap_lo + off, *lm = tail_hi + off, *cp = cap_hi + off, *lp = tail_lo + off;
   if (stage) {
-    char *st = reinterpret_cast<char *>(work) + lex_work_bytes(P.K, P.G, P.optoff[P.NT]);
+    char *st = reinterpret_cast<char *>(work) + lex_work_bytes(P.K, P.G);
     int8_t *sb = reinterpret_cast<int8_t *>(((uintptr_t)st + 15) & ~(uintptr_t)15);
     float *sc = reinterpret_cast<float *>(sb + (((size_t)P.K * (P.G + 1) + 3) & ~(size_t)3));
     stage_copy_bmap(P, bmap, sb);
@@ -2830,6 +2850,352 @@ __global__ __launch_bounds__(64) void k_score_lex_wave(DevProblem P, const int8_
   }
   const double sum_mm = wave_pairwise_sum(mine_mm);
   const double sum_gp = wave_pairwise_sum(mine_gp);
+  if (lane == 0) {
+    part_mm[tile * n_partial + chunk] = sum_mm;
+    part_gp[tile * n_partial + chunk] = sum_gp;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// The stage-wise score's goodput stage without full solves (no critical
+// floors).  Level (3) of the objective on a scenario keeps every class's
+// ratio at least the scenario's tau* and maximises the total served
+// goodput.  Splitting off the candidate's class i,
+//   gp = max over allowed options q of class i of served_q + V_i(tau*)[G - cost_q],
+// where V_i(tau)[g] is the best goodput of the other classes with at most g
+// GPUs when only options of ratio >= tau are allowed (the empty option only
+// when tau <= 0).  Only the candidate cell's options depend on the sample;
+// V_i and the allowed set of every other option change only where tau
+// crosses an option's ratio.  Over the sorted distinct ratios b_0 = 0 <
+// b_1 < ... < b_{n-1} of the realisation's options (every class, every
+// cell), tau* falls in interval j = #{b_m < tau*}; there the options of
+// ratio >= b_j are allowed (none for j = n) and the empty option only in
+// interval 0 (tau* = 0).  Per (realisation, order, class i) and interval
+// the set-up tabulates V_i and, for class i's options off the candidate
+// cell, the best value per cell reduced to the largest (at its cell), the
+// largest over every other cell and the empty option's; a scenario then
+// needs its interval (a bisection over the ratios) and its cell's options.
+// Goodput sums are binary64, exact under the same condition as the full
+// solve's (nonzero served rates within a factor 2^23 of each other), so the
+// association does not change them.
+// ---------------------------------------------------------------------------
+constexpr int kLexPrepThreads = 256;
+
+// Keys the breakpoint sort takes: every option's ratio and the 0, padded to
+// a power of two (at least one per thread).
+__host__ __device__ inline int lex_sort_keys(int nopt) {
+  int n = kLexPrepThreads;
+  while (n < nopt + 1) n <<= 1;
+  return n;
+}
+
+// LDS of a k_lex_breaks block: the sort keys and one count per thread.
+__host__ __device__ inline size_t lex_breaks_lds(int nopt) {
+  return 4 * ((size_t)lex_sort_keys(nopt) + kLexPrepThreads);
+}
+
+// LDS of a k_lex_tables block: every option's (ratio, served rate), the
+// candidate class's replica range per cell, then per wavefront two
+// knapsack layers (binary64) and one class's best served rate per cost.
+__host__ __device__ inline size_t lex_tables_lds(int nopt, int per_class, int G) {
+  const size_t nw = kLexPrepThreads / kWave;
+  return 8 * (size_t)nopt + 8 * (size_t)per_class + nw * (16 * ((size_t)G + 1) + 4 * (((size_t)G + 2) & ~(size_t)1));
+}
+
+// Per (realisation R, order o): every option of every class (ratio bits, -1
+// when no load level holds it; served rate) to opt_out, and the sorted
+// distinct ratios, 0 always among them, to bp_out (nb of them to nbp).
+// The ratios are sorted by a bitonic network in LDS, then each first
+// occurrence is placed by a block-wide count of the ones before it.
+__global__ __launch_bounds__(kLexPrepThreads) void k_lex_breaks(DevProblem P, const int8_t *__restrict__ bmap,
+                                                               const float *__restrict__ cap_lo,
+                                                               const float *__restrict__ cap_hi,
+                                                               const float *__restrict__ tail_lo,
+                                                               const float *__restrict__ tail_hi, int32_t nbmax,
+                                                               int2 *__restrict__ opt_out, float *__restrict__ bp_out,
+                                                               int32_t *__restrict__ nbp) {
+  extern __shared__ int lex_keys[];
+  const int R = blockIdx.x, o = blockIdx.y, tid = threadIdx.x;
+  const int K = P.K, G = P.G, N = P.N, B = P.B, NT = P.NT, per_class = NT * B, PP = P.optoff[NT];
+  const int nopt = K * PP, n2 = lex_sort_keys(nopt);
+  int *cnt = lex_keys + n2;
+  const size_t off = (size_t)o * N;
+  const float *gcap = (R == 0 ? cap_lo : cap_hi) + off;
+  const float *gtail = (R == 0 ? tail_hi : tail_lo) + off;
+  int2 *opt = opt_out + ((size_t)o * 2 + R) * nopt;
+  for (int q = tid; q < n2; q += kLexPrepThreads) {
+    int key = INT_MAX;  // padding and options that do not exist sort last
+    if (q < nopt) {
+      const int k = q / PP, p = q - k * PP;
+      int ti = 0;
+      while (ti + 1 < NT && p >= P.optoff[ti + 1]) ++ti;
+      const int r = p - P.optoff[ti] + 1;
+      const int b = bmap[k * (G + 1) + r];
+      int f = -1;
+      float sv = 0.0f;
+      if (b >= 0) {
+        const int cell = k * per_class + ti * B + b;
+        const float c = gcap[cell], l = gtail[cell];
+        f = ratio_bits(c, l, r, P.slo[k], P.rcp_demand[k]);
+        sv = l <= P.slo[k] ? served_rps(c, r, P.demand[k]) : 0.0f;
+        key = f;
+      }
+      opt[q] = make_int2(f, __float_as_int(sv));
+    } else if (q == nopt) {
+      key = 0;  // tau* = 0 is its own interval (the empty option's)
+    }
+    lex_keys[q] = key;
+  }
+  __syncthreads();
+  for (int size = 2; size <= n2; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int idx = tid; idx < (n2 >> 1); idx += kLexPrepThreads) {
+        const int lo = ((idx & ~(stride - 1)) << 1) | (idx & (stride - 1)), hi = lo + stride;
+        const int a = lex_keys[lo], c = lex_keys[hi];
+        const bool up = (lo & size) == 0;
+        if ((a > c) == up) {
+          lex_keys[lo] = c;
+          lex_keys[hi] = a;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // thread t owns keys [t seg, (t + 1) seg): count its first occurrences,
+  // then an exclusive count over the threads places them
+  const int seg = n2 / kLexPrepThreads, a0 = tid * seg;
+  int mine = 0;
+  for (int a = a0; a < a0 + seg; ++a) {
+    const int v = lex_keys[a];
+    mine += (v != INT_MAX && (a == 0 || lex_keys[a - 1] != v)) ? 1 : 0;
+  }
+  cnt[tid] = mine;
+  __syncthreads();
+  int before = 0;
+  for (int t = 0; t < tid; ++t) before += cnt[t];
+  float *bp = bp_out + ((size_t)o * 2 + R) * nbmax;
+  for (int a = a0; a < a0 + seg; ++a) {
+    const int v = lex_keys[a];
+    if (v != INT_MAX && (a == 0 || lex_keys[a - 1] != v)) bp[before++] = __int_as_float(v);
+  }
+  if (tid == kLexPrepThreads - 1) nbp[o * 2 + R] = before;
+}
+
+// Per (realisation R, order o, class i) and interval j of the breakpoints
+// (one wavefront each): V_i, the best goodput of the classes other than i
+// with at most g GPUs, g = 0..G, when only options of ratio >= bp[j] are
+// allowed (none when j = nb) and the empty option only when j = 0; then
+// class i's best served + V_i[G - cost] per cell, reduced to the largest
+// (and its cell), the largest over the other cells, and the empty
+// option's.  The knapsack takes the classes from the last to the first
+// with a best-served-per-cost vector each (the options of one cost merged):
+//   V'[g] = max(V[g] if empty allowed, max_{c=1..g} A[c] + V[g - c]),
+// lanes over g from the top down, so each chunk loops c only up to its
+// largest g.  Blocks split the intervals of one (R, o, i) four wavefronts
+// at a time.
+__global__ __launch_bounds__(kLexPrepThreads) void k_lex_tables(DevProblem P, const int8_t *__restrict__ bmap,
+                                                               const int2 *__restrict__ opt_in,
+                                                               const float *__restrict__ bp_in,
+                                                               const int32_t *__restrict__ nbp, int32_t nbmax,
+                                                               int32_t nsplit, double *__restrict__ Vout,
+                                                               double *__restrict__ Wout) {
+  extern __shared__ double lex_tab_lds[];
+  const int R = blockIdx.x & 1, part = blockIdx.x >> 1, o = blockIdx.y, i = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  constexpr int nw = kLexPrepThreads / kWave;
+  const int K = P.K, G = P.G, B = P.B, NT = P.NT, per_class = NT * B, PP = P.optoff[NT];
+  const int nopt = K * PP;
+  const int nb = nbp[o * 2 + R];
+  const int first = part * nw + wave, step = nsplit * nw;
+  int *oratio = reinterpret_cast<int *>(lex_tab_lds);  // [nopt]
+  float *oserved = reinterpret_cast<float *>(oratio + nopt);
+  int2 *crange = reinterpret_cast<int2 *>(oserved + nopt);  // [per_class] class i's replica range per cell
+  double *Va = reinterpret_cast<double *>(crange + per_class) + (size_t)wave * 2 * (G + 1);
+  double *Vb = Va + G + 1;
+  float *Ak = reinterpret_cast<float *>(reinterpret_cast<double *>(crange + per_class) + (size_t)nw * 2 * (G + 1)) +
+              (size_t)wave * ((G + 2) & ~1);
+  if (part * nw > nb) return;  // no interval for this block
+  const int2 *opt = opt_in + ((size_t)o * 2 + R) * nopt;
+  for (int q = tid; q < nopt; q += kLexPrepThreads) {
+    const int2 v = opt[q];
+    oratio[q] = v.x;
+    oserved[q] = __int_as_float(v.y);
+  }
+  for (int c = tid; c < per_class; c += kLexPrepThreads) {
+    const int ti = c / B, b = c - ti * B, t = P.tp[ti];
+    int rlo = INT_MAX, rhi = -1;
+    for (int r = 1; r <= G / t; ++r) {
+      if (bmap[i * (G + 1) + r] == b) {
+        rlo = min(rlo, r);
+        rhi = max(rhi, r);
+      }
+    }
+    crange[c] = make_int2(rlo, rhi);
+  }
+  __syncthreads();
+  const double NEG = -__builtin_inf();
+  const float NEGF = -__builtin_inff();
+  const float *bp = bp_in + ((size_t)o * 2 + R) * nbmax;
+  const size_t row0 = (((size_t)o * 2 + R) * K + i) * (size_t)(nbmax + 1);
+  for (int j = first; j <= nb; j += step) {
+    const int thr = j < nb ? __float_as_int(bp[j]) : INT_MAX;  // allowed: ratio >= thr
+    const bool empty_ok = j == 0;
+    for (int g = lane; g <= G; g += kWave) Va[g] = 0.0;  // no class yet: nothing served
+    wave_lds_fence();
+    double *Vp = Va, *Vc = Vb;
+    for (int k = K - 1; k >= 0; --k) {
+      if (k == i) continue;
+      // A[c]: the best served rate of class k's allowed options of cost c
+      for (int c = lane + 1; c <= G; c += kWave) {
+        float a = NEGF;
+        for (int ti = 0; ti < NT; ++ti) {
+          const int t = P.tp[ti];
+          const int r = c / t;
+          if (r * t == c) {
+            const int q = k * PP + P.optoff[ti] + r - 1;
+            a = oratio[q] >= thr ? fmaxf(a, oserved[q]) : a;
+          }
+        }
+        Ak[c] = a;
+      }
+      wave_lds_fence();
+      for (int top = G; top >= 0; top -= kWave) {
+        const int g = top - lane;  // lanes past g = 0 compute nothing
+        const int gs = g >= 0 ? g : 0;
+        double best = empty_ok ? Vp[gs] : NEG;
+        int c = 1;
+        for (; c + 3 <= top; c += 4) {
+          const float a0 = Ak[c], a1 = Ak[c + 1], a2 = Ak[c + 2], a3 = Ak[c + 3];
+          const double v0 = Vp[max(gs - c, 0)], v1 = Vp[max(gs - c - 1, 0)], v2 = Vp[max(gs - c - 2, 0)],
+                       v3 = Vp[max(gs - c - 3, 0)];
+          best = gs >= c ? fmax(best, (double)a0 + v0) : best;
+          best = gs >= c + 1 ? fmax(best, (double)a1 + v1) : best;
+          best = gs >= c + 2 ? fmax(best, (double)a2 + v2) : best;
+          best = gs >= c + 3 ? fmax(best, (double)a3 + v3) : best;
+        }
+        for (; c <= top; ++c) {
+          const double v = Vp[max(gs - c, 0)];
+          best = gs >= c ? fmax(best, (double)Ak[c] + v) : best;
+        }
+        if (g >= 0) Vc[g] = best;
+      }
+      wave_lds_fence();
+      double *t2 = Vp;
+      Vp = Vc;
+      Vc = t2;
+    }
+    double *Vg = Vout + (row0 + j) * (size_t)(G + 1);
+    for (int g = lane; g <= G; g += kWave) Vg[g] = Vp[g];
+    // class i's options per cell: the best served + V[G - cost]; the two
+    // largest over the cells (and the first one's cell) by a butterfly
+    double w1 = NEG, w2 = NEG;
+    int c1 = -1;
+    for (int c = lane; c < per_class; c += kWave) {
+      const int2 rr = crange[c];
+      const int ti = c / B, t = P.tp[ti];
+      double best = NEG;
+      for (int r = rr.x; r <= rr.y; ++r) {
+        const int q = i * PP + P.optoff[ti] + r - 1;
+        if (oratio[q] >= thr) best = fmax(best, (double)oserved[q] + Vp[G - t * r]);
+      }
+      if (best > w1) {
+        w2 = w1;
+        w1 = best;
+        c1 = c;
+      } else if (best > w2) {
+        w2 = best;
+      }
+    }
+#pragma unroll
+    for (int m = 1; m < kWave; m <<= 1) {
+      const double o1 = __shfl_xor(w1, m, kWave), o2 = __shfl_xor(w2, m, kWave);
+      const int oc = __shfl_xor(c1, m, kWave);
+      if (o1 > w1 || (o1 == w1 && oc > c1)) {  // the larger first, equal ones by the larger cell index
+        w2 = fmax(o2, w1);
+        w1 = o1;
+        c1 = oc;
+      } else {
+        w2 = fmax(w2, o1);
+      }
+    }
+    if (lane == 0) {
+      double *Wj = Wout + (row0 + j) * 4;
+      Wj[0] = w1;
+      Wj[1] = w2;
+      Wj[2] = empty_ok ? Vp[G] : NEG;
+      Wj[3] = (double)c1;
+    }
+    wave_lds_fence();
+  }
+}
+
+// Scenarios of the stage-wise score without full solves: block (chunk of 64
+// samples, candidate, order), lane = sample.  Per realisation tau* by the
+// exclusion identity of the max-min score (U, and M of the range's options),
+// its interval among the breakpoints (bisection in LDS), then
+// gp = max(the class's best off the candidate cell, the empty option, the
+// candidate cell's allowed options at the sample: served + V[G - cost]);
+// both stages' gaps reduced by the pairwise wave tree, one partial each.
+__global__ __launch_bounds__(64) void k_score_lex_excl(DevProblem P, const TileInfo *__restrict__ tiles,
+                                                       const int32_t *__restrict__ mopt, int32_t n_thr,
+                                                       const float *__restrict__ cap_s,
+                                                       const float *__restrict__ tail_s, int32_t E, int32_t S,
+                                                       const float *__restrict__ bp, const int32_t *__restrict__ nbp,
+                                                       int32_t nbmax, const double *__restrict__ V,
+                                                       const double *__restrict__ W, double *__restrict__ part_mm,
+                                                       double *__restrict__ part_gp, int64_t n_partial) {
+  extern __shared__ int lex_bp[];
+  const int chunk = blockIdx.x, e = blockIdx.y, o = blockIdx.z, lane = threadIdx.x;
+  const size_t tile = (size_t)o * E + e;
+  const TileInfo tl = tiles[tile];
+  if (tl.state != 0) return;  // measured or invalid: the finalize writes those
+  const int G = P.G, K = P.K, per_class = P.NT * P.B;
+  const int nb0 = nbp[o * 2 + 0], nb1 = nbp[o * 2 + 1];
+  for (int m = lane; m < nb0; m += kWave) lex_bp[m] = __float_as_int(bp[((size_t)o * 2 + 0) * nbmax + m]);
+  for (int m = lane; m < nb1; m += kWave) lex_bp[nbmax + m] = __float_as_int(bp[((size_t)o * 2 + 1) * nbmax + m]);
+  wave_lds_fence();
+  const int s = chunk * kWave + lane;
+  const bool live = s < S;
+  const float cs = cap_s[tile * S + (live ? s : 0)];
+  const float ls = tail_s[tile * S + (live ? s : 0)];
+  const int i = tl.cls, local = tl.cell - i * per_class;
+  const float slo = P.slo[i], lam = P.demand[i];
+  const double rcp = P.rcp_demand[i];
+  int tau[2];
+  double gp[2];
+#pragma unroll
+  for (int R = 0; R < 2; ++R) {
+    const int32_t *M = mopt + ((size_t)o * 2 + R) * n_thr + tl.toff;
+    int t = R == 0 ? tl.u_m : tl.u_p;
+    for (int r = tl.rlo; r <= tl.rhi; ++r) t = max(t, min(ratio_bits(cs, ls, r, slo, rcp), M[r - tl.rlo]));
+    tau[R] = t;
+    // interval: the count of breakpoints below tau
+    const int nb = R == 0 ? nb0 : nb1;
+    const int *b = lex_bp + R * nbmax;
+    int lo = 0, hi = nb;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (b[mid] < t) lo = mid + 1;
+      else hi = mid;
+    }
+    const size_t row = ((((size_t)o * 2 + R) * K + i) * (size_t)(nbmax + 1) + lo);
+    const double *Wj = W + row * 4;
+    const double *Vj = V + row * (size_t)(G + 1);
+    double g = (int)Wj[3] == local ? Wj[1] : Wj[0];
+    g = fmax(g, Wj[2]);
+    for (int r = tl.rlo; r <= tl.rhi; ++r) {
+      if (ratio_bits(cs, ls, r, slo, rcp) >= t) {
+        const float sv = ls <= slo ? served_rps(cs, r, lam) : 0.0f;
+        g = fmax(g, (double)sv + Vj[G - tl.t * r]);
+      }
+    }
+    gp[R] = g;
+  }
+  double mm, gg;
+  stage_gaps(tau[0], tau[1], gp[0], gp[1], &mm, &gg);
+  const double sum_mm = wave_pairwise_sum(live ? mm : 0.0);
+  const double sum_gp = wave_pairwise_sum(live ? gg : 0.0);
   if (lane == 0) {
     part_mm[tile * n_partial + chunk] = sum_mm;
     part_gp[tile * n_partial + chunk] = sum_gp;
@@ -3397,6 +3763,73 @@ hipError_t launch_setup(const DevProblem &P, const int32_t *cand, int32_t E, uin
   return hipGetLastError();
 }
 
+// The exclusion scorer's set-up: per-order tables (U, M and thresholds of
+// every option, base objectives, tile records) and the work list.
+static hipError_t launch_excl_setup(const DevProblem &P, const ScoreArgs &a, hipStream_t s) {
+  int32_t *base = (int32_t *)(a.ws + a.L.base);
+  TileInfo *tiles = (TileInfo *)(a.ws + a.L.tiles);
+  int32_t *mopt = (int32_t *)(a.ws + a.L.mopt);
+  float *thr = (float *)(a.ws + a.L.thr);
+  int4 *list = (int4 *)(a.ws + a.L.list);
+  int32_t *live = (int32_t *)(a.ws + a.L.live);
+  const int32_t n_thr = excl_thresholds(P);
+  const int dump = a.tau_dump != nullptr;
+  const size_t small = prep_lds_small(P), big = small + prep_lds_tables(P);
+  if (a.setup == 0 && prep_order_fits(P, a.O, a.E)) {
+    // the smallest level holding lambda / r; it falls as r grows, so one
+    // pass over r per class moves it downwards only
+    PrepLevels LV{};
+    for (int k = 0; k < P.K; ++k) {
+      int b = P.B;
+      for (int r = 1; r <= P.G; ++r) {
+        const float u = P.demand[k] / (float)r;
+        while (b > 0 && !(P.levels[b - 1] < u)) --b;
+        LV.lvl[k * kPrepOrderMaxG + r - 1] = (int8_t)(b < P.B ? b : -1);
+      }
+    }
+    // compiled for the rank step's table count rounded up to 4, 8 or 16
+    // and for at most 4 or 8 TP degrees (loops over them are unrolled)
+#define FS_PREP_ORDER(KP, NTP)                                                                                    \
+  k_prep_order<KP, NTP><<<2 * a.O + 1, prep_order_waves(P, a.O, a.E) * kWave, prep_order_lds(P, a.O, a.E), s>>>(    \
+    P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured, a.cand, a.E, a.O, dump, tiles, base, mopt, thr,  \
+    n_thr, list, live, a.thr_search, LV)
+#define FS_PREP_ORDER_K(NTP)                  \
+  if (P.K <= 4) FS_PREP_ORDER(4, NTP);        \
+  else if (P.K <= 8) FS_PREP_ORDER(8, NTP);   \
+  else FS_PREP_ORDER(16, NTP);
+    if (P.NT <= 4) {
+      FS_PREP_ORDER_K(4)
+    } else {
+      FS_PREP_ORDER_K(8)
+    }
+#undef FS_PREP_ORDER_K
+#undef FS_PREP_ORDER
+  } else {
+    // the work-list block reads staged inputs when they fit; tables in
+    // LDS when they fit, else in the workspace
+    const size_t lst = prep_list_lds(P, a.O, a.E);
+    const int staged = lst <= kPrepGeneralLdsLimit;
+    const bool in_lds = big <= kPrepGeneralLdsLimit;
+    size_t lds = in_lds ? big : small;
+    if (staged && lst > lds) lds = lst;
+    const void *fn = in_lds ? reinterpret_cast<const void *>(&k_prep<true>)
+                            : reinterpret_cast<const void *>(&k_prep<false>);
+    if (lds > 64 * 1024) {
+      const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+    }
+    if (in_lds)
+      k_prep<true><<<dim3(2, a.O, P.K + 1), kPrepThreads, lds, s>>>(
+          P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured, a.cand, a.E, dump, nullptr, tiles, base, mopt,
+          thr, n_thr, list, live, a.thr_search, staged);
+    else
+      k_prep<false><<<dim3(2, a.O, P.K + 1), kPrepThreads, lds, s>>>(
+          P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured, a.cand, a.E, dump, (int32_t *)(a.ws + a.L.tabB),
+          tiles, base, mopt, thr, n_thr, list, live, a.thr_search, staged);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) {
   const int8_t *bmap = (const int8_t *)(a.ws + a.L.bmap);
   CandInfo *info = (CandInfo *)(a.ws + a.L.cand);
@@ -3410,62 +3843,9 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
     int32_t *mopt = (int32_t *)(a.ws + a.L.mopt);
     float *thr = (float *)(a.ws + a.L.thr);
     int4 *list = (int4 *)(a.ws + a.L.list);
-    int32_t *live = (int32_t *)(a.ws + a.L.live);
     const int32_t n_thr = excl_thresholds(P);
-    const int dump = a.tau_dump != nullptr;
-    const size_t small = prep_lds_small(P), big = small + prep_lds_tables(P);
-    if (a.setup == 0 && prep_order_fits(P, a.O, a.E)) {
-      // the smallest level holding lambda / r; it falls as r grows, so one
-      // pass over r per class moves it downwards only
-      PrepLevels LV{};
-      for (int k = 0; k < P.K; ++k) {
-        int b = P.B;
-        for (int r = 1; r <= P.G; ++r) {
-          const float u = P.demand[k] / (float)r;
-          while (b > 0 && !(P.levels[b - 1] < u)) --b;
-          LV.lvl[k * kPrepOrderMaxG + r - 1] = (int8_t)(b < P.B ? b : -1);
-        }
-      }
-      // compiled for the rank step's table count rounded up to 4, 8 or 16
-      // and for at most 4 or 8 TP degrees (loops over them are unrolled)
-#define FS_PREP_ORDER(KP, NTP)                                                                                    \
-  k_prep_order<KP, NTP><<<2 * a.O + 1, prep_order_waves(P, a.O, a.E) * kWave, prep_order_lds(P, a.O, a.E), s>>>(    \
-      P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured, a.cand, a.E, a.O, dump, tiles, base, mopt, thr,  \
-      n_thr, list, live, a.thr_search, LV)
-#define FS_PREP_ORDER_K(NTP)                  \
-  if (P.K <= 4) FS_PREP_ORDER(4, NTP);        \
-  else if (P.K <= 8) FS_PREP_ORDER(8, NTP);   \
-  else FS_PREP_ORDER(16, NTP);
-      if (P.NT <= 4) {
-        FS_PREP_ORDER_K(4)
-      } else {
-        FS_PREP_ORDER_K(8)
-      }
-#undef FS_PREP_ORDER_K
-#undef FS_PREP_ORDER
-    } else {
-      // the work-list block reads staged inputs when they fit; tables in
-      // LDS when they fit, else in the workspace
-      const size_t lst = prep_list_lds(P, a.O, a.E);
-      const int staged = lst <= kPrepGeneralLdsLimit;
-      const bool in_lds = big <= kPrepGeneralLdsLimit;
-      size_t lds = in_lds ? big : small;
-      if (staged && lst > lds) lds = lst;
-      const void *fn = in_lds ? reinterpret_cast<const void *>(&k_prep<true>)
-                              : reinterpret_cast<const void *>(&k_prep<false>);
-      if (lds > 64 * 1024) {
-        const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-      }
-      if (in_lds)
-        k_prep<true><<<dim3(2, a.O, P.K + 1), kPrepThreads, lds, s>>>(
-            P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured, a.cand, a.E, dump, nullptr, tiles, base, mopt,
-            thr, n_thr, list, live, a.thr_search, staged);
-      else
-        k_prep<false><<<dim3(2, a.O, P.K + 1), kPrepThreads, lds, s>>>(
-            P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured, a.cand, a.E, dump, (int32_t *)(a.ws + a.L.tabB),
-            tiles, base, mopt, thr, n_thr, list, live, a.thr_search, staged);
-    }
+    hipError_t es = launch_excl_setup(P, a, s);
+    if (es != hipSuccess) return es;
     if (a.E == 0) {
       k_finalize<<<a.O, 64, 0, s>>>(P, info, a.measured, 0, a.S, base, partial, 1, a.score, a.gap_now,
                                     a.best);
@@ -3567,7 +3947,7 @@ hipError_t launch_solve_batch(const DevProblem &P, const float *cap, const float
 }
 
 size_t lds_bytes_lex(const DevProblem &P, int n_alloc) {
-  return sizeof(int) * (size_t)n_alloc * 2 * kMaxClasses + lex_work_bytes(P.K, P.G, P.optoff[P.NT]);
+  return sizeof(int) * (size_t)n_alloc * 2 * kMaxClasses + lex_work_bytes(P.K, P.G);
 }
 
 hipError_t launch_solve_batch_lex(const DevProblem &P, const float *cap, const float *tail, int64_t n,
@@ -3641,6 +4021,7 @@ LoopLayout loop_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
   L.gap_mm = take(8 * (size_t)O);
   L.gap_gp = take(8 * (size_t)O);
   L.lex_state = take(4 * (size_t)O);
+  L.lex_fast = lex_excl_regions(P, O, &at);
   L.total = at;
   return L;
 }
@@ -3704,6 +4085,28 @@ hipError_t launch_clamp_samples(const DevProblem &P, const int32_t *cand, int32_
   return hipGetLastError();
 }
 
+LexExclRegions lex_excl_regions(const DevProblem &P, int64_t O, size_t *at) {
+  LexExclRegions R{};
+  const int PP = P.optoff[P.NT], per_class = P.NT * P.B, nopt = P.K * PP;
+  R.nbmax = nopt + 1;
+  const size_t rows = (size_t)O * 2 * P.K * (size_t)(R.nbmax + 1);
+  const size_t vbytes = sizeof(double) * rows * ((size_t)P.G + 1);
+  R.fast = excl_kernel_supported(P) && lex_breaks_lds(nopt) <= kPrepGeneralLdsLimit &&
+           lex_tables_lds(nopt, per_class, P.G) <= kPrepGeneralLdsLimit && vbytes <= ((size_t)4 << 30);
+  auto take = [&](size_t bytes) {
+    const size_t here = *at;
+    *at = align256(*at + (bytes > 0 ? bytes : 1));
+    return here;
+  };
+  if (!R.fast) return R;
+  R.opt = take(sizeof(int2) * (size_t)O * 2 * nopt);
+  R.bp = take(sizeof(float) * (size_t)O * 2 * R.nbmax);
+  R.nbp = take(sizeof(int32_t) * (size_t)O * 2);
+  R.V = take(vbytes);
+  R.W = take(sizeof(double) * 4 * rows);
+  return R;
+}
+
 LexScoreLayout lex_score_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
   LexScoreLayout L{};
   L.score = ws_layout(P, O, E, S);
@@ -3717,14 +4120,16 @@ LexScoreLayout lex_score_layout(const DevProblem &P, int64_t O, int64_t E, int64
   L.gap_mm = take(sizeof(double) * (size_t)O);
   L.gap_gp = take(sizeof(double) * (size_t)O);
   L.state = take(sizeof(int32_t) * (size_t)O);
+  L.fast = lex_excl_regions(P, O, &at);
   L.total = at;
   return L;
 }
 
 hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const float *cap_hi, const float *tail_lo,
-                            const float *tail_hi, const uint8_t *measured, const float *cap_s, const float *tail_s,
-                            int32_t O, int32_t E, int32_t S, double *score_mm, double *score_gp, double *gap_mm,
-                            double *gap_gp, int32_t *best, uint8_t *ws, const LexScoreLayout &L, hipStream_t s) {
+                            const float *tail_hi, const uint8_t *measured, const int32_t *cand, const float *cap_s,
+                            const float *tail_s, int32_t O, int32_t E, int32_t S, double *score_mm,
+                            double *score_gp, double *gap_mm, double *gap_gp, int32_t *best, uint8_t *ws,
+                            const LexScoreLayout &L, int fast, hipStream_t s) {
   if (O == 0) return hipSuccess;
   double *gmm = gap_mm ? gap_mm : (double *)(ws + L.gap_mm);
   double *ggp = gap_gp ? gap_gp : (double *)(ws + L.gap_gp);
@@ -3735,7 +4140,52 @@ hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const floa
   const int64_t n_partial = L.score.n_partial;
   double *pmm = (double *)(ws + L.score.partial), *pgp = (double *)(ws + L.part_gp);
   const CandInfo *info = (const CandInfo *)(ws + L.score.cand);
-  if (S > 0) {
+  if (S > 0 && fast && L.fast.fast) {
+    // the max-min stage's set-up (U, M of every option), then the goodput
+    // stage's, then the scenarios
+    ScoreArgs a{};
+    a.cap_lo = cap_lo; a.cap_hi = cap_hi; a.tail_lo = tail_lo; a.tail_hi = tail_hi; a.measured = measured;
+    a.cand = cand; a.cap_s = cap_s; a.tail_s = tail_s; a.O = O; a.E = E; a.S = S;
+    a.ws = ws; a.L = L.score; a.kernel = 3;
+    e = launch_excl_setup(P, a, s);
+    if (e != hipSuccess) return e;
+    const LexExclRegions &X = L.fast;
+    const int nopt = P.K * P.optoff[P.NT], per_class = P.NT * P.B;
+    const size_t lds_b = lex_breaks_lds(nopt), lds_t = lex_tables_lds(nopt, per_class, P.G);
+    if (lds_b > 64 * 1024) {
+      e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_lex_breaks),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_b);
+      if (e != hipSuccess) return e;
+    }
+    if (lds_t > 64 * 1024) {
+      e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_lex_tables),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_t);
+      if (e != hipSuccess) return e;
+    }
+    k_lex_breaks<<<dim3(2, O), kLexPrepThreads, lds_b, s>>>(P, (const int8_t *)(ws + L.score.bmap), cap_lo, cap_hi,
+                                                           tail_lo, tail_hi, X.nbmax, (int2 *)(ws + X.opt),
+                                                           (float *)(ws + X.bp), (int32_t *)(ws + X.nbp));
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // blocks per (realisation, order, class): about 4096 wavefronts in all,
+    // no more than the intervals can use
+    const int64_t per = (int64_t)2 * O * P.K;
+    const int64_t want = (4096 / (per * (kLexPrepThreads / kWave))) + 1;
+    const int64_t cap_split = (X.nbmax + 1 + kLexPrepThreads / kWave - 1) / (kLexPrepThreads / kWave);
+    const int nsplit = (int)(want < cap_split ? want : cap_split);
+    k_lex_tables<<<dim3(2 * nsplit, O, P.K), kLexPrepThreads, lds_t, s>>>(
+        P, (const int8_t *)(ws + L.score.bmap), (const int2 *)(ws + X.opt), (const float *)(ws + X.bp),
+        (const int32_t *)(ws + X.nbp), X.nbmax, nsplit, (double *)(ws + X.V), (double *)(ws + X.W));
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const dim3 grid((unsigned)((S + kWave - 1) / kWave), (unsigned)E, (unsigned)O);
+    k_score_lex_excl<<<grid, kWave, sizeof(int) * 2 * (size_t)X.nbmax, s>>>(
+        P, (const TileInfo *)(ws + L.score.tiles), (const int32_t *)(ws + L.score.mopt), excl_thresholds(P), cap_s,
+        tail_s, E, S, (const float *)(ws + X.bp), (const int32_t *)(ws + X.nbp), X.nbmax,
+        (const double *)(ws + X.V), (const double *)(ws + X.W), pmm, pgp, n_partial);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  } else if (S > 0) {
     const size_t base = lds_bytes_lex(P, 1), staged = base + stage2_bytes(P);
     const int stage = stage_fits(staged) ? 1 : 0;
     const dim3 grid((unsigned)((S + kWave - 1) / kWave), (unsigned)E, (unsigned)O);

@@ -150,9 +150,10 @@ def test_unsupported_sizes_are_rejected(env):
     assert e.value.status == fs.FS_ERR_UNSUPPORTED
 
 
-def _gpu_loop(env, p, iv, tc, tt, cand, cs, ts, eps, objective, max_rounds=None):
+def _gpu_loop(env, p, iv, tc, tt, cand, cs, ts, eps, objective, max_rounds=None, kernel=0):
     torch, fs, ctx = env
     ctx.set_option(fs.OPT_LOOP_OBJECTIVE, objective)
+    ctx.set_score_kernel(kernel)
     try:
         r = fs.profile_loop(ctx, p, fs.DeviceIntervals.from_host(iv, "cuda:0"), _t(env, tc), _t(env, tt),
                             _t(env, np.asarray(cand, np.int32)), _t(env, cs), _t(env, ts), eps=eps,
@@ -160,6 +161,7 @@ def _gpu_loop(env, p, iv, tc, tt, cand, cs, ts, eps, objective, max_rounds=None)
         torch.cuda.synchronize()
     finally:
         ctx.set_option(fs.OPT_LOOP_OBJECTIVE, fs.OBJECTIVE_MAXMIN)
+        ctx.set_score_kernel(0)
     return {k: (v.cpu().numpy() if hasattr(v, "cpu") else {kk: vv.cpu().numpy() for kk, vv in v.items()})
             for k, v in vars(r).items()}
 
@@ -183,20 +185,21 @@ def test_hand_derived_loop_on_gpu(env, objective):
     assert r["tau_truth"][0] == np.float32(want["tau_truth"])
 
 
+@pytest.mark.parametrize("kernel", [0, 1])
 @pytest.mark.parametrize("name,orders,S,max_rounds", [("paper-shaped-2class-G16", list(range(8)), 64, None),
-                                                      ("4class-G64", [1, 2], 8, 12)])
-def test_loop_under_whole_objective_matches_oracle(env, name, orders, S, max_rounds):
+                                                      ("4class-G64", [1, 2], 8, 12), ("6class-G32", [0], 16, 8)])
+def test_loop_under_whole_objective_matches_oracle(env, name, orders, S, max_rounds, kernel):
     torch, fs, ctx = env
     w = make_workload(name, orders=orders)
     O = len(orders)
     tc = np.repeat(w.truth_cap[None], O, axis=0)
     tt = np.repeat(w.truth_tail[None], O, axis=0)
     cs, ts = np.ascontiguousarray(w.cap_s[:, :, :S]), np.ascontiguousarray(w.tail_s[:, :, :S])
-    note(f"lex loop {name} orders={orders} S={S}")
+    note(f"lex loop {name} orders={orders} S={S} kernel={kernel}")
     o = oracle.profile_loop(w.problem, w.intervals, tc, tt, w.cand, cs, ts, eps=0.05, max_rounds=max_rounds,
                             n_threads=8, objective="lex")
     r = _gpu_loop(env, w.problem, w.intervals, tc, tt, w.cand, cs, ts, 0.05, fs.OBJECTIVE_LEXICOGRAPHIC,
-                  max_rounds)
+                  max_rounds, kernel)
     np.testing.assert_array_equal(r["state"], o.state)
     np.testing.assert_array_equal(r["rounds"], o.rounds)
     np.testing.assert_array_equal(r["reveals"], o.reveals)
@@ -222,21 +225,79 @@ def test_hand_derived_stagewise_score_on_gpu(env):
     assert r.best.item() == c["best"]
 
 
+def _score_lex(env, w, cs, ts, kernel=0):
+    """The stage-wise score through the C ABI; kernel 1 solves every scenario
+    in full, the default takes the goodput stage from per-interval tables
+    where the problem allows it."""
+    torch, fs, ctx = env
+    div = fs.DeviceIntervals.from_host(w.intervals, "cuda:0")
+    ctx.set_score_kernel(kernel)
+    try:
+        r = fs.score_candidates_lex(ctx, w.problem, div, _t(env, w.cand), _t(env, cs), _t(env, ts))
+        torch.cuda.synchronize()
+    finally:
+        ctx.set_score_kernel(0)
+    return {k: getattr(r, k).cpu().numpy() for k in ("score_maxmin", "score_goodput", "gap_maxmin", "gap_goodput",
+                                                     "best")}
+
+
+def _assert_score_lex_equal(g, o, what):
+    np.testing.assert_array_equal(g["score_maxmin"], o.score_mm, err_msg=what)
+    np.testing.assert_array_equal(g["score_goodput"], o.score_gp, err_msg=what)
+    np.testing.assert_array_equal(g["gap_maxmin"], o.gap_mm, err_msg=what)
+    np.testing.assert_array_equal(g["gap_goodput"], o.gap_gp, err_msg=what)
+    np.testing.assert_array_equal(g["best"], o.best, err_msg=what)
+
+
+@pytest.mark.parametrize("kernel", [0, 1])
 @pytest.mark.parametrize("name,orders,S", [("paper-shaped-2class-G16", [0, 3, 5], 16), ("4class-G64", [1], 8),
-                                           ("tiny-2class-G16", None, 65)])
-def test_stagewise_score_matches_oracle(env, name, orders, S):
+                                           ("tiny-2class-G16", None, 65), ("6class-G32", [0, 1], 64),
+                                           ("12class-G64", [2], 16), ("4class-G64", [0, 5], 130)])
+def test_stagewise_score_matches_oracle(env, name, orders, S, kernel):
+    """Both scorers (full solves, kernel 1; per-interval tables, the default)
+    against the oracle bit for bit, with a ragged last chunk of samples where
+    S is not a multiple of 64; the max-min stage also against the max-min
+    scorer."""
     torch, fs, ctx = env
     w = make_workload(name, orders=orders)
     cs, ts = np.ascontiguousarray(w.cap_s[:, :, :S]), np.ascontiguousarray(w.tail_s[:, :, :S])
-    note(f"stage-wise score {name} orders={orders} S={S}")
-    div = fs.DeviceIntervals.from_host(w.intervals, "cuda:0")
-    r = fs.score_candidates_lex(ctx, w.problem, div, _t(env, w.cand), _t(env, cs), _t(env, ts))
-    m = fs.score_candidates(ctx, w.problem, div, _t(env, w.cand), _t(env, cs), _t(env, ts))
+    note(f"stage-wise score {name} orders={orders} S={S} kernel={kernel}")
+    g = _score_lex(env, w, cs, ts, kernel)
+    m = fs.score_candidates(ctx, w.problem, fs.DeviceIntervals.from_host(w.intervals, "cuda:0"), _t(env, w.cand),
+                            _t(env, cs), _t(env, ts))
     torch.cuda.synchronize()
     o = oracle.score_lex(w.problem, w.intervals, w.cand, cs, ts, n_threads=16)
-    np.testing.assert_array_equal(r.score_maxmin.cpu().numpy(), o.score_mm)
-    np.testing.assert_array_equal(r.score_goodput.cpu().numpy(), o.score_gp)
-    np.testing.assert_array_equal(r.gap_maxmin.cpu().numpy(), o.gap_mm)
-    np.testing.assert_array_equal(r.gap_goodput.cpu().numpy(), o.gap_gp)
-    np.testing.assert_array_equal(r.best.cpu().numpy(), o.best)
-    np.testing.assert_array_equal(r.score_maxmin.cpu().numpy(), m.score.cpu().numpy())
+    _assert_score_lex_equal(g, o, f"{name} kernel {kernel}")
+    np.testing.assert_array_equal(g["score_maxmin"], m.score.cpu().numpy())
+
+
+def test_stagewise_score_8class_matches_oracle(env):
+    """8 classes, G = 256 (about 450 distinct option ratios per realisation):
+    the per-interval tables against the oracle on one order."""
+    w = make_workload("8class-G256", orders=[3])
+    S = 4
+    cs, ts = np.ascontiguousarray(w.cap_s[:, :, :S]), np.ascontiguousarray(w.tail_s[:, :, :S])
+    note("stage-wise score 8class-G256 order 3 S=4")
+    g = _score_lex(env, w, cs, ts)
+    o = oracle.score_lex(w.problem, w.intervals, w.cand, cs, ts, n_threads=16)
+    _assert_score_lex_equal(g, o, "8class-G256")
+
+
+def test_stagewise_scorers_agree_at_bench_size(env):
+    """The configuration the stage-wise score is timed on (4 classes, G = 64,
+    16 orders, every cell a candidate, 64 samples): the per-interval tables
+    against the full solves bit for bit, and the oracle on sampled tiles."""
+    w = make_workload("4class-G64")
+    S = 64
+    cs, ts = np.ascontiguousarray(w.cap_s[:, :, :S]), np.ascontiguousarray(w.tail_s[:, :, :S])
+    note("stage-wise score 4class-G64 all orders S=64: tables vs full solves")
+    fast = _score_lex(env, w, cs, ts, 0)
+    full = _score_lex(env, w, cs, ts, 1)
+    for k in fast:
+        np.testing.assert_array_equal(fast[k], full[k], err_msg=k)
+    from paper_2608_19659_amd.synth import seeded_tiles, tile_mask
+    tiles = seeded_tiles(w, 24, seed=77)
+    o = oracle.score_lex(w.problem, w.intervals, w.cand, cs, ts, tile_mask=tile_mask(w, tiles), n_threads=16)
+    for (oi, e) in tiles:
+        assert fast["score_maxmin"][oi, e] == o.score_mm[oi, e], (oi, e)
+        assert fast["score_goodput"][oi, e] == o.score_gp[oi, e], (oi, e)
