@@ -491,24 +491,25 @@ def lex_work_per_scenario(problem) -> float:
     its budget slot: 5 + DIV_OPS); per class the prefix maximum (G - 1);
     each (max,min) target a crossing search (per step a compare and a
     select, then two selects and a max) -- every budget of the K - 2 middle
-    classes and budget G of the last; then per class and budget g one
-    candidate of level (3)'s knapsack per existing option with cost <= g: a
-    binary64 add, two compares and a select (4; binary64 adds issue at the
-    full rate on gfx950)."""
-    import numpy as np
+    classes and budget G of the last; then level (3)'s knapsack: per class
+    and cost c the options of that cost merged (per existing option its
+    ratio test and served rate, 5 + DIV_OPS, and a compare and two selects),
+    and per class and budget g one candidate per cost c <= g (a conversion,
+    a binary64 add, the (goodput, GPUs, option) order in four compares and
+    two logic ops, and four selects: 12; binary64 adds issue at the full
+    rate on gfx950)."""
     G, K = problem.budget, problem.n_classes
     ex = existing_options(problem)
-    per = int(ex.sum()) * (5 + DIV_OPS) + K * (G - 1)
+    n_ex = int(ex.sum())
+    per = n_ex * (5 + DIV_OPS) + K * (G - 1)
     if K >= 2:
         top = 1
         while 2 * top <= G + 1:
             top *= 2
         steps = int(math.log2(top)) + 1
         per += ((K - 2) * (G + 1) + 1) * (2 * steps + 3)
-    ex = ex.reshape(K, -1)
-    costs = np.concatenate([np.arange(1, G // int(t) + 1) * int(t) for t in problem.tp])
-    per_g = np.array([[(costs[ex[k] > 0] <= g).sum() for g in range(G + 1)] for k in range(K)])
-    return float(per) + 4.0 * float(per_g.sum())
+    per += n_ex * (5 + DIV_OPS + 3)
+    return float(per) + 12.0 * K * G * (G + 1) / 2
 
 
 def lex_bench(args):
@@ -553,8 +554,9 @@ def lex_bench(args):
 
     r_lex, ms_lex = timed(lambda: fs.solve_batch_lex(ctx, p, cap, tail, stream=stream, workspace=ws))
     _, ms_mm = timed(lambda: fs.solve_batch(ctx, p, cap, tail, stream=stream, workspace=ws))
-    # the stage-wise score (every scenario solved in full) on the workload's first
-    # args.lex_score_samples samples, against the max-min score on the same inputs
+    # the stage-wise score on the workload's first args.lex_score_samples samples:
+    # per-interval goodput tables (the default), every scenario solved in full
+    # (scoring kernel 1), and the max-min score on the same inputs
     ws_full = make_workload(name)
     Sx = min(args.lex_score_samples, ws_full.cap_s.shape[2])
     O, E = ws_full.cap_s.shape[:2]
@@ -563,6 +565,10 @@ def lex_bench(args):
     cand_d, cs_d, ts_d = t(ws_full.cand), t(ws_full.cap_s[:, :, :Sx]), t(ws_full.tail_s[:, :, :Sx])
     wsl = ctx.workspace(fs.score_lex_workspace_size(p, O, E, Sx))
     _, ms_sl = timed(lambda: fs.score_candidates_lex(ctx, p, div, cand_d, cs_d, ts_d, stream=stream, workspace=wsl))
+    ctx.set_score_kernel(1)
+    _, ms_full = timed(lambda: fs.score_candidates_lex(ctx, p, div, cand_d, cs_d, ts_d, stream=stream,
+                                                       workspace=wsl))
+    ctx.set_score_kernel(0)
     _, ms_sm = timed(lambda: fs.score_candidates(ctx, p, div, cand_d, cs_d, ts_d, stream=stream))
     live = int((~ws_full.intervals.measured[:, ws_full.cand].astype(bool)).sum()) * Sx
     slots = lex_work_per_scenario(p)
@@ -593,7 +599,7 @@ def lex_bench(args):
         "maxmin_only": {"value": n / (ms_mm / 1e3), "ms_per_step": ms_mm},
         "stagewise_score": {"samples": Sx, "scenarios_per_call": live, "ms_per_call": ms_sl,
                             "value": live / (ms_sl / 1e3), "unit": "scenarios/s",
-                            "maxmin_score_ms_per_call": ms_sm},
+                            "full_solves_ms_per_call": ms_full, "maxmin_score_ms_per_call": ms_sm},
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_OPS / 1e12, "unit": "TOP/s",
                      "frac": achieved / VALU_PEAK_OPS, "traffic": None, "kernel": "k_solve_dense_lex",
                      "op": "VALU lane-slot", "slots_per_scenario": slots, "scenarios_per_launch": n,

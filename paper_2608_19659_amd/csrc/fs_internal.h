@@ -73,6 +73,7 @@ struct WsLayout {
   size_t thr;        // float [O][2][K*P] capacity threshold of every option
   size_t list;       // int4 [O * E] live tiles of every order, longest replica range first
   size_t live;       // int32 [1] number of listed tiles
+  size_t crec;       // [O][2] per-realisation results of the certificate under the whole objective
   size_t flag;     // int32 [4]        validation / error flags
   size_t total;
   int64_t n_partial;  // ceil(S / 64)

@@ -2708,59 +2708,81 @@ __global__ __launch_bounds__(64) void k_solve_dense_lex(DevProblem P, const int8
 
 // Certificate with the stage-wise gap: both allocations under the whole
 // objective; max-min gap tau+ - tau-, goodput gap |gp+ - gp-| / max(gp+,
-// gp-) (0 when both are 0); within eps means both stages are.
+// gp-) (0 when both are 0); within eps means both stages are.  Block (R, o)
+// solves realisation R of order o (0: conservative, 1: optimistic) and
+// keeps its result in a record; k_certify_lex_state then takes each
+// order's gaps and state from the two records.
+struct CertRec {
+  int32_t tau, floors_met;
+  float goodput;
+  int32_t pad;
+  double goodput64;
+  int32_t tp_index[kMaxClasses], replicas[kMaxClasses];
+};
+
 __global__ __launch_bounds__(64) void k_certify_lex(DevProblem P, const int8_t *__restrict__ bmap,
                                                     const float *__restrict__ cap_lo,
                                                     const float *__restrict__ cap_hi,
                                                     const float *__restrict__ tail_lo,
-                                                    const float *__restrict__ tail_hi,
-                                                    const uint8_t *__restrict__ measured, float eps,
-                                                    int32_t *__restrict__ state, AllocOut cons, AllocOut opt,
-                                                    double *__restrict__ gap_mm_out,
-                                                    double *__restrict__ gap_gp_out, int stage) {
+                                                    const float *__restrict__ tail_hi, AllocOut cons,
+                                                    AllocOut opt, CertRec *__restrict__ rec, int stage) {
   extern __shared__ int lds[];
-  const int o = blockIdx.x, lane = threadIdx.x;
+  const int R = blockIdx.x, o = blockIdx.y, lane = threadIdx.x;
   const size_t off = (size_t)o * P.N;
-  int *tm_index = lds;
-  int *tm_rep = tm_index + kMaxClasses;
-  int *tp_index = tm_rep + kMaxClasses;
-  int *tp_rep = tp_index + kMaxClasses;
-  int *work = tp_rep + kMaxClasses;
-  WaveAlloc am{tm_index, tm_rep}, ap{tp_index, tp_rep};
+  int *t_index = lds;
+  int *t_rep = t_index + kMaxClasses;
+  int *work = t_rep + kMaxClasses;
+  WaveAlloc wa{t_index, t_rep};
   const LexLds X = lex_lds(P, work);
   const StageArea A = stage_area(P, reinterpret_cast<char *>(work) + lex_work_bytes(P.K, P.G));
   const int8_t *bm = bmap;
-  int fm_m, fm_p;
-  float gp_m, gp_p;
-  double g64_m, g64_p;
-  Realisation rm{cap_lo + off, tail_hi + off, -1, 0.0f, 0.0f};
+  Realisation rz = R == 0 ? Realisation{cap_lo + off, tail_hi + off, -1, 0.0f, 0.0f}
+                          : Realisation{cap_hi + off, tail_lo + off, -1, 0.0f, 0.0f};
   if (stage) {
     stage_copy_bmap(P, bmap, A.bmap);
-    stage_copy_cells(P, rm.cap, rm.tail, A.cap, A.tail);
+    stage_copy_cells(P, rz.cap, rz.tail, A.cap, A.tail);
     bm = A.bmap;
-    rm = Realisation{A.cap, A.tail, -1, 0.0f, 0.0f};
+    rz = Realisation{A.cap, A.tail, -1, 0.0f, 0.0f};
     __syncthreads();
   }
-  const int tau_m = wave_solve(P, bm, rm, work, &fm_m, nullptr, nullptr);
-  wave_lex_stage(P, bm, rm, tau_m, fm_m, X, am, &gp_m, &g64_m);
-  Realisation rp{cap_hi + off, tail_lo + off, -1, 0.0f, 0.0f};
-  if (stage) {
-    stage_copy_cells(P, rp.cap, rp.tail, A.cap, A.tail);
-    rp = Realisation{A.cap, A.tail, -1, 0.0f, 0.0f};
-    __syncthreads();
+  int fm;
+  float gp;
+  double g64;
+  const int tau = wave_solve(P, bm, rz, work, &fm, nullptr, nullptr);
+  wave_lex_stage(P, bm, rz, tau, fm, X, wa, &gp, &g64);
+  write_alloc(R == 0 ? cons : opt, o, P.K, tau, fm, gp, wa);
+  CertRec *me = rec + (size_t)o * 2 + R;
+  if (lane == 0) {
+    me->tau = tau;
+    me->floors_met = fm;
+    me->goodput = gp;
+    me->goodput64 = g64;
   }
-  const int tau_p = wave_solve(P, bm, rp, work, &fm_p, nullptr, nullptr);
-  wave_lex_stage(P, bm, rp, tau_p, fm_p, X, ap, &gp_p, &g64_p);
-  write_alloc(cons, o, P.K, tau_m, fm_m, gp_m, am);
-  write_alloc(opt, o, P.K, tau_p, fm_p, gp_p, ap);
-  if (lane != 0) return;
-  const double gap_mm = (double)__int_as_float(tau_p) - (double)__int_as_float(tau_m);
+  for (int k = lane; k < P.K; k += kWave) {
+    me->tp_index[k] = t_index[k];
+    me->replicas[k] = t_rep[k];
+  }
+}
+
+__global__ __launch_bounds__(64) void k_certify_lex_state(DevProblem P, const int8_t *__restrict__ bmap,
+                                                          const float *__restrict__ tail_hi,
+                                                          const uint8_t *__restrict__ measured, float eps,
+                                                          const CertRec *__restrict__ rec,
+                                                          int32_t *__restrict__ state,
+                                                          double *__restrict__ gap_mm_out,
+                                                          double *__restrict__ gap_gp_out) {
+  const int o = blockIdx.x;
+  if (threadIdx.x != 0) return;
+  const size_t off = (size_t)o * P.N;
+  const CertRec *m = rec + (size_t)o * 2, *p = m + 1;
+  const double gap_mm = (double)__int_as_float(p->tau) - (double)__int_as_float(m->tau);
+  const double g64_m = m->goodput64, g64_p = p->goodput64;
   const double top = g64_p > g64_m ? g64_p : g64_m;
   const double gap_gp = top > 0.0 ? fabs(g64_p - g64_m) / top : 0.0;
   if (gap_mm_out) gap_mm_out[o] = gap_mm;
   if (gap_gp_out) gap_gp_out[o] = gap_gp;
-  state[o] = certificate_state(P, bmap, measured, tail_hi, off, fm_m, fm_p, tm_index, tm_rep,
-                               gap_mm <= (double)eps && gap_gp <= (double)eps);
+  state[o] = certificate_state(P, bmap, measured, tail_hi, off, m->floors_met, p->floors_met, m->tp_index,
+                               m->replicas, gap_mm <= (double)eps && gap_gp <= (double)eps);
 }
 
 // ---------------------------------------------------------------------------
@@ -2895,11 +2917,12 @@ __host__ __device__ inline size_t lex_breaks_lds(int nopt) {
 }
 
 // LDS of a k_lex_tables block: every option's (ratio, served rate), the
-// candidate class's replica range per cell, then per wavefront two
-// knapsack layers (binary64) and one class's best served rate per cost.
-__host__ __device__ inline size_t lex_tables_lds(int nopt, int per_class, int G) {
+// candidate class's options (cost, cell), then per wavefront two knapsack
+// layers (binary64) and one class's best served rate per cost.
+__host__ __device__ inline size_t lex_tables_lds(int nopt, int per_class_options, int G) {
   const size_t nw = kLexPrepThreads / kWave;
-  return 8 * (size_t)nopt + 8 * (size_t)per_class + nw * (16 * ((size_t)G + 1) + 4 * (((size_t)G + 2) & ~(size_t)1));
+  return 8 * (size_t)nopt + 8 * (size_t)per_class_options +
+         nw * (16 * ((size_t)G + 1) + 4 * (((size_t)G + 2) & ~(size_t)1));
 }
 
 // Per (realisation R, order o): every option of every class (ratio bits, -1
@@ -2969,16 +2992,27 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_breaks(DevProblem P, co
     const int v = lex_keys[a];
     mine += (v != INT_MAX && (a == 0 || lex_keys[a - 1] != v)) ? 1 : 0;
   }
-  cnt[tid] = mine;
+  // inclusive scan within the wavefront, then the totals of the ones before
+  const int lane = tid & (kWave - 1), wave = tid >> 6;
+  int incl = mine;
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int v = __shfl_up(incl, d, kWave);
+    if (lane >= d) incl += v;
+  }
+  if (lane == kWave - 1) cnt[wave] = incl;
   __syncthreads();
-  int before = 0;
-  for (int t = 0; t < tid; ++t) before += cnt[t];
+  int before = incl - mine, total = 0;
+  for (int w = 0; w < kLexPrepThreads / kWave; ++w) {
+    before += w < wave ? cnt[w] : 0;
+    total += cnt[w];
+  }
   float *bp = bp_out + ((size_t)o * 2 + R) * nbmax;
   for (int a = a0; a < a0 + seg; ++a) {
     const int v = lex_keys[a];
     if (v != INT_MAX && (a == 0 || lex_keys[a - 1] != v)) bp[before++] = __int_as_float(v);
   }
-  if (tid == kLexPrepThreads - 1) nbp[o * 2 + R] = before;
+  if (tid == 0) nbp[o * 2 + R] = total;
 }
 
 // Per (realisation R, order o, class i) and interval j of the breakpoints
@@ -3004,16 +3038,16 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_tables(DevProblem P, co
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   constexpr int nw = kLexPrepThreads / kWave;
-  const int K = P.K, G = P.G, B = P.B, NT = P.NT, per_class = NT * B, PP = P.optoff[NT];
+  const int K = P.K, G = P.G, B = P.B, NT = P.NT, PP = P.optoff[NT];
   const int nopt = K * PP;
   const int nb = nbp[o * 2 + R];
   const int first = part * nw + wave, step = nsplit * nw;
   int *oratio = reinterpret_cast<int *>(lex_tab_lds);  // [nopt]
   float *oserved = reinterpret_cast<float *>(oratio + nopt);
-  int2 *crange = reinterpret_cast<int2 *>(oserved + nopt);  // [per_class] class i's replica range per cell
-  double *Va = reinterpret_cast<double *>(crange + per_class) + (size_t)wave * 2 * (G + 1);
+  int2 *icost = reinterpret_cast<int2 *>(oserved + nopt);  // [PP] class i's options: cost, cell
+  double *Va = reinterpret_cast<double *>(icost + PP) + (size_t)wave * 2 * (G + 1);
   double *Vb = Va + G + 1;
-  float *Ak = reinterpret_cast<float *>(reinterpret_cast<double *>(crange + per_class) + (size_t)nw * 2 * (G + 1)) +
+  float *Ak = reinterpret_cast<float *>(reinterpret_cast<double *>(icost + PP) + (size_t)nw * 2 * (G + 1)) +
               (size_t)wave * ((G + 2) & ~1);
   if (part * nw > nb) return;  // no interval for this block
   const int2 *opt = opt_in + ((size_t)o * 2 + R) * nopt;
@@ -3022,16 +3056,13 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_tables(DevProblem P, co
     oratio[q] = v.x;
     oserved[q] = __int_as_float(v.y);
   }
-  for (int c = tid; c < per_class; c += kLexPrepThreads) {
-    const int ti = c / B, b = c - ti * B, t = P.tp[ti];
-    int rlo = INT_MAX, rhi = -1;
-    for (int r = 1; r <= G / t; ++r) {
-      if (bmap[i * (G + 1) + r] == b) {
-        rlo = min(rlo, r);
-        rhi = max(rhi, r);
-      }
-    }
-    crange[c] = make_int2(rlo, rhi);
+  // class i's options: (cost, cell within the class; -1 when no level holds it)
+  for (int p = tid; p < PP; p += kLexPrepThreads) {
+    int ti = 0;
+    while (ti + 1 < NT && p >= P.optoff[ti + 1]) ++ti;
+    const int r = p - P.optoff[ti] + 1;
+    const int b = bmap[i * (G + 1) + r];
+    icost[p] = make_int2(P.tp[ti] * r, b >= 0 ? ti * B + b : -1);
   }
   __syncthreads();
   const double NEG = -__builtin_inf();
@@ -3087,37 +3118,36 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_tables(DevProblem P, co
     }
     double *Vg = Vout + (row0 + j) * (size_t)(G + 1);
     for (int g = lane; g <= G; g += kWave) Vg[g] = Vp[g];
-    // class i's options per cell: the best served + V[G - cost]; the two
-    // largest over the cells (and the first one's cell) by a butterfly
+    // class i's allowed options: served + V[G - cost], reduced to the
+    // largest value w1 (with a cell c1 holding it) and w2, the largest over
+    // the cells other than c1.  Merging two such summaries: same c1, the
+    // larger of each; else the larger w1 leads and the other's w1 (from
+    // another cell) competes for w2.  Lanes over the options, then a
+    // butterfly (the merge is symmetric, so every lane ends with the same).
     double w1 = NEG, w2 = NEG;
     int c1 = -1;
-    for (int c = lane; c < per_class; c += kWave) {
-      const int2 rr = crange[c];
-      const int ti = c / B, t = P.tp[ti];
-      double best = NEG;
-      for (int r = rr.x; r <= rr.y; ++r) {
-        const int q = i * PP + P.optoff[ti] + r - 1;
-        if (oratio[q] >= thr) best = fmax(best, (double)oserved[q] + Vp[G - t * r]);
+    auto merge = [&](double b1, int bc, double b2) {
+      if (bc == c1) {
+        w1 = fmax(w1, b1);
+        w2 = fmax(w2, b2);
+      } else if (b1 > w1 || (b1 == w1 && bc > c1)) {
+        w2 = fmax(b2, w1);
+        w1 = b1;
+        c1 = bc;
+      } else {
+        w2 = fmax(w2, b1);
       }
-      if (best > w1) {
-        w2 = w1;
-        w1 = best;
-        c1 = c;
-      } else if (best > w2) {
-        w2 = best;
-      }
+    };
+    for (int p = lane; p < PP; p += kWave) {
+      const int2 ic = icost[p];
+      const int q = i * PP + p;
+      if (ic.y >= 0 && oratio[q] >= thr) merge((double)oserved[q] + Vp[G - ic.x], ic.y, NEG);
     }
 #pragma unroll
     for (int m = 1; m < kWave; m <<= 1) {
       const double o1 = __shfl_xor(w1, m, kWave), o2 = __shfl_xor(w2, m, kWave);
       const int oc = __shfl_xor(c1, m, kWave);
-      if (o1 > w1 || (o1 == w1 && oc > c1)) {  // the larger first, equal ones by the larger cell index
-        w2 = fmax(o2, w1);
-        w1 = o1;
-        c1 = oc;
-      } else {
-        w2 = fmax(w2, o1);
-      }
+      merge(o1, oc, o2);
     }
     if (lane == 0) {
       double *Wj = Wout + (row0 + j) * 4;
@@ -3748,6 +3778,7 @@ WsLayout ws_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
   L.thr = at; at = align256(at + sizeof(float) * n_opt);
   L.list = at; at = align256(at + sizeof(int4) * (size_t)O * (size_t)E);
   L.live = at; at = align256(at + sizeof(int32_t));
+  L.crec = at; at = align256(at + sizeof(CertRec) * 2 * (size_t)(O > 0 ? O : 1));
   L.total = at;
   return L;
 }
@@ -3965,11 +3996,15 @@ hipError_t launch_certify_lex(const DevProblem &P, const float *cap_lo, const fl
                               AllocOut cons, AllocOut opt, double *gap_mm, double *gap_gp, uint8_t *ws,
                               const WsLayout &L, hipStream_t s) {
   if (O == 0) return hipSuccess;
-  const size_t base = lds_bytes_lex(P, 2), staged = base + stage_bytes(P);
+  const size_t base = lds_bytes_lex(P, 1), staged = base + stage_bytes(P);
   const int stage = stage_fits(staged) ? 1 : 0;
-  k_certify_lex<<<O, 64, stage ? staged : base, s>>>(P, (const int8_t *)(ws + L.bmap), cap_lo, cap_hi, tail_lo,
-                                                     tail_hi, measured, eps, state, cons, opt, gap_mm, gap_gp,
-                                                     stage);
+  CertRec *rec = (CertRec *)(ws + L.crec);
+  const int8_t *bmap = (const int8_t *)(ws + L.bmap);
+  k_certify_lex<<<dim3(2, O), 64, stage ? staged : base, s>>>(P, bmap, cap_lo, cap_hi, tail_lo, tail_hi, cons, opt,
+                                                              rec, stage);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  k_certify_lex_state<<<O, 64, 0, s>>>(P, bmap, tail_hi, measured, eps, rec, state, gap_mm, gap_gp);
   return hipGetLastError();
 }
 
@@ -4087,12 +4122,12 @@ hipError_t launch_clamp_samples(const DevProblem &P, const int32_t *cand, int32_
 
 LexExclRegions lex_excl_regions(const DevProblem &P, int64_t O, size_t *at) {
   LexExclRegions R{};
-  const int PP = P.optoff[P.NT], per_class = P.NT * P.B, nopt = P.K * PP;
+  const int PP = P.optoff[P.NT], nopt = P.K * PP;
   R.nbmax = nopt + 1;
   const size_t rows = (size_t)O * 2 * P.K * (size_t)(R.nbmax + 1);
   const size_t vbytes = sizeof(double) * rows * ((size_t)P.G + 1);
   R.fast = excl_kernel_supported(P) && lex_breaks_lds(nopt) <= kPrepGeneralLdsLimit &&
-           lex_tables_lds(nopt, per_class, P.G) <= kPrepGeneralLdsLimit && vbytes <= ((size_t)4 << 30);
+           lex_tables_lds(nopt, PP, P.G) <= kPrepGeneralLdsLimit && vbytes <= ((size_t)4 << 30);
   auto take = [&](size_t bytes) {
     const size_t here = *at;
     *at = align256(*at + (bytes > 0 ? bytes : 1));
@@ -4150,8 +4185,8 @@ hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const floa
     e = launch_excl_setup(P, a, s);
     if (e != hipSuccess) return e;
     const LexExclRegions &X = L.fast;
-    const int nopt = P.K * P.optoff[P.NT], per_class = P.NT * P.B;
-    const size_t lds_b = lex_breaks_lds(nopt), lds_t = lex_tables_lds(nopt, per_class, P.G);
+    const int nopt = P.K * P.optoff[P.NT];
+    const size_t lds_b = lex_breaks_lds(nopt), lds_t = lex_tables_lds(nopt, P.optoff[P.NT], P.G);
     if (lds_b > 64 * 1024) {
       e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_lex_breaks),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_b);
