@@ -284,6 +284,33 @@ __device__ __forceinline__ int conv_mono(const int *X, const int *Y, int g, int 
   return max(pos >= 1 ? left : INT_MIN, pos <= g ? right : INT_MIN);
 }
 
+// Folds options into their cells' maxima and replica ranges.  Lanes holding
+// consecutive options of one TP degree fall on few cells (the load level
+// falls as r grows), in runs of lanes; the first lane of each run folds the
+// run's largest value and replica range in with one LDS atomic each, where
+// one per lane would queue up on the same bank.  key: the cell within the
+// class, -1 for a lane with no option.  Every lane of the wavefront calls
+// it (the shuffles read every lane); r grows along a run.
+__device__ __forceinline__ void fold_cell_runs(int key, int w, int r, int *mc, int *crlo, int *crhi) {
+  const int lane = threadIdx.x & (kWave - 1);
+  int wmax = w, rmax = r;
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int k2 = __shfl_down(key, d, kWave);
+    const int w2 = __shfl_down(wmax, d, kWave);
+    const int r2 = __shfl_down(rmax, d, kWave);
+    const bool in = lane + d < kWave && k2 == key;
+    wmax = in ? max(wmax, w2) : wmax;
+    rmax = in ? max(rmax, r2) : rmax;
+  }
+  const int kprev = __shfl_up(key, 1, kWave);
+  if (key >= 0 && (lane == 0 || kprev != key)) {
+    atomicMax(&mc[key], wmax);
+    atomicMin(&crlo[key], r);
+    atomicMax(&crhi[key], rmax);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Wave-per-scenario solver.
 // ---------------------------------------------------------------------------
@@ -1069,8 +1096,8 @@ __device__ void prep_list_staged(const DevProblem &P, const int8_t *lvl_tab, int
                                  int dump, int PPc, TileInfo *__restrict__ tiles, int4 *__restrict__ list,
                                  int32_t *__restrict__ n_listed, int *lds);
 
-template <bool kLds>
-__global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restrict__ cap_lo,
+template <bool kLds, int kThreads>
+__global__ __launch_bounds__(kThreads) void k_prep(DevProblem P, const float *__restrict__ cap_lo,
                                              const float *__restrict__ cap_hi,
                                              const float *__restrict__ tail_lo,
                                              const float *__restrict__ tail_hi,
@@ -1256,26 +1283,32 @@ __global__ __launch_bounds__(512) void k_prep(DevProblem P, const float *__restr
     float *To = thr + ((size_t)o * 2 + R) * n_thr + (size_t)ci * PPc;
     const float slo = P.slo[ci], demand = P.demand[ci];
     const double rcp = P.rcp_demand[ci];
-    for (int p = tid; p < PPc; p += nth) {
-      int ti = 0;
-      while (ti + 1 < NT && p >= C.optoff[ti + 1]) ++ti;
-      const int r = p - C.optoff[ti] + 1, t = C.tp[ti];
-      const int b = lvl[ci * G + r - 1];
-      if (b < 0) {
-        Mo[p] = INT_MIN;
-        To[p] = __builtin_nanf("");
-        continue;
+    // whole wavefronts per pass (the cell folds shuffle across lanes)
+    for (int p0 = tid - lane; p0 < PPc; p0 += nth) {
+      const int p = p0 + lane;
+      int key = -1, w = 0, r = 1;
+      if (p < PPc) {
+        int ti = 0;
+        while (ti + 1 < NT && p >= C.optoff[ti + 1]) ++ti;
+        r = p - C.optoff[ti] + 1;
+        const int t = C.tp[ti];
+        const int b = lvl[ci * G + r - 1];
+        if (b < 0) {
+          Mo[p] = INT_MIN;
+          To[p] = __builtin_nanf("");
+        } else {
+          const int local = ti * B + b, cell = ci * per_class + local;
+          // ratios never exceed 1, so M above 1 acts as 1 (min(f, M) and the
+          // crossing are unchanged) and the scorer can skip the clamp of f
+          const int M = min(H[G - t * r], __float_as_int(1.0f));
+          const int f = ratio_bits(ccap[cell], ctail[cell], r, slo, rcp);
+          key = local;
+          w = min(f, M);
+          Mo[p] = M;
+          To[p] = capacity_threshold(r, M, demand, rcp, thr_mode);
+        }
       }
-      const int local = ti * B + b, cell = ci * per_class + local;
-      // ratios never exceed 1, so M above 1 acts as 1 (min(f, M) and the
-      // crossing are unchanged) and the scorer can skip the clamp of f
-      const int M = min(H[G - t * r], __float_as_int(1.0f));
-      const int f = ratio_bits(ccap[cell], ctail[cell], r, slo, rcp);
-      atomicMax(&mc[local], min(f, M));
-      atomicMin(&crlo[local], r);
-      atomicMax(&crhi[local], r);
-      Mo[p] = M;
-      To[p] = capacity_threshold(r, M, demand, rcp, thr_mode);
+      fold_cell_runs(key, w, r, mc, crlo, crhi);
     }
   }
   __syncthreads();
@@ -1732,14 +1765,9 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
       }
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        if (!has[u]) continue;
+        if (do_cells) fold_cell_runs(ok[u] ? loc[u] : -1, min(fv[u], Mv[u]), rr[u], mc, crlo, crhi);
         const int p = base + lane + u * kWave;
-        if (do_cells && ok[u]) {
-          atomicMax(&mc[loc[u]], min(fv[u], Mv[u]));
-          atomicMin(&crlo[loc[u]], rr[u]);
-          atomicMax(&crhi[loc[u]], rr[u]);
-        }
-        if (do_thr) {
+        if (do_thr && has[u]) {
           Mo[p] = Mv[u];
           To[p] = Tv[u];
         }
@@ -2267,24 +2295,28 @@ __device__ __forceinline__ uint64_t wave_ext_u64(uint64_t v) {
   return pick(pick(readlane_u64(v, 0), readlane_u64(v, 16)), pick(readlane_u64(v, 32), readlane_u64(v, 48)));
 }
 
-// Scores and best candidate of the exclusion scorer: one wavefront per
-// order, lane l taking candidates l, l + 64, ... two at a time (their loads
-// overlap).  Each tile's partials (at most 16 here) are summed by the
-// pairwise tree in registers.  The arg-max is two key reductions: the
-// largest score, then the smallest (TP, cell, index) among the lanes
-// holding it -- the order that `better` defines.
-__global__ __launch_bounds__(64) void k_finalize_excl(const TileInfo *__restrict__ tiles, int32_t E,
-                                                      int32_t S, const int32_t *__restrict__ base,
-                                                      const double *__restrict__ partial,
-                                                      int64_t n_partial, double *__restrict__ score,
-                                                      double *__restrict__ gap_now,
-                                                      int32_t *__restrict__ best) {
-  const int o = blockIdx.x, lane = threadIdx.x;
+// Scores and best candidate of the exclusion scorer: one block per order
+// of one wavefront per 128 candidates (at most 16), lane l of wavefront w
+// taking candidates 128 w + l, 128 w + l + 64, then the next 128 nw, ...
+// two at a time (their loads overlap).  Each tile's partials (at most 16
+// here) are summed by the pairwise tree in registers.  The arg-max is two
+// key reductions per wavefront -- the largest score, then the smallest
+// (TP, cell, index) among the lanes holding it, the order that `better`
+// defines -- then the same over the wavefronts' results.
+constexpr int kFinalizeMaxWaves = 16;
+
+__global__ __launch_bounds__(64 * kFinalizeMaxWaves) void k_finalize_excl(
+    const TileInfo *__restrict__ tiles, int32_t E, int32_t S, const int32_t *__restrict__ base,
+    const double *__restrict__ partial, int64_t n_partial, double *__restrict__ score,
+    double *__restrict__ gap_now, int32_t *__restrict__ best) {
+  __shared__ uint64_t s_key[kFinalizeMaxWaves], s_tie[kFinalizeMaxWaves];
+  const int o = blockIdx.x, lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const double gap = (double)__int_as_float(base[o * 2 + 1]) - (double)__int_as_float(base[o * 2 + 0]);
   int p2 = 1;
   while (p2 < n_partial) p2 <<= 1;
   uint64_t kbest = 0, tbest = ~0ull;
-  for (int e0 = lane; e0 < E; e0 += 2 * kWave) {
+  for (int e0 = wave * 2 * kWave + lane; e0 < E; e0 += nw * 2 * kWave) {
     double v[2][16];
     TileInfo tl[2];
 #pragma unroll
@@ -2332,7 +2364,19 @@ __global__ __launch_bounds__(64) void k_finalize_excl(const TileInfo *__restrict
   const uint64_t kmax = wave_ext_u64<true>(kbest);
   const uint64_t tmin = wave_ext_u64<false>(kbest == kmax ? tbest : ~0ull);
   if (lane == 0) {
-    if (best) best[o] = kmax != 0 ? (int32_t)(uint32_t)tmin : -1;
+    s_key[wave] = kmax;
+    s_tie[wave] = tmin;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t K = 0, T = ~0ull;
+    for (int w = 0; w < nw; ++w) {
+      if (s_key[w] > K || (s_key[w] == K && s_tie[w] < T)) {
+        K = s_key[w];
+        T = s_tie[w];
+      }
+    }
+    if (best) best[o] = K != 0 ? (int32_t)(uint32_t)T : -1;
     if (gap_now) gap_now[o] = gap;
   }
 }
@@ -3708,9 +3752,12 @@ hipError_t scratch_address(void **ptr) { return hipGetSymbolAddress(ptr, HIP_SYM
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // Dynamic LDS the exclusion set-up kernel may request, and its block size
-// (its passes are short and latency-bound: width shortens them).
+// (its passes are short and latency-bound: width shortens them).  Budgets
+// of 512 GPUs and more take 1024 threads: the 16-class, G = 1024 scoring
+// step took 94.7 us with 512 and 75.9 with 1024, the 8-class, G = 256 one
+// 119.6 with 512 and 139.5 with 1024.
 constexpr size_t kPrepLdsLimit = 60 * 1024;
-constexpr int kPrepThreads = 512;
+constexpr int kPrepThreads = 512, kPrepThreadsWide = 1024, kPrepWideBudget = 512;
 
 // LDS of the exclusion set-up besides its tables: cells (cap, tail), the
 // class's cell maxima and replica ranges, and the load-level table.
@@ -3843,20 +3890,27 @@ static hipError_t launch_excl_setup(const DevProblem &P, const ScoreArgs &a, hip
     const bool in_lds = big <= kPrepGeneralLdsLimit;
     size_t lds = in_lds ? big : small;
     if (staged && lst > lds) lds = lst;
-    const void *fn = in_lds ? reinterpret_cast<const void *>(&k_prep<true>)
-                            : reinterpret_cast<const void *>(&k_prep<false>);
-    if (lds > 64 * 1024) {
-      const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-      if (e != hipSuccess) return e;
+    int32_t *gtab = in_lds ? nullptr : (int32_t *)(a.ws + a.L.tabB);
+    const dim3 grid(2, a.O, P.K + 1);
+#define FS_PREP_GENERAL(LDS, TH)                                                                                  \
+  {                                                                                                               \
+    if (lds > 64 * 1024) {                                                                                        \
+      const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_prep<LDS, TH>),                  \
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);             \
+      if (e != hipSuccess) return e;                                                                              \
+    }                                                                                                             \
+    k_prep<LDS, TH><<<grid, TH, lds, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured, a.cand, a.E,   \
+                                          dump, gtab, tiles, base, mopt, thr, n_thr, list, live, a.thr_search,    \
+                                          staged);                                                                \
+  }
+    if (P.G >= kPrepWideBudget) {
+      if (in_lds) FS_PREP_GENERAL(true, kPrepThreadsWide)
+      else FS_PREP_GENERAL(false, kPrepThreadsWide)
+    } else {
+      if (in_lds) FS_PREP_GENERAL(true, kPrepThreads)
+      else FS_PREP_GENERAL(false, kPrepThreads)
     }
-    if (in_lds)
-      k_prep<true><<<dim3(2, a.O, P.K + 1), kPrepThreads, lds, s>>>(
-          P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured, a.cand, a.E, dump, nullptr, tiles, base, mopt,
-          thr, n_thr, list, live, a.thr_search, staged);
-    else
-      k_prep<false><<<dim3(2, a.O, P.K + 1), kPrepThreads, lds, s>>>(
-          P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured, a.cand, a.E, dump, (int32_t *)(a.ws + a.L.tabB),
-          tiles, base, mopt, thr, n_thr, list, live, a.thr_search, staged);
+#undef FS_PREP_GENERAL
   }
   return hipGetLastError();
 }
@@ -3916,8 +3970,10 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
     }
     if (a.ev_end) (void)hipEventRecord(a.ev_end, s);
     if (n_partial <= 16) {
-      k_finalize_excl<<<a.O, kWave, 0, s>>>(tiles, a.E, a.S, base, partial, n_partial, a.score, a.gap_now,
-                                          a.best);
+      const int fw = (int)((a.E + 2 * kWave - 1) / (2 * kWave));
+      const int nwf = fw < 1 ? 1 : (fw > kFinalizeMaxWaves ? kFinalizeMaxWaves : fw);
+      k_finalize_excl<<<a.O, kWave * nwf, 0, s>>>(tiles, a.E, a.S, base, partial, n_partial, a.score,
+                                                  a.gap_now, a.best);
     } else {
       k_tile_scores_wave<<<dim3((a.E + 3) / 4, a.O), 256, 0, s>>>(tiles, a.E, a.S, base, partial, n_partial,
                                                                  a.score);
