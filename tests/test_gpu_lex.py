@@ -301,3 +301,58 @@ def test_stagewise_scorers_agree_at_bench_size(env):
     for (oi, e) in tiles:
         assert fast["score_maxmin"][oi, e] == o.score_mm[oi, e], (oi, e)
         assert fast["score_goodput"][oi, e] == o.score_gp[oi, e], (oi, e)
+
+
+def _random_score_inputs(p, O, S, seed, measured_frac=0.2):
+    rng = np.random.default_rng(seed)
+    N = p.n_cells
+    lo = (np.rint(rng.uniform(0.0, 3.0, (O, N)) * 64) / 64).astype(np.float32)
+    hi = (lo + np.rint(rng.uniform(0.0, 1.0, (O, N)) * 64) / 64).astype(np.float32)
+    tl = rng.uniform(2.0, 50.0, (O, N)).astype(np.float32)
+    th = (tl * rng.uniform(1.0, 1.6, (O, N))).astype(np.float32)
+    meas = (rng.random((O, N)) < measured_frac).astype(np.uint8)
+    hi = np.where(meas == 1, lo, hi).astype(np.float32)
+    th = np.where(meas == 1, tl, th).astype(np.float32)
+    cand = np.arange(N, dtype=np.int32)
+    u = rng.uniform(0, 1, (O, N, S)).astype(np.float32)
+    cs = (lo[:, :, None] + (hi - lo)[:, :, None] * u).astype(np.float32)
+    ts = (tl[:, :, None] + (th - tl)[:, :, None] * rng.uniform(0, 1, (O, N, S))).astype(np.float32)
+    return Intervals(lo, hi, tl, th, meas), cand, cs, ts
+
+
+@pytest.mark.parametrize("kernel", [0, 1])
+def test_stagewise_score_random_problems(env, kernel):
+    """Random problems without floors (TP sets with odd degrees, a single
+    class, budgets that are not powers of two, tails on both sides of the
+    SLO, some revealed cells, S not a multiple of 64): both scorers against
+    the oracle bit for bit."""
+    rng = np.random.default_rng(41)
+    for inst in range(16):
+        tp = [[1, 2, 4, 8], [2, 4, 8], [1], [1, 3, 5], [2, 4]][inst % 5]
+        K = int(rng.integers(1, 6))
+        G = int(rng.integers(max(tp[0], 2), 90))
+        p = random_problem(seed=5100 + inst, K=K, tp=tp, G=G, n_levels=int(rng.integers(1, 6)))
+        O, S = int(rng.integers(1, 4)), int(rng.integers(1, 130))
+        iv, cand, cs, ts = _random_score_inputs(p, O, S, seed=inst)
+        note(f"stage-wise random inst {inst} K={K} G={G} tp={tp} O={O} S={S} kernel={kernel}")
+        w = SimpleNamespace(problem=p, intervals=iv, cand=cand)
+        g = _score_lex(env, w, cs, ts, kernel)
+        o = oracle.score_lex(p, iv, cand, cs, ts, n_threads=16)
+        _assert_score_lex_equal(g, o, f"inst {inst}")
+
+
+def test_stagewise_score_all_measured_and_no_candidate(env):
+    """Every candidate revealed: scores 0, best -1, the stages from the
+    certificate alone, on both scorers."""
+    w = make_workload("tiny-2class-G16")
+    p = w.problem
+    iv = Intervals(w.intervals.cap_lo, w.intervals.cap_lo.copy(), w.intervals.tail_hi, w.intervals.tail_hi.copy(),
+                   np.ones_like(w.intervals.measured))
+    cs, ts = np.ascontiguousarray(w.cap_s[:, :, :8]), np.ascontiguousarray(w.tail_s[:, :, :8])
+    note("stage-wise score, every candidate revealed")
+    ww = SimpleNamespace(problem=p, intervals=iv, cand=w.cand)
+    for kernel in (0, 1):
+        g = _score_lex(env, ww, cs, ts, kernel)
+        o = oracle.score_lex(p, iv, w.cand, cs, ts)
+        _assert_score_lex_equal(g, o, f"all revealed, kernel {kernel}")
+        assert np.all(g["score_maxmin"] == 0.0) and np.all(g["best"] == -1)
