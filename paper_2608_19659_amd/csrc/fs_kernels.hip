@@ -2499,49 +2499,90 @@ __device__ __forceinline__ int certificate_state(const DevProblem &P, const int8
   return (ok && gap_ok) ? 1 : 0;
 }
 
+// Result of one realisation's solve in a certificate: tau, floors, goodput
+// (binary32 and, under the whole objective, level (3)'s binary64 total) and
+// the allocation.
+struct CertRec {
+  int32_t tau, floors_met;
+  float goodput;
+  int32_t pad;
+  double goodput64;
+  int32_t tp_index[kMaxClasses], replicas[kMaxClasses];
+};
+
+__device__ __forceinline__ void write_cert_rec(CertRec *me, int K, int tau, int fm, float gp, double g64,
+                                               const WaveAlloc &wa) {
+  const int lane = threadIdx.x & (kWave - 1);
+  if (lane == 0) {
+    me->tau = tau;
+    me->floors_met = fm;
+    me->goodput = gp;
+    me->goodput64 = g64;
+  }
+  for (int k = lane; k < K; k += kWave) {
+    me->tp_index[k] = wa.tp_index[k];
+    me->replicas[k] = wa.replicas[k];
+  }
+}
+
+// Certificate (Section 4.2): block (R, o) solves realisation R of order o
+// (0: conservative, 1: optimistic) and keeps its result in a record;
+// k_certify_state then forms each order's gap and state from the two.
 __global__ __launch_bounds__(64) void k_certify(DevProblem P, const int8_t *__restrict__ bmap,
                                                 const float *__restrict__ cap_lo,
                                                 const float *__restrict__ cap_hi,
                                                 const float *__restrict__ tail_lo,
-                                                const float *__restrict__ tail_hi,
-                                                const uint8_t *__restrict__ measured, float eps,
-                                                int32_t *__restrict__ state, AllocOut cons,
-                                                AllocOut opt, double *__restrict__ gap_out, int stage) {
+                                                const float *__restrict__ tail_hi, AllocOut cons, AllocOut opt,
+                                                CertRec *__restrict__ rec, int stage) {
   extern __shared__ int lds[];
-  const int o = blockIdx.x, lane = threadIdx.x;
+  const int R = blockIdx.x, o = blockIdx.y;
   const size_t off = (size_t)o * P.N;
-  int *tm_index = lds + 3 * (P.G + 1);
-  int *tm_rep = tm_index + kMaxClasses;
-  int *tp_index = tm_rep + kMaxClasses;
-  int *tp_rep = tp_index + kMaxClasses;
-  WaveAlloc am{tm_index, tm_rep}, ap{tp_index, tp_rep};
-  const StageArea A = stage_area(P, tp_rep + kMaxClasses);
+  int *t_index = lds + 3 * (P.G + 1);
+  int *t_rep = t_index + kMaxClasses;
+  WaveAlloc wa{t_index, t_rep};
+  const StageArea A = stage_area(P, t_rep + kMaxClasses);
   const int8_t *bm = bmap;
-  int fm_m, fm_p;
-  float gp_m, gp_p;
-  Realisation rm{cap_lo + off, tail_hi + off, -1, 0.0f, 0.0f};
+  Realisation rz = R == 0 ? Realisation{cap_lo + off, tail_hi + off, -1, 0.0f, 0.0f}
+                          : Realisation{cap_hi + off, tail_lo + off, -1, 0.0f, 0.0f};
   if (stage) {
     stage_copy_bmap(P, bmap, A.bmap);
-    stage_copy_cells(P, rm.cap, rm.tail, A.cap, A.tail);
+    stage_copy_cells(P, rz.cap, rz.tail, A.cap, A.tail);
     bm = A.bmap;
-    rm = Realisation{A.cap, A.tail, -1, 0.0f, 0.0f};
+    rz = Realisation{A.cap, A.tail, -1, 0.0f, 0.0f};
     __syncthreads();
   }
-  const int tau_m = wave_solve(P, bm, rm, lds, &fm_m, &am, &gp_m);
-  Realisation rp{cap_hi + off, tail_lo + off, -1, 0.0f, 0.0f};
-  if (stage) {
-    stage_copy_cells(P, rp.cap, rp.tail, A.cap, A.tail);
-    rp = Realisation{A.cap, A.tail, -1, 0.0f, 0.0f};
-    __syncthreads();
+  int fm;
+  float gp;
+  const int tau = wave_solve(P, bm, rz, lds, &fm, &wa, &gp);
+  write_alloc(R == 0 ? cons : opt, o, P.K, tau, fm, gp, wa);
+  write_cert_rec(rec + (size_t)o * 2 + R, P.K, tau, fm, gp, 0.0, wa);
+}
+
+// Gap and state of each order from its two records: the max-min gap
+// tau+ - tau-, and with lex the goodput gap |gp+ - gp-| / max(gp+, gp-) (0
+// when both are 0) of level (3)'s totals; within eps means every stage is.
+__global__ __launch_bounds__(64) void k_certify_state(DevProblem P, const int8_t *__restrict__ bmap,
+                                                      const float *__restrict__ tail_hi,
+                                                      const uint8_t *__restrict__ measured, float eps,
+                                                      const CertRec *__restrict__ rec, int lex,
+                                                      int32_t *__restrict__ state, double *__restrict__ gap_mm_out,
+                                                      double *__restrict__ gap_gp_out) {
+  const int o = blockIdx.x;
+  if (threadIdx.x != 0) return;
+  const size_t off = (size_t)o * P.N;
+  const CertRec *m = rec + (size_t)o * 2, *p = m + 1;
+  const double gap_mm = (double)__int_as_float(p->tau) - (double)__int_as_float(m->tau);
+  bool ok = gap_mm <= (double)eps;
+  if (gap_mm_out) gap_mm_out[o] = gap_mm;
+  if (lex) {
+    const double g64_m = m->goodput64, g64_p = p->goodput64;
+    const double top = g64_p > g64_m ? g64_p : g64_m;
+    const double gap_gp = top > 0.0 ? fabs(g64_p - g64_m) / top : 0.0;
+    if (gap_gp_out) gap_gp_out[o] = gap_gp;
+    ok = ok && gap_gp <= (double)eps;
   }
-  const int tau_p = wave_solve(P, bm, rp, lds, &fm_p, &ap, &gp_p);
-  write_alloc(cons, o, P.K, tau_m, fm_m, gp_m, am);
-  write_alloc(opt, o, P.K, tau_p, fm_p, gp_p, ap);
-  if (lane != 0) return;
-  const double gap = (double)__int_as_float(tau_p) - (double)__int_as_float(tau_m);
-  if (gap_out) gap_out[o] = gap;
-  state[o] = certificate_state(P, bmap, measured, tail_hi, off, fm_m, fm_p, tm_index, tm_rep,
-                               gap <= (double)eps);
+  state[o] = certificate_state(P, bmap, measured, tail_hi, off, m->floors_met, p->floors_met, m->tp_index,
+                               m->replicas, ok);
 }
 
 // ---------------------------------------------------------------------------
@@ -2754,16 +2795,8 @@ __global__ __launch_bounds__(64) void k_solve_dense_lex(DevProblem P, const int8
 // objective; max-min gap tau+ - tau-, goodput gap |gp+ - gp-| / max(gp+,
 // gp-) (0 when both are 0); within eps means both stages are.  Block (R, o)
 // solves realisation R of order o (0: conservative, 1: optimistic) and
-// keeps its result in a record; k_certify_lex_state then takes each
+// keeps its result in a record; k_certify_state then takes each
 // order's gaps and state from the two records.
-struct CertRec {
-  int32_t tau, floors_met;
-  float goodput;
-  int32_t pad;
-  double goodput64;
-  int32_t tp_index[kMaxClasses], replicas[kMaxClasses];
-};
-
 __global__ __launch_bounds__(64) void k_certify_lex(DevProblem P, const int8_t *__restrict__ bmap,
                                                     const float *__restrict__ cap_lo,
                                                     const float *__restrict__ cap_hi,
@@ -2771,7 +2804,7 @@ __global__ __launch_bounds__(64) void k_certify_lex(DevProblem P, const int8_t *
                                                     const float *__restrict__ tail_hi, AllocOut cons,
                                                     AllocOut opt, CertRec *__restrict__ rec, int stage) {
   extern __shared__ int lds[];
-  const int R = blockIdx.x, o = blockIdx.y, lane = threadIdx.x;
+  const int R = blockIdx.x, o = blockIdx.y;
   const size_t off = (size_t)o * P.N;
   int *t_index = lds;
   int *t_rep = t_index + kMaxClasses;
@@ -2795,39 +2828,9 @@ __global__ __launch_bounds__(64) void k_certify_lex(DevProblem P, const int8_t *
   const int tau = wave_solve(P, bm, rz, work, &fm, nullptr, nullptr);
   wave_lex_stage(P, bm, rz, tau, fm, X, wa, &gp, &g64);
   write_alloc(R == 0 ? cons : opt, o, P.K, tau, fm, gp, wa);
-  CertRec *me = rec + (size_t)o * 2 + R;
-  if (lane == 0) {
-    me->tau = tau;
-    me->floors_met = fm;
-    me->goodput = gp;
-    me->goodput64 = g64;
-  }
-  for (int k = lane; k < P.K; k += kWave) {
-    me->tp_index[k] = t_index[k];
-    me->replicas[k] = t_rep[k];
-  }
+  write_cert_rec(rec + (size_t)o * 2 + R, P.K, tau, fm, gp, g64, wa);
 }
 
-__global__ __launch_bounds__(64) void k_certify_lex_state(DevProblem P, const int8_t *__restrict__ bmap,
-                                                          const float *__restrict__ tail_hi,
-                                                          const uint8_t *__restrict__ measured, float eps,
-                                                          const CertRec *__restrict__ rec,
-                                                          int32_t *__restrict__ state,
-                                                          double *__restrict__ gap_mm_out,
-                                                          double *__restrict__ gap_gp_out) {
-  const int o = blockIdx.x;
-  if (threadIdx.x != 0) return;
-  const size_t off = (size_t)o * P.N;
-  const CertRec *m = rec + (size_t)o * 2, *p = m + 1;
-  const double gap_mm = (double)__int_as_float(p->tau) - (double)__int_as_float(m->tau);
-  const double g64_m = m->goodput64, g64_p = p->goodput64;
-  const double top = g64_p > g64_m ? g64_p : g64_m;
-  const double gap_gp = top > 0.0 ? fabs(g64_p - g64_m) / top : 0.0;
-  if (gap_mm_out) gap_mm_out[o] = gap_mm;
-  if (gap_gp_out) gap_gp_out[o] = gap_gp;
-  state[o] = certificate_state(P, bmap, measured, tail_hi, off, m->floors_met, p->floors_met, m->tp_index,
-                               m->replicas, gap_mm <= (double)eps && gap_gp <= (double)eps);
-}
 
 // ---------------------------------------------------------------------------
 // The acquisition score with the stage-wise gap under the whole objective:
@@ -4060,7 +4063,7 @@ hipError_t launch_certify_lex(const DevProblem &P, const float *cap_lo, const fl
                                                               rec, stage);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  k_certify_lex_state<<<O, 64, 0, s>>>(P, bmap, tail_hi, measured, eps, rec, state, gap_mm, gap_gp);
+  k_certify_state<<<O, 64, 0, s>>>(P, bmap, tail_hi, measured, eps, rec, 1, state, gap_mm, gap_gp);
   return hipGetLastError();
 }
 
@@ -4069,10 +4072,15 @@ hipError_t launch_certify(const DevProblem &P, const float *cap_lo, const float 
                           int32_t O, float eps, int32_t *state, AllocOut cons, AllocOut opt,
                           double *gap, uint8_t *ws, const WsLayout &L, hipStream_t s) {
   if (O == 0) return hipSuccess;
-  const size_t base = lds_bytes_solver(P, 2), staged = base + stage_bytes(P);
+  const size_t base = lds_bytes_solver(P, 1), staged = base + stage_bytes(P);
   const int stage = stage_fits(staged) ? 1 : 0;
-  k_certify<<<O, 64, stage ? staged : base, s>>>(P, (const int8_t *)(ws + L.bmap), cap_lo, cap_hi, tail_lo,
-                                                 tail_hi, measured, eps, state, cons, opt, gap, stage);
+  CertRec *rec = (CertRec *)(ws + L.crec);
+  const int8_t *bmap = (const int8_t *)(ws + L.bmap);
+  k_certify<<<dim3(2, O), 64, stage ? staged : base, s>>>(P, bmap, cap_lo, cap_hi, tail_lo, tail_hi, cons, opt, rec,
+                                                          stage);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  k_certify_state<<<O, 64, 0, s>>>(P, bmap, tail_hi, measured, eps, rec, 0, state, gap, nullptr);
   return hipGetLastError();
 }
 
