@@ -280,9 +280,8 @@ def test_score_8class_g256_full_size_seeded_tiles(env, orc):
 
 def test_score_16class_g1024_full_size_seeded_tiles(env, orc):
     """The 16-class G=1024 workload at full size (4 orders x 960 candidates
-    x 256 samples) through the general set-up with its tables in global
-    memory: 8 seeded tiles (2,048 scenarios) re-scored by the oracle, bit for
-    bit."""
+    x 256 samples) through the general set-up (1024 threads, tables in LDS):
+    8 seeded tiles (2,048 scenarios) re-scored by the oracle, bit for bit."""
     w = make_workload("16class-G1024")
     note("score 16class-G1024 full size")
     score, gap, best, dump = gpu_score(env, w.problem, w.intervals, w.cand, w.cap_s, w.tail_s, kernel=0)
@@ -293,6 +292,39 @@ def test_score_16class_g1024_full_size_seeded_tiles(env, orc):
     assert_scores_equal((score, gap, best, dump), o_ref, tile_mask=mask)
     np.testing.assert_array_equal(gap, o_ref.gap_now)
     _check_invariants(w, score, gap, best, dump)
+
+
+def test_score_general_setup_tables_in_global_memory(env, orc):
+    """16 classes at G = 2048: the general set-up's tables (B and the two
+    tree buffers, 229 KiB per block) exceed a workgroup's LDS and live in the
+    workspace; candidates are the cells both corner allocations use (one of
+    them decision-critical), 8 samples each; every tau, score, gap and the
+    best candidate against the oracle bit for bit."""
+    p = random_problem(seed=8100, K=16, tp=[1, 2, 4, 8, 16], G=2048, n_levels=5)
+    rng = np.random.default_rng(8100)
+    N, O, S = p.n_cells, 1, 8
+    lo = rng.uniform(0.004, 0.03, (O, N)).astype(np.float32)
+    hi = (lo * rng.uniform(1.05, 1.5, (O, N))).astype(np.float32)
+    tl = rng.uniform(5.0, 40.0, (O, N)).astype(np.float32)
+    th = (tl * rng.uniform(1.0, 1.3, (O, N))).astype(np.float32)
+    iv = Intervals(lo, hi, tl, th, np.zeros((O, N), np.uint8))
+    per_class = len(p.tp) * len(p.levels)
+    cells = set()
+    for alloc in (orc.solve(p, lo[0], th[0]), orc.solve(p, hi[0], tl[0])):
+        for k, (t, r) in enumerate(zip(alloc.tp_index, alloc.replicas)):
+            if t >= 0 and r > 0:
+                u = np.float32(p.demand[k]) / np.float32(r)
+                b = next(j for j in range(len(p.levels)) if p.levels[j] >= u)
+                cells.add(k * per_class + t * len(p.levels) + b)
+    cand = np.array(sorted(cells), np.int32)
+    E = len(cand)
+    cs = (lo[:, cand, None] + (hi - lo)[:, cand, None] * rng.uniform(0, 1, (O, E, S))).astype(np.float32)
+    ts = (tl[:, cand, None] + (th - tl)[:, cand, None] * rng.uniform(0, 1, (O, E, S))).astype(np.float32)
+    note(f"score K=16 G=2048, general set-up with tables in global memory, {E} candidates")
+    g = gpu_score(env, p, iv, cand, cs, ts, kernel=3)
+    o = orc.score(p, iv, cand, cs, ts, n_threads=16)
+    assert_scores_equal(g, o)
+    assert (o.score > 0).any()
 
 
 def _check_invariants(w, score, gap, best, dump):
