@@ -72,6 +72,7 @@ struct WsLayout {
   size_t mopt;       // int32 [O][2][K*P] M = H[G - t*r] of every option (class, TP, r)
   size_t thr;        // float [O][2][K*P] capacity threshold of every option
   size_t list;       // int4 [O * E] live tiles of every order, longest replica range first
+  size_t btab;       // int32 [O][2][K][G] B tables of the general set-up
   size_t live;       // int32 [1] number of listed tiles
   size_t crec;       // [O][2] per-realisation results of the certificate under the whole objective
   size_t flag;     // int32 [4]        validation / error flags

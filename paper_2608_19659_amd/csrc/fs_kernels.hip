@@ -1074,6 +1074,76 @@ __device__ void prep_list(const DevProblem &P, int O, const uint8_t *__restrict_
   for (int z = *n_live + tid; z < O * E; z += nth) list[z] = make_int4(-1, 0, 0, 0);
 }
 
+// B_k of the general set-up, once per (realisation R, order o, class k):
+// every option (t, r) with t r < G max-merged into its exact GPU count, then
+// the prefix maximum (best ratio with at most g GPUs, g in [0, G)).  Every
+// class block of k_prep reads the tables of the other classes from here
+// instead of building them itself.
+constexpr int kBtabThreads = 256;
+
+__global__ __launch_bounds__(kBtabThreads) void k_prep_btab(DevProblem P, const float *__restrict__ cap_lo,
+                                                           const float *__restrict__ cap_hi,
+                                                           const float *__restrict__ tail_lo,
+                                                           const float *__restrict__ tail_hi,
+                                                           int32_t *__restrict__ btab) {
+  extern __shared__ int bt_lds[];
+  const int R = blockIdx.x, o = blockIdx.y, k = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int G = P.G, B = P.B, NT = P.NT, per_class = NT * B, PP = P.optoff[NT];
+  int *T = bt_lds;                                         // [G]
+  float *cc = reinterpret_cast<float *>(T + G), *ct = cc + per_class;  // class k's cells
+  __shared__ float lv[kMaxLevels];
+  const size_t off = (size_t)o * P.N + (size_t)k * per_class;
+  const float *gcap = (R == 0 ? cap_lo : cap_hi) + off;
+  const float *gtail = (R == 0 ? tail_hi : tail_lo) + off;
+  for (int g = tid; g < G; g += kBtabThreads) T[g] = 0;  // no option: ratio 0
+  for (int c = tid; c < per_class; c += kBtabThreads) {
+    cc[c] = gcap[c];
+    ct[c] = gtail[c];
+  }
+  if (tid < B) lv[tid] = P.levels[tid];
+  __syncthreads();
+  const float dm = P.demand[k], slo = P.slo[k];
+  const double rcp = P.rcp_demand[k];
+  for (int q = tid; q < PP; q += kBtabThreads) {
+    int ti = 0;
+    while (ti + 1 < NT && q >= P.optoff[ti + 1]) ++ti;
+    const int r = q - P.optoff[ti] + 1, t = P.tp[ti];
+    if (t * r >= G) continue;
+    const float u = dm / (float)r;
+    int lo = 0, hi = B;  // first level >= u; B = none
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (u <= lv[mid]) hi = mid;
+      else lo = mid + 1;
+    }
+    if (lo >= B) continue;
+    const int c = ti * B + lo;
+    atomicMax(&T[t * r], ratio_bits(cc[c], ct[c], r, slo, rcp));
+  }
+  __syncthreads();
+  if (tid < kWave) {
+    const int L = (G + kWave - 1) / kWave;  // lane l owns [l * L, l * L + L)
+    int run = 0;
+    for (int j = 0; j < L; ++j) {
+      const int g = lane * L + j;
+      if (g < G) {
+        run = max(run, T[g]);
+        T[g] = run;
+      }
+    }
+    int carry = __shfl_up(wave_scan_max(run, lane), 1, kWave);
+    if (lane == 0) carry = 0;
+    for (int j = 0; j < L; ++j) {
+      const int g = lane * L + j;
+      if (g < G) T[g] = max(T[g], carry);
+    }
+  }
+  __syncthreads();
+  int32_t *dst = btab + (((size_t)o * 2 + R) * P.K + k) * G;
+  for (int g = tid; g < G; g += kBtabThreads) dst[g] = T[g];
+}
+
 // Set-up of the exclusion scorer, one block per (realisation R, order o,
 // class i), plus blocks with i = K of which (R = 0, o = 0) builds the work
 // list of every order and the others return at once; R = 0 is the
@@ -1091,9 +1161,9 @@ __device__ void prep_list(const DevProblem &P, int O, const uint8_t *__restrict_
 // Dynamic LDS: all cells (cap, tail) of this realisation; the class's cell
 // maxima and replica ranges; the load-level table (K x G int8); and, when
 // kLds, the tables (B and two tree buffers, 3 x K x G ints), else in gtab.
-__device__ void prep_list_staged(const DevProblem &P, const int8_t *lvl_tab, int lvl_stride, int O,
-                                 const uint8_t *__restrict__ measured, const int32_t *__restrict__ cand, int E,
-                                 int dump, int PPc, TileInfo *__restrict__ tiles, int4 *__restrict__ list,
+__device__ void prep_list_staged(const DevProblem &P, int O, const uint8_t *__restrict__ measured,
+                                 const int32_t *__restrict__ cand, int E, int dump, int PPc,
+                                 TileInfo *__restrict__ tiles, int4 *__restrict__ list,
                                  int32_t *__restrict__ n_listed, int *lds);
 
 template <bool kLds, int kThreads>
@@ -1107,13 +1177,14 @@ __global__ __launch_bounds__(kThreads) void k_prep(DevProblem P, const float *__
                                              int32_t *__restrict__ base, int32_t *__restrict__ mopt,
                                              float *__restrict__ thr, int32_t n_thr,
                                              int4 *__restrict__ list, int32_t *__restrict__ n_listed,
-                                             int32_t thr_mode, int32_t staged_list) {
+                                             int32_t thr_mode, int32_t staged_list,
+                                             const int32_t *__restrict__ btab) {
   extern __shared__ int lds[];
   __shared__ PrepConsts C;
   __shared__ int bucket_count[32], bucket_start[32], n_live;
   const int R = blockIdx.x, o = blockIdx.y, ci = blockIdx.z;
   const int tid = threadIdx.x, nth = blockDim.x;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & (kWave - 1), nw = nth >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & (kWave - 1);
   const int G = P.G, K = P.K, N = P.N, NT = P.NT, B = P.B, KG = K * G;
   const int per_class = NT * B;
   const int PPc = n_thr / K;
@@ -1129,22 +1200,7 @@ __global__ __launch_bounds__(kThreads) void k_prep(DevProblem P, const float *__
   if (ci == K) {  // one block builds the work list of every order
     if (R != 0 || o != 0) return;
     if (staged_list) {
-      // the load level of every (class, r), then the list from staged inputs
-      int8_t *lvl_tab = reinterpret_cast<int8_t *>(lds);
-      for (int idx = tid; idx < KG; idx += nth) {
-        const int k = idx / G, r = idx - k * G + 1;
-        const float per_replica = P.demand[k] / (float)r;
-        int lo = 0, hi = B;  // first level >= per_replica; B = none
-        while (lo < hi) {
-          const int mid = (lo + hi) >> 1;
-          if (per_replica <= P.levels[mid]) hi = mid;
-          else lo = mid + 1;
-        }
-        lvl_tab[idx] = (int8_t)(lo < B ? lo : -1);
-      }
-      __syncthreads();
-      prep_list_staged(P, lvl_tab, G, (int)gridDim.y, measured, cand, E, dump, PPc, tiles, list, n_listed,
-                       lds + (KG + 15) / 16 * 4);
+      prep_list_staged(P, (int)gridDim.y, measured, cand, E, dump, PPc, tiles, list, n_listed, lds);
       return;
     }
     if (tid < 32) bucket_count[tid] = 0;
@@ -1187,9 +1243,10 @@ __global__ __launch_bounds__(kThreads) void k_prep(DevProblem P, const float *__
   const bool my_valid = my_cell >= 0 && my_cell < N;
   const int my_meas = (R == 0 && my_valid && my_cell / per_class == ci) ? measured[off + my_cell] : 0;
 
-  // --- load level of every (class, r): the smallest level holding demand / r
-  for (int idx = tid; idx < KG; idx += nth) {
-    const int k = idx / G, r = idx - k * G + 1;
+  // --- load level of class ci's replica counts: the smallest level holding
+  // demand / r (the other classes enter through their B tables only)
+  for (int idx = ci * G + tid; idx < (ci + 1) * G; idx += nth) {
+    const int k = ci, r = idx - k * G + 1;
     const float per_replica = C.demand[k] / (float)r;
     int lo = 0, hi = B;  // first level >= per_replica; B = none
     while (lo < hi) {
@@ -1201,45 +1258,22 @@ __global__ __launch_bounds__(kThreads) void k_prep(DevProblem P, const float *__
   }
   __syncthreads();
 
-  // --- B tables of the other classes, one wavefront per class: every option
-  // max-merged into its exact GPU count, then the prefix maximum
-  const int nbw = min(nw, K);
-  if (wave < nbw) {
-    for (int k = wave; k < K; k += nbw) {
-      if (k == ci) continue;
-      int *T = Bt + k * G;
-      for (int g = lane; g < G; g += kWave) T[g] = 0;  // no option: ratio 0
-      wave_lds_fence();
-      const float slo = P.slo[k];
-      const double rcp = P.rcp_demand[k];
-      for (int ti = 0; ti < NT; ++ti) {
-        const int t = P.tp[ti];
-        for (int r = lane + 1; t * r < G; r += kWave) {
-          const int b = lvl[k * G + r - 1];
-          if (b < 0) continue;
-          const int cell = cell_of(P, k, ti, b);
-          atomicMax(&T[t * r], ratio_bits(ccap[cell], ctail[cell], r, slo, rcp));
-        }
-      }
-      wave_lds_fence();
-      const int L = (G + kWave - 1) / kWave;  // lane l owns [l * L, l * L + L)
-      int run = 0;
-      for (int j = 0; j < L; ++j) {
-        const int g = lane * L + j;
-        if (g < G) {
-          run = max(run, T[g]);
-          T[g] = run;
-        }
-      }
-      int carry = __shfl_up(wave_scan_max(run, lane), 1, kWave);
-      if (lane == 0) carry = 0;
-      for (int j = 0; j < L; ++j) {
-        const int g = lane * L + j;
-        if (g < G) T[g] = max(T[g], carry);
-      }
+  // --- B tables of the other classes, built once per (realisation, order)
+  // by k_prep_btab: copied into LDS (16-byte moves when they align), or read
+  // in place when the tables live in global memory
+  const int32_t *gB = btab + ((size_t)o * 2 + R) * (size_t)KG;
+  const int *Bsrc = gB;
+  if (kLds) {
+    if ((KG & 3) == 0 && (reinterpret_cast<uintptr_t>(Bt) & 15) == 0) {
+      const int4 *src4 = reinterpret_cast<const int4 *>(gB);
+      int4 *dst4 = reinterpret_cast<int4 *>(Bt);
+      for (int x = tid; x < KG / 4; x += nth) dst4[x] = src4[x];
+    } else {
+      for (int x = tid; x < KG; x += nth) Bt[x] = gB[x];
     }
+    Bsrc = Bt;
+    __syncthreads();
   }
-  __syncthreads();
 
   // --- H_ci: tree over the tables k != ci.  Level 0 reads B (logical table
   // j is class j, or j + 1 from ci on); later levels alternate Xa / Xb.
@@ -1250,7 +1284,7 @@ __global__ __launch_bounds__(kThreads) void k_prep(DevProblem P, const float *__
     H = Xa;
     __syncthreads();
   } else if (n0 == 1) {
-    H = Bt + (ci == 0 ? 1 : 0) * G;
+    H = Bsrc + (ci == 0 ? 1 : 0) * G;
   } else {
     int n = n0;
     int *src = nullptr, *dst = Xa;
@@ -1259,10 +1293,10 @@ __global__ __launch_bounds__(kThreads) void k_prep(DevProblem P, const float *__
       for (int item = tid; item < (pairs + odd) * G; item += nth) {
         const int p = item / G, g = item - p * G;
         const int ja = 2 * p, jb = 2 * p + 1;
-        const int *X = src ? src + ja * G : Bt + (ja < ci ? ja : ja + 1) * G;
+        const int *X = src ? src + ja * G : Bsrc + (ja < ci ? ja : ja + 1) * G;
         int v;
         if (p < pairs) {
-          const int *Y = src ? src + jb * G : Bt + (jb < ci ? jb : jb + 1) * G;
+          const int *Y = src ? src + jb * G : Bsrc + (jb < ci ? jb : jb + 1) * G;
           v = conv_mono(X, Y, g, top);
         } else {
           v = X[g];  // the odd table passes through
@@ -1380,8 +1414,8 @@ static int prep_order_waves(const DevProblem &P, int64_t O, int64_t E) {
 // candidates' cells and every order's revealed flags are read into LDS in
 // one round trip, during which the block finds, for every (class, level),
 // the first and last replica count r in [1, G] whose per-replica load lands
-// in that level (the level is nonincreasing in r, so these form a range; a
-// cell of TP t keeps the part with t r <= G).  The list holds every tile the
+// in that level, by two bisections (the level is nonincreasing in r, so
+// these form a range; a cell of TP t keeps the part with t r <= G).  The list holds every tile the
 // scorer visits -- an unrevealed (order, candidate) pair whose cell some
 // replica count reaches, or every valid pair when dumping -- over all
 // orders, longest range first (bucketed by bit length), then end markers up
@@ -1393,9 +1427,9 @@ static int prep_order_waves(const DevProblem &P, int64_t O, int64_t E) {
 // LDS: bucket counters and starts (2 x 32 + 4), the level ranges (2 x K x B),
 // per candidate its cell and range code (2 x E), the revealed flags (O x N
 // bytes).
-__device__ void prep_list_staged(const DevProblem &P, const int8_t *lvl_tab, int lvl_stride, int O,
-                                 const uint8_t *__restrict__ measured, const int32_t *__restrict__ cand, int E,
-                                 int dump, int PPc, TileInfo *__restrict__ tiles, int4 *__restrict__ list,
+__device__ void prep_list_staged(const DevProblem &P, int O, const uint8_t *__restrict__ measured,
+                                 const int32_t *__restrict__ cand, int E, int dump, int PPc,
+                                 TileInfo *__restrict__ tiles, int4 *__restrict__ list,
                                  int32_t *__restrict__ n_listed, int *lds) {
   const int tid = threadIdx.x, nth = blockDim.x, lane = tid & (kWave - 1);
   const int N = P.N, G = P.G, K = P.K, B = P.B, per_class = P.NT * P.B;
@@ -1407,21 +1441,16 @@ __device__ void prep_list_staged(const DevProblem &P, const int8_t *lvl_tab, int
   if (tid < P.NT) c_tp[tid] = P.tp[tid];
   if (tid <= P.NT) c_optoff[tid] = P.optoff[tid];
   if (tid < 32) bucket_count[tid] = 0;
-  for (int x = tid; x < K * B; x += nth) {
-    lv_first[x] = INT_MAX;
-    lv_last[x] = 0;
-  }
   stage_u8(meas, measured, O * N, tid, nth);
   for (int e = tid; e < E; e += nth) c_cell[e] = cand[e];
-  __syncthreads();
-  // one thread per (class, replica count)
-  for (int x = tid; x < K * G; x += nth) {
-    const int k = x / G, r = x - k * G + 1;
-    const int b = lvl_tab[k * lvl_stride + r - 1];
-    if (b >= 0) {
-      atomicMin(&lv_first[k * B + b], r);
-      atomicMax(&lv_last[k * B + b], r);
-    }
+  // every (class, level)'s replica range in [1, G]: the level falls as r
+  // grows, so it is [first r at the level or below, first r at the level
+  // below) -- two bisections per pair instead of a level per (class, r)
+  for (int x = tid; x < K * B; x += nth) {
+    const int k = x / B, b = x - k * B;
+    const float dm = P.demand[k];
+    lv_first[x] = first_r_at_most(dm, P.levels[b], G);
+    lv_last[x] = b == 0 ? G : first_r_at_most(dm, P.levels[b - 1], G) - 1;
   }
   __syncthreads();
   // range code of a candidate: -1 invalid cell, -2 never visited (no replica
@@ -1558,7 +1587,7 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
   const int G = P.G, K = P.K, N = P.N, NT = P.NT, B = P.B, per_class = NT * B;
   const int PPc = n_thr / K;
   if ((int)blockIdx.x == 2 * O) {
-    prep_list_staged(P, LV.lvl, kPrepOrderMaxG, O, measured, cand, E, dump, PPc, tiles, list, n_listed, lds);
+    prep_list_staged(P, O, measured, cand, E, dump, PPc, tiles, list, n_listed, lds);
     return;
   }
   const int o = blockIdx.x >> 1, R = blockIdx.x & 1;
@@ -3774,11 +3803,10 @@ static size_t prep_lds_tables(const DevProblem &P) {
   return sizeof(int) * (size_t)(P.K + prep_tree_a(P.K) + prep_tree_b(P.K)) * P.G;
 }
 
-// LDS of the general set-up's work-list block from staged inputs: the load
-// levels (K x G bytes), counters, level ranges, candidates, revealed flags.
+// LDS of the general set-up's work-list block from staged inputs: counters,
+// level ranges, candidates, revealed flags.
 static size_t prep_list_lds(const DevProblem &P, int64_t O, int64_t E) {
-  const size_t KG = (size_t)P.K * P.G;
-  return ((KG + 15) & ~(size_t)15) + 4 * (68 + 2 * (size_t)P.K * P.B + 2 * (size_t)E) + (size_t)O * P.N;
+  return 4 * (68 + 2 * (size_t)P.K * P.B + 2 * (size_t)E) + (size_t)O * P.N;
 }
 
 // Dynamic LDS of one general set-up block: a workgroup may hold 160 KiB on
@@ -3827,6 +3855,8 @@ WsLayout ws_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
   L.mopt = at; at = align256(at + sizeof(int32_t) * n_opt);
   L.thr = at; at = align256(at + sizeof(float) * n_opt);
   L.list = at; at = align256(at + sizeof(int4) * (size_t)O * (size_t)E);
+  // B tables of the general set-up, one per (order, realisation, class)
+  L.btab = at; at = align256(at + (excl ? sizeof(int32_t) * (size_t)O * 2 * P.K * P.G : 0));
   L.live = at; at = align256(at + sizeof(int32_t));
   L.crec = at; at = align256(at + sizeof(CertRec) * 2 * (size_t)(O > 0 ? O : 1));
   L.total = at;
@@ -3894,6 +3924,18 @@ static hipError_t launch_excl_setup(const DevProblem &P, const ScoreArgs &a, hip
     size_t lds = in_lds ? big : small;
     if (staged && lst > lds) lds = lst;
     int32_t *gtab = in_lds ? nullptr : (int32_t *)(a.ws + a.L.tabB);
+    int32_t *btab = (int32_t *)(a.ws + a.L.btab);
+    {
+      const size_t blds = sizeof(int) * (size_t)P.G + 2 * sizeof(float) * (size_t)P.NT * P.B;
+      if (blds > 64 * 1024) {
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_prep_btab),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)blds);
+        if (e != hipSuccess) return e;
+      }
+      k_prep_btab<<<dim3(2, a.O, P.K), kBtabThreads, blds, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, btab);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
     const dim3 grid(2, a.O, P.K + 1);
 #define FS_PREP_GENERAL(LDS, TH)                                                                                  \
   {                                                                                                               \
@@ -3904,7 +3946,7 @@ static hipError_t launch_excl_setup(const DevProblem &P, const ScoreArgs &a, hip
     }                                                                                                             \
     k_prep<LDS, TH><<<grid, TH, lds, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, a.measured, a.cand, a.E,   \
                                           dump, gtab, tiles, base, mopt, thr, n_thr, list, live, a.thr_search,    \
-                                          staged);                                                                \
+                                          staged, btab);                                                          \
   }
     if (P.G >= kPrepWideBudget) {
       if (in_lds) FS_PREP_GENERAL(true, kPrepThreadsWide)
