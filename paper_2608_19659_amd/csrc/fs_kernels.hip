@@ -1093,6 +1093,7 @@ __global__ __launch_bounds__(kBtabThreads) void k_prep_btab(DevProblem P, const 
   int *T = bt_lds;                                         // [G]
   float *cc = reinterpret_cast<float *>(T + G), *ct = cc + per_class;  // class k's cells
   __shared__ float lv[kMaxLevels];
+  __shared__ int s_tp[kMaxTp], s_off[kMaxTp + 1];  // indexed per lane below: staged, not kernel arguments
   const size_t off = (size_t)o * P.N + (size_t)k * per_class;
   const float *gcap = (R == 0 ? cap_lo : cap_hi) + off;
   const float *gtail = (R == 0 ? tail_hi : tail_lo) + off;
@@ -1102,13 +1103,15 @@ __global__ __launch_bounds__(kBtabThreads) void k_prep_btab(DevProblem P, const 
     ct[c] = gtail[c];
   }
   if (tid < B) lv[tid] = P.levels[tid];
+  if (tid < NT) s_tp[tid] = P.tp[tid];
+  if (tid <= NT) s_off[tid] = P.optoff[tid];
   __syncthreads();
   const float dm = P.demand[k], slo = P.slo[k];
   const double rcp = P.rcp_demand[k];
   for (int q = tid; q < PP; q += kBtabThreads) {
     int ti = 0;
-    while (ti + 1 < NT && q >= P.optoff[ti + 1]) ++ti;
-    const int r = q - P.optoff[ti] + 1, t = P.tp[ti];
+    while (ti + 1 < NT && q >= s_off[ti + 1]) ++ti;
+    const int r = q - s_off[ti] + 1, t = s_tp[ti];
     if (t * r >= G) continue;
     const float u = dm / (float)r;
     int lo = 0, hi = B;  // first level >= u; B = none
@@ -1122,20 +1125,28 @@ __global__ __launch_bounds__(kBtabThreads) void k_prep_btab(DevProblem P, const 
     atomicMax(&T[t * r], ratio_bits(cc[c], ct[c], r, slo, rcp));
   }
   __syncthreads();
-  if (tid < kWave) {
-    const int L = (G + kWave - 1) / kWave;  // lane l owns [l * L, l * L + L)
+  // prefix maximum over the block: thread j owns [j L, j L + L); its running
+  // maximum, then the maximum of the threads before it (wave scans, then the
+  // wavefronts' totals)
+  {
+    __shared__ int wtot[kBtabThreads / kWave];
+    const int L = (G + kBtabThreads - 1) / kBtabThreads;
     int run = 0;
     for (int j = 0; j < L; ++j) {
-      const int g = lane * L + j;
+      const int g = tid * L + j;
       if (g < G) {
         run = max(run, T[g]);
         T[g] = run;
       }
     }
-    int carry = __shfl_up(wave_scan_max(run, lane), 1, kWave);
+    const int incl = wave_scan_max(run, lane);
+    if (lane == kWave - 1) wtot[tid >> 6] = incl;
+    __syncthreads();
+    int carry = __shfl_up(incl, 1, kWave);
     if (lane == 0) carry = 0;
+    for (int w = 0; w < (tid >> 6); ++w) carry = max(carry, wtot[w]);
     for (int j = 0; j < L; ++j) {
-      const int g = lane * L + j;
+      const int g = tid * L + j;
       if (g < G) T[g] = max(T[g], carry);
     }
   }
@@ -3022,21 +3033,33 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_breaks(DevProblem P, co
   const float *gcap = (R == 0 ? cap_lo : cap_hi) + off;
   const float *gtail = (R == 0 ? tail_hi : tail_lo) + off;
   int2 *opt = opt_out + ((size_t)o * 2 + R) * nopt;
+  // problem constants indexed per lane below: staged (kernel arguments
+  // indexed per lane are a memory load per access)
+  __shared__ int s_off[kMaxTp + 1];
+  __shared__ float s_slo[kMaxClasses], s_dm[kMaxClasses];
+  __shared__ double s_rcp[kMaxClasses];
+  if (tid <= NT) s_off[tid] = P.optoff[tid];
+  if (tid < K) {
+    s_slo[tid] = P.slo[tid];
+    s_dm[tid] = P.demand[tid];
+    s_rcp[tid] = P.rcp_demand[tid];
+  }
+  __syncthreads();
   for (int q = tid; q < n2; q += kLexPrepThreads) {
     int key = INT_MAX;  // padding and options that do not exist sort last
     if (q < nopt) {
       const int k = q / PP, p = q - k * PP;
       int ti = 0;
-      while (ti + 1 < NT && p >= P.optoff[ti + 1]) ++ti;
-      const int r = p - P.optoff[ti] + 1;
+      while (ti + 1 < NT && p >= s_off[ti + 1]) ++ti;
+      const int r = p - s_off[ti] + 1;
       const int b = bmap[k * (G + 1) + r];
       int f = -1;
       float sv = 0.0f;
       if (b >= 0) {
         const int cell = k * per_class + ti * B + b;
         const float c = gcap[cell], l = gtail[cell];
-        f = ratio_bits(c, l, r, P.slo[k], P.rcp_demand[k]);
-        sv = l <= P.slo[k] ? served_rps(c, r, P.demand[k]) : 0.0f;
+        f = ratio_bits(c, l, r, s_slo[k], s_rcp[k]);
+        sv = l <= s_slo[k] ? served_rps(c, r, s_dm[k]) : 0.0f;
         key = f;
       }
       opt[q] = make_int2(f, __float_as_int(sv));
@@ -3132,13 +3155,18 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_tables(DevProblem P, co
     oratio[q] = v.x;
     oserved[q] = __int_as_float(v.y);
   }
-  // class i's options: (cost, cell within the class; -1 when no level holds it)
+  // class i's options: (cost, cell within the class; -1 when no level holds
+  // it); TP decode from staged constants
+  __shared__ int s_tp[kMaxTp], s_off[kMaxTp + 1];
+  if (tid < NT) s_tp[tid] = P.tp[tid];
+  if (tid <= NT) s_off[tid] = P.optoff[tid];
+  __syncthreads();
   for (int p = tid; p < PP; p += kLexPrepThreads) {
     int ti = 0;
-    while (ti + 1 < NT && p >= P.optoff[ti + 1]) ++ti;
-    const int r = p - P.optoff[ti] + 1;
+    while (ti + 1 < NT && p >= s_off[ti + 1]) ++ti;
+    const int r = p - s_off[ti] + 1;
     const int b = bmap[i * (G + 1) + r];
-    icost[p] = make_int2(P.tp[ti] * r, b >= 0 ? ti * B + b : -1);
+    icost[p] = make_int2(s_tp[ti] * r, b >= 0 ? ti * B + b : -1);
   }
   __syncthreads();
   const double NEG = -__builtin_inf();
