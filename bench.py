@@ -239,17 +239,36 @@ def excl_slots_per_scenario(n_e: int) -> float:
     return 2 * (2 * steps + (1 + DIV_OPS) + 2) + 7
 
 
-def excl_work(problem, cand, live_tiles, S):
+def excl_work(problem, cand, live_tiles, S, fixed=frozenset()):
     """Algorithmic work of one exclusion-scorer launch: VALU lane-slots
     (excl_slots_per_scenario) and bytes (the two binary32 samples, 8 B) of
     every scenario whose samples can matter.  A tile whose cell no replica
-    count reaches (n_e = 0) has tau = U in every scenario: its samples
-    cannot matter, so it contributes neither slots nor bytes (its score is
-    formed in closed form)."""
+    count reaches (n_e = 0), or whose tau is U in both realisations whatever
+    its samples (`fixed`, see sample_independent_tiles), has the same gap in
+    every scenario: its samples cannot matter, so it contributes neither
+    slots nor bytes (its score is formed in closed form)."""
     n_e = replica_range_sizes(problem, cand)
-    used = [(o, e) for (o, e) in live_tiles if n_e[e] > 0]
+    used = [(o, e) for (o, e) in live_tiles if n_e[e] > 0 and (o, e) not in fixed]
     slots = float(sum(S * excl_slots_per_scenario(int(n_e[e])) for (_, e) in used))
     return slots, 8.0 * S * len(used), float(n_e.mean()), S * len(used)
+
+
+def sample_independent_tiles(fs, ctx, problem, iv, cand, O, E, dev):
+    """Tiles (o, e) whose tau is U in both realisations for every sample:
+    tau = max(U, max_r min(f_r, M_r)) with f_r <= 1, so that happens exactly
+    when tau at the largest valid sample (capacity 2^64, tail 0: every f_r
+    is 1) equals tau at capacity 0 (every f_r is 0).  Counted with one dump
+    of tau at each of those two samples."""
+    import numpy as np
+    import torch
+    n_e = replica_range_sizes(problem, cand.cpu().numpy())
+    zeros = torch.zeros((O, E, 1), dtype=torch.float32, device=dev)
+    hi = torch.full((O, E, 1), 2.0 ** 64, dtype=torch.float32, device=dev)
+    d_hi = fs.score_candidates(ctx, problem, iv, cand, hi, zeros, dump=True).tau_dump.cpu().numpy()
+    d_lo = fs.score_candidates(ctx, problem, iv, cand, zeros, zeros, dump=True).tau_dump.cpu().numpy()
+    same = np.all(d_hi[:, :, 0, :] == d_lo[:, :, 0, :], axis=2)
+    return frozenset((o, e) for o in range(O) for e in range(E)
+                     if same[o, e] and n_e[e] >= 1)
 
 
 def loop_bench(args):
@@ -711,15 +730,19 @@ def main():
     live_tiles = [(o, e) for o in range(O) for e in range(E) if not measured_cand[o, e]]
     scenarios = len(live_tiles) * S
     kernel = args.kernel if args.kernel else (3 if p.floor_rps is None else 1)
-    slots, nbytes, mean_ne, sampled = excl_work(p, w.cand, live_tiles, S)
+    fixed = frozenset()
+    if kernel == 3:
+        ctx.set_score_kernel(3)
+        fixed = sample_independent_tiles(fs, ctx, p, iv, cand, O, E, dev)
+    slots, nbytes, mean_ne, sampled = excl_work(p, w.cand, live_tiles, S, fixed)
 
     # Copies of the samples for the cold pass: enough that the samples one
-    # rotation reads exceed three times the 256 MB Infinity Cache, within 4 GB
+    # rotation reads exceed three times the 256 MB Infinity Cache, within 8 GB
     # and 256 copies; a workload whose samples cannot reach that (a few MB or
     # less per step) has no cold pass.
     copies = args.cold_copies
     if copies < 0:
-        copies = int(min(max(2, math.ceil(3 * 256e6 / max(nbytes, 1.0))), max(2, 4e9 // (8.0 * O * E * S)), 256))
+        copies = int(min(max(2, math.ceil(3 * 256e6 / max(nbytes, 1.0))), max(2, 8e9 // (8.0 * O * E * S)), 256))
         if copies * nbytes < 3 * 256e6:
             copies = 0
     plans = [fs.ScorePlan(ctx, p, iv, cand, cap_s, tail_s, out=out, workspace=ws, stream=stream)]

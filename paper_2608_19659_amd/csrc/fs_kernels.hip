@@ -1873,6 +1873,21 @@ __device__ __forceinline__ int sampled_quotient(float rf, float cs, double rcp) 
   return __float_as_int((float)((double)capacity * rcp));
 }
 
+// Pairwise sum (balanced tree over the sample order, zero-padded to a power
+// of two) of n copies of c.  Every full aligned block of 2^j copies sums to
+// 2^j c exactly, so the tree is its lowest set bit of n as one full block,
+// then one addition per higher set bit, innermost first.
+__device__ __forceinline__ double pairwise_run(double c, int64_t n) {
+  if (n <= 0) return 0.0;
+  int64_t low = n & -n;
+  double acc = (double)low * c;
+  for (int64_t rest = n - low; rest != 0; rest -= low) {
+    low = rest & -rest;
+    acc = (double)low * c + acc;
+  }
+  return acc;
+}
+
 // Largest replica range handled by the unrolled scan; longer ranges use the
 // crossing search.
 constexpr int kScanMax = 4;
@@ -1912,10 +1927,11 @@ __device__ __forceinline__ void load_chunk(const float *__restrict__ cap_s, cons
   }
 }
 
-// Everything one work item reads: its work-list entry, the lane's samples,
-// U of both realisations, and M and the capacity threshold of option
+// Everything one work item reads: its work-list entry, U of both
+// realisations, M and the capacity threshold of option
 // rlo + min(lane, nr - 1) of both realisations (a scan reads M lane by lane,
-// the crossing search looks both up across lanes).
+// the crossing search looks both up across lanes), and -- unless no sample
+// can matter (triv) -- the lane's samples.
 template <int SPL>
 struct ScoreItem {
   int4 ent;
@@ -1923,6 +1939,7 @@ struct ScoreItem {
   int u0, u1;
   int vm0, vm1;
   float vt0, vt1;
+  bool triv;
 };
 
 // Value of lane idx (0 <= idx < 64) of v, per lane.
@@ -1933,13 +1950,22 @@ __device__ __forceinline__ int lane_lookup(int v, int idx) { return __builtin_am
 // every wavefront gets the same number of items to within one, and the
 // chunks of one tile are neighbours.  Each wavefront of the grid takes the
 // items it, it + W, it + 2W, ... (W wavefronts) and runs them as a
-// two-stage pipeline: the list entry of the
-// item after next, then the samples and constants of the next item, are in
-// flight while the current item is evaluated.  All of these are vector loads
+// three-stage pipeline: while the current item is evaluated, the list entry
+// of the third item ahead, the constants (U, M, thresholds) of the second
+// and the samples of the next are in flight.  All of these are vector loads
 // at unconditional (clamped) addresses, so each wait covers exactly the item
 // it is for; the per-class constants sit in LDS.  Lane l owns samples
 // [c * 64 * SPL + l * SPL, + SPL) of the item's tile, and the chunk's sum
 // is written as one partial (a node of the pairwise tree over s).
+//
+// An item whose M over the whole range is at most U in both realisations
+// has tau = U in every scenario, whatever its samples (every term
+// min(f_r, M_r) is at most M_r): its samples are not read (the item's loads
+// go to one line at the start of the arrays, still unconditionally) and its
+// partial is the closed-form pairwise sum of the constant gap U+ - U-.
+// M falls along a range (M_r = min(H[G - t*r], 1) with H a prefix
+// maximum, as signed integers on its bits), so M at the range's first
+// count, in lane 0, is its largest.
 //
 // Per realisation, tau = max(U, max_r min(f_r, M_r)) with M_r = H[G - t*r].
 // Ranges of at most kScanMax replica counts are scanned.  For longer ones:
@@ -1998,14 +2024,13 @@ __global__ __launch_bounds__(64) void k_score_excl(
                      __builtin_amdgcn_readfirstlane(v.z), __builtin_amdgcn_readfirstlane(v.w));
   };
   auto list_at = [&](const Pos &p) { return list[(p.j < n_list ? p.j : 0) + vz]; };
-  // Issues the loads of an item whose list entry is known.  Items without a
-  // tile read one line at the start of the arrays instead.
-  auto issue = [&](ScoreItem<SPL> &X, const Pos &p) {
+  // Issues the constant loads of an item whose list entry is known.  Items
+  // without a tile read one line at the start of the arrays instead.
+  auto issue_head = [&](ScoreItem<SPL> &X) {
     const int4 en = X.ent;
     const bool live = en.x >= 0;
     const int nr = en.z >> 16, o = en.w >> 8;
     const size_t tile = live ? (size_t)o * E + en.x : 0;
-    load_chunk<SPL, VEC>(cap_s, tail_s, tile * S, live ? p.c * CHUNK + lane * SPL : 0, S, live, X.cs, X.ls);
     const size_t row0 = live ? (size_t)o * 2 * n_thr : 0, row1 = live ? row0 + n_thr : 0;
     const int toff = live ? en.y : 0;
     const int2 u = *reinterpret_cast<const int2 *>(&tiles[tile + vz].u_m);
@@ -2017,6 +2042,20 @@ __global__ __launch_bounds__(64) void k_score_excl(
     X.vt0 = thr[row0 + at];
     X.vt1 = thr[row1 + at];
   };
+  // Decides, from an item's constants, whether its samples can matter, and
+  // issues their loads if so.  The test uses the comparisons the evaluation
+  // makes (signed integers on binary32 bits).
+  auto issue_samples = [&](ScoreItem<SPL> &X, const Pos &p) {
+    const int4 en = X.ent;
+    const int o = en.w >> 8;
+    const int m0 = __builtin_amdgcn_readfirstlane(X.vm0), m1 = __builtin_amdgcn_readfirstlane(X.vm1);
+    const int u0 = __builtin_amdgcn_readfirstlane(X.u0), u1 = __builtin_amdgcn_readfirstlane(X.u1);
+    const bool triv = !DUMP && en.x >= 0 && m0 <= u0 && m1 <= u1;
+    X.triv = triv;
+    const bool live = en.x >= 0 && !triv;
+    const size_t tile = live ? (size_t)o * E + en.x : 0;
+    load_chunk<SPL, VEC>(cap_s, tail_s, tile * S, live ? p.c * CHUNK + lane * SPL : 0, S, live, X.cs, X.ls);
+  };
   // Evaluates an item whose loads were issued.
   auto evaluate = [&](const ScoreItem<SPL> &X, const Pos &p) {
     const int4 en = X.ent;
@@ -2025,6 +2064,16 @@ __global__ __launch_bounds__(64) void k_score_excl(
     const int cls = en.w & 0x3F, state = (en.w >> 6) & 3, o = en.w >> 8;
     const size_t tile = (size_t)o * E + e;
     const int s_first = p.c * CHUNK + lane * SPL;
+    if (X.triv) {
+      // the chunk's samples past S add 0
+      if (lane == 0) {
+        const int u0 = __builtin_amdgcn_readfirstlane(X.u0), u1 = __builtin_amdgcn_readfirstlane(X.u1);
+        const int n = min(CHUNK, S - p.c * CHUNK);
+        partial[tile * n_chunk + p.c] =
+            pairwise_run((double)__int_as_float(u1) - (double)__int_as_float(u0), n);
+      }
+      return;
+    }
     if (DUMP && (state != 0 || nr == 0)) {
       // listed only when dumping: a revealed cell keeps the base values; a
       // cell no replica count reaches leaves tau at U
@@ -2239,52 +2288,52 @@ __global__ __launch_bounds__(64) void k_score_excl(
     if (lane == 0) partial[tile * n_chunk + p.c] = v;
   };
 
+  // Items a (current), m (next) and n (second next).
   Pos pa;
   pa.j = wv / n_chunk;
   pa.c = wv - (int)pa.j * n_chunk;
   pa.odd = 0;
-  ScoreItem<SPL> A, B;
-  A.ent = uniform4(list_at(pa));
+  ScoreItem<SPL> A, B, C;
+  // the first three list entries are requested together
+  const int4 raw_a = list_at(pa);
+  Pos pm = advance(pa);
+  const int4 raw_m = list_at(pm);
+  Pos pn = advance(pm);
+  int4 raw_n = list_at(pn);
+  A.ent = uniform4(raw_a);
   if (pa.j >= n_list) A.ent.x = -1;
-  issue(A, pa);
-  Pos pb = advance(pa);
-  int4 raw_b = list_at(pb);
-  // One pipeline stage: the list entry of the item after next is requested,
-  // the next item's loads are issued, the current item is evaluated.  The
-  // two item buffers alternate roles (no copies, so no early waits).  Places
-  // only grow, so the first end marker ends the wavefront's work.
-  auto stage = [&](ScoreItem<SPL> &cur, ScoreItem<SPL> &nxt) {
-    nxt.ent = uniform4(raw_b);
-    if (pb.j >= n_list) nxt.ent.x = -1;
-    const Pos pc = advance(pb);
-    const int4 raw_c = list_at(pc);
-    issue(nxt, pb);
+  issue_head(A);
+  B.ent = uniform4(raw_m);
+  if (pm.j >= n_list) B.ent.x = -1;
+  issue_head(B);
+  issue_samples(A, pa);
+  // One pipeline stage: the list entry of the third item ahead and the
+  // constants of the second are requested, the next item's samples are
+  // issued (its constants arrived during the previous stage), the current
+  // item is evaluated.  The three item buffers rotate roles (no copies, so
+  // no early waits).  Places only grow, so the first end marker ends the
+  // wavefront's work.
+  auto stage = [&](ScoreItem<SPL> &cur, ScoreItem<SPL> &mid, ScoreItem<SPL> &nxt) {
+    nxt.ent = uniform4(raw_n);
+    if (pn.j >= n_list) nxt.ent.x = -1;
+    const Pos pq = advance(pn);
+    const int4 raw_q = list_at(pq);
+    issue_head(nxt);
+    issue_samples(mid, pm);
     evaluate(cur, pa);
-    pa = pb;
-    pb = pc;
-    raw_b = raw_c;
+    pa = pm;
+    pm = pn;
+    pn = pq;
+    raw_n = raw_q;
   };
   for (;;) {
     if (A.ent.x < 0) break;
-    stage(A, B);
+    stage(A, B, C);
     if (B.ent.x < 0) break;
-    stage(B, A);
+    stage(B, C, A);
+    if (C.ent.x < 0) break;
+    stage(C, A, B);
   }
-}
-
-// Pairwise sum (balanced tree over the sample order, zero-padded to a power
-// of two) of n copies of c.  Every full aligned block of 2^j copies sums to
-// 2^j c exactly, so the tree is its lowest set bit of n as one full block,
-// then one addition per higher set bit, innermost first.
-__device__ __forceinline__ double pairwise_run(double c, int64_t n) {
-  if (n <= 0) return 0.0;
-  int64_t low = n & -n;
-  double acc = (double)low * c;
-  for (int64_t rest = n - low; rest != 0; rest -= low) {
-    low = rest & -rest;
-    acc = (double)low * c + acc;
-  }
-  return acc;
 }
 
 // Tile score of the exclusion scorer: Gamma_t - (sum over s of the

@@ -52,15 +52,27 @@ def assert_alloc_equal(problem, g, j, a, what=""):
 
 
 def gpu_score(env, problem, iv, cand, cap_s, tail_s, kernel, dump=True):
+    """Scores of one call; with dump, also tau of every scenario, and the
+    same call without the dump (a different scorer instance: the one that
+    skips the samples of tiles they cannot change) must give the same
+    scores, gaps and best candidates bit for bit."""
     torch, fs, ctx = env
     dev = "cuda:0"
     ctx.set_score_kernel(kernel)
     div = fs.DeviceIntervals.from_host(iv, dev)
     t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
-    r = fs.score_candidates(ctx, problem, div, t(np.asarray(cand, np.int32)), t(cap_s), t(tail_s), dump=dump)
+    args = (ctx, problem, div, t(np.asarray(cand, np.int32)), t(cap_s), t(tail_s))
+    r = fs.score_candidates(*args, dump=dump)
     torch.cuda.synchronize()
-    return (r.score.cpu().numpy(), r.gap_now.cpu().numpy(), r.best.cpu().numpy(),
-            None if r.tau_dump is None else r.tau_dump.cpu().numpy())
+    res = (r.score.cpu().numpy(), r.gap_now.cpu().numpy(), r.best.cpu().numpy(),
+           None if r.tau_dump is None else r.tau_dump.cpu().numpy())
+    if dump:
+        r2 = fs.score_candidates(*args, dump=False)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(r2.score.cpu().numpy().view(np.uint64), res[0].view(np.uint64))
+        np.testing.assert_array_equal(r2.gap_now.cpu().numpy(), res[1])
+        np.testing.assert_array_equal(r2.best.cpu().numpy(), res[2])
+    return res
 
 
 def assert_scores_equal(g, o, tile_mask=None):
@@ -373,6 +385,41 @@ def test_score_ragged_samples(env, orc, kernel, S):
     g = gpu_score(env, w.problem, w.intervals, w.cand, cs, ts, kernel)
     o = orc.score(w.problem, w.intervals, w.cand, cs, ts, n_threads=16)
     assert_scores_equal(g, o)
+
+
+@pytest.mark.parametrize("S", [1100, 4096])
+def test_samples_of_sample_independent_tiles_do_not_matter(env, orc, S):
+    """A tile whose M over its replica range is at most U in both
+    realisations has tau = U whatever its samples (Section 4.2's exclusion
+    form: every min(f_r, M_r) is at most M_r), and the scorer does not read
+    its samples.  Such tiles -- found with the oracle, as those whose tau at
+    the largest valid capacity equals tau at capacity 0 -- get samples at
+    the ends of the valid range (0, 2^-64, 2^64, tails above and below the
+    SLO) and the scores stay the oracle's, bit for bit; S = 1100 ends in a
+    ragged chunk."""
+    w = make_workload("4class-G64", orders=[0, 1, 2, 3])
+    O, E = w.intervals.measured.shape[0], len(w.cand)
+    hi = np.full((O, E, 1), 2.0 ** 64, np.float32)
+    zero = np.zeros((O, E, 1), np.float32)
+    d_hi = orc.score(w.problem, w.intervals, w.cand, hi, zero, n_threads=8).tau_dump
+    d_lo = orc.score(w.problem, w.intervals, w.cand, zero, zero, n_threads=8).tau_dump
+    fixed = np.all(d_hi[:, :, 0, :] == d_lo[:, :, 0, :], axis=2)
+    live = ~w.intervals.measured[:, w.cand].astype(bool)
+    assert (fixed & live).sum() > 50
+    rng = np.random.default_rng(77)
+    cs = np.ascontiguousarray(w.cap_s[:, :, :S]).copy()
+    ts = np.ascontiguousarray(w.tail_s[:, :, :S]).copy()
+    ends = np.array([0.0, 2.0 ** -64, 2.0 ** 64], np.float32)
+    slo_hi = np.float32(max(w.problem.slo) * 4)
+    pick = rng.integers(0, 3, size=cs.shape)
+    cs[fixed] = ends[pick[fixed]]
+    ts[fixed] = np.where(rng.random(size=ts[fixed].shape) < 0.5, np.float32(0.0), slo_hi)
+    note(f"sample-independent tiles, S={S}: {(fixed & live).sum()} of {live.sum()} live tiles")
+    g = gpu_score(env, w.problem, w.intervals, w.cand, cs, ts, kernel=3, dump=False)
+    o = orc.score(w.problem, w.intervals, w.cand, cs, ts, dump=False, n_threads=16)
+    np.testing.assert_array_equal(g[0], o.score)
+    np.testing.assert_array_equal(g[1], o.gap_now)
+    np.testing.assert_array_equal(g[2], o.best)
 
 
 def test_score_no_candidates_and_all_measured(env, orc):
