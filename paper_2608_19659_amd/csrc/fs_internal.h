@@ -54,10 +54,11 @@ struct CandInfo {
 struct TileInfo {
   int32_t cls, t, rlo, rhi;  // class, TP degree, replica range (rlo > rhi: unused cell)
   int32_t u_m, u_p;          // U of the conservative / optimistic realisation (bits)
+  int32_t m_m, m_p;          // M at rlo, the largest over the range, of each realisation (bits; 0 when unused)
   int32_t state;             // 0 = solve, 1 = measured, -1 = invalid candidate
   int32_t cell;              // candidate cell index
   int32_t toff;              // option index of (class, TP, rlo): M and thresholds of the range
-  int32_t pad[3];
+  int32_t pad;
 };
 
 // Workspace layout; every region is 256-byte aligned.

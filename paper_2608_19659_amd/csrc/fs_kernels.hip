@@ -1025,7 +1025,7 @@ __device__ void prep_list(const DevProblem &P, int O, const uint8_t *__restrict_
           for (int o = sub; o < O; o += g) {
             TileInfo *tl = tiles + (size_t)o * E + e;
             tl->state = -1; tl->cell = cell; tl->cls = 0; tl->t = 0; tl->rlo = 1; tl->rhi = 0;
-            tl->toff = 0; tl->u_m = 0; tl->u_p = 0;
+            tl->toff = 0; tl->u_m = 0; tl->u_p = 0; tl->m_m = 0; tl->m_p = 0;
           }
         }
         continue;
@@ -1374,9 +1374,11 @@ __global__ __launch_bounds__(kThreads) void k_prep(DevProblem P, const float *__
     }
     for (; c < per_class; ++c) u0 = max(u0, c != local ? mc[c] : 0);
     const int u = max(max(u0, u1), max(u2, u3));
+    const int ti = local / B;
+    const int nr = crhi[local] >= crlo[local] ? crhi[local] - crlo[local] + 1 : 0;
+    // M at rlo, the same value as the option's
+    const int m_lo = nr > 0 ? min(H[G - C.tp[ti] * crlo[local]], __float_as_int(1.0f)) : 0;
     if (R == 0) {
-      const int ti = local / B;
-      const int nr = crhi[local] >= crlo[local] ? crhi[local] - crlo[local] + 1 : 0;
       const int meas = e == tid ? my_meas : measured[off + cell];
       tl->cls = ci; tl->t = C.tp[ti]; tl->cell = cell;
       tl->rlo = nr > 0 ? crlo[local] : 1;
@@ -1384,8 +1386,10 @@ __global__ __launch_bounds__(kThreads) void k_prep(DevProblem P, const float *__
       tl->state = meas ? 1 : 0;
       tl->toff = ci * PPc + C.optoff[ti] + (nr > 0 ? crlo[local] : 1) - 1;
       tl->u_m = u;
+      tl->m_m = m_lo;
     } else {
       tl->u_p = u;
+      tl->m_p = m_lo;
     }
   }
   if (ci == 0 && wave == 0) {
@@ -1492,7 +1496,7 @@ __device__ void prep_list_staged(const DevProblem &P, int O, const uint8_t *__re
           for (int o = sub; o < O; o += g) {
             TileInfo *tl = tiles + (size_t)o * E + e;
             tl->state = -1; tl->cell = cell; tl->cls = 0; tl->t = 0; tl->rlo = 1; tl->rhi = 0;
-            tl->toff = 0; tl->u_m = 0; tl->u_p = 0;
+            tl->toff = 0; tl->u_m = 0; tl->u_p = 0; tl->m_m = 0; tl->m_p = 0;
           }
         }
         continue;
@@ -1832,9 +1836,10 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
   int m2 = INT_MIN;
   for (int c = lane; c < per_class; c += kWave) m2 = max(m2, c != wc1 ? mc[c] : INT_MIN);
   const int wm2 = wave_max_dpp(m2);
-  for (int e = lane; e < E; e += kWave) {
-    const int cell = ccand[e];
-    const bool mine = cell >= 0 && cell < N && cell / per_class == i;
+  for (int e0 = 0; e0 < E; e0 += kWave) {
+    const int e = e0 + lane;
+    const int cell = ccand[min(e, E - 1)];
+    const bool mine = e < E && cell >= 0 && cell < N && cell / per_class == i;
     // the reads use a valid cell of class i for every candidate (so they
     // are unconditional and overlap); other candidates' values are unused
     const int local = mine ? cell - i * per_class : 0;
@@ -1842,19 +1847,25 @@ __global__ __launch_bounds__(1024) void k_prep_order(DevProblem P, const float *
     const int t = c_tp[ti], first = c_optoff[ti];
     const int lo = crlo[local], hi = crhi[local];
     const uint8_t rev = mrow[i * per_class + local];
+    const int nr = hi >= lo ? hi - lo + 1 : 0;
+    // M at rlo, the same value as the option's (every lane takes part in
+    // the lookup)
+    const int m_lo = min(__builtin_amdgcn_ds_bpermute(4 * max(G - t * (nr > 0 ? lo : 1), 0), hreg),
+                         __float_as_int(1.0f));
     if (!mine) continue;
     TileInfo *tl = tiles + (size_t)o * E + e;
     const int u = max(0, local == wc1 ? wm2 : wm1);
     if (R == 0) {
-      const int nr = hi >= lo ? hi - lo + 1 : 0;
       tl->cls = i; tl->t = t; tl->cell = cell;
       tl->rlo = nr > 0 ? lo : 1;
       tl->rhi = nr > 0 ? hi : 0;
       tl->state = rev ? 1 : 0;
       tl->toff = i * PPc + first + (nr > 0 ? lo : 1) - 1;
       tl->u_m = u;
+      tl->m_m = nr > 0 ? m_lo : 0;
     } else {
       tl->u_p = u;
+      tl->m_p = nr > 0 ? m_lo : 0;
     }
   }
   if (i == 0 && lane == 0) base[o * 2 + R] = max(0, wm1);  // 0: the empty allocation
@@ -1927,16 +1938,16 @@ __device__ __forceinline__ void load_chunk(const float *__restrict__ cap_s, cons
   }
 }
 
-// Everything one work item reads: its work-list entry, U of both
-// realisations, M and the capacity threshold of option
-// rlo + min(lane, nr - 1) of both realisations (a scan reads M lane by lane,
-// the crossing search looks both up across lanes), and -- unless no sample
-// can matter (triv) -- the lane's samples.
+// Everything one work item reads: its work-list entry, U and M at rlo of
+// both realisations (one 16-byte load of the tile record), and -- unless no
+// sample can matter (triv) -- the lane's samples and M and the capacity
+// threshold of option rlo + min(lane, nr - 1) of both realisations (a scan
+// reads M lane by lane, the crossing search looks both up across lanes).
 template <int SPL>
 struct ScoreItem {
   int4 ent;
   float cs[SPL], ls[SPL];
-  int u0, u1;
+  int u0, u1, mr0, mr1;
   int vm0, vm1;
   float vt0, vt1;
   bool triv;
@@ -1965,7 +1976,7 @@ __device__ __forceinline__ int lane_lookup(int v, int idx) { return __builtin_am
 // partial is the closed-form pairwise sum of the constant gap U+ - U-.
 // M falls along a range (M_r = min(H[G - t*r], 1) with H a prefix
 // maximum, as signed integers on its bits), so M at the range's first
-// count, in lane 0, is its largest.
+// count, which the set-up puts in the tile record, is its largest.
 //
 // Per realisation, tau = max(U, max_r min(f_r, M_r)) with M_r = H[G - t*r].
 // Ranges of at most kScanMax replica counts are scanned.  For longer ones:
@@ -2024,37 +2035,39 @@ __global__ __launch_bounds__(64) void k_score_excl(
                      __builtin_amdgcn_readfirstlane(v.z), __builtin_amdgcn_readfirstlane(v.w));
   };
   auto list_at = [&](const Pos &p) { return list[(p.j < n_list ? p.j : 0) + vz]; };
-  // Issues the constant loads of an item whose list entry is known.  Items
-  // without a tile read one line at the start of the arrays instead.
+  // Issues the tile-record load of an item whose list entry is known.
+  // Items without a tile read the first record instead.
   auto issue_head = [&](ScoreItem<SPL> &X) {
     const int4 en = X.ent;
     const bool live = en.x >= 0;
-    const int nr = en.z >> 16, o = en.w >> 8;
+    const int o = en.w >> 8;
     const size_t tile = live ? (size_t)o * E + en.x : 0;
-    const size_t row0 = live ? (size_t)o * 2 * n_thr : 0, row1 = live ? row0 + n_thr : 0;
-    const int toff = live ? en.y : 0;
-    const int2 u = *reinterpret_cast<const int2 *>(&tiles[tile + vz].u_m);
-    X.u0 = u.x;
-    X.u1 = u.y;
-    const int at = toff + (live && nr > 0 ? min(lane, nr - 1) : 0);
-    X.vm0 = mopt[row0 + at];
-    X.vm1 = mopt[row1 + at];
-    X.vt0 = thr[row0 + at];
-    X.vt1 = thr[row1 + at];
+    const int4 h = *reinterpret_cast<const int4 *>(&tiles[tile + vz].u_m);  // (u_m, u_p, m_m, m_p)
+    X.u0 = h.x;
+    X.u1 = h.y;
+    X.mr0 = h.z;
+    X.mr1 = h.w;
   };
-  // Decides, from an item's constants, whether its samples can matter, and
-  // issues their loads if so.  The test uses the comparisons the evaluation
-  // makes (signed integers on binary32 bits).
+  // Decides, from an item's record, whether its samples can matter, and
+  // issues their loads and the range's M and thresholds if so.  The test
+  // uses the comparisons the evaluation makes (signed integers on binary32
+  // bits).
   auto issue_samples = [&](ScoreItem<SPL> &X, const Pos &p) {
     const int4 en = X.ent;
-    const int o = en.w >> 8;
-    const int m0 = __builtin_amdgcn_readfirstlane(X.vm0), m1 = __builtin_amdgcn_readfirstlane(X.vm1);
+    const int nr = en.z >> 16, o = en.w >> 8;
+    const int m0 = __builtin_amdgcn_readfirstlane(X.mr0), m1 = __builtin_amdgcn_readfirstlane(X.mr1);
     const int u0 = __builtin_amdgcn_readfirstlane(X.u0), u1 = __builtin_amdgcn_readfirstlane(X.u1);
     const bool triv = !DUMP && en.x >= 0 && m0 <= u0 && m1 <= u1;
     X.triv = triv;
     const bool live = en.x >= 0 && !triv;
     const size_t tile = live ? (size_t)o * E + en.x : 0;
     load_chunk<SPL, VEC>(cap_s, tail_s, tile * S, live ? p.c * CHUNK + lane * SPL : 0, S, live, X.cs, X.ls);
+    const size_t row0 = live ? (size_t)o * 2 * n_thr : 0, row1 = live ? row0 + n_thr : 0;
+    const int at = (live ? en.y : 0) + (live && nr > 0 ? min(lane, nr - 1) : 0) + vz;
+    X.vm0 = mopt[row0 + at];
+    X.vm1 = mopt[row1 + at];
+    X.vt0 = thr[row0 + at];
+    X.vt1 = thr[row1 + at];
   };
   // Evaluates an item whose loads were issued.
   auto evaluate = [&](const ScoreItem<SPL> &X, const Pos &p) {
