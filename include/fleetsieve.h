@@ -162,8 +162,9 @@ typedef enum fs_option {
 
 typedef enum fs_objective { FS_OBJECTIVE_MAXMIN = 0, FS_OBJECTIVE_LEXICOGRAPHIC = 1 } fs_objective;
 
-/* Creates a context bound to HIP device `hip_device`.  One context per host
- * thread; a context is not thread-safe. */
+/* Creates a context bound to HIP device `hip_device` (with a stream and two
+ * events of its own, used inside fs_score_candidates_lex).  One context per
+ * host thread; a context is not thread-safe. */
 fs_status fs_context_create(int hip_device, fs_context **out);
 void fs_context_destroy(fs_context *ctx);
 fs_status fs_context_set_option(fs_context *ctx, fs_option option, int64_t value);
@@ -292,9 +293,16 @@ fs_status fs_certify_lex(fs_context *ctx, const fs_problem *p, fs_intervals iv, 
  * then the smaller TP, cell index, candidate (measured candidates score
  * (0, 0) and are never picked; -1 when none is left).  d_gap_*[o] (or NULL)
  * receive the order's current stages.  The max-min score equals
- * fs_score_candidates' score bit for bit.  Every scenario is a full solve
- * (two max-min solves and two knapsacks, one wavefront): far slower than
- * fs_score_candidates.  Workspace: fs_score_lex_workspace_size; sizes as in
+ * fs_score_candidates' score bit for bit.  By default the goodput stage of a
+ * scenario comes from per-order tables (the best goodput of the other
+ * classes per budget for every interval of the option ratios, built once per
+ * call) plus the candidate cell's options at the sample; with
+ * FS_OPT_SCORE_KERNEL set to 1, or where those tables do not fit, every scenario
+ * is solved in full (two max-min solves and two knapsacks, one wavefront:
+ * far slower).  Both give the same bits.  The orders' own stages are solved
+ * on a second stream of the context, forked from and joined back into
+ * `stream` within the call, so every output is ordered before later work on
+ * `stream`.  Workspace: fs_score_lex_workspace_size; sizes as in
  * fs_score_candidates; FS_ERR_UNSUPPORTED where the whole objective does not
  * fit (see fs_solve_batch_lex). */
 fs_status fs_score_lex_workspace_size(const fs_problem *p, int32_t n_orders, int32_t n_cand, int32_t n_samples,

@@ -206,7 +206,9 @@ hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const floa
                             const float *tail_hi, const uint8_t *measured, const int32_t *cand, const float *cap_s,
                             const float *tail_s, int32_t O, int32_t E, int32_t S, double *score_mm,
                             double *score_gp, double *gap_mm, double *gap_gp, int32_t *best, uint8_t *ws,
-                            const LexScoreLayout &L, int fast, hipStream_t s);
+                            const LexScoreLayout &L, int fast, hipStream_t s, hipStream_t side = nullptr,
+                            hipEvent_t fork = nullptr, hipEvent_t mid = nullptr, hipEvent_t join = nullptr,
+                            bool cand_here = false);
 
 // Interval refit and sample clamping (Algorithm 1's fit step).  The refit
 // outputs may alias its inputs.

@@ -2711,8 +2711,9 @@ __global__ __launch_bounds__(64) void k_certify_state(DevProblem P, const int8_t
 // ---------------------------------------------------------------------------
 struct LexLds {
   double *vgp;      // [G + 1] goodput of the layer, updated in place
-  int2 *aopt;       // [G + 1] per cost: (served rate bits, option index; -1 = none allowed)
+  int2 *aopt;       // [G + 4] the costs with an allowed option, ascending: (served rate bits, option index)
   int *vn;          // [G + 1] GPUs, -1 = no allowed completion
+  int *acost;       // [G + 4] their costs (padded with G + 1 to a multiple of 4)
   int16_t *choice;  // [K][G + 1] option index, -1 = empty, -2 = none
 };
 
@@ -2749,10 +2750,15 @@ __device__ void wave_lex_stage(const DevProblem &P, const int8_t *__restrict__ b
     const bool empty_ok = !restricted && tau <= 0;
     const float slo = P.slo[k], demand = P.demand[k], fl = P.floor_rps[k];
     const double rcp = P.rcp_demand[k];
-    for (int c = lane + 1; c <= G; c += kWave) {
+    // per cost the best allowed option (served rate, then the first in
+    // (TP, replicas) order), listed for the costs that have one (a ballot per
+    // 64 costs)
+    int n_c = 0;
+    for (int c0 = 1; c0 <= G; c0 += kWave) {
+      const int c = c0 + lane;
       float best = 0.0f;
       int bq = -1;
-      for (int ti = 0; ti < NT; ++ti) {  // options of cost c in (TP, replicas) order
+      for (int ti = 0; ti < NT && c <= G; ++ti) {  // options of cost c in (TP, replicas) order
         const int t = P.tp[ti], r = c / t;
         if (r * t != c) continue;
         const int b = bmap[k * (G + 1) + r];
@@ -2768,7 +2774,17 @@ __device__ void wave_lex_stage(const DevProblem &P, const int8_t *__restrict__ b
           bq = P.optoff[ti] + r - 1;
         }
       }
-      X.aopt[c] = make_int2(__float_as_int(best), bq);
+      const uint64_t m = __builtin_amdgcn_ballot_w64(bq >= 0);
+      if (bq >= 0) {
+        const int at = n_c + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+        X.aopt[at] = make_int2(__float_as_int(best), bq);
+        X.acost[at] = c;
+      }
+      n_c += __builtin_popcountll(m);
+    }
+    if (lane < 4) {
+      X.aopt[n_c + lane] = make_int2(0, -1);
+      X.acost[n_c + lane] = G + 1;  // padding: a cost no budget reaches
     }
     __syncthreads();
     for (int top = G; top >= 0; top -= kWave) {
@@ -2792,20 +2808,18 @@ __device__ void wave_lex_stage(const DevProblem &P, const int8_t *__restrict__ b
           bq = a.y;
         }
       };
-      int c = 1;
-      for (; c + 3 <= top; c += 4) {
-        const int2 a0 = X.aopt[c], a1 = X.aopt[c + 1], a2 = X.aopt[c + 2], a3 = X.aopt[c + 3];
-        const int i0 = max(gs - c, 0), i1 = max(gs - c - 1, 0), i2 = max(gs - c - 2, 0), i3 = max(gs - c - 3, 0);
+      // the listed costs, four at a time (the preference order is a total
+      // order, so the order of the terms does not matter)
+      for (int x = 0; x < n_c && X.acost[x] <= top; x += 4) {
+        const int c0 = X.acost[x], c1 = X.acost[x + 1], c2 = X.acost[x + 2], c3 = X.acost[x + 3];
+        const int2 a0 = X.aopt[x], a1 = X.aopt[x + 1], a2 = X.aopt[x + 2], a3 = X.aopt[x + 3];
+        const int i0 = max(gs - c0, 0), i1 = max(gs - c1, 0), i2 = max(gs - c2, 0), i3 = max(gs - c3, 0);
         const int n0 = X.vn[i0], n1 = X.vn[i1], n2 = X.vn[i2], n3 = X.vn[i3];
         const double v0 = X.vgp[i0], v1 = X.vgp[i1], v2 = X.vgp[i2], v3 = X.vgp[i3];
-        take(c, a0, n0, v0);
-        take(c + 1, a1, n1, v1);
-        take(c + 2, a2, n2, v2);
-        take(c + 3, a3, n3, v3);
-      }
-      for (; c <= top; ++c) {
-        const int i0 = max(gs - c, 0);
-        take(c, X.aopt[c], X.vn[i0], X.vgp[i0]);
+        take(c0, a0, n0, v0);
+        take(c1, a1, n1, v1);
+        take(c2, a2, n2, v2);
+        take(c3, a3, n3, v3);
       }
       wave_lds_fence();
       if (g >= 0) {
@@ -2844,7 +2858,8 @@ __device__ void wave_lex_stage(const DevProblem &P, const int8_t *__restrict__ b
 // choices, from an 8-byte aligned start.
 __device__ __host__ inline size_t lex_work_bytes(int K, int G) {
   const size_t g1 = (size_t)G + 1;
-  const size_t b = g1 * (sizeof(double) + sizeof(int2) + sizeof(int)) + (size_t)K * g1 * sizeof(int16_t);
+  const size_t b = g1 * (sizeof(double) + sizeof(int)) + (g1 + 3) * (sizeof(int2) + sizeof(int)) +
+                   (size_t)K * g1 * sizeof(int16_t);
   const size_t solver = 3 * g1 * sizeof(int);
   return 8 + (b > solver ? b : solver);  // 8: aligning the start
 }
@@ -2855,8 +2870,9 @@ __device__ __forceinline__ LexLds lex_lds(const DevProblem &P, void *start) {
   LexLds X;
   X.vgp = reinterpret_cast<double *>(base);
   X.aopt = reinterpret_cast<int2 *>(X.vgp + g1);
-  X.vn = reinterpret_cast<int *>(X.aopt + g1);
-  X.choice = reinterpret_cast<int16_t *>(X.vn + g1);
+  X.vn = reinterpret_cast<int *>(X.aopt + g1 + 3);
+  X.acost = X.vn + g1;
+  X.choice = reinterpret_cast<int16_t *>(X.acost + g1 + 3);
   return X;
 }
 
@@ -3070,8 +3086,7 @@ __host__ __device__ inline size_t lex_breaks_lds(int nopt) {
 // layers (binary64) and one class's best served rate per cost.
 __host__ __device__ inline size_t lex_tables_lds(int nopt, int per_class_options, int G) {
   const size_t nw = kLexPrepThreads / kWave;
-  return 8 * (size_t)nopt + 8 * (size_t)per_class_options +
-         nw * (16 * ((size_t)G + 1) + 4 * (((size_t)G + 2) & ~(size_t)1));
+  return 8 * (size_t)nopt + 8 * (size_t)per_class_options + nw * (16 * ((size_t)G + 1) + 8 * ((size_t)G + 4));
 }
 
 // Per (realisation R, order o): every option of every class (ratio bits, -1
@@ -3208,8 +3223,11 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_tables(DevProblem P, co
   int2 *icost = reinterpret_cast<int2 *>(oserved + nopt);  // [PP] class i's options: cost, cell
   double *Va = reinterpret_cast<double *>(icost + PP) + (size_t)wave * 2 * (G + 1);
   double *Vb = Va + G + 1;
+  // per wavefront: the costs with an allowed option and their best served
+  // rates, ascending, padded to a multiple of 4
   float *Ak = reinterpret_cast<float *>(reinterpret_cast<double *>(icost + PP) + (size_t)nw * 2 * (G + 1)) +
-              (size_t)wave * ((G + 2) & ~1);
+              (size_t)wave * 2 * (G + 4);
+  int *Ck = reinterpret_cast<int *>(Ak + G + 4);
   if (part * nw > nb) return;  // no interval for this block
   const int2 *opt = opt_in + ((size_t)o * 2 + R) * nopt;
   for (int q = tid; q < nopt; q += kLexPrepThreads) {
@@ -3243,37 +3261,46 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_tables(DevProblem P, co
     double *Vp = Va, *Vc = Vb;
     for (int k = K - 1; k >= 0; --k) {
       if (k == i) continue;
-      // A[c]: the best served rate of class k's allowed options of cost c
-      for (int c = lane + 1; c <= G; c += kWave) {
+      // A[c]: the best served rate of class k's allowed options of cost c,
+      // listed only for the costs that have one (a ballot per 64 costs)
+      int n_c = 0;
+      for (int c0 = 1; c0 <= G; c0 += kWave) {
+        const int c = c0 + lane;
         float a = NEGF;
         for (int ti = 0; ti < NT; ++ti) {
           const int t = P.tp[ti];
           const int r = c / t;
-          if (r * t == c) {
+          if (c <= G && r * t == c) {
             const int q = k * PP + P.optoff[ti] + r - 1;
             a = oratio[q] >= thr ? fmaxf(a, oserved[q]) : a;
           }
         }
-        Ak[c] = a;
+        const bool has = a > NEGF;
+        const uint64_t m = __builtin_amdgcn_ballot_w64(has);
+        if (has) {
+          const int at = n_c + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+          Ak[at] = a;
+          Ck[at] = c;
+        }
+        n_c += __builtin_popcountll(m);
       }
+      if (lane < 4) Ck[n_c + lane] = G + 1;  // padding: a cost no budget reaches
       wave_lds_fence();
+      // V'[g] = max(V[g] if empty allowed, max over listed c <= g of A[c] + V[g - c]):
+      // the max is exact, so the order of the terms does not matter
       for (int top = G; top >= 0; top -= kWave) {
         const int g = top - lane;  // lanes past g = 0 compute nothing
         const int gs = g >= 0 ? g : 0;
         double best = empty_ok ? Vp[gs] : NEG;
-        int c = 1;
-        for (; c + 3 <= top; c += 4) {
-          const float a0 = Ak[c], a1 = Ak[c + 1], a2 = Ak[c + 2], a3 = Ak[c + 3];
-          const double v0 = Vp[max(gs - c, 0)], v1 = Vp[max(gs - c - 1, 0)], v2 = Vp[max(gs - c - 2, 0)],
-                       v3 = Vp[max(gs - c - 3, 0)];
-          best = gs >= c ? fmax(best, (double)a0 + v0) : best;
-          best = gs >= c + 1 ? fmax(best, (double)a1 + v1) : best;
-          best = gs >= c + 2 ? fmax(best, (double)a2 + v2) : best;
-          best = gs >= c + 3 ? fmax(best, (double)a3 + v3) : best;
-        }
-        for (; c <= top; ++c) {
-          const double v = Vp[max(gs - c, 0)];
-          best = gs >= c ? fmax(best, (double)Ak[c] + v) : best;
+        for (int x = 0; x < n_c && Ck[x] <= top; x += 4) {
+          const int c0 = Ck[x], c1 = Ck[x + 1], c2 = Ck[x + 2], c3 = Ck[x + 3];
+          const float a0 = Ak[x], a1 = Ak[x + 1], a2 = Ak[x + 2], a3 = Ak[x + 3];
+          const double v0 = Vp[max(gs - c0, 0)], v1 = Vp[max(gs - c1, 0)], v2 = Vp[max(gs - c2, 0)],
+                       v3 = Vp[max(gs - c3, 0)];
+          best = gs >= c0 ? fmax(best, (double)a0 + v0) : best;
+          best = gs >= c1 ? fmax(best, (double)a1 + v1) : best;
+          best = gs >= c2 ? fmax(best, (double)a2 + v2) : best;
+          best = gs >= c3 ? fmax(best, (double)a3 + v3) : best;
         }
         if (g >= 0) Vc[g] = best;
       }
@@ -4360,20 +4387,31 @@ hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const floa
                             const float *tail_hi, const uint8_t *measured, const int32_t *cand, const float *cap_s,
                             const float *tail_s, int32_t O, int32_t E, int32_t S, double *score_mm,
                             double *score_gp, double *gap_mm, double *gap_gp, int32_t *best, uint8_t *ws,
-                            const LexScoreLayout &L, int fast, hipStream_t s) {
+                            const LexScoreLayout &L, int fast, hipStream_t s, hipStream_t side,
+                            hipEvent_t fork, hipEvent_t mid, hipEvent_t join, bool cand_here) {
   if (O == 0) return hipSuccess;
   double *gmm = gap_mm ? gap_mm : (double *)(ws + L.gap_mm);
   double *ggp = gap_gp ? gap_gp : (double *)(ws + L.gap_gp);
   const AllocOut none{nullptr, nullptr, nullptr, nullptr, nullptr};
-  hipError_t e = launch_certify_lex(P, cap_lo, cap_hi, tail_lo, tail_hi, measured, O, 0.0f,
-                                    (int32_t *)(ws + L.state), none, none, gmm, ggp, ws, L.score, s);
-  if (e != hipSuccess || E == 0) return e;
-  const int64_t n_partial = L.score.n_partial;
-  double *pmm = (double *)(ws + L.score.partial), *pgp = (double *)(ws + L.part_gp);
-  const CandInfo *info = (const CandInfo *)(ws + L.score.cand);
-  if (S > 0 && fast && L.fast.fast) {
-    // the max-min stage's set-up (U, M of every option), then the goodput
-    // stage's, then the scenarios
+  // Two chains after the bucket map.  The main stream builds the max-min
+  // stage's set-up (U, M of every option) and the goodput stage's tables
+  // (when the goodput stage uses them); the second stream, when there is
+  // one, takes the candidate records (with cand_here) and the orders' own
+  // stages (the certificate solves: a few wavefronts, bound by their
+  // latency).  The scenarios of the full-solve path wait for the records
+  // (mid), the finalize for all of the second chain (join): each wait
+  // between streams costs the host about as much as two launches.  The two
+  // chains write disjoint workspace regions.  The main chain is enqueued
+  // first, so that its kernels start while the host enqueues the other.
+  const bool par = side && fork && mid && join;
+  hipStream_t cs = par ? side : s;
+  const bool tables = S > 0 && fast && L.fast.fast && E > 0;
+  hipError_t e = hipSuccess;
+  if (par) {
+    e = hipEventRecord(fork, s);
+    if (e != hipSuccess) return e;
+  }
+  if (tables) {
     ScoreArgs a{};
     a.cap_lo = cap_lo; a.cap_hi = cap_hi; a.tail_lo = tail_lo; a.tail_hi = tail_hi; a.measured = measured;
     a.cand = cand; a.cap_s = cap_s; a.tail_s = tail_s; a.O = O; a.E = E; a.S = S;
@@ -4409,6 +4447,37 @@ hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const floa
         (const int32_t *)(ws + X.nbp), X.nbmax, nsplit, (double *)(ws + X.V), (double *)(ws + X.W));
     e = hipGetLastError();
     if (e != hipSuccess) return e;
+  }
+  // the second chain
+  if (par) {
+    e = hipStreamWaitEvent(side, fork, 0);
+    if (e != hipSuccess) return e;
+  }
+  if (cand_here && E > 0) {
+    k_setup_cand<<<(E + 255) / 256, 256, 0, cs>>>(P, cand, E, (const int8_t *)(ws + L.score.bmap),
+                                                  (CandInfo *)(ws + L.score.cand));
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (par && !tables) {
+    e = hipEventRecord(mid, side);
+    if (e != hipSuccess) return e;
+  }
+  e = launch_certify_lex(P, cap_lo, cap_hi, tail_lo, tail_hi, measured, O, 0.0f, (int32_t *)(ws + L.state), none,
+                         none, gmm, ggp, ws, L.score, cs);
+  if (e != hipSuccess) return e;
+  if (par) {
+    e = hipEventRecord(join, side);
+    if (e != hipSuccess) return e;
+  }
+  auto wait_mid = [&]() { return par ? hipStreamWaitEvent(s, mid, 0) : hipSuccess; };
+  auto joined = [&]() { return par ? hipStreamWaitEvent(s, join, 0) : hipSuccess; };
+  if (E == 0) return joined();
+  const int64_t n_partial = L.score.n_partial;
+  double *pmm = (double *)(ws + L.score.partial), *pgp = (double *)(ws + L.part_gp);
+  const CandInfo *info = (const CandInfo *)(ws + L.score.cand);
+  if (tables) {
+    const LexExclRegions &X = L.fast;
     const dim3 grid((unsigned)((S + kWave - 1) / kWave), (unsigned)E, (unsigned)O);
     k_score_lex_excl<<<grid, kWave, sizeof(int) * 2 * (size_t)X.nbmax, s>>>(
         P, (const TileInfo *)(ws + L.score.tiles), (const int32_t *)(ws + L.score.mopt), excl_thresholds(P), cap_s,
@@ -4419,6 +4488,8 @@ hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const floa
   } else if (S > 0) {
     const size_t base = lds_bytes_lex(P, 1), staged = base + stage2_bytes(P);
     const int stage = stage_fits(staged) ? 1 : 0;
+    e = wait_mid();
+    if (e != hipSuccess) return e;
     const dim3 grid((unsigned)((S + kWave - 1) / kWave), (unsigned)E, (unsigned)O);
     k_score_lex_wave<<<grid, 64, stage ? staged : base, s>>>(P, (const int8_t *)(ws + L.score.bmap), info, cap_lo,
                                                              cap_hi, tail_lo, tail_hi, measured, cap_s, tail_s, E,
@@ -4426,6 +4497,8 @@ hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const floa
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
+  e = joined();
+  if (e != hipSuccess) return e;
   k_finalize_lex<<<O, 64, 0, s>>>(P, info, measured, E, S, gmm, ggp, pmm, pgp, S > 0 ? n_partial : 0, score_mm,
                                   score_gp, best);
   return hipGetLastError();

@@ -465,32 +465,47 @@ def score_lex_workspace_size(problem, n_orders: int, n_cand: int, n_samples: int
     return int(out.value)
 
 
+class ScoreLexPlan:
+    """One fs_score_candidates_lex call with its arguments checked and
+    marshalled once; run() enqueues the call again on the same device
+    buffers.  Shapes as in ScorePlan."""
+
+    def __init__(self, ctx: Context, problem, iv: DeviceIntervals, cand, cap_s, tail_s, stream=None,
+                 workspace=None):
+        torch = _torch()
+        self._ref = _ProblemRef(problem)
+        O = int(iv.cap_lo.shape[0])
+        E = int(cand.shape[0])
+        S = int(cap_s.shape[2]) if E > 0 else 0
+        dev = iv.cap_lo.device
+        self._ivs = _intervals_struct(iv, O, self._ref.N)
+        pcand = _dev_ptr(cand, torch.int32, (E,), "cand")
+        pcs = _dev_ptr(cap_s, torch.float32, (O, E, S), "cap_s")
+        pts = _dev_ptr(tail_s, torch.float32, (O, E, S), "tail_s")
+        out = ScoreLexOutput(torch.empty((O, E), dtype=torch.float64, device=dev),
+                             torch.empty((O, E), dtype=torch.float64, device=dev),
+                             torch.empty(O, dtype=torch.float64, device=dev),
+                             torch.empty(O, dtype=torch.float64, device=dev),
+                             torch.empty(O, dtype=torch.int32, device=dev))
+        ws_bytes = score_lex_workspace_size(problem, O, E, S)
+        ws = workspace if workspace is not None else ctx.workspace(ws_bytes)
+        self.out, self._ws, self._keep = out, ws, (iv, cand, cap_s, tail_s)
+        self._fn = load_library().fs_score_candidates_lex
+        self._args = (ctx.handle, self._ref.ptr, self._ivs, O, pcand, E, pcs, pts, S,
+                      out.score_maxmin.data_ptr(), out.score_goodput.data_ptr(), out.gap_maxmin.data_ptr(),
+                      out.gap_goodput.data_ptr(), out.best.data_ptr(), ws.data_ptr(), ws.numel(),
+                      _stream(dev, stream))
+
+    def run(self) -> ScoreLexOutput:
+        _check(self._fn(*self._args))
+        return self.out
+
+
 def score_candidates_lex(ctx: Context, problem, iv: DeviceIntervals, cand, cap_s, tail_s, stream=None,
                          workspace=None) -> ScoreLexOutput:
     """The stage-wise score under the whole objective
     (fs_score_candidates_lex); shapes as in score_candidates."""
-    torch = _torch()
-    ref = _ProblemRef(problem)
-    O = int(iv.cap_lo.shape[0])
-    E = int(cand.shape[0])
-    S = int(cap_s.shape[2]) if E > 0 else 0
-    dev = iv.cap_lo.device
-    ivs = _intervals_struct(iv, O, ref.N)
-    pcand = _dev_ptr(cand, torch.int32, (E,), "cand")
-    pcs = _dev_ptr(cap_s, torch.float32, (O, E, S), "cap_s")
-    pts = _dev_ptr(tail_s, torch.float32, (O, E, S), "tail_s")
-    out = ScoreLexOutput(torch.empty((O, E), dtype=torch.float64, device=dev),
-                         torch.empty((O, E), dtype=torch.float64, device=dev),
-                         torch.empty(O, dtype=torch.float64, device=dev), torch.empty(O, dtype=torch.float64, device=dev),
-                         torch.empty(O, dtype=torch.int32, device=dev))
-    ws_bytes = score_lex_workspace_size(problem, O, E, S)
-    ws = workspace if workspace is not None else ctx.workspace(ws_bytes)
-    _check(load_library().fs_score_candidates_lex(ctx.handle, ref.ptr, ivs, O, pcand, E, pcs, pts, S,
-                                                  out.score_maxmin.data_ptr(), out.score_goodput.data_ptr(),
-                                                  out.gap_maxmin.data_ptr(), out.gap_goodput.data_ptr(),
-                                                  out.best.data_ptr(), ws.data_ptr(), ws.numel(),
-                                                  _stream(dev, stream)))
-    return out
+    return ScoreLexPlan(ctx, problem, iv, cand, cap_s, tail_s, stream, workspace).run()
 
 
 def refit_intervals(ctx: Context, problem, iv: DeviceIntervals, stream=None) -> DeviceIntervals:
