@@ -210,9 +210,15 @@ fs_status fs_solve_batch(fs_context *ctx, const fs_problem *p, const float *d_ca
  *   d_best    [n_orders] int32 (may be NULL)
  *   d_tau_dump NULL or [n_orders][n_cand][n_samples][2] = (tau-, tau+); for a
  *             measured candidate it holds the order's base values.
+ * Samples whose values cannot change the result are not read: the exclusion
+ * scorer (kernel 3, the default without critical floors) skips a tile whose
+ * cell no replica count reaches, and a tile whose tau is U in both
+ * realisations whatever its samples (in the exclusion form of Section 3's
+ * max-min knapsack: M at the range's first replica count at most U), and
+ * forms their sums in closed form.
  * Limits: n_orders and n_cand in [0, 65535], n_samples in [1, 2^20]; the
- * exclusion scorer (kernel 3) also needs n_orders * n_cand < 2^31 and
- * returns FS_ERR_UNSUPPORTED otherwise. */
+ * exclusion scorer also needs n_orders * n_cand < 2^31 and returns
+ * FS_ERR_UNSUPPORTED otherwise. */
 fs_status fs_score_candidates(fs_context *ctx, const fs_problem *p, fs_intervals iv,
                               int32_t n_orders, const int32_t *d_cand, int32_t n_cand,
                               const float *d_cap_s, const float *d_tail_s, int32_t n_samples,
