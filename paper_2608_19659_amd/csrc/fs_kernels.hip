@@ -284,6 +284,18 @@ __device__ __forceinline__ int conv_mono(const int *X, const int *Y, int g, int 
   return max(pos >= 1 ? left : INT_MIN, pos <= g ? right : INT_MIN);
 }
 
+// Entries of X among the first d entries of the ascending merge of X and Y
+// (n entries each, X first among equal values): a bisection over the split.
+__device__ __forceinline__ int merge_split(const int *X, const int *Y, int n, int d) {
+  int lo = max(0, d - n), hi = min(d, n);
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (X[mid] <= Y[d - 1 - mid]) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
 // Folds options into their cells' maxima and replica ranges.  Lanes holding
 // consecutive options of one TP degree fall on few cells (the load level
 // falls as r grows), in runs of lanes; the first lane of each run folds the
@@ -1287,7 +1299,13 @@ __global__ __launch_bounds__(kThreads) void k_prep(DevProblem P, const float *__
   }
 
   // --- H_ci: tree over the tables k != ci.  Level 0 reads B (logical table
-  // j is class j, or j + 1 from ci on); later levels alternate Xa / Xb.
+  // j is class j, or j + 1 from ci on); later levels alternate Xa / Xb.  For
+  // nondecreasing tables the (max,min) convolution of two is the first G
+  // entries of their ascending merge (Z[g] >= v iff at most g entries of
+  // the two lie below v), so a pair is merged: each thread takes `cw`
+  // consecutive outputs, finds where they start by a bisection over the
+  // split and then takes them one merge step at a time (one read per step,
+  // where a bisection per output reads 2 log2 G entries).
   const int n0 = K - 1;
   const int *H;
   if (K == 1) {
@@ -1301,18 +1319,34 @@ __global__ __launch_bounds__(kThreads) void k_prep(DevProblem P, const float *__
     int *src = nullptr, *dst = Xa;
     while (n > 1) {
       const int pairs = n >> 1, odd = n & 1;
-      for (int item = tid; item < (pairs + odd) * G; item += nth) {
-        const int p = item / G, g = item - p * G;
+      // outputs per thread: enough that the pairs fill the block, at least 4
+      int cw = (pairs * G + nth - 1) / nth;
+      cw = cw < 4 ? 4 : cw;
+      const int per = (G + cw - 1) / cw;
+      for (int item = tid; item < pairs * per; item += nth) {
+        const int p = item / per, c0 = (item - p * per) * cw;
         const int ja = 2 * p, jb = 2 * p + 1;
         const int *X = src ? src + ja * G : Bsrc + (ja < ci ? ja : ja + 1) * G;
-        int v;
-        if (p < pairs) {
-          const int *Y = src ? src + jb * G : Bsrc + (jb < ci ? jb : jb + 1) * G;
-          v = conv_mono(X, Y, g, top);
-        } else {
-          v = X[g];  // the odd table passes through
+        const int *Y = src ? src + jb * G : Bsrc + (jb < ci ? jb : jb + 1) * G;
+        int i = merge_split(X, Y, G, c0), j = c0 - i;
+        int xv = X[min(i, G - 1)], yv = Y[min(j, G - 1)];
+        const int c1 = min(c0 + cw, G);
+        for (int g = c0; g < c1; ++g) {
+          const bool take_x = i < G && (j >= G || xv <= yv);
+          dst[p * G + g] = take_x ? xv : yv;
+          if (take_x) {
+            ++i;
+            xv = X[min(i, G - 1)];
+          } else {
+            ++j;
+            yv = Y[min(j, G - 1)];
+          }
         }
-        dst[p * G + g] = v;
+      }
+      if (odd) {  // the odd table passes through
+        const int ja = 2 * pairs;
+        const int *X = src ? src + ja * G : Bsrc + (ja < ci ? ja : ja + 1) * G;
+        for (int g = tid; g < G; g += nth) dst[pairs * G + g] = X[g];
       }
       __syncthreads();
       n = pairs + odd;
