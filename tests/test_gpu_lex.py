@@ -356,3 +356,45 @@ def test_stagewise_score_all_measured_and_no_candidate(env):
         o = oracle.score_lex(p, iv, w.cand, cs, ts)
         _assert_score_lex_equal(g, o, f"all revealed, kernel {kernel}")
         assert np.all(g["score_maxmin"] == 0.0) and np.all(g["best"] == -1)
+
+
+def test_stagewise_score_in_a_captured_graph(env):
+    """fs_score_candidates_lex forks its certificate solves onto the
+    context's second stream and joins them back with events, which stream
+    capture follows: the call captured into a graph and replayed several
+    times, with eager work and synchronizations between the replays, gives
+    the eager call's outputs every time (the outputs are cleared before each
+    replay)."""
+    torch, fs, ctx = env
+    w = make_workload("4class-G64", orders=[0, 1, 2])
+    S = 16
+    cs, ts = np.ascontiguousarray(w.cap_s[:, :, :S]), np.ascontiguousarray(w.tail_s[:, :, :S])
+    div = fs.DeviceIntervals.from_host(w.intervals, "cuda:0")
+    cand_d, cs_d, ts_d = _t(env, w.cand), _t(env, cs), _t(env, ts)
+    note("stage-wise score captured in a graph, 4class-G64 orders 0-2 S=16")
+    eager = fs.score_candidates_lex(ctx, w.problem, div, cand_d, cs_d, ts_d)
+    torch.cuda.synchronize()
+    want = {k: getattr(eager, k).clone() for k in ("score_maxmin", "score_goodput", "gap_maxmin", "gap_goodput",
+                                                    "best")}
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        plan = fs.ScoreLexPlan(ctx, w.problem, div, cand_d, cs_d, ts_d, stream=side)
+        plan.run()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=side):
+            plan.run()
+    torch.cuda.synchronize()
+    for rep in range(4):
+        for k in want:
+            getattr(plan.out, k).fill_(-7)
+        torch.cuda.synchronize()
+        # eager work of the program between the replays
+        other = fs.score_candidates(ctx, w.problem, div, cand_d, cs_d, ts_d)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for k in want:
+            assert torch.equal(getattr(plan.out, k), want[k]), (rep, k)
+        np.testing.assert_array_equal(other.score.cpu().numpy(), want["score_maxmin"].cpu().numpy())
