@@ -3940,7 +3940,7 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // step took 94.7 us with 512 and 75.9 with 1024, the 8-class, G = 256 one
 // 119.6 with 512 and 139.5 with 1024.
 constexpr size_t kPrepLdsLimit = 60 * 1024;
-constexpr int kPrepThreads = 512, kPrepThreadsWide = 1024, kPrepWideBudget = 512;
+constexpr int kPrepThreads = 512, kPrepThreadsWide = 1024, kPrepThreadsNarrow = 256, kPrepWideBudget = 512;
 
 // LDS of the exclusion set-up besides its tables: cells (cap, tail), the
 // class's cell maxima and replica ranges, and the load-level table.
@@ -4099,7 +4099,14 @@ static hipError_t launch_excl_setup(const DevProblem &P, const ScoreArgs &a, hip
                                           dump, gtab, tiles, base, mopt, thr, n_thr, list, live, a.thr_search,    \
                                           staged, btab);                                                          \
   }
-    if (P.G >= kPrepWideBudget) {
+    // below a budget of 512: 256 threads per block once the class blocks
+    // fill the GPU (more blocks resident at a time; 8 classes at G = 256
+    // over 64 orders: step 80.5 -> 74 us; 128 threads: 82 us), else 512
+    const bool narrow = (int64_t)2 * a.O * P.K >= 256;
+    if (narrow && P.G < kPrepWideBudget) {
+      if (in_lds) FS_PREP_GENERAL(true, kPrepThreadsNarrow)
+      else FS_PREP_GENERAL(false, kPrepThreadsNarrow)
+    } else if (P.G >= kPrepWideBudget) {
       if (in_lds) FS_PREP_GENERAL(true, kPrepThreadsWide)
       else FS_PREP_GENERAL(false, kPrepThreadsWide)
     } else {
