@@ -1091,8 +1091,12 @@ __device__ void prep_list(const DevProblem &P, int O, const uint8_t *__restrict_
 // the prefix maximum (best ratio with at most g GPUs, g in [0, G)).  Every
 // class block of k_prep reads the tables of the other classes from here
 // instead of building them itself.
-constexpr int kBtabThreads = 256;
+// Threads per B-table block: 256, or 1024 for budgets of 512 and more
+// (about 2,000 options per class at G = 1024: 16 classes over 4 orders,
+// step 40.6 -> 37.2 us; at G = 256, 1024 threads cost 4 us).
+constexpr int kBtabThreadsSmall = 256, kBtabThreadsLarge = 1024;
 
+template <int kBtabThreads>
 __global__ __launch_bounds__(kBtabThreads) void k_prep_btab(DevProblem P, const float *__restrict__ cap_lo,
                                                            const float *__restrict__ cap_hi,
                                                            const float *__restrict__ tail_lo,
@@ -4078,12 +4082,20 @@ static hipError_t launch_excl_setup(const DevProblem &P, const ScoreArgs &a, hip
     int32_t *btab = (int32_t *)(a.ws + a.L.btab);
     {
       const size_t blds = sizeof(int) * (size_t)P.G + 2 * sizeof(float) * (size_t)P.NT * P.B;
+      const bool large = P.G >= kPrepWideBudget;
+      const void *fn = large ? reinterpret_cast<const void *>(&k_prep_btab<kBtabThreadsLarge>)
+                             : reinterpret_cast<const void *>(&k_prep_btab<kBtabThreadsSmall>);
       if (blds > 64 * 1024) {
-        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_prep_btab),
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)blds);
+        const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)blds);
         if (e != hipSuccess) return e;
       }
-      k_prep_btab<<<dim3(2, a.O, P.K), kBtabThreads, blds, s>>>(P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, btab);
+      if (large) {
+        k_prep_btab<kBtabThreadsLarge><<<dim3(2, a.O, P.K), kBtabThreadsLarge, blds, s>>>(
+            P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, btab);
+      } else {
+        k_prep_btab<kBtabThreadsSmall><<<dim3(2, a.O, P.K), kBtabThreadsSmall, blds, s>>>(
+            P, a.cap_lo, a.cap_hi, a.tail_lo, a.tail_hi, btab);
+      }
       const hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
     }
