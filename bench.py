@@ -91,11 +91,20 @@ def existing_options(problem):
     return np.array(rows)
 
 
+def kernel_code_text(src: str) -> str:
+    """The kernel source as code: comments, trailing blanks and empty lines
+    removed, so that a change of comments alone keeps the profiles taken on
+    the same code valid.  (The source has no comment markers inside string
+    literals.)"""
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    return "\n".join(line.rstrip() for line in src.splitlines() if line.strip())
+
+
 def _kernel_source_digest() -> str:
-    h = hashlib.sha256()
-    with open(os.path.join(ROOT, "paper_2608_19659_amd", "csrc", "fs_kernels.hip"), "rb") as f:
-        h.update(f.read())
-    return h.hexdigest()[:16]
+    """sha256/16 of fs_kernels.hip as code (kernel_code_text)."""
+    with open(os.path.join(ROOT, "paper_2608_19659_amd", "csrc", "fs_kernels.hip")) as f:
+        return hashlib.sha256(kernel_code_text(f.read()).encode()).hexdigest()[:16]
 
 
 def committed_traffic(kernel: str, workload_tag: str):

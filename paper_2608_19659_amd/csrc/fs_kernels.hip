@@ -2000,8 +2000,9 @@ __device__ __forceinline__ int lane_lookup(int v, int idx) { return __builtin_am
 // chunks of one tile are neighbours.  Each wavefront of the grid takes the
 // items it, it + W, it + 2W, ... (W wavefronts) and runs them as a
 // three-stage pipeline: while the current item is evaluated, the list entry
-// of the third item ahead, the constants (U, M, thresholds) of the second
-// and the samples of the next are in flight.  All of these are vector loads
+// of the third item ahead, the tile-record words of the second (U and M at
+// rlo, both realisations) and the samples and the range's M and thresholds
+// of the next are in flight.  All of these are vector loads
 // at unconditional (clamped) addresses, so each wait covers exactly the item
 // it is for; the per-class constants sit in LDS.  Lane l owns samples
 // [c * 64 * SPL + l * SPL, + SPL) of the item's tile, and the chunk's sum
