@@ -3128,6 +3128,12 @@ __host__ __device__ inline size_t lex_tables_lds(int nopt, int per_class_options
   return 8 * (size_t)nopt + 8 * (size_t)per_class_options + nw * (16 * ((size_t)G + 1) + 8 * ((size_t)G + 4));
 }
 
+// LDS of a k_score_lex_excl block: both realisations' breakpoints and M of
+// the candidate's replica range.
+__host__ __device__ inline size_t lex_score_lds(int nbmax, int rmax) {
+  return sizeof(int) * (2 * (size_t)nbmax + 2 * (size_t)rmax);
+}
+
 // Per (realisation R, order o): every option of every class (ratio bits, -1
 // when no load level holds it; served rate) to opt_out, and the sorted
 // distinct ratios, 0 always among them, to bp_out (nb of them to nbp).
@@ -3404,33 +3410,44 @@ __global__ __launch_bounds__(64) void k_score_lex_excl(DevProblem P, const TileI
                                                        const float *__restrict__ cap_s,
                                                        const float *__restrict__ tail_s, int32_t E, int32_t S,
                                                        const float *__restrict__ bp, const int32_t *__restrict__ nbp,
-                                                       int32_t nbmax, const double *__restrict__ V,
+                                                       int32_t nbmax, int32_t rmax, const double *__restrict__ V,
                                                        const double *__restrict__ W, double *__restrict__ part_mm,
                                                        double *__restrict__ part_gp, int64_t n_partial) {
-  extern __shared__ int lex_bp[];
+  extern __shared__ int lex_bp[];  // [2][nbmax] breakpoints, then [2][rmax] M of the range
+  int *Ml = lex_bp + 2 * nbmax;
   const int chunk = blockIdx.x, e = blockIdx.y, o = blockIdx.z, lane = threadIdx.x;
   const size_t tile = (size_t)o * E + e;
+  // the loads that need nothing else come first, together: the tile
+  // record, both realisations' breakpoints (every slot; those past the
+  // count are not used), the lane's sample
   const TileInfo tl = tiles[tile];
-  if (tl.state != 0) return;  // measured or invalid: the finalize writes those
-  const int G = P.G, K = P.K, per_class = P.NT * P.B;
   const int nb0 = nbp[o * 2 + 0], nb1 = nbp[o * 2 + 1];
-  for (int m = lane; m < nb0; m += kWave) lex_bp[m] = __float_as_int(bp[((size_t)o * 2 + 0) * nbmax + m]);
-  for (int m = lane; m < nb1; m += kWave) lex_bp[nbmax + m] = __float_as_int(bp[((size_t)o * 2 + 1) * nbmax + m]);
-  wave_lds_fence();
+  for (int m = lane; m < nbmax; m += kWave) {
+    lex_bp[m] = __float_as_int(bp[((size_t)o * 2 + 0) * nbmax + m]);
+    lex_bp[nbmax + m] = __float_as_int(bp[((size_t)o * 2 + 1) * nbmax + m]);
+  }
   const int s = chunk * kWave + lane;
   const bool live = s < S;
   const float cs = cap_s[tile * S + (live ? s : 0)];
   const float ls = tail_s[tile * S + (live ? s : 0)];
+  if (tl.state != 0) return;  // measured or invalid: the finalize writes those
+  // M of the range's options, both realisations, into LDS
+  const int nr = tl.rhi >= tl.rlo ? tl.rhi - tl.rlo + 1 : 0;
+  for (int j = lane; j < nr; j += kWave) {
+    Ml[j] = mopt[((size_t)o * 2 + 0) * n_thr + tl.toff + j];
+    Ml[rmax + j] = mopt[((size_t)o * 2 + 1) * n_thr + tl.toff + j];
+  }
+  wave_lds_fence();
+  const int G = P.G, K = P.K, per_class = P.NT * P.B;
   const int i = tl.cls, local = tl.cell - i * per_class;
   const float slo = P.slo[i], lam = P.demand[i];
   const double rcp = P.rcp_demand[i];
-  int tau[2];
-  double gp[2];
+  // tau* and its interval, both realisations
+  int tau[2], row_j[2];
 #pragma unroll
   for (int R = 0; R < 2; ++R) {
-    const int32_t *M = mopt + ((size_t)o * 2 + R) * n_thr + tl.toff;
     int t = R == 0 ? tl.u_m : tl.u_p;
-    for (int r = tl.rlo; r <= tl.rhi; ++r) t = max(t, min(ratio_bits(cs, ls, r, slo, rcp), M[r - tl.rlo]));
+    for (int r = tl.rlo; r <= tl.rhi; ++r) t = max(t, min(ratio_bits(cs, ls, r, slo, rcp), Ml[R * rmax + r - tl.rlo]));
     tau[R] = t;
     // interval: the count of breakpoints below tau
     const int nb = R == 0 ? nb0 : nb1;
@@ -3441,18 +3458,32 @@ __global__ __launch_bounds__(64) void k_score_lex_excl(DevProblem P, const TileI
       if (b[mid] < t) lo = mid + 1;
       else hi = mid;
     }
-    const size_t row = ((((size_t)o * 2 + R) * K + i) * (size_t)(nbmax + 1) + lo);
-    const double *Wj = W + row * 4;
-    const double *Vj = V + row * (size_t)(G + 1);
-    double g = (int)Wj[3] == local ? Wj[1] : Wj[0];
-    g = fmax(g, Wj[2]);
-    for (int r = tl.rlo; r <= tl.rhi; ++r) {
-      if (ratio_bits(cs, ls, r, slo, rcp) >= t) {
-        const float sv = ls <= slo ? served_rps(cs, r, lam) : 0.0f;
-        g = fmax(g, (double)sv + Vj[G - tl.t * r]);
-      }
-    }
-    gp[R] = g;
+    row_j[R] = lo;
+  }
+  // the interval tables of both realisations: the summary first (both
+  // rows' loads together), then the candidate cell's allowed options
+  const double *Wj[2], *Vj[2];
+  double w[2][4];
+#pragma unroll
+  for (int R = 0; R < 2; ++R) {
+    const size_t row = ((((size_t)o * 2 + R) * K + i) * (size_t)(nbmax + 1) + row_j[R]);
+    Wj[R] = W + row * 4;
+    Vj[R] = V + row * (size_t)(G + 1);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) w[R][q] = Wj[R][q];
+  }
+  double gp[2];
+#pragma unroll
+  for (int R = 0; R < 2; ++R) {
+    double g = (int)w[R][3] == local ? w[R][1] : w[R][0];
+    gp[R] = fmax(g, w[R][2]);
+  }
+  for (int r = tl.rlo; r <= tl.rhi; ++r) {
+    const int f = ratio_bits(cs, ls, r, slo, rcp);
+    const float sv = ls <= slo ? served_rps(cs, r, lam) : 0.0f;
+    const double v0 = Vj[0][G - tl.t * r], v1 = Vj[1][G - tl.t * r];
+    if (f >= tau[0]) gp[0] = fmax(gp[0], (double)sv + v0);
+    if (f >= tau[1]) gp[1] = fmax(gp[1], (double)sv + v1);
   }
   double mm, gg;
   stage_gaps(tau[0], tau[1], gp[0], gp[1], &mm, &gg);
@@ -4404,7 +4435,8 @@ LexExclRegions lex_excl_regions(const DevProblem &P, int64_t O, size_t *at) {
   const size_t rows = (size_t)O * 2 * P.K * (size_t)(R.nbmax + 1);
   const size_t vbytes = sizeof(double) * rows * ((size_t)P.G + 1);
   R.fast = excl_kernel_supported(P) && lex_breaks_lds(nopt) <= kPrepGeneralLdsLimit &&
-           lex_tables_lds(nopt, PP, P.G) <= kPrepGeneralLdsLimit && vbytes <= ((size_t)4 << 30);
+           lex_tables_lds(nopt, PP, P.G) <= kPrepGeneralLdsLimit &&
+           lex_score_lds(R.nbmax, P.G / P.tp[0]) <= kPrepGeneralLdsLimit && vbytes <= ((size_t)4 << 30);
   auto take = [&](size_t bytes) {
     const size_t here = *at;
     *at = align256(*at + (bytes > 0 ? bytes : 1));
@@ -4533,9 +4565,16 @@ hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const floa
   if (tables) {
     const LexExclRegions &X = L.fast;
     const dim3 grid((unsigned)((S + kWave - 1) / kWave), (unsigned)E, (unsigned)O);
-    k_score_lex_excl<<<grid, kWave, sizeof(int) * 2 * (size_t)X.nbmax, s>>>(
+    const int32_t rmax = P.G / P.tp[0];  // the longest replica range
+    const size_t lds_s = lex_score_lds(X.nbmax, rmax);
+    if (lds_s > 64 * 1024) {
+      e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_score_lex_excl),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_s);
+      if (e != hipSuccess) return e;
+    }
+    k_score_lex_excl<<<grid, kWave, lds_s, s>>>(
         P, (const TileInfo *)(ws + L.score.tiles), (const int32_t *)(ws + L.score.mopt), excl_thresholds(P), cap_s,
-        tail_s, E, S, (const float *)(ws + X.bp), (const int32_t *)(ws + X.nbp), X.nbmax,
+        tail_s, E, S, (const float *)(ws + X.bp), (const int32_t *)(ws + X.nbp), X.nbmax, rmax,
         (const double *)(ws + X.V), (const double *)(ws + X.W), pmm, pgp, n_partial);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
