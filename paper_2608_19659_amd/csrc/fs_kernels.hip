@@ -3125,7 +3125,7 @@ __host__ __device__ inline size_t lex_breaks_lds(int nopt) {
 // layers (binary64) and one class's best served rate per cost.
 __host__ __device__ inline size_t lex_tables_lds(int nopt, int per_class_options, int G) {
   const size_t nw = kLexPrepThreads / kWave;
-  return 8 * (size_t)nopt + 8 * (size_t)per_class_options + nw * (16 * ((size_t)G + 1) + 8 * ((size_t)G + 4));
+  return 8 * (size_t)nopt + 8 * (size_t)per_class_options + nw * (16 * (2 * (size_t)G + 2) + 8 * ((size_t)G + 4));
 }
 
 // LDS of a k_score_lex_excl block: both realisations' breakpoints and M of
@@ -3266,11 +3266,14 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_tables(DevProblem P, co
   int *oratio = reinterpret_cast<int *>(lex_tab_lds);  // [nopt]
   float *oserved = reinterpret_cast<float *>(oratio + nopt);
   int2 *icost = reinterpret_cast<int2 *>(oserved + nopt);  // [PP] class i's options: cost, cell
-  double *Va = reinterpret_cast<double *>(icost + PP) + (size_t)wave * 2 * (G + 1);
-  double *Vb = Va + G + 1;
+  // per wavefront two knapsack layers, each with G + 1 entries of -inf
+  // below index 0, so that V[g - c] for a cost above the budget reads -inf
+  // (which the max ignores) instead of needing a clamp and a mask
+  double *Va = reinterpret_cast<double *>(icost + PP) + (size_t)wave * 2 * (2 * G + 2) + (G + 1);
+  double *Vb = Va + 2 * G + 2;
   // per wavefront: the costs with an allowed option and their best served
   // rates, ascending, padded to a multiple of 4
-  float *Ak = reinterpret_cast<float *>(reinterpret_cast<double *>(icost + PP) + (size_t)nw * 2 * (G + 1)) +
+  float *Ak = reinterpret_cast<float *>(reinterpret_cast<double *>(icost + PP) + (size_t)nw * 2 * (2 * G + 2)) +
               (size_t)wave * 2 * (G + 4);
   int *Ck = reinterpret_cast<int *>(Ak + G + 4);
   if (part * nw > nb) return;  // no interval for this block
@@ -3296,6 +3299,10 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_tables(DevProblem P, co
   __syncthreads();
   const double NEG = -__builtin_inf();
   const float NEGF = -__builtin_inff();
+  for (int g = lane; g <= G; g += kWave) {  // the padding below index 0, never written again
+    Va[-1 - g] = NEG;
+    Vb[-1 - g] = NEG;
+  }
   const float *bp = bp_in + ((size_t)o * 2 + R) * nbmax;
   const size_t row0 = (((size_t)o * 2 + R) * K + i) * (size_t)(nbmax + 1);
   for (int j = first; j <= nb; j += step) {
@@ -3332,7 +3339,10 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_tables(DevProblem P, co
       if (lane < 4) Ck[n_c + lane] = G + 1;  // padding: a cost no budget reaches
       wave_lds_fence();
       // V'[g] = max(V[g] if empty allowed, max over listed c <= g of A[c] + V[g - c]):
-      // the max is exact, so the order of the terms does not matter
+      // the max is exact, so the order of the terms does not matter; a
+      // listed cost above g reads the padding (-inf), and A[c] + -inf is
+      // -inf, so no term needs a mask (the list's own padding, cost G + 1,
+      // reads at most G + 1 below index 0)
       for (int top = G; top >= 0; top -= kWave) {
         const int g = top - lane;  // lanes past g = 0 compute nothing
         const int gs = g >= 0 ? g : 0;
@@ -3340,12 +3350,11 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_tables(DevProblem P, co
         for (int x = 0; x < n_c && Ck[x] <= top; x += 4) {
           const int c0 = Ck[x], c1 = Ck[x + 1], c2 = Ck[x + 2], c3 = Ck[x + 3];
           const float a0 = Ak[x], a1 = Ak[x + 1], a2 = Ak[x + 2], a3 = Ak[x + 3];
-          const double v0 = Vp[max(gs - c0, 0)], v1 = Vp[max(gs - c1, 0)], v2 = Vp[max(gs - c2, 0)],
-                       v3 = Vp[max(gs - c3, 0)];
-          best = gs >= c0 ? fmax(best, (double)a0 + v0) : best;
-          best = gs >= c1 ? fmax(best, (double)a1 + v1) : best;
-          best = gs >= c2 ? fmax(best, (double)a2 + v2) : best;
-          best = gs >= c3 ? fmax(best, (double)a3 + v3) : best;
+          const double v0 = Vp[gs - c0], v1 = Vp[gs - c1], v2 = Vp[gs - c2], v3 = Vp[gs - c3];
+          best = fmax(best, (double)a0 + v0);
+          best = fmax(best, (double)a1 + v1);
+          best = fmax(best, (double)a2 + v2);
+          best = fmax(best, (double)a3 + v3);
         }
         if (g >= 0) Vc[g] = best;
       }
