@@ -3106,6 +3106,14 @@ __global__ __launch_bounds__(64) void k_score_lex_wave(DevProblem P, const int8_
 // association does not change them.
 // ---------------------------------------------------------------------------
 constexpr int kLexPrepThreads = 256;
+// Wavefronts of the interval tables kernel in all (blocks per realisation,
+// order and class follow from it, no more than the intervals can use): a
+// wavefront walks its intervals one after another, so more and shorter-lived
+// wavefronts shorten the kernel, until they take the SIMDs from the
+// certificate solves running beside it on the second stream (on 4 classes at
+// G = 64 the whole call took 87.8, 87.0 and 88.0 us with 4096, 8192 and
+// 12288).
+constexpr int kLexTableWaves = 8192;
 
 // Keys the breakpoint sort takes: every option's ratio and the 0, padded to
 // a power of two (at least one per thread).
@@ -3121,11 +3129,18 @@ __host__ __device__ inline size_t lex_breaks_lds(int nopt) {
 }
 
 // LDS of a k_lex_tables block: every option's (ratio, served rate), the
-// candidate class's options (cost, cell), then per wavefront two knapsack
-// layers (binary64) and one class's best served rate per cost.
+// candidate class's options (cost, cell), then (from a 16-byte boundary)
+// per wavefront two knapsack layers (binary64, each with G + 1 entries of
+// padding), one class's best served rates (binary64) and its listed costs,
+// G + 8 of each rounded up to a multiple of 4.
+__host__ __device__ inline int lex_list_stride(int G) { return (G + 8 + 3) & ~3; }
+__host__ __device__ inline size_t lex_tables_head(int nopt, int per_class_options) {
+  return (8 * ((size_t)nopt + per_class_options) + 15) & ~(size_t)15;
+}
 __host__ __device__ inline size_t lex_tables_lds(int nopt, int per_class_options, int G) {
   const size_t nw = kLexPrepThreads / kWave;
-  return 8 * (size_t)nopt + 8 * (size_t)per_class_options + nw * (16 * (2 * (size_t)G + 2) + 8 * ((size_t)G + 4));
+  return lex_tables_head(nopt, per_class_options) +
+         nw * (16 * (2 * (size_t)G + 2) + 12 * (size_t)lex_list_stride(G));
 }
 
 // LDS of a k_score_lex_excl block: both realisations' breakpoints and M of
@@ -3248,13 +3263,14 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_breaks(DevProblem P, co
 // lanes over g from the top down, so each chunk loops c only up to its
 // largest g.  Blocks split the intervals of one (R, o, i) four wavefronts
 // at a time.
+template <int NTP>
 __global__ __launch_bounds__(kLexPrepThreads) void k_lex_tables(DevProblem P, const int8_t *__restrict__ bmap,
                                                                const int2 *__restrict__ opt_in,
                                                                const float *__restrict__ bp_in,
                                                                const int32_t *__restrict__ nbp, int32_t nbmax,
                                                                int32_t nsplit, double *__restrict__ Vout,
                                                                double *__restrict__ Wout) {
-  extern __shared__ double lex_tab_lds[];
+  extern __shared__ __attribute__((aligned(16))) double lex_tab_lds[];  // 16-byte reads below
   const int R = blockIdx.x & 1, part = blockIdx.x >> 1, o = blockIdx.y, i = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -3263,26 +3279,22 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_tables(DevProblem P, co
   const int nopt = K * PP;
   const int nb = nbp[o * 2 + R];
   const int first = part * nw + wave, step = nsplit * nw;
-  int *oratio = reinterpret_cast<int *>(lex_tab_lds);  // [nopt]
-  float *oserved = reinterpret_cast<float *>(oratio + nopt);
-  int2 *icost = reinterpret_cast<int2 *>(oserved + nopt);  // [PP] class i's options: cost, cell
+  int2 *oinfo = reinterpret_cast<int2 *>(lex_tab_lds);  // [nopt] ratio bits, served rate bits
+  int2 *icost = oinfo + nopt;                            // [PP] class i's options: cost, cell
   // per wavefront two knapsack layers, each with G + 1 entries of -inf
   // below index 0, so that V[g - c] for a cost above the budget reads -inf
   // (which the max ignores) instead of needing a clamp and a mask
-  double *Va = reinterpret_cast<double *>(icost + PP) + (size_t)wave * 2 * (2 * G + 2) + (G + 1);
+  double *vreg = reinterpret_cast<double *>(reinterpret_cast<char *>(lex_tab_lds) + lex_tables_head(nopt, PP));
+  double *Va = vreg + (size_t)wave * 2 * (2 * G + 2) + (G + 1);
   double *Vb = Va + 2 * G + 2;
-  // per wavefront: the costs with an allowed option and their best served
-  // rates, ascending, padded to a multiple of 4
-  float *Ak = reinterpret_cast<float *>(reinterpret_cast<double *>(icost + PP) + (size_t)nw * 2 * (2 * G + 2)) +
-              (size_t)wave * 2 * (G + 4);
-  int *Ck = reinterpret_cast<int *>(Ak + G + 4);
+  // per wavefront: the costs with an allowed option (as byte offsets into a
+  // layer) and their best served rates, ascending, then padding
+  const int LS = lex_list_stride(G);
+  double *Ad = vreg + (size_t)nw * 2 * (2 * G + 2) + (size_t)wave * LS;
+  int *Ck = reinterpret_cast<int *>(vreg + (size_t)nw * 2 * (2 * G + 2) + (size_t)nw * LS) + (size_t)wave * LS;
   if (part * nw > nb) return;  // no interval for this block
   const int2 *opt = opt_in + ((size_t)o * 2 + R) * nopt;
-  for (int q = tid; q < nopt; q += kLexPrepThreads) {
-    const int2 v = opt[q];
-    oratio[q] = v.x;
-    oserved[q] = __int_as_float(v.y);
-  }
+  for (int q = tid; q < nopt; q += kLexPrepThreads) oinfo[q] = opt[q];
   // class i's options: (cost, cell within the class; -1 when no level holds
   // it); TP decode from staged constants
   __shared__ int s_tp[kMaxTp], s_off[kMaxTp + 1];
@@ -3299,6 +3311,15 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_tables(DevProblem P, co
   __syncthreads();
   const double NEG = -__builtin_inf();
   const float NEGF = -__builtin_inff();
+  // the TP degrees, their reciprocals and option offsets in registers
+  int tpr[NTP], ofr[NTP];
+  float tpinv[NTP];
+#pragma unroll
+  for (int ti = 0; ti < NTP; ++ti) {
+    tpr[ti] = ti < NT ? P.tp[ti] : 0;
+    ofr[ti] = ti < NT ? P.optoff[ti] : 0;
+    tpinv[ti] = tpr[ti] > 0 ? 1.0f / (float)tpr[ti] : 0.0f;
+  }
   for (int g = lane; g <= G; g += kWave) {  // the padding below index 0, never written again
     Va[-1 - g] = NEG;
     Vb[-1 - g] = NEG;
@@ -3314,47 +3335,79 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_tables(DevProblem P, co
     for (int k = K - 1; k >= 0; --k) {
       if (k == i) continue;
       // A[c]: the best served rate of class k's allowed options of cost c,
-      // listed only for the costs that have one (a ballot per 64 costs)
+      // listed only for the costs that have one (a ballot per 64 costs).
+      // The options of cost c are (t, c / t) for the TP degrees t dividing
+      // c; every degree's read is issued (at option 0 when t does not
+      // divide c), so they overlap.
       int n_c = 0;
       for (int c0 = 1; c0 <= G; c0 += kWave) {
         const int c = c0 + lane;
-        float a = NEGF;
-        for (int ti = 0; ti < NT; ++ti) {
-          const int t = P.tp[ti];
-          const int r = c / t;
-          if (c <= G && r * t == c) {
-            const int q = k * PP + P.optoff[ti] + r - 1;
-            a = oratio[q] >= thr ? fmaxf(a, oserved[q]) : a;
-          }
+        int2 ov[NTP];
+        bool okv[NTP];
+#pragma unroll
+        for (int ti = 0; ti < NTP; ++ti) {
+          // c / t, exact whenever t divides c (the float quotient is within
+          // 1/2 of it for c <= 2^22)
+          const int r = (int)((float)c * tpinv[ti] + 0.5f);
+          okv[ti] = (ti < NT) & (c <= G) & (r >= 1) & (r * tpr[ti] == c);  // no short-circuit branches
+          ov[ti] = oinfo[okv[ti] ? k * PP + ofr[ti] + r - 1 : 0];
         }
+        float a = NEGF;
+#pragma unroll
+        for (int ti = 0; ti < NTP; ++ti)
+          a = okv[ti] && ov[ti].x >= thr ? fmaxf(a, __int_as_float(ov[ti].y)) : a;
         const bool has = a > NEGF;
         const uint64_t m = __builtin_amdgcn_ballot_w64(has);
         if (has) {
           const int at = n_c + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
-          Ak[at] = a;
-          Ck[at] = c;
+          Ad[at] = (double)a;
+          Ck[at] = 8 * c;
         }
         n_c += __builtin_popcountll(m);
       }
-      if (lane < 4) Ck[n_c + lane] = G + 1;  // padding: a cost no budget reaches
+      if (lane < 8) {  // padding: a cost no budget reaches
+        Ck[n_c + lane] = 8 * (G + 1);
+        Ad[n_c + lane] = 0.0;
+      }
       wave_lds_fence();
       // V'[g] = max(V[g] if empty allowed, max over listed c <= g of A[c] + V[g - c]):
-      // the max is exact, so the order of the terms does not matter; a
-      // listed cost above g reads the padding (-inf), and A[c] + -inf is
-      // -inf, so no term needs a mask (the list's own padding, cost G + 1,
-      // reads at most G + 1 below index 0)
+      // the max is exact, so the order of the terms does not matter, and a
+      // term with c > g reads the padding (-inf; A[c] + -inf is -inf), so
+      // any superset of the terms c <= g gives the same value.  A lane reads
+      // V[g - c] at its own V[g] minus c's byte offset, and the costs and
+      // rates eight at a time (16-byte reads at the same address in every
+      // lane): per term one subtraction, one addition and one maximum, and
+      // per eight terms two round trips to LDS.
       for (int top = G; top >= 0; top -= kWave) {
         const int g = top - lane;  // lanes past g = 0 compute nothing
         const int gs = g >= 0 ? g : 0;
+        const char *vg = reinterpret_cast<const char *>(Vp + gs);
         double best = empty_ok ? Vp[gs] : NEG;
-        for (int x = 0; x < n_c && Ck[x] <= top; x += 4) {
-          const int c0 = Ck[x], c1 = Ck[x + 1], c2 = Ck[x + 2], c3 = Ck[x + 3];
-          const float a0 = Ak[x], a1 = Ak[x + 1], a2 = Ak[x + 2], a3 = Ak[x + 3];
-          const double v0 = Vp[gs - c0], v1 = Vp[gs - c1], v2 = Vp[gs - c2], v3 = Vp[gs - c3];
-          best = fmax(best, (double)a0 + v0);
-          best = fmax(best, (double)a1 + v1);
-          best = fmax(best, (double)a2 + v2);
-          best = fmax(best, (double)a3 + v3);
+        // listed costs up to top: the first nuse (ascending)
+        int nuse = 0;
+        for (int xb = 0; xb < n_c; xb += kWave) {
+          const int x = xb + lane;
+          const int m = __builtin_popcountll(__builtin_amdgcn_ballot_w64(x < n_c && Ck[min(x, n_c)] <= 8 * top));
+          nuse += m;
+          if (m < kWave) break;
+        }
+        // past nuse (up to 7 entries): listed costs above top or the padding
+        // (cost G + 1, at most G + 1 below index 0), both reading -inf here
+        for (int x = 0; x < nuse; x += 8) {
+          int cq[8];
+          double aq[8], vq[8];
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int4 c4 = *reinterpret_cast<const int4 *>(Ck + x + 4 * h);
+            const double2 a01 = *reinterpret_cast<const double2 *>(Ad + x + 4 * h);
+            const double2 a23 = *reinterpret_cast<const double2 *>(Ad + x + 4 * h + 2);
+            cq[4 * h] = c4.x; cq[4 * h + 1] = c4.y; cq[4 * h + 2] = c4.z; cq[4 * h + 3] = c4.w;
+            aq[4 * h] = a01.x; aq[4 * h + 1] = a01.y; aq[4 * h + 2] = a23.x; aq[4 * h + 3] = a23.y;
+          }
+#pragma unroll
+          for (int u = 0; u < 8; ++u) vq[u] = *reinterpret_cast<const double *>(vg - cq[u]);
+#pragma unroll
+          for (int u = 0; u < 8; ++u) best = fmax(best, aq[u] + vq[u]);
         }
         if (g >= 0) Vc[g] = best;
       }
@@ -3387,8 +3440,8 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_tables(DevProblem P, co
     };
     for (int p = lane; p < PP; p += kWave) {
       const int2 ic = icost[p];
-      const int q = i * PP + p;
-      if (ic.y >= 0 && oratio[q] >= thr) merge((double)oserved[q] + Vp[G - ic.x], ic.y, NEG);
+      const int2 ov = oinfo[i * PP + p];
+      if (ic.y >= 0 && ov.x >= thr) merge((double)__int_as_float(ov.y) + Vp[G - ic.x], ic.y, NEG);
     }
 #pragma unroll
     for (int m = 1; m < kWave; m <<= 1) {
@@ -4522,7 +4575,8 @@ hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const floa
       if (e != hipSuccess) return e;
     }
     if (lds_t > 64 * 1024) {
-      e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_lex_tables),
+      e = hipFuncSetAttribute(P.NT <= 4 ? reinterpret_cast<const void *>(&k_lex_tables<4>)
+                                        : reinterpret_cast<const void *>(&k_lex_tables<8>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_t);
       if (e != hipSuccess) return e;
     }
@@ -4531,15 +4585,22 @@ hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const floa
                                                            (float *)(ws + X.bp), (int32_t *)(ws + X.nbp));
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    // blocks per (realisation, order, class): about 4096 wavefronts in all,
-    // no more than the intervals can use
+    // blocks per (realisation, order, class): about kLexTableWaves
+    // wavefronts in all, no more than the intervals can use
     const int64_t per = (int64_t)2 * O * P.K;
-    const int64_t want = (4096 / (per * (kLexPrepThreads / kWave))) + 1;
+    const int64_t want = (kLexTableWaves / (per * (kLexPrepThreads / kWave))) + 1;
     const int64_t cap_split = (X.nbmax + 1 + kLexPrepThreads / kWave - 1) / (kLexPrepThreads / kWave);
     const int nsplit = (int)(want < cap_split ? want : cap_split);
-    k_lex_tables<<<dim3(2 * nsplit, O, P.K), kLexPrepThreads, lds_t, s>>>(
-        P, (const int8_t *)(ws + L.score.bmap), (const int2 *)(ws + X.opt), (const float *)(ws + X.bp),
-        (const int32_t *)(ws + X.nbp), X.nbmax, nsplit, (double *)(ws + X.V), (double *)(ws + X.W));
+    // compiled for at most 4 or 8 TP degrees (the loop over them is unrolled)
+    if (P.NT <= 4) {
+      k_lex_tables<4><<<dim3(2 * nsplit, O, P.K), kLexPrepThreads, lds_t, s>>>(
+          P, (const int8_t *)(ws + L.score.bmap), (const int2 *)(ws + X.opt), (const float *)(ws + X.bp),
+          (const int32_t *)(ws + X.nbp), X.nbmax, nsplit, (double *)(ws + X.V), (double *)(ws + X.W));
+    } else {
+      k_lex_tables<8><<<dim3(2 * nsplit, O, P.K), kLexPrepThreads, lds_t, s>>>(
+          P, (const int8_t *)(ws + L.score.bmap), (const int2 *)(ws + X.opt), (const float *)(ws + X.bp),
+          (const int32_t *)(ws + X.nbp), X.nbmax, nsplit, (double *)(ws + X.V), (double *)(ws + X.W));
+    }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
