@@ -327,8 +327,8 @@ static fs_status lex_supported(const fs::DevProblem &P, int n_alloc) {
   const size_t need = fs::lds_bytes_lex(P, n_alloc);
   if (need > fs::kLexLdsLimit)
     return fail(FS_ERR_UNSUPPORTED, "the whole objective needs " + std::to_string(need) +
-                                        " bytes of LDS for this problem (at most 65536: about (12 + 2 K)(G + 1) "
-                                        "+ 6 x options per class + 1 KiB)");
+                                        " bytes of LDS for this problem (at most 65536: about (28 + 2 K)(G + 1) "
+                                        "+ 1 KiB)");
   return FS_OK;
 }
 

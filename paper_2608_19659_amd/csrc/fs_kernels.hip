@@ -501,9 +501,17 @@ struct StageArea {
   float *cap, *tail;
 };
 
+// p rounded up to a 16-byte boundary.  The pointer stays derived from p (an
+// offset added, not an integer turned back into a pointer), so the compiler
+// still sees LDS and emits LDS instructions rather than flat ones.
+__device__ __forceinline__ char *align16(void *p) {
+  char *c = reinterpret_cast<char *>(p);
+  return static_cast<char *>(__builtin_assume_aligned(c + ((16 - ((uintptr_t)c & 15)) & 15), 16));
+}
+
 __device__ __forceinline__ StageArea stage_area(const DevProblem &P, void *start) {
   StageArea A;
-  A.bmap = reinterpret_cast<int8_t *>(((uintptr_t)start + 15) & ~(uintptr_t)15);
+  A.bmap = reinterpret_cast<int8_t *>(align16(start));
   A.cap = reinterpret_cast<float *>(A.bmap + (((size_t)P.K * (P.G + 1) + 3) & ~(size_t)3));
   A.tail = A.cap + P.N;
   return A;
@@ -2748,13 +2756,25 @@ __global__ __launch_bounds__(64) void k_certify_state(DevProblem P, const int8_t
 // The choice of every (class, budget) is kept, and the allocation is read
 // in class order from the full budget.
 // ---------------------------------------------------------------------------
+// A budget's entry of the layer: its best goodput (-inf: no allowed
+// completion) and key = GPUs << 16 (the low 16 bits zero).
+struct alignas(16) LexCell {
+  double gp;
+  int key;
+  int pad;
+};
+
 struct LexLds {
-  double *vgp;      // [G + 1] goodput of the layer, updated in place
-  int2 *aopt;       // [G + 4] the costs with an allowed option, ascending: (served rate bits, option index)
-  int *vn;          // [G + 1] GPUs, -1 = no allowed completion
-  int *acost;       // [G + 4] their costs (padded with G + 1 to a multiple of 4)
+  LexCell *v;       // [G + 1] the layer, updated in place; v[-1] holds -inf
+  float *arate;     // [LS] the costs with an allowed option, ascending: served rate
+  int *akey;        // [LS] (cost << 16) | (option index + 1)
+  int *aoff;        // [LS] 16 x cost, the byte offset of V[g - cost] below V[g]
   int16_t *choice;  // [K][G + 1] option index, -1 = empty, -2 = none
 };
+
+// Listed-cost arrays: G costs at most and 8 entries of padding, rounded up to
+// a multiple of 4 (16-byte reads).
+__device__ __host__ inline int lex_cost_stride(int G) { return (G + 8 + 3) & ~3; }
 
 // Options of a class are numbered by TP index, then replicas:
 // q = optoff[t] + r - 1.  TP index, degree and replicas of option q.
@@ -2775,15 +2795,24 @@ __device__ __forceinline__ void option_of(const DevProblem &P, int q, int *ti, i
 // One layer suffices: V_k[g] reads V_{k+1} at budgets <= g only, so the
 // budgets are rewritten from the top down, 64 at a time (lane l takes
 // g = top - l), every lane's reads of a group before its writes.
+//
+// The preference (larger goodput, then fewer GPUs, then the earlier option,
+// the empty one first) is one comparison of the goodput and one of an
+// integer key: (GPUs << 16) | (option index + 1), 0 for the empty option,
+// which is the entry's key plus the listed cost's (GPUs and option indices
+// stay below 2^15 and 2^16).  No allowed completion is a goodput of -inf:
+// it loses to every allowed one, and a budget where nothing is allowed ends
+// with -inf (written as "none").  A term whose cost exceeds the budget reads
+// V[-1] (-inf) through a clamped offset, so no term needs a mask.
 __device__ void wave_lex_stage(const DevProblem &P, const int8_t *__restrict__ bmap, const Realisation &R,
                                int tau, int floors_met, const LexLds &X, const WaveAlloc &alloc,
                                float *goodput, double *goodput64) {
   const int lane = threadIdx.x & (kWave - 1);
   const int K = P.K, G = P.G, NT = P.NT;
-  for (int g = lane; g <= G; g += kWave) {
-    X.vgp[g] = 0.0;
-    X.vn[g] = 0;
-  }
+  const double NEG = -__builtin_inf();
+  for (int g = lane; g <= G; g += kWave) X.v[g] = LexCell{0.0, 0, 0};
+  if (lane == 0) X.v[-1] = LexCell{NEG, 0, 0};
+  const char *vbase = reinterpret_cast<const char *>(X.v);
   for (int k = K - 1; k >= 0; --k) {
     const bool restricted = P.has_floor && floors_met && (P.floor_rps[k] > 0.0f);
     const bool empty_ok = !restricted && tau <= 0;
@@ -2816,55 +2845,65 @@ __device__ void wave_lex_stage(const DevProblem &P, const int8_t *__restrict__ b
       const uint64_t m = __builtin_amdgcn_ballot_w64(bq >= 0);
       if (bq >= 0) {
         const int at = n_c + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
-        X.aopt[at] = make_int2(__float_as_int(best), bq);
-        X.acost[at] = c;
+        X.arate[at] = best;
+        X.akey[at] = (c << 16) | (bq + 1);
+        X.aoff[at] = 16 * c;
       }
       n_c += __builtin_popcountll(m);
     }
-    if (lane < 4) {
-      X.aopt[n_c + lane] = make_int2(0, -1);
-      X.acost[n_c + lane] = G + 1;  // padding: a cost no budget reaches
+    if (lane < 8) {  // padding: a cost no budget reaches
+      X.arate[n_c + lane] = 0.0f;
+      X.akey[n_c + lane] = 0;
+      X.aoff[n_c + lane] = 16 * (G + 1);
     }
     __syncthreads();
     for (int top = G; top >= 0; top -= kWave) {
       const int g = top - lane;
-      const int gs = g >= 0 ? g : 0;
-      double bgp = 0.0;
-      int bn = -1, bq = -2;
-      if (empty_ok && X.vn[gs] >= 0) {
-        bgp = X.vgp[gs];
-        bn = X.vn[gs];
-        bq = -1;
+      const int gs = g >= 0 ? g : top;  // lanes past g = 0 compute nothing (valid reads)
+      const LexCell e0 = X.v[gs];
+      double bgp = empty_ok ? e0.gp : NEG;
+      int bkey = empty_ok ? e0.key : INT_MAX;
+      // listed costs up to top: the first nuse (ascending)
+      int nuse = 0;
+      for (int xb = 0; xb < n_c; xb += kWave) {
+        const int x = xb + lane;
+        const int m = __builtin_popcountll(__builtin_amdgcn_ballot_w64(x < n_c && X.aoff[min(x, n_c)] <= 16 * top));
+        nuse += m;
+        if (m < kWave) break;
       }
-      auto take = [&](int c, int2 a, int n2, double v2) {
-        const double v = (double)__int_as_float(a.x) + v2;
-        const int vn = c + n2;
-        const bool ok = a.y >= 0 && gs >= c && n2 >= 0;
-        const bool better = bn < 0 || v > bgp || (v == bgp && (vn < bn || (vn == bn && a.y < bq)));
-        if (ok && better) {
-          bgp = v;
-          bn = vn;
-          bq = a.y;
+      // eight terms at a time (the preference is a total order, so the
+      // order of the terms does not matter); past nuse (up to 7 entries):
+      // costs above top or the padding, both reading -inf
+      const int goff = 16 * gs;
+      for (int x = 0; x < nuse; x += 8) {
+        float ra[8];
+        int ka[8], oa[8];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const float4 r4 = *reinterpret_cast<const float4 *>(X.arate + x + 4 * h);
+          const int4 k4 = *reinterpret_cast<const int4 *>(X.akey + x + 4 * h);
+          const int4 o4 = *reinterpret_cast<const int4 *>(X.aoff + x + 4 * h);
+          ra[4 * h] = r4.x; ra[4 * h + 1] = r4.y; ra[4 * h + 2] = r4.z; ra[4 * h + 3] = r4.w;
+          ka[4 * h] = k4.x; ka[4 * h + 1] = k4.y; ka[4 * h + 2] = k4.z; ka[4 * h + 3] = k4.w;
+          oa[4 * h] = o4.x; oa[4 * h + 1] = o4.y; oa[4 * h + 2] = o4.z; oa[4 * h + 3] = o4.w;
         }
-      };
-      // the listed costs, four at a time (the preference order is a total
-      // order, so the order of the terms does not matter)
-      for (int x = 0; x < n_c && X.acost[x] <= top; x += 4) {
-        const int c0 = X.acost[x], c1 = X.acost[x + 1], c2 = X.acost[x + 2], c3 = X.acost[x + 3];
-        const int2 a0 = X.aopt[x], a1 = X.aopt[x + 1], a2 = X.aopt[x + 2], a3 = X.aopt[x + 3];
-        const int i0 = max(gs - c0, 0), i1 = max(gs - c1, 0), i2 = max(gs - c2, 0), i3 = max(gs - c3, 0);
-        const int n0 = X.vn[i0], n1 = X.vn[i1], n2 = X.vn[i2], n3 = X.vn[i3];
-        const double v0 = X.vgp[i0], v1 = X.vgp[i1], v2 = X.vgp[i2], v3 = X.vgp[i3];
-        take(c0, a0, n0, v0);
-        take(c1, a1, n1, v1);
-        take(c2, a2, n2, v2);
-        take(c3, a3, n3, v3);
+        LexCell vv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) vv[u] = *reinterpret_cast<const LexCell *>(vbase + max(goff - oa[u], -16));
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const double v = (double)ra[u] + vv[u].gp;
+          const int key = ka[u] + vv[u].key;
+          const bool better = v > bgp || (v == bgp && key < bkey);
+          bgp = better ? v : bgp;
+          bkey = better ? key : bkey;
+        }
       }
       wave_lds_fence();
       if (g >= 0) {
-        X.vgp[g] = bgp;
-        X.vn[g] = bn;
-        X.choice[k * (G + 1) + g] = (int16_t)bq;
+        const bool none = bgp == NEG;
+        X.v[g] = LexCell{bgp, none ? 0 : (bkey & ~0xFFFF), 0};
+        X.choice[k * (G + 1) + g] = (int16_t)(none ? -2 : (bkey & 0xFFFF) - 1);
       }
       wave_lds_fence();
     }
@@ -2887,31 +2926,32 @@ __device__ void wave_lex_stage(const DevProblem &P, const int8_t *__restrict__ b
       alloc.replicas[k] = r_sel;
     }
     *goodput = gp;
-    *goodput64 = X.vgp[G];
+    const double top_gp = X.v[G].gp;
+    *goodput64 = top_gp == NEG ? 0.0 : top_gp;  // no allowed completion: 0
   }
   __syncthreads();
 }
 
 // Work area of a lexicographic solve, shared in turn by the max-min solver
-// (3 (G + 1) ints) and the stage: the layer, the per-cost options and the
-// choices, from an 8-byte aligned start.
+// (3 (G + 1) ints) and the stage: the layer (with v[-1]), the listed costs
+// and the choices, from a 16-byte aligned start.
 __device__ __host__ inline size_t lex_work_bytes(int K, int G) {
   const size_t g1 = (size_t)G + 1;
-  const size_t b = g1 * (sizeof(double) + sizeof(int)) + (g1 + 3) * (sizeof(int2) + sizeof(int)) +
-                   (size_t)K * g1 * sizeof(int16_t);
+  const size_t b = 16 * (g1 + 1) + 12 * (size_t)lex_cost_stride(G) + (size_t)K * g1 * sizeof(int16_t);
   const size_t solver = 3 * g1 * sizeof(int);
-  return 8 + (b > solver ? b : solver);  // 8: aligning the start
+  return 16 + (b > solver ? b : solver);  // 16: aligning the start
 }
 
 __device__ __forceinline__ LexLds lex_lds(const DevProblem &P, void *start) {
   const size_t g1 = (size_t)P.G + 1;
-  char *base = reinterpret_cast<char *>(((uintptr_t)start + 7) & ~(uintptr_t)7);
+  const int LS = lex_cost_stride(P.G);
+  char *base = align16(start);
   LexLds X;
-  X.vgp = reinterpret_cast<double *>(base);
-  X.aopt = reinterpret_cast<int2 *>(X.vgp + g1);
-  X.vn = reinterpret_cast<int *>(X.aopt + g1 + 3);
-  X.acost = X.vn + g1;
-  X.choice = reinterpret_cast<int16_t *>(X.acost + g1 + 3);
+  X.v = reinterpret_cast<LexCell *>(base) + 1;
+  X.arate = reinterpret_cast<float *>(X.v + g1);
+  X.akey = reinterpret_cast<int *>(X.arate + LS);
+  X.aoff = X.akey + LS;
+  X.choice = reinterpret_cast<int16_t *>(X.aoff + LS);
   return X;
 }
 
@@ -3035,7 +3075,7 @@ __global__ __launch_bounds__(64) void k_score_lex_wave(DevProblem P, const int8_
   const float *cm = cap_lo + off, *lm = tail_hi + off, *cp = cap_hi + off, *lp = tail_lo + off;
   if (stage) {
     char *st = reinterpret_cast<char *>(work) + lex_work_bytes(P.K, P.G);
-    int8_t *sb = reinterpret_cast<int8_t *>(((uintptr_t)st + 15) & ~(uintptr_t)15);
+    int8_t *sb = reinterpret_cast<int8_t *>(align16(st));
     float *sc = reinterpret_cast<float *>(sb + (((size_t)P.K * (P.G + 1) + 3) & ~(size_t)3));
     stage_copy_bmap(P, bmap, sb);
     stage_copy_cells(P, cm, lm, sc, sc + P.N);
