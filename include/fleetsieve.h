@@ -267,9 +267,8 @@ fs_status fs_certify(fs_context *ctx, const fs_problem *p, fs_intervals iv, int3
  * each other).  fs_solve_batch and fs_certify use levels (1)-(2) with the
  * tie-breaks fewer GPUs, then smaller TP degrees.
  *
- * Supported while the solve's LDS fits 64 KiB: about (12 + 2K)(G + 1) + 6 x
- * (options of one class) + 1 KiB (with TP {1, 2, 4, 8}: K = 4 up to
- * G = 2063, K = 16 up to G = 1166, K = 64 up to G = 425);
+ * Supported while the solve's LDS fits 64 KiB: about (28 + 2K)(G + 1) +
+ * 1 KiB (K = 4 up to G = 1787, K = 16 up to G = 1072, K = 64 up to G = 411);
  * FS_ERR_UNSUPPORTED otherwise.
  *
  * Dense batch under the whole objective: out as in fs_solve_batch (objective

@@ -533,10 +533,14 @@ __device__ __forceinline__ void stage_copy_cells(const DevProblem &P, const floa
 // ---------------------------------------------------------------------------
 // Dense batch solve: one wavefront per scenario.
 // ---------------------------------------------------------------------------
+// STAGE: inputs staged in LDS (1) or read from global memory (0), fixed at
+// compile time so that every access compiles for its own memory.
+template <int STAGE>
 __global__ __launch_bounds__(64) void k_solve_dense(DevProblem P, const int8_t *__restrict__ bmap,
                                                     const float *__restrict__ cap,
                                                     const float *__restrict__ tail, int64_t n,
-                                                    AllocOut out, int stage) {
+                                                    AllocOut out) {
+  constexpr int stage = STAGE;
   extern __shared__ int lds[];
   const int64_t j = blockIdx.x;
   if (j >= n) return;
@@ -2677,12 +2681,16 @@ __device__ __forceinline__ void write_cert_rec(CertRec *me, int K, int tau, int 
 // Certificate (Section 4.2): block (R, o) solves realisation R of order o
 // (0: conservative, 1: optimistic) and keeps its result in a record;
 // k_certify_state then forms each order's gap and state from the two.
+// STAGE: inputs staged in LDS (1) or read from global memory (0), fixed at
+// compile time so that every access compiles for its own memory.
+template <int STAGE>
 __global__ __launch_bounds__(64) void k_certify(DevProblem P, const int8_t *__restrict__ bmap,
                                                 const float *__restrict__ cap_lo,
                                                 const float *__restrict__ cap_hi,
                                                 const float *__restrict__ tail_lo,
                                                 const float *__restrict__ tail_hi, AllocOut cons, AllocOut opt,
-                                                CertRec *__restrict__ rec, int stage) {
+                                                CertRec *__restrict__ rec) {
+  constexpr int stage = STAGE;
   extern __shared__ int lds[];
   const int R = blockIdx.x, o = blockIdx.y;
   const size_t off = (size_t)o * P.N;
@@ -2956,11 +2964,14 @@ __device__ __forceinline__ LexLds lex_lds(const DevProblem &P, void *start) {
 }
 
 // Dense batch under the whole objective: one wavefront per scenario.
+// STAGE: inputs staged in LDS (1) or read from global memory (0), fixed at
+// compile time so that every access compiles for its own memory.
+template <int STAGE>
 __global__ __launch_bounds__(64) void k_solve_dense_lex(DevProblem P, const int8_t *__restrict__ bmap,
                                                         const float *__restrict__ cap,
                                                         const float *__restrict__ tail, int64_t n,
-                                                        AllocOut out, double *__restrict__ gp64_out,
-                                                        int stage) {
+                                                        AllocOut out, double *__restrict__ gp64_out) {
+  constexpr int stage = STAGE;
   extern __shared__ int lds[];
   const int64_t j = blockIdx.x;
   if (j >= n) return;
@@ -2994,12 +3005,16 @@ __global__ __launch_bounds__(64) void k_solve_dense_lex(DevProblem P, const int8
 // solves realisation R of order o (0: conservative, 1: optimistic) and
 // keeps its result in a record; k_certify_state then takes each
 // order's gaps and state from the two records.
+// STAGE: inputs staged in LDS (1) or read from global memory (0), fixed at
+// compile time so that every access compiles for its own memory.
+template <int STAGE>
 __global__ __launch_bounds__(64) void k_certify_lex(DevProblem P, const int8_t *__restrict__ bmap,
                                                     const float *__restrict__ cap_lo,
                                                     const float *__restrict__ cap_hi,
                                                     const float *__restrict__ tail_lo,
                                                     const float *__restrict__ tail_hi, AllocOut cons,
-                                                    AllocOut opt, CertRec *__restrict__ rec, int stage) {
+                                                    AllocOut opt, CertRec *__restrict__ rec) {
+  constexpr int stage = STAGE;
   extern __shared__ int lds[];
   const int R = blockIdx.x, o = blockIdx.y;
   const size_t off = (size_t)o * P.N;
@@ -3048,6 +3063,9 @@ __device__ __forceinline__ void stage_gaps(int tau_m, int tau_p, double gm, doub
   *gg = top > 0.0 ? fabs(gp - gm) / top : 0.0;
 }
 
+// STAGE: inputs staged in LDS (1) or read from global memory (0), fixed at
+// compile time so that every access compiles for its own memory.
+template <int STAGE>
 __global__ __launch_bounds__(64) void k_score_lex_wave(DevProblem P, const int8_t *__restrict__ bmap,
                                                        const CandInfo *__restrict__ info,
                                                        const float *__restrict__ cap_lo,
@@ -3058,7 +3076,8 @@ __global__ __launch_bounds__(64) void k_score_lex_wave(DevProblem P, const int8_
                                                        const float *__restrict__ cap_s,
                                                        const float *__restrict__ tail_s, int32_t E, int32_t S,
                                                        double *__restrict__ part_mm, double *__restrict__ part_gp,
-                                                       int64_t n_partial, int stage) {
+                                                       int64_t n_partial) {
+  constexpr int stage = STAGE;
   extern __shared__ int lds[];
   const int chunk = blockIdx.x, e = blockIdx.y, o = blockIdx.z;
   const int lane = threadIdx.x;
@@ -4377,8 +4396,10 @@ hipError_t launch_solve_batch(const DevProblem &P, const float *cap, const float
   if (n == 0) return hipSuccess;
   const size_t base = lds_bytes_solver(P, 1), staged = base + stage_bytes(P);
   const int stage = stage_fits(staged) ? 1 : 0;
-  k_solve_dense<<<(unsigned)n, 64, stage ? staged : base, s>>>(P, (const int8_t *)(ws + L.bmap), cap, tail, n,
-                                                               out, stage);
+  if (stage)
+    k_solve_dense<1><<<(unsigned)n, 64, staged, s>>>(P, (const int8_t *)(ws + L.bmap), cap, tail, n, out);
+  else
+    k_solve_dense<0><<<(unsigned)n, 64, base, s>>>(P, (const int8_t *)(ws + L.bmap), cap, tail, n, out);
   return hipGetLastError();
 }
 
@@ -4391,8 +4412,10 @@ hipError_t launch_solve_batch_lex(const DevProblem &P, const float *cap, const f
   if (n == 0) return hipSuccess;
   const size_t base = lds_bytes_lex(P, 1), staged = base + stage_bytes(P);
   const int stage = stage_fits(staged) ? 1 : 0;
-  k_solve_dense_lex<<<(unsigned)n, 64, stage ? staged : base, s>>>(P, (const int8_t *)(ws + L.bmap), cap, tail,
-                                                                   n, out, gp64, stage);
+  if (stage)
+    k_solve_dense_lex<1><<<(unsigned)n, 64, staged, s>>>(P, (const int8_t *)(ws + L.bmap), cap, tail, n, out, gp64);
+  else
+    k_solve_dense_lex<0><<<(unsigned)n, 64, base, s>>>(P, (const int8_t *)(ws + L.bmap), cap, tail, n, out, gp64);
   return hipGetLastError();
 }
 
@@ -4405,8 +4428,10 @@ hipError_t launch_certify_lex(const DevProblem &P, const float *cap_lo, const fl
   const int stage = stage_fits(staged) ? 1 : 0;
   CertRec *rec = (CertRec *)(ws + L.crec);
   const int8_t *bmap = (const int8_t *)(ws + L.bmap);
-  k_certify_lex<<<dim3(2, O), 64, stage ? staged : base, s>>>(P, bmap, cap_lo, cap_hi, tail_lo, tail_hi, cons, opt,
-                                                              rec, stage);
+  if (stage)
+    k_certify_lex<1><<<dim3(2, O), 64, staged, s>>>(P, bmap, cap_lo, cap_hi, tail_lo, tail_hi, cons, opt, rec);
+  else
+    k_certify_lex<0><<<dim3(2, O), 64, base, s>>>(P, bmap, cap_lo, cap_hi, tail_lo, tail_hi, cons, opt, rec);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   k_certify_state<<<O, 64, 0, s>>>(P, bmap, tail_hi, measured, eps, rec, 1, state, gap_mm, gap_gp);
@@ -4422,8 +4447,10 @@ hipError_t launch_certify(const DevProblem &P, const float *cap_lo, const float 
   const int stage = stage_fits(staged) ? 1 : 0;
   CertRec *rec = (CertRec *)(ws + L.crec);
   const int8_t *bmap = (const int8_t *)(ws + L.bmap);
-  k_certify<<<dim3(2, O), 64, stage ? staged : base, s>>>(P, bmap, cap_lo, cap_hi, tail_lo, tail_hi, cons, opt, rec,
-                                                          stage);
+  if (stage)
+    k_certify<1><<<dim3(2, O), 64, staged, s>>>(P, bmap, cap_lo, cap_hi, tail_lo, tail_hi, cons, opt, rec);
+  else
+    k_certify<0><<<dim3(2, O), 64, base, s>>>(P, bmap, cap_lo, cap_hi, tail_lo, tail_hi, cons, opt, rec);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   k_certify_state<<<O, 64, 0, s>>>(P, bmap, tail_hi, measured, eps, rec, 0, state, gap, nullptr);
@@ -4694,9 +4721,12 @@ hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const floa
     e = wait_mid();
     if (e != hipSuccess) return e;
     const dim3 grid((unsigned)((S + kWave - 1) / kWave), (unsigned)E, (unsigned)O);
-    k_score_lex_wave<<<grid, 64, stage ? staged : base, s>>>(P, (const int8_t *)(ws + L.score.bmap), info, cap_lo,
-                                                             cap_hi, tail_lo, tail_hi, measured, cap_s, tail_s, E,
-                                                             S, pmm, pgp, n_partial, stage);
+    if (stage)
+      k_score_lex_wave<1><<<grid, 64, staged, s>>>(P, (const int8_t *)(ws + L.score.bmap), info, cap_lo, cap_hi,
+          tail_lo, tail_hi, measured, cap_s, tail_s, E, S, pmm, pgp, n_partial);
+    else
+      k_score_lex_wave<0><<<grid, 64, base, s>>>(P, (const int8_t *)(ws + L.score.bmap), info, cap_lo, cap_hi,
+          tail_lo, tail_hi, measured, cap_s, tail_s, E, S, pmm, pgp, n_partial);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
