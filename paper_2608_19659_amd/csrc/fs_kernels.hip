@@ -3170,9 +3170,9 @@ constexpr int kLexPrepThreads = 256;
 // wavefront walks its intervals one after another, so more and shorter-lived
 // wavefronts shorten the kernel, until they take the SIMDs from the
 // certificate solves running beside it on the second stream (on 4 classes at
-// G = 64 the whole call took 87.8, 87.0 and 88.0 us with 4096, 8192 and
-// 12288).
-constexpr int kLexTableWaves = 8192;
+// G = 64 the whole call took 86.1-86.2, 81.8-83.8 and 83.4 us with 8192,
+// 12288 and 16384).
+constexpr int kLexTableWaves = 12288;
 
 // Keys the breakpoint sort takes: every option's ratio and the 0, padded to
 // a power of two (at least one per thread).
