@@ -571,17 +571,18 @@ def lex_bench(args):
     ws = ctx.workspace(fs.workspace_size(p))
     stream = torch.cuda.current_stream()
 
-    def timed(fn):
+    def timed(fn, steps=None):
+        steps = steps or args.steps
         for _ in range(args.warmup):
             r = fn()
         ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         ev0.record(stream)
-        for _ in range(args.steps):
+        for _ in range(steps):
             r = fn()
         ev1.record(stream)
         torch.cuda.synchronize()
-        return r, ev0.elapsed_time(ev1) / args.steps
+        return r, ev0.elapsed_time(ev1) / steps
 
     r_lex, ms_lex = timed(lambda: fs.solve_batch_lex(ctx, p, cap, tail, stream=stream, workspace=ws))
     _, ms_mm = timed(lambda: fs.solve_batch(ctx, p, cap, tail, stream=stream, workspace=ws))
@@ -598,12 +599,14 @@ def lex_bench(args):
     # calls marshalled once (a plain call re-marshals its arguments in Python
     # every time, which takes about as long as the GPU work here)
     lex_plan = fs.ScoreLexPlan(ctx, p, div, cand_d, cs_d, ts_d, stream=stream, workspace=wsl)
-    _, ms_sl = timed(lex_plan.run)
+    # calls of about 0.1 ms: at least 200 of them per timing
+    n_short = max(args.steps, 200)
+    _, ms_sl = timed(lex_plan.run, n_short)
     ctx.set_score_kernel(1)
     _, ms_full = timed(lex_plan.run)
     ctx.set_score_kernel(0)
     mm_plan = fs.ScorePlan(ctx, p, div, cand_d, cs_d, ts_d, stream=stream)
-    _, ms_sm = timed(mm_plan.run)
+    _, ms_sm = timed(mm_plan.run, n_short)
     live = int((~ws_full.intervals.measured[:, ws_full.cand].astype(bool)).sum()) * Sx
     slots = lex_work_per_scenario(p)
     achieved = slots * n / (ms_lex / 1e3)
@@ -631,7 +634,7 @@ def lex_bench(args):
                                f"{n} point realisations drawn inside its intervals",
                    "parallelism": "single GPU"},
         "maxmin_only": {"value": n / (ms_mm / 1e3), "ms_per_step": ms_mm},
-        "stagewise_score": {"samples": Sx, "scenarios_per_call": live, "ms_per_call": ms_sl,
+        "stagewise_score": {"samples": Sx, "scenarios_per_call": live, "calls_timed": n_short, "ms_per_call": ms_sl,
                             "value": live / (ms_sl / 1e3), "unit": "scenarios/s",
                             "full_solves_ms_per_call": ms_full, "maxmin_score_ms_per_call": ms_sm},
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_OPS / 1e12, "unit": "TOP/s",
