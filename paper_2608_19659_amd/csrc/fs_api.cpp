@@ -31,7 +31,7 @@ struct fs_context {
   // a second stream (default priority) and the fork / join events of the
   // stage-wise score
   hipStream_t side;
-  hipEvent_t fork, mid, join;
+  hipEvent_t fork, join;
   struct Timed {
     hipEvent_t begin, end;
     int launches;
@@ -171,19 +171,17 @@ fs_status fs_context_create(int hip_device, fs_context **out) {
   }
   // the stage-wise score's second stream and its fork / join events
   hipStream_t side = nullptr;
-  hipEvent_t fork = nullptr, mid = nullptr, join = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
   e = hipStreamCreateWithFlags(&side, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&fork, hipEventDisableTiming);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&mid, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&join, hipEventDisableTiming);
   if (e != hipSuccess) {
     if (fork) (void)hipEventDestroy(fork);
-    if (mid) (void)hipEventDestroy(mid);
     if (side) (void)hipStreamDestroy(side);
     (void)hipHostFree(pinned);
     return hip_fail(e, "second stream of the stage-wise score");
   }
-  *out = new fs_context{hip_device, 0, 0, 0, 0, 0, 0, 0, 0, pinned, scratch, side, fork, mid, join, {}};
+  *out = new fs_context{hip_device, 0, 0, 0, 0, 0, 0, 0, 0, pinned, scratch, side, fork, join, {}};
   return FS_OK;
 }
 
@@ -191,7 +189,6 @@ void fs_context_destroy(fs_context *ctx) {
   if (!ctx) return;
   if (ctx->pinned) (void)hipHostFree(ctx->pinned);
   if (ctx->fork) (void)hipEventDestroy(ctx->fork);
-  if (ctx->mid) (void)hipEventDestroy(ctx->mid);
   if (ctx->join) (void)hipEventDestroy(ctx->join);
   if (ctx->side) (void)hipStreamDestroy(ctx->side);
   for (auto &ev : ctx->events) {
@@ -408,15 +405,13 @@ fs_status fs_score_candidates_lex(fs_context *ctx, const fs_problem *p, fs_inter
   DeviceGuard dg(ctx->device);
   if (dg.err != hipSuccess) return hip_fail(dg.err, "hipSetDevice");
   uint8_t *ws = (uint8_t *)d_workspace;
-  // the bucket map here; the candidate records inside, on the second stream
-  hipError_t e = fs::launch_setup(P, d_cand, 0, ws, L.score, stream);
-  // the goodput stage without full solves unless scoring kernel 1 (full
-  // solves) is asked for
-  if (e == hipSuccess)
-    e = fs::launch_score_lex(P, iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi, iv.measured, d_cand, d_cap_s,
-                             d_tail_s, n_orders, n_cand, S, d_score_maxmin, d_score_goodput, d_gap_maxmin,
-                             d_gap_goodput, d_best, ws, L, ctx->score_kernel != 1, stream, ctx->side, ctx->fork,
-                             ctx->mid, ctx->join, true);
+  // the bucket map and the candidate records in the call's first launch; the
+  // goodput stage without full solves unless scoring kernel 1 (full solves)
+  // is asked for
+  hipError_t e = fs::launch_score_lex(P, iv.cap_lo, iv.cap_hi, iv.tail_lo, iv.tail_hi, iv.measured, d_cand, d_cap_s,
+                                      d_tail_s, n_orders, n_cand, S, d_score_maxmin, d_score_goodput, d_gap_maxmin,
+                                      d_gap_goodput, d_best, ws, L, ctx->score_kernel != 1, true, stream, ctx->side,
+                                      ctx->fork, ctx->join);
   if (e != hipSuccess) return hip_fail(e, "stage-wise score launch");
   return FS_OK;
 }
@@ -731,7 +726,7 @@ fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv,
         XL.fast = LL.lex_fast;
         e = fs::launch_score_lex(P, R_cap_lo, D.cap_hi, R_tail_lo, R_tail_hi, D.measured, d_cand, cs, ts, n_orders,
                                  n_cand, S, D.score, (double *)(ws + LL.scores_gp), nullptr, nullptr, D.best, ws, XL,
-                                 ctx->score_kernel != 1, stream);
+                                 ctx->score_kernel != 1, false, stream);
       } else {
         fs::ScoreArgs a{R_cap_lo, D.cap_hi, R_tail_lo, R_tail_hi, D.measured, d_cand, cs, ts,
                         n_orders, n_cand, S, D.score, D.gap_now, D.best, nullptr, ws, LL.score, kernel,

@@ -139,7 +139,7 @@ hipError_t launch_solve_batch_lex(const DevProblem &P, const float *cap, const f
 hipError_t launch_certify_lex(const DevProblem &P, const float *cap_lo, const float *cap_hi, const float *tail_lo,
                               const float *tail_hi, const uint8_t *measured, int32_t O, float eps, int32_t *state,
                               AllocOut cons, AllocOut opt, double *gap_mm, double *gap_gp, uint8_t *ws,
-                              const WsLayout &L, hipStream_t s);
+                              const WsLayout &L, hipStream_t s, bool with_state = true);
 hipError_t launch_certify(const DevProblem &P, const float *cap_lo, const float *cap_hi,
                           const float *tail_lo, const float *tail_hi, const uint8_t *measured,
                           int32_t O, float eps, int32_t *state, AllocOut cons, AllocOut opt,
@@ -201,14 +201,16 @@ struct LexScoreLayout {
 };
 LexScoreLayout lex_score_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S);
 // fast: the goodput stage without full solves where the layout has it (else
-// every scenario is solved in full, as with fast = 0).
+// every scenario is solved in full, as with fast = 0).  setup_here: build the
+// bucket map and the candidate records in the call's first launch (else
+// they are in the workspace already).  side, fork, join: a second stream
+// and two events for the certificate solves (all three, or none).
 hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const float *cap_hi, const float *tail_lo,
                             const float *tail_hi, const uint8_t *measured, const int32_t *cand, const float *cap_s,
                             const float *tail_s, int32_t O, int32_t E, int32_t S, double *score_mm,
                             double *score_gp, double *gap_mm, double *gap_gp, int32_t *best, uint8_t *ws,
-                            const LexScoreLayout &L, int fast, hipStream_t s, hipStream_t side = nullptr,
-                            hipEvent_t fork = nullptr, hipEvent_t mid = nullptr, hipEvent_t join = nullptr,
-                            bool cand_here = false);
+                            const LexScoreLayout &L, int fast, bool setup_here, hipStream_t s,
+                            hipStream_t side = nullptr, hipEvent_t fork = nullptr, hipEvent_t join = nullptr);
 
 // Interval refit and sample clamping (Algorithm 1's fit step).  The refit
 // outputs may alias its inputs.

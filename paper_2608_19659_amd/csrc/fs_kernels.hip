@@ -197,12 +197,19 @@ __device__ __forceinline__ int cell_of(const DevProblem &P, int k, int ti, int b
 // ---------------------------------------------------------------------------
 // Load level of r replicas of class k: the offered load per replica is
 // lambda_k / r in binary32, and the replica runs in the smallest level that
-// is at least that load; -1 when no level is large enough.
+// is at least that load; -1 when no level is large enough.  level_from takes
+// the per-replica load; its loop runs over the largest level count, so the
+// levels (kernel arguments) come in a few wide scalar loads rather than one
+// per compare.
+__device__ __forceinline__ int level_from(const DevProblem &P, float per_replica) {
+  int b = -1;
+#pragma unroll
+  for (int j = kMaxLevels - 1; j >= 0; --j) b = (j < P.B && per_replica <= P.levels[j]) ? j : b;
+  return b;
+}
+
 __device__ __forceinline__ int level_of(const DevProblem &P, int k, int r) {
-  const float per_replica = P.demand[k] / (float)r;
-  for (int j = 0; j < P.B; ++j)
-    if (per_replica <= P.levels[j]) return j;
-  return -1;
+  return level_from(P, P.demand[k] / (float)r);
 }
 
 // Number of load levels below a per-replica load: the index of the smallest
@@ -230,41 +237,13 @@ __device__ __forceinline__ void stage_u8(uint8_t *__restrict__ dst, const uint8_
   }
 }
 
-__global__ void k_setup_bucket(DevProblem P, int8_t *__restrict__ bmap) {
-  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+// Bucket map entry idx = k (G + 1) + r: the load level of r replicas of
+// class k (-1 for r = 0).
+__device__ __forceinline__ void setup_bucket_at(const DevProblem &P, int8_t *__restrict__ bmap, int idx) {
   const int n = P.K * (P.G + 1);
   if (idx >= n) return;
   const int k = idx / (P.G + 1), r = idx % (P.G + 1);
   bmap[idx] = (int8_t)(r >= 1 ? level_of(P, k, r) : -1);
-}
-
-__global__ void k_setup_cand(DevProblem P, const int32_t *__restrict__ cand, int32_t E,
-                             const int8_t *__restrict__ bmap, CandInfo *__restrict__ info) {
-  const int e = blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= E) return;
-  const int cell = cand[e];
-  CandInfo ci;
-  ci.cell = cell;
-  ci.pad0 = ci.pad1 = 0;
-  if (cell < 0 || cell >= P.N) {
-    ci.cls = -1; ci.ti = 0; ci.rlo = 1; ci.rhi = 0; ci.tp = 0;
-    info[e] = ci;
-    return;
-  }
-  const int b = cell % P.B;
-  const int ti = (cell / P.B) % P.NT;
-  const int k = cell / (P.B * P.NT);
-  const int t = P.tp[ti];
-  int rlo = 1, rhi = 0;
-  bool seen = false;
-  for (int r = 1; t * r <= P.G; ++r) {
-    if (bmap[k * (P.G + 1) + r] == b) {
-      if (!seen) { rlo = r; seen = true; }
-      rhi = r;
-    }
-  }
-  ci.cls = k; ci.ti = ti; ci.rlo = rlo; ci.rhi = rhi; ci.tp = t;
-  info[e] = ci;
 }
 
 // Z[g] = max_{a <= g} min(X[g - a], Y[a]) for nondecreasing X and Y.  The
@@ -1016,6 +995,32 @@ __device__ __forceinline__ void cell_range(const DevProblem &P, int cell, int *r
   const float demand = P.demand[k], lb = P.levels[b], lb1 = P.levels[b > 0 ? b - 1 : 0];
   *rlo = first_r_at_most(demand, lb, rmax);
   *rhi = b == 0 ? rmax : first_r_at_most(demand, lb1, rmax) - 1;
+}
+
+// Candidate record e: class, TP index and degree, and the replica range
+// whose load level is the cell's (1, 0 when none; by bisection, from the
+// problem alone, so that it does not wait for the bucket map).
+__device__ __forceinline__ void setup_cand_at(const DevProblem &P, const int32_t *__restrict__ cand, int32_t E,
+                                              CandInfo *__restrict__ info, int e) {
+  if (e >= E) return;
+  const int cell = cand[e];
+  CandInfo ci;
+  ci.cell = cell;
+  ci.pad0 = ci.pad1 = 0;
+  if (cell < 0 || cell >= P.N) {
+    ci.cls = -1; ci.ti = 0; ci.rlo = 1; ci.rhi = 0; ci.tp = 0;
+    info[e] = ci;
+    return;
+  }
+  const int ti = (cell / P.B) % P.NT;
+  int rlo, rhi;
+  cell_range(P, cell, &rlo, &rhi);
+  if (rlo > rhi) {
+    rlo = 1;
+    rhi = 0;
+  }
+  ci.cls = cell / (P.B * P.NT); ci.ti = ti; ci.rlo = rlo; ci.rhi = rhi; ci.tp = P.tp[ti];
+  info[e] = ci;
 }
 
 // The scorer's work list (built by one extra block of the set-up): every
@@ -3208,21 +3213,20 @@ __host__ __device__ inline size_t lex_score_lds(int nbmax, int rmax) {
   return sizeof(int) * (2 * (size_t)nbmax + 2 * (size_t)rmax);
 }
 
-// Per (realisation R, order o): every option of every class (ratio bits, -1
-// when no load level holds it; served rate) to opt_out, and the sorted
-// distinct ratios, 0 always among them, to bp_out (nb of them to nbp).
-// The ratios are sorted by a bitonic network in LDS, then each first
-// occurrence is placed by a block-wide count of the ones before it.
-__global__ __launch_bounds__(kLexPrepThreads) void k_lex_breaks(DevProblem P, const int8_t *__restrict__ bmap,
-                                                               const float *__restrict__ cap_lo,
-                                                               const float *__restrict__ cap_hi,
-                                                               const float *__restrict__ tail_lo,
-                                                               const float *__restrict__ tail_hi, int32_t nbmax,
-                                                               int2 *__restrict__ opt_out, float *__restrict__ bp_out,
-                                                               int32_t *__restrict__ nbp) {
+// Per (realisation R, order o), one block of kLexPrepThreads threads: every
+// option of every class (ratio bits, -1 when no load level holds it; served
+// rate) to opt_out, and the sorted distinct ratios, 0 always among them, to
+// bp_out (nb of them to nbp).  The ratios are sorted by a bitonic network in
+// LDS, then each first occurrence is placed by a block-wide count of the
+// ones before it.  Load levels come from the problem (the bucket map's
+// values), so the block does not wait for the map.
+__device__ void lex_breaks_block(const DevProblem &P, int R, int o, const float *__restrict__ cap_lo,
+                                 const float *__restrict__ cap_hi, const float *__restrict__ tail_lo,
+                                 const float *__restrict__ tail_hi, int32_t nbmax, int2 *__restrict__ opt_out,
+                                 float *__restrict__ bp_out, int32_t *__restrict__ nbp) {
   extern __shared__ int lex_keys[];
-  const int R = blockIdx.x, o = blockIdx.y, tid = threadIdx.x;
-  const int K = P.K, G = P.G, N = P.N, B = P.B, NT = P.NT, per_class = NT * B, PP = P.optoff[NT];
+  const int tid = threadIdx.x;
+  const int K = P.K, N = P.N, B = P.B, NT = P.NT, per_class = NT * B, PP = P.optoff[NT];
   const int nopt = K * PP, n2 = lex_sort_keys(nopt);
   int *cnt = lex_keys + n2;
   const size_t off = (size_t)o * N;
@@ -3248,7 +3252,7 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_breaks(DevProblem P, co
       int ti = 0;
       while (ti + 1 < NT && p >= s_off[ti + 1]) ++ti;
       const int r = p - s_off[ti] + 1;
-      const int b = bmap[k * (G + 1) + r];
+      const int b = level_from(P, s_dm[k] / (float)r);  // level_of with the staged demand
       int f = -1;
       float sv = 0.0f;
       if (b >= 0) {
@@ -3308,6 +3312,33 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_breaks(DevProblem P, co
     if (v != INT_MAX && (a == 0 || lex_keys[a - 1] != v)) bp[before++] = __int_as_float(v);
   }
   if (tid == 0) nbp[o * 2 + R] = total;
+}
+
+// A call's set-up in one launch of kLexPrepThreads-thread blocks: blocks
+// [0, nb) the bucket map (one entry per thread), [nb, nb + nc) the candidate
+// records (one per thread), then n_br blocks of option ratios and
+// breakpoints, block 2 o + R for realisation R of order o.  The parts are
+// independent: each takes the load levels from the problem.
+__global__ __launch_bounds__(kLexPrepThreads) void k_setup(DevProblem P, int8_t *__restrict__ bmap, int32_t nb,
+                                                          const int32_t *__restrict__ cand, int32_t E,
+                                                          CandInfo *__restrict__ info, int32_t nc,
+                                                          const float *__restrict__ cap_lo,
+                                                          const float *__restrict__ cap_hi,
+                                                          const float *__restrict__ tail_lo,
+                                                          const float *__restrict__ tail_hi, int32_t nbmax,
+                                                          int2 *__restrict__ opt_out, float *__restrict__ bp_out,
+                                                          int32_t *__restrict__ nbp) {
+  const int b = blockIdx.x;
+  if (b < nb) {
+    setup_bucket_at(P, bmap, b * kLexPrepThreads + (int)threadIdx.x);
+    return;
+  }
+  if (b < nb + nc) {
+    setup_cand_at(P, cand, E, info, (b - nb) * kLexPrepThreads + (int)threadIdx.x);
+    return;
+  }
+  const int z = b - nb - nc;
+  lex_breaks_block(P, z & 1, z >> 1, cap_lo, cap_hi, tail_lo, tail_hi, nbmax, opt_out, bp_out, nbp);
 }
 
 // Per (realisation R, order o, class i) and interval j of the breakpoints
@@ -3646,16 +3677,29 @@ __device__ __forceinline__ bool better_lex(const PickLex &a, const PickLex &b) {
 }
 
 // Scores of both stages and the lexicographic argmax: one wavefront per
-// order, lanes over the candidates, then a shuffle reduction.
+// order, lanes over the candidates, then a shuffle reduction.  First the
+// order's current gaps from its two certificate records (the max-min gap
+// tau+ - tau-, the goodput gap |gp+ - gp-| / max(gp+, gp-), 0 when both are
+// 0), written to gap_mm_out and gap_gp_out.
 __global__ __launch_bounds__(64) void k_finalize_lex(DevProblem P, const CandInfo *__restrict__ info,
                                                      const uint8_t *__restrict__ measured, int32_t E, int32_t S,
-                                                     const double *__restrict__ gap_mm,
-                                                     const double *__restrict__ gap_gp,
+                                                     const CertRec *__restrict__ rec,
+                                                     double *__restrict__ gap_mm_out,
+                                                     double *__restrict__ gap_gp_out,
                                                      const double *__restrict__ part_mm,
                                                      const double *__restrict__ part_gp, int64_t n_partial,
                                                      double *__restrict__ score_mm, double *__restrict__ score_gp,
                                                      int32_t *__restrict__ best) {
   const int o = blockIdx.x, lane = threadIdx.x;
+  const CertRec *rm = rec + (size_t)o * 2, *rp = rm + 1;
+  const double g_mm = (double)__int_as_float(rp->tau) - (double)__int_as_float(rm->tau);
+  const double g64_m = rm->goodput64, g64_p = rp->goodput64;
+  const double g_top = g64_p > g64_m ? g64_p : g64_m;
+  const double g_gp = g_top > 0.0 ? fabs(g64_p - g64_m) / g_top : 0.0;
+  if (lane == 0) {
+    gap_mm_out[o] = g_mm;
+    gap_gp_out[o] = g_gp;
+  }
   PickLex mine{0.0, 0.0, 0, 0, -1};
   for (int e = lane; e < E; e += kWave) {
     const CandInfo ci = info[e];
@@ -3668,8 +3712,8 @@ __global__ __launch_bounds__(64) void k_finalize_lex(DevProblem P, const CandInf
       score_mm[tile] = score_gp[tile] = 0.0;
       continue;
     }
-    const double smm = gap_mm[o] - partial_tree(part_mm + tile * n_partial, n_partial) / (double)S;
-    const double sgp = gap_gp[o] - partial_tree(part_gp + tile * n_partial, n_partial) / (double)S;
+    const double smm = g_mm - partial_tree(part_mm + tile * n_partial, n_partial) / (double)S;
+    const double sgp = g_gp - partial_tree(part_gp + tile * n_partial, n_partial) / (double)S;
     score_mm[tile] = smm;
     score_gp[tile] = sgp;
     const PickLex c{smm, sgp, ci.tp, ci.cell, e};
@@ -4171,14 +4215,17 @@ WsLayout ws_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
   return L;
 }
 
+// Blocks of k_setup for the bucket map and for E candidate records.
+static int setup_bucket_blocks(const DevProblem &P) {
+  return (P.K * (P.G + 1) + kLexPrepThreads - 1) / kLexPrepThreads;
+}
+static int setup_cand_blocks(int32_t E) { return E > 0 ? (E + kLexPrepThreads - 1) / kLexPrepThreads : 0; }
+
 hipError_t launch_setup(const DevProblem &P, const int32_t *cand, int32_t E, uint8_t *ws,
                         const WsLayout &L, hipStream_t s) {
-  const int n = P.K * (P.G + 1);
-  k_setup_bucket<<<(n + 255) / 256, 256, 0, s>>>(P, (int8_t *)(ws + L.bmap));
-  if (E > 0) {
-    k_setup_cand<<<(E + 255) / 256, 256, 0, s>>>(P, cand, E, (const int8_t *)(ws + L.bmap),
-                                                (CandInfo *)(ws + L.cand));
-  }
+  const int nb = setup_bucket_blocks(P), nc = setup_cand_blocks(E);
+  k_setup<<<nb + nc, kLexPrepThreads, 0, s>>>(P, (int8_t *)(ws + L.bmap), nb, cand, E, (CandInfo *)(ws + L.cand), nc,
+                                              nullptr, nullptr, nullptr, nullptr, 0, nullptr, nullptr, nullptr);
   return hipGetLastError();
 }
 
@@ -4422,7 +4469,7 @@ hipError_t launch_solve_batch_lex(const DevProblem &P, const float *cap, const f
 hipError_t launch_certify_lex(const DevProblem &P, const float *cap_lo, const float *cap_hi, const float *tail_lo,
                               const float *tail_hi, const uint8_t *measured, int32_t O, float eps, int32_t *state,
                               AllocOut cons, AllocOut opt, double *gap_mm, double *gap_gp, uint8_t *ws,
-                              const WsLayout &L, hipStream_t s) {
+                              const WsLayout &L, hipStream_t s, bool with_state) {
   if (O == 0) return hipSuccess;
   const size_t base = lds_bytes_lex(P, 1), staged = base + stage_bytes(P);
   const int stage = stage_fits(staged) ? 1 : 0;
@@ -4433,7 +4480,7 @@ hipError_t launch_certify_lex(const DevProblem &P, const float *cap_lo, const fl
   else
     k_certify_lex<0><<<dim3(2, O), 64, base, s>>>(P, bmap, cap_lo, cap_hi, tail_lo, tail_hi, cons, opt, rec);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || !with_state) return e;
   k_certify_state<<<O, 64, 0, s>>>(P, bmap, tail_hi, measured, eps, rec, 1, state, gap_mm, gap_gp);
   return hipGetLastError();
 }
@@ -4602,26 +4649,46 @@ hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const floa
                             const float *tail_hi, const uint8_t *measured, const int32_t *cand, const float *cap_s,
                             const float *tail_s, int32_t O, int32_t E, int32_t S, double *score_mm,
                             double *score_gp, double *gap_mm, double *gap_gp, int32_t *best, uint8_t *ws,
-                            const LexScoreLayout &L, int fast, hipStream_t s, hipStream_t side,
-                            hipEvent_t fork, hipEvent_t mid, hipEvent_t join, bool cand_here) {
+                            const LexScoreLayout &L, int fast, bool setup_here, hipStream_t s, hipStream_t side,
+                            hipEvent_t fork, hipEvent_t join) {
   if (O == 0) return hipSuccess;
   double *gmm = gap_mm ? gap_mm : (double *)(ws + L.gap_mm);
   double *ggp = gap_gp ? gap_gp : (double *)(ws + L.gap_gp);
   const AllocOut none{nullptr, nullptr, nullptr, nullptr, nullptr};
-  // Two chains after the bucket map.  The main stream builds the max-min
-  // stage's set-up (U, M of every option) and the goodput stage's tables
-  // (when the goodput stage uses them); the second stream, when there is
-  // one, takes the candidate records (with cand_here) and the orders' own
-  // stages (the certificate solves: a few wavefronts, bound by their
-  // latency).  The scenarios of the full-solve path wait for the records
-  // (mid), the finalize for all of the second chain (join): each wait
-  // between streams costs the host about as much as two launches.  The two
-  // chains write disjoint workspace regions.  The main chain is enqueued
-  // first, so that its kernels start while the host enqueues the other.
-  const bool par = side && fork && mid && join;
+  // One set-up launch (with setup_here the bucket map and the candidate
+  // records; with the tables every order's option ratios and breakpoints),
+  // then two chains.  The main stream builds the max-min stage's set-up (U, M
+  // of every option), the goodput stage's tables and the scenarios; the
+  // second stream, when there is one, solves the orders' own two
+  // realisations (the certificate solves: a few wavefronts, bound by their
+  // latency) into records, which the finalize turns into the current gaps.
+  // The finalize waits for the second chain (join); a wait between streams
+  // costs the host about as much as two launches.  The two chains write
+  // disjoint workspace regions.  The main chain's set-up and tables are
+  // enqueued first, so that they run while the host enqueues the rest.
+  const bool par = side && fork && join;
   hipStream_t cs = par ? side : s;
   const bool tables = S > 0 && fast && L.fast.fast && E > 0;
+  const LexExclRegions &X = L.fast;
+  const int nopt = P.K * P.optoff[P.NT];
   hipError_t e = hipSuccess;
+  {
+    const int nb = setup_here ? setup_bucket_blocks(P) : 0, nc = setup_here ? setup_cand_blocks(E) : 0;
+    const int nbr = tables ? 2 * O : 0;
+    const size_t lds_b = nbr > 0 ? lex_breaks_lds(nopt) : 0;
+    if (lds_b > 64 * 1024) {
+      e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_setup), hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)lds_b);
+      if (e != hipSuccess) return e;
+    }
+    if (nb + nc + nbr > 0) {
+      k_setup<<<nb + nc + nbr, kLexPrepThreads, lds_b, s>>>(
+          P, (int8_t *)(ws + L.score.bmap), nb, cand, E, (CandInfo *)(ws + L.score.cand), nc, cap_lo, cap_hi,
+          tail_lo, tail_hi, X.nbmax, (int2 *)(ws + X.opt), (float *)(ws + X.bp), (int32_t *)(ws + X.nbp));
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+  }
   if (par) {
     e = hipEventRecord(fork, s);
     if (e != hipSuccess) return e;
@@ -4633,25 +4700,13 @@ hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const floa
     a.ws = ws; a.L = L.score; a.kernel = 3;
     e = launch_excl_setup(P, a, s);
     if (e != hipSuccess) return e;
-    const LexExclRegions &X = L.fast;
-    const int nopt = P.K * P.optoff[P.NT];
-    const size_t lds_b = lex_breaks_lds(nopt), lds_t = lex_tables_lds(nopt, P.optoff[P.NT], P.G);
-    if (lds_b > 64 * 1024) {
-      e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_lex_breaks),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_b);
-      if (e != hipSuccess) return e;
-    }
+    const size_t lds_t = lex_tables_lds(nopt, P.optoff[P.NT], P.G);
     if (lds_t > 64 * 1024) {
       e = hipFuncSetAttribute(P.NT <= 4 ? reinterpret_cast<const void *>(&k_lex_tables<4>)
                                         : reinterpret_cast<const void *>(&k_lex_tables<8>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_t);
       if (e != hipSuccess) return e;
     }
-    k_lex_breaks<<<dim3(2, O), kLexPrepThreads, lds_b, s>>>(P, (const int8_t *)(ws + L.score.bmap), cap_lo, cap_hi,
-                                                           tail_lo, tail_hi, X.nbmax, (int2 *)(ws + X.opt),
-                                                           (float *)(ws + X.bp), (int32_t *)(ws + X.nbp));
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
     // blocks per (realisation, order, class): about kLexTableWaves
     // wavefronts in all, no more than the intervals can use
     const int64_t per = (int64_t)2 * O * P.K;
@@ -4671,36 +4726,22 @@ hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const floa
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  // the second chain
+  // the second chain: the certificate records only (the finalize forms the gaps)
   if (par) {
     e = hipStreamWaitEvent(side, fork, 0);
     if (e != hipSuccess) return e;
   }
-  if (cand_here && E > 0) {
-    k_setup_cand<<<(E + 255) / 256, 256, 0, cs>>>(P, cand, E, (const int8_t *)(ws + L.score.bmap),
-                                                  (CandInfo *)(ws + L.score.cand));
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  if (par && !tables) {
-    e = hipEventRecord(mid, side);
-    if (e != hipSuccess) return e;
-  }
   e = launch_certify_lex(P, cap_lo, cap_hi, tail_lo, tail_hi, measured, O, 0.0f, (int32_t *)(ws + L.state), none,
-                         none, gmm, ggp, ws, L.score, cs);
+                         none, gmm, ggp, ws, L.score, cs, false);
   if (e != hipSuccess) return e;
   if (par) {
     e = hipEventRecord(join, side);
     if (e != hipSuccess) return e;
   }
-  auto wait_mid = [&]() { return par ? hipStreamWaitEvent(s, mid, 0) : hipSuccess; };
-  auto joined = [&]() { return par ? hipStreamWaitEvent(s, join, 0) : hipSuccess; };
-  if (E == 0) return joined();
   const int64_t n_partial = L.score.n_partial;
   double *pmm = (double *)(ws + L.score.partial), *pgp = (double *)(ws + L.part_gp);
   const CandInfo *info = (const CandInfo *)(ws + L.score.cand);
   if (tables) {
-    const LexExclRegions &X = L.fast;
     const dim3 grid((unsigned)((S + kWave - 1) / kWave), (unsigned)E, (unsigned)O);
     const int32_t rmax = P.G / P.tp[0];  // the longest replica range
     const size_t lds_s = lex_score_lds(X.nbmax, rmax);
@@ -4715,11 +4756,9 @@ hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const floa
         (const double *)(ws + X.V), (const double *)(ws + X.W), pmm, pgp, n_partial);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-  } else if (S > 0) {
+  } else if (S > 0 && E > 0) {
     const size_t base = lds_bytes_lex(P, 1), staged = base + stage2_bytes(P);
     const int stage = stage_fits(staged) ? 1 : 0;
-    e = wait_mid();
-    if (e != hipSuccess) return e;
     const dim3 grid((unsigned)((S + kWave - 1) / kWave), (unsigned)E, (unsigned)O);
     if (stage)
       k_score_lex_wave<1><<<grid, 64, staged, s>>>(P, (const int8_t *)(ws + L.score.bmap), info, cap_lo, cap_hi,
@@ -4730,10 +4769,13 @@ hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const floa
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  e = joined();
-  if (e != hipSuccess) return e;
-  k_finalize_lex<<<O, 64, 0, s>>>(P, info, measured, E, S, gmm, ggp, pmm, pgp, S > 0 ? n_partial : 0, score_mm,
-                                  score_gp, best);
+  if (par) {
+    e = hipStreamWaitEvent(s, join, 0);
+    if (e != hipSuccess) return e;
+  }
+  // with no candidates only the gaps are written (best stays as it was)
+  k_finalize_lex<<<O, 64, 0, s>>>(P, info, measured, E, S, (const CertRec *)(ws + L.score.crec), gmm, ggp, pmm,
+                                  pgp, S > 0 ? n_partial : 0, score_mm, score_gp, E > 0 ? best : nullptr);
   return hipGetLastError();
 }
 
