@@ -3187,9 +3187,10 @@ __host__ __device__ inline int lex_sort_keys(int nopt) {
   return n;
 }
 
-// LDS of a k_lex_breaks block: the sort keys and one count per thread.
-__host__ __device__ inline size_t lex_breaks_lds(int nopt) {
-  return 4 * ((size_t)lex_sort_keys(nopt) + kLexPrepThreads);
+// LDS of a breakpoint block: the sort keys, one count per thread and the
+// realisation's cells (capacity and tail).
+__host__ __device__ inline size_t lex_breaks_lds(int nopt, int N) {
+  return 4 * ((size_t)lex_sort_keys(nopt) + kLexPrepThreads) + 8 * (size_t)N;
 }
 
 // LDS of a k_lex_tables block: every option's (ratio, served rate), the
@@ -3213,6 +3214,56 @@ __host__ __device__ inline size_t lex_score_lds(int nbmax, int rmax) {
   return sizeof(int) * (2 * (size_t)nbmax + 2 * (size_t)rmax);
 }
 
+// Bitonic sort of n2 = M x kLexPrepThreads keys (M = 1 or 2) held in
+// registers: thread t holds positions M t .. M t + M - 1.  A stage pairs
+// position p with p ^ stride; the lower one keeps the minimum when the run
+// of length size it lies in ascends ((p & size) == 0), else the maximum.
+// Within a wavefront (stride / M < 64) the partner's key comes by a lane
+// shuffle, one round trip per stage with no LDS write or barrier (DPP row
+// moves for the short distances measured slower); the stages across
+// wavefronts go through keys (LDS) between block barriers.
+// On return keys holds the sorted keys (block-synchronised).
+template <int M>
+__device__ __forceinline__ void bitonic_regs(int *keys, int n2, int tid) {
+  int v[M];
+#pragma unroll
+  for (int j = 0; j < M; ++j) v[j] = keys[M * tid + j];
+  for (int size = 2; size <= n2; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      if (stride < M) {  // M = 2, stride 1: both positions in this thread
+        const bool up = ((M * tid) & size) == 0;
+        const int a = v[0], b = v[M - 1];
+        v[0] = up ? min(a, b) : max(a, b);
+        v[M - 1] = up ? max(a, b) : min(a, b);
+      } else if (stride / M < kWave) {
+#pragma unroll
+        for (int j = 0; j < M; ++j) {
+          const int p = M * tid + j;
+          const int w = __shfl_xor(v[j], stride / M, kWave);
+          const bool keep_min = ((p & stride) == 0) == ((p & size) == 0);
+          v[j] = keep_min ? min(v[j], w) : max(v[j], w);
+        }
+      } else {
+        __syncthreads();  // earlier reads of keys are done
+#pragma unroll
+        for (int j = 0; j < M; ++j) keys[M * tid + j] = v[j];
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < M; ++j) {
+          const int p = M * tid + j;
+          const int w = keys[p ^ stride];
+          const bool keep_min = ((p & stride) == 0) == ((p & size) == 0);
+          v[j] = keep_min ? min(v[j], w) : max(v[j], w);
+        }
+      }
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < M; ++j) keys[M * tid + j] = v[j];
+  __syncthreads();
+}
+
 // Per (realisation R, order o), one block of kLexPrepThreads threads: every
 // option of every class (ratio bits, -1 when no load level holds it; served
 // rate) to opt_out, and the sorted distinct ratios, 0 always among them, to
@@ -3229,39 +3280,47 @@ __device__ void lex_breaks_block(const DevProblem &P, int R, int o, const float 
   const int K = P.K, N = P.N, B = P.B, NT = P.NT, per_class = NT * B, PP = P.optoff[NT];
   const int nopt = K * PP, n2 = lex_sort_keys(nopt);
   int *cnt = lex_keys + n2;
+  float *ccap = reinterpret_cast<float *>(cnt + kLexPrepThreads), *ctail = ccap + N;
   const size_t off = (size_t)o * N;
   const float *gcap = (R == 0 ? cap_lo : cap_hi) + off;
   const float *gtail = (R == 0 ? tail_hi : tail_lo) + off;
   int2 *opt = opt_out + ((size_t)o * 2 + R) * nopt;
-  // problem constants indexed per lane below: staged (kernel arguments
-  // indexed per lane are a memory load per access)
-  __shared__ int s_off[kMaxTp + 1];
+  // problem constants indexed per lane below, and the realisation's cells,
+  // staged in one round trip (kernel arguments indexed per lane are a
+  // memory load per access); the option offsets in registers
   __shared__ float s_slo[kMaxClasses], s_dm[kMaxClasses];
   __shared__ double s_rcp[kMaxClasses];
-  if (tid <= NT) s_off[tid] = P.optoff[tid];
   if (tid < K) {
     s_slo[tid] = P.slo[tid];
     s_dm[tid] = P.demand[tid];
     s_rcp[tid] = P.rcp_demand[tid];
   }
+  for (int c = tid; c < N; c += kLexPrepThreads) {
+    ccap[c] = gcap[c];
+    ctail[c] = gtail[c];
+  }
+  int ofr[kMaxTp];
+#pragma unroll
+  for (int j = 0; j < kMaxTp; ++j) ofr[j] = j < NT ? P.optoff[j] : INT_MAX;
   __syncthreads();
   for (int q = tid; q < n2; q += kLexPrepThreads) {
     int key = INT_MAX;  // padding and options that do not exist sort last
     if (q < nopt) {
       const int k = q / PP, p = q - k * PP;
-      int ti = 0;
-      while (ti + 1 < NT && p >= s_off[ti + 1]) ++ti;
-      const int r = p - s_off[ti] + 1;
-      const int b = level_from(P, s_dm[k] / (float)r);  // level_of with the staged demand
-      int f = -1;
-      float sv = 0.0f;
-      if (b >= 0) {
-        const int cell = k * per_class + ti * B + b;
-        const float c = gcap[cell], l = gtail[cell];
-        f = ratio_bits(c, l, r, s_slo[k], s_rcp[k]);
-        sv = l <= s_slo[k] ? served_rps(c, r, s_dm[k]) : 0.0f;
-        key = f;
+      int ti = 0, first = 0;
+#pragma unroll
+      for (int j = 1; j < kMaxTp; ++j) {
+        const bool in = p >= ofr[j];
+        ti = in ? j : ti;
+        first = in ? ofr[j] : first;
       }
+      const int r = p - first + 1;
+      const int b = level_from(P, s_dm[k] / (float)r);  // level_of with the staged demand
+      const int cell = k * per_class + ti * B + max(b, 0);
+      const float c = ccap[cell], l = ctail[cell];
+      const int f = b >= 0 ? ratio_bits(c, l, r, s_slo[k], s_rcp[k]) : -1;
+      const float sv = b >= 0 && l <= s_slo[k] ? served_rps(c, r, s_dm[k]) : 0.0f;
+      if (b >= 0) key = f;
       opt[q] = make_int2(f, __float_as_int(sv));
     } else if (q == nopt) {
       key = 0;  // tau* = 0 is its own interval (the empty option's)
@@ -3269,19 +3328,34 @@ __device__ void lex_breaks_block(const DevProblem &P, int R, int o, const float 
     lex_keys[q] = key;
   }
   __syncthreads();
-  for (int size = 2; size <= n2; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int idx = tid; idx < (n2 >> 1); idx += kLexPrepThreads) {
-        const int lo = ((idx & ~(stride - 1)) << 1) | (idx & (stride - 1)), hi = lo + stride;
-        const int a = lex_keys[lo], c = lex_keys[hi];
-        const bool up = (lo & size) == 0;
-        if ((a > c) == up) {
-          lex_keys[lo] = c;
-          lex_keys[hi] = a;
+  if (n2 == kLexPrepThreads) {
+    bitonic_regs<1>(lex_keys, n2, tid);
+  } else if (n2 == 2 * kLexPrepThreads) {
+    bitonic_regs<2>(lex_keys, n2, tid);
+  } else {
+    // Bitonic sort in LDS.  A stage of stride at most 64 pairs keys inside
+    // aligned runs of 128, and one wavefront handles every pair of a run (the
+    // 64 pair indices of a wavefront map to one run), so such a stage only
+    // waits for its own wavefront's writes, unless the stage before it
+    // crossed runs.
+    int prev = n2;
+    for (int size = 2; size <= n2; size <<= 1) {
+      for (int stride = size >> 1; stride > 0; stride >>= 1) {
+        if (stride > kWave || prev > kWave) __syncthreads();
+        else wave_lds_fence();
+        prev = stride;
+        for (int idx = tid; idx < (n2 >> 1); idx += kLexPrepThreads) {
+          const int lo = ((idx & ~(stride - 1)) << 1) | (idx & (stride - 1)), hi = lo + stride;
+          const int a = lex_keys[lo], c = lex_keys[hi];
+          const bool up = (lo & size) == 0;
+          if ((a > c) == up) {
+            lex_keys[lo] = c;
+            lex_keys[hi] = a;
+          }
         }
       }
-      __syncthreads();
     }
+    __syncthreads();
   }
   // thread t owns keys [t seg, (t + 1) seg): count its first occurrences,
   // then an exclusive count over the threads places them
@@ -4610,7 +4684,7 @@ LexExclRegions lex_excl_regions(const DevProblem &P, int64_t O, size_t *at) {
   R.nbmax = nopt + 1;
   const size_t rows = (size_t)O * 2 * P.K * (size_t)(R.nbmax + 1);
   const size_t vbytes = sizeof(double) * rows * ((size_t)P.G + 1);
-  R.fast = excl_kernel_supported(P) && lex_breaks_lds(nopt) <= kPrepGeneralLdsLimit &&
+  R.fast = excl_kernel_supported(P) && lex_breaks_lds(nopt, P.N) <= kPrepGeneralLdsLimit &&
            lex_tables_lds(nopt, PP, P.G) <= kPrepGeneralLdsLimit &&
            lex_score_lds(R.nbmax, P.G / P.tp[0]) <= kPrepGeneralLdsLimit && vbytes <= ((size_t)4 << 30);
   auto take = [&](size_t bytes) {
@@ -4675,7 +4749,7 @@ hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const floa
   {
     const int nb = setup_here ? setup_bucket_blocks(P) : 0, nc = setup_here ? setup_cand_blocks(E) : 0;
     const int nbr = tables ? 2 * O : 0;
-    const size_t lds_b = nbr > 0 ? lex_breaks_lds(nopt) : 0;
+    const size_t lds_b = nbr > 0 ? lex_breaks_lds(nopt, P.N) : 0;
     if (lds_b > 64 * 1024) {
       e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_setup), hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)lds_b);
