@@ -3721,9 +3721,12 @@ __global__ __launch_bounds__(64) void k_score_lex_excl(DevProblem P, const TileI
   }
 }
 
-// Pairwise tree over n partials zero-padded to a power of two.
+// Pairwise tree over n partials zero-padded to a power of two.  The stack
+// holds one sum per set bit of the count so far: at most 15 for the largest
+// count (2^20 samples / 64 per partial), so 16 entries, which the compiler
+// keeps in registers.
 __device__ __forceinline__ double partial_tree(const double *__restrict__ x, int64_t n) {
-  double stack[32];
+  double stack[16];
   int depth = 0;
   for (int64_t i = 0; i < n; ++i) {
     double v = x[i];
