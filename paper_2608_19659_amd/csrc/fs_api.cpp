@@ -722,7 +722,6 @@ fs_status fs_profile_loop(fs_context *ctx, const fs_problem *p, fs_intervals iv,
         XL.part_gp = LL.part_gp;
         XL.gap_mm = LL.gap_mm;
         XL.gap_gp = LL.gap_gp;
-        XL.state = LL.lex_state;
         XL.fast = LL.lex_fast;
         e = fs::launch_score_lex(P, R_cap_lo, D.cap_hi, R_tail_lo, R_tail_hi, D.measured, d_cand, cs, ts, n_orders,
                                  n_cand, S, D.score, (double *)(ws + LL.scores_gp), nullptr, nullptr, D.best, ws, XL,

@@ -136,6 +136,8 @@ size_t lds_bytes_lex(const DevProblem &P, int n_alloc);
 constexpr size_t kLexLdsLimit = 64 * 1024;
 hipError_t launch_solve_batch_lex(const DevProblem &P, const float *cap, const float *tail, int64_t n,
                                   AllocOut out, double *gp64, uint8_t *ws, const WsLayout &L, hipStream_t s);
+// with_state false: only the orders' two records (for a caller that forms
+// the gaps itself; state, gap_mm and gap_gp are then not written).
 hipError_t launch_certify_lex(const DevProblem &P, const float *cap_lo, const float *cap_hi, const float *tail_lo,
                               const float *tail_hi, const uint8_t *measured, int32_t O, float eps, int32_t *state,
                               AllocOut cons, AllocOut opt, double *gap_mm, double *gap_gp, uint8_t *ws,
@@ -185,7 +187,7 @@ struct LoopLayout {
   WsLayout score;
   size_t cap_lo, cap_hi, tail_lo, tail_hi, measured, cert_state, cons_obj, cons_tp, cons_rep, cons_fm,
       cons_gp, fin_obj, fin_tp, fin_rep, fin_fm, fin_gp, scores, gap_now, best, running, n_running;
-  size_t scores_gp, part_gp, gap_mm, gap_gp, lex_state;  // the stage-wise score (whole objective)
+  size_t scores_gp, part_gp, gap_mm, gap_gp;  // the stage-wise score (whole objective)
   LexExclRegions lex_fast;
   size_t total;
 };
@@ -196,7 +198,7 @@ LoopLayout loop_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S);
 // second array of partials, the order's two stages and a scratch state.
 struct LexScoreLayout {
   WsLayout score;
-  size_t part_gp, gap_mm, gap_gp, state, total;
+  size_t part_gp, gap_mm, gap_gp, total;
   LexExclRegions fast;
 };
 LexScoreLayout lex_score_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S);

@@ -4616,7 +4616,6 @@ LoopLayout loop_layout(const DevProblem &P, int64_t O, int64_t E, int64_t S) {
   L.part_gp = take(8 * (size_t)O * (size_t)E * L.score.n_partial);
   L.gap_mm = take(8 * (size_t)O);
   L.gap_gp = take(8 * (size_t)O);
-  L.lex_state = take(4 * (size_t)O);
   L.lex_fast = lex_excl_regions(P, O, &at);
   L.total = at;
   return L;
@@ -4716,7 +4715,6 @@ LexScoreLayout lex_score_layout(const DevProblem &P, int64_t O, int64_t E, int64
   L.part_gp = take(sizeof(double) * (size_t)O * (size_t)E * L.score.n_partial);
   L.gap_mm = take(sizeof(double) * (size_t)O);
   L.gap_gp = take(sizeof(double) * (size_t)O);
-  L.state = take(sizeof(int32_t) * (size_t)O);
   L.fast = lex_excl_regions(P, O, &at);
   L.total = at;
   return L;
@@ -4808,7 +4806,7 @@ hipError_t launch_score_lex(const DevProblem &P, const float *cap_lo, const floa
     e = hipStreamWaitEvent(side, fork, 0);
     if (e != hipSuccess) return e;
   }
-  e = launch_certify_lex(P, cap_lo, cap_hi, tail_lo, tail_hi, measured, O, 0.0f, (int32_t *)(ws + L.state), none,
+  e = launch_certify_lex(P, cap_lo, cap_hi, tail_lo, tail_hi, measured, O, 0.0f, nullptr, none,
                          none, gmm, ggp, ws, L.score, cs, false);
   if (e != hipSuccess) return e;
   if (par) {
