@@ -341,6 +341,25 @@ def test_stagewise_score_random_problems(env, kernel):
         _assert_score_lex_equal(g, o, f"inst {inst}")
 
 
+@pytest.mark.parametrize("kernel", [0, 1])
+def test_stagewise_score_many_tp_degrees(env, kernel):
+    """Five to eight TP degrees (the interval tables compiled for eight):
+    both scorers against the oracle bit for bit."""
+    rng = np.random.default_rng(61)
+    for inst in range(6):
+        tp = [[1, 2, 4, 8, 16], [1, 2, 3, 4, 6, 8], [1, 2, 3, 4, 5, 6, 7, 8]][inst % 3]
+        K = int(rng.integers(1, 5))
+        G = int(rng.integers(tp[-1], 90))
+        p = random_problem(seed=6100 + inst, K=K, tp=tp, G=G, n_levels=int(rng.integers(1, 5)))
+        O, S = int(rng.integers(1, 3)), int(rng.integers(1, 100))
+        iv, cand, cs, ts = _random_score_inputs(p, O, S, seed=60 + inst)
+        note(f"stage-wise many TP degrees inst {inst} K={K} G={G} tp={tp} O={O} S={S} kernel={kernel}")
+        w = SimpleNamespace(problem=p, intervals=iv, cand=cand)
+        g = _score_lex(env, w, cs, ts, kernel)
+        o = oracle.score_lex(p, iv, cand, cs, ts, n_threads=16)
+        _assert_score_lex_equal(g, o, f"inst {inst}")
+
+
 def test_stagewise_score_all_measured_and_no_candidate(env):
     """Every candidate revealed: scores 0, best -1, the stages from the
     certificate alone, on both scorers."""

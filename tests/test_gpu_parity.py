@@ -657,6 +657,45 @@ def test_score_many_partials(env, orc, S):
         np.testing.assert_array_equal(best, o.best)
 
 
+def _random_intervals_and_samples(p, O, S, seed, measured_frac=0.2):
+    """Seeded intervals on the 1/64 capacity grid (some cells revealed: a
+    point interval), every cell a candidate, samples uniform inside."""
+    rng = np.random.default_rng(seed)
+    N = p.n_cells
+    lo = (np.maximum(np.rint(rng.uniform(0.0, 3.0, (O, N)) * 64), 1) / 64).astype(np.float32)
+    hi = (lo + np.rint(rng.uniform(0.0, 1.0, (O, N)) * 64) / 64).astype(np.float32)
+    tl = rng.uniform(2.0, 50.0, (O, N)).astype(np.float32)
+    th = (tl * rng.uniform(1.0, 1.6, (O, N))).astype(np.float32)
+    meas = (rng.random((O, N)) < measured_frac).astype(np.uint8)
+    hi = np.where(meas == 1, lo, hi).astype(np.float32)
+    th = np.where(meas == 1, tl, th).astype(np.float32)
+    cand = np.arange(N, dtype=np.int32)
+    cs = (lo[:, :, None] + (hi - lo)[:, :, None] * rng.uniform(0, 1, (O, N, S))).astype(np.float32)
+    ts = (tl[:, :, None] + (th - tl)[:, :, None] * rng.uniform(0, 1, (O, N, S))).astype(np.float32)
+    return Intervals(lo, hi, tl, th, meas), cand, cs, ts
+
+
+@pytest.mark.parametrize("inst", range(6))
+def test_exclusion_score_many_tp_degrees(env, orc, inst):
+    """Five to eight TP degrees with a budget of at most 64: the per-order
+    set-up compiled for eight degrees, with 2-4, 5-8 and 9-12 classes (its
+    three class-count builds), ragged and vector sample counts: every tau of
+    the dump, scores, gaps and best candidates equal the oracle's."""
+    tps = [[1, 2, 4, 8, 16], [1, 2, 3, 4, 6, 8], [1, 2, 3, 4, 5, 6, 7, 8]]
+    tp = tps[inst % 3]
+    K = [3, 6, 12][inst // 2]
+    rng = np.random.default_rng(1500 + inst)
+    G = int(rng.integers(max(tp[-1], 17), 65))
+    S = [100, 128][inst % 2]
+    p = random_problem(seed=1510 + inst, K=K, tp=tp, G=G, n_levels=int(rng.integers(2, 6)))
+    iv, cand, cs, ts = _random_intervals_and_samples(p, 2, S, seed=1520 + inst)
+    note(f"score many TP degrees inst {inst} K={K} G={G} tp={tp} S={S}")
+    g = gpu_score(env, p, iv, cand, cs, ts, kernel=3)
+    o = orc.score(p, iv, cand, cs, ts, n_threads=16)
+    assert_scores_equal(g, o)
+    assert (o.gap_now > 0).any()  # the seeds give every instance something to learn
+
+
 @pytest.mark.parametrize("name", ["6class-G32", "12class-G64"])
 def test_setup_wavefront_layouts_match_oracle(env, orc, name):
     """The per-order set-up with two wavefronts per class (6 classes, 12
