@@ -379,8 +379,11 @@ __device__ int wave_solve(const DevProblem &P, const int8_t *__restrict__ bmap,
     }
     __syncthreads();
     // B_k[g] = max over options with at most g GPUs: prefix maximum.
-    int carry = INT_MIN;
-    for (int base = 0; base <= G; base += kWave) {
+    // budget 0 holds no option (costs are at least 1): T[0] keeps its
+    // initial value and the scan runs over budgets 1..G (one pass when G
+    // is 64)
+    int carry = T[0];
+    for (int base = 1; base <= G; base += kWave) {
       const int g = base + lane;
       int v = (g <= G) ? T[g] : INT_MIN;
       v = max(wave_scan_max(v, lane), carry);
@@ -393,7 +396,9 @@ __device__ int wave_solve(const DevProblem &P, const int8_t *__restrict__ bmap,
     } else if (k + 1 < K) {
       // both tables are nondecreasing in the budget (prefix maxima, and
       // (max,min) convolutions of such), so every target is a crossing search
-      for (int g = lane; g <= G; g += kWave) Dn[g] = conv_mono(D, T, g, top);
+      // budget 0 is min(D[0], T[0]) (a = 0 only); the others by the search
+      if (lane == 0) Dn[0] = min(D[0], T[0]);
+      for (int g = 1 + lane; g <= G; g += kWave) Dn[g] = conv_mono(D, T, g, top);
       __syncthreads();
       int *tmp = D; D = Dn; Dn = tmp;
     } else {
@@ -2870,9 +2875,12 @@ __device__ void wave_lex_stage(const DevProblem &P, const int8_t *__restrict__ b
       X.aoff[n_c + lane] = 16 * (G + 1);
     }
     __syncthreads();
-    for (int top = G; top >= 0; top -= kWave) {
+    // budgets 1..G in groups of 64 (one group when G is 64); budget 0 takes
+    // no listed cost, only the empty option, and is rewritten after every
+    // group has read it
+    for (int top = G; top >= 1; top -= kWave) {
       const int g = top - lane;
-      const int gs = g >= 0 ? g : top;  // lanes past g = 0 compute nothing (valid reads)
+      const int gs = g >= 1 ? g : top;  // lanes past g = 1 compute nothing (valid reads)
       const LexCell e0 = X.v[gs];
       double bgp = empty_ok ? e0.gp : NEG;
       int bkey = empty_ok ? e0.key : INT_MAX;
@@ -2913,12 +2921,18 @@ __device__ void wave_lex_stage(const DevProblem &P, const int8_t *__restrict__ b
         }
       }
       wave_lds_fence();
-      if (g >= 0) {
+      if (g >= 1) {
         const bool none = bgp == NEG;
         X.v[g] = LexCell{bgp, none ? 0 : (bkey & ~0xFFFF), 0};
         X.choice[k * (G + 1) + g] = (int16_t)(none ? -2 : (bkey & 0xFFFF) - 1);
       }
       wave_lds_fence();
+    }
+    if (lane == 0) {  // budget 0: the empty option, when allowed and completed
+      const LexCell e0 = X.v[0];
+      const bool none = !empty_ok || e0.gp == NEG;
+      X.v[0] = none ? LexCell{NEG, 0, 0} : e0;
+      X.choice[k * (G + 1)] = (int16_t)(none ? -2 : -1);
     }
     __syncthreads();
   }
@@ -3542,8 +3556,11 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_tables(DevProblem P, co
       // rates eight at a time (16-byte reads at the same address in every
       // lane): per term one subtraction, one addition and one maximum, and
       // per eight terms two round trips to LDS.
-      for (int top = G; top >= 0; top -= kWave) {
-        const int g = top - lane;  // lanes past g = 0 compute nothing
+      // budget 0 takes no listed cost (costs are at least 1); budgets 1..G
+      // in groups of 64 (one group when G is 64)
+      if (lane == 0) Vc[0] = empty_ok ? Vp[0] : NEG;
+      for (int top = G; top >= 1; top -= kWave) {
+        const int g = top - lane;  // lanes past g = 1 compute nothing
         const int gs = g >= 0 ? g : 0;
         const char *vg = reinterpret_cast<const char *>(Vp + gs);
         double best = empty_ok ? Vp[gs] : NEG;
@@ -3573,7 +3590,7 @@ __global__ __launch_bounds__(kLexPrepThreads) void k_lex_tables(DevProblem P, co
 #pragma unroll
           for (int u = 0; u < 8; ++u) best = fmax(best, aq[u] + vq[u]);
         }
-        if (g >= 0) Vc[g] = best;
+        if (g >= 1) Vc[g] = best;
       }
       wave_lds_fence();
       double *t2 = Vp;
