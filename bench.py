@@ -12,7 +12,11 @@ Two passes are timed: "warm" repeats the step on one copy of the samples
 (which then sit in the 256 MB Infinity Cache), "cold" rotates the step over
 enough copies of the samples that each step reads them from HBM.  The
 headline value is the cold step throughput; a workload whose samples are too
-few to exceed the cache (the 2-class ones) has only the warm pass.
+few to exceed the cache (the 2-class ones) has only the warm pass.  The
+timed steps of each pass are captured once into a HIP graph (every step a
+whole call: set-up, scorer, finalize) and replayed as one launch after one
+untimed replay; the same steps launched one call at a time from Python are
+timed beside them ("eager").
 
 Prints one JSON line.  The roofline object reports the dominant kernel (the
 per-scenario scorer) against the HBM bandwidth peak (the binding roofline of
@@ -650,8 +654,10 @@ def lex_bench(args):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default 200 for the scorer, 20 for --loop, --policy and --lex)")
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed warm-up steps (default 20 for the scorer, 5 for the others)")
     ap.add_argument("--workload", default=BENCH_WORKLOAD,
                     help=f"synthetic workload name (default {BENCH_WORKLOAD})")
     ap.add_argument("--kernel", type=int, default=0,
@@ -684,11 +690,18 @@ def main():
     ap.add_argument("--cold-copies", type=int, default=-1,
                     help="sample copies the cold pass rotates over (-1: enough to exceed the Infinity Cache "
                          "three times; 0 or 1: no cold pass)")
+    ap.add_argument("--eager", action="store_true",
+                    help="time the steps as calls launched one by one (no HIP graph) for the headline")
     ap.add_argument("--warm-headline", action="store_true",
                     help="report the warm pass (one sample copy, cached) as the headline instead of the cold one")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (scales the HBM byte counters)")
     args = ap.parse_args()
+    other = args.loop or args.policy or args.lex
+    if args.steps is None:
+        args.steps = 20 if other else 200
+    if args.warmup is None:
+        args.warmup = 5 if other else 20
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the scorer is measured per GPU",
               file=sys.stderr)
@@ -739,7 +752,10 @@ def main():
                          torch.empty(O, dtype=torch.float64, device=dev),
                          torch.empty(O, dtype=torch.int32, device=dev), None)
     ws = ctx.workspace(fs.workspace_size(p, O, E, S))
-    stream = torch.cuda.current_stream()
+    # a stream of our own (default priority): a HIP graph is captured from it
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    torch.cuda.set_stream(stream)
 
     measured_cand = w.intervals.measured[:, w.cand].astype(bool)
     live_tiles = [(o, e) for o in range(O) for e in range(E) if not measured_cand[o, e]]
@@ -768,43 +784,58 @@ def main():
         plans.append(fs.ScorePlan(ctx, p, iv, cand, c2, t2, out=out, workspace=ws, stream=stream))
     torch.cuda.synchronize()
 
+    def run_steps(pl, n):
+        for j in range(n):
+            pl[j % len(pl)].run()
+
+    def span_ms(fn, n):
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        fn()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1) / n
+
     def timed(kernel_id, steps, warmup, rotate):
         """Time `steps` whole steps (set-up, scorer, finalize) with no timing
-        markers in the stream, rotating over the sample copies when asked;
-        then the same number of steps again with the library's HIP event
-        pair around the scorer: TIMING_REPEATS back-to-back launches per
-        step when warm (an event pair around one launch adds its own queue
-        work to the span), one launch per step when cold (a repeat would
-        read the samples from the cache)."""
+        markers in the stream, rotating over the sample copies when asked:
+        once launched call by call (eager) and once as a HIP graph of the
+        same steps, replayed after one untimed replay.  Then the same number
+        of steps again, eager, with the library's HIP event pair around the
+        scorer: TIMING_REPEATS back-to-back launches per step when warm (an
+        event pair around one launch adds its own queue work to the span),
+        one launch per step when cold (a repeat would read the samples from
+        the cache).  Returns (ms per step of the headline mode, ms per step
+        eager, ms per step graph, scorer ms per launch, launches timed)."""
         ctx.set_score_kernel(kernel_id)
         ctx.set_option(fs.OPT_KERNEL_TIMING, 0)
         pl = plans if rotate else plans[:1]
         torch.cuda.synchronize()
-        for j in range(warmup):
-            pl[j % len(pl)].run()
-        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        run_steps(pl, warmup)
+        ms_eager = span_ms(lambda: run_steps(pl, steps), steps)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            run_steps(pl, steps)
+        g.replay()
         torch.cuda.synchronize()
-        ev0.record(stream)
-        for j in range(steps):
-            pl[j % len(pl)].run()
-        ev1.record(stream)
-        torch.cuda.synchronize()
-        ms_per_step = ev0.elapsed_time(ev1) / steps
+        ms_graph = span_ms(g.replay, steps)
+        del g
         ctx.set_option(fs.OPT_KERNEL_TIMING, 1 if rotate else TIMING_REPEATS)
         ctx.kernel_timing()  # nothing pending
-        for j in range(steps):
-            pl[j % len(pl)].run()
+        run_steps(pl, steps)
         torch.cuda.synchronize()
         kernel_ms, launches = ctx.kernel_timing()
         ctx.set_option(fs.OPT_KERNEL_TIMING, 0)
-        return ms_per_step, kernel_ms / max(launches, 1), launches
+        ms = ms_eager if args.eager else ms_graph
+        return ms, ms_eager, ms_graph, kernel_ms / max(launches, 1), launches
 
     print(f"[bench] kernel {kernel}: warmup {args.warmup}, {args.steps} warm steps, {args.steps} cold steps over "
           f"{copies} sample copies", file=sys.stderr, flush=True)
-    ms_warm, kms_warm, n_warm = timed(kernel, args.steps, args.warmup, False)
+    ms_warm, ms_warm_eager, ms_warm_graph, kms_warm, n_warm = timed(kernel, args.steps, args.warmup, False)
     cold = None
     if copies >= 2:
-        ms_cold, kms_cold, n_cold = timed(kernel, args.steps, args.warmup, True)
+        ms_cold, ms_cold_eager, ms_cold_graph, kms_cold, n_cold = timed(kernel, args.steps, args.warmup, True)
         # An event pair around a single launch adds its own queue work to the
         # span (about 2 us here), so the cold scorer time is taken as the warm
         # one (ten launches per event pair) plus what the cold step adds to
@@ -812,6 +843,7 @@ def main():
         kms_cold_est = kms_warm + max(ms_cold - ms_warm, 0.0)
         cold = {"ms_per_step": ms_cold, "value": scenarios / (ms_cold / 1e3), "kernel_ms_avg": kms_cold_est,
                 "kernel_ms_events_one_launch": kms_cold, "sample_copies": copies,
+                "ms_per_step_eager": ms_cold_eager, "ms_per_step_graph": ms_cold_graph,
                 "bytes_per_rotation": nbytes * copies}
     plans[0].run()  # the outputs checked below come from a step like every timed one
     torch.cuda.synchronize()
@@ -867,7 +899,7 @@ def main():
     full = None
     if not args.no_full_resolve and kernel != 2 and lane_ok:
         print("[bench] full re-solve kernel (lane per scenario)", file=sys.stderr, flush=True)
-        f_ms, f_kms, f_n = timed(2, 5, 2, False)
+        f_ms, _, _, f_kms, f_n = timed(2, 5, 2, False)
         full = {"kernel": f"k_score_lane<{p.budget}>", "value": scenarios / (f_ms / 1e3),
                 "ms_per_step": f_ms, "roofline": roofline_of(2, f_kms, f_ms) if f_n else None}
         ctx.set_score_kernel(kernel)
@@ -896,7 +928,12 @@ def main():
                                      "intervals": sha256_arrays(w.intervals.cap_lo, w.intervals.cap_hi,
                                                                 w.intervals.tail_lo, w.intervals.tail_hi,
                                                                 w.intervals.measured, w.cand)}},
-        "warm": {"ms_per_step": ms_warm, "value": scenarios / (ms_warm / 1e3), "kernel_ms_avg": kms_warm},
+        "timing": {"mode": "eager" if args.eager else "hip_graph",
+                   "graph": "the timed steps captured once into one HIP graph, replayed once untimed, "
+                            "then timed as one replay",
+                   "eager": "the same steps launched call by call from Python"},
+        "warm": {"ms_per_step": ms_warm, "value": scenarios / (ms_warm / 1e3), "kernel_ms_avg": kms_warm,
+                 "ms_per_step_eager": ms_warm_eager, "ms_per_step_graph": ms_warm_graph},
         "cold": cold,
         "roofline": roofline, "parity": parity, "cpu_baseline": cpu, "full_resolve": full,
     }
