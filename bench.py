@@ -23,7 +23,8 @@ per-scenario scorer) against the HBM bandwidth peak (the binding roofline of
 its work model): achieved = the algorithmic bytes per launch over the
 kernel's mean launch duration, measured with HIP events the library records
 on its stream around ten back-to-back launches (warm); the cold duration is
-the warm one plus what the cold step adds to the warm step.  step_frac is
+the one-launch event figure of the cold pass less the event pair's own
+cost (the warm pass's one-launch figure less its ten-launch one).  step_frac is
 the same bytes over the whole step.  After
 timing, the outputs of the timed steps are compared with the oracle's on
 the tiles its CPU baseline solved (bit for bit); a mismatch exits with
@@ -821,28 +822,39 @@ def main():
         torch.cuda.synchronize()
         ms_graph = span_ms(g.replay, steps)
         del g
-        ctx.set_option(fs.OPT_KERNEL_TIMING, 1 if rotate else TIMING_REPEATS)
-        ctx.kernel_timing()  # nothing pending
-        run_steps(pl, steps)
-        torch.cuda.synchronize()
-        kernel_ms, launches = ctx.kernel_timing()
-        ctx.set_option(fs.OPT_KERNEL_TIMING, 0)
+        def event_ms(repeats):
+            ctx.set_option(fs.OPT_KERNEL_TIMING, repeats)
+            ctx.kernel_timing()  # nothing pending
+            run_steps(pl, steps)
+            torch.cuda.synchronize()
+            kernel_ms, launches = ctx.kernel_timing()
+            ctx.set_option(fs.OPT_KERNEL_TIMING, 0)
+            return kernel_ms / max(launches, 1), launches
+
+        kms, launches = event_ms(1 if rotate else TIMING_REPEATS)
+        # one launch per event pair, also warm: its excess over the ten-launch
+        # figure is the event pair's own cost, taken off the cold one-launch
+        # figure
+        kms_one = kms if rotate else event_ms(1)[0]
         ms = ms_eager if args.eager else ms_graph
-        return ms, ms_eager, ms_graph, kernel_ms / max(launches, 1), launches
+        return ms, ms_eager, ms_graph, kms, launches, kms_one
 
     print(f"[bench] kernel {kernel}: warmup {args.warmup}, {args.steps} warm steps, {args.steps} cold steps over "
           f"{copies} sample copies", file=sys.stderr, flush=True)
-    ms_warm, ms_warm_eager, ms_warm_graph, kms_warm, n_warm = timed(kernel, args.steps, args.warmup, False)
+    ms_warm, ms_warm_eager, ms_warm_graph, kms_warm, n_warm, kms_warm_one = timed(kernel, args.steps, args.warmup, False)
     cold = None
     if copies >= 2:
-        ms_cold, ms_cold_eager, ms_cold_graph, kms_cold, n_cold = timed(kernel, args.steps, args.warmup, True)
+        ms_cold, ms_cold_eager, ms_cold_graph, kms_cold, n_cold, _ = timed(kernel, args.steps, args.warmup, True)
         # An event pair around a single launch adds its own queue work to the
-        # span (about 2 us here), so the cold scorer time is taken as the warm
-        # one (ten launches per event pair) plus what the cold step adds to
-        # the warm step: set-up and finalize read the same few KB either way.
-        kms_cold_est = kms_warm + max(ms_cold - ms_warm, 0.0)
+        # span (about 2 us here; a repeat would read the samples from the
+        # cache), so the cold scorer time is the cold one-launch figure less
+        # that cost, measured warm as one-launch minus ten-launch figures.
+        pair_cost = max(kms_warm_one - kms_warm, 0.0)
+        kms_cold_est = max(kms_cold - pair_cost, kms_warm)
         cold = {"ms_per_step": ms_cold, "value": scenarios / (ms_cold / 1e3), "kernel_ms_avg": kms_cold_est,
-                "kernel_ms_events_one_launch": kms_cold, "sample_copies": copies,
+                "kernel_ms_events_one_launch": kms_cold, "event_pair_cost_ms": pair_cost,
+                "kernel_ms_warm_plus_step_delta": kms_warm + max(ms_cold - ms_warm, 0.0),
+                "sample_copies": copies,
                 "ms_per_step_eager": ms_cold_eager, "ms_per_step_graph": ms_cold_graph,
                 "bytes_per_rotation": nbytes * copies}
     plans[0].run()  # the outputs checked below come from a step like every timed one
@@ -899,7 +911,7 @@ def main():
     full = None
     if not args.no_full_resolve and kernel != 2 and lane_ok:
         print("[bench] full re-solve kernel (lane per scenario)", file=sys.stderr, flush=True)
-        f_ms, _, _, f_kms, f_n = timed(2, 5, 2, False)
+        f_ms, _, _, f_kms, f_n, _ = timed(2, 5, 2, False)
         full = {"kernel": f"k_score_lane<{p.budget}>", "value": scenarios / (f_ms / 1e3),
                 "ms_per_step": f_ms, "roofline": roofline_of(2, f_kms, f_ms) if f_n else None}
         ctx.set_score_kernel(kernel)
