@@ -4445,7 +4445,13 @@ hipError_t launch_score(const DevProblem &P, const ScoreArgs &a, hipStream_t s) 
                                     a.best);
       return hipGetLastError();
     }
-    const int spl = a.spl == 4 || a.spl == 8 || a.spl == 16 ? a.spl : kSpl;
+    // Chunks of 1024 samples when the default grid would get more than 16
+    // chunks of 512 per wavefront: on the 8-class, G = 256 workload (43
+    // per wavefront) the scorer ran 33.0 us against 35.9 with 512; with
+    // about 5 per wavefront (the 4-class, G = 64 one) 512 stays faster.
+    const int64_t chunks512 = (int64_t)(a.S + 511) / 512 * a.O * a.E;
+    const int spl = a.spl == 4 || a.spl == 8 || a.spl == 16 ? a.spl
+                    : chunks512 > 16 * (int64_t)kScorerWaves ? 16 : kSpl;
     const int64_t chunk = 64 * spl;
     const int64_t n_partial = (a.S + chunk - 1) / chunk;
     // LDS: per-class constants, then M and thresholds of a range longer
